@@ -1,0 +1,443 @@
+/*
+ * QuadTree attention forward: plain, slow CPU oracle.
+ *
+ * TEST INFRASTRUCTURE ONLY. This file is the correctness reference for the GPU library. Only the
+ * test suite, the smoke check and the benchmark's CPU-baseline leg may load it. The product path
+ * never calls it, and it shares no code, header, table or helper with the GPU library.
+ *
+ * It follows Tang et al., "QuadTree Attention for Vision Transformers" (ICLR 2022), Sec. 3.2:
+ *   - L-level token pyramids of Q, K and V by 2x2 average pooling (Sec. 3.2, pyramid paragraph);
+ *   - plain softmax attention, Eq. (1), at the coarsest level, where every query sees every key;
+ *   - per query, the K keys with the highest attention scores are kept (Sec. 3.2, Fig. 1);
+ *   - at each finer level a query only meets the 2x2 children of its parent's kept keys;
+ *   - QuadTree-A: scores s^l = s^{l-1} t^l with t a softmax over the 2x2 children of one kept key,
+ *     partial messages over Omega^l = Gamma^l - Gamma^{l+1}, summed over levels (Eqs. 2-4);
+ *   - QuadTree-B: per-level attention over the whole region Gamma^l, combined with per-query
+ *     level weights w (Eqs. 5-6).
+ *
+ * Level numbering: l = 0 is the finest level (the input map) and l = L-1 the coarsest. (The paper's
+ * Sec. 3.2 counts from the coarsest, its complexity appendix from the finest.)
+ *
+ * Readings where the paper is silent (each also listed in the design notes of the repository):
+ *   - ceil pooling: a level-(l+1) token (y,x) averages its valid children (2y+dy, 2x+dx) at level
+ *     l, dividing by their count; the sum is taken in fp32 as ((c00 + c01) + (c10 + c11)) with
+ *     missing children left out, then multiplied by 1/n and rounded to the storage type;
+ *   - the recursion base is s = 1 above the coarsest level, so coarse scores are the full softmax;
+ *   - t is normalised over the valid 2x2 children of one kept parent key;
+ *   - A ranks candidates by s, B by its softmax probability; ties go to the lower flat index;
+ *   - A's message at a level that selects leaves out that query's own kept keys; at l = 0 (no
+ *     further level) every candidate contributes;
+ *   - temperature tau = 1/sqrt(d) (head dimension) at every level unless a scale is given;
+ *   - w is used as given, [B][H*W][heads][L]; NULL means 1/L everywhere;
+ *   - every head is an independent quadtree.
+ *
+ * Arithmetic: every dot product, softmax and message sum is in double, from the stored (already
+ * rounded) pyramid values. Pyramids are computed in fp32 exactly as stated above.
+ *
+ * Teacher forcing: a caller may supply the kept-key lists of every selecting level. The oracle then
+ * uses them instead of its own choices (for A, with its own scores of the supplied keys), so a
+ * GPU run whose selections differ at near-ties can still be compared level by level.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define QO_MAX_LEVELS 16
+
+enum { QO_F32 = 0, QO_BF16 = 1 };
+enum { QO_A = 0, QO_B = 1 };
+
+typedef struct {
+    /* inputs: NHWC, [B][H][W][heads*d]; values must be representable in `dtype` */
+    const float* q;
+    const float* k;
+    const float* v;
+    const float* w;               /* variant B only: [B][H*W][heads][L]; NULL means 1/L */
+    int B, heads, H, W, d, L, K, variant, dtype;
+    double scale;                 /* <= 0 means 1/sqrt(d) */
+    const int32_t* const* forced; /* NULL, or per level l in 1..L-1: [B][heads][N_l][K] */
+    /* outputs, all optional (NULL pointers or NULL entries are skipped) */
+    double* out;                  /* [B][H][W][heads][d] */
+    float* const* pyr_q;          /* per level l in 1..L-1: [B][H_l][W_l][C] */
+    float* const* pyr_k;
+    float* const* pyr_v;
+    double* const* msg;           /* per level l in 0..L-1: [B][N_l][heads][d] */
+    int32_t* const* sel_idx;      /* per level l in 1..L-1: [B][heads][N_l][K], -1 padded */
+    double* const* sel_key;       /* same shape; 0 where idx is -1 */
+    int32_t* const* cand_idx;     /* per level l in 0..L-1: [B][heads][N_l][ncand_l] */
+    double* const* cand_key;      /*   ncand = N_{L-1} at the coarsest level, 4K elsewhere */
+} qo_forward_args;
+
+/* ----------------------------------------------------------------------------------------- */
+/* geometry                                                                                   */
+/* ----------------------------------------------------------------------------------------- */
+
+/* Level sizes: each level halves the previous one, rounding up (Sec. 3.2; App. A.1 gives
+ * HW/4^l tokens at level l for maps that divide exactly). */
+int qo_level_dims(int H, int W, int L, int* Hl, int* Wl)
+{
+    if (H <= 0 || W <= 0 || L <= 0 || L > QO_MAX_LEVELS) return -1;
+    Hl[0] = H;
+    Wl[0] = W;
+    for (int l = 1; l < L; ++l) {
+        Hl[l] = (Hl[l - 1] + 1) / 2;
+        Wl[l] = (Wl[l - 1] + 1) / 2;
+    }
+    return 0;
+}
+
+/* ----------------------------------------------------------------------------------------- */
+/* storage rounding                                                                           */
+/* ----------------------------------------------------------------------------------------- */
+
+/* Round an fp32 value to the nearest bfloat16 (ties to even) and return it as fp32. */
+static float round_to_bf16(float x)
+{
+    uint32_t u;
+    memcpy(&u, &x, 4);
+    uint32_t lsb = (u >> 16) & 1u;
+    u += 0x7FFFu + lsb;
+    u &= 0xFFFF0000u;
+    float y;
+    memcpy(&y, &u, 4);
+    return y;
+}
+
+static float round_to_dtype(float x, int dtype)
+{
+    return dtype == QO_BF16 ? round_to_bf16(x) : x;
+}
+
+/* ----------------------------------------------------------------------------------------- */
+/* pyramid                                                                                    */
+/* ----------------------------------------------------------------------------------------- */
+
+/* One pooling step (Sec. 3.2: query, key and value pyramids by average pooling; QuadTree-A uses
+ * it for all three). dst[b][y][x][c] is the mean of the valid children of (y,x) in src. */
+int qo_pool_level(const float* src, int B, int Hs, int Ws, int C, int dtype, float* dst)
+{
+    if (!src || !dst || B <= 0 || Hs <= 0 || Ws <= 0 || C <= 0) return -1;
+    const int Hd = (Hs + 1) / 2, Wd = (Ws + 1) / 2;
+    for (int b = 0; b < B; ++b)
+        for (int y = 0; y < Hd; ++y)
+            for (int x = 0; x < Wd; ++x) {
+                const int has_right = (2 * x + 1) < Ws;
+                const int has_below = (2 * y + 1) < Hs;
+                const int n = (1 + has_right) * (1 + has_below);
+                const float inv_n = 1.0f / (float)n;
+                for (int c = 0; c < C; ++c) {
+                    const float c00 = src[(((size_t)b * Hs + 2 * y) * Ws + 2 * x) * C + c];
+                    float row0 = c00;
+                    if (has_right) row0 = row0 + src[(((size_t)b * Hs + 2 * y) * Ws + 2 * x + 1) * C + c];
+                    float sum = row0;
+                    if (has_below) {
+                        float row1 = src[(((size_t)b * Hs + 2 * y + 1) * Ws + 2 * x) * C + c];
+                        if (has_right)
+                            row1 = row1 + src[(((size_t)b * Hs + 2 * y + 1) * Ws + 2 * x + 1) * C + c];
+                        sum = row0 + row1;
+                    }
+                    const float mean = sum * inv_n;
+                    dst[(((size_t)b * Hd + y) * Wd + x) * C + c] = round_to_dtype(mean, dtype);
+                }
+            }
+    return 0;
+}
+
+/* ----------------------------------------------------------------------------------------- */
+/* small helpers                                                                              */
+/* ----------------------------------------------------------------------------------------- */
+
+/* <q_i, k_j> over one head's d channels, in double. */
+static double dot_head(const float* qrow, const float* krow, int d)
+{
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) acc += (double)qrow[c] * (double)krow[c];
+    return acc;
+}
+
+/* Is candidate a ranked before candidate b? Higher key first, then lower flat index. */
+static int ranks_before(double key_a, int idx_a, double key_b, int idx_b)
+{
+    if (key_a != key_b) return key_a > key_b;
+    return idx_a < idx_b;
+}
+
+/* Top-K by plain repeated selection: out_pos[r] is the candidate position of the r-th kept key,
+ * for r < min(K, number of valid candidates); returns that count. valid[] marks candidates. */
+static int select_top_k(const double* key, const int* idx, const int* valid, int n, int K, int* out_pos,
+                        char* taken)
+{
+    for (int j = 0; j < n; ++j) taken[j] = 0;
+    int kept = 0;
+    for (int r = 0; r < K; ++r) {
+        int best = -1;
+        for (int j = 0; j < n; ++j) {
+            if (!valid[j] || taken[j]) continue;
+            if (best < 0 || ranks_before(key[j], idx[j], key[best], idx[best])) best = j;
+        }
+        if (best < 0) break;
+        taken[best] = 1;
+        out_pos[kept++] = best;
+    }
+    return kept;
+}
+
+/* ----------------------------------------------------------------------------------------- */
+/* forward                                                                                    */
+/* ----------------------------------------------------------------------------------------- */
+
+/* Return codes: 0 ok, -1 bad arguments, -2 a forced selection is not a candidate of its query,
+ * -3 out of memory. */
+int qo_forward(const qo_forward_args* a)
+{
+    if (!a || !a->q || !a->k || !a->v) return -1;
+    const int B = a->B, NH = a->heads, H = a->H, W = a->W, d = a->d, L = a->L, K = a->K;
+    if (B <= 0 || NH <= 0 || d <= 0 || K <= 0) return -1;
+    if (a->variant != QO_A && a->variant != QO_B) return -1;
+    if (a->dtype != QO_F32 && a->dtype != QO_BF16) return -1;
+    int Hl[QO_MAX_LEVELS], Wl[QO_MAX_LEVELS];
+    if (qo_level_dims(H, W, L, Hl, Wl) != 0) return -1;
+    const int C = NH * d;
+    const double tau = a->scale > 0.0 ? a->scale : 1.0 / sqrt((double)d);
+    const int isB = a->variant == QO_B;
+    size_t Nl[QO_MAX_LEVELS];
+    for (int l = 0; l < L; ++l) Nl[l] = (size_t)Hl[l] * (size_t)Wl[l];
+    const int Lc = L - 1;           /* coarsest level */
+    const int nc_coarse = (int)Nl[Lc];
+
+    int rc = 0;
+    float* pq[QO_MAX_LEVELS] = {0};
+    float* pk[QO_MAX_LEVELS] = {0};
+    float* pv[QO_MAX_LEVELS] = {0};
+    double* msg[QO_MAX_LEVELS] = {0};
+    int32_t* sel[QO_MAX_LEVELS] = {0};
+    double* key[QO_MAX_LEVELS] = {0};
+    int ncand_max = nc_coarse > 4 * K ? nc_coarse : 4 * K;
+    double* ck = malloc(sizeof(double) * ncand_max);
+    int* ci = malloc(sizeof(int) * ncand_max);
+    int* cv = malloc(sizeof(int) * ncand_max);
+    double* cx = malloc(sizeof(double) * ncand_max);
+    int* pos = malloc(sizeof(int) * (K + 1));
+    char* taken = malloc(ncand_max);
+    char* in_sel = malloc(ncand_max);
+    double* acc = malloc(sizeof(double) * d);
+    if (!ck || !ci || !cv || !cx || !pos || !taken || !in_sel || !acc) { rc = -3; goto done; }
+
+    /* level 0 of each pyramid is the input as stored */
+    for (int l = 0; l < L; ++l) {
+        const size_t n = (size_t)B * Nl[l] * C;
+        pq[l] = malloc(sizeof(float) * n);
+        pk[l] = malloc(sizeof(float) * n);
+        pv[l] = malloc(sizeof(float) * n);
+        msg[l] = malloc(sizeof(double) * (size_t)B * Nl[l] * NH * d);
+        if (!pq[l] || !pk[l] || !pv[l] || !msg[l]) { rc = -3; goto done; }
+        if (l >= 1) {
+            sel[l] = malloc(sizeof(int32_t) * (size_t)B * NH * Nl[l] * K);
+            key[l] = malloc(sizeof(double) * (size_t)B * NH * Nl[l] * K);
+            if (!sel[l] || !key[l]) { rc = -3; goto done; }
+        }
+    }
+    for (size_t i = 0; i < (size_t)B * Nl[0] * C; ++i) {
+        pq[0][i] = round_to_dtype(a->q[i], a->dtype);
+        pk[0][i] = round_to_dtype(a->k[i], a->dtype);
+        pv[0][i] = round_to_dtype(a->v[i], a->dtype);
+    }
+    for (int l = 1; l < L; ++l) {
+        qo_pool_level(pq[l - 1], B, Hl[l - 1], Wl[l - 1], C, a->dtype, pq[l]);
+        qo_pool_level(pk[l - 1], B, Hl[l - 1], Wl[l - 1], C, a->dtype, pk[l]);
+        qo_pool_level(pv[l - 1], B, Hl[l - 1], Wl[l - 1], C, a->dtype, pv[l]);
+    }
+
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < NH; ++h) {
+            /* ---- coarsest level: every query against every key (Eq. 1) ---- */
+            {
+                const int l = Lc;
+                const size_t N = Nl[l];
+                for (size_t i = 0; i < N; ++i) {
+                    const float* qi = pq[l] + ((size_t)b * N + i) * C + (size_t)h * d;
+                    double mx = -INFINITY;
+                    for (size_t j = 0; j < N; ++j) {
+                        const float* kj = pk[l] + ((size_t)b * N + j) * C + (size_t)h * d;
+                        cx[j] = tau * dot_head(qi, kj, d);
+                        if (cx[j] > mx) mx = cx[j];
+                    }
+                    double den = 0.0;
+                    for (size_t j = 0; j < N; ++j) { ck[j] = exp(cx[j] - mx); den += ck[j]; }
+                    for (size_t j = 0; j < N; ++j) { ck[j] /= den; ci[j] = (int)j; cv[j] = 1; in_sel[j] = 0; }
+
+                    if (L > 1) {
+                        int kept;
+                        int32_t* srow = sel[l] + (((size_t)b * NH + h) * N + i) * K;
+                        double* krow = key[l] + (((size_t)b * NH + h) * N + i) * K;
+                        if (a->forced && a->forced[l]) {
+                            const int32_t* frow = a->forced[l] + (((size_t)b * NH + h) * N + i) * K;
+                            kept = 0;
+                            for (int r = 0; r < K; ++r) {
+                                if (frow[r] < 0) break;
+                                if (frow[r] >= (int32_t)N) { rc = -2; goto done; }
+                                pos[kept++] = frow[r];
+                            }
+                        } else {
+                            kept = select_top_k(ck, ci, cv, (int)N, K, pos, taken);
+                        }
+                        for (int r = 0; r < K; ++r) {
+                            srow[r] = r < kept ? ci[pos[r]] : -1;
+                            krow[r] = r < kept ? ck[pos[r]] : 0.0;
+                        }
+                        /* QuadTree-A: the kept keys are refined at the next level, so this level's
+                         * message covers only the rest of the map (Omega = Gamma - Gamma'). */
+                        if (!isB)
+                            for (int r = 0; r < kept; ++r) in_sel[pos[r]] = 1;
+                    }
+                    for (int c = 0; c < d; ++c) acc[c] = 0.0;
+                    for (size_t j = 0; j < N; ++j) {
+                        if (in_sel[j]) continue;
+                        const float* vj = pv[l] + ((size_t)b * N + j) * C + (size_t)h * d;
+                        for (int c = 0; c < d; ++c) acc[c] += ck[j] * (double)vj[c];
+                    }
+                    double* m = msg[l] + (((size_t)b * N + i) * NH + h) * d;
+                    for (int c = 0; c < d; ++c) m[c] = acc[c];
+                    if (a->cand_key && a->cand_key[l]) {
+                        double* o = a->cand_key[l] + (((size_t)b * NH + h) * N + i) * N;
+                        for (size_t j = 0; j < N; ++j) o[j] = ck[j];
+                    }
+                    if (a->cand_idx && a->cand_idx[l]) {
+                        int32_t* o = a->cand_idx[l] + (((size_t)b * NH + h) * N + i) * N;
+                        for (size_t j = 0; j < N; ++j) o[j] = (int32_t)j;
+                    }
+                }
+            }
+
+            /* ---- finer levels: a query meets the children of its parent's kept keys ---- */
+            for (int l = Lc - 1; l >= 0; --l) {
+                const size_t N = Nl[l], Np = Nl[l + 1];
+                const int Hh = Hl[l], Ww = Wl[l], Wp = Wl[l + 1];
+                const int ncand = 4 * K;
+                for (int y = 0; y < Hh; ++y)
+                    for (int x = 0; x < Ww; ++x) {
+                        const size_t i = (size_t)y * Ww + x;
+                        const size_t P = (size_t)(y >> 1) * Wp + (size_t)(x >> 1);
+                        const int32_t* psel = sel[l + 1] + (((size_t)b * NH + h) * Np + P) * K;
+                        const double* pkey = key[l + 1] + (((size_t)b * NH + h) * Np + P) * K;
+                        const float* qi = pq[l] + ((size_t)b * N + i) * C + (size_t)h * d;
+                        /* candidate slot 4r+c: child c (order (0,0),(0,1),(1,0),(1,1)) of the parent's
+                         * r-th kept key; slots of missing keys or off-map children are invalid */
+                        for (int r = 0; r < K; ++r) {
+                            const int J = psel[r];
+                            for (int c = 0; c < 4; ++c) {
+                                const int s = 4 * r + c;
+                                cv[s] = 0;
+                                ci[s] = -1;
+                                ck[s] = 0.0;
+                                in_sel[s] = 0;
+                                if (J < 0) continue;
+                                const int cy = 2 * (J / Wp) + (c >> 1);
+                                const int cxx = 2 * (J % Wp) + (c & 1);
+                                if (cy >= Hh || cxx >= Ww) continue;
+                                cv[s] = 1;
+                                ci[s] = cy * Ww + cxx;
+                                const float* kj = pk[l] + ((size_t)b * N + ci[s]) * C + (size_t)h * d;
+                                cx[s] = tau * dot_head(qi, kj, d);
+                            }
+                        }
+                        if (isB) {
+                            /* Eq. (6): softmax over every key of the region Gamma */
+                            double mx = -INFINITY, den = 0.0;
+                            for (int s = 0; s < ncand; ++s) if (cv[s] && cx[s] > mx) mx = cx[s];
+                            for (int s = 0; s < ncand; ++s) if (cv[s]) { ck[s] = exp(cx[s] - mx); den += ck[s]; }
+                            for (int s = 0; s < ncand; ++s) if (cv[s]) ck[s] /= den;
+                        } else {
+                            /* Eq. (4): s = s_parent * t, t a softmax over the children of one kept key */
+                            for (int r = 0; r < K; ++r) {
+                                double mx = -INFINITY, den = 0.0;
+                                for (int c = 0; c < 4; ++c) { const int s = 4 * r + c; if (cv[s] && cx[s] > mx) mx = cx[s]; }
+                                for (int c = 0; c < 4; ++c) { const int s = 4 * r + c; if (cv[s]) { ck[s] = exp(cx[s] - mx); den += ck[s]; } }
+                                for (int c = 0; c < 4; ++c) { const int s = 4 * r + c; if (cv[s]) ck[s] = pkey[r] * (ck[s] / den); }
+                            }
+                        }
+                        if (l >= 1) {
+                            int kept;
+                            int32_t* srow = sel[l] + (((size_t)b * NH + h) * N + i) * K;
+                            double* krow = key[l] + (((size_t)b * NH + h) * N + i) * K;
+                            if (a->forced && a->forced[l]) {
+                                const int32_t* frow = a->forced[l] + (((size_t)b * NH + h) * N + i) * K;
+                                kept = 0;
+                                for (int r = 0; r < K; ++r) {
+                                    if (frow[r] < 0) break;
+                                    int found = -1;
+                                    for (int s = 0; s < ncand; ++s) if (cv[s] && ci[s] == frow[r]) found = s;
+                                    if (found < 0) { rc = -2; goto done; }
+                                    pos[kept++] = found;
+                                }
+                            } else {
+                                kept = select_top_k(ck, ci, cv, ncand, K, pos, taken);
+                            }
+                            for (int r = 0; r < K; ++r) {
+                                srow[r] = r < kept ? ci[pos[r]] : -1;
+                                krow[r] = r < kept ? ck[pos[r]] : 0.0;
+                            }
+                            if (!isB)
+                                for (int r = 0; r < kept; ++r) in_sel[pos[r]] = 1;
+                        }
+                        for (int c = 0; c < d; ++c) acc[c] = 0.0;
+                        for (int s = 0; s < ncand; ++s) {
+                            if (!cv[s] || in_sel[s]) continue;
+                            const float* vj = pv[l] + ((size_t)b * N + ci[s]) * C + (size_t)h * d;
+                            for (int c = 0; c < d; ++c) acc[c] += ck[s] * (double)vj[c];
+                        }
+                        double* m = msg[l] + (((size_t)b * N + i) * NH + h) * d;
+                        for (int c = 0; c < d; ++c) m[c] = acc[c];
+                        if (a->cand_key && a->cand_key[l]) {
+                            double* o = a->cand_key[l] + (((size_t)b * NH + h) * N + i) * ncand;
+                            for (int s = 0; s < ncand; ++s) o[s] = cv[s] ? ck[s] : 0.0;
+                        }
+                        if (a->cand_idx && a->cand_idx[l]) {
+                            int32_t* o = a->cand_idx[l] + (((size_t)b * NH + h) * N + i) * ncand;
+                            for (int s = 0; s < ncand; ++s) o[s] = ci[s];
+                        }
+                    }
+            }
+        }
+
+    /* ---- combination: Eq. (2) for A, Eq. (5) for B; a finest query takes the message of its
+     * ancestor at every level, since sub-patches share their parent's coarse messages ---- */
+    if (a->out) {
+        for (int b = 0; b < B; ++b)
+            for (int y = 0; y < H; ++y)
+                for (int x = 0; x < W; ++x)
+                    for (int h = 0; h < NH; ++h) {
+                        const size_t i = (size_t)y * W + x;
+                        double* o = a->out + (((size_t)b * Nl[0] + i) * NH + h) * d;
+                        for (int c = 0; c < d; ++c) o[c] = 0.0;
+                        for (int l = 0; l < L; ++l) {
+                            const size_t anc = (size_t)(y >> l) * Wl[l] + (size_t)(x >> l);
+                            double wl = 1.0;
+                            if (isB) wl = a->w ? (double)a->w[(((size_t)b * Nl[0] + i) * NH + h) * L + l] : 1.0 / L;
+                            const double* m = msg[l] + (((size_t)b * Nl[l] + anc) * NH + h) * d;
+                            for (int c = 0; c < d; ++c) o[c] += wl * m[c];
+                        }
+                    }
+    }
+
+    /* ---- copy requested intermediates ---- */
+    for (int l = 0; l < L; ++l) {
+        const size_t n = (size_t)B * Nl[l] * C;
+        if (l >= 1) {
+            if (a->pyr_q && a->pyr_q[l]) memcpy(a->pyr_q[l], pq[l], sizeof(float) * n);
+            if (a->pyr_k && a->pyr_k[l]) memcpy(a->pyr_k[l], pk[l], sizeof(float) * n);
+            if (a->pyr_v && a->pyr_v[l]) memcpy(a->pyr_v[l], pv[l], sizeof(float) * n);
+            if (a->sel_idx && a->sel_idx[l]) memcpy(a->sel_idx[l], sel[l], sizeof(int32_t) * (size_t)B * NH * Nl[l] * K);
+            if (a->sel_key && a->sel_key[l]) memcpy(a->sel_key[l], key[l], sizeof(double) * (size_t)B * NH * Nl[l] * K);
+        }
+        if (a->msg && a->msg[l]) memcpy(a->msg[l], msg[l], sizeof(double) * (size_t)B * Nl[l] * NH * d);
+    }
+
+done:
+    for (int l = 0; l < QO_MAX_LEVELS; ++l) {
+        free(pq[l]); free(pk[l]); free(pv[l]); free(msg[l]); free(sel[l]); free(key[l]);
+    }
+    free(ck); free(ci); free(cv); free(cx); free(pos); free(taken); free(in_sel); free(acc);
+    return rc;
+}
