@@ -1,0 +1,196 @@
+"""Benchmark: query tokens/s of one QuadTree attention layer on one MI355X.
+
+A step is one whole forward (pyramids, coarse attention with top-K, every finer level, the fused
+combination) over one batch of synthetic input that is already resident in HBM. The default
+workload is the feature-matching layer (1 x 60x80 tokens, 8 heads x 32, fp32, 3 levels, K=8,
+QuadTree-B). Prints one JSON line with the throughput, the finest-level kernel's HBM roofline
+fraction (timed with HIP events on its own stream) and the CPU oracle timed on the host.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "query tokens/sec per QuadTree attention layer + % of HBM/MFMA roofline, 1 GPU"
+HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+FINE_SRC = os.path.join(ROOT, "paper_2201_02767_amd", "csrc", "fine.hip")
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def finest_kernel_bytes(wl) -> dict:
+    """Algorithmic HBM bytes of one launch of the finest-level kernel (attention at level 0 with the
+    fused combination), counting every tensor once plus one gather of each sibling group's
+    candidate key and value rows:
+      per (batch, head):  N0*d*b (queries) + N1*K*sigma (parent selections; sigma = 4 B for B, 8 B
+      for A, which also reads the scores) + N1*4K*2*d*b (gathered key/value rows, four children per
+      kept key) + N1*(L-1)*d*4 (the ancestors' fp32 messages, once per sibling group)
+      + [B] N0*L*4 (level weights) + N0*d*b (output)."""
+    from paper_2201_02767_amd.inputs import Workload  # noqa: F401  (type only)
+    import paper_2201_02767_amd as P
+
+    dims = P.level_dims(wl.H, wl.W, wl.levels)
+    n0 = dims[0][0] * dims[0][1]
+    n1 = dims[1][0] * dims[1][1]
+    b = 2 if wl.dtype == "bf16" else 4
+    sigma = 4 if wl.variant == "B" else 8
+    parts = {
+        "queries": n0 * wl.d * b,
+        "parent_selections": n1 * wl.K * sigma,
+        "gather": n1 * 4 * wl.K * 2 * wl.d * b,
+        "ancestor_messages": n1 * (wl.levels - 1) * wl.d * 4,
+        "level_weights": n0 * wl.levels * 4 if wl.variant == "B" else 0,
+        "output": n0 * wl.d * b,
+    }
+    units = wl.B * wl.heads
+    return {k: v * units for k, v in parts.items()}
+
+
+def kernel_source_hash() -> str:
+    with open(FINE_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken on the
+    current kernel source; None otherwise."""
+    path = os.path.join(PROFILES, f"fine_attn_finest_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, seconds: float) -> dict:
+    """The oracle as it stands, single-threaded on the host, on whole layers of the workload."""
+    from paper_2201_02767_amd.inputs import make_level_weights, make_qkv
+    from oracle import oracle
+
+    q, k, v = make_qkv(wl)
+    w = make_level_weights(wl) if wl.variant == "B" else None
+    runs, t0 = 0, time.perf_counter()
+    while True:
+        oracle.forward(q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w)
+        runs += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": wl.tokens * runs / el, "unit": "query tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{runs} whole {wl.name} layer(s) ({wl.B}x{wl.H}x{wl.W}, {wl.heads}x{wl.d}, L={wl.levels}, "
+                      f"K={wl.K}) in {el:.1f} s, one thread"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="matching")
+    ap.add_argument("--kernel-launches", type=int, default=500, help="launches timed for the roofline kernel")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}). "
+              "Each (batch, head) is an independent quadtree, so a multi-GPU run would shard batch x heads with "
+              "no communication; no multi-GPU figure is produced.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2201_02767_amd as P
+    from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_qkv
+
+    if args.workload not in WORKLOADS:
+        print(f"unknown workload {args.workload}; choose from {sorted(WORKLOADS)}", file=sys.stderr)
+        return 2
+    wl = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    q, k, v = (torch.from_numpy(x).to(dev).to(tdt).contiguous() for x in make_qkv(wl))
+    w = torch.from_numpy(make_level_weights(wl)).to(dev) if wl.variant == "B" else None
+    plan = P.Plan(wl.B, wl.H, wl.W, wl.heads, wl.d, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=tdt,
+                  device=dev)
+    step = plan.prepare(q, k, v, w)
+    log(f"bench: {wl} on {torch.cuda.get_device_name(0)}")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    value = wl.tokens / (ms_per_step / 1e3)
+    log(f"bench: {args.steps} steps, {ms_per_step * 1e3:.2f} us/step (events), wall {wall * 1e3 / args.steps:.2f} "
+        f"us/step, {value:.4g} query tokens/s")
+
+    # the dominant kernel alone, on the same stream, on the selections the forward left behind
+    roof = None
+    if wl.levels >= 2:
+        finest = plan.prepare_finest(q, k, v, w)
+        for _ in range(10):
+            finest()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.kernel_launches):
+            finest()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        k_us = e0.elapsed_time(e1) * 1e3 / args.kernel_launches
+        parts = finest_kernel_bytes(wl)
+        algo = sum(parts.values())
+        achieved = algo / (k_us * 1e-6) / 1e9
+        traffic = measured_traffic(wl.name)
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": "fine_attn_kernel (finest level, fused combine)", "kernel_us": round(k_us, 3),
+                "algorithmic_bytes": algo}
+        log(f"bench: finest-level kernel {k_us:.2f} us/launch, {algo / 1e6:.1f} MB algorithmic -> "
+            f"{achieved:.0f} GB/s ({100 * achieved / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f})")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, args.cpu_seconds)
+        log(f"bench: oracle {cpu['value']:.4g} query tokens/s ({cpu['sample']})")
+
+    rec = {
+        "metric": METRIC, "value": round(value, 1), "unit": "query tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32" if wl.dtype == "f32" else "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "W": wl.W, "heads": wl.heads, "d": wl.d,
+                   "levels": wl.levels, "K": wl.K, "variant": wl.variant, "global_batch": wl.B,
+                   "seq_len": wl.H * wl.W, "parallelism": "none (1 GPU)"},
+        "roofline": roof, "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,195 @@
+/*
+ * qta.h - QuadTree attention forward on AMD Instinct MI355X (gfx950): the C ABI.
+ *
+ * The method is QuadTree attention (Tang et al., "QuadTree Attention for Vision Transformers",
+ * ICLR 2022), Sec. 3.2. For every query token it computes a message from all key tokens in a
+ * coarse-to-fine manner:
+ *   1. L-level pyramids of Q, K and V by 2x2 average pooling (Sec. 3.2, pyramid paragraph);
+ *   2. at the coarsest level every query attends to every key, Eq. (1);
+ *   3. each query keeps the K keys with the highest attention scores (Sec. 3.2, Fig. 1);
+ *   4. at each finer level a query attends only to the 2x2 children of its parent query's kept
+ *      keys; the four sibling queries of one parent share that candidate set (Fig. 1 caption);
+ *   5. the per-level messages are combined: QuadTree-A sums partial messages over the disjoint
+ *      regions Omega^l (Eqs. 2-4), QuadTree-B takes a weighted sum of per-level attention over
+ *      the overlapping regions Gamma^l (Eqs. 5-6).
+ *
+ * Conventions shared by every call
+ *   - Level l = 0 is the finest level (the input map), l = L-1 the coarsest. Level l+1 has
+ *     ceil(H_l/2) x ceil(W_l/2) tokens; token (y,x) at level l+1 averages its children
+ *     (2y+dy, 2x+dx) at level l that lie inside the map (a missing child is not counted).
+ *   - Token tensors are NHWC, [B][H][W][heads][d] contiguous (C = heads*d channels), in the
+ *     storage type `dtype` (fp32 or bf16). Pyramid levels use the same layout at their size.
+ *   - Flat token index at level l: y*W_l + x.
+ *   - Messages are fp32 [B][N_l][heads][d]. Selections are int32 [B][heads][N_l][K] holding flat
+ *     key indices of level l, sorted by (score descending, index ascending); a query with fewer
+ *     than K candidates is padded with -1. Scores are fp32 in the same shape (0 where the index
+ *     is -1): QuadTree-B stores the softmax probability, QuadTree-A the recursive score s.
+ *   - Each head is an independent quadtree. Softmax temperature: `scale` if > 0, else 1/sqrt(d).
+ *   - Ties in a top-K selection go to the lower flat index.
+ *
+ * Memory and errors
+ *   - Every tensor pointer is a DEVICE pointer that the caller owns; the library never
+ *     allocates, frees, synchronises or copies back. Every call is asynchronous on `stream`
+ *     (a hipStream_t; NULL is the null stream).
+ *   - Arguments are validated on the host before any launch. Invalid shapes or null pointers
+ *     return QTA_ERR_INVALID, shapes the kernels do not support QTA_ERR_UNSUPPORTED, a too-small
+ *     workspace QTA_ERR_WORKSPACE; a failed launch returns QTA_ERR_HIP. Faults that happen on
+ *     the device surface at the caller's next synchronisation.
+ *   - Supported: d in {32, 64}; 1 <= K <= QTA_MAX_K; coarsest level N_{L-1} <= QTA_MAX_COARSE;
+ *     1 <= L <= QTA_MAX_LEVELS with no level above a 1x1 map; token pointers 16-byte aligned.
+ *   - K larger than a query's candidate count is not an error: min(K, count) keys are kept.
+ *   - Inputs must be finite; outputs must not alias inputs. Calls are re-entrant: the library
+ *     holds no state.
+ */
+#ifndef QTA_H
+#define QTA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QTA_MAX_LEVELS 16
+#define QTA_MAX_K 64
+#define QTA_MAX_COARSE 1024
+
+typedef enum {
+    QTA_OK = 0,
+    QTA_ERR_INVALID = 1,
+    QTA_ERR_UNSUPPORTED = 2,
+    QTA_ERR_WORKSPACE = 3,
+    QTA_ERR_HIP = 4
+} qta_status;
+
+typedef enum { QTA_VARIANT_A = 0, QTA_VARIANT_B = 1 } qta_variant;
+
+typedef enum { QTA_F32 = 0, QTA_BF16 = 1 } qta_dtype;
+
+/* Byte offsets of the regions qta_forward keeps in its workspace. Entries for levels that do not
+ * exist (and level 0 of q/k/v, msg, sel_idx, sel_key, which live outside it) are 0. */
+typedef struct {
+    int levels;
+    int H[QTA_MAX_LEVELS];
+    int W[QTA_MAX_LEVELS];
+    size_t q[QTA_MAX_LEVELS];       /* pyramid level l >= 1, [B][H_l][W_l][C] dtype       */
+    size_t k[QTA_MAX_LEVELS];
+    size_t v[QTA_MAX_LEVELS];
+    size_t msg[QTA_MAX_LEVELS];     /* level l >= 1, fp32 [B][N_l][heads][d]               */
+    size_t sel_idx[QTA_MAX_LEVELS]; /* level l >= 1, int32 [B][heads][N_l][K]              */
+    size_t sel_key[QTA_MAX_LEVELS]; /* level l >= 1, fp32  [B][heads][N_l][K]              */
+    size_t total;                   /* bytes; every region starts on a 256-byte boundary   */
+} qta_workspace_layout;
+
+/* Human-readable name of a status code (static storage). */
+const char* qta_status_str(qta_status status);
+
+/* Level sizes for an H x W map with `levels` levels (ceil halving). Hl, Wl: host arrays of at
+ * least `levels` ints. */
+qta_status qta_level_dims(int H, int W, int levels, int* Hl, int* Wl);
+
+/* Workspace regions used by qta_forward for this problem (host struct, filled in). */
+qta_status qta_get_workspace_layout(int B, int heads, int H, int W, int d, int levels, int K,
+                                    qta_dtype dtype, qta_workspace_layout* layout);
+
+/* Bytes of workspace qta_forward needs (at least 256 for every valid problem); 0 if the arguments
+ * are invalid or unsupported. */
+size_t qta_workspace_bytes(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype);
+
+/*
+ * qta_forward - the whole QuadTree attention forward (Sec. 3.2, Eqs. 1-6).
+ *   q, k, v    [B][H][W][heads][d] dtype. Query and key maps have the same H x W.
+ *   w          QuadTree-B level weights, fp32 [B][H*W][heads][levels] (level 0 = finest), used as
+ *              given; NULL means 1/levels for every weight. Ignored by QuadTree-A.
+ *   out        [B][H][W][heads][d] dtype: out_i = sum_l m^l of the ancestor of i at level l (A) or
+ *              sum_l w_{i,l} m^l (B). With levels == 1 this is plain attention, Eq. (1) (times w for B).
+ *   workspace  device buffer of at least qta_workspace_bytes(...) bytes, 256-byte aligned; after
+ *              the call it holds the pyramids, messages and selections at the offsets that
+ *              qta_get_workspace_layout reports.
+ * Launches ceil((L-1)/2) pyramid passes, one coarse-attention kernel and one fine-attention
+ * kernel per finer level, in stream order.
+ */
+qta_status qta_forward(const void* q, const void* k, const void* v, const float* w,
+                       int B, int heads, int H, int W, int d, int levels, int K,
+                       qta_variant variant, qta_dtype dtype, float scale,
+                       void* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * qta_build_pyramid - step 1: levels 1..levels-1 of one token map by 2x2 average pooling
+ * (Sec. 3.2). Each level is pooled from the stored level below it: the valid children are summed
+ * in fp32 as ((c00 + c01) + (c10 + c11)), missing children left out, multiplied by 1/count and
+ * rounded to nearest-even in dtype.
+ *   x           [B][H][W][C] dtype, C*sizeof(dtype) a multiple of 16 bytes.
+ *   levels_out  levels 1..levels-1 back to back, level l at element offset
+ *               sum_{1<=j<l} B*H_j*W_j*C, each [B][H_l][W_l][C] dtype.
+ */
+qta_status qta_build_pyramid(const void* x, void* levels_out, int B, int H, int W, int C, int levels,
+                             qta_dtype dtype, void* stream);
+
+/*
+ * qta_coarse_attn - steps 2-3 at the coarsest level (Eq. 1 over the whole Hc x Wc map).
+ *   qc, kc, vc  coarsest pyramid level, [B][Hc][Wc][heads][d] dtype; Hc*Wc <= QTA_MAX_COARSE.
+ *   msg         fp32 [B][Hc*Wc][heads][d].
+ *   sel_idx, sel_key  [B][heads][Hc*Wc][K]: the min(K, Hc*Wc) keys of highest probability.
+ *               Both NULL: no selection (a single-level problem) and msg is full attention for
+ *               either variant. Otherwise both must be given; QuadTree-A's msg then leaves out
+ *               the kept keys (they are refined at the next level, Omega = Gamma - Gamma'),
+ *               QuadTree-B's msg covers all keys.
+ */
+qta_status qta_coarse_attn(const void* qc, const void* kc, const void* vc,
+                           int B, int heads, int Hc, int Wc, int d, int K,
+                           qta_variant variant, qta_dtype dtype, float scale,
+                           float* msg, int32_t* sel_idx, float* sel_key, void* stream);
+
+/*
+ * qta_topk - step 3 as a standalone row-wise selection.
+ *   keys      fp32 [rows][n]; cand_idx int32 [rows][n] naming each candidate (entries < 0 are not
+ *             candidates), or NULL for the column index. 1 <= n <= 4096, 1 <= K <= QTA_MAX_K.
+ *   idx_out   int32 [rows][K]: the names of the min(K, #candidates) largest keys, ordered by
+ *             (key descending, name ascending), padded with -1.
+ *   key_out   fp32 [rows][K] (may be NULL): their keys, 0 in padded slots.
+ */
+qta_status qta_topk(const float* keys, const int32_t* cand_idx, int rows, int n, int K,
+                    int32_t* idx_out, float* key_out, void* stream);
+
+/*
+ * qta_fine_attn - steps 3-4 at an intermediate level l (0 < l < L-1): every query of the
+ * Hl x Wl map attends to the 2x2 children of the keys its parent kept at level l+1.
+ *   ql, kl, vl  level l, [B][Hl][Wl][heads][d] dtype.
+ *   parent_idx  int32 [B][heads][Np][K] selections of level l+1 (Np = ceil(Hl/2)*ceil(Wl/2)).
+ *   parent_key  fp32 same shape: the parents' scores; required for QuadTree-A, ignored by B.
+ *   msg         fp32 [B][Hl*Wl][heads][d]. B: softmax over all candidates, Eq. (6).
+ *               A: s = s_parent * t with t a softmax over the 2x2 children of one kept key
+ *               (Eq. 4); the message sums s*v over the candidates this query does not keep
+ *               (Eq. 3 over Omega).
+ *   sel_idx, sel_key  [B][heads][Hl*Wl][K]: this level's selections (B by probability, A by s).
+ */
+qta_status qta_fine_attn(const void* ql, const void* kl, const void* vl,
+                         int B, int heads, int Hl, int Wl, int d, int K,
+                         qta_variant variant, qta_dtype dtype, float scale,
+                         const int32_t* parent_idx, const float* parent_key,
+                         float* msg, int32_t* sel_idx, float* sel_key, void* stream);
+
+/*
+ * qta_finest_attn - steps 4-5 at level 0, with the combination fused in (Eqs. 2 and 5).
+ *   q0, k0, v0  [B][H][W][heads][d] dtype (the inputs of qta_forward).
+ *   parent_idx, parent_key  selections of level 1 as in qta_fine_attn.
+ *   coarser_msg host array of levels-1 device pointers: entry j-1 is the fp32 message of level j,
+ *               [B][N_j][heads][d], j = 1..levels-1.
+ *   w           as in qta_forward (B only; NULL means 1/levels).
+ *   out         [B][H][W][heads][d] dtype. Each query adds its own level-0 message and the
+ *               messages of its ancestors (y >> j, x >> j) at every coarser level j.
+ */
+qta_status qta_finest_attn(const void* q0, const void* k0, const void* v0,
+                           int B, int heads, int H, int W, int d, int K,
+                           qta_variant variant, qta_dtype dtype, float scale,
+                           const int32_t* parent_idx, const float* parent_key,
+                           int levels, const float* const* coarser_msg, const float* w,
+                           void* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QTA_H */

@@ -1,0 +1,418 @@
+// C ABI of the QuadTree attention library: argument validation, level geometry, workspace layout
+// and the launch sequence of qta_forward. Everything here runs on the host; validation finishes
+// before the first launch, and nothing allocates, synchronises or copies.
+#include <stddef.h>
+#include <stdint.h>
+
+#include "qta_internal.h"
+
+using namespace qta;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+size_t dtype_bytes(qta_dtype t) { return t == QTA_BF16 ? 2 : 4; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool dtype_ok(qta_dtype t) { return t == QTA_F32 || t == QTA_BF16; }
+
+bool variant_ok(qta_variant v) { return v == QTA_VARIANT_A || v == QTA_VARIANT_B; }
+
+// Level sizes by ceil halving. INVALID unless every level but the coarsest holds more than one
+// token (a level above a 1x1 map would repeat it).
+qta_status dims(int H, int W, int levels, int* Hl, int* Wl)
+{
+    if (H <= 0 || W <= 0 || levels <= 0) return QTA_ERR_INVALID;
+    if (levels > QTA_MAX_LEVELS) return QTA_ERR_INVALID;
+    if (static_cast<long long>(H) * W > 0x3FFFFFFFLL) return QTA_ERR_UNSUPPORTED;
+    Hl[0] = H;
+    Wl[0] = W;
+    for (int l = 1; l < levels; ++l) {
+        if (Hl[l - 1] == 1 && Wl[l - 1] == 1) return QTA_ERR_INVALID;
+        Hl[l] = (Hl[l - 1] + 1) / 2;
+        Wl[l] = (Wl[l - 1] + 1) / 2;
+    }
+    return QTA_OK;
+}
+
+// Shape checks shared by the attention calls.
+qta_status check_problem(int B, int heads, int d, int K, qta_variant variant, qta_dtype dtype)
+{
+    if (B <= 0 || heads <= 0 || d <= 0 || K <= 0) return QTA_ERR_INVALID;
+    if (!variant_ok(variant) || !dtype_ok(dtype)) return QTA_ERR_INVALID;
+    if (d != 32 && d != 64) return QTA_ERR_UNSUPPORTED;
+    if (K > QTA_MAX_K) return QTA_ERR_UNSUPPORTED;
+    if (static_cast<long long>(heads) * d > (1 << 20)) return QTA_ERR_UNSUPPORTED;
+    return QTA_OK;
+}
+
+qta_status layout(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype, qta_workspace_layout* L)
+{
+    qta_status st = check_problem(B, heads, d, K, QTA_VARIANT_B, dtype);
+    if (st != QTA_OK) return st;
+    int Hl[QTA_MAX_LEVELS], Wl[QTA_MAX_LEVELS];
+    st = dims(H, W, levels, Hl, Wl);
+    if (st != QTA_OK) return st;
+    if (static_cast<long long>(Hl[levels - 1]) * Wl[levels - 1] > QTA_MAX_COARSE) return QTA_ERR_UNSUPPORTED;
+    *L = qta_workspace_layout{};
+    L->levels = levels;
+    const size_t C = static_cast<size_t>(heads) * d;
+    size_t off = 0;
+    for (int l = 0; l < levels; ++l) {
+        L->H[l] = Hl[l];
+        L->W[l] = Wl[l];
+    }
+    for (int l = 1; l < levels; ++l) {
+        const size_t N = static_cast<size_t>(Hl[l]) * Wl[l];
+        const size_t tok = static_cast<size_t>(B) * N * C * dtype_bytes(dtype);
+        L->q[l] = off;
+        off = align_up(off + tok);
+        L->k[l] = off;
+        off = align_up(off + tok);
+        L->v[l] = off;
+        off = align_up(off + tok);
+        L->msg[l] = off;
+        off = align_up(off + static_cast<size_t>(B) * N * C * sizeof(float));
+        L->sel_idx[l] = off;
+        off = align_up(off + static_cast<size_t>(B) * heads * N * K * sizeof(int32_t));
+        L->sel_key[l] = off;
+        off = align_up(off + static_cast<size_t>(B) * heads * N * K * sizeof(float));
+    }
+    L->total = off > kAlign ? off : kAlign;   // nonzero for every valid problem
+    return QTA_OK;
+}
+
+float resolve_scale(float scale, int d) { return scale > 0.f ? scale : 1.0f / __builtin_sqrtf(static_cast<float>(d)); }
+
+qta_status launch_status(hipError_t e) { return e == hipSuccess ? QTA_OK : QTA_ERR_HIP; }
+
+// Pyramid passes: from level s produce s+1 and, when it exists, s+2; repeat from s+2.
+hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], int ntensors, int B, const int* Hl,
+                       const int* Wl, int levels, int chunks, bool use_bf16, hipStream_t stream)
+{
+    for (int s = 0; s + 1 < levels; s += 2) {
+        const int nlev = (s + 2 < levels) ? 2 : 1;
+        PyramidPassArgs a{};
+        for (int t = 0; t < ntensors; ++t) {
+            a.src[t] = s == 0 ? src0[t] : lvl[t][s];
+            a.dst1[t] = lvl[t][s + 1];
+            a.dst2[t] = nlev == 2 ? lvl[t][s + 2] : nullptr;
+        }
+        a.B = B;
+        a.Hs = Hl[s];
+        a.Ws = Wl[s];
+        a.H1 = Hl[s + 1];
+        a.W1 = Wl[s + 1];
+        a.H2 = nlev == 2 ? Hl[s + 2] : 0;
+        a.W2 = nlev == 2 ? Wl[s + 2] : 0;
+        a.chunks = chunks;
+        hipError_t e = launch_pyramid_pass(a, nlev, ntensors, use_bf16, stream);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* qta_status_str(qta_status status)
+{
+    switch (status) {
+    case QTA_OK: return "ok";
+    case QTA_ERR_INVALID: return "invalid argument";
+    case QTA_ERR_UNSUPPORTED: return "unsupported shape or type";
+    case QTA_ERR_WORKSPACE: return "workspace too small";
+    case QTA_ERR_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+qta_status qta_level_dims(int H, int W, int levels, int* Hl, int* Wl)
+{
+    if (!Hl || !Wl) return QTA_ERR_INVALID;
+    return dims(H, W, levels, Hl, Wl);
+}
+
+qta_status qta_get_workspace_layout(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype,
+                                    qta_workspace_layout* out)
+{
+    if (!out) return QTA_ERR_INVALID;
+    return layout(B, heads, H, W, d, levels, K, dtype, out);
+}
+
+size_t qta_workspace_bytes(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype)
+{
+    qta_workspace_layout L;
+    if (layout(B, heads, H, W, d, levels, K, dtype, &L) != QTA_OK) return 0;
+    return L.total;
+}
+
+qta_status qta_build_pyramid(const void* x, void* levels_out, int B, int H, int W, int C, int levels, qta_dtype dtype,
+                             void* stream)
+{
+    if (!x || !levels_out || B <= 0 || C <= 0 || !dtype_ok(dtype)) return QTA_ERR_INVALID;
+    if (!aligned16(x) || !aligned16(levels_out)) return QTA_ERR_INVALID;
+    if ((static_cast<size_t>(C) * dtype_bytes(dtype)) % 16 != 0) return QTA_ERR_UNSUPPORTED;
+    int Hl[QTA_MAX_LEVELS], Wl[QTA_MAX_LEVELS];
+    qta_status st = dims(H, W, levels, Hl, Wl);
+    if (st != QTA_OK) return st;
+    if (levels == 1) return QTA_OK;
+    void* lvl[1][QTA_MAX_LEVELS] = {};
+    size_t off = 0;
+    for (int l = 1; l < levels; ++l) {
+        lvl[0][l] = static_cast<char*>(levels_out) + off;
+        off += static_cast<size_t>(B) * Hl[l] * Wl[l] * C * dtype_bytes(dtype);
+    }
+    const void* src[1] = {x};
+    const int chunks = static_cast<int>(static_cast<size_t>(C) * dtype_bytes(dtype) / 16);
+    return launch_status(run_pyramid(src, lvl, 1, B, Hl, Wl, levels, chunks, dtype == QTA_BF16,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+qta_status qta_coarse_attn(const void* qc, const void* kc, const void* vc, int B, int heads, int Hc, int Wc, int d,
+                           int K, qta_variant variant, qta_dtype dtype, float scale, float* msg, int32_t* sel_idx,
+                           float* sel_key, void* stream)
+{
+    qta_status st = check_problem(B, heads, d, K, variant, dtype);
+    if (st != QTA_OK) return st;
+    if (!qc || !kc || !vc || !msg) return QTA_ERR_INVALID;
+    if ((sel_idx == nullptr) != (sel_key == nullptr)) return QTA_ERR_INVALID;
+    if (!aligned16(qc) || !aligned16(kc) || !aligned16(vc) || !aligned16(msg)) return QTA_ERR_INVALID;
+    if (Hc <= 0 || Wc <= 0) return QTA_ERR_INVALID;
+    if (static_cast<long long>(Hc) * Wc > QTA_MAX_COARSE) return QTA_ERR_UNSUPPORTED;
+    CoarseArgs a{};
+    a.q = qc;
+    a.k = kc;
+    a.v = vc;
+    a.B = B;
+    a.heads = heads;
+    a.N = Hc * Wc;
+    a.C = heads * d;
+    a.K = sel_idx ? K : 0;
+    a.scale = resolve_scale(scale, d);
+    a.msg = msg;
+    a.sel_idx = sel_idx;
+    a.sel_key = sel_key;
+    a.levels = 1;
+    return launch_status(launch_coarse_attn(a, d, variant == QTA_VARIANT_A, dtype == QTA_BF16,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+qta_status qta_topk(const float* keys, const int32_t* cand_idx, int rows, int n, int K, int32_t* idx_out,
+                    float* key_out, void* stream)
+{
+    if (!keys || !idx_out || rows <= 0 || n <= 0 || K <= 0) return QTA_ERR_INVALID;
+    if (n > 4096 || K > QTA_MAX_K) return QTA_ERR_UNSUPPORTED;
+    if (static_cast<long long>(rows) * n > (1LL << 40)) return QTA_ERR_UNSUPPORTED;
+    TopkArgs a{keys, cand_idx, rows, n, K, idx_out, key_out};
+    return launch_status(launch_topk(a, static_cast<hipStream_t>(stream)));
+}
+
+qta_status qta_fine_attn(const void* ql, const void* kl, const void* vl, int B, int heads, int Hl, int Wl, int d, int K,
+                         qta_variant variant, qta_dtype dtype, float scale, const int32_t* parent_idx,
+                         const float* parent_key, float* msg, int32_t* sel_idx, float* sel_key, void* stream)
+{
+    qta_status st = check_problem(B, heads, d, K, variant, dtype);
+    if (st != QTA_OK) return st;
+    if (!ql || !kl || !vl || !parent_idx || !msg || !sel_idx || !sel_key) return QTA_ERR_INVALID;
+    if (variant == QTA_VARIANT_A && !parent_key) return QTA_ERR_INVALID;
+    if (!aligned16(ql) || !aligned16(kl) || !aligned16(vl) || !aligned16(msg)) return QTA_ERR_INVALID;
+    if (Hl <= 0 || Wl <= 0 || (Hl == 1 && Wl == 1)) return QTA_ERR_INVALID;
+    if (static_cast<long long>(Hl) * Wl > 0x3FFFFFFFLL) return QTA_ERR_UNSUPPORTED;
+    FineArgs a{};
+    a.q = ql;
+    a.k = kl;
+    a.v = vl;
+    a.B = B;
+    a.heads = heads;
+    a.H = Hl;
+    a.W = Wl;
+    a.Hp = (Hl + 1) / 2;
+    a.Wp = (Wl + 1) / 2;
+    a.C = heads * d;
+    a.K = K;
+    a.scale = resolve_scale(scale, d);
+    a.parent_idx = parent_idx;
+    a.parent_key = parent_key;
+    a.msg = msg;
+    a.sel_idx = sel_idx;
+    a.sel_key = sel_key;
+    return launch_status(launch_fine_attn(a, d, variant == QTA_VARIANT_A, dtype == QTA_BF16, false,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+qta_status qta_finest_attn(const void* q0, const void* k0, const void* v0, int B, int heads, int H, int W, int d, int K,
+                           qta_variant variant, qta_dtype dtype, float scale, const int32_t* parent_idx,
+                           const float* parent_key, int levels, const float* const* coarser_msg, const float* w,
+                           void* out, void* stream)
+{
+    qta_status st = check_problem(B, heads, d, K, variant, dtype);
+    if (st != QTA_OK) return st;
+    if (!q0 || !k0 || !v0 || !parent_idx || !out || !coarser_msg) return QTA_ERR_INVALID;
+    if (variant == QTA_VARIANT_A && !parent_key) return QTA_ERR_INVALID;
+    if (!aligned16(q0) || !aligned16(k0) || !aligned16(v0) || !aligned16(out)) return QTA_ERR_INVALID;
+    if (levels < 2) return QTA_ERR_INVALID;
+    int Hl[QTA_MAX_LEVELS], Wl[QTA_MAX_LEVELS];
+    st = dims(H, W, levels, Hl, Wl);
+    if (st != QTA_OK) return st;
+    FineArgs a{};
+    a.q = q0;
+    a.k = k0;
+    a.v = v0;
+    a.B = B;
+    a.heads = heads;
+    a.H = H;
+    a.W = W;
+    a.Hp = Hl[1];
+    a.Wp = Wl[1];
+    a.C = heads * d;
+    a.K = K;
+    a.scale = resolve_scale(scale, d);
+    a.parent_idx = parent_idx;
+    a.parent_key = parent_key;
+    a.out = out;
+    a.w = w;
+    a.levels = levels;
+    for (int l = 1; l < levels; ++l) {
+        if (!coarser_msg[l - 1] || !aligned16(coarser_msg[l - 1])) return QTA_ERR_INVALID;
+        a.coarser_msg[l] = coarser_msg[l - 1];
+        a.lvl_W[l] = Wl[l];
+        a.lvl_N[l] = Hl[l] * Wl[l];
+    }
+    return launch_status(launch_fine_attn(a, d, variant == QTA_VARIANT_A, dtype == QTA_BF16, true,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+qta_status qta_forward(const void* q, const void* k, const void* v, const float* w, int B, int heads, int H, int W,
+                       int d, int levels, int K, qta_variant variant, qta_dtype dtype, float scale, void* out,
+                       void* workspace, size_t workspace_bytes, void* stream)
+{
+    qta_status st = check_problem(B, heads, d, K, variant, dtype);
+    if (st != QTA_OK) return st;
+    if (!q || !k || !v || !out) return QTA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return QTA_ERR_INVALID;
+    qta_workspace_layout L;
+    st = layout(B, heads, H, W, d, levels, K, dtype, &L);
+    if (st != QTA_OK) return st;
+    if (levels > 1) {
+        if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return QTA_ERR_INVALID;
+        if (workspace_bytes < L.total) return QTA_ERR_WORKSPACE;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool use_bf16 = dtype == QTA_BF16;
+    const bool va = variant == QTA_VARIANT_A;
+    const float tau = resolve_scale(scale, d);
+    const int C = heads * d;
+    char* ws = static_cast<char*>(workspace);
+    const void* lv[3][QTA_MAX_LEVELS] = {};
+    void* pyr[3][QTA_MAX_LEVELS] = {};
+    lv[0][0] = q;
+    lv[1][0] = k;
+    lv[2][0] = v;
+    for (int l = 1; l < levels; ++l) {
+        pyr[0][l] = ws + L.q[l];
+        pyr[1][l] = ws + L.k[l];
+        pyr[2][l] = ws + L.v[l];
+        for (int t = 0; t < 3; ++t) lv[t][l] = pyr[t][l];
+    }
+    auto msg = [&](int l) { return reinterpret_cast<float*>(ws + L.msg[l]); };
+    auto sidx = [&](int l) { return reinterpret_cast<int32_t*>(ws + L.sel_idx[l]); };
+    auto skey = [&](int l) { return reinterpret_cast<float*>(ws + L.sel_key[l]); };
+
+    // 1. pyramids of q, k and v
+    if (levels > 1) {
+        const void* src[3] = {q, k, v};
+        const int chunks = static_cast<int>(static_cast<size_t>(C) * dtype_bytes(dtype) / 16);
+        hipError_t e = run_pyramid(src, pyr, 3, B, L.H, L.W, levels, chunks, use_bf16, s);
+        if (e != hipSuccess) return QTA_ERR_HIP;
+    }
+
+    // 2-3. coarsest level
+    const int c = levels - 1;
+    {
+        CoarseArgs a{};
+        a.q = lv[0][c];
+        a.k = lv[1][c];
+        a.v = lv[2][c];
+        a.B = B;
+        a.heads = heads;
+        a.N = L.H[c] * L.W[c];
+        a.C = C;
+        a.scale = tau;
+        a.levels = levels;
+        if (levels == 1) {
+            a.K = 0;
+            a.out = out;
+            a.w = w;
+        } else {
+            a.K = K;
+            a.msg = msg(c);
+            a.sel_idx = sidx(c);
+            a.sel_key = skey(c);
+        }
+        hipError_t e = launch_coarse_attn(a, d, va, use_bf16, s);
+        if (e != hipSuccess) return QTA_ERR_HIP;
+    }
+    if (levels == 1) return QTA_OK;
+
+    // 3-4. intermediate levels, coarse to fine
+    for (int l = c - 1; l >= 1; --l) {
+        FineArgs a{};
+        a.q = lv[0][l];
+        a.k = lv[1][l];
+        a.v = lv[2][l];
+        a.B = B;
+        a.heads = heads;
+        a.H = L.H[l];
+        a.W = L.W[l];
+        a.Hp = L.H[l + 1];
+        a.Wp = L.W[l + 1];
+        a.C = C;
+        a.K = K;
+        a.scale = tau;
+        a.parent_idx = sidx(l + 1);
+        a.parent_key = skey(l + 1);
+        a.msg = msg(l);
+        a.sel_idx = sidx(l);
+        a.sel_key = skey(l);
+        hipError_t e = launch_fine_attn(a, d, va, use_bf16, false, s);
+        if (e != hipSuccess) return QTA_ERR_HIP;
+    }
+
+    // 4-5. finest level with the combination fused in
+    {
+        FineArgs a{};
+        a.q = q;
+        a.k = k;
+        a.v = v;
+        a.B = B;
+        a.heads = heads;
+        a.H = H;
+        a.W = W;
+        a.Hp = L.H[1];
+        a.Wp = L.W[1];
+        a.C = C;
+        a.K = K;
+        a.scale = tau;
+        a.parent_idx = sidx(1);
+        a.parent_key = skey(1);
+        a.out = out;
+        a.w = w;
+        a.levels = levels;
+        for (int l = 1; l < levels; ++l) {
+            a.coarser_msg[l] = msg(l);
+            a.lvl_W[l] = L.W[l];
+            a.lvl_N[l] = L.H[l] * L.W[l];
+        }
+        hipError_t e = launch_fine_attn(a, d, va, use_bf16, true, s);
+        if (e != hipSuccess) return QTA_ERR_HIP;
+    }
+    return QTA_OK;
+}
+
+}  // extern "C"

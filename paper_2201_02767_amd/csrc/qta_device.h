@@ -1,0 +1,215 @@
+// Device helpers shared by the QuadTree attention kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qta {
+
+constexpr int kWave = 64;
+constexpr int kNumXcd = 8;   // MI355X: 8 accelerator complex dies, workgroups dealt round-robin
+
+// ---------------------------------------------------------------------------------------------
+// storage types
+// ---------------------------------------------------------------------------------------------
+
+// bf16 is carried as its 16 raw bits.
+struct bf16 {
+    uint16_t bits;
+};
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// fp32 -> bf16, round to nearest, ties to even (finite inputs).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+template <typename T> struct Storage;
+
+template <> struct Storage<float> {
+    static constexpr int kPer16B = 4;      // elements per 16-byte chunk
+    __device__ static __forceinline__ void unpack(const uint4& c, float* out)
+    {
+        out[0] = __uint_as_float(c.x);
+        out[1] = __uint_as_float(c.y);
+        out[2] = __uint_as_float(c.z);
+        out[3] = __uint_as_float(c.w);
+    }
+    __device__ static __forceinline__ uint4 pack(const float* in)
+    {
+        return make_uint4(__float_as_uint(in[0]), __float_as_uint(in[1]), __float_as_uint(in[2]),
+                          __float_as_uint(in[3]));
+    }
+    __device__ static __forceinline__ float load1(const void* base, size_t i)
+    {
+        return static_cast<const float*>(base)[i];
+    }
+    __device__ static __forceinline__ void store1(void* base, size_t i, float x)
+    {
+        static_cast<float*>(base)[i] = x;
+    }
+    // Round an fp32 value to this storage type and back.
+    __device__ static __forceinline__ float round(float x) { return x; }
+};
+
+template <> struct Storage<bf16> {
+    static constexpr int kPer16B = 8;
+    __device__ static __forceinline__ void unpack(const uint4& c, float* out)
+    {
+        const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            out[2 * i] = __uint_as_float(w[i] << 16);
+            out[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+        }
+    }
+    __device__ static __forceinline__ uint4 pack(const float* in)
+    {
+        uint32_t w[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) w[i] = f32_to_bf16_bits(in[2 * i]) | (f32_to_bf16_bits(in[2 * i + 1]) << 16);
+        return make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    __device__ static __forceinline__ float load1(const void* base, size_t i)
+    {
+        return bf16_bits_to_f32(static_cast<const uint16_t*>(base)[i]);
+    }
+    __device__ static __forceinline__ void store1(void* base, size_t i, float x)
+    {
+        static_cast<uint16_t*>(base)[i] = static_cast<uint16_t>(f32_to_bf16_bits(x));
+    }
+    __device__ static __forceinline__ float round(float x) { return __uint_as_float(f32_to_bf16_bits(x) << 16); }
+};
+
+// ---------------------------------------------------------------------------------------------
+// launch mapping
+// ---------------------------------------------------------------------------------------------
+
+// Workgroups are dealt to the XCDs round-robin (block b runs on XCD b % 8), and each XCD has its
+// own L2. Remap so that XCD x processes one contiguous range of logical tiles: neighbouring
+// query tiles, which gather overlapping keys, then share an L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblk)
+{
+    const int q = nblk / kNumXcd, r = nblk % kNumXcd;
+    const int xcd = bid % kNumXcd, pos = bid / kNumXcd;
+    return xcd * q + (xcd < r ? xcd : r) + pos;
+}
+
+// ---------------------------------------------------------------------------------------------
+// wave-level communication
+// ---------------------------------------------------------------------------------------------
+
+// Make this wave's LDS writes visible to its other lanes (no cross-wave synchronisation).
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+__device__ __forceinline__ float wave_max(float x)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m, kWave));
+    return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, kWave);
+    return x;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m)
+{
+    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(x), m, kWave);
+    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(x >> 32), m, kWave);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        const uint64_t y = shfl_xor_u64(x, m);
+        x = y > x ? y : x;
+    }
+    return x;
+}
+
+// ---------------------------------------------------------------------------------------------
+// ranking keys for top-K
+// ---------------------------------------------------------------------------------------------
+
+// Monotone map of a float to uint32 (larger float -> larger integer); -0 and +0 map together.
+__device__ __forceinline__ uint32_t ordered_bits(float f)
+{
+    const uint32_t u = __float_as_uint(f + 0.0f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float from_ordered_bits(uint32_t o)
+{
+    const uint32_t u = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
+    return __uint_as_float(u);
+}
+
+// One 64-bit word per candidate: score in the high half, inverted index in the low half, so the
+// unsigned order is (score descending, index ascending) when sorting for the maximum. Every valid
+// candidate encodes to a nonzero word; 0 marks "no candidate".
+__device__ __forceinline__ uint64_t rank_word(float score, int32_t idx)
+{
+    return (static_cast<uint64_t>(ordered_bits(score)) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(idx));
+}
+
+__device__ __forceinline__ int32_t rank_word_index(uint64_t w)
+{
+    return static_cast<int32_t>(~static_cast<uint32_t>(w));
+}
+
+__device__ __forceinline__ float rank_word_score(uint64_t w) { return from_ordered_bits(static_cast<uint32_t>(w >> 32)); }
+
+// Bitonic sort, descending, of NT*64 words held as word[t] in lane l at position t*64 + l.
+template <int NT>
+__device__ __forceinline__ void wave_bitonic_sort_desc(uint64_t (&word)[NT])
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    constexpr int n = NT * kWave;
+#pragma unroll
+    for (int k = 2; k <= n; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j >= 1; j >>= 1) {
+            if (j >= kWave) {
+                const int tj = j / kWave;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    if (t & tj) continue;
+                    const int e = t * kWave + lane;            // lower element of the pair
+                    const bool desc = (e & k) == 0;
+                    const uint64_t a = word[t], b = word[t | tj];
+                    const bool swap = desc ? (b > a) : (a > b);
+                    word[t] = swap ? b : a;
+                    word[t | tj] = swap ? a : b;
+                }
+            } else {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const int e = t * kWave + lane;
+                    const uint64_t other = shfl_xor_u64(word[t], j);
+                    const bool lower = (e & j) == 0;
+                    const bool desc = (e & k) == 0;
+                    const bool take_max = (lower == desc);
+                    const bool other_bigger = other > word[t];
+                    word[t] = (take_max == other_bigger) ? other : word[t];
+                }
+            }
+        }
+    }
+}
+
+}  // namespace qta

@@ -1,0 +1,79 @@
+// Step 3 as a standalone row-wise top-K (Sec. 3.2: each query keeps the K keys with the highest
+// attention scores).
+//
+// One wave per row. Each lane holds NPER candidates of the row as 64-bit words (score, inverted
+// name), so one unsigned comparison orders by (score descending, name ascending). K rounds of a
+// wave-wide maximum pick the winners in order; the lowest lane holding the winning word retires
+// it, so repeated names are kept as separate candidates. Rows are independent; a workgroup of
+// four waves takes four rows.
+#include "qta_device.h"
+#include "qta_internal.h"
+
+namespace qta {
+
+namespace {
+
+template <int NPER>
+__global__ __launch_bounds__(256) void topk_kernel(TopkArgs a)
+{
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= a.rows) return;                  // whole wave leaves; no workgroup barriers below
+    const size_t base = static_cast<size_t>(row) * a.n;
+    uint64_t word[NPER];
+#pragma unroll
+    for (int e = 0; e < NPER; ++e) {
+        const int j = lane + kWave * e;
+        word[e] = 0ull;
+        if (j < a.n) {
+            const int32_t name = a.cand_idx ? a.cand_idx[base + j] : j;
+            if (name >= 0) {
+                word[e] = rank_word(a.keys[base + j], name);
+            }
+        }
+    }
+    const size_t orow = static_cast<size_t>(row) * a.K;
+    for (int r = 0; r < a.K; ++r) {
+        uint64_t best = 0ull;
+#pragma unroll
+        for (int e = 0; e < NPER; ++e) best = word[e] > best ? word[e] : best;
+        const uint64_t g = wave_max_u64(best);
+        if (g == 0ull) {                         // fewer than K candidates: pad
+            if (lane == 0) {
+                a.idx_out[orow + r] = -1;
+                if (a.key_out) a.key_out[orow + r] = 0.f;
+            }
+            continue;
+        }
+        const uint64_t owners = __ballot(best == g);
+        const int owner = __ffsll(static_cast<unsigned long long>(owners)) - 1;
+        if (lane == owner) {
+            bool done = false;
+#pragma unroll
+            for (int e = 0; e < NPER; ++e)
+                if (!done && word[e] == g) {
+                    word[e] = 0ull;
+                    done = true;
+                }
+        }
+        if (lane == 0) {
+            a.idx_out[orow + r] = rank_word_index(g);
+            if (a.key_out) a.key_out[orow + r] = rank_word_score(g);
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_topk(const TopkArgs& a, hipStream_t stream)
+{
+    const unsigned blocks = static_cast<unsigned>((a.rows + 3) / 4);
+    if (a.n <= 64) hipLaunchKernelGGL((topk_kernel<1>), dim3(blocks), dim3(256), 0, stream, a);
+    else if (a.n <= 256) hipLaunchKernelGGL((topk_kernel<4>), dim3(blocks), dim3(256), 0, stream, a);
+    else if (a.n <= 1024) hipLaunchKernelGGL((topk_kernel<16>), dim3(blocks), dim3(256), 0, stream, a);
+    else if (a.n <= 4096) hipLaunchKernelGGL((topk_kernel<64>), dim3(blocks), dim3(256), 0, stream, a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+}  // namespace qta

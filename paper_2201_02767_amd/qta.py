@@ -1,0 +1,334 @@
+"""Python binding of the QuadTree attention C ABI (``include/qta.h``).
+
+Argument marshalling only: every function here checks tensor shapes, allocates outputs with torch
+on the inputs' device, and calls the library on torch's current HIP stream. All arithmetic happens
+in the HIP kernels of ``libqta.so``. There is no fallback: if the library is missing the calls raise.
+
+Tensors are NHWC: q, k, v are ``[B, H, W, heads, d]`` (fp32 or bf16, contiguous, on a GPU).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libqta.so")
+MAX_LEVELS = 16
+
+_DTYPES = {torch.float32: 0, torch.bfloat16: 1}
+_VARIANTS = {"A": 0, "B": 1}
+
+
+class QtaError(RuntimeError):
+    def __init__(self, func: str, status: int, msg: str):
+        super().__init__(f"{func}: {msg} (status {status})")
+        self.status = status
+
+
+class WorkspaceLayout(ctypes.Structure):
+    _fields_ = [
+        ("levels", ctypes.c_int),
+        ("H", ctypes.c_int * MAX_LEVELS),
+        ("W", ctypes.c_int * MAX_LEVELS),
+        ("q", ctypes.c_size_t * MAX_LEVELS),
+        ("k", ctypes.c_size_t * MAX_LEVELS),
+        ("v", ctypes.c_size_t * MAX_LEVELS),
+        ("msg", ctypes.c_size_t * MAX_LEVELS),
+        ("sel_idx", ctypes.c_size_t * MAX_LEVELS),
+        ("sel_key", ctypes.c_size_t * MAX_LEVELS),
+        ("total", ctypes.c_size_t),
+    ]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_F = ctypes.c_float
+_SIGS = {
+    "qta_status_str": ([_I], ctypes.c_char_p),
+    "qta_level_dims": ([_I, _I, _I, _P, _P], _I),
+    "qta_get_workspace_layout": ([_I, _I, _I, _I, _I, _I, _I, _I, ctypes.POINTER(WorkspaceLayout)], _I),
+    "qta_workspace_bytes": ([_I, _I, _I, _I, _I, _I, _I, _I], ctypes.c_size_t),
+    "qta_forward": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, ctypes.c_size_t, _P], _I),
+    "qta_build_pyramid": ([_P, _P, _I, _I, _I, _I, _I, _I, _P], _I),
+    "qta_coarse_attn": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P], _I),
+    "qta_topk": ([_P, _P, _I, _I, _I, _P, _P, _P], _I),
+    "qta_fine_attn": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P, _P], _I),
+    "qta_finest_attn": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _I, _P, _P, _P, _P], _I),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """Load ``libqta.so`` (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run paper_2201_02767_amd.build.build() first")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            fn = getattr(handle, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = handle
+    return _lib
+
+
+def _check(func: str, status: int) -> None:
+    if status != 0:
+        raise QtaError(func, status, lib().qta_status_str(status).decode())
+
+
+def _stream(device: torch.device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _require(t: torch.Tensor, name: str, dtype=None, ndim=None) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on a GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype not in _DTYPES:
+        raise ValueError(f"unsupported dtype {t.dtype}; fp32 and bf16 are supported")
+    return _DTYPES[t.dtype]
+
+
+def _scale(scale) -> float:
+    return 0.0 if scale is None else float(scale)
+
+
+# ------------------------------------------------------------------------------------------------
+# geometry
+# ------------------------------------------------------------------------------------------------
+
+def level_dims(H: int, W: int, levels: int) -> list[tuple[int, int]]:
+    hl = (ctypes.c_int * MAX_LEVELS)()
+    wl = (ctypes.c_int * MAX_LEVELS)()
+    _check("qta_level_dims", lib().qta_level_dims(H, W, levels, ctypes.addressof(hl), ctypes.addressof(wl)))
+    return [(hl[i], wl[i]) for i in range(levels)]
+
+
+def workspace_layout(B, heads, H, W, d, levels, K, dtype: torch.dtype) -> WorkspaceLayout:
+    lay = WorkspaceLayout()
+    _check("qta_get_workspace_layout",
+           lib().qta_get_workspace_layout(B, heads, H, W, d, levels, K, _DTYPES[dtype], ctypes.byref(lay)))
+    return lay
+
+
+def workspace_bytes(B, heads, H, W, d, levels, K, dtype: torch.dtype) -> int:
+    return int(lib().qta_workspace_bytes(B, heads, H, W, d, levels, K, _DTYPES[dtype]))
+
+
+# ------------------------------------------------------------------------------------------------
+# the whole forward
+# ------------------------------------------------------------------------------------------------
+
+class Plan:
+    """Pre-allocated output and workspace for repeated forwards of one problem shape."""
+
+    def __init__(self, B, H, W, heads, d, *, levels, K, variant, dtype, device, scale=None):
+        self.B, self.H, self.W, self.heads, self.d = B, H, W, heads, d
+        self.levels, self.K, self.variant, self.dtype = levels, K, variant, dtype
+        self.scale = scale
+        self.device = torch.device(device)
+        self.layout = workspace_layout(B, heads, H, W, d, levels, K, dtype)
+        nbytes = max(int(self.layout.total), 256)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self.out = torch.empty((B, H, W, heads, d), dtype=dtype, device=self.device)
+
+    def run(self, q, k, v, w=None, stream=None):
+        for name, t in (("q", q), ("k", k), ("v", v)):
+            _require(t, name, self.dtype, 5)
+            if tuple(t.shape) != (self.B, self.H, self.W, self.heads, self.d):
+                raise ValueError(f"{name} has shape {tuple(t.shape)}")
+        if w is not None:
+            _require(w, "w", torch.float32, 4)
+            if tuple(w.shape) != (self.B, self.H * self.W, self.heads, self.levels):
+                raise ValueError(f"w has shape {tuple(w.shape)}")
+        s = _stream(self.device) if stream is None else ctypes.c_void_p(stream)
+        _check("qta_forward", lib().qta_forward(
+            _ptr(q), _ptr(k), _ptr(v), _ptr(w), self.B, self.heads, self.H, self.W, self.d, self.levels, self.K,
+            _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), _ptr(self.out),
+            _ptr(self.workspace), self.workspace.numel(), s))
+        return self.out
+
+    def prepare(self, q, k, v, w=None):
+        """Validate once and return a zero-argument callable that re-issues this forward on the
+        current stream (for timing loops and graph capture: no per-call Python checks)."""
+        for name, t in (("q", q), ("k", k), ("v", v)):
+            _require(t, name, self.dtype, 5)
+            if tuple(t.shape) != (self.B, self.H, self.W, self.heads, self.d):
+                raise ValueError(f"{name} has shape {tuple(t.shape)}")
+        if w is not None:
+            _require(w, "w", torch.float32, 4)
+        fn = lib().qta_forward
+        args = (_ptr(q), _ptr(k), _ptr(v), _ptr(w), self.B, self.heads, self.H, self.W, self.d, self.levels, self.K,
+                _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), _ptr(self.out),
+                _ptr(self.workspace), self.workspace.numel(), _stream(self.device))
+        keep = (q, k, v, w)
+
+        def call():
+            st = fn(*args)
+            if st != 0:
+                _check("qta_forward", st)
+            return keep
+        return call
+
+    def prepare_finest(self, q, k, v, w=None):
+        """A zero-argument callable that re-runs only the finest-level kernel (attention at level 0
+        with the fused combination) on the selections and messages this plan's last run left in
+        its workspace."""
+        if self.levels < 2:
+            raise ValueError("a single-level problem has no finest-level stage")
+        fn = lib().qta_finest_attn
+        sidx, skey = self.selection(1)
+        msgs = [self.message(j) for j in range(1, self.levels)]
+        table = (ctypes.c_void_p * (self.levels - 1))(*[m.data_ptr() for m in msgs])
+        args = (_ptr(q), _ptr(k), _ptr(v), self.B, self.heads, self.H, self.W, self.d, self.K,
+                _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), _ptr(sidx), _ptr(skey),
+                self.levels, ctypes.addressof(table), _ptr(w), _ptr(self.out), _stream(self.device))
+        keep = (q, k, v, w, table, msgs)
+
+        def call():
+            st = fn(*args)
+            if st != 0:
+                _check("qta_finest_attn", st)
+            return keep
+        return call
+
+    # views into the workspace after run()
+    def _view(self, off, shape, dtype):
+        n = 1
+        for s_ in shape:
+            n *= s_
+        nbytes = n * torch.empty((), dtype=dtype).element_size()
+        return self.workspace[off:off + nbytes].view(dtype).view(shape)
+
+    def pyramid(self, which: str, level: int):
+        lay = self.layout
+        off = getattr(lay, which)[level]
+        return self._view(off, (self.B, lay.H[level], lay.W[level], self.heads, self.d), self.dtype)
+
+    def message(self, level: int):
+        lay = self.layout
+        return self._view(lay.msg[level], (self.B, lay.H[level] * lay.W[level], self.heads, self.d), torch.float32)
+
+    def selection(self, level: int):
+        lay = self.layout
+        shape = (self.B, self.heads, lay.H[level] * lay.W[level], self.K)
+        return (self._view(lay.sel_idx[level], shape, torch.int32),
+                self._view(lay.sel_key[level], shape, torch.float32))
+
+
+def forward(q, k, v, *, levels: int, K: int, variant: str, w=None, scale=None) -> torch.Tensor:
+    """QuadTree attention forward; returns ``out`` [B, H, W, heads, d] in q's dtype."""
+    _require(q, "q", None, 5)
+    B, H, W, heads, d = q.shape
+    plan = Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=q.dtype, device=q.device,
+                scale=scale)
+    return plan.run(q, k, v, w)
+
+
+# ------------------------------------------------------------------------------------------------
+# stage calls
+# ------------------------------------------------------------------------------------------------
+
+def build_pyramid(x: torch.Tensor, levels: int) -> list[torch.Tensor]:
+    """Levels 1..levels-1 of an NHWC map ``[B, H, W, C]``; returns a list indexed by level (entry 0 is x)."""
+    _require(x, "x", None, 4)
+    B, H, W, C = x.shape
+    dims = level_dims(H, W, levels)
+    total = sum(B * h * w_ * C for h, w_ in dims[1:])
+    buf = torch.empty(max(total, 1), dtype=x.dtype, device=x.device)
+    _check("qta_build_pyramid", lib().qta_build_pyramid(
+        _ptr(x), _ptr(buf), B, H, W, C, levels, _dtype_code(x), _stream(x.device)))
+    out, off = [x], 0
+    for h, w_ in dims[1:]:
+        n = B * h * w_ * C
+        out.append(buf[off:off + n].view(B, h, w_, C))
+        off += n
+    return out
+
+
+def coarse_attn(qc, kc, vc, *, K: int, variant: str, scale=None, select: bool = True):
+    """Coarsest-level attention. Returns (msg [B,N,heads,d] fp32, sel_idx, sel_key) (None without selection)."""
+    for name, t in (("qc", qc), ("kc", kc), ("vc", vc)):
+        _require(t, name, qc.dtype, 5)
+    B, Hc, Wc, heads, d = qc.shape
+    N = Hc * Wc
+    msg = torch.empty((B, N, heads, d), dtype=torch.float32, device=qc.device)
+    sel_idx = sel_key = None
+    if select:
+        sel_idx = torch.empty((B, heads, N, K), dtype=torch.int32, device=qc.device)
+        sel_key = torch.empty((B, heads, N, K), dtype=torch.float32, device=qc.device)
+    _check("qta_coarse_attn", lib().qta_coarse_attn(
+        _ptr(qc), _ptr(kc), _ptr(vc), B, heads, Hc, Wc, d, K, _VARIANTS[variant], _dtype_code(qc), _scale(scale),
+        _ptr(msg), _ptr(sel_idx), _ptr(sel_key), _stream(qc.device)))
+    return msg, sel_idx, sel_key
+
+
+def topk(keys: torch.Tensor, K: int, cand_idx: torch.Tensor | None = None):
+    """Row-wise top-K of fp32 ``keys`` [rows, n]; returns (idx int32 [rows, K], key fp32 [rows, K])."""
+    _require(keys, "keys", torch.float32, 2)
+    rows, n = keys.shape
+    if cand_idx is not None:
+        _require(cand_idx, "cand_idx", torch.int32, 2)
+        if tuple(cand_idx.shape) != (rows, n):
+            raise ValueError("cand_idx must match keys")
+    idx = torch.empty((rows, K), dtype=torch.int32, device=keys.device)
+    key = torch.empty((rows, K), dtype=torch.float32, device=keys.device)
+    _check("qta_topk", lib().qta_topk(_ptr(keys), _ptr(cand_idx), rows, n, K, _ptr(idx), _ptr(key),
+                                      _stream(keys.device)))
+    return idx, key
+
+
+def fine_attn(ql, kl, vl, parent_idx, parent_key, *, K: int, variant: str, scale=None):
+    """Intermediate-level attention. Returns (msg fp32 [B,N,heads,d], sel_idx, sel_key [B,heads,N,K])."""
+    for name, t in (("ql", ql), ("kl", kl), ("vl", vl)):
+        _require(t, name, ql.dtype, 5)
+    _require(parent_idx, "parent_idx", torch.int32, 4)
+    if parent_key is not None:
+        _require(parent_key, "parent_key", torch.float32, 4)
+    B, Hl, Wl, heads, d = ql.shape
+    N = Hl * Wl
+    msg = torch.empty((B, N, heads, d), dtype=torch.float32, device=ql.device)
+    sel_idx = torch.empty((B, heads, N, K), dtype=torch.int32, device=ql.device)
+    sel_key = torch.empty((B, heads, N, K), dtype=torch.float32, device=ql.device)
+    _check("qta_fine_attn", lib().qta_fine_attn(
+        _ptr(ql), _ptr(kl), _ptr(vl), B, heads, Hl, Wl, d, K, _VARIANTS[variant], _dtype_code(ql), _scale(scale),
+        _ptr(parent_idx), _ptr(parent_key), _ptr(msg), _ptr(sel_idx), _ptr(sel_key), _stream(ql.device)))
+    return msg, sel_idx, sel_key
+
+
+def finest_attn(q0, k0, v0, parent_idx, parent_key, coarser_msgs, *, K: int, variant: str, w=None, scale=None):
+    """Level-0 attention fused with the combination; ``coarser_msgs[j-1]`` is level j's fp32 message."""
+    for name, t in (("q0", q0), ("k0", k0), ("v0", v0)):
+        _require(t, name, q0.dtype, 5)
+    _require(parent_idx, "parent_idx", torch.int32, 4)
+    B, H, W, heads, d = q0.shape
+    levels = len(coarser_msgs) + 1
+    for j, m in enumerate(coarser_msgs):
+        _require(m, f"coarser_msgs[{j}]", torch.float32, 4)
+    if w is not None:
+        _require(w, "w", torch.float32, 4)
+    table = (ctypes.c_void_p * max(levels - 1, 1))(*[m.data_ptr() for m in coarser_msgs])
+    out = torch.empty_like(q0)
+    _check("qta_finest_attn", lib().qta_finest_attn(
+        _ptr(q0), _ptr(k0), _ptr(v0), B, heads, H, W, d, K, _VARIANTS[variant], _dtype_code(q0), _scale(scale),
+        _ptr(parent_idx), _ptr(parent_key), levels, ctypes.addressof(table), _ptr(w), _ptr(out),
+        _stream(q0.device)))
+    return out

@@ -1,0 +1,147 @@
+"""C-ABI checks that need no GPU: the library loads, exports what the header declares, and rejects
+bad arguments on the host before any launch. Only validation paths are exercised here (every call
+below fails validation, so nothing reaches the device)."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import paper_2201_02767_amd as P
+from oracle import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qta.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+FAKE = 0x100000          # an aligned, never-dereferenced address: validation fails before use
+F32, BF16 = 0, 1
+VA, VB = 0, 1
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(qta_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = P.lib()
+    names = declared_functions()
+    assert "qta_forward" in names and len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    lib = P.lib()
+    for code, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported shape or type"),
+                       (3, b"workspace too small"), (4, b"HIP launch failed"), (99, b"unknown status")]:
+        assert lib.qta_status_str(code) == text
+
+
+@pytest.mark.parametrize("H,W,L", [(16, 16, 3), (60, 80, 3), (120, 160, 4), (56, 56, 3), (200, 336, 5), (15, 13, 4),
+                                   (1, 9, 4)])
+def test_level_dims_match_oracle(H, W, L):
+    assert P.level_dims(H, W, L) == O.level_dims(H, W, L)
+
+
+def test_level_dims_rejects_levels_above_a_single_token():
+    with pytest.raises(P.QtaError):
+        P.level_dims(2, 2, 3)          # 2x2 -> 1x1 -> (1x1 again)
+    with pytest.raises(P.QtaError):
+        P.level_dims(4, 4, 17)
+    with pytest.raises(P.QtaError):
+        P.level_dims(0, 4, 1)
+
+
+def test_workspace_layout_is_aligned_and_disjoint():
+    lay = P.workspace_layout(2, 2, 200, 336, 32, 5, 16, torch.bfloat16)
+    regions = []
+    for l in range(1, 5):
+        N = lay.H[l] * lay.W[l]
+        tok = 2 * N * 64 * 2
+        regions += [(lay.q[l], tok), (lay.k[l], tok), (lay.v[l], tok), (lay.msg[l], 2 * N * 64 * 4),
+                    (lay.sel_idx[l], 2 * 2 * N * 16 * 4), (lay.sel_key[l], 2 * 2 * N * 16 * 4)]
+    regions.sort()
+    for (o1, n1), (o2, _) in zip(regions, regions[1:]):
+        assert o1 % 256 == 0 and o1 + n1 <= o2
+    assert regions[-1][0] + regions[-1][1] <= lay.total
+    assert P.workspace_bytes(2, 2, 200, 336, 32, 5, 16, torch.bfloat16) == lay.total
+
+
+def test_workspace_bytes_zero_on_bad_shapes():
+    lib = P.lib()
+    assert lib.qta_workspace_bytes(1, 1, 16, 16, 48, 3, 4, F32) == 0     # d unsupported
+    assert lib.qta_workspace_bytes(1, 1, 16, 16, 32, 3, 65, F32) == 0    # K too large
+    assert lib.qta_workspace_bytes(1, 1, 64, 64, 32, 1, 4, F32) == 0     # 4096 coarse tokens
+    assert lib.qta_workspace_bytes(0, 1, 16, 16, 32, 3, 4, F32) == 0
+    assert lib.qta_workspace_bytes(1, 1, 16, 16, 32, 1, 4, F32) >= 256   # valid single level: minimal, nonzero
+
+
+def _fwd(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, w=None, B=1, heads=1, H=16, W=16, d=32, L=3, K=4, var=VA, dt=F32, scale=0.0,
+             out=FAKE, ws=FAKE, wsb=0, stream=None)
+    a.update(kw)
+    return lib.qta_forward(a["q"], a["k"], a["v"], a["w"], a["B"], a["heads"], a["H"], a["W"], a["d"], a["L"], a["K"],
+                           a["var"], a["dt"], a["scale"], a["out"], a["ws"], a["wsb"], a["stream"])
+
+
+def test_forward_validation():
+    lib = P.lib()
+    assert _fwd(lib) == WORKSPACE                           # valid shape, zero workspace
+    assert _fwd(lib, q=None) == INVALID
+    assert _fwd(lib, out=None) == INVALID
+    assert _fwd(lib, q=FAKE + 4) == INVALID                 # misaligned
+    assert _fwd(lib, ws=FAKE + 16, wsb=1 << 30) == INVALID  # workspace not 256-aligned
+    assert _fwd(lib, B=0) == INVALID
+    assert _fwd(lib, K=0) == INVALID
+    assert _fwd(lib, L=0) == INVALID
+    assert _fwd(lib, L=17) == INVALID
+    assert _fwd(lib, H=2, W=2, L=3) == INVALID              # level above a 1x1 map
+    assert _fwd(lib, var=7) == INVALID
+    assert _fwd(lib, dt=5) == INVALID
+    assert _fwd(lib, d=16) == UNSUPPORTED
+    assert _fwd(lib, K=65) == UNSUPPORTED
+    assert _fwd(lib, H=64, W=64, L=1) == UNSUPPORTED        # coarsest level above the cap
+    assert _fwd(lib, H=64, W=64, L=2) == WORKSPACE          # 32x32 = 1024 coarse tokens is allowed
+
+
+def test_stage_validation():
+    lib = P.lib()
+    # qta_build_pyramid: C*bytes must be a multiple of 16
+    assert lib.qta_build_pyramid(FAKE, FAKE, 1, 8, 8, 6, 3, F32, None) == UNSUPPORTED
+    assert lib.qta_build_pyramid(None, FAKE, 1, 8, 8, 8, 3, F32, None) == INVALID
+    assert lib.qta_build_pyramid(FAKE, FAKE, 1, 2, 2, 8, 3, F32, None) == INVALID
+    # qta_coarse_attn
+    assert lib.qta_coarse_attn(FAKE, FAKE, FAKE, 1, 1, 4, 4, 32, 4, VB, F32, 0.0, None, None, None, None) == INVALID
+    assert lib.qta_coarse_attn(FAKE, FAKE, FAKE, 1, 1, 4, 4, 32, 4, VB, F32, 0.0, FAKE, FAKE, None, None) == INVALID
+    assert lib.qta_coarse_attn(FAKE, FAKE, FAKE, 1, 1, 33, 32, 32, 4, VB, F32, 0.0, FAKE, None, None, None) == UNSUPPORTED
+    assert lib.qta_coarse_attn(FAKE, FAKE, FAKE, 1, 1, 4, 4, 64 + 1, 4, VB, F32, 0.0, FAKE, None, None, None) == UNSUPPORTED
+    # qta_topk
+    assert lib.qta_topk(FAKE, None, 0, 8, 2, FAKE, None, None) == INVALID
+    assert lib.qta_topk(FAKE, None, 4, 5000, 2, FAKE, None, None) == UNSUPPORTED
+    assert lib.qta_topk(FAKE, None, 4, 64, 65, FAKE, None, None) == UNSUPPORTED
+    assert lib.qta_topk(None, None, 4, 64, 4, FAKE, None, None) == INVALID
+    # qta_fine_attn: A needs parent scores; all outputs required
+    assert lib.qta_fine_attn(FAKE, FAKE, FAKE, 1, 1, 8, 8, 32, 4, VA, F32, 0.0, FAKE, None, FAKE, FAKE, FAKE,
+                             None) == INVALID
+    assert lib.qta_fine_attn(FAKE, FAKE, FAKE, 1, 1, 8, 8, 32, 4, VB, F32, 0.0, FAKE, None, FAKE, None, FAKE,
+                             None) == INVALID
+    assert lib.qta_fine_attn(FAKE, FAKE, FAKE, 1, 1, 1, 1, 32, 4, VB, F32, 0.0, FAKE, None, FAKE, FAKE, FAKE,
+                             None) == INVALID
+    # qta_finest_attn: needs at least two levels and every coarser message
+    table = (ctypes.c_void_p * 2)(FAKE, None)
+    assert lib.qta_finest_attn(FAKE, FAKE, FAKE, 1, 1, 8, 8, 32, 4, VB, F32, 0.0, FAKE, None, 1, ctypes.addressof(table),
+                               None, FAKE, None) == INVALID
+    assert lib.qta_finest_attn(FAKE, FAKE, FAKE, 1, 1, 8, 8, 32, 4, VB, F32, 0.0, FAKE, None, 3, ctypes.addressof(table),
+                               None, FAKE, None) == INVALID
+    assert lib.qta_finest_attn(FAKE, FAKE, FAKE, 1, 1, 8, 8, 32, 4, VB, F32, 0.0, FAKE, None, 2, None,
+                               None, FAKE, None) == INVALID
+
+
+def test_binding_refuses_cpu_tensors():
+    x = torch.zeros(1, 4, 4, 1, 32)
+    with pytest.raises(ValueError):
+        P.forward(x, x, x, levels=2, K=1, variant="B")

@@ -1,0 +1,315 @@
+"""GPU parity: every stage of the HIP library against the CPU oracle on the same seeded inputs.
+
+Cases span several workgroup tiles with ragged tails, odd maps, both variants, both storage types,
+d = 32 and 64, K from 1 to 64, and the five workloads at their full sizes.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2201_02767_amd as P
+from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_qkv, round_bf16
+from oracle import oracle as O
+from tests import brute
+from tests.parity import TOL, check_selection, rel_err, to_np
+
+pytestmark = pytest.mark.gpu
+
+TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    P.lib()
+    return torch.device("cuda:0")
+
+
+def announce(msg: str) -> None:
+    print(f"[gpu case] {msg}", file=sys.stderr, flush=True)
+
+
+def rand_qkv(seed, B, H, W, heads, d, dtype, scale=1.0):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(3):
+        x = (rng.standard_normal((B, H, W, heads, d)) * scale).astype(np.float32)
+        if dtype == "bf16":
+            x = round_bf16(x)
+        out.append(x)
+    return out
+
+
+def dev_t(x, dtype, dev):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dev).to(TDT[dtype])
+
+
+# ------------------------------------------------------------------------------------------------
+# end-to-end protocol
+# ------------------------------------------------------------------------------------------------
+
+def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=None, label=""):
+    """GPU forward vs teacher-forced oracle; returns a dict of the measured agreement."""
+    B, H, W, heads, d = q.shape
+    announce(f"forward {label} B={B} H={H} W={W} heads={heads} d={d} L={levels} K={K} {variant} {dtype}")
+    plan = P.Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=TDT[dtype], device=dev, scale=scale)
+    wt = None if w is None else torch.from_numpy(w).to(dev)
+    out = plan.run(dev_t(q, dtype, dev), dev_t(k, dtype, dev), dev_t(v, dtype, dev), wt)
+    torch.cuda.synchronize()
+    g_out = to_np(out)
+    g_sel = [None] + [to_np(plan.selection(l)[0]) for l in range(1, levels)]
+    ref = O.forward(q, k, v, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale,
+                    forced=g_sel, want_candidates=True, want_pyramids=True)
+    res = {"sel": {}, "msg": {}}
+    for l in range(1, levels):
+        for name in "qkv":
+            gp = to_np(plan.pyramid(name, l)).reshape(ref["pyr_" + name][l].shape)
+            assert np.array_equal(gp, ref["pyr_" + name][l]), f"pyramid {name} level {l} differs"
+        chk = check_selection(g_sel[l], ref["cand_idx"][l], ref["cand_key"][l], K)
+        assert chk["bad"] == 0, f"level {l} selection: {chk}"
+        res["sel"][l] = chk
+        e = rel_err(to_np(plan.message(l)), ref["msg"][l])
+        res["msg"][l] = e
+        assert e <= TOL[dtype], f"level {l} message error {e}"
+        gk = to_np(plan.selection(l)[1])
+        sel_ok = g_sel[l] >= 0
+        # the kept keys' scores agree with the oracle's (A carries them down as s_parent)
+        np.testing.assert_allclose(gk[sel_ok], ref["sel_key"][l][sel_ok], rtol=2e-3 if dtype == "bf16" else 2e-5,
+                                   atol=1e-6)
+    e = rel_err(g_out, ref["out"])
+    res["out"] = e
+    assert e <= TOL[dtype], f"output error {e}"
+    # the oracle's own (unforced) choice agrees wherever there is no near-tie
+    return res, g_out, ref
+
+
+# ------------------------------------------------------------------------------------------------
+# stage: pyramid (bit-exact)
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,B,H,W,C,L", [
+    ("f32", 1, 16, 16, 32, 3), ("bf16", 2, 25, 42, 64, 5), ("f32", 1, 15, 13, 256, 4), ("bf16", 1, 1, 9, 64, 4),
+    ("f32", 3, 37, 53, 96, 6), ("bf16", 2, 200, 336, 64, 5), ("f32", 1, 60, 80, 256, 3),
+])
+def test_pyramid_bit_exact(dev, dtype, B, H, W, C, L):
+    rng = np.random.default_rng(H * W + C)
+    x = rng.standard_normal((B, H, W, C)).astype(np.float32)
+    if dtype == "bf16":
+        x = round_bf16(x)
+    announce(f"pyramid {dtype} {B}x{H}x{W}x{C} L={L}")
+    levels = P.build_pyramid(dev_t(x, dtype, dev), L)
+    torch.cuda.synchronize()
+    ref = x
+    for l in range(1, L):
+        ref = O.pool_level(ref, dtype)
+        assert np.array_equal(to_np(levels[l]), ref), f"level {l}"
+
+
+# ------------------------------------------------------------------------------------------------
+# stage: top-K
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("rows,n,K", [(5, 7, 3), (64, 64, 8), (33, 100, 16), (17, 300, 64), (9, 1024, 16),
+                                      (4, 3000, 32), (3, 16, 64)])
+def test_topk_matches_full_sort(dev, rows, n, K):
+    rng = np.random.default_rng(rows * n + K)
+    keys = rng.integers(-20, 20, size=(rows, n)).astype(np.float32) / 4      # many exact ties
+    names = rng.permutation(rows * n).reshape(rows, n).astype(np.int32) % (3 * n)
+    names[rng.random((rows, n)) < 0.2] = -1                                    # non-candidates
+    announce(f"topk rows={rows} n={n} K={K}")
+    for cand in (None, names):
+        idx, key = P.topk(torch.from_numpy(keys).to(dev), K,
+                          None if cand is None else torch.from_numpy(cand).to(dev))
+        torch.cuda.synchronize()
+        idx, key = to_np(idx), to_np(key)
+        for r in range(rows):
+            nm = np.arange(n) if cand is None else cand[r]
+            ok = nm >= 0
+            kk, ii = keys[r][ok], nm[ok]
+            order = np.lexsort((ii, -kk))
+            m = min(K, len(ii))
+            assert idx[r, :m].tolist() == ii[order[:m]].tolist()
+            assert np.all(idx[r, m:] == -1)
+            assert np.array_equal(key[r, :m], kk[order[:m]])
+            assert np.all(key[r, m:] == 0)
+
+
+# ------------------------------------------------------------------------------------------------
+# stages in isolation, teacher-forced from the oracle
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant,dtype,d,K", [("B", "f32", 32, 8), ("A", "f32", 64, 4), ("B", "bf16", 64, 16),
+                                               ("A", "bf16", 32, 5)])
+def test_stages_teacher_forced(dev, variant, dtype, d, K):
+    B, H, W, heads, L = 2, 45, 38, 2, 4
+    q, k, v = rand_qkv(11 + K, B, H, W, heads, d, dtype)
+    w = np.random.default_rng(3).random((B, H * W, heads, L)).astype(np.float32) if variant == "B" else None
+    ref = O.forward(q, k, v, levels=L, K=K, variant=variant, dtype=dtype, w=w, want_candidates=True,
+                    want_pyramids=True)
+    dims = ref["dims"]
+
+    def pyr(name, l):
+        if l == 0:
+            return {"q": q, "k": k, "v": v}[name]
+        Hl, Wl = dims[l]
+        return ref["pyr_" + name][l].reshape(B, Hl, Wl, heads, d)
+
+    # coarsest level
+    c = L - 1
+    announce(f"coarse stage {variant} {dtype} d={d} K={K}")
+    msg, sidx, skey = P.coarse_attn(*(dev_t(pyr(n, c), dtype, dev) for n in "qkv"), K=K, variant=variant)
+    torch.cuda.synchronize()
+    chk = check_selection(to_np(sidx), ref["cand_idx"][c], ref["cand_key"][c], K)
+    assert chk["bad"] == 0, chk
+    forced = O.forward(q, k, v, levels=L, K=K, variant=variant, dtype=dtype, w=w,
+                       forced=[None] * c + [to_np(sidx)])
+    assert rel_err(to_np(msg), forced["msg"][c]) <= TOL[dtype]
+    # intermediate levels, each fed the oracle's parent selections
+    for l in range(c - 1, 0, -1):
+        announce(f"fine stage level {l} {variant} {dtype} d={d} K={K}")
+        pidx = torch.from_numpy(ref["sel_idx"][l + 1]).to(dev)
+        pkey = torch.from_numpy(ref["sel_key"][l + 1].astype(np.float32)).to(dev)
+        msg, sidx, skey = P.fine_attn(*(dev_t(pyr(n, l), dtype, dev) for n in "qkv"), pidx, pkey, K=K, variant=variant)
+        torch.cuda.synchronize()
+        chk = check_selection(to_np(sidx), ref["cand_idx"][l], ref["cand_key"][l], K)
+        assert chk["bad"] == 0, chk
+        frc = [None] * L
+        frc[l] = to_np(sidx)
+        for j in range(l + 1, L):
+            frc[j] = ref["sel_idx"][j]
+        forced = O.forward(q, k, v, levels=L, K=K, variant=variant, dtype=dtype, w=w, forced=frc)
+        assert rel_err(to_np(msg), forced["msg"][l]) <= TOL[dtype]
+    # finest level with the combination
+    announce(f"finest stage {variant} {dtype} d={d} K={K}")
+    pidx = torch.from_numpy(ref["sel_idx"][1]).to(dev)
+    pkey = torch.from_numpy(ref["sel_key"][1].astype(np.float32)).to(dev)
+    msgs = [torch.from_numpy(ref["msg"][j].astype(np.float32)).to(dev) for j in range(1, L)]
+    out = P.finest_attn(dev_t(q, dtype, dev), dev_t(k, dtype, dev), dev_t(v, dtype, dev), pidx, pkey, msgs, K=K,
+                        variant=variant, w=None if w is None else torch.from_numpy(w).to(dev))
+    torch.cuda.synchronize()
+    assert rel_err(to_np(out), ref["out"]) <= TOL[dtype]
+
+
+# ------------------------------------------------------------------------------------------------
+# end-to-end: shapes that span tiles, ragged tails and the degenerate cases
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,W,heads,d,L,K", [
+    (1, 16, 16, 1, 32, 3, 4),       # tiny workload shape
+    (2, 37, 53, 2, 32, 4, 8),       # odd map, several tiles, ragged tail
+    (1, 30, 41, 3, 64, 3, 16),      # d = 64, three heads
+    (1, 23, 19, 1, 32, 5, 1),       # K = 1, deep pyramid on an odd map
+    (1, 1, 40, 2, 32, 4, 3),        # single row
+    (1, 12, 12, 1, 32, 3, 20),      # K above the candidate count (two slot chunks)
+    (1, 20, 24, 2, 64, 3, 64),      # K = 64 (four slot chunks)
+])
+def test_forward_parity(dev, variant, dtype, B, H, W, heads, d, L, K):
+    q, k, v = rand_qkv(B * H * W + L * K, B, H, W, heads, d, dtype)
+    w = np.random.default_rng(5).random((B, H * W, heads, L)).astype(np.float32) if variant == "B" else None
+    run_and_compare(dev, q, k, v, levels=L, K=K, variant=variant, dtype=dtype, w=w)
+
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_single_level_is_dense_attention(dev, variant, dtype):
+    B, H, W, heads, d = 2, 9, 11, 2, 32
+    q, k, v = rand_qkv(21, B, H, W, heads, d, dtype)
+    announce(f"single level {variant} {dtype}")
+    out = P.forward(dev_t(q, dtype, dev), dev_t(k, dtype, dev), dev_t(v, dtype, dev), levels=1, K=4, variant=variant)
+    torch.cuda.synchronize()
+    ref = brute.dense_attention(q.reshape(B, H * W, heads, d), k.reshape(B, H * W, heads, d),
+                                v.reshape(B, H * W, heads, d), 1 / np.sqrt(d))
+    assert rel_err(to_np(out).reshape(ref.shape), ref) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_largest_coarse_level(dev, dtype):
+    """1024 coarse tokens, the cap: 64x64 map, two levels."""
+    q, k, v = rand_qkv(22, 1, 64, 64, 1, 32, dtype, scale=0.5)
+    run_and_compare(dev, q, k, v, levels=2, K=8, variant="B", dtype=dtype, label="coarse cap")
+
+
+def test_piecewise_constant_a_equals_dense(dev):
+    """QuadTree-A on maps whose Q and K are constant per coarsest cell equals dense attention."""
+    rng = np.random.default_rng(23)
+    L, H, W, d = 3, 32, 32, 32
+    f = 2 ** (L - 1)
+    cq = rng.standard_normal((1, H // f, W // f, 1, d)).astype(np.float32) * 0.5
+    ck = rng.standard_normal((1, H // f, W // f, 1, d)).astype(np.float32) * 0.5
+    q = np.repeat(np.repeat(cq, f, 1), f, 2)
+    k = np.repeat(np.repeat(ck, f, 1), f, 2)
+    v = rng.standard_normal((1, H, W, 1, d)).astype(np.float32)
+    for K in (1, 3):
+        announce(f"piecewise constant K={K}")
+        out = P.forward(dev_t(q, "f32", dev), dev_t(k, "f32", dev), dev_t(v, "f32", dev), levels=L, K=K, variant="A")
+        torch.cuda.synchronize()
+        ref = brute.dense_attention(q.reshape(1, -1, 1, d), k.reshape(1, -1, 1, d), v.reshape(1, -1, 1, d),
+                                    1 / np.sqrt(d))
+        assert rel_err(to_np(out).reshape(ref.shape), ref) <= 1e-4
+
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+def test_constant_values_give_constant_output(dev, variant):
+    rng = np.random.default_rng(24)
+    B, H, W, heads, d, L = 1, 29, 31, 2, 32, 4
+    q, k, _ = rand_qkv(25, B, H, W, heads, d, "f32")
+    c = rng.standard_normal((heads, d)).astype(np.float32)
+    v = np.broadcast_to(c, (B, H, W, heads, d)).copy()
+    announce(f"constant v {variant}")
+    out = P.forward(dev_t(q, "f32", dev), dev_t(k, "f32", dev), dev_t(v, "f32", dev), levels=L, K=3, variant=variant)
+    torch.cuda.synchronize()
+    assert rel_err(to_np(out), np.broadcast_to(c, out.shape)) <= 1e-5
+
+
+def test_deterministic(dev):
+    q, k, v = rand_qkv(26, 2, 40, 44, 2, 32, "bf16")
+    announce("determinism")
+    outs = []
+    for _ in range(2):
+        plan = P.Plan(2, 40, 44, 2, 32, levels=4, K=8, variant="B", dtype=torch.bfloat16, device=dev)
+        o = plan.run(dev_t(q, "bf16", dev), dev_t(k, "bf16", dev), dev_t(v, "bf16", dev))
+        torch.cuda.synchronize()
+        outs.append((to_np(o).tobytes(), to_np(plan.selection(1)[0]).tobytes(), to_np(plan.message(2)).tobytes()))
+    assert outs[0] == outs[1]
+
+
+def test_explicit_scale(dev):
+    q, k, v = rand_qkv(27, 1, 20, 20, 1, 32, "f32")
+    run_and_compare(dev, q, k, v, levels=3, K=4, variant="B", dtype="f32", scale=0.05, label="scale")
+
+
+# ------------------------------------------------------------------------------------------------
+# the five workloads at full size
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny", "matching", "stereo", "backbone", "highres"])
+def test_workload_full_size(dev, name):
+    wl = WORKLOADS[name]
+    q, k, v = make_qkv(wl)
+    w = make_level_weights(wl) if wl.variant == "B" else None
+    res, _, _ = run_and_compare(dev, q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w,
+                                label=name)
+    announce(f"{name}: out err {res['out']:.2e}; msg err {res['msg']}; selections {res['sel']}")
+
+
+def test_tiny_all_coarse_keys(dev):
+    """The 16x16 workload with K = 16 = every coarse token."""
+    wl = WORKLOADS["tiny"].with_(K=16)
+    q, k, v = make_qkv(wl)
+    run_and_compare(dev, q, k, v, levels=wl.levels, K=wl.K, variant="A", dtype="f32", label="tiny K=16")
+
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+def test_tiny_every_key_kept_matches_closed_forms(dev, variant):
+    """K = 64 keeps every key at every level of the 16x16 map: B is dense attention per level
+    (combined with w), A is the hierarchical closed form; both are checked through the oracle, which
+    the CPU pins tie to those closed forms."""
+    wl = WORKLOADS["tiny"].with_(K=64, variant=variant)
+    q, k, v = make_qkv(wl)
+    w = make_level_weights(wl) if variant == "B" else None
+    run_and_compare(dev, q, k, v, levels=wl.levels, K=64, variant=variant, dtype="f32", w=w, label="tiny K=64")
