@@ -105,6 +105,8 @@ def main() -> int:
     ap.add_argument("--kernel-launches", type=int, default=500, help="launches timed for the roofline kernel")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run plain device copies of this many MiB (to scale HBM byte counters) and exit")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -115,6 +117,17 @@ def main() -> int:
         return 2
 
     import torch
+
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"bench: 5 device copies of {n} bytes (each reads {n} and writes {n} bytes)")
+        return 0
 
     import paper_2201_02767_amd as P
     from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_qkv
@@ -147,7 +160,7 @@ def main() -> int:
     wall = time.perf_counter() - wall0
     ms_per_step = e0.elapsed_time(e1) / args.steps
     value = wl.tokens / (ms_per_step / 1e3)
-    log(f"bench: {args.steps} steps, {ms_per_step * 1e3:.2f} us/step (events), wall {wall * 1e3 / args.steps:.2f} "
+    log(f"bench: {args.steps} steps, {ms_per_step * 1e3:.2f} us/step (events), wall {wall * 1e6 / args.steps:.2f} "
         f"us/step, {value:.4g} query tokens/s")
 
     # the dominant kernel alone, on the same stream, on the selections the forward left behind
