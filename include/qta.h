@@ -20,12 +20,13 @@
  *   - Token tensors are NHWC, [B][H][W][heads][d] contiguous (C = heads*d channels), in the
  *     storage type `dtype` (fp32 or bf16). Pyramid levels use the same layout at their size.
  *   - Flat token index at level l: y*W_l + x.
- *   - Messages are fp32 [B][N_l][heads][d]. Selections are int32 [B][heads][N_l][K] holding flat
- *     key indices of level l, sorted by (score descending, index ascending); a query with fewer
- *     than K candidates is padded with -1. Scores are fp32 in the same shape (0 where the index
- *     is -1): QuadTree-B stores the softmax probability, QuadTree-A the recursive score s.
+ *   - Messages are fp32 [B][N_l][heads][d]. Selections are int32 [B][heads][N_l][K] holding the
+ *     flat key indices of level l that a query keeps. They form a set: the first min(K, number of
+ *     candidates) entries are the kept keys in an unspecified (but deterministic) order, the rest
+ *     are -1. Scores are fp32 in the same shape, aligned with the indices (0 where the index is
+ *     -1): QuadTree-B stores the softmax probability, QuadTree-A the recursive score s.
  *   - Each head is an independent quadtree. Softmax temperature: `scale` if > 0, else 1/sqrt(d).
- *   - Ties in a top-K selection go to the lower flat index.
+ *   - A query keeps the K candidates of highest score; ties at the cut go to the lower flat index.
  *
  * Memory and errors
  *   - Every tensor pointer is a DEVICE pointer that the caller owns; the library never
@@ -68,18 +69,26 @@ typedef enum { QTA_VARIANT_A = 0, QTA_VARIANT_B = 1 } qta_variant;
 typedef enum { QTA_F32 = 0, QTA_BF16 = 1 } qta_dtype;
 
 /* Byte offsets of the regions qta_forward keeps in its workspace. Entries for levels that do not
- * exist (and level 0 of q/k/v, msg, sel_idx, sel_key, which live outside it) are 0. */
+ * exist (and level 0 of q/k/v, msg, sel_idx, sel_key, which live outside it) are 0.
+ * Pyramid levels that later levels gather from (every level but the coarsest) are stored
+ * parent-blocked when blocked[l] is 1: [B][heads][ceil(H_l/2)][ceil(W_l/2)][2][2][d], i.e. the 2x2
+ * children of one parent position of one head are 4*d contiguous elements (off-map children are
+ * unused padding). The coarsest level is NHWC. With blocking on, the workspace also holds blocked
+ * copies of the input k and v. Blocking is used when 4*K <= 64. */
 typedef struct {
     int levels;
     int H[QTA_MAX_LEVELS];
     int W[QTA_MAX_LEVELS];
-    size_t q[QTA_MAX_LEVELS];       /* pyramid level l >= 1, [B][H_l][W_l][C] dtype       */
+    int blocked[QTA_MAX_LEVELS];    /* storage of pyramid level l (l >= 1) and of the k0/v0 copies */
+    size_t q[QTA_MAX_LEVELS];       /* pyramid level l >= 1, dtype                          */
     size_t k[QTA_MAX_LEVELS];
     size_t v[QTA_MAX_LEVELS];
-    size_t msg[QTA_MAX_LEVELS];     /* level l >= 1, fp32 [B][N_l][heads][d]               */
-    size_t sel_idx[QTA_MAX_LEVELS]; /* level l >= 1, int32 [B][heads][N_l][K]              */
-    size_t sel_key[QTA_MAX_LEVELS]; /* level l >= 1, fp32  [B][heads][N_l][K]              */
-    size_t total;                   /* bytes; every region starts on a 256-byte boundary   */
+    size_t msg[QTA_MAX_LEVELS];     /* level l >= 1, fp32 [B][N_l][heads][d]                 */
+    size_t sel_idx[QTA_MAX_LEVELS]; /* level l >= 1, int32 [B][heads][N_l][K]                */
+    size_t sel_key[QTA_MAX_LEVELS]; /* level l >= 1, fp32  [B][heads][N_l][K]                */
+    size_t k0_blocked;              /* blocked copy of the input k (valid when blocked[0])   */
+    size_t v0_blocked;              /* blocked copy of the input v (valid when blocked[0])   */
+    size_t total;                   /* bytes; every region starts on a 256-byte boundary     */
 } qta_workspace_layout;
 
 /* Human-readable name of a status code (static storage). */

@@ -3,12 +3,14 @@
 // One workgroup of 16 waves owns a 16-query tile of one (batch, head):
 //   phase 1  logits S = tau * Q_tile K^T on MFMA (16x16 output tiles, waves take key tiles in
 //            turn), kept in LDS as fp32 [16][N];
-//   phase 2  wave r owns query row r: max, exp and sum over the row, then the K best keys by
-//            repeated wave-wide maximum of a (logit, index) word, so ties go to the lower index;
-//            QuadTree-A zeroes the kept keys' weights (their mass is refined at the next level);
-//   phase 3  m = P V on MFMA: waves split the d columns into 16-wide tiles and the keys into
-//            chunks; partial tiles are summed through LDS and written as fp32 messages (or, for a
-//            single-level problem, straight to the output in the storage type).
+//   phase 2  wave r owns query row r: max, exp and sum over the row (register butterflies), then
+//            the K best keys by a bitwise radix select on wave ballots (ties at the cut go to the
+//            lower index), listed in index order; QuadTree-A zeroes the kept keys' weights (their
+//            mass is refined at the next level);
+//   phase 3  m = P V on fp32 MFMA (values widened to fp32 as they are loaded): waves split the d
+//            columns into 16-wide tiles and the keys into chunks; partial tiles are summed through
+//            LDS and written as fp32 messages (or, for a single-level problem, straight to the
+//            output in the storage type).
 // The coarsest map holds at most QTA_MAX_COARSE tokens, so a row fits in 16 registers per lane.
 #include "qta_device.h"
 #include "qta_internal.h"
@@ -22,15 +24,27 @@ typedef float float4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kRows = 16;                         // queries per workgroup
 constexpr int kWaves = 16;
-constexpr int kPerLane = QTA_MAX_COARSE / kWave;  // row elements per lane
 
-__host__ __device__ inline int coarse_pitch(int N) { return (N + 63) / 64 * 64; }
+// LDS pitch of a logit row: whole 64-element groups plus 4 floats, so the 16 rows that one MFMA
+// operand read touches fall in different banks.
+__host__ __device__ inline int coarse_pitch(int N) { return (N + 63) / 64 * 64 + 4; }
 
-template <typename T, int D, bool VA>
+// Row elements per lane, rounded up to a power of two (a template parameter, so the selection
+// loops carry no bounds checks).
+inline int coarse_per_lane(int N)
+{
+    const int need = (N + kWave - 1) / kWave;
+    int p = 1;
+    while (p < need) p <<= 1;
+    return p;
+}
+
+template <typename T, int D, bool VA, int kPerLane>
 __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
 {
     using S = Storage<T>;
     constexpr bool kBf16 = sizeof(T) == 2;
+    constexpr int kMaxTilesPerWave = QTA_MAX_COARSE / 16 / kWaves;
     extern __shared__ __align__(16) float smem[];
     const int N = a.N, C = a.C, pitch = coarse_pitch(N);
     float* Sm = smem;                              // [16][pitch]
@@ -45,38 +59,65 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     const size_t tok0 = static_cast<size_t>(b) * N;           // first token of this batch element
     const size_t hoff = static_cast<size_t>(h) * D;
 
-    // ---- phase 1: logits on MFMA ----
+    // ---- phase 1: logits on MFMA; a wave takes key tiles wave, wave+16, ... (at most 4) ----
     {
         const int arow = lane & 15, kgrp = lane >> 4;
         const int qi = tile * kRows + arow;
         const bool qok = qi < N;
-        for (int kt = wave; kt < tiles; kt += kWaves) {
-            const int n = kt * 16 + (lane & 15);
-            const bool nok = n < N;
-            float4_t acc = {0.f, 0.f, 0.f, 0.f};
-            if constexpr (kBf16) {
-                const uint16_t* qb = static_cast<const uint16_t*>(a.q) + (tok0 + qi) * C + hoff;
-                const uint16_t* kb = static_cast<const uint16_t*>(a.k) + (tok0 + n) * C + hoff;
+        if constexpr (kBf16) {
+            constexpr int KS = D / 16;
+            short4_t av[KS], bv[kMaxTilesPerWave][KS];
+            const uint16_t* qb = static_cast<const uint16_t*>(a.q) + (tok0 + (qok ? qi : 0)) * C + hoff;
 #pragma unroll
-                for (int ks = 0; ks < D / 16; ++ks) {
-                    short4_t av = {0, 0, 0, 0}, bv = {0, 0, 0, 0};
-                    if (qok) av = *reinterpret_cast<const short4_t*>(qb + ks * 16 + 4 * kgrp);
-                    if (nok) bv = *reinterpret_cast<const short4_t*>(kb + ks * 16 + 4 * kgrp);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, bv, acc, 0, 0, 0);
-                }
-            } else {
-                const float* qf = static_cast<const float*>(a.q) + (tok0 + qi) * C + hoff;
-                const float* kf = static_cast<const float*>(a.k) + (tok0 + n) * C + hoff;
+            for (int ks = 0; ks < KS; ++ks) {
+                av[ks] = short4_t{0, 0, 0, 0};
+                if (qok) av[ks] = *reinterpret_cast<const short4_t*>(qb + ks * 16 + 4 * kgrp);
+            }
 #pragma unroll
-                for (int ks = 0; ks < D / 4; ++ks) {
-                    const float av = qok ? qf[ks * 4 + kgrp] : 0.f;
-                    const float bv = nok ? kf[ks * 4 + kgrp] : 0.f;
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
+            for (int it = 0; it < kMaxTilesPerWave; ++it) {
+                const int n = (wave + kWaves * it) * 16 + (lane & 15);
+                const uint16_t* kb = static_cast<const uint16_t*>(a.k) + (tok0 + (n < N ? n : 0)) * C + hoff;
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    bv[it][ks] = short4_t{0, 0, 0, 0};
+                    if (n < N) bv[it][ks] = *reinterpret_cast<const short4_t*>(kb + ks * 16 + 4 * kgrp);
                 }
             }
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                Sm[(4 * kgrp + j) * pitch + n] = nok ? acc[j] * a.scale : -INFINITY;
+            for (int it = 0; it < kMaxTilesPerWave; ++it) {
+                const int kt = wave + kWaves * it;
+                if (kt >= tiles) break;
+                float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av[ks], bv[it][ks], acc, 0, 0, 0);
+                const int n = kt * 16 + (lane & 15);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) Sm[(4 * kgrp + j) * pitch + n] = n < N ? acc[j] * a.scale : -INFINITY;
+            }
+        } else {
+            constexpr int KS = D / 4;
+            float av[KS], bv[kMaxTilesPerWave][KS];
+            const float* qf = static_cast<const float*>(a.q) + (tok0 + (qok ? qi : 0)) * C + hoff;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) av[ks] = qok ? qf[ks * 4 + kgrp] : 0.f;
+#pragma unroll
+            for (int it = 0; it < kMaxTilesPerWave; ++it) {
+                const int n = (wave + kWaves * it) * 16 + (lane & 15);
+                const float* kf = static_cast<const float*>(a.k) + (tok0 + (n < N ? n : 0)) * C + hoff;
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) bv[it][ks] = n < N ? kf[ks * 4 + kgrp] : 0.f;
+            }
+#pragma unroll
+            for (int it = 0; it < kMaxTilesPerWave; ++it) {
+                const int kt = wave + kWaves * it;
+                if (kt >= tiles) break;
+                float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[ks], bv[it][ks], acc, 0, 0, 0);
+                const int n = kt * 16 + (lane & 15);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) Sm[(4 * kgrp + j) * pitch + n] = n < N ? acc[j] * a.scale : -INFINITY;
+            }
         }
     }
     __syncthreads();
@@ -94,7 +135,7 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
             x[e] = j < N ? row[j] : -INFINITY;
             mx = fmaxf(mx, x[e]);
         }
-        mx = wave_max(mx);
+        mx = wave_max_fast(mx);
         float p[kPerLane];
         float sum = 0.f;
 #pragma unroll
@@ -103,51 +144,38 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
             p[e] = j < N ? __expf(x[e] - mx) : 0.f;
             sum += p[e];
         }
-        sum = wave_sum(sum);
-        const float inv = 1.0f / sum;
+        const float inv = 1.0f / wave_sum_fast(sum);
 #pragma unroll
         for (int e = 0; e < kPerLane; ++e) p[e] *= inv;
 
         if (a.K > 0 && qi < N) {
-            uint64_t word[kPerLane];
+            // the K best keys by logit (ties to the lower index), listed in index order
+            uint32_t key[kPerLane], name[kPerLane];
+            bool kept[kPerLane];
 #pragma unroll
             for (int e = 0; e < kPerLane; ++e) {
                 const int j = lane + kWave * e;
-                word[e] = j < N ? rank_word(x[e], j) : 0ull;
+                key[e] = j < N ? ordered_bits(x[e]) : 0u;
+                name[e] = static_cast<uint32_t>(j);
             }
             const int keff = a.K < N ? a.K : N;
+            wave_select_top<kPerLane>(key, name, keff, kept);
             const size_t orow = ((static_cast<size_t>(b) * a.heads + h) * N + qi) * a.K;
-            for (int rr = 0; rr < a.K; ++rr) {
-                if (rr >= keff) {
-                    if (lane == 0) {
-                        a.sel_idx[orow + rr] = -1;
-                        a.sel_key[orow + rr] = 0.f;
-                    }
-                    continue;
-                }
-                uint64_t best = 0;
-                float bestp = 0.f;
+            int before = 0;
 #pragma unroll
-                for (int e = 0; e < kPerLane; ++e)
-                    if (word[e] > best) {
-                        best = word[e];
-                        bestp = p[e];
-                    }
-                const uint64_t g = wave_max_u64(best);
-                const int j = rank_word_index(g);
-                const float pj = __shfl(bestp, j & 63, kWave);
-                if (lane == (j & 63)) {
-#pragma unroll
-                    for (int e = 0; e < kPerLane; ++e)
-                        if (e == (j >> 6)) {
-                            word[e] = 0ull;
-                            if constexpr (VA) p[e] = 0.f;
-                        }
+            for (int e = 0; e < kPerLane; ++e) {
+                const uint64_t mask = __ballot(kept[e]);
+                if (kept[e]) {
+                    const int pos = before + lanes_below(mask);
+                    a.sel_idx[orow + pos] = lane + kWave * e;
+                    a.sel_key[orow + pos] = p[e];
+                    if constexpr (VA) p[e] = 0.f;           // refined at the next level (Omega)
                 }
-                if (lane == 0) {
-                    a.sel_idx[orow + rr] = j;
-                    a.sel_key[orow + rr] = pj;
-                }
+                before += __popcll(mask);
+            }
+            if (lane >= keff && lane < a.K) {
+                a.sel_idx[orow + lane] = -1;
+                a.sel_key[orow + lane] = 0.f;
             }
         }
 #pragma unroll
@@ -158,40 +186,28 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     }
     __syncthreads();
 
-    // ---- phase 3: messages m = P V on MFMA ----
+    // ---- phase 3: messages m = P V on fp32 MFMA (values widened on load, so no transpose) ----
     constexpr int NCT = D / 16;          // 16-wide column tiles
     constexpr int NKS = kWaves / NCT;    // key chunks
     {
         const int ct = wave % NCT, ks = wave / NCT;
         const int arow = lane & 15, kgrp = lane >> 4;
         const int ch = ct * 16 + (lane & 15);
+        const int steps = (N + 3) / 4;
         float4_t acc = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (kBf16) {
-            const uint16_t* vb = static_cast<const uint16_t*>(a.v) + tok0 * C + hoff + ch;
-            const int steps = (N + 15) / 16;
-            for (int st = ks; st < steps; st += NKS) {
-                const float4 pv = *reinterpret_cast<const float4*>(Sm + arow * pitch + st * 16 + 4 * kgrp);
-                short4_t av;
-                av[0] = static_cast<short>(f32_to_bf16_bits(pv.x));
-                av[1] = static_cast<short>(f32_to_bf16_bits(pv.y));
-                av[2] = static_cast<short>(f32_to_bf16_bits(pv.z));
-                av[3] = static_cast<short>(f32_to_bf16_bits(pv.w));
-                short4_t bv;
+        constexpr int kBatch = 8;
+        for (int st0 = ks; st0 < steps; st0 += NKS * kBatch) {
+            float bv[kBatch];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int cand = st * 16 + 4 * kgrp + e;
-                    bv[e] = cand < N ? static_cast<short>(vb[static_cast<size_t>(cand) * C]) : short(0);
-                }
-                acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, bv, acc, 0, 0, 0);
+            for (int u = 0; u < kBatch; ++u) {
+                const int cand = (st0 + u * NKS) * 4 + kgrp;
+                bv[u] = cand < N ? S::load1(a.v, (tok0 + cand) * C + hoff + ch) : 0.f;
             }
-        } else {
-            const float* vf = static_cast<const float*>(a.v) + tok0 * C + hoff + ch;
-            const int steps = (N + 3) / 4;
-            for (int st = ks; st < steps; st += NKS) {
-                const float av = Sm[arow * pitch + st * 4 + kgrp];
-                const int cand = st * 4 + kgrp;
-                const float bv = cand < N ? vf[static_cast<size_t>(cand) * C] : 0.f;
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int st = st0 + u * NKS;
+                if (st >= steps) break;
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Sm[arow * pitch + st * 4 + kgrp], bv[u], acc, 0, 0, 0);
             }
         }
 #pragma unroll
@@ -216,14 +232,14 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     }
 }
 
-template <typename T, int D, bool VA>
+template <typename T, int D, bool VA, int kPerLane>
 hipError_t launch_one(const CoarseArgs& a, hipStream_t stream)
 {
     const size_t lds = (static_cast<size_t>(kRows) * coarse_pitch(a.N) + kWaves * 16 * 16) * sizeof(float);
     if (lds > device_max_lds()) return hipErrorInvalidValue;
     static bool configured = false;
     if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&coarse_attn_kernel<T, D, VA>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&coarse_attn_kernel<T, D, VA, kPerLane>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            static_cast<int>(device_max_lds()));
         if (e != hipSuccess) return e;
@@ -232,17 +248,30 @@ hipError_t launch_one(const CoarseArgs& a, hipStream_t stream)
     const int tiles = (a.N + kRows - 1) / kRows;
     const long long blocks = static_cast<long long>(a.B) * a.heads * tiles;
     if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((coarse_attn_kernel<T, D, VA>), dim3(static_cast<unsigned>(blocks)), dim3(kWaves * kWave),
+    hipLaunchKernelGGL((coarse_attn_kernel<T, D, VA, kPerLane>), dim3(static_cast<unsigned>(blocks)), dim3(kWaves * kWave),
                        lds, stream, a);
     return hipGetLastError();
+}
+
+template <typename T, int D, bool VA>
+hipError_t launch_per_lane(const CoarseArgs& a, hipStream_t stream)
+{
+    switch (coarse_per_lane(a.N)) {
+    case 1: return launch_one<T, D, VA, 1>(a, stream);
+    case 2: return launch_one<T, D, VA, 2>(a, stream);
+    case 4: return launch_one<T, D, VA, 4>(a, stream);
+    case 8: return launch_one<T, D, VA, 8>(a, stream);
+    case 16: return launch_one<T, D, VA, 16>(a, stream);
+    }
+    return hipErrorInvalidValue;
 }
 
 }  // namespace
 
 hipError_t launch_coarse_attn(const CoarseArgs& a, int d, bool variant_a, bool bf16_in, hipStream_t stream)
 {
-#define QTA_COARSE_CASE(T, D)                                                        \
-    if (d == D) return variant_a ? launch_one<T, D, true>(a, stream) : launch_one<T, D, false>(a, stream);
+#define QTA_COARSE_CASE(T, D)                                                                     \
+    if (d == D) return variant_a ? launch_per_lane<T, D, true>(a, stream) : launch_per_lane<T, D, false>(a, stream);
     if (bf16_in) {
         QTA_COARSE_CASE(bf16, 32)
         QTA_COARSE_CASE(bf16, 64)

@@ -3,21 +3,23 @@
 // top-K, and at level 0 the combination of all levels' messages (Eqs. 2 and 5).
 //
 // Work item = one parent query P at level l+1 and one head. Its four children at level l are
-// sibling queries with the same candidate set: the 2x2 children of the K keys P kept. One wave
-// owns one item:
-//   1. slot 4r+c names child c ((0,0),(0,1),(1,0),(1,1)) of kept key r; lane = slot;
-//   2. the candidates' key and value rows of this head (d elements each) are gathered once with
-//      16-byte loads, several lanes per row, into wave-private LDS, together with the four
-//      queries (scaled by the temperature);
-//   3. each lane computes its candidate's logits against the four queries;
-//   4. B: a wave-wide softmax per query; A: a softmax over each quad of lanes (the children of
-//      one kept key) times the parent's score;
-//   5. levels above 0: a wave-wide bitonic sort per query of (score, flat index) words yields
-//      this level's kept keys; A drops their weight from the message (refined one level down);
-//   6. the message m = sum w v: lane = (query, d/16 channels), reading weights and values from LDS;
-//   7. levels above 0 store m; level 0 adds the ancestors' messages (times w for B) and stores
-//      the output in the storage type.
-// A workgroup holds up to four independent waves; nothing synchronises across waves.
+// sibling queries with one shared candidate set: the 2x2 children of the K keys P kept (4K <= 64
+// candidates here; larger K runs the kernel of fine_wide.hip). One wave owns one item, and lane s
+// owns candidate slot s = 4r + c (child c, in the order (0,0),(0,1),(1,0),(1,1), of kept key r):
+//   1. the candidates' key and value rows of this head are gathered once for the four queries,
+//      with 16-byte loads, several lanes per row, into wave-private LDS (values transposed). In the
+//      blocked layout a kept key's four children are one contiguous run, so a gather instruction
+//      reads whole cache lines;
+//   2. logits S[query][slot] on the 4x4x4 MFMA: each of the 16 blocks multiplies the four queries
+//      by the four candidates of one lane quad, so lane s ends with the four logits of slot s;
+//   3. B: a softmax per query over the wave (DPP and permlane butterflies, no LDS);
+//      A: a softmax over each lane quad (the children of one kept key) times the parent's score;
+//   4. levels above 0: the K best candidates of each query by a bitwise radix select on wave
+//      ballots (ties at the cut to the lower flat index); A drops their weight from its message;
+//   5. messages m = P V on the same MFMA, blocks split over 4-channel groups (and slot halves);
+//   6. levels above 0 store m; level 0 adds the ancestors' messages (times w for B) and stores the
+//      output in the storage type.
+// A workgroup holds four independent waves; nothing synchronises across waves.
 #include "qta_device.h"
 #include "qta_internal.h"
 
@@ -25,79 +27,70 @@ namespace qta {
 
 namespace {
 
-__host__ __device__ inline size_t fine_wave_bytes(int nslot, int d, int tbytes)
-{
-    const size_t rb = static_cast<size_t>(d) * tbytes;
-    return static_cast<size_t>(nslot) * (rb + 16) + static_cast<size_t>(nslot) * rb + 4 * d * sizeof(float) +
-           4 * static_cast<size_t>(nslot) * sizeof(float);
-}
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
 
-template <typename T, int CPL>
-__device__ __forceinline__ void load_vals(const unsigned char* p, float (&o)[CPL])
+constexpr int kMaxSlots = 64;
+constexpr int kPrefetchLevels = 7;    // the finest level prefetches up to this many ancestors
+
+// Byte layout of one wave's LDS region for nsp padded slots (a multiple of 16).
+struct WaveLds {
+    int q, k, v, p, total;
+    int vpitch;    // bf16: elements per transposed value row; fp32: floats per value row
+};
+
+template <typename T, int D>
+__host__ __device__ inline WaveLds wave_lds(int nsp)
 {
-    if constexpr (sizeof(T) == 4) {
-        if constexpr (CPL == 2) {
-            const float2 v = *reinterpret_cast<const float2*>(p);
-            o[0] = v.x;
-            o[1] = v.y;
-        } else {
-            const float4 v = *reinterpret_cast<const float4*>(p);
-            o[0] = v.x;
-            o[1] = v.y;
-            o[2] = v.z;
-            o[3] = v.w;
-        }
+    constexpr int TB = sizeof(T), RB = D * TB, KP = RB + 16;
+    WaveLds L;
+    L.q = 0;
+    L.k = 4 * RB;
+    L.v = L.k + nsp * KP;
+    int vbytes;
+    if (TB == 2) {
+        L.vpitch = nsp + 8;                 // Vt[channel][slot]
+        vbytes = D * L.vpitch * 2;
     } else {
-        if constexpr (CPL == 2) {
-            const uint32_t v = *reinterpret_cast<const uint32_t*>(p);
-            o[0] = __uint_as_float(v << 16);
-            o[1] = __uint_as_float(v & 0xFFFF0000u);
-        } else {
-            const uint2 v = *reinterpret_cast<const uint2*>(p);
-            o[0] = __uint_as_float(v.x << 16);
-            o[1] = __uint_as_float(v.x & 0xFFFF0000u);
-            o[2] = __uint_as_float(v.y << 16);
-            o[3] = __uint_as_float(v.y & 0xFFFF0000u);
-        }
+        L.vpitch = D + 4;                   // Vs[slot][channel]
+        vbytes = nsp * L.vpitch * 4;
     }
+    L.p = L.v + vbytes;
+    L.total = (L.p + 4 * nsp * TB + 15) / 16 * 16;
+    return L;
 }
 
-template <typename T, int CPL>
-__device__ __forceinline__ void store_vals(void* base, size_t elem, const float (&o)[CPL])
+__device__ __forceinline__ float pick4(const float4_t& v, int i)
 {
-    if constexpr (sizeof(T) == 4) {
-        float* p = static_cast<float*>(base) + elem;
-        if constexpr (CPL == 2) *reinterpret_cast<float2*>(p) = make_float2(o[0], o[1]);
-        else *reinterpret_cast<float4*>(p) = make_float4(o[0], o[1], o[2], o[3]);
-    } else {
-        uint16_t* p = static_cast<uint16_t*>(base) + elem;
-        if constexpr (CPL == 2) {
-            *reinterpret_cast<uint32_t*>(p) = f32_to_bf16_bits(o[0]) | (f32_to_bf16_bits(o[1]) << 16);
-        } else {
-            *reinterpret_cast<uint2*>(p) = make_uint2(f32_to_bf16_bits(o[0]) | (f32_to_bf16_bits(o[1]) << 16),
-                                                      f32_to_bf16_bits(o[2]) | (f32_to_bf16_bits(o[3]) << 16));
-        }
-    }
+    return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
 }
 
-template <typename T, int D, bool VA, bool FINEST, int NT>
+__device__ __forceinline__ float pick4(const float (&v)[4], int i)
+{
+    return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
+}
+
+template <typename T, int D, bool VA, bool FINEST>
 __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
 {
     using S = Storage<T>;
+    constexpr bool kBf16 = sizeof(T) == 2;
     constexpr int TB = sizeof(T);
-    constexpr int RB = D * TB;            // bytes of one head's row
-    constexpr int KP = RB + 16;           // LDS pitch of key rows (padding spreads the banks)
-    constexpr int E = S::kPer16B;
-    constexpr int LPR = RB / 16;          // lanes per row when gathering
-    constexpr int RPP = kWave / LPR;      // rows per gather instruction
-    constexpr int CPL = D / 16;           // message channels per lane
+    constexpr int RB = D * TB;             // bytes of one head's row
+    constexpr int KP = RB + 16;            // LDS pitch of key rows (padding spreads the banks)
+    constexpr int E = S::kPer16B;          // elements per 16-byte chunk
+    constexpr int LPR = RB / 16;           // lanes per row when gathering
+    constexpr int RPP = kWave / LPR;       // rows per gather instruction
+    constexpr int NCG = D / 4;             // PV: 4-channel groups
+    constexpr int NH = 16 / NCG;           // PV: slot halves (2 for d = 32, 1 for d = 64)
+    constexpr int QPL = 4 / NH;            // output queries per lane
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wpb = blockDim.x >> 6;
     const int Np = a.Hp * a.Wp;
     const long long nitems = static_cast<long long>(a.B) * a.heads * Np;
     const long long item = static_cast<long long>(xcd_remap(blockIdx.x, gridDim.x)) * wpb + wave;
-    if (item >= nitems) return;           // whole wave leaves; only wave-level syncs follow
+    if (item >= nitems) return;            // whole wave leaves; only wave-level syncs follow
 
     const int h = static_cast<int>(item % a.heads);
     const long long bp = item / a.heads;
@@ -107,314 +100,324 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     const int H = a.H, W = a.W, C = a.C, K = a.K;
     const int N = H * W;
     const int nslot = 4 * K;
+    const int nsp = (nslot + 15) & ~15;
 
     extern __shared__ __align__(16) unsigned char smem[];
-    unsigned char* Ks = smem + static_cast<size_t>(wave) * fine_wave_bytes(nslot, D, TB);
-    unsigned char* Vs = Ks + static_cast<size_t>(nslot) * KP;
-    float* Qs = reinterpret_cast<float*>(Vs + static_cast<size_t>(nslot) * RB);
-    float* Ps = Qs + 4 * D;
+    const WaveLds lay = wave_lds<T, D>(nsp);
+    unsigned char* base = smem + static_cast<size_t>(wave) * lay.total;
+    unsigned char* Qs = base + lay.q;
+    unsigned char* Ks = base + lay.k;
+    unsigned char* Vb = base + lay.v;
+    unsigned char* Pb = base + lay.p;
 
-    // ---- 1. candidate slots ----
     const size_t prow = ((static_cast<size_t>(b) * a.heads + h) * Np + P) * K;
-    int flat[NT];
-    float pkey[NT];
+    auto child_of_slot = [&](int s) -> int {           // flat index at level l, or -1
+        if (s >= nslot) return -1;
+        const int J = a.parent_idx[prow + (s >> 2)];
+        if (J < 0) return -1;
+        const int Jy = J / a.Wp, Jx = J - Jy * a.Wp;
+        const int cy = 2 * Jy + ((s >> 1) & 1), cx = 2 * Jx + (s & 1);
+        return (cy < H && cx < W) ? cy * W + cx : -1;
+    };
+
+    // ---- 1. this lane's slot; gather key/value rows and the four queries into LDS ----
+    const int flat = child_of_slot(lane);
+    const bool ok = flat >= 0;
+    float pkey = 0.f;
+    if constexpr (VA)
+        if (lane < nslot) pkey = a.parent_key[prow + (lane >> 2)];
+
+    // Output ownership (step 6): lane 4*blk + t4 with blk = cg*NH + hh owns channel 4*cg + t4 of
+    // queries hh*QPL .. hh*QPL + QPL-1. At the finest level the ancestors' messages and the level
+    // weights of those queries are loaded here, so their latency overlaps the gather.
+    const int blk = lane >> 2, t4 = lane & 3;
+    const int cg = blk / NH, hh = blk % NH;
+    const int ch = 4 * cg + t4;
+    constexpr int kPre = FINEST ? kPrefetchLevels : 1;
+    float anc[kPre] = {};
+    float wq[FINEST ? QPL : 1][kPre + 1] = {};
+    const bool prefetch = FINEST && a.levels <= kPre + 1;
+    if constexpr (FINEST) {
+        if (prefetch) {
+            const int qy0 = 2 * Py, qx0 = 2 * Px;                // ancestors are shared by the siblings
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        const int s = lane + kWave * t;
-        flat[t] = -1;
-        pkey[t] = 0.f;
-        if (s < nslot) {
-            const int r = s >> 2, c = s & 3;
-            const int J = a.parent_idx[prow + r];
-            if (J >= 0) {
-                const int Jy = J / a.Wp, Jx = J - Jy * a.Wp;
-                const int cy = 2 * Jy + (c >> 1), cx = 2 * Jx + (c & 1);
-                if (cy < H && cx < W) flat[t] = cy * W + cx;
+            for (int lev = 1; lev <= kPre; ++lev) {
+                if (lev >= a.levels) break;
+                const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
+                                  static_cast<size_t>(qy0 >> lev) * a.lvl_W[lev] + (qx0 >> lev);
+                anc[lev - 1] = a.coarser_msg[lev][(an * a.heads + h) * D + ch];
             }
-            if constexpr (VA) pkey[t] = a.parent_key[prow + r];
+            if (!VA && a.w) {
+#pragma unroll
+                for (int u = 0; u < QPL; ++u) {
+                    const int qi = (NH == 2 ? hh * QPL : 0) + u;
+                    const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
+                    if (qy >= H || qx >= W) continue;
+                    const float* wrow = a.w + ((static_cast<size_t>(b) * N + qy * W + qx) * a.heads + h) * a.levels;
+#pragma unroll
+                    for (int lev = 0; lev <= kPre; ++lev)
+                        if (lev < a.levels) wq[u][lev] = wrow[lev];
+                }
+            }
         }
     }
-
-    // ---- 2. gather key/value rows and the four queries into LDS ----
     {
-        const unsigned char* kg = static_cast<const unsigned char*>(a.k) + (static_cast<size_t>(b) * N * C + h * D) * TB;
-        const unsigned char* vg = static_cast<const unsigned char*>(a.v) + (static_cast<size_t>(b) * N * C + h * D) * TB;
-        const int sub = lane / LPR, chunk = lane % LPR;
+        // NHWC: child f of this head at kg + f*C*TB. Blocked: the four children of kept key J are
+        // the 4*RB bytes at kg + J*4*RB (this (batch, head)'s blocks start at kg).
+        const bool kvb = a.kv_blocked;
+        const size_t kv_base = kvb ? (static_cast<size_t>(b) * a.heads + h) * Np * 4 * RB
+                                   : (static_cast<size_t>(b) * N * C + h * D) * TB;
         const size_t tok_bytes = static_cast<size_t>(C) * TB;
-        constexpr int kBatch = 4;
-        for (int s0 = 0; s0 < nslot; s0 += RPP * kBatch) {
-            uint4 kc[kBatch], vc[kBatch];
-            int ss[kBatch];
+        const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base;
+        const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base;
+        const int sub = lane / LPR, chunk = lane % LPR;
+        constexpr int kRounds = kMaxSlots / RPP;           // gather instructions per tensor
+        constexpr int kGroup = kRounds < 4 ? kRounds : 4;  // loads in flight per tensor
+        // the four sibling queries (off-map ones as zeros)
+        if (sub < 4) {
+            const int qy = 2 * Py + (sub >> 1), qx = 2 * Px + (sub & 1);
+            uint4 qc = make_uint4(0, 0, 0, 0);
+            if (qy < H && qx < W) {
+                const size_t qoff = a.q_blocked
+                                        ? (((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 + sub) * RB
+                                        : ((static_cast<size_t>(b) * N + qy * W + qx) * C + h * D) * TB;
+                qc = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.q) + qoff + chunk * 16);
+            }
+            *reinterpret_cast<uint4*>(Qs + sub * RB + chunk * 16) = qc;
+        }
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-                const int s = s0 + u * RPP + sub;
-                ss[u] = s;
-                int f = -1;
+        for (int g = 0; g < kRounds; g += kGroup) {
+            if (g * RPP >= nsp) break;
+            uint4 kc[kGroup], vc[kGroup];
 #pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const int ft = __shfl(flat[t], s & 63, kWave);
-                    if ((s >> 6) == t) f = ft;
-                }
+            for (int u = 0; u < kGroup; ++u) {
+                const int s = (g + u) * RPP + sub;
                 kc[u] = make_uint4(0, 0, 0, 0);
                 vc[u] = make_uint4(0, 0, 0, 0);
-                if (s < nslot && f >= 0) {
-                    kc[u] = *reinterpret_cast<const uint4*>(kg + f * tok_bytes + chunk * 16);
-                    vc[u] = *reinterpret_cast<const uint4*>(vg + f * tok_bytes + chunk * 16);
+                const int f = s < nsp ? child_of_slot(s) : -1;
+                if (f >= 0) {
+                    const size_t off = kvb ? (static_cast<size_t>(a.parent_idx[prow + (s >> 2)]) * 4 + (s & 3)) * RB
+                                           : f * tok_bytes;
+                    kc[u] = *reinterpret_cast<const uint4*>(kg + off + chunk * 16);
+                    vc[u] = *reinterpret_cast<const uint4*>(vg + off + chunk * 16);
                 }
             }
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-                if (ss[u] < nslot) {
-                    *reinterpret_cast<uint4*>(Ks + static_cast<size_t>(ss[u]) * KP + chunk * 16) = kc[u];
-                    *reinterpret_cast<uint4*>(Vs + static_cast<size_t>(ss[u]) * RB + chunk * 16) = vc[u];
+            for (int u = 0; u < kGroup; ++u) {
+                const int s = (g + u) * RPP + sub;
+                if (s >= nsp) continue;
+                *reinterpret_cast<uint4*>(Ks + s * KP + chunk * 16) = kc[u];
+                if constexpr (kBf16) {
+                    uint16_t* vt = reinterpret_cast<uint16_t*>(Vb);
+                    const uint32_t w4[4] = {vc[u].x, vc[u].y, vc[u].z, vc[u].w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const uint32_t bits = (e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xFFFFu);
+                        vt[(chunk * E + e) * lay.vpitch + s] = static_cast<uint16_t>(bits);
+                    }
+                } else {
+                    *reinterpret_cast<uint4*>(Vb + (s * lay.vpitch + chunk * E) * 4) = vc[u];
                 }
             }
-        }
-        for (int e = lane; e < 4 * D; e += kWave) {
-            const int qi = e / D, c = e - qi * D;
-            const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
-            float val = 0.f;
-            if (qy < H && qx < W)
-                val = S::load1(a.q, (static_cast<size_t>(b) * N + qy * W + qx) * C + h * D + c) * a.scale;
-            Qs[e] = val;
         }
     }
     wave_lds_sync();
 
-    // ---- 3. logits: lane = candidate slot ----
-    bool ok[NT];
-    float x[NT][4];
+    // ---- 2. logits on MFMA: lane 4*blk + j holds S[query r][slot lane] in register r ----
+    float x[4];
+    {
+        const int srow = lane < nsp ? lane : nsp - 1;
+        const int qi = lane & 3;
+        float4_t acc = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (kBf16) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        const int s = lane + kWave * t;
-        ok[t] = s < nslot && flat[t] >= 0;
-        const int sr = s < nslot ? s : nslot - 1;
-        float kf[D];
-#pragma unroll
-        for (int cc = 0; cc < RB / 16; ++cc) {
-            const uint4 c = *reinterpret_cast<const uint4*>(Ks + static_cast<size_t>(sr) * KP + cc * 16);
-            float tmp[E];
-            S::unpack(c, tmp);
-#pragma unroll
-            for (int e = 0; e < E; ++e) kf[cc * E + e] = tmp[e];
-        }
-#pragma unroll
-        for (int qi = 0; qi < 4; ++qi) {
-            float acc = 0.f;
-#pragma unroll
-            for (int c = 0; c < D; c += 4) {
-                const float4 q4 = *reinterpret_cast<const float4*>(Qs + qi * D + c);
-                acc += q4.x * kf[c] + q4.y * kf[c + 1] + q4.z * kf[c + 2] + q4.w * kf[c + 3];
+            for (int c0 = 0; c0 < D; c0 += 8) {
+                const uint4 kq = *reinterpret_cast<const uint4*>(Ks + srow * KP + c0 * 2);
+                const uint4 qq = *reinterpret_cast<const uint4*>(Qs + qi * RB + c0 * 2);
+                short4_t a0, b0, a1, b1;
+                a0[0] = static_cast<short>(qq.x); a0[1] = static_cast<short>(qq.x >> 16);
+                a0[2] = static_cast<short>(qq.y); a0[3] = static_cast<short>(qq.y >> 16);
+                a1[0] = static_cast<short>(qq.z); a1[1] = static_cast<short>(qq.z >> 16);
+                a1[2] = static_cast<short>(qq.w); a1[3] = static_cast<short>(qq.w >> 16);
+                b0[0] = static_cast<short>(kq.x); b0[1] = static_cast<short>(kq.x >> 16);
+                b0[2] = static_cast<short>(kq.y); b0[3] = static_cast<short>(kq.y >> 16);
+                b1[0] = static_cast<short>(kq.z); b1[1] = static_cast<short>(kq.z >> 16);
+                b1[2] = static_cast<short>(kq.w); b1[3] = static_cast<short>(kq.w >> 16);
+                acc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a0, b0, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a1, b1, acc, 0, 0, 0);
             }
-            x[t][qi] = ok[t] ? acc : -INFINITY;
+        } else {
+#pragma unroll
+            for (int c0 = 0; c0 < D; c0 += 4) {
+                const float4 kq = *reinterpret_cast<const float4*>(Ks + srow * KP + c0 * 4);
+                const float4 qq = *reinterpret_cast<const float4*>(Qs + qi * RB + c0 * 4);
+                acc = __builtin_amdgcn_mfma_f32_4x4x1f32(qq.x, kq.x, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_4x4x1f32(qq.y, kq.y, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_4x4x1f32(qq.z, kq.z, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_4x4x1f32(qq.w, kq.w, acc, 0, 0, 0);
+            }
         }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[r] = ok ? acc[r] * a.scale : -INFINITY;
     }
 
-    // ---- 4. weights ----
-    float wgt[NT][4];
-    float mx[4], inv_sum[4];
+    // ---- 3. weights ----
+    float wgt[4], inv_sum[4] = {1.f, 1.f, 1.f, 1.f};
     if constexpr (!VA) {
 #pragma unroll
-        for (int qi = 0; qi < 4; ++qi) {
-            float m = -INFINITY;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) m = fmaxf(m, x[t][qi]);
-            m = wave_max(m);
-            float sum = 0.f;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                wgt[t][qi] = ok[t] ? __expf(x[t][qi] - m) : 0.f;
-                sum += wgt[t][qi];
-            }
-            sum = wave_sum(sum);
-            mx[qi] = m;
-            inv_sum[qi] = 1.0f / sum;
+        for (int r = 0; r < 4; ++r) {
+            const float m = wave_max_fast(x[r]);
+            wgt[r] = ok ? __expf(x[r] - m) : 0.f;
+            inv_sum[r] = 1.0f / wave_sum_fast(wgt[r]);
         }
     } else {
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
-#pragma unroll
-            for (int qi = 0; qi < 4; ++qi) {
-                float m = x[t][qi];
-                m = fmaxf(m, __shfl_xor(m, 1, kWave));
-                m = fmaxf(m, __shfl_xor(m, 2, kWave));
-                const float e = ok[t] ? __expf(x[t][qi] - m) : 0.f;
-                float s = e;
-                s += __shfl_xor(s, 1, kWave);
-                s += __shfl_xor(s, 2, kWave);
-                wgt[t][qi] = ok[t] ? pkey[t] * (e / s) : 0.f;
-            }
-#pragma unroll
-        for (int qi = 0; qi < 4; ++qi) {
-            mx[qi] = 0.f;
-            inv_sum[qi] = 1.f;
+        for (int r = 0; r < 4; ++r) {
+            float m = fmaxf(x[r], xchg_f32<1>(x[r]));
+            m = fmaxf(m, xchg_f32<2>(m));
+            const float e = ok ? __expf(x[r] - m) : 0.f;
+            float s = e + xchg_f32<1>(e);
+            s += xchg_f32<2>(s);
+            wgt[r] = ok ? pkey * (e / s) : 0.f;
         }
     }
 
-    // ---- 5. this level's selection (levels above the finest) ----
+    // ---- 4. this level's selection (levels above the finest) ----
     if constexpr (!FINEST) {
-        int nvalid = 0;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) nvalid += __popcll(__ballot(ok[t]));
+        const int nvalid = __popcll(__ballot(ok));
         const int keff = K < nvalid ? K : nvalid;
 #pragma unroll
-        for (int qi = 0; qi < 4; ++qi) {
-            const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
-            if (qy >= H || qx >= W) continue;                  // uniform across the wave
-            uint64_t word[NT];
-#pragma unroll
-            for (int t = 0; t < NT; ++t) word[t] = ok[t] ? rank_word(VA ? wgt[t][qi] : x[t][qi], flat[t]) : 0ull;
-            wave_bitonic_sort_desc<NT>(word);
+        for (int r = 0; r < 4; ++r) {
+            const int qy = 2 * Py + (r >> 1), qx = 2 * Px + (r & 1);
+            if (qy >= H || qx >= W) continue;                 // uniform across the wave
+            const uint32_t key[1] = {ok ? ordered_bits(VA ? wgt[r] : x[r]) : 0u};
+            const uint32_t name[1] = {static_cast<uint32_t>(flat)};
+            bool kept[1];
+            wave_select_top<1>(key, name, keff, kept);
+            const uint64_t mask = __ballot(kept[0]);
             const size_t orow = ((static_cast<size_t>(b) * a.heads + h) * N + qy * W + qx) * K;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const int r = kWave * t + lane;
-                if (r < K) {
-                    const uint64_t wd = word[t];
-                    int32_t idx = -1;
-                    float key = 0.f;
-                    if (wd != 0ull) {
-                        idx = rank_word_index(wd);
-                        const float sc = rank_word_score(wd);
-                        key = VA ? sc : __expf(sc - mx[qi]) * inv_sum[qi];
-                    }
-                    a.sel_idx[orow + r] = idx;
-                    a.sel_key[orow + r] = key;
-                }
+            if (kept[0]) {
+                const int pos = lanes_below(mask);
+                a.sel_idx[orow + pos] = flat;
+                a.sel_key[orow + pos] = VA ? wgt[r] : wgt[r] * inv_sum[r];
+                if constexpr (VA) wgt[r] = 0.f;               // refined at the next level (Omega)
             }
-            if constexpr (VA) {
-                // the kept keys are exactly the candidates whose word is >= the keff-th largest
-                if (keff > 0) {
-                    const int last = keff - 1;
-                    uint64_t thr = 0ull;
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) {
-                        const uint32_t lo = __shfl(static_cast<uint32_t>(word[t]), last & 63, kWave);
-                        const uint32_t hi = __shfl(static_cast<uint32_t>(word[t] >> 32), last & 63, kWave);
-                        if ((last >> 6) == t) thr = (static_cast<uint64_t>(hi) << 32) | lo;
-                    }
-#pragma unroll
-                    for (int t = 0; t < NT; ++t)
-                        if (ok[t] && rank_word(wgt[t][qi], flat[t]) >= thr) wgt[t][qi] = 0.f;
-                }
+            if (lane >= keff && lane < K) {
+                a.sel_idx[orow + lane] = -1;
+                a.sel_key[orow + lane] = 0.f;
             }
         }
     }
 
-    // ---- 6. message m = sum_slot w * v ----
+    // ---- 5. messages on MFMA ----
+    if (lane < nsp) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        const int s = lane + kWave * t;
-        if (s < nslot)
-#pragma unroll
-            for (int qi = 0; qi < 4; ++qi) Ps[qi * nslot + s] = wgt[t][qi];
+        for (int r = 0; r < 4; ++r) {
+            if constexpr (kBf16)
+                reinterpret_cast<uint16_t*>(Pb)[r * nsp + lane] = static_cast<uint16_t>(f32_to_bf16_bits(wgt[r]));
+            else
+                reinterpret_cast<float*>(Pb)[r * nsp + lane] = wgt[r];
+        }
     }
     wave_lds_sync();
 
-    const int pq = lane >> 4, cg = lane & 15;
-    float acc[CPL];
-#pragma unroll
-    for (int e = 0; e < CPL; ++e) acc[e] = 0.f;
-    for (int s = 0; s < nslot; s += 4) {
-        const float4 p4 = *reinterpret_cast<const float4*>(Ps + pq * nslot + s);
-        const float pw[4] = {p4.x, p4.y, p4.z, p4.w};
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            float vv[CPL];
-            load_vals<T, CPL>(Vs + static_cast<size_t>(s + u) * RB + cg * CPL * TB, vv);
-#pragma unroll
-            for (int e = 0; e < CPL; ++e) acc[e] += pw[u] * vv[e];
+    const int sph = nsp / NH;
+    float4_t o = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (kBf16) {
+        const uint16_t* prow_l = reinterpret_cast<const uint16_t*>(Pb) + t4 * nsp + hh * sph;
+        const uint16_t* vrow_l = reinterpret_cast<const uint16_t*>(Vb) + (4 * cg + t4) * lay.vpitch + hh * sph;
+        for (int st = 0; st < sph; st += 4) {
+            const uint2 pa = *reinterpret_cast<const uint2*>(prow_l + st);
+            const uint2 vb = *reinterpret_cast<const uint2*>(vrow_l + st);
+            short4_t av, bv;
+            av[0] = static_cast<short>(pa.x); av[1] = static_cast<short>(pa.x >> 16);
+            av[2] = static_cast<short>(pa.y); av[3] = static_cast<short>(pa.y >> 16);
+            bv[0] = static_cast<short>(vb.x); bv[1] = static_cast<short>(vb.x >> 16);
+            bv[2] = static_cast<short>(vb.y); bv[3] = static_cast<short>(vb.y >> 16);
+            o = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(av, bv, o, 0, 0, 0);
         }
-    }
-    const float my_inv = pq == 0 ? inv_sum[0] : pq == 1 ? inv_sum[1] : pq == 2 ? inv_sum[2] : inv_sum[3];
-#pragma unroll
-    for (int e = 0; e < CPL; ++e) acc[e] *= my_inv;
-
-    // ---- 7. outputs ----
-    const int qy = 2 * Py + (pq >> 1), qx = 2 * Px + (pq & 1);
-    if (qy >= H || qx >= W) return;
-    const size_t qtok = static_cast<size_t>(b) * N + qy * W + qx;
-    if constexpr (!FINEST) {
-        float* m = a.msg + (qtok * a.heads + h) * D + cg * CPL;
-        if constexpr (CPL == 2) *reinterpret_cast<float2*>(m) = make_float2(acc[0], acc[1]);
-        else *reinterpret_cast<float4*>(m) = make_float4(acc[0], acc[1], acc[2], acc[3]);
     } else {
-        const int L = a.levels;
-        const float* wrow = a.w ? a.w + (qtok * a.heads + h) * L : nullptr;
-        const float wdef = 1.0f / L;
-        float o[CPL];
-        const float w0 = VA ? 1.0f : (wrow ? wrow[0] : wdef);
+        const float* prow_l = reinterpret_cast<const float*>(Pb) + t4 * nsp + hh * sph;
+        const float* vcol = reinterpret_cast<const float*>(Vb) + 4 * cg + t4;
+        for (int st = 0; st < sph; ++st)
+            o = __builtin_amdgcn_mfma_f32_4x4x1f32(prow_l[st], vcol[(hh * sph + st) * lay.vpitch], o, 0, 0, 0);
+    }
+    if constexpr (NH == 2) {
 #pragma unroll
-        for (int e = 0; e < CPL; ++e) o[e] = w0 * acc[e];
-        for (int lev = 1; lev < L; ++lev) {
-            const size_t anc = static_cast<size_t>(b) * a.lvl_N[lev] + static_cast<size_t>(qy >> lev) * a.lvl_W[lev] +
-                               (qx >> lev);
-            const float* m = a.coarser_msg[lev] + (anc * a.heads + h) * D + cg * CPL;
-            const float wl = VA ? 1.0f : (wrow ? wrow[lev] : wdef);
-            float mv[CPL];
-            if constexpr (CPL == 2) {
-                const float2 t2 = *reinterpret_cast<const float2*>(m);
-                mv[0] = t2.x;
-                mv[1] = t2.y;
+        for (int r = 0; r < 4; ++r) o[r] += xchg_f32<4>(o[r]);
+    }
+
+    // ---- 6. outputs ----
+#pragma unroll
+    for (int u = 0; u < QPL; ++u) {
+        const int qi = (NH == 2 ? hh * QPL : 0) + u;
+        const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
+        if (qy >= H || qx >= W) continue;
+        const float m = pick4(o, qi) * pick4(inv_sum, qi);
+        const size_t qtok = static_cast<size_t>(b) * N + qy * W + qx;
+        if constexpr (!FINEST) {
+            a.msg[(qtok * a.heads + h) * D + ch] = m;
+        } else {
+            const int L = a.levels;
+            const float wdef = 1.0f / L;
+            float out;
+            if (prefetch) {
+                out = (VA ? 1.0f : (a.w ? wq[u][0] : wdef)) * m;
+#pragma unroll
+                for (int lev = 1; lev <= kPre; ++lev) {
+                    if (lev >= L) break;
+                    out += (VA ? 1.0f : (a.w ? wq[u][lev] : wdef)) * anc[lev - 1];
+                }
             } else {
-                const float4 t4 = *reinterpret_cast<const float4*>(m);
-                mv[0] = t4.x;
-                mv[1] = t4.y;
-                mv[2] = t4.z;
-                mv[3] = t4.w;
+                const float* wrow = a.w ? a.w + (qtok * a.heads + h) * L : nullptr;
+                out = (VA ? 1.0f : (wrow ? wrow[0] : wdef)) * m;
+                for (int lev = 1; lev < L; ++lev) {
+                    const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
+                                      static_cast<size_t>(qy >> lev) * a.lvl_W[lev] + (qx >> lev);
+                    const float wl = VA ? 1.0f : (wrow ? wrow[lev] : wdef);
+                    out += wl * a.coarser_msg[lev][(an * a.heads + h) * D + ch];
+                }
             }
-#pragma unroll
-            for (int e = 0; e < CPL; ++e) o[e] += wl * mv[e];
+            S::store1(a.out, qtok * C + h * D + ch, out);
         }
-        store_vals<T, CPL>(a.out, qtok * C + h * D + cg * CPL, o);
     }
 }
 
-template <typename T, int D, bool VA, bool FINEST, int NT>
+template <typename T, int D, bool VA, bool FINEST>
 hipError_t launch_one(const FineArgs& a, hipStream_t stream)
 {
-    const int nslot = 4 * a.K;
-    const size_t wave_bytes = fine_wave_bytes(nslot, D, sizeof(T));
-    const size_t kLdsMax = device_max_lds();
-    int wpb = 4;
-    while (wpb > 1 && wpb * wave_bytes > kLdsMax) --wpb;
-    if (wave_bytes > kLdsMax) return hipErrorInvalidValue;
+    const int nsp = (4 * a.K + 15) & ~15;
+    const size_t wave_bytes = wave_lds<T, D>(nsp).total;
+    const int wpb = 4;
+    if (wpb * wave_bytes > device_max_lds()) return hipErrorInvalidValue;
     static bool configured = false;
     if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, VA, FINEST, NT>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kLdsMax));
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, VA, FINEST>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           static_cast<int>(device_max_lds()));
         if (e != hipSuccess) return e;
         configured = true;
     }
     const long long items = static_cast<long long>(a.B) * a.heads * a.Hp * a.Wp;
     const long long blocks = (items + wpb - 1) / wpb;
     if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((fine_attn_kernel<T, D, VA, FINEST, NT>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(wpb * kWave), wpb * wave_bytes, stream, a);
+    hipLaunchKernelGGL((fine_attn_kernel<T, D, VA, FINEST>), dim3(static_cast<unsigned>(blocks)), dim3(wpb * kWave),
+                       wpb * wave_bytes, stream, a);
     return hipGetLastError();
-}
-
-template <typename T, int D, bool VA, bool FINEST>
-hipError_t launch_nt(const FineArgs& a, hipStream_t stream)
-{
-    const int nslot = 4 * a.K;
-    if (nslot <= 64) return launch_one<T, D, VA, FINEST, 1>(a, stream);
-    if (nslot <= 128) return launch_one<T, D, VA, FINEST, 2>(a, stream);
-    if (nslot <= 256) return launch_one<T, D, VA, FINEST, 4>(a, stream);
-    return hipErrorInvalidValue;
 }
 
 template <typename T, int D>
 hipError_t launch_td(const FineArgs& a, bool variant_a, bool finest, hipStream_t stream)
 {
-    if (variant_a) return finest ? launch_nt<T, D, true, true>(a, stream) : launch_nt<T, D, true, false>(a, stream);
-    return finest ? launch_nt<T, D, false, true>(a, stream) : launch_nt<T, D, false, false>(a, stream);
+    if (variant_a) return finest ? launch_one<T, D, true, true>(a, stream) : launch_one<T, D, true, false>(a, stream);
+    return finest ? launch_one<T, D, false, true>(a, stream) : launch_one<T, D, false, false>(a, stream);
 }
 
 }  // namespace
 
 hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool bf16_in, bool finest, hipStream_t stream)
 {
+    if (4 * a.K > kMaxSlots) return launch_fine_attn_wide(a, d, variant_a, bf16_in, finest, stream);
     if (bf16_in) {
         if (d == 32) return launch_td<bf16, 32>(a, variant_a, finest, stream);
         if (d == 64) return launch_td<bf16, 64>(a, variant_a, finest, stream);

@@ -3,9 +3,10 @@
 // One pass produces up to two coarser levels from a source level. A thread owns one 16-byte
 // channel chunk of one token of the top level it produces: it reads that token's (up to) 4x4
 // source tokens with 16-byte loads (consecutive threads take consecutive chunks of a token, so a
-// wave reads whole NHWC rows), writes the (up to) four intermediate tokens, then pools those
-// rounded values again for the top token. Two levels per pass read each map once and keep about
-// 4*B*N_top*C/chunk threads in flight; deeper pyramids take more passes.
+// wave reads whole rows), writes the (up to) four intermediate tokens, then pools those rounded
+// values again for the top token. Two levels per pass read each map once; deeper pyramids take
+// more passes. Each level is written NHWC or parent-blocked as asked, and the first pass can also
+// write a blocked copy of the input level (every input chunk is read by exactly one thread).
 //
 // Arithmetic, fixed so that every implementation stores the same bits: the valid children are
 // summed in fp32 as ((c00 + c01) + (c10 + c11)) with missing children left out, multiplied by
@@ -46,6 +47,7 @@ __global__ __launch_bounds__(256) void pyramid_pass_kernel(PyramidPassArgs a)
     const char* __restrict__ src = static_cast<const char*>(a.src[tensor]);
     char* __restrict__ dst1 = static_cast<char*>(a.dst1[tensor]);
     char* __restrict__ dst2 = static_cast<char*>(a.dst2[tensor]);
+    char* __restrict__ copy = static_cast<char*>(a.copy[tensor]);
     const int chunks = a.chunks;                       // 16-byte chunks per token
     const int Ht = NLEV == 2 ? a.H2 : a.H1;
     const int Wt = NLEV == 2 ? a.W2 : a.W1;
@@ -58,16 +60,16 @@ __global__ __launch_bounds__(256) void pyramid_pass_kernel(PyramidPassArgs a)
     tok /= Wt;
     const int Y = static_cast<int>(tok % Ht);
     const int b = static_cast<int>(tok / Ht);
-    const size_t row_bytes = static_cast<size_t>(chunks) * 16;
 
+    // load one source chunk; the blocked copy of the source (when asked for) is written on the way
     auto load = [&](int y, int x, float (&o)[E]) {
         const uint4 c = *reinterpret_cast<const uint4*>(
-            src + ((static_cast<size_t>(b) * a.Hs + y) * a.Ws + x) * row_bytes + static_cast<size_t>(ch) * 16);
+            src + chunk_offset(a.src_blocked, b, y, x, a.Hs, a.Ws, ch, chunks, a.head_chunks));
+        if (copy) *reinterpret_cast<uint4*>(copy + chunk_offset(true, b, y, x, a.Hs, a.Ws, ch, chunks, a.head_chunks)) = c;
         S::unpack(c, o);
     };
-    auto store = [&](char* base, int H, int W, int y, int x, const float (&v)[E]) {
-        *reinterpret_cast<uint4*>(base + ((static_cast<size_t>(b) * H + y) * W + x) * row_bytes +
-                                  static_cast<size_t>(ch) * 16) = S::pack(v);
+    auto store = [&](char* base, bool blocked, int H, int W, int y, int x, const float (&v)[E]) {
+        *reinterpret_cast<uint4*>(base + chunk_offset(blocked, b, y, x, H, W, ch, chunks, a.head_chunks)) = S::pack(v);
     };
 
     if constexpr (NLEV == 1) {
@@ -80,7 +82,7 @@ __global__ __launch_bounds__(256) void pyramid_pass_kernel(PyramidPassArgs a)
         pool_children<E>(c00, c01, c10, c11, right, below, o);
 #pragma unroll
         for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
-        store(dst1, a.H1, a.W1, Y, X, o);
+        store(dst1, a.dst1_blocked, a.H1, a.W1, Y, X, o);
     } else {
         // the four level-1 children of (Y, X), each pooled from its own source children
         float mid[4][E];
@@ -103,13 +105,13 @@ __global__ __launch_bounds__(256) void pyramid_pass_kernel(PyramidPassArgs a)
             pool_children<E>(c00, c01, c10, c11, right, below, mid[q]);
 #pragma unroll
             for (int e = 0; e < E; ++e) mid[q][e] = S::round(mid[q][e]);
-            store(dst1, a.H1, a.W1, y1, x1, mid[q]);
+            store(dst1, a.dst1_blocked, a.H1, a.W1, y1, x1, mid[q]);
         }
         float o[E];
         pool_children<E>(mid[0], mid[1], mid[2], mid[3], mid_ok[1], mid_ok[2], o);
 #pragma unroll
         for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
-        store(dst2, a.H2, a.W2, Y, X, o);
+        store(dst2, a.dst2_blocked, a.H2, a.W2, Y, X, o);
     }
 }
 

@@ -50,6 +50,9 @@ qta_status check_problem(int B, int heads, int d, int K, qta_variant variant, qt
     return QTA_OK;
 }
 
+// Gathered levels are stored parent-blocked when the fine kernels take the blocked path (4K <= 64).
+bool use_blocked(int K, int levels) { return levels > 1 && 4 * K <= 64; }
+
 qta_status layout(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype, qta_workspace_layout* L)
 {
     qta_status st = check_problem(B, heads, d, K, QTA_VARIANT_B, dtype);
@@ -60,15 +63,25 @@ qta_status layout(int B, int heads, int H, int W, int d, int levels, int K, qta_
     if (static_cast<long long>(Hl[levels - 1]) * Wl[levels - 1] > QTA_MAX_COARSE) return QTA_ERR_UNSUPPORTED;
     *L = qta_workspace_layout{};
     L->levels = levels;
-    const size_t C = static_cast<size_t>(heads) * d;
+    const int C = heads * d;
+    const int tb = static_cast<int>(dtype_bytes(dtype));
+    const bool blk = use_blocked(K, levels);
     size_t off = 0;
     for (int l = 0; l < levels; ++l) {
         L->H[l] = Hl[l];
         L->W[l] = Wl[l];
+        L->blocked[l] = (blk && l <= levels - 2) ? 1 : 0;
+    }
+    if (blk) {
+        const size_t b0 = level_bytes(true, B, Hl[0], Wl[0], C, tb);
+        L->k0_blocked = off;
+        off = align_up(off + b0);
+        L->v0_blocked = off;
+        off = align_up(off + b0);
     }
     for (int l = 1; l < levels; ++l) {
         const size_t N = static_cast<size_t>(Hl[l]) * Wl[l];
-        const size_t tok = static_cast<size_t>(B) * N * C * dtype_bytes(dtype);
+        const size_t tok = level_bytes(L->blocked[l] != 0, B, Hl[l], Wl[l], C, tb);
         L->q[l] = off;
         off = align_up(off + tok);
         L->k[l] = off;
@@ -90,9 +103,12 @@ float resolve_scale(float scale, int d) { return scale > 0.f ? scale : 1.0f / __
 
 qta_status launch_status(hipError_t e) { return e == hipSuccess ? QTA_OK : QTA_ERR_HIP; }
 
-// Pyramid passes: from level s produce s+1 and, when it exists, s+2; repeat from s+2.
-hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], int ntensors, int B, const int* Hl,
-                       const int* Wl, int levels, int chunks, bool use_bf16, hipStream_t stream)
+// Pyramid passes: from level s produce s+1 and, when it exists, s+2; repeat from s+2. `blocked`
+// gives the storage of each level (level 0, the input, is NHWC); copy0[t], when not NULL, receives
+// a blocked copy of tensor t's input level during the first pass.
+hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], void* const* copy0, int ntensors, int B,
+                       const int* Hl, const int* Wl, const int* blocked, int levels, int chunks, int head_chunks,
+                       bool use_bf16, hipStream_t stream)
 {
     for (int s = 0; s + 1 < levels; s += 2) {
         const int nlev = (s + 2 < levels) ? 2 : 1;
@@ -101,6 +117,7 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], in
             a.src[t] = s == 0 ? src0[t] : lvl[t][s];
             a.dst1[t] = lvl[t][s + 1];
             a.dst2[t] = nlev == 2 ? lvl[t][s + 2] : nullptr;
+            a.copy[t] = (s == 0 && copy0) ? copy0[t] : nullptr;
         }
         a.B = B;
         a.Hs = Hl[s];
@@ -110,6 +127,10 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], in
         a.H2 = nlev == 2 ? Hl[s + 2] : 0;
         a.W2 = nlev == 2 ? Wl[s + 2] : 0;
         a.chunks = chunks;
+        a.head_chunks = head_chunks;
+        a.src_blocked = s > 0 && blocked[s];
+        a.dst1_blocked = blocked[s + 1] != 0;
+        a.dst2_blocked = nlev == 2 && blocked[s + 2] != 0;
         hipError_t e = launch_pyramid_pass(a, nlev, ntensors, use_bf16, stream);
         if (e != hipSuccess) return e;
     }
@@ -170,8 +191,9 @@ qta_status qta_build_pyramid(const void* x, void* levels_out, int B, int H, int 
     }
     const void* src[1] = {x};
     const int chunks = static_cast<int>(static_cast<size_t>(C) * dtype_bytes(dtype) / 16);
-    return launch_status(run_pyramid(src, lvl, 1, B, Hl, Wl, levels, chunks, dtype == QTA_BF16,
-                                     static_cast<hipStream_t>(stream)));
+    const int nhwc[QTA_MAX_LEVELS] = {};
+    return launch_status(run_pyramid(src, lvl, nullptr, 1, B, Hl, Wl, nhwc, levels, chunks, chunks,
+                                     dtype == QTA_BF16, static_cast<hipStream_t>(stream)));
 }
 
 qta_status qta_coarse_attn(const void* qc, const void* kc, const void* vc, int B, int heads, int Hc, int Wc, int d,
@@ -324,11 +346,17 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
     auto sidx = [&](int l) { return reinterpret_cast<int32_t*>(ws + L.sel_idx[l]); };
     auto skey = [&](int l) { return reinterpret_cast<float*>(ws + L.sel_key[l]); };
 
-    // 1. pyramids of q, k and v
+    // 1. pyramids of q, k and v (gathered levels blocked; blocked copies of the input k and v)
+    const bool blk = L.blocked[0] != 0;
+    void* k0b = blk ? ws + L.k0_blocked : nullptr;
+    void* v0b = blk ? ws + L.v0_blocked : nullptr;
     if (levels > 1) {
         const void* src[3] = {q, k, v};
+        void* copy0[3] = {nullptr, k0b, v0b};
         const int chunks = static_cast<int>(static_cast<size_t>(C) * dtype_bytes(dtype) / 16);
-        hipError_t e = run_pyramid(src, pyr, 3, B, L.H, L.W, levels, chunks, use_bf16, s);
+        const int head_chunks = static_cast<int>(static_cast<size_t>(d) * dtype_bytes(dtype) / 16);
+        hipError_t e = run_pyramid(src, pyr, blk ? copy0 : nullptr, 3, B, L.H, L.W, L.blocked, levels, chunks,
+                                   head_chunks, use_bf16, s);
         if (e != hipSuccess) return QTA_ERR_HIP;
     }
 
@@ -366,6 +394,8 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
         a.q = lv[0][l];
         a.k = lv[1][l];
         a.v = lv[2][l];
+        a.q_blocked = L.blocked[l] != 0;
+        a.kv_blocked = L.blocked[l] != 0;
         a.B = B;
         a.heads = heads;
         a.H = L.H[l];
@@ -388,8 +418,10 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
     {
         FineArgs a{};
         a.q = q;
-        a.k = k;
-        a.v = v;
+        a.k = blk ? k0b : k;
+        a.v = blk ? v0b : v;
+        a.q_blocked = false;
+        a.kv_blocked = blk;
         a.B = B;
         a.heads = heads;
         a.H = H;

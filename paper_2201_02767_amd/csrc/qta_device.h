@@ -111,6 +111,88 @@ __device__ __forceinline__ void wave_lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
+// ---- register-only exchanges (DPP and permlane swaps; no LDS round trip) ----
+
+// DPP controls used below.
+constexpr int kDppXor1 = 0xB1;         // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;         // quad_perm [2,3,0,1]
+constexpr int kDppRowShl4 = 0x104;
+constexpr int kDppRowShr4 = 0x114;
+constexpr int kDppRowRor8 = 0x128;     // within a 16-lane row: lane ^ 8
+constexpr int kDppRowMirror = 0x140;   // within a row: lane -> 15 - lane
+constexpr int kDppRowHalfMirror = 0x141;  // within 8 lanes: lane -> 7 - lane
+
+// The value held by lane (lane ^ M), M a power of two below 64.
+template <int M>
+__device__ __forceinline__ uint32_t xchg_u32(uint32_t x)
+{
+    if constexpr (M == 1) {
+        return __builtin_amdgcn_update_dpp(0u, x, kDppXor1, 0xF, 0xF, false);
+    } else if constexpr (M == 2) {
+        return __builtin_amdgcn_update_dpp(0u, x, kDppXor2, 0xF, 0xF, false);
+    } else if constexpr (M == 4) {
+        // banks 1 and 3 of each row read four lanes down, banks 0 and 2 four lanes up
+        const uint32_t t = __builtin_amdgcn_update_dpp(x, x, kDppRowShr4, 0xF, 0xA, false);
+        return __builtin_amdgcn_update_dpp(t, x, kDppRowShl4, 0xF, 0x5, false);
+    } else if constexpr (M == 8) {
+        return __builtin_amdgcn_update_dpp(0u, x, kDppRowRor8, 0xF, 0xF, false);
+    } else if constexpr (M == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        return (threadIdx.x & 16) ? r[0] : r[1];
+    } else {
+        static_assert(M == 32, "exchange distance");
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return (threadIdx.x & 32) ? r[0] : r[1];
+    }
+}
+
+template <int M>
+__device__ __forceinline__ float xchg_f32(float x) { return __uint_as_float(xchg_u32<M>(__float_as_uint(x))); }
+
+// Butterfly all-reduce over the 64 lanes (every lane ends with the same value).
+template <typename Op>
+__device__ __forceinline__ float wave_allreduce(float x, Op op)
+{
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppXor1, 0xF, 0xF, false)));
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppXor2, 0xF, 0xF, false)));
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppRowHalfMirror, 0xF, 0xF, false)));
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppRowMirror, 0xF, 0xF, false)));
+    const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = op(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+    const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return op(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+}
+
+__device__ __forceinline__ float wave_max_fast(float x)
+{
+    return wave_allreduce(x, [](float a, float b) { return fmaxf(a, b); });
+}
+
+__device__ __forceinline__ float wave_sum_fast(float x)
+{
+    return wave_allreduce(x, [](float a, float b) { return a + b; });
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x)
+{
+    auto mn = [](uint32_t a, uint32_t b) { return a < b ? a : b; };
+    x = mn(x, __builtin_amdgcn_update_dpp(0u, x, kDppXor1, 0xF, 0xF, false));
+    x = mn(x, __builtin_amdgcn_update_dpp(0u, x, kDppXor2, 0xF, 0xF, false));
+    x = mn(x, __builtin_amdgcn_update_dpp(0u, x, kDppRowHalfMirror, 0xF, 0xF, false));
+    x = mn(x, __builtin_amdgcn_update_dpp(0u, x, kDppRowMirror, 0xF, 0xF, false));
+    const auto r16 = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    x = mn(r16[0], r16[1]);
+    const auto r32 = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return mn(r32[0], r32[1]);
+}
+
+// Number of set bits of `mask` below this lane.
+__device__ __forceinline__ int lanes_below(uint64_t mask)
+{
+    return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+
 __device__ __forceinline__ float wave_max(float x)
 {
 #pragma unroll
@@ -173,6 +255,63 @@ __device__ __forceinline__ int32_t rank_word_index(uint64_t w)
 }
 
 __device__ __forceinline__ float rank_word_score(uint64_t w) { return from_ordered_bits(static_cast<uint32_t>(w >> 32)); }
+
+// Exact top-`keff` selection over NPER candidates per lane, held as 32-bit ranking keys (larger is
+// better, 0 = not a candidate) with distinct 32-bit names. Returns, per candidate, whether it is
+// kept: every key above the cut, and at the cut the lowest names first. The cut (the keff-th
+// largest key) is built bit by bit from the top with wave ballots; the search stops as soon as the
+// keys at or above the partial cut number exactly keff, which for distinct scores happens after
+// about log2(candidates) bits. No sorting and no LDS traffic. Requires 1 <= keff <= number of
+// candidates.
+template <int NPER>
+__device__ __forceinline__ void wave_select_top(const uint32_t (&key)[NPER], const uint32_t (&name)[NPER], int keff,
+                                                bool (&kept)[NPER])
+{
+    uint32_t cut = 0;
+    bool exact = false;
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t c = cut | (1u << bit);
+        int cnt = 0;
+#pragma unroll
+        for (int e = 0; e < NPER; ++e) cnt += __popcll(__ballot(key[e] >= c));
+        if (cnt >= keff) {
+            cut = c;
+            if (cnt == keff) {
+                exact = true;
+                break;
+            }
+        }
+    }
+    if (exact) {
+#pragma unroll
+        for (int e = 0; e < NPER; ++e) kept[e] = key[e] >= cut;
+        return;
+    }
+    // the cut is the keff-th largest key and more than one candidate sits on it
+    int above = 0;
+#pragma unroll
+    for (int e = 0; e < NPER; ++e) {
+        above += __popcll(__ballot(key[e] > cut));
+        kept[e] = key[e] > cut;
+    }
+    const int need = keff - above;                   // places left for candidates at the cut
+    bool open[NPER];
+#pragma unroll
+    for (int e = 0; e < NPER; ++e) open[e] = key[e] == cut;
+    for (int r = 0; r < need; ++r) {
+        uint32_t mine = 0xFFFFFFFFu;
+#pragma unroll
+        for (int e = 0; e < NPER; ++e)
+            if (open[e] && name[e] < mine) mine = name[e];
+        const uint32_t low = wave_min_u32(mine);
+#pragma unroll
+        for (int e = 0; e < NPER; ++e)
+            if (open[e] && name[e] == low) {
+                open[e] = false;
+                kept[e] = true;
+            }
+    }
+}
 
 // Bitonic sort, descending, of NT*64 words held as word[t] in lane l at position t*64 + l.
 template <int NT>

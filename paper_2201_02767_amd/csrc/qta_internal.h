@@ -8,14 +8,48 @@
 
 namespace qta {
 
+// Storage of one pyramid level (and of the inputs) in HBM:
+//  - NHWC:    [B][H][W][heads][d], one token's heads contiguous;
+//  - blocked: [B][heads][ceil(H/2)][ceil(W/2)][2][2][d], the 2x2 children of one parent position
+//             of one head contiguous (4*d elements; off-map children are unused padding).
+// qta_forward keeps every level that is gathered (all but the coarsest) blocked, so a kept key's
+// four children are one contiguous run of 4*d*sizeof(dtype) bytes.
+struct LevelLayout {
+    bool blocked;
+};
+
+// Byte offset of the 16-byte chunk `ch` (0 <= ch < C*sizeof(dtype)/16) of token (y, x) in a level
+// of H x W tokens; `cpt` chunks per token, `cph` chunks per head row.
+__host__ __device__ inline size_t chunk_offset(bool blocked, int b, int y, int x, int H, int W, int ch, int cpt,
+                                               int cph)
+{
+    if (!blocked) return ((static_cast<size_t>(b) * H + y) * W + x) * cpt * 16 + static_cast<size_t>(ch) * 16;
+    const int heads = cpt / cph;
+    const int h = ch / cph, c2 = ch - h * cph;
+    const int Hp = (H + 1) / 2, Wp = (W + 1) / 2;
+    const size_t blk = ((static_cast<size_t>(b) * heads + h) * Hp + (y >> 1)) * Wp + (x >> 1);
+    const int child = (y & 1) * 2 + (x & 1);
+    return ((blk * 4 + child) * cph + c2) * 16;
+}
+
+// Bytes of one level of B x H x W tokens with C*tb bytes each.
+inline size_t level_bytes(bool blocked, int B, int H, int W, int C, int tb)
+{
+    if (!blocked) return static_cast<size_t>(B) * H * W * C * tb;
+    return static_cast<size_t>(B) * ((H + 1) / 2) * ((W + 1) / 2) * 4 * C * tb;
+}
+
 // One pyramid pass over up to three token maps (q, k, v): from a source level produce one or two
-// coarser levels.
+// coarser levels. Optionally also copies the source (level 0) into the blocked layout.
 struct PyramidPassArgs {
     const void* src[3];
     void* dst1[3];
     void* dst2[3];
+    void* copy[3];              // blocked copy of the source level, or NULL
     int B, Hs, Ws, H1, W1, H2, W2;
     int chunks;                 // 16-byte chunks per token (C * sizeof(dtype) / 16)
+    int head_chunks;            // 16-byte chunks per head row (d * sizeof(dtype) / 16)
+    bool src_blocked, dst1_blocked, dst2_blocked;
 };
 
 struct CoarseArgs {
@@ -37,6 +71,8 @@ struct FineArgs {
     const void* q;
     const void* k;
     const void* v;
+    bool q_blocked;             // queries of this level stored blocked (else NHWC)
+    bool kv_blocked;            // keys and values of this level stored blocked (else NHWC)
     int B, heads, H, W, Hp, Wp, C, K;
     float scale;
     const int32_t* parent_idx;
@@ -80,6 +116,8 @@ inline size_t device_max_lds()
 hipError_t launch_pyramid_pass(const PyramidPassArgs& a, int nlev, int ntensors, bool use_bf16, hipStream_t stream);
 hipError_t launch_coarse_attn(const CoarseArgs& a, int d, bool variant_a, bool use_bf16, hipStream_t stream);
 hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest, hipStream_t stream);
+hipError_t launch_fine_attn_wide(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
+                                 hipStream_t stream);
 hipError_t launch_topk(const TopkArgs& a, hipStream_t stream);
 
 }  // namespace qta

@@ -32,12 +32,15 @@ class WorkspaceLayout(ctypes.Structure):
         ("levels", ctypes.c_int),
         ("H", ctypes.c_int * MAX_LEVELS),
         ("W", ctypes.c_int * MAX_LEVELS),
+        ("blocked", ctypes.c_int * MAX_LEVELS),
         ("q", ctypes.c_size_t * MAX_LEVELS),
         ("k", ctypes.c_size_t * MAX_LEVELS),
         ("v", ctypes.c_size_t * MAX_LEVELS),
         ("msg", ctypes.c_size_t * MAX_LEVELS),
         ("sel_idx", ctypes.c_size_t * MAX_LEVELS),
         ("sel_key", ctypes.c_size_t * MAX_LEVELS),
+        ("k0_blocked", ctypes.c_size_t),
+        ("v0_blocked", ctypes.c_size_t),
         ("total", ctypes.c_size_t),
     ]
 
@@ -219,9 +222,27 @@ class Plan:
         return self.workspace[off:off + nbytes].view(dtype).view(shape)
 
     def pyramid(self, which: str, level: int):
+        """Pyramid level `level` (>= 1) of q, k or v as [B, H_l, W_l, heads, d]; blocked storage is
+        unpacked into a new tensor."""
         lay = self.layout
         off = getattr(lay, which)[level]
-        return self._view(off, (self.B, lay.H[level], lay.W[level], self.heads, self.d), self.dtype)
+        H, W = lay.H[level], lay.W[level]
+        if not lay.blocked[level]:
+            return self._view(off, (self.B, H, W, self.heads, self.d), self.dtype)
+        return self._unblock(off, H, W)
+
+    def blocked_input(self, which: str):
+        """The blocked copy of the input k or v that the finest level gathers from."""
+        lay = self.layout
+        if not lay.blocked[0]:
+            raise ValueError("this problem keeps its inputs NHWC")
+        return self._unblock(getattr(lay, which + "0_blocked"), self.H, self.W)
+
+    def _unblock(self, off, H, W):
+        Hp, Wp = (H + 1) // 2, (W + 1) // 2
+        t = self._view(off, (self.B, self.heads, Hp, Wp, 2, 2, self.d), self.dtype)
+        t = t.permute(0, 2, 4, 3, 5, 1, 6).reshape(self.B, 2 * Hp, 2 * Wp, self.heads, self.d)
+        return t[:, :H, :W].contiguous()
 
     def message(self, level: int):
         lay = self.layout

@@ -56,19 +56,31 @@ def test_level_dims_rejects_levels_above_a_single_token():
         P.level_dims(0, 4, 1)
 
 
-def test_workspace_layout_is_aligned_and_disjoint():
-    lay = P.workspace_layout(2, 2, 200, 336, 32, 5, 16, torch.bfloat16)
+def _tok_bytes(blocked, B, H, W, C, tb):
+    if blocked:
+        return B * ((H + 1) // 2) * ((W + 1) // 2) * 4 * C * tb
+    return B * H * W * C * tb
+
+
+@pytest.mark.parametrize("K,expect_blocked", [(16, True), (20, False)])
+def test_workspace_layout_is_aligned_and_disjoint(K, expect_blocked):
+    lay = P.workspace_layout(2, 2, 200, 336, 32, 5, K, torch.bfloat16)
     regions = []
+    assert bool(lay.blocked[0]) == expect_blocked
+    if expect_blocked:
+        b0 = _tok_bytes(True, 2, 200, 336, 64, 2)
+        regions += [(lay.k0_blocked, b0), (lay.v0_blocked, b0)]
     for l in range(1, 5):
         N = lay.H[l] * lay.W[l]
-        tok = 2 * N * 64 * 2
+        assert lay.blocked[l] == (1 if expect_blocked and l <= 3 else 0)
+        tok = _tok_bytes(lay.blocked[l], 2, lay.H[l], lay.W[l], 64, 2)
         regions += [(lay.q[l], tok), (lay.k[l], tok), (lay.v[l], tok), (lay.msg[l], 2 * N * 64 * 4),
-                    (lay.sel_idx[l], 2 * 2 * N * 16 * 4), (lay.sel_key[l], 2 * 2 * N * 16 * 4)]
+                    (lay.sel_idx[l], 2 * 2 * N * K * 4), (lay.sel_key[l], 2 * 2 * N * K * 4)]
     regions.sort()
     for (o1, n1), (o2, _) in zip(regions, regions[1:]):
         assert o1 % 256 == 0 and o1 + n1 <= o2
     assert regions[-1][0] + regions[-1][1] <= lay.total
-    assert P.workspace_bytes(2, 2, 200, 336, 32, 5, 16, torch.bfloat16) == lay.total
+    assert P.workspace_bytes(2, 2, 200, 336, 32, 5, K, torch.bfloat16) == lay.total
 
 
 def test_workspace_bytes_zero_on_bad_shapes():
