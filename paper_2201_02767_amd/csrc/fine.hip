@@ -70,7 +70,7 @@ __device__ __forceinline__ float pick4(const float (&v)[4], int i)
     return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
 }
 
-template <typename T, int D, bool VA, bool FINEST>
+template <typename T, int D, int NSP, bool VA, bool FINEST>
 __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
 {
     using S = Storage<T>;
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     const int H = a.H, W = a.W, C = a.C, K = a.K;
     const int N = H * W;
     const int nslot = 4 * K;
-    const int nsp = (nslot + 15) & ~15;
+    const int nsp = (nslot + 15) & ~15;                // <= NSP
 
     extern __shared__ __align__(16) unsigned char smem[];
     const WaveLds lay = wave_lds<T, D>(nsp);
@@ -111,25 +111,88 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     unsigned char* Pb = base + lay.p;
 
     const size_t prow = ((static_cast<size_t>(b) * a.heads + h) * Np + P) * K;
-    auto child_of_slot = [&](int s) -> int {           // flat index at level l, or -1
-        if (s >= nslot) return -1;
-        const int J = a.parent_idx[prow + (s >> 2)];
-        if (J < 0) return -1;
+    // flat index at level l of child (s & 3) of kept key J (a level l+1 index), or -1
+    auto child_of_slot_J = [&](int J, int s) -> int {
+        if (s >= nslot || J < 0) return -1;
         const int Jy = J / a.Wp, Jx = J - Jy * a.Wp;
         const int cy = 2 * Jy + ((s >> 1) & 1), cx = 2 * Jx + (s & 1);
         return (cy < H && cx < W) ? cy * W + cx : -1;
     };
 
-    // ---- 1. this lane's slot; gather key/value rows and the four queries into LDS ----
-    const int flat = child_of_slot(lane);
-    const bool ok = flat >= 0;
+    // ---- 1. loads. Vector memory counters drain in order, and a load inside a divergent branch
+    //      makes the compiler wait for it at the join, so every load below is unconditional, at a
+    //      clamped address that is always in bounds, with validity applied when the value is used.
+    //      Phase A holds every load that needs no other load; phase B the gathers. ----
+    const int sub = lane / LPR, chunk = lane % LPR;
+    constexpr int kRounds = (NSP + RPP - 1) / RPP;     // gather instructions per tensor (upper bound)
+    // phase A: the parents' kept keys (own slot and gather slots), the parents' scores (A), the
+    // query chunk, and at the finest level the ancestors' messages and this lane's level weights
+    const int last_sel = K - 1;
+    const int J_own_raw = a.parent_idx[prow + min(lane >> 2, last_sel)];
+    int J_g[kRounds];
+#pragma unroll
+    for (int u = 0; u < kRounds; ++u) J_g[u] = a.parent_idx[prow + min((u * RPP + sub) >> 2, last_sel)];
     float pkey = 0.f;
-    if constexpr (VA)
-        if (lane < nslot) pkey = a.parent_key[prow + (lane >> 2)];
-
+    if constexpr (VA) pkey = a.parent_key[prow + min(lane >> 2, last_sel)];
+    const int qsub = sub & 3;
+    const int qy = 2 * Py + (qsub >> 1), qx = 2 * Px + (qsub & 1);
+    const bool q_ok = sub < 4 && qy < H && qx < W;
+    uint4 qraw;
+    {
+        const int qyc = qy < H ? qy : H - 1, qxc = qx < W ? qx : W - 1;
+        const size_t qoff = a.q_blocked ? (((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 + qsub) * RB
+                                        : ((static_cast<size_t>(b) * N + qyc * W + qxc) * C + h * D) * TB;
+        qraw = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.q) + qoff + chunk * 16);
+    }
+    // phase B: the gathers. NHWC: child f of this head at kg + f*C*TB. Blocked: the four children
+    // of kept key J are the 4*RB bytes at kg + J*4*RB (this (batch, head)'s blocks start at kg).
+    const bool kvb = a.kv_blocked;
+    const size_t kv_base = kvb ? (static_cast<size_t>(b) * a.heads + h) * Np * 4 * RB
+                               : (static_cast<size_t>(b) * N * C + h * D) * TB;
+    const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base + chunk * 16;
+    const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base + chunk * 16;
+    const size_t tok_bytes = static_cast<size_t>(C) * TB;
+    // at most kBatch rounds of gathered rows are held in registers at a time
+    constexpr int kBatch = kRounds < 8 ? kRounds : 8;
+    bool gok[kRounds];
+    uint4 kc[kBatch], vc[kBatch];
+    auto load_batch = [&](int u0) {
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            const int u = u0 + i, s = u * RPP + sub;
+            if (u >= kRounds || u * RPP >= nsp) break;        // uniform
+            const int f = child_of_slot_J(J_g[u], s);
+            gok[u] = f >= 0;
+            const size_t goff = !gok[u] ? 0 : (kvb ? (static_cast<size_t>(J_g[u]) * 4 + (s & 3)) * RB : f * tok_bytes);
+            kc[i] = *reinterpret_cast<const uint4*>(kg + goff);
+            vc[i] = *reinterpret_cast<const uint4*>(vg + goff);
+        }
+    };
+    auto store_batch = [&](int u0) {
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            const int u = u0 + i, s = u * RPP + sub;
+            if (u >= kRounds || u * RPP >= nsp) break;        // uniform
+            const uint4 zero = make_uint4(0, 0, 0, 0);
+            const uint4 kk = gok[u] ? kc[i] : zero;
+            const uint4 vv = gok[u] ? vc[i] : zero;
+            *reinterpret_cast<uint4*>(Ks + s * KP + chunk * 16) = kk;
+            if constexpr (kBf16) {
+                uint16_t* vt = reinterpret_cast<uint16_t*>(Vb);
+                const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t bits = (e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xFFFFu);
+                    vt[(chunk * E + e) * lay.vpitch + s] = static_cast<uint16_t>(bits);
+                }
+            } else {
+                *reinterpret_cast<uint4*>(Vb + (s * lay.vpitch + chunk * E) * 4) = vv;
+            }
+        }
+    };
+    load_batch(0);
     // Output ownership (step 6): lane 4*blk + t4 with blk = cg*NH + hh owns channel 4*cg + t4 of
-    // queries hh*QPL .. hh*QPL + QPL-1. At the finest level the ancestors' messages and the level
-    // weights of those queries are loaded here, so their latency overlaps the gather.
+    // queries hh*QPL .. hh*QPL + QPL-1.
     const int blk = lane >> 2, t4 = lane & 3;
     const int cg = blk / NH, hh = blk % NH;
     const int ch = 4 * cg + t4;
@@ -137,89 +200,39 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     float anc[kPre] = {};
     float wq[FINEST ? QPL : 1][kPre + 1] = {};
     const bool prefetch = FINEST && a.levels <= kPre + 1;
+    // phase C (after the gathers are in flight): the finest level's combination inputs
     if constexpr (FINEST) {
-        if (prefetch) {
-            const int qy0 = 2 * Py, qx0 = 2 * Px;                // ancestors are shared by the siblings
+        if (prefetch) {                                      // uniform
+            const int L = a.levels;
 #pragma unroll
             for (int lev = 1; lev <= kPre; ++lev) {
-                if (lev >= a.levels) break;
-                const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
-                                  static_cast<size_t>(qy0 >> lev) * a.lvl_W[lev] + (qx0 >> lev);
-                anc[lev - 1] = a.coarser_msg[lev][(an * a.heads + h) * D + ch];
+                const int lv = lev < L ? lev : L - 1;        // >= 1: the finest level has L >= 2
+                const size_t an = static_cast<size_t>(b) * a.lvl_N[lv] +
+                                  static_cast<size_t>((2 * Py) >> lv) * a.lvl_W[lv] + ((2 * Px) >> lv);
+                anc[lev - 1] = a.coarser_msg[lv][(an * a.heads + h) * D + ch];   // ancestors shared by siblings
             }
-            if (!VA && a.w) {
+            if (!VA && a.w) {                                // uniform
 #pragma unroll
                 for (int u = 0; u < QPL; ++u) {
                     const int qi = (NH == 2 ? hh * QPL : 0) + u;
-                    const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
-                    if (qy >= H || qx >= W) continue;
-                    const float* wrow = a.w + ((static_cast<size_t>(b) * N + qy * W + qx) * a.heads + h) * a.levels;
+                    const int wy = min(2 * Py + (qi >> 1), H - 1), wx = min(2 * Px + (qi & 1), W - 1);
+                    const float* wrow = a.w + ((static_cast<size_t>(b) * N + wy * W + wx) * a.heads + h) * L;
 #pragma unroll
-                    for (int lev = 0; lev <= kPre; ++lev)
-                        if (lev < a.levels) wq[u][lev] = wrow[lev];
+                    for (int lev = 0; lev <= kPre; ++lev) wq[u][lev] = wrow[lev < L ? lev : L - 1];
                 }
             }
         }
     }
-    {
-        // NHWC: child f of this head at kg + f*C*TB. Blocked: the four children of kept key J are
-        // the 4*RB bytes at kg + J*4*RB (this (batch, head)'s blocks start at kg).
-        const bool kvb = a.kv_blocked;
-        const size_t kv_base = kvb ? (static_cast<size_t>(b) * a.heads + h) * Np * 4 * RB
-                                   : (static_cast<size_t>(b) * N * C + h * D) * TB;
-        const size_t tok_bytes = static_cast<size_t>(C) * TB;
-        const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base;
-        const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base;
-        const int sub = lane / LPR, chunk = lane % LPR;
-        constexpr int kRounds = kMaxSlots / RPP;           // gather instructions per tensor
-        constexpr int kGroup = kRounds < 4 ? kRounds : 4;  // loads in flight per tensor
-        // the four sibling queries (off-map ones as zeros)
-        if (sub < 4) {
-            const int qy = 2 * Py + (sub >> 1), qx = 2 * Px + (sub & 1);
-            uint4 qc = make_uint4(0, 0, 0, 0);
-            if (qy < H && qx < W) {
-                const size_t qoff = a.q_blocked
-                                        ? (((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 + sub) * RB
-                                        : ((static_cast<size_t>(b) * N + qy * W + qx) * C + h * D) * TB;
-                qc = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.q) + qoff + chunk * 16);
-            }
-            *reinterpret_cast<uint4*>(Qs + sub * RB + chunk * 16) = qc;
-        }
+    const int flat = child_of_slot_J(lane < nslot ? J_own_raw : -1, lane);
+    const bool ok = flat >= 0;
+    // LDS stores: the query (loaded first), then the gathered rows (off-map or missing candidates
+    // as zeros)
+    if (sub < 4) *reinterpret_cast<uint4*>(Qs + sub * RB + chunk * 16) = q_ok ? qraw : make_uint4(0, 0, 0, 0);
+    store_batch(0);
 #pragma unroll
-        for (int g = 0; g < kRounds; g += kGroup) {
-            if (g * RPP >= nsp) break;
-            uint4 kc[kGroup], vc[kGroup];
-#pragma unroll
-            for (int u = 0; u < kGroup; ++u) {
-                const int s = (g + u) * RPP + sub;
-                kc[u] = make_uint4(0, 0, 0, 0);
-                vc[u] = make_uint4(0, 0, 0, 0);
-                const int f = s < nsp ? child_of_slot(s) : -1;
-                if (f >= 0) {
-                    const size_t off = kvb ? (static_cast<size_t>(a.parent_idx[prow + (s >> 2)]) * 4 + (s & 3)) * RB
-                                           : f * tok_bytes;
-                    kc[u] = *reinterpret_cast<const uint4*>(kg + off + chunk * 16);
-                    vc[u] = *reinterpret_cast<const uint4*>(vg + off + chunk * 16);
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < kGroup; ++u) {
-                const int s = (g + u) * RPP + sub;
-                if (s >= nsp) continue;
-                *reinterpret_cast<uint4*>(Ks + s * KP + chunk * 16) = kc[u];
-                if constexpr (kBf16) {
-                    uint16_t* vt = reinterpret_cast<uint16_t*>(Vb);
-                    const uint32_t w4[4] = {vc[u].x, vc[u].y, vc[u].z, vc[u].w};
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const uint32_t bits = (e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xFFFFu);
-                        vt[(chunk * E + e) * lay.vpitch + s] = static_cast<uint16_t>(bits);
-                    }
-                } else {
-                    *reinterpret_cast<uint4*>(Vb + (s * lay.vpitch + chunk * E) * 4) = vc[u];
-                }
-            }
-        }
+    for (int u0 = kBatch; u0 < kRounds; u0 += kBatch) {
+        load_batch(u0);
+        store_batch(u0);
     }
     wave_lds_sync();
 
@@ -383,7 +396,7 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     }
 }
 
-template <typename T, int D, bool VA, bool FINEST>
+template <typename T, int D, int NSP, bool VA, bool FINEST>
 hipError_t launch_one(const FineArgs& a, hipStream_t stream)
 {
     const int nsp = (4 * a.K + 15) & ~15;
@@ -392,7 +405,7 @@ hipError_t launch_one(const FineArgs& a, hipStream_t stream)
     if (wpb * wave_bytes > device_max_lds()) return hipErrorInvalidValue;
     static bool configured = false;
     if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, VA, FINEST>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, NSP, VA, FINEST>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            static_cast<int>(device_max_lds()));
         if (e != hipSuccess) return e;
@@ -401,16 +414,25 @@ hipError_t launch_one(const FineArgs& a, hipStream_t stream)
     const long long items = static_cast<long long>(a.B) * a.heads * a.Hp * a.Wp;
     const long long blocks = (items + wpb - 1) / wpb;
     if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((fine_attn_kernel<T, D, VA, FINEST>), dim3(static_cast<unsigned>(blocks)), dim3(wpb * kWave),
-                       wpb * wave_bytes, stream, a);
+    hipLaunchKernelGGL((fine_attn_kernel<T, D, NSP, VA, FINEST>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(wpb * kWave), wpb * wave_bytes, stream, a);
     return hipGetLastError();
+}
+
+template <typename T, int D, bool VA, bool FINEST>
+hipError_t launch_nsp(const FineArgs& a, hipStream_t stream)
+{
+    const int nslot = 4 * a.K;
+    if (nslot <= 16) return launch_one<T, D, 16, VA, FINEST>(a, stream);
+    if (nslot <= 32) return launch_one<T, D, 32, VA, FINEST>(a, stream);
+    return launch_one<T, D, 64, VA, FINEST>(a, stream);
 }
 
 template <typename T, int D>
 hipError_t launch_td(const FineArgs& a, bool variant_a, bool finest, hipStream_t stream)
 {
-    if (variant_a) return finest ? launch_one<T, D, true, true>(a, stream) : launch_one<T, D, true, false>(a, stream);
-    return finest ? launch_one<T, D, false, true>(a, stream) : launch_one<T, D, false, false>(a, stream);
+    if (variant_a) return finest ? launch_nsp<T, D, true, true>(a, stream) : launch_nsp<T, D, true, false>(a, stream);
+    return finest ? launch_nsp<T, D, false, true>(a, stream) : launch_nsp<T, D, false, false>(a, stream);
 }
 
 }  // namespace
