@@ -70,24 +70,22 @@ typedef enum { QTA_F32 = 0, QTA_BF16 = 1 } qta_dtype;
 
 /* Byte offsets of the regions qta_forward keeps in its workspace. Entries for levels that do not
  * exist (and level 0 of q/k/v, msg, sel_idx, sel_key, which live outside it) are 0.
- * Pyramid levels that later levels gather from (every level but the coarsest) are stored
- * parent-blocked when blocked[l] is 1: [B][heads][ceil(H_l/2)][ceil(W_l/2)][2][2][d], i.e. the 2x2
- * children of one parent position of one head are 4*d contiguous elements (off-map children are
- * unused padding). The coarsest level is NHWC. With blocking on, the workspace also holds blocked
- * copies of the input k and v. Blocking is used when 4*K <= 64. */
+ * Intermediate pyramid levels (1 <= l <= levels-2: produced by pooling and gathered by level l's
+ * attention) are stored parent-blocked when blocked[l] is 1:
+ * [B][heads][ceil(H_l/2)][ceil(W_l/2)][2][2][d], i.e. the 2x2 children of one parent position of
+ * one head are 4*d contiguous elements (off-map children are unused padding). The input level 0
+ * and the coarsest level are NHWC. Blocking is used when 4*K <= 64. */
 typedef struct {
     int levels;
     int H[QTA_MAX_LEVELS];
     int W[QTA_MAX_LEVELS];
-    int blocked[QTA_MAX_LEVELS];    /* storage of pyramid level l (l >= 1) and of the k0/v0 copies */
+    int blocked[QTA_MAX_LEVELS];    /* 1: pyramid level l is parent-blocked, 0: NHWC         */
     size_t q[QTA_MAX_LEVELS];       /* pyramid level l >= 1, dtype                          */
     size_t k[QTA_MAX_LEVELS];
     size_t v[QTA_MAX_LEVELS];
     size_t msg[QTA_MAX_LEVELS];     /* level l >= 1, fp32 [B][N_l][heads][d]                 */
     size_t sel_idx[QTA_MAX_LEVELS]; /* level l >= 1, int32 [B][heads][N_l][K]                */
     size_t sel_key[QTA_MAX_LEVELS]; /* level l >= 1, fp32  [B][heads][N_l][K]                */
-    size_t k0_blocked;              /* blocked copy of the input k (valid when blocked[0])   */
-    size_t v0_blocked;              /* blocked copy of the input v (valid when blocked[0])   */
     size_t total;                   /* bytes; every region starts on a 256-byte boundary     */
 } qta_workspace_layout;
 

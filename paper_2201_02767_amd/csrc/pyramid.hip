@@ -1,12 +1,12 @@
 // Step 1: token pyramids by 2x2 average pooling (Sec. 3.2, pyramid paragraph).
 //
 // One pass produces up to two coarser levels from a source level. A thread owns one 16-byte
-// channel chunk of one token of the top level it produces: it reads that token's (up to) 4x4
-// source tokens with 16-byte loads (consecutive threads take consecutive chunks of a token, so a
-// wave reads whole rows), writes the (up to) four intermediate tokens, then pools those rounded
-// values again for the top token. Two levels per pass read each map once; deeper pyramids take
-// more passes. Each level is written NHWC or parent-blocked as asked, and the first pass can also
-// write a blocked copy of the input level (every input chunk is read by exactly one thread).
+// channel chunk of one token of the top level it produces: it issues the 16-byte loads of that
+// token's (up to) 4x4 source tokens all at once (consecutive threads take consecutive chunks of a
+// token, so a wave reads whole rows; addresses past the map's edge are clamped onto it and the
+// values ignored), writes the (up to) four intermediate tokens, then pools those rounded values
+// again for the top token. Two levels per pass read each map once; deeper pyramids take more
+// passes. Each level is written NHWC or parent-blocked as asked.
 //
 // Arithmetic, fixed so that every implementation stores the same bits: the valid children are
 // summed in fp32 as ((c00 + c01) + (c10 + c11)) with missing children left out, multiplied by
@@ -43,11 +43,11 @@ __global__ __launch_bounds__(256) void pyramid_pass_kernel(PyramidPassArgs a)
 {
     using S = Storage<T>;
     constexpr int E = S::kPer16B;
+    constexpr int R = NLEV == 2 ? 4 : 2;                // source rows / columns under one top token
     const int tensor = blockIdx.y;
     const char* __restrict__ src = static_cast<const char*>(a.src[tensor]);
     char* __restrict__ dst1 = static_cast<char*>(a.dst1[tensor]);
     char* __restrict__ dst2 = static_cast<char*>(a.dst2[tensor]);
-    char* __restrict__ copy = static_cast<char*>(a.copy[tensor]);
     const int chunks = a.chunks;                       // 16-byte chunks per token
     const int Ht = NLEV == 2 ? a.H2 : a.H1;
     const int Wt = NLEV == 2 ? a.W2 : a.W1;
@@ -61,27 +61,37 @@ __global__ __launch_bounds__(256) void pyramid_pass_kernel(PyramidPassArgs a)
     const int Y = static_cast<int>(tok % Ht);
     const int b = static_cast<int>(tok / Ht);
 
-    // load one source chunk; the blocked copy of the source (when asked for) is written on the way
-    auto load = [&](int y, int x, float (&o)[E]) {
-        const uint4 c = *reinterpret_cast<const uint4*>(
-            src + chunk_offset(a.src_blocked, b, y, x, a.Hs, a.Ws, ch, chunks, a.head_chunks));
-        if (copy) *reinterpret_cast<uint4*>(copy + chunk_offset(true, b, y, x, a.Hs, a.Ws, ch, chunks, a.head_chunks)) = c;
-        S::unpack(c, o);
-    };
+    // every source chunk under (Y, X), loaded before any is used
+    uint4 raw[R][R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const int y = min(R * Y + i, a.Hs - 1);
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            const int x = min(R * X + j, a.Ws - 1);
+            raw[i][j] = *reinterpret_cast<const uint4*>(
+                src + chunk_offset(a.src_blocked, b, y, x, a.Hs, a.Ws, ch, chunks, a.head_chunks));
+        }
+    }
     auto store = [&](char* base, bool blocked, int H, int W, int y, int x, const float (&v)[E]) {
         *reinterpret_cast<uint4*>(base + chunk_offset(blocked, b, y, x, H, W, ch, chunks, a.head_chunks)) = S::pack(v);
     };
-
-    if constexpr (NLEV == 1) {
-        const bool right = 2 * X + 1 < a.Ws, below = 2 * Y + 1 < a.Hs;
-        float c00[E], c01[E], c10[E], c11[E], o[E];
-        load(2 * Y, 2 * X, c00);
-        if (right) load(2 * Y, 2 * X + 1, c01);
-        if (below) load(2 * Y + 1, 2 * X, c10);
-        if (right && below) load(2 * Y + 1, 2 * X + 1, c11);
+    // pool the 2x2 source block whose top-left is (i0, j0) of raw into level-1 token (y1, x1)
+    auto pool1 = [&](int i0, int j0, int y1, int x1, float (&o)[E]) {
+        const bool right = 2 * x1 + 1 < a.Ws, below = 2 * y1 + 1 < a.Hs;
+        float c00[E], c01[E], c10[E], c11[E];
+        S::unpack(raw[i0][j0], c00);
+        S::unpack(raw[i0][j0 + 1], c01);
+        S::unpack(raw[i0 + 1][j0], c10);
+        S::unpack(raw[i0 + 1][j0 + 1], c11);
         pool_children<E>(c00, c01, c10, c11, right, below, o);
 #pragma unroll
         for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
+    };
+
+    if constexpr (NLEV == 1) {
+        float o[E];
+        pool1(0, 0, Y, X, o);
         store(dst1, a.dst1_blocked, a.H1, a.W1, Y, X, o);
     } else {
         // the four level-1 children of (Y, X), each pooled from its own source children
@@ -91,21 +101,8 @@ __global__ __launch_bounds__(256) void pyramid_pass_kernel(PyramidPassArgs a)
         for (int q = 0; q < 4; ++q) {
             const int y1 = 2 * Y + (q >> 1), x1 = 2 * X + (q & 1);
             mid_ok[q] = y1 < a.H1 && x1 < a.W1;
-            if (!mid_ok[q]) {
-#pragma unroll
-                for (int e = 0; e < E; ++e) mid[q][e] = 0.0f;
-                continue;
-            }
-            const bool right = 2 * x1 + 1 < a.Ws, below = 2 * y1 + 1 < a.Hs;
-            float c00[E], c01[E], c10[E], c11[E];
-            load(2 * y1, 2 * x1, c00);
-            if (right) load(2 * y1, 2 * x1 + 1, c01);
-            if (below) load(2 * y1 + 1, 2 * x1, c10);
-            if (right && below) load(2 * y1 + 1, 2 * x1 + 1, c11);
-            pool_children<E>(c00, c01, c10, c11, right, below, mid[q]);
-#pragma unroll
-            for (int e = 0; e < E; ++e) mid[q][e] = S::round(mid[q][e]);
-            store(dst1, a.dst1_blocked, a.H1, a.W1, y1, x1, mid[q]);
+            pool1(2 * (q >> 1), 2 * (q & 1), y1, x1, mid[q]);
+            if (mid_ok[q]) store(dst1, a.dst1_blocked, a.H1, a.W1, y1, x1, mid[q]);
         }
         float o[E];
         pool_children<E>(mid[0], mid[1], mid[2], mid[3], mid_ok[1], mid_ok[2], o);

@@ -50,8 +50,10 @@ qta_status check_problem(int B, int heads, int d, int K, qta_variant variant, qt
     return QTA_OK;
 }
 
-// Gathered levels are stored parent-blocked when the fine kernels take the blocked path (4K <= 64).
-bool use_blocked(int K, int levels) { return levels > 1 && 4 * K <= 64; }
+// Intermediate levels (produced by the pyramid, gathered by the next finer level) are stored
+// parent-blocked when the fine kernels take the blocked path (4K <= 64). The input level stays
+// NHWC: a blocked copy of it would cost a write and a read of k and v for no gain in the gathers.
+bool use_blocked(int K, int levels) { return levels > 2 && 4 * K <= 64; }
 
 qta_status layout(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype, qta_workspace_layout* L)
 {
@@ -70,14 +72,7 @@ qta_status layout(int B, int heads, int H, int W, int d, int levels, int K, qta_
     for (int l = 0; l < levels; ++l) {
         L->H[l] = Hl[l];
         L->W[l] = Wl[l];
-        L->blocked[l] = (blk && l <= levels - 2) ? 1 : 0;
-    }
-    if (blk) {
-        const size_t b0 = level_bytes(true, B, Hl[0], Wl[0], C, tb);
-        L->k0_blocked = off;
-        off = align_up(off + b0);
-        L->v0_blocked = off;
-        off = align_up(off + b0);
+        L->blocked[l] = (blk && l >= 1 && l <= levels - 2) ? 1 : 0;
     }
     for (int l = 1; l < levels; ++l) {
         const size_t N = static_cast<size_t>(Hl[l]) * Wl[l];
@@ -104,9 +99,8 @@ float resolve_scale(float scale, int d) { return scale > 0.f ? scale : 1.0f / __
 qta_status launch_status(hipError_t e) { return e == hipSuccess ? QTA_OK : QTA_ERR_HIP; }
 
 // Pyramid passes: from level s produce s+1 and, when it exists, s+2; repeat from s+2. `blocked`
-// gives the storage of each level (level 0, the input, is NHWC); copy0[t], when not NULL, receives
-// a blocked copy of tensor t's input level during the first pass.
-hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], void* const* copy0, int ntensors, int B,
+// gives the storage of each level (level 0, the input, is NHWC).
+hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], int ntensors, int B,
                        const int* Hl, const int* Wl, const int* blocked, int levels, int chunks, int head_chunks,
                        bool use_bf16, hipStream_t stream)
 {
@@ -117,7 +111,6 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], vo
             a.src[t] = s == 0 ? src0[t] : lvl[t][s];
             a.dst1[t] = lvl[t][s + 1];
             a.dst2[t] = nlev == 2 ? lvl[t][s + 2] : nullptr;
-            a.copy[t] = (s == 0 && copy0) ? copy0[t] : nullptr;
         }
         a.B = B;
         a.Hs = Hl[s];
@@ -192,7 +185,7 @@ qta_status qta_build_pyramid(const void* x, void* levels_out, int B, int H, int 
     const void* src[1] = {x};
     const int chunks = static_cast<int>(static_cast<size_t>(C) * dtype_bytes(dtype) / 16);
     const int nhwc[QTA_MAX_LEVELS] = {};
-    return launch_status(run_pyramid(src, lvl, nullptr, 1, B, Hl, Wl, nhwc, levels, chunks, chunks,
+    return launch_status(run_pyramid(src, lvl, 1, B, Hl, Wl, nhwc, levels, chunks, chunks,
                                      dtype == QTA_BF16, static_cast<hipStream_t>(stream)));
 }
 
@@ -346,16 +339,12 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
     auto sidx = [&](int l) { return reinterpret_cast<int32_t*>(ws + L.sel_idx[l]); };
     auto skey = [&](int l) { return reinterpret_cast<float*>(ws + L.sel_key[l]); };
 
-    // 1. pyramids of q, k and v (gathered levels blocked; blocked copies of the input k and v)
-    const bool blk = L.blocked[0] != 0;
-    void* k0b = blk ? ws + L.k0_blocked : nullptr;
-    void* v0b = blk ? ws + L.v0_blocked : nullptr;
+    // 1. pyramids of q, k and v (intermediate levels blocked when the layout says so)
     if (levels > 1) {
         const void* src[3] = {q, k, v};
-        void* copy0[3] = {nullptr, k0b, v0b};
         const int chunks = static_cast<int>(static_cast<size_t>(C) * dtype_bytes(dtype) / 16);
         const int head_chunks = static_cast<int>(static_cast<size_t>(d) * dtype_bytes(dtype) / 16);
-        hipError_t e = run_pyramid(src, pyr, blk ? copy0 : nullptr, 3, B, L.H, L.W, L.blocked, levels, chunks,
+        hipError_t e = run_pyramid(src, pyr, 3, B, L.H, L.W, L.blocked, levels, chunks,
                                    head_chunks, use_bf16, s);
         if (e != hipSuccess) return QTA_ERR_HIP;
     }
@@ -418,10 +407,10 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
     {
         FineArgs a{};
         a.q = q;
-        a.k = blk ? k0b : k;
-        a.v = blk ? v0b : v;
+        a.k = k;
+        a.v = v;
         a.q_blocked = false;
-        a.kv_blocked = blk;
+        a.kv_blocked = false;
         a.B = B;
         a.heads = heads;
         a.H = H;

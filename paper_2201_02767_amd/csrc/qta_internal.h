@@ -40,12 +40,11 @@ inline size_t level_bytes(bool blocked, int B, int H, int W, int C, int tb)
 }
 
 // One pyramid pass over up to three token maps (q, k, v): from a source level produce one or two
-// coarser levels. Optionally also copies the source (level 0) into the blocked layout.
+// coarser levels.
 struct PyramidPassArgs {
     const void* src[3];
     void* dst1[3];
     void* dst2[3];
-    void* copy[3];              // blocked copy of the source level, or NULL
     int B, Hs, Ws, H1, W1, H2, W2;
     int chunks;                 // 16-byte chunks per token (C * sizeof(dtype) / 16)
     int head_chunks;            // 16-byte chunks per head row (d * sizeof(dtype) / 16)

@@ -39,8 +39,6 @@ class WorkspaceLayout(ctypes.Structure):
         ("msg", ctypes.c_size_t * MAX_LEVELS),
         ("sel_idx", ctypes.c_size_t * MAX_LEVELS),
         ("sel_key", ctypes.c_size_t * MAX_LEVELS),
-        ("k0_blocked", ctypes.c_size_t),
-        ("v0_blocked", ctypes.c_size_t),
         ("total", ctypes.c_size_t),
     ]
 
@@ -230,13 +228,6 @@ class Plan:
         if not lay.blocked[level]:
             return self._view(off, (self.B, H, W, self.heads, self.d), self.dtype)
         return self._unblock(off, H, W)
-
-    def blocked_input(self, which: str):
-        """The blocked copy of the input k or v that the finest level gathers from."""
-        lay = self.layout
-        if not lay.blocked[0]:
-            raise ValueError("this problem keeps its inputs NHWC")
-        return self._unblock(getattr(lay, which + "0_blocked"), self.H, self.W)
 
     def _unblock(self, off, H, W):
         Hp, Wp = (H + 1) // 2, (W + 1) // 2

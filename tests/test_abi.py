@@ -66,13 +66,10 @@ def _tok_bytes(blocked, B, H, W, C, tb):
 def test_workspace_layout_is_aligned_and_disjoint(K, expect_blocked):
     lay = P.workspace_layout(2, 2, 200, 336, 32, 5, K, torch.bfloat16)
     regions = []
-    assert bool(lay.blocked[0]) == expect_blocked
-    if expect_blocked:
-        b0 = _tok_bytes(True, 2, 200, 336, 64, 2)
-        regions += [(lay.k0_blocked, b0), (lay.v0_blocked, b0)]
+    assert lay.blocked[0] == 0 and lay.blocked[4] == 0     # input and coarsest level stay NHWC
     for l in range(1, 5):
         N = lay.H[l] * lay.W[l]
-        assert lay.blocked[l] == (1 if expect_blocked and l <= 3 else 0)
+        assert lay.blocked[l] == (1 if expect_blocked and 1 <= l <= 3 else 0)
         tok = _tok_bytes(lay.blocked[l], 2, lay.H[l], lay.W[l], 64, 2)
         regions += [(lay.q[l], tok), (lay.k[l], tok), (lay.v[l], tok), (lay.msg[l], 2 * N * 64 * 4),
                     (lay.sel_idx[l], 2 * 2 * N * K * 4), (lay.sel_key[l], 2 * 2 * N * K * 4)]

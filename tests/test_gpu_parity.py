@@ -64,10 +64,6 @@ def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=No
     ref = O.forward(q, k, v, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale,
                     forced=g_sel, want_candidates=True, want_pyramids=True)
     res = {"sel": {}, "msg": {}}
-    if plan.layout.blocked[0]:
-        # the blocked copies of the input k and v hold exactly the input values
-        assert np.array_equal(to_np(plan.blocked_input("k")).reshape(k.shape), k.astype(np.float32))
-        assert np.array_equal(to_np(plan.blocked_input("v")).reshape(v.shape), v.astype(np.float32))
     for l in range(1, levels):
         for name in "qkv":
             gp = to_np(plan.pyramid(name, l)).reshape(ref["pyr_" + name][l].shape)
