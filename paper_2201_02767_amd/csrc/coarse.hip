@@ -29,14 +29,15 @@ constexpr int kWaves = 16;
 // operand read touches fall in different banks.
 __host__ __device__ inline int coarse_pitch(int N) { return (N + 63) / 64 * 64 + 4; }
 
-// Row elements per lane, rounded up to a power of two (a template parameter, so the selection
-// loops carry no bounds checks).
+// Row elements per lane: ceil(N / 64) rounded up to the next instantiated count (a template
+// parameter, so the selection loops carry no bounds checks and no empty slots for common sizes).
 inline int coarse_per_lane(int N)
 {
     const int need = (N + kWave - 1) / kWave;
-    int p = 1;
-    while (p < need) p <<= 1;
-    return p;
+    static const int counts[] = {1, 2, 3, 4, 5, 6, 8, 12, 16};
+    for (int c : counts)
+        if (need <= c) return c;
+    return 0;
 }
 
 template <typename T, int D, bool VA, int kPerLane>
@@ -59,65 +60,77 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     const size_t tok0 = static_cast<size_t>(b) * N;           // first token of this batch element
     const size_t hoff = static_cast<size_t>(h) * D;
 
+    // V operands of phase 3's first key batch, requested now so that their latency overlaps the
+    // logits and the selection (phase 3 layout: lane (kgrp, col) holds V[4*step + kgrp][16*ct + col])
+    constexpr int NCT = D / 16;          // 16-wide column tiles of the messages
+    constexpr int NKS = kWaves / NCT;    // key chunks
+    constexpr int kVBatch = 8;           // key steps per V batch
+    const int p3_ct = wave % NCT, p3_ks = wave / NCT;
+    const int p3_ch = p3_ct * 16 + (lane & 15);
+    const int steps = (N + 3) / 4;
+    float vb[kVBatch];
+    auto load_v = [&](int st0) {
+#pragma unroll
+        for (int u = 0; u < kVBatch; ++u) {
+            const int cand = min((st0 + u * NKS) * 4 + (lane >> 4), N - 1);    // clamped; weight 0 beyond N
+            vb[u] = S::load1(a.v, (tok0 + cand) * C + hoff + p3_ch);
+        }
+    };
+    load_v(p3_ks);
+
     // ---- phase 1: logits on MFMA; a wave takes key tiles wave, wave+16, ... (at most 4) ----
+    // The contraction over the d channels is taken in a permuted order so that each lane loads
+    // whole 16-byte chunks of its query or key row: lane (kgrp, r) loads chunks kgrp, kgrp+4, ...
+    // of row r and feeds their elements to consecutive k-steps; Q and K use the same permutation.
     {
         const int arow = lane & 15, kgrp = lane >> 4;
-        const int qi = tile * kRows + arow;
-        const bool qok = qi < N;
-        if constexpr (kBf16) {
-            constexpr int KS = D / 16;
-            short4_t av[KS], bv[kMaxTilesPerWave][KS];
-            const uint16_t* qb = static_cast<const uint16_t*>(a.q) + (tok0 + (qok ? qi : 0)) * C + hoff;
+        const int qi = min(tile * kRows + arow, N - 1);   // rows past N are computed and ignored
+        constexpr int NJ = D * static_cast<int>(sizeof(T)) / 64;    // 16-byte chunks per lane and row
+        uint4 qa[NJ], kb[kMaxTilesPerWave][NJ];
+        const unsigned char* qrow = static_cast<const unsigned char*>(a.q) + ((tok0 + qi) * C + hoff) * sizeof(T);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                av[ks] = short4_t{0, 0, 0, 0};
-                if (qok) av[ks] = *reinterpret_cast<const short4_t*>(qb + ks * 16 + 4 * kgrp);
-            }
+        for (int jj = 0; jj < NJ; ++jj) qa[jj] = *reinterpret_cast<const uint4*>(qrow + (kgrp + 4 * jj) * 16);
 #pragma unroll
-            for (int it = 0; it < kMaxTilesPerWave; ++it) {
-                const int n = (wave + kWaves * it) * 16 + (lane & 15);
-                const uint16_t* kb = static_cast<const uint16_t*>(a.k) + (tok0 + (n < N ? n : 0)) * C + hoff;
+        for (int it = 0; it < kMaxTilesPerWave; ++it) {
+            if (wave + kWaves * it >= tiles) break;                           // uniform
+            const int n = min((wave + kWaves * it) * 16 + arow, N - 1);       // columns past N set to -inf
+            const unsigned char* krow = static_cast<const unsigned char*>(a.k) + ((tok0 + n) * C + hoff) * sizeof(T);
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    bv[it][ks] = short4_t{0, 0, 0, 0};
-                    if (n < N) bv[it][ks] = *reinterpret_cast<const short4_t*>(kb + ks * 16 + 4 * kgrp);
+            for (int jj = 0; jj < NJ; ++jj) kb[it][jj] = *reinterpret_cast<const uint4*>(krow + (kgrp + 4 * jj) * 16);
+        }
+#pragma unroll
+        for (int it = 0; it < kMaxTilesPerWave; ++it) {
+            const int kt = wave + kWaves * it;
+            if (kt >= tiles) break;
+            float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int jj = 0; jj < NJ; ++jj) {
+                if constexpr (kBf16) {
+                    // 8 bf16 per chunk: k-steps 2*jj and 2*jj+1, four channels each
+                    const uint4 qq = qa[jj], kk = kb[it][jj];
+                    short4_t a0, b0, a1, b1;
+                    a0[0] = static_cast<short>(qq.x); a0[1] = static_cast<short>(qq.x >> 16);
+                    a0[2] = static_cast<short>(qq.y); a0[3] = static_cast<short>(qq.y >> 16);
+                    a1[0] = static_cast<short>(qq.z); a1[1] = static_cast<short>(qq.z >> 16);
+                    a1[2] = static_cast<short>(qq.w); a1[3] = static_cast<short>(qq.w >> 16);
+                    b0[0] = static_cast<short>(kk.x); b0[1] = static_cast<short>(kk.x >> 16);
+                    b0[2] = static_cast<short>(kk.y); b0[3] = static_cast<short>(kk.y >> 16);
+                    b1[0] = static_cast<short>(kk.z); b1[1] = static_cast<short>(kk.z >> 16);
+                    b1[2] = static_cast<short>(kk.w); b1[3] = static_cast<short>(kk.w >> 16);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, b0, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, b1, acc, 0, 0, 0);
+                } else {
+                    // 4 floats per chunk: four k-steps
+                    const uint4 qq = qa[jj], kk = kb[it][jj];
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.x), __uint_as_float(kk.x), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.y), __uint_as_float(kk.y), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.z), __uint_as_float(kk.z), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.w), __uint_as_float(kk.w), acc, 0, 0, 0);
                 }
             }
+            const int n = kt * 16 + (lane & 15);
 #pragma unroll
-            for (int it = 0; it < kMaxTilesPerWave; ++it) {
-                const int kt = wave + kWaves * it;
-                if (kt >= tiles) break;
-                float4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av[ks], bv[it][ks], acc, 0, 0, 0);
-                const int n = kt * 16 + (lane & 15);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) Sm[(4 * kgrp + j) * pitch + n] = n < N ? acc[j] * a.scale : -INFINITY;
-            }
-        } else {
-            constexpr int KS = D / 4;
-            float av[KS], bv[kMaxTilesPerWave][KS];
-            const float* qf = static_cast<const float*>(a.q) + (tok0 + (qok ? qi : 0)) * C + hoff;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) av[ks] = qok ? qf[ks * 4 + kgrp] : 0.f;
-#pragma unroll
-            for (int it = 0; it < kMaxTilesPerWave; ++it) {
-                const int n = (wave + kWaves * it) * 16 + (lane & 15);
-                const float* kf = static_cast<const float*>(a.k) + (tok0 + (n < N ? n : 0)) * C + hoff;
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) bv[it][ks] = n < N ? kf[ks * 4 + kgrp] : 0.f;
-            }
-#pragma unroll
-            for (int it = 0; it < kMaxTilesPerWave; ++it) {
-                const int kt = wave + kWaves * it;
-                if (kt >= tiles) break;
-                float4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[ks], bv[it][ks], acc, 0, 0, 0);
-                const int n = kt * 16 + (lane & 15);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) Sm[(4 * kgrp + j) * pitch + n] = n < N ? acc[j] * a.scale : -INFINITY;
-            }
+            for (int jr = 0; jr < 4; ++jr) Sm[(4 * kgrp + jr) * pitch + n] = n < N ? acc[jr] * a.scale : -INFINITY;
         }
     }
     __syncthreads();
@@ -187,27 +200,16 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     __syncthreads();
 
     // ---- phase 3: messages m = P V on fp32 MFMA (values widened on load, so no transpose) ----
-    constexpr int NCT = D / 16;          // 16-wide column tiles
-    constexpr int NKS = kWaves / NCT;    // key chunks
     {
-        const int ct = wave % NCT, ks = wave / NCT;
         const int arow = lane & 15, kgrp = lane >> 4;
-        const int ch = ct * 16 + (lane & 15);
-        const int steps = (N + 3) / 4;
         float4_t acc = {0.f, 0.f, 0.f, 0.f};
-        constexpr int kBatch = 8;
-        for (int st0 = ks; st0 < steps; st0 += NKS * kBatch) {
-            float bv[kBatch];
+        for (int st0 = p3_ks; st0 < steps; st0 += NKS * kVBatch) {
+            if (st0 != p3_ks) load_v(st0);                    // the first batch came in at the start
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-                const int cand = (st0 + u * NKS) * 4 + kgrp;
-                bv[u] = cand < N ? S::load1(a.v, (tok0 + cand) * C + hoff + ch) : 0.f;
-            }
-#pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
+            for (int u = 0; u < kVBatch; ++u) {
                 const int st = st0 + u * NKS;
                 if (st >= steps) break;
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Sm[arow * pitch + st * 4 + kgrp], bv[u], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Sm[arow * pitch + st * 4 + kgrp], vb[u], acc, 0, 0, 0);
             }
         }
 #pragma unroll
@@ -259,8 +261,12 @@ hipError_t launch_per_lane(const CoarseArgs& a, hipStream_t stream)
     switch (coarse_per_lane(a.N)) {
     case 1: return launch_one<T, D, VA, 1>(a, stream);
     case 2: return launch_one<T, D, VA, 2>(a, stream);
+    case 3: return launch_one<T, D, VA, 3>(a, stream);
     case 4: return launch_one<T, D, VA, 4>(a, stream);
+    case 5: return launch_one<T, D, VA, 5>(a, stream);
+    case 6: return launch_one<T, D, VA, 6>(a, stream);
     case 8: return launch_one<T, D, VA, 8>(a, stream);
+    case 12: return launch_one<T, D, VA, 12>(a, stream);
     case 16: return launch_one<T, D, VA, 16>(a, stream);
     }
     return hipErrorInvalidValue;
