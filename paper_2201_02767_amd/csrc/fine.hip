@@ -4,19 +4,23 @@
 //
 // Work item = one parent query P at level l+1 and one head. Its four children at level l are
 // sibling queries with one shared candidate set: the 2x2 children of the K keys P kept (4K <= 64
-// candidates here; larger K runs the kernel of fine_wide.hip). One wave owns one item, and lane s
-// owns candidate slot s = 4r + c (child c, in the order (0,0),(0,1),(1,0),(1,1), of kept key r):
-//   1. the candidates' key and value rows of this head are gathered once for the four queries,
-//      with 16-byte loads, several lanes per row, into wave-private LDS (values transposed). In the
-//      blocked layout a kept key's four children are one contiguous run, so a gather instruction
-//      reads whole cache lines;
-//   2. logits S[query][slot] on the 4x4x4 MFMA: each of the 16 blocks multiplies the four queries
-//      by the four candidates of one lane quad, so lane s ends with the four logits of slot s;
+// candidates here; larger K runs the kernel of fine_wide.hip). One wave owns one item; candidate
+// slot s = 4r + c is child c, in the order (0,0),(0,1),(1,0),(1,1), of kept key r, and the slots
+// are taken in tiles of 16:
+//   1. the candidates' key and value rows of this head are gathered once for the four queries with
+//      16-byte loads: lane 16g + n loads chunks g, g+4, ... of the row of slot n of each tile, so
+//      one instruction reads 16 whole rows. The value rows go to wave-private LDS (transposed for
+//      bf16); the key rows stay in registers;
+//   2. logits on the 16x16 MFMA straight from those registers: the key chunks are the B operand,
+//      the four queries, repeated over the 16 rows, the A operand (the d channels are contracted in
+//      the order the chunks arrive, the same for both operands). Every lane group then holds all
+//      four logits of its slot column for every tile, and lane 16g + n keeps tile g, so lane s ends
+//      with the four logits of slot s;
 //   3. B: a softmax per query over the wave (DPP and permlane butterflies, no LDS);
 //      A: a softmax over each lane quad (the children of one kept key) times the parent's score;
 //   4. levels above 0: the K best candidates of each query by a bitwise radix select on wave
 //      ballots (ties at the cut to the lower flat index); A drops their weight from its message;
-//   5. messages m = P V on the same MFMA, blocks split over 4-channel groups (and slot halves);
+//   5. messages m = P V on the 4x4 MFMA, blocks split over 4-channel groups (and slot halves);
 //   6. levels above 0 store m; level 0 adds the ancestors' messages (times w for B) and stores the
 //      output in the storage type.
 // A workgroup holds four independent waves; nothing synchronises across waves.
@@ -29,24 +33,24 @@ namespace {
 
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
 constexpr int kMaxSlots = 64;
-constexpr int kPrefetchLevels = 7;    // the finest level prefetches up to this many ancestors
+constexpr int kPrefetchLevels = 4;    // the finest level prefetches up to this many ancestors
 
-// Byte layout of one wave's LDS region for nsp padded slots (a multiple of 16).
+// Byte layout of one wave's LDS region for nsp padded slots (a multiple of 16): the value rows
+// and the weights P.
 struct WaveLds {
-    int q, k, v, p, total;
+    int v, p, total;
     int vpitch;    // bf16: elements per transposed value row; fp32: floats per value row
 };
 
 template <typename T, int D>
 __host__ __device__ inline WaveLds wave_lds(int nsp)
 {
-    constexpr int TB = sizeof(T), RB = D * TB, KP = RB + 16;
+    constexpr int TB = sizeof(T);
     WaveLds L;
-    L.q = 0;
-    L.k = 4 * RB;
-    L.v = L.k + nsp * KP;
+    L.v = 0;
     int vbytes;
     if (TB == 2) {
         L.vpitch = nsp + 8;                 // Vt[channel][slot]
@@ -77,10 +81,10 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     constexpr bool kBf16 = sizeof(T) == 2;
     constexpr int TB = sizeof(T);
     constexpr int RB = D * TB;             // bytes of one head's row
-    constexpr int KP = RB + 16;            // LDS pitch of key rows (padding spreads the banks)
     constexpr int E = S::kPer16B;          // elements per 16-byte chunk
-    constexpr int LPR = RB / 16;           // lanes per row when gathering
-    constexpr int RPP = kWave / LPR;       // rows per gather instruction
+    constexpr int NJ = RB / 64;            // 16-byte chunks per lane and row (lane group g: g, g+4, ...)
+    constexpr int NT = NSP / 16;           // slot tiles (upper bound)
+    constexpr int kTB = (8 / NJ) < NT ? (8 / NJ) : NT;   // tiles whose rows are in registers at once
     constexpr int NCG = D / 4;             // PV: 4-channel groups
     constexpr int NH = 16 / NCG;           // PV: slot halves (2 for d = 32, 1 for d = 64)
     constexpr int QPL = 4 / NH;            // output queries per lane
@@ -105,8 +109,6 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     extern __shared__ __align__(16) unsigned char smem[];
     const WaveLds lay = wave_lds<T, D>(nsp);
     unsigned char* base = smem + static_cast<size_t>(wave) * lay.total;
-    unsigned char* Qs = base + lay.q;
-    unsigned char* Ks = base + lay.k;
     unsigned char* Vb = base + lay.v;
     unsigned char* Pb = base + lay.p;
 
@@ -123,74 +125,56 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     //      makes the compiler wait for it at the join, so every load below is unconditional, at a
     //      clamped address that is always in bounds, with validity applied when the value is used.
     //      Phase A holds every load that needs no other load; phase B the gathers. ----
-    const int sub = lane / LPR, chunk = lane % LPR;
-    constexpr int kRounds = (NSP + RPP - 1) / RPP;     // gather instructions per tensor (upper bound)
-    // phase A: the parents' kept keys (own slot and gather slots), the parents' scores (A), the
-    // query chunk, and at the finest level the ancestors' messages and this lane's level weights
+    const int n16 = lane & 15, g = lane >> 4;
+    const int ntile = nsp / 16;
+    // phase A: the parents' kept keys (own slot and this lane's gather slot of each tile), the
+    // parents' scores (A) and the query chunks (A operand: row n16 holds query n16 & 3)
     const int last_sel = K - 1;
     const int J_own_raw = a.parent_idx[prow + min(lane >> 2, last_sel)];
-    int J_g[kRounds];
+    int J_g[NT];
 #pragma unroll
-    for (int u = 0; u < kRounds; ++u) J_g[u] = a.parent_idx[prow + min((u * RPP + sub) >> 2, last_sel)];
+    for (int t = 0; t < NT; ++t) J_g[t] = a.parent_idx[prow + min(4 * t + (n16 >> 2), last_sel)];
     float pkey = 0.f;
     if constexpr (VA) pkey = a.parent_key[prow + min(lane >> 2, last_sel)];
-    const int qsub = sub & 3;
-    const int qy = 2 * Py + (qsub >> 1), qx = 2 * Px + (qsub & 1);
-    const bool q_ok = sub < 4 && qy < H && qx < W;
-    uint4 qraw;
+    uint4 qa[NJ];
+    bool q_ok;
     {
+        const int qi = n16 & 3;
+        const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
+        q_ok = qy < H && qx < W;
         const int qyc = qy < H ? qy : H - 1, qxc = qx < W ? qx : W - 1;
-        const size_t qoff = a.q_blocked ? (((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 + qsub) * RB
+        const size_t qoff = a.q_blocked ? (((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 + qi) * RB
                                         : ((static_cast<size_t>(b) * N + qyc * W + qxc) * C + h * D) * TB;
-        qraw = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.q) + qoff + chunk * 16);
+        const unsigned char* qrow = static_cast<const unsigned char*>(a.q) + qoff;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) qa[j] = *reinterpret_cast<const uint4*>(qrow + (g + 4 * j) * 16);
     }
     // phase B: the gathers. NHWC: child f of this head at kg + f*C*TB. Blocked: the four children
     // of kept key J are the 4*RB bytes at kg + J*4*RB (this (batch, head)'s blocks start at kg).
     const bool kvb = a.kv_blocked;
     const size_t kv_base = kvb ? (static_cast<size_t>(b) * a.heads + h) * Np * 4 * RB
                                : (static_cast<size_t>(b) * N * C + h * D) * TB;
-    const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base + chunk * 16;
-    const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base + chunk * 16;
+    const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base + g * 16;
+    const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base + g * 16;
     const size_t tok_bytes = static_cast<size_t>(C) * TB;
-    // at most kBatch rounds of gathered rows are held in registers at a time
-    constexpr int kBatch = kRounds < 8 ? kRounds : 8;
-    bool gok[kRounds];
-    uint4 kc[kBatch], vc[kBatch];
-    auto load_batch = [&](int u0) {
+    bool gok[NT];
+    uint4 kc[kTB][NJ], vc[kTB][NJ];
+    auto load_tiles = [&](int t0) {
 #pragma unroll
-        for (int i = 0; i < kBatch; ++i) {
-            const int u = u0 + i, s = u * RPP + sub;
-            if (u >= kRounds || u * RPP >= nsp) break;        // uniform
-            const int f = child_of_slot_J(J_g[u], s);
-            gok[u] = f >= 0;
-            const size_t goff = !gok[u] ? 0 : (kvb ? (static_cast<size_t>(J_g[u]) * 4 + (s & 3)) * RB : f * tok_bytes);
-            kc[i] = *reinterpret_cast<const uint4*>(kg + goff);
-            vc[i] = *reinterpret_cast<const uint4*>(vg + goff);
-        }
-    };
-    auto store_batch = [&](int u0) {
+        for (int i = 0; i < kTB; ++i) {
+            const int t = t0 + i, s = 16 * t + n16;
+            if (t >= NT || t >= ntile) break;                 // uniform
+            const int f = child_of_slot_J(J_g[t], s);
+            gok[t] = f >= 0;
+            const size_t goff = !gok[t] ? 0 : (kvb ? (static_cast<size_t>(J_g[t]) * 4 + (s & 3)) * RB : f * tok_bytes);
 #pragma unroll
-        for (int i = 0; i < kBatch; ++i) {
-            const int u = u0 + i, s = u * RPP + sub;
-            if (u >= kRounds || u * RPP >= nsp) break;        // uniform
-            const uint4 zero = make_uint4(0, 0, 0, 0);
-            const uint4 kk = gok[u] ? kc[i] : zero;
-            const uint4 vv = gok[u] ? vc[i] : zero;
-            *reinterpret_cast<uint4*>(Ks + s * KP + chunk * 16) = kk;
-            if constexpr (kBf16) {
-                uint16_t* vt = reinterpret_cast<uint16_t*>(Vb);
-                const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const uint32_t bits = (e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xFFFFu);
-                    vt[(chunk * E + e) * lay.vpitch + s] = static_cast<uint16_t>(bits);
-                }
-            } else {
-                *reinterpret_cast<uint4*>(Vb + (s * lay.vpitch + chunk * E) * 4) = vv;
+            for (int j = 0; j < NJ; ++j) {
+                kc[i][j] = *reinterpret_cast<const uint4*>(kg + goff + 64 * j);
+                vc[i][j] = *reinterpret_cast<const uint4*>(vg + goff + 64 * j);
             }
         }
     };
-    load_batch(0);
+    load_tiles(0);
     // Output ownership (step 6): lane 4*blk + t4 with blk = cg*NH + hh owns channel 4*cg + t4 of
     // queries hh*QPL .. hh*QPL + QPL-1.
     const int blk = lane >> 2, t4 = lane & 3;
@@ -225,54 +209,61 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     }
     const int flat = child_of_slot_J(lane < nslot ? J_own_raw : -1, lane);
     const bool ok = flat >= 0;
-    // LDS stores: the query (loaded first), then the gathered rows (off-map or missing candidates
-    // as zeros)
-    if (sub < 4) *reinterpret_cast<uint4*>(Qs + sub * RB + chunk * 16) = q_ok ? qraw : make_uint4(0, 0, 0, 0);
-    store_batch(0);
-#pragma unroll
-    for (int u0 = kBatch; u0 < kRounds; u0 += kBatch) {
-        load_batch(u0);
-        store_batch(u0);
-    }
-    wave_lds_sync();
 
-    // ---- 2. logits on MFMA: lane 4*blk + j holds S[query r][slot lane] in register r ----
-    float x[4];
-    {
-        const int srow = lane < nsp ? lane : nsp - 1;
-        const int qi = lane & 3;
-        float4_t acc = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (kBf16) {
+    // ---- 2. logits on MFMA and the value rows into LDS, one batch of tiles at a time ----
+    float acc_own[4] = {0.f, 0.f, 0.f, 0.f};
+    auto consume_tiles = [&](int t0) {
 #pragma unroll
-            for (int c0 = 0; c0 < D; c0 += 8) {
-                const uint4 kq = *reinterpret_cast<const uint4*>(Ks + srow * KP + c0 * 2);
-                const uint4 qq = *reinterpret_cast<const uint4*>(Qs + qi * RB + c0 * 2);
-                short4_t a0, b0, a1, b1;
-                a0[0] = static_cast<short>(qq.x); a0[1] = static_cast<short>(qq.x >> 16);
-                a0[2] = static_cast<short>(qq.y); a0[3] = static_cast<short>(qq.y >> 16);
-                a1[0] = static_cast<short>(qq.z); a1[1] = static_cast<short>(qq.z >> 16);
-                a1[2] = static_cast<short>(qq.w); a1[3] = static_cast<short>(qq.w >> 16);
-                b0[0] = static_cast<short>(kq.x); b0[1] = static_cast<short>(kq.x >> 16);
-                b0[2] = static_cast<short>(kq.y); b0[3] = static_cast<short>(kq.y >> 16);
-                b1[0] = static_cast<short>(kq.z); b1[1] = static_cast<short>(kq.z >> 16);
-                b1[2] = static_cast<short>(kq.w); b1[3] = static_cast<short>(kq.w >> 16);
-                acc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a0, b0, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a1, b1, acc, 0, 0, 0);
+        for (int i = 0; i < kTB; ++i) {
+            const int t = t0 + i, s = 16 * t + n16;
+            if (t >= NT || t >= ntile) break;                 // uniform
+            float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const uint4 qq = q_ok ? qa[j] : make_uint4(0, 0, 0, 0);
+                const uint4 kk = gok[t] ? kc[i][j] : make_uint4(0, 0, 0, 0);
+                if constexpr (kBf16) {
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qq),
+                                                                  __builtin_bit_cast(bf16x8_t, kk), acc, 0, 0, 0);
+                } else {
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.x), __uint_as_float(kk.x), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.y), __uint_as_float(kk.y), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.z), __uint_as_float(kk.z), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.w), __uint_as_float(kk.w), acc, 0, 0, 0);
+                }
             }
-        } else {
+            // rows 4g + r of the product are query r for every g: lane 16g + n keeps tile g
 #pragma unroll
-            for (int c0 = 0; c0 < D; c0 += 4) {
-                const float4 kq = *reinterpret_cast<const float4*>(Ks + srow * KP + c0 * 4);
-                const float4 qq = *reinterpret_cast<const float4*>(Qs + qi * RB + c0 * 4);
-                acc = __builtin_amdgcn_mfma_f32_4x4x1f32(qq.x, kq.x, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_4x4x1f32(qq.y, kq.y, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_4x4x1f32(qq.z, kq.z, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_4x4x1f32(qq.w, kq.w, acc, 0, 0, 0);
+            for (int r = 0; r < 4; ++r) acc_own[r] = g == t ? acc[r] : acc_own[r];
+            // value rows (off-map or missing candidates as zeros)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const uint4 vv = gok[t] ? vc[i][j] : make_uint4(0, 0, 0, 0);
+                const int c0 = (g + 4 * j) * E;               // first channel of this chunk
+                if constexpr (kBf16) {
+                    uint16_t* vt = reinterpret_cast<uint16_t*>(Vb);
+                    const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const uint32_t bits = (e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xFFFFu);
+                        vt[(c0 + e) * lay.vpitch + s] = static_cast<uint16_t>(bits);
+                    }
+                } else {
+                    *reinterpret_cast<uint4*>(Vb + (s * lay.vpitch + c0) * 4) = vv;
+                }
             }
         }
+    };
+    consume_tiles(0);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) x[r] = ok ? acc[r] * a.scale : -INFINITY;
+    for (int t0 = kTB; t0 < NT; t0 += kTB) {
+        if (t0 >= ntile) break;                               // uniform
+        load_tiles(t0);
+        consume_tiles(t0);
     }
+    float x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) x[r] = ok ? acc_own[r] * a.scale : -INFINITY;
 
     // ---- 3. weights ----
     float wgt[4], inv_sum[4] = {1.f, 1.f, 1.f, 1.f};
