@@ -175,38 +175,6 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
         }
     };
     load_tiles(0);
-    // Output ownership (step 6): lane 4*blk + t4 with blk = cg*NH + hh owns channel 4*cg + t4 of
-    // queries hh*QPL .. hh*QPL + QPL-1.
-    const int blk = lane >> 2, t4 = lane & 3;
-    const int cg = blk / NH, hh = blk % NH;
-    const int ch = 4 * cg + t4;
-    constexpr int kPre = FINEST ? kPrefetchLevels : 1;
-    float anc[kPre] = {};
-    float wq[FINEST ? QPL : 1][kPre + 1] = {};
-    const bool prefetch = FINEST && a.levels <= kPre + 1;
-    // phase C (after the gathers are in flight): the finest level's combination inputs
-    if constexpr (FINEST) {
-        if (prefetch) {                                      // uniform
-            const int L = a.levels;
-#pragma unroll
-            for (int lev = 1; lev <= kPre; ++lev) {
-                const int lv = lev < L ? lev : L - 1;        // >= 1: the finest level has L >= 2
-                const size_t an = static_cast<size_t>(b) * a.lvl_N[lv] +
-                                  static_cast<size_t>((2 * Py) >> lv) * a.lvl_W[lv] + ((2 * Px) >> lv);
-                anc[lev - 1] = a.coarser_msg[lv][(an * a.heads + h) * D + ch];   // ancestors shared by siblings
-            }
-            if (!VA && a.w) {                                // uniform
-#pragma unroll
-                for (int u = 0; u < QPL; ++u) {
-                    const int qi = (NH == 2 ? hh * QPL : 0) + u;
-                    const int wy = min(2 * Py + (qi >> 1), H - 1), wx = min(2 * Px + (qi & 1), W - 1);
-                    const float* wrow = a.w + ((static_cast<size_t>(b) * N + wy * W + wx) * a.heads + h) * L;
-#pragma unroll
-                    for (int lev = 0; lev <= kPre; ++lev) wq[u][lev] = wrow[lev < L ? lev : L - 1];
-                }
-            }
-        }
-    }
     const int flat = child_of_slot_J(lane < nslot ? J_own_raw : -1, lane);
     const bool ok = flat >= 0;
 
@@ -260,6 +228,39 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
         if (t0 >= ntile) break;                               // uniform
         load_tiles(t0);
         consume_tiles(t0);
+    }
+    // Output ownership (step 6): lane 4*blk + t4 with blk = cg*NH + hh owns channel 4*cg + t4 of
+    // queries hh*QPL .. hh*QPL + QPL-1.
+    const int blk = lane >> 2, t4 = lane & 3;
+    const int cg = blk / NH, hh = blk % NH;
+    const int ch = 4 * cg + t4;
+    constexpr int kPre = FINEST ? kPrefetchLevels : 1;
+    float anc[kPre] = {};
+    float wq[FINEST ? QPL : 1][kPre + 1] = {};
+    const bool prefetch = FINEST && a.levels <= kPre + 1;
+    // the finest level's combination inputs, requested once the gathered registers are free; their
+    // latency overlaps the softmax and the messages
+    if constexpr (FINEST) {
+        if (prefetch) {                                      // uniform
+            const int L = a.levels;
+#pragma unroll
+            for (int lev = 1; lev <= kPre; ++lev) {
+                const int lv = lev < L ? lev : L - 1;        // >= 1: the finest level has L >= 2
+                const size_t an = static_cast<size_t>(b) * a.lvl_N[lv] +
+                                  static_cast<size_t>((2 * Py) >> lv) * a.lvl_W[lv] + ((2 * Px) >> lv);
+                anc[lev - 1] = a.coarser_msg[lv][(an * a.heads + h) * D + ch];   // ancestors shared by siblings
+            }
+            if (!VA && a.w) {                                // uniform
+#pragma unroll
+                for (int u = 0; u < QPL; ++u) {
+                    const int qi = (NH == 2 ? hh * QPL : 0) + u;
+                    const int wy = min(2 * Py + (qi >> 1), H - 1), wx = min(2 * Px + (qi & 1), W - 1);
+                    const float* wrow = a.w + ((static_cast<size_t>(b) * N + wy * W + wx) * a.heads + h) * L;
+#pragma unroll
+                    for (int lev = 0; lev <= kPre; ++lev) wq[u][lev] = wrow[lev < L ? lev : L - 1];
+                }
+            }
+        }
     }
     float x[4];
 #pragma unroll
