@@ -37,7 +37,8 @@
  *     workspace QTA_ERR_WORKSPACE; a failed launch returns QTA_ERR_HIP. Faults that happen on
  *     the device surface at the caller's next synchronisation.
  *   - Supported: d in {32, 64}; 1 <= K <= QTA_MAX_K; coarsest level N_{L-1} <= QTA_MAX_COARSE;
- *     1 <= L <= QTA_MAX_LEVELS with no level above a 1x1 map; token pointers 16-byte aligned.
+ *     1 <= L <= QTA_MAX_LEVELS with no level above a 1x1 map; token pointers 16-byte aligned;
+ *     per batch element fewer than 2^24 tokens and 2^31 bytes in the token map (attention calls).
  *   - K larger than a query's candidate count is not an error: min(K, count) keys are kept.
  *   - Inputs must be finite; outputs must not alias inputs. Calls are re-entrant: the library
  *     holds no state.

@@ -93,13 +93,14 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     const int wpb = blockDim.x >> 6;
     const int Np = a.Hp * a.Wp;
     const long long nitems = static_cast<long long>(a.B) * a.heads * Np;
-    const long long item = static_cast<long long>(xcd_remap(blockIdx.x, gridDim.x)) * wpb + wave;
+    // the work item is the same for the whole wave: keep it (and all that derives from it) scalar
+    const int item = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, gridDim.x) * wpb + wave);
     if (item >= nitems) return;            // whole wave leaves; only wave-level syncs follow
 
-    const int h = static_cast<int>(item % a.heads);
-    const long long bp = item / a.heads;
-    const int P = static_cast<int>(bp % Np);
-    const int b = static_cast<int>(bp / Np);
+    const int h = item % a.heads;
+    const int bp = item / a.heads;
+    const int P = bp % Np;
+    const int b = bp / Np;
     const int Py = P / a.Wp, Px = P - Py * a.Wp;
     const int H = a.H, W = a.W, C = a.C, K = a.K;
     const int N = H * W;
@@ -112,13 +113,14 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     unsigned char* Vb = base + lay.v;
     unsigned char* Pb = base + lay.p;
 
-    const size_t prow = ((static_cast<size_t>(b) * a.heads + h) * Np + P) * K;
-    // flat index at level l of child (s & 3) of kept key J (a level l+1 index), or -1
+    const int32_t* prow = a.parent_idx + ((static_cast<size_t>(b) * a.heads + h) * Np + P) * K;
+    // flat index at level l of child (s & 3) of kept key J (a level l+1 index), or -1. Map sizes are
+    // below 2^24 tokens, so coordinate products fit the 24-bit multiplier.
     auto child_of_slot_J = [&](int J, int s) -> int {
         if (s >= nslot || J < 0) return -1;
-        const int Jy = J / a.Wp, Jx = J - Jy * a.Wp;
+        const int Jy = fast_div(J, a.div_Wp), Jx = J - __mul24(Jy, a.Wp);
         const int cy = 2 * Jy + ((s >> 1) & 1), cx = 2 * Jx + (s & 1);
-        return (cy < H && cx < W) ? cy * W + cx : -1;
+        return (cy < H && cx < W) ? __mul24(cy, W) + cx : -1;
     };
 
     // ---- 1. loads. Vector memory counters drain in order, and a load inside a divergent branch
@@ -130,12 +132,15 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     // phase A: the parents' kept keys (own slot and this lane's gather slot of each tile), the
     // parents' scores (A) and the query chunks (A operand: row n16 holds query n16 & 3)
     const int last_sel = K - 1;
-    const int J_own_raw = a.parent_idx[prow + min(lane >> 2, last_sel)];
     int J_g[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) J_g[t] = a.parent_idx[prow + min(4 * t + (n16 >> 2), last_sel)];
+    for (int t = 0; t < NT; ++t) J_g[t] = prow[min(4 * t + (n16 >> 2), last_sel)];
+    // lane = slot 16g + n16 belongs to kept key 4g + (n16 >> 2): tile g's gather key
+    int J_own_raw = -1;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) J_own_raw = g == t ? J_g[t] : J_own_raw;
     float pkey = 0.f;
-    if constexpr (VA) pkey = a.parent_key[prow + min(lane >> 2, last_sel)];
+    if constexpr (VA) pkey = a.parent_key[((static_cast<size_t>(b) * a.heads + h) * Np + P) * K + min(lane >> 2, last_sel)];
     uint4 qa[NJ];
     bool q_ok;
     {
@@ -143,20 +148,24 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
         const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
         q_ok = qy < H && qx < W;
         const int qyc = qy < H ? qy : H - 1, qxc = qx < W ? qx : W - 1;
-        const size_t qoff = a.q_blocked ? (((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 + qi) * RB
-                                        : ((static_cast<size_t>(b) * N + qyc * W + qxc) * C + h * D) * TB;
-        const unsigned char* qrow = static_cast<const unsigned char*>(a.q) + qoff;
+        // uniform base of this (batch, head) plus a 32-bit per-lane offset
+        const unsigned char* qbase = static_cast<const unsigned char*>(a.q) +
+            (a.q_blocked ? ((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 * RB
+                         : (static_cast<size_t>(b) * N * C + h * D) * TB);
+        const uint32_t qoff = a.q_blocked ? static_cast<uint32_t>(qi * RB)
+                                          : static_cast<uint32_t>(__mul24(qyc, W) + qxc) * static_cast<uint32_t>(C * TB);
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) qa[j] = *reinterpret_cast<const uint4*>(qrow + (g + 4 * j) * 16);
+        for (int j = 0; j < NJ; ++j)
+            qa[j] = *reinterpret_cast<const uint4*>(qbase + (qoff + static_cast<uint32_t>((g + 4 * j) * 16)));
     }
     // phase B: the gathers. NHWC: child f of this head at kg + f*C*TB. Blocked: the four children
     // of kept key J are the 4*RB bytes at kg + J*4*RB (this (batch, head)'s blocks start at kg).
     const bool kvb = a.kv_blocked;
     const size_t kv_base = kvb ? (static_cast<size_t>(b) * a.heads + h) * Np * 4 * RB
                                : (static_cast<size_t>(b) * N * C + h * D) * TB;
-    const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base + g * 16;
-    const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base + g * 16;
-    const size_t tok_bytes = static_cast<size_t>(C) * TB;
+    const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base;
+    const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base;
+    const uint32_t tok_bytes = static_cast<uint32_t>(C * TB);
     bool gok[NT];
     uint4 kc[kTB][NJ], vc[kTB][NJ];
     auto load_tiles = [&](int t0) {
@@ -166,11 +175,13 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
             if (t >= NT || t >= ntile) break;                 // uniform
             const int f = child_of_slot_J(J_g[t], s);
             gok[t] = f >= 0;
-            const size_t goff = !gok[t] ? 0 : (kvb ? (static_cast<size_t>(J_g[t]) * 4 + (s & 3)) * RB : f * tok_bytes);
+            // 32-bit byte offset within this (batch, head)'s map (below 2^31 by the host's checks)
+            const uint32_t goff = (!gok[t] ? 0u : (kvb ? static_cast<uint32_t>(J_g[t] * 4 + (s & 3)) * RB
+                                                        : static_cast<uint32_t>(f) * tok_bytes)) + g * 16;
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
-                kc[i][j] = *reinterpret_cast<const uint4*>(kg + goff + 64 * j);
-                vc[i][j] = *reinterpret_cast<const uint4*>(vg + goff + 64 * j);
+                kc[i][j] = *reinterpret_cast<const uint4*>(kg + (goff + 64 * j));
+                vc[i][j] = *reinterpret_cast<const uint4*>(vg + (goff + 64 * j));
             }
         }
     };
@@ -235,8 +246,8 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     const int cg = blk / NH, hh = blk % NH;
     const int ch = 4 * cg + t4;
     constexpr int kPre = FINEST ? kPrefetchLevels : 1;
-    float anc[kPre] = {};
-    float wq[FINEST ? QPL : 1][kPre + 1] = {};
+    float anc[kPre];
+    float wq[FINEST ? QPL : 1][kPre + 1];
     const bool prefetch = FINEST && a.levels <= kPre + 1;
     // the finest level's combination inputs, requested once the gathered registers are free; their
     // latency overlaps the softmax and the messages
@@ -245,19 +256,24 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
             const int L = a.levels;
 #pragma unroll
             for (int lev = 1; lev <= kPre; ++lev) {
-                const int lv = lev < L ? lev : L - 1;        // >= 1: the finest level has L >= 2
-                const size_t an = static_cast<size_t>(b) * a.lvl_N[lv] +
-                                  static_cast<size_t>((2 * Py) >> lv) * a.lvl_W[lv] + ((2 * Px) >> lv);
-                anc[lev - 1] = a.coarser_msg[lv][(an * a.heads + h) * D + ch];   // ancestors shared by siblings
+                if (lev >= L) break;                         // uniform
+                // the ancestor is shared by the four siblings: a uniform address plus the channel
+                const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
+                                  static_cast<size_t>((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev);
+                anc[lev - 1] = (a.coarser_msg[lev] + (an * a.heads + h) * D)[ch];
             }
             if (!VA && a.w) {                                // uniform
+                const float* wb = a.w + (static_cast<size_t>(b) * N * a.heads + h) * L;
 #pragma unroll
                 for (int u = 0; u < QPL; ++u) {
                     const int qi = (NH == 2 ? hh * QPL : 0) + u;
                     const int wy = min(2 * Py + (qi >> 1), H - 1), wx = min(2 * Px + (qi & 1), W - 1);
-                    const float* wrow = a.w + ((static_cast<size_t>(b) * N + wy * W + wx) * a.heads + h) * L;
+                    const float* wrow = wb + static_cast<uint32_t>(__mul24(wy, W) + wx) * static_cast<uint32_t>(a.heads * L);
 #pragma unroll
-                    for (int lev = 0; lev <= kPre; ++lev) wq[u][lev] = wrow[lev < L ? lev : L - 1];
+                    for (int lev = 0; lev <= kPre; ++lev) {
+                        if (lev >= L) break;                 // uniform
+                        wq[u][lev] = wrow[lev];
+                    }
                 }
             }
         }
@@ -359,10 +375,12 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
         const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
         if (qy >= H || qx >= W) continue;
         const float m = pick4(o, qi) * pick4(inv_sum, qi);
-        const size_t qtok = static_cast<size_t>(b) * N + qy * W + qx;
+        const uint32_t qpos = static_cast<uint32_t>(__mul24(qy, W) + qx);      // token within the map
         if constexpr (!FINEST) {
-            a.msg[(qtok * a.heads + h) * D + ch] = m;
+            float* mb = a.msg + (static_cast<size_t>(b) * N * a.heads + h) * D;  // uniform
+            mb[qpos * static_cast<uint32_t>(a.heads * D) + ch] = m;
         } else {
+            const size_t qtok = static_cast<size_t>(b) * N + qpos;
             const int L = a.levels;
             const float wdef = 1.0f / L;
             float out;
@@ -383,7 +401,8 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
                     out += wl * a.coarser_msg[lev][(an * a.heads + h) * D + ch];
                 }
             }
-            S::store1(a.out, qtok * C + h * D + ch, out);
+            void* ob = static_cast<unsigned char*>(a.out) + (static_cast<size_t>(b) * N * C + h * D) * TB;  // uniform
+            S::store1(ob, qpos * static_cast<uint32_t>(C) + ch, out);
         }
     }
 }
@@ -405,7 +424,7 @@ hipError_t launch_one(const FineArgs& a, hipStream_t stream)
     }
     const long long items = static_cast<long long>(a.B) * a.heads * a.Hp * a.Wp;
     const long long blocks = (items + wpb - 1) / wpb;
-    if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    if (blocks * wpb >= 0x7FFFFFFFLL) return hipErrorInvalidValue;     // work items are int
     hipLaunchKernelGGL((fine_attn_kernel<T, D, NSP, VA, FINEST>), dim3(static_cast<unsigned>(blocks)),
                        dim3(wpb * kWave), wpb * wave_bytes, stream, a);
     return hipGetLastError();
@@ -432,12 +451,14 @@ hipError_t launch_td(const FineArgs& a, bool variant_a, bool finest, hipStream_t
 hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool bf16_in, bool finest, hipStream_t stream)
 {
     if (4 * a.K > kMaxSlots) return launch_fine_attn_wide(a, d, variant_a, bf16_in, finest, stream);
+    FineArgs b = a;
+    b.div_Wp = make_fastdiv(a.Wp);
     if (bf16_in) {
-        if (d == 32) return launch_td<bf16, 32>(a, variant_a, finest, stream);
-        if (d == 64) return launch_td<bf16, 64>(a, variant_a, finest, stream);
+        if (d == 32) return launch_td<bf16, 32>(b, variant_a, finest, stream);
+        if (d == 64) return launch_td<bf16, 64>(b, variant_a, finest, stream);
     } else {
-        if (d == 32) return launch_td<float, 32>(a, variant_a, finest, stream);
-        if (d == 64) return launch_td<float, 64>(a, variant_a, finest, stream);
+        if (d == 32) return launch_td<float, 32>(b, variant_a, finest, stream);
+        if (d == 64) return launch_td<float, 64>(b, variant_a, finest, stream);
     }
     return hipErrorInvalidValue;
 }

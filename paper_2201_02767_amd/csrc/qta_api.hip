@@ -50,6 +50,16 @@ qta_status check_problem(int B, int heads, int d, int K, qta_variant variant, qt
     return QTA_OK;
 }
 
+// One batch element's token map must stay below 2^24 tokens and 2^31 bytes: the attention
+// kernels address it with 32-bit offsets and 24-bit coordinate products.
+qta_status map_ok(int H, int W, int heads, int d, qta_dtype dtype)
+{
+    const long long n = static_cast<long long>(H) * W;
+    if (n >= (1LL << 24)) return QTA_ERR_UNSUPPORTED;
+    if (n * heads * d * static_cast<long long>(dtype_bytes(dtype)) >= (1LL << 31)) return QTA_ERR_UNSUPPORTED;
+    return QTA_OK;
+}
+
 // Intermediate levels (produced by the pyramid, gathered by the next finer level) are stored
 // parent-blocked when the fine kernels take the blocked path (4K <= 64). The input level stays
 // NHWC: a blocked copy of it would cost a write and a read of k and v for no gain in the gathers.
@@ -63,6 +73,8 @@ qta_status layout(int B, int heads, int H, int W, int d, int levels, int K, qta_
     st = dims(H, W, levels, Hl, Wl);
     if (st != QTA_OK) return st;
     if (static_cast<long long>(Hl[levels - 1]) * Wl[levels - 1] > QTA_MAX_COARSE) return QTA_ERR_UNSUPPORTED;
+    st = map_ok(H, W, heads, d, dtype);
+    if (st != QTA_OK) return st;
     *L = qta_workspace_layout{};
     L->levels = levels;
     const int C = heads * d;
@@ -238,7 +250,8 @@ qta_status qta_fine_attn(const void* ql, const void* kl, const void* vl, int B, 
     if (variant == QTA_VARIANT_A && !parent_key) return QTA_ERR_INVALID;
     if (!aligned16(ql) || !aligned16(kl) || !aligned16(vl) || !aligned16(msg)) return QTA_ERR_INVALID;
     if (Hl <= 0 || Wl <= 0 || (Hl == 1 && Wl == 1)) return QTA_ERR_INVALID;
-    if (static_cast<long long>(Hl) * Wl > 0x3FFFFFFFLL) return QTA_ERR_UNSUPPORTED;
+    st = map_ok(Hl, Wl, heads, d, dtype);
+    if (st != QTA_OK) return st;
     FineArgs a{};
     a.q = ql;
     a.k = kl;
@@ -274,6 +287,8 @@ qta_status qta_finest_attn(const void* q0, const void* k0, const void* v0, int B
     if (levels < 2) return QTA_ERR_INVALID;
     int Hl[QTA_MAX_LEVELS], Wl[QTA_MAX_LEVELS];
     st = dims(H, W, levels, Hl, Wl);
+    if (st != QTA_OK) return st;
+    st = map_ok(H, W, heads, d, dtype);
     if (st != QTA_OK) return st;
     FineArgs a{};
     a.q = q0;

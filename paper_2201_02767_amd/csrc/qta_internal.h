@@ -66,6 +66,32 @@ struct CoarseArgs {
     int levels;
 };
 
+// Division of 0 <= n < 2^31 by a fixed divisor d >= 1 with one high multiply and a shift:
+// q = (umulhi(n, m) + n) >> s, s = ceil(log2 d), m = floor(2^(32+s) / d) - 2^32 + 1 (the round-up
+// method of Granlund and Montgomery, "Division by invariant integers using multiplication",
+// PLDI 1994). umulhi(n, m) <= n, so the sum stays below 2^32.
+struct FastDiv {
+    uint32_t m;
+    int s;
+    int d;
+};
+
+inline FastDiv make_fastdiv(int d)
+{
+    int s = 0;
+    while ((1LL << s) < d) ++s;
+    const unsigned __int128 one = 1;
+    const uint64_t m = static_cast<uint64_t>(((one << (32 + s)) / static_cast<unsigned>(d)) - (one << 32) + 1);
+    return FastDiv{static_cast<uint32_t>(m), s, d};
+}
+
+__host__ __device__ __forceinline__ int fast_div(int n, const FastDiv& f)
+{
+    const uint32_t u = static_cast<uint32_t>(n);
+    const uint32_t hi = static_cast<uint32_t>((static_cast<uint64_t>(u) * f.m) >> 32);
+    return static_cast<int>((hi + u) >> f.s);
+}
+
 struct FineArgs {
     const void* q;
     const void* k;
@@ -73,6 +99,7 @@ struct FineArgs {
     bool q_blocked;             // queries of this level stored blocked (else NHWC)
     bool kv_blocked;            // keys and values of this level stored blocked (else NHWC)
     int B, heads, H, W, Hp, Wp, C, K;
+    FastDiv div_Wp;             // division by Wp (flat parent index -> row)
     float scale;
     const int32_t* parent_idx;
     const float* parent_key;

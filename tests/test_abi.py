@@ -5,6 +5,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 import torch
 
@@ -115,6 +116,9 @@ def test_forward_validation():
     assert _fwd(lib, K=65) == UNSUPPORTED
     assert _fwd(lib, H=64, W=64, L=1) == UNSUPPORTED        # coarsest level above the cap
     assert _fwd(lib, H=64, W=64, L=2) == WORKSPACE          # 32x32 = 1024 coarse tokens is allowed
+    assert _fwd(lib, H=4096, W=4096, L=8) == UNSUPPORTED    # 2^24 tokens in one map
+    assert _fwd(lib, H=2048, W=4096, heads=32, L=8) == UNSUPPORTED   # 2^31 bytes in one map
+    assert _fwd(lib, H=2048, W=4096, L=8) == WORKSPACE
 
 
 def test_stage_validation():
@@ -154,3 +158,28 @@ def test_binding_refuses_cpu_tensors():
     x = torch.zeros(1, 4, 4, 1, 32)
     with pytest.raises(ValueError):
         P.forward(x, x, x, levels=2, K=1, variant="B")
+
+
+def _fastdiv_params(d):
+    # the divisor parameters the library derives on the host (round-up multiply-high division)
+    s = 0
+    while (1 << s) < d:
+        s += 1
+    m = (1 << (32 + s)) // d - (1 << 32) + 1
+    return m, s
+
+
+@pytest.mark.parametrize("d", list(range(1, 70)) + [99, 127, 128, 129, 168, 1000, 4095, 4096, 4097, 65535, 1 << 20,
+                                                      (1 << 23) + 1])
+def test_fast_division_parameters_are_exact(d):
+    """Quotients by multiply-high + shift equal floor division for every index the kernels divide:
+    0 <= n < 2^24 (map sizes are below 2^24 tokens), checked at the edges and on a random sample."""
+    m, s = _fastdiv_params(d)
+    assert 0 <= m < (1 << 32)
+    rng = np.random.default_rng(d)
+    n = np.concatenate([np.arange(0, 4 * d + 8), rng.integers(0, 1 << 24, 4096), [(1 << 24) - 1, (1 << 31) - 1],
+                        np.arange(max(0, (1 << 24) - 3 * d), 1 << 24, max(1, d // 7))]).astype(np.uint64)
+    hi = (n * np.uint64(m)) >> np.uint64(32)
+    q = (hi + n) >> np.uint64(s)
+    assert np.all(hi + n < (1 << 32))
+    assert np.array_equal(q, n // np.uint64(d))
