@@ -1,12 +1,14 @@
 // Step 1: token pyramids by 2x2 average pooling (Sec. 3.2, pyramid paragraph).
 //
-// One pass produces up to two coarser levels from a source level. A thread owns one 16-byte
-// channel chunk of one token of the top level it produces: it issues the 16-byte loads of that
-// token's (up to) 4x4 source tokens all at once (consecutive threads take consecutive chunks of a
-// token, so a wave reads whole rows; addresses past the map's edge are clamped onto it and the
-// values ignored), writes the (up to) four intermediate tokens, then pools those rounded values
-// again for the top token. Two levels per pass read each map once; deeper pyramids take more
-// passes. Each level is written NHWC or parent-blocked as asked.
+// One pass produces up to two coarser levels from a source level. In the two-level pass a
+// workgroup owns whole top-level tokens: one thread per 16-byte channel chunk of each of their four
+// level-1 children loads that child's 2x2 source chunks (consecutive threads take consecutive
+// chunks of a token, so a wave reads whole rows; addresses past the map's edge are clamped onto
+// it and the values ignored), writes the level-1 token and stages it in LDS; after a barrier one
+// thread in four pools the staged children again for the top token. Tokens too wide for one
+// workgroup take the older path in which one thread owns a top-token chunk and loads all 4x4
+// source chunks. Deeper pyramids take more passes. Each level is written NHWC or parent-blocked
+// as asked.
 //
 // Arithmetic, fixed so that every implementation stores the same bits: the valid children are
 // summed in fp32 as ((c00 + c01) + (c10 + c11)) with missing children left out, multiplied by
@@ -112,10 +114,86 @@ __global__ __launch_bounds__(256) void pyramid_pass_kernel(PyramidPassArgs a)
     }
 }
 
+// Two-level pass, workgroup = tpb top tokens x 4 children x `chunks` chunks (at most 256 threads).
+template <typename T>
+__global__ __launch_bounds__(256) void pyramid_pass2_kernel(PyramidPassArgs a, int tpb)
+{
+    using S = Storage<T>;
+    constexpr int E = S::kPer16B;
+    __shared__ uint4 stage[256];
+    const int tensor = blockIdx.y;
+    const char* __restrict__ src = static_cast<const char*>(a.src[tensor]);
+    char* __restrict__ dst1 = static_cast<char*>(a.dst1[tensor]);
+    char* __restrict__ dst2 = static_cast<char*>(a.dst2[tensor]);
+    const int chunks = a.chunks;
+    const int li = threadIdx.x;
+    const int ch = li % chunks;
+    const int q = (li / chunks) & 3;
+    const int t = li / (4 * chunks);
+    const long long ntop = static_cast<long long>(a.B) * a.H2 * a.W2;
+    const long long top = static_cast<long long>(blockIdx.x) * tpb + t;
+    const bool active = top < ntop;                    // inactive threads still reach the barrier
+    const long long topc = active ? top : ntop - 1;
+    const int X = static_cast<int>(topc % a.W2);
+    const int Y = static_cast<int>((topc / a.W2) % a.H2);
+    const int b = static_cast<int>(topc / (static_cast<long long>(a.W2) * a.H2));
+
+    const int y1 = 2 * Y + (q >> 1), x1 = 2 * X + (q & 1);
+    const bool mid_ok = y1 < a.H1 && x1 < a.W1;
+    uint4 raw[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int y = min(2 * y1 + i, a.Hs - 1);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int x = min(2 * x1 + j, a.Ws - 1);
+            raw[i][j] = *reinterpret_cast<const uint4*>(
+                src + chunk_offset(a.src_blocked, b, y, x, a.Hs, a.Ws, ch, chunks, a.head_chunks));
+        }
+    }
+    float c00[E], c01[E], c10[E], c11[E], mid[E];
+    S::unpack(raw[0][0], c00);
+    S::unpack(raw[0][1], c01);
+    S::unpack(raw[1][0], c10);
+    S::unpack(raw[1][1], c11);
+    pool_children<E>(c00, c01, c10, c11, 2 * x1 + 1 < a.Ws, 2 * y1 + 1 < a.Hs, mid);
+#pragma unroll
+    for (int e = 0; e < E; ++e) mid[e] = S::round(mid[e]);
+    const uint4 packed = S::pack(mid);
+    if (active && mid_ok)
+        *reinterpret_cast<uint4*>(dst1 + chunk_offset(a.dst1_blocked, b, y1, x1, a.H1, a.W1, ch, chunks,
+                                                      a.head_chunks)) = packed;
+    stage[li] = packed;
+    __syncthreads();
+    if (!active || q != 0) return;
+    const int base = t * 4 * chunks + ch;
+    float m0[E], m1[E], m2[E], m3[E], o[E];
+    S::unpack(stage[base], m0);
+    S::unpack(stage[base + chunks], m1);
+    S::unpack(stage[base + 2 * chunks], m2);
+    S::unpack(stage[base + 3 * chunks], m3);
+    pool_children<E>(m0, m1, m2, m3, 2 * X + 1 < a.W1, 2 * Y + 1 < a.H1, o);
+#pragma unroll
+    for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
+    *reinterpret_cast<uint4*>(dst2 + chunk_offset(a.dst2_blocked, b, Y, X, a.H2, a.W2, ch, chunks, a.head_chunks)) =
+        S::pack(o);
+}
+
 }  // namespace
 
 hipError_t launch_pyramid_pass(const PyramidPassArgs& a, int nlev, int ntensors, bool use_bf16, hipStream_t stream)
 {
+    if (nlev == 2 && 4 * a.chunks <= 256) {
+        const int tpb = 256 / (4 * a.chunks);
+        const long long ntop = static_cast<long long>(a.B) * a.H2 * a.W2;
+        const long long blocks = (ntop + tpb - 1) / tpb;
+        if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+        dim3 grid(static_cast<unsigned>(blocks), ntensors);
+        const dim3 block(tpb * 4 * a.chunks);
+        if (use_bf16) hipLaunchKernelGGL((pyramid_pass2_kernel<bf16>), grid, block, 0, stream, a, tpb);
+        else hipLaunchKernelGGL((pyramid_pass2_kernel<float>), grid, block, 0, stream, a, tpb);
+        return hipGetLastError();
+    }
     const int Ht = nlev == 2 ? a.H2 : a.H1, Wt = nlev == 2 ? a.W2 : a.W1;
     const long long total = static_cast<long long>(a.B) * Ht * Wt * a.chunks;
     const int threads = 256;

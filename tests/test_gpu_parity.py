@@ -93,6 +93,8 @@ def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=No
 @pytest.mark.parametrize("dtype,B,H,W,C,L", [
     ("f32", 1, 16, 16, 32, 3), ("bf16", 2, 25, 42, 64, 5), ("f32", 1, 15, 13, 256, 4), ("bf16", 1, 1, 9, 64, 4),
     ("f32", 3, 37, 53, 96, 6), ("bf16", 2, 200, 336, 64, 5), ("f32", 1, 60, 80, 256, 3),
+    # 16 top tokens per workgroup; tokens too wide for the staged pass (80 chunks, fp32 and bf16)
+    ("bf16", 1, 33, 17, 32, 4), ("f32", 1, 19, 23, 320, 4), ("bf16", 2, 9, 11, 640, 3),
 ])
 def test_pyramid_bit_exact(dev, dtype, B, H, W, C, L):
     rng = np.random.default_rng(H * W + C)
