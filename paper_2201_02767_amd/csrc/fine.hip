@@ -1,410 +1,27 @@
-// Steps 3-5 at the finer levels: gathered attention over the children of the parent's kept keys
-// (Sec. 3.2, Fig. 1), QuadTree-A scores (Eq. 4) or QuadTree-B softmax (Eq. 6), the next level's
-// top-K, and at level 0 the combination of all levels' messages (Eqs. 2 and 5).
-//
-// Work item = one parent query P at level l+1 and one head. Its four children at level l are
-// sibling queries with one shared candidate set: the 2x2 children of the K keys P kept (4K <= 64
-// candidates here; larger K runs the kernel of fine_wide.hip). One wave owns one item; candidate
-// slot s = 4r + c is child c, in the order (0,0),(0,1),(1,0),(1,1), of kept key r, and the slots
-// are taken in tiles of 16:
-//   1. the candidates' key and value rows of this head are gathered once for the four queries with
-//      16-byte loads: lane 16g + n loads chunks g, g+4, ... of the row of slot n of each tile, so
-//      one instruction reads 16 whole rows. The value rows go to wave-private LDS (transposed for
-//      bf16); the key rows stay in registers;
-//   2. logits on the 16x16 MFMA straight from those registers: the key chunks are the B operand,
-//      the four queries, repeated over the 16 rows, the A operand (the d channels are contracted in
-//      the order the chunks arrive, the same for both operands). Every lane group then holds all
-//      four logits of its slot column for every tile, and lane 16g + n keeps tile g, so lane s ends
-//      with the four logits of slot s;
-//   3. B: a softmax per query over the wave (DPP and permlane butterflies, no LDS);
-//      A: a softmax over each lane quad (the children of one kept key) times the parent's score;
-//   4. levels above 0: the K best candidates of each query by a bitwise radix select on wave
-//      ballots (ties at the cut to the lower flat index); A drops their weight from its message;
-//   5. messages m = P V on the 4x4 MFMA, blocks split over 4-channel groups (and slot halves);
-//   6. levels above 0 store m; level 0 adds the ancestors' messages (times w for B) and stores the
-//      output in the storage type.
-// A workgroup holds four independent waves; nothing synchronises across waves.
-#include "qta_device.h"
-#include "qta_internal.h"
+// Gathered fine attention at the finer levels: one wave per (parent query, head) work item; the
+// per-item work (gather, MFMA logits, softmax, top-K, messages, the finest level's combination) is
+// fine_item in fine_item.h. A workgroup holds four independent waves; nothing synchronises across
+// waves. Candidate sets of more than 64 slots run the kernel of fine_wide.hip.
+#include "fine_item.h"
 
 namespace qta {
 
 namespace {
 
-typedef short short4_t __attribute__((ext_vector_type(4)));
-typedef float float4_t __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-
-constexpr int kMaxSlots = 64;
-constexpr int kPrefetchLevels = 4;    // the finest level prefetches up to this many ancestors
-
-// Byte layout of one wave's LDS region for nsp padded slots (a multiple of 16): the value rows
-// and the weights P.
-struct WaveLds {
-    int v, p, total;
-    int vpitch;    // bf16: elements per transposed value row; fp32: floats per value row
-};
-
-template <typename T, int D>
-__host__ __device__ inline WaveLds wave_lds(int nsp)
-{
-    constexpr int TB = sizeof(T);
-    WaveLds L;
-    L.v = 0;
-    int vbytes;
-    if (TB == 2) {
-        L.vpitch = nsp + 8;                 // Vt[channel][slot]
-        vbytes = D * L.vpitch * 2;
-    } else {
-        L.vpitch = D + 4;                   // Vs[slot][channel]
-        vbytes = nsp * L.vpitch * 4;
-    }
-    L.p = L.v + vbytes;
-    L.total = (L.p + 4 * nsp * TB + 15) / 16 * 16;
-    return L;
-}
-
-__device__ __forceinline__ float pick4(const float4_t& v, int i)
-{
-    return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
-}
-
-__device__ __forceinline__ float pick4(const float (&v)[4], int i)
-{
-    return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
-}
+using namespace fine;
 
 template <typename T, int D, int NSP, bool VA, bool FINEST>
 __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
 {
-    using S = Storage<T>;
-    constexpr bool kBf16 = sizeof(T) == 2;
-    constexpr int TB = sizeof(T);
-    constexpr int RB = D * TB;             // bytes of one head's row
-    constexpr int E = S::kPer16B;          // elements per 16-byte chunk
-    constexpr int NJ = RB / 64;            // 16-byte chunks per lane and row (lane group g: g, g+4, ...)
-    constexpr int NT = NSP / 16;           // slot tiles (upper bound)
-    constexpr int kTB = (8 / NJ) < NT ? (8 / NJ) : NT;   // tiles whose rows are in registers at once
-    constexpr int NCG = D / 4;             // PV: 4-channel groups
-    constexpr int NH = 16 / NCG;           // PV: slot halves (2 for d = 32, 1 for d = 64)
-    constexpr int QPL = 4 / NH;            // output queries per lane
-
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wave = threadIdx.x >> 6;
     const int wpb = blockDim.x >> 6;
-    const int Np = a.Hp * a.Wp;
-    const long long nitems = static_cast<long long>(a.B) * a.heads * Np;
+    const long long nitems = static_cast<long long>(a.B) * a.heads * a.Hp * a.Wp;
     // the work item is the same for the whole wave: keep it (and all that derives from it) scalar
     const int item = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, gridDim.x) * wpb + wave);
     if (item >= nitems) return;            // whole wave leaves; only wave-level syncs follow
-
-    const int h = item % a.heads;
-    const int bp = item / a.heads;
-    const int P = bp % Np;
-    const int b = bp / Np;
-    const int Py = P / a.Wp, Px = P - Py * a.Wp;
-    const int H = a.H, W = a.W, C = a.C, K = a.K;
-    const int N = H * W;
-    const int nslot = 4 * K;
-    const int nsp = (nslot + 15) & ~15;                // <= NSP
-
     extern __shared__ __align__(16) unsigned char smem[];
-    const WaveLds lay = wave_lds<T, D>(nsp);
-    unsigned char* base = smem + static_cast<size_t>(wave) * lay.total;
-    unsigned char* Vb = base + lay.v;
-    unsigned char* Pb = base + lay.p;
-
-    const int32_t* prow = a.parent_idx + ((static_cast<size_t>(b) * a.heads + h) * Np + P) * K;
-    // flat index at level l of child (s & 3) of kept key J (a level l+1 index), or -1. Map sizes are
-    // below 2^24 tokens, so coordinate products fit the 24-bit multiplier.
-    auto child_of_slot_J = [&](int J, int s) -> int {
-        if (s >= nslot || J < 0) return -1;
-        const int Jy = fast_div(J, a.div_Wp), Jx = J - __mul24(Jy, a.Wp);
-        const int cy = 2 * Jy + ((s >> 1) & 1), cx = 2 * Jx + (s & 1);
-        return (cy < H && cx < W) ? __mul24(cy, W) + cx : -1;
-    };
-
-    // ---- 1. loads. Vector memory counters drain in order, and a load inside a divergent branch
-    //      makes the compiler wait for it at the join, so every load below is unconditional, at a
-    //      clamped address that is always in bounds, with validity applied when the value is used.
-    //      Phase A holds every load that needs no other load; phase B the gathers. ----
-    const int n16 = lane & 15, g = lane >> 4;
-    const int ntile = nsp / 16;
-    // phase A: the parents' kept keys (own slot and this lane's gather slot of each tile), the
-    // parents' scores (A) and the query chunks (A operand: row n16 holds query n16 & 3)
-    const int last_sel = K - 1;
-    int J_g[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) J_g[t] = prow[min(4 * t + (n16 >> 2), last_sel)];
-    // lane = slot 16g + n16 belongs to kept key 4g + (n16 >> 2): tile g's gather key
-    int J_own_raw = -1;
-#pragma unroll
-    for (int t = 0; t < NT; ++t) J_own_raw = g == t ? J_g[t] : J_own_raw;
-    float pkey = 0.f;
-    if constexpr (VA) pkey = a.parent_key[((static_cast<size_t>(b) * a.heads + h) * Np + P) * K + min(lane >> 2, last_sel)];
-    uint4 qa[NJ];
-    bool q_ok;
-    {
-        const int qi = n16 & 3;
-        const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
-        q_ok = qy < H && qx < W;
-        const int qyc = qy < H ? qy : H - 1, qxc = qx < W ? qx : W - 1;
-        // uniform base of this (batch, head) plus a 32-bit per-lane offset
-        const unsigned char* qbase = static_cast<const unsigned char*>(a.q) +
-            (a.q_blocked ? ((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 * RB
-                         : (static_cast<size_t>(b) * N * C + h * D) * TB);
-        const uint32_t qoff = a.q_blocked ? static_cast<uint32_t>(qi * RB)
-                                          : static_cast<uint32_t>(__mul24(qyc, W) + qxc) * static_cast<uint32_t>(C * TB);
-#pragma unroll
-        for (int j = 0; j < NJ; ++j)
-            qa[j] = *reinterpret_cast<const uint4*>(qbase + (qoff + static_cast<uint32_t>((g + 4 * j) * 16)));
-    }
-    // phase B: the gathers. NHWC: child f of this head at kg + f*C*TB. Blocked: the four children
-    // of kept key J are the 4*RB bytes at kg + J*4*RB (this (batch, head)'s blocks start at kg).
-    const bool kvb = a.kv_blocked;
-    const size_t kv_base = kvb ? (static_cast<size_t>(b) * a.heads + h) * Np * 4 * RB
-                               : (static_cast<size_t>(b) * N * C + h * D) * TB;
-    const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base;
-    const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base;
-    const uint32_t tok_bytes = static_cast<uint32_t>(C * TB);
-    bool gok[NT];
-    uint4 kc[kTB][NJ], vc[kTB][NJ];
-    auto load_tiles = [&](int t0) {
-#pragma unroll
-        for (int i = 0; i < kTB; ++i) {
-            const int t = t0 + i, s = 16 * t + n16;
-            if (t >= NT || t >= ntile) break;                 // uniform
-            const int f = child_of_slot_J(J_g[t], s);
-            gok[t] = f >= 0;
-            // 32-bit byte offset within this (batch, head)'s map (below 2^31 by the host's checks)
-            const uint32_t goff = (!gok[t] ? 0u : (kvb ? static_cast<uint32_t>(J_g[t] * 4 + (s & 3)) * RB
-                                                        : static_cast<uint32_t>(f) * tok_bytes)) + g * 16;
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                kc[i][j] = *reinterpret_cast<const uint4*>(kg + (goff + 64 * j));
-                vc[i][j] = *reinterpret_cast<const uint4*>(vg + (goff + 64 * j));
-            }
-        }
-    };
-    load_tiles(0);
-    const int flat = child_of_slot_J(lane < nslot ? J_own_raw : -1, lane);
-    const bool ok = flat >= 0;
-
-    // ---- 2. logits on MFMA and the value rows into LDS, one batch of tiles at a time ----
-    float acc_own[4] = {0.f, 0.f, 0.f, 0.f};
-    auto consume_tiles = [&](int t0) {
-#pragma unroll
-        for (int i = 0; i < kTB; ++i) {
-            const int t = t0 + i, s = 16 * t + n16;
-            if (t >= NT || t >= ntile) break;                 // uniform
-            float4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                const uint4 qq = q_ok ? qa[j] : make_uint4(0, 0, 0, 0);
-                const uint4 kk = gok[t] ? kc[i][j] : make_uint4(0, 0, 0, 0);
-                if constexpr (kBf16) {
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qq),
-                                                                  __builtin_bit_cast(bf16x8_t, kk), acc, 0, 0, 0);
-                } else {
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.x), __uint_as_float(kk.x), acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.y), __uint_as_float(kk.y), acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.z), __uint_as_float(kk.z), acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.w), __uint_as_float(kk.w), acc, 0, 0, 0);
-                }
-            }
-            // rows 4g + r of the product are query r for every g: lane 16g + n keeps tile g
-#pragma unroll
-            for (int r = 0; r < 4; ++r) acc_own[r] = g == t ? acc[r] : acc_own[r];
-            // value rows (off-map or missing candidates as zeros)
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                const uint4 vv = gok[t] ? vc[i][j] : make_uint4(0, 0, 0, 0);
-                const int c0 = (g + 4 * j) * E;               // first channel of this chunk
-                if constexpr (kBf16) {
-                    uint16_t* vt = reinterpret_cast<uint16_t*>(Vb);
-                    const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const uint32_t bits = (e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xFFFFu);
-                        vt[(c0 + e) * lay.vpitch + s] = static_cast<uint16_t>(bits);
-                    }
-                } else {
-                    *reinterpret_cast<uint4*>(Vb + (s * lay.vpitch + c0) * 4) = vv;
-                }
-            }
-        }
-    };
-    consume_tiles(0);
-#pragma unroll
-    for (int t0 = kTB; t0 < NT; t0 += kTB) {
-        if (t0 >= ntile) break;                               // uniform
-        load_tiles(t0);
-        consume_tiles(t0);
-    }
-    // Output ownership (step 6): lane 4*blk + t4 with blk = cg*NH + hh owns channel 4*cg + t4 of
-    // queries hh*QPL .. hh*QPL + QPL-1.
-    const int blk = lane >> 2, t4 = lane & 3;
-    const int cg = blk / NH, hh = blk % NH;
-    const int ch = 4 * cg + t4;
-    constexpr int kPre = FINEST ? kPrefetchLevels : 1;
-    float anc[kPre];
-    float wq[FINEST ? QPL : 1][kPre + 1];
-    const bool prefetch = FINEST && a.levels <= kPre + 1;
-    // the finest level's combination inputs, requested once the gathered registers are free; their
-    // latency overlaps the softmax and the messages
-    if constexpr (FINEST) {
-        if (prefetch) {                                      // uniform
-            const int L = a.levels;
-#pragma unroll
-            for (int lev = 1; lev <= kPre; ++lev) {
-                if (lev >= L) break;                         // uniform
-                // the ancestor is shared by the four siblings: a uniform address plus the channel
-                const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
-                                  static_cast<size_t>((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev);
-                anc[lev - 1] = (a.coarser_msg[lev] + (an * a.heads + h) * D)[ch];
-            }
-            if (!VA && a.w) {                                // uniform
-                const float* wb = a.w + (static_cast<size_t>(b) * N * a.heads + h) * L;
-#pragma unroll
-                for (int u = 0; u < QPL; ++u) {
-                    const int qi = (NH == 2 ? hh * QPL : 0) + u;
-                    const int wy = min(2 * Py + (qi >> 1), H - 1), wx = min(2 * Px + (qi & 1), W - 1);
-                    const float* wrow = wb + static_cast<uint32_t>(__mul24(wy, W) + wx) * static_cast<uint32_t>(a.heads * L);
-#pragma unroll
-                    for (int lev = 0; lev <= kPre; ++lev) {
-                        if (lev >= L) break;                 // uniform
-                        wq[u][lev] = wrow[lev];
-                    }
-                }
-            }
-        }
-    }
-    float x[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) x[r] = ok ? acc_own[r] * a.scale : -INFINITY;
-
-    // ---- 3. weights ----
-    float wgt[4], inv_sum[4] = {1.f, 1.f, 1.f, 1.f};
-    if constexpr (!VA) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float m = wave_max_fast(x[r]);
-            wgt[r] = ok ? __expf(x[r] - m) : 0.f;
-            inv_sum[r] = 1.0f / wave_sum_fast(wgt[r]);
-        }
-    } else {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float m = fmaxf(x[r], xchg_f32<1>(x[r]));
-            m = fmaxf(m, xchg_f32<2>(m));
-            const float e = ok ? __expf(x[r] - m) : 0.f;
-            float s = e + xchg_f32<1>(e);
-            s += xchg_f32<2>(s);
-            wgt[r] = ok ? pkey * (e / s) : 0.f;
-        }
-    }
-
-    // ---- 4. this level's selection (levels above the finest) ----
-    if constexpr (!FINEST) {
-        const int nvalid = __popcll(__ballot(ok));
-        const int keff = K < nvalid ? K : nvalid;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int qy = 2 * Py + (r >> 1), qx = 2 * Px + (r & 1);
-            if (qy >= H || qx >= W) continue;                 // uniform across the wave
-            const uint32_t key[1] = {ok ? ordered_bits(VA ? wgt[r] : x[r]) : 0u};
-            const uint32_t name[1] = {static_cast<uint32_t>(flat)};
-            bool kept[1];
-            wave_select_top<1>(key, name, keff, kept);
-            const uint64_t mask = __ballot(kept[0]);
-            const size_t orow = ((static_cast<size_t>(b) * a.heads + h) * N + qy * W + qx) * K;
-            if (kept[0]) {
-                const int pos = lanes_below(mask);
-                a.sel_idx[orow + pos] = flat;
-                a.sel_key[orow + pos] = VA ? wgt[r] : wgt[r] * inv_sum[r];
-                if constexpr (VA) wgt[r] = 0.f;               // refined at the next level (Omega)
-            }
-            if (lane >= keff && lane < K) {
-                a.sel_idx[orow + lane] = -1;
-                a.sel_key[orow + lane] = 0.f;
-            }
-        }
-    }
-
-    // ---- 5. messages on MFMA ----
-    if (lane < nsp) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            if constexpr (kBf16)
-                reinterpret_cast<uint16_t*>(Pb)[r * nsp + lane] = static_cast<uint16_t>(f32_to_bf16_bits(wgt[r]));
-            else
-                reinterpret_cast<float*>(Pb)[r * nsp + lane] = wgt[r];
-        }
-    }
-    wave_lds_sync();
-
-    const int sph = nsp / NH;
-    float4_t o = {0.f, 0.f, 0.f, 0.f};
-    if constexpr (kBf16) {
-        const uint16_t* prow_l = reinterpret_cast<const uint16_t*>(Pb) + t4 * nsp + hh * sph;
-        const uint16_t* vrow_l = reinterpret_cast<const uint16_t*>(Vb) + (4 * cg + t4) * lay.vpitch + hh * sph;
-        for (int st = 0; st < sph; st += 4) {
-            const uint2 pa = *reinterpret_cast<const uint2*>(prow_l + st);
-            const uint2 vb = *reinterpret_cast<const uint2*>(vrow_l + st);
-            short4_t av, bv;
-            av[0] = static_cast<short>(pa.x); av[1] = static_cast<short>(pa.x >> 16);
-            av[2] = static_cast<short>(pa.y); av[3] = static_cast<short>(pa.y >> 16);
-            bv[0] = static_cast<short>(vb.x); bv[1] = static_cast<short>(vb.x >> 16);
-            bv[2] = static_cast<short>(vb.y); bv[3] = static_cast<short>(vb.y >> 16);
-            o = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(av, bv, o, 0, 0, 0);
-        }
-    } else {
-        const float* prow_l = reinterpret_cast<const float*>(Pb) + t4 * nsp + hh * sph;
-        const float* vcol = reinterpret_cast<const float*>(Vb) + 4 * cg + t4;
-        for (int st = 0; st < sph; ++st)
-            o = __builtin_amdgcn_mfma_f32_4x4x1f32(prow_l[st], vcol[(hh * sph + st) * lay.vpitch], o, 0, 0, 0);
-    }
-    if constexpr (NH == 2) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) o[r] += xchg_f32<4>(o[r]);
-    }
-
-    // ---- 6. outputs ----
-#pragma unroll
-    for (int u = 0; u < QPL; ++u) {
-        const int qi = (NH == 2 ? hh * QPL : 0) + u;
-        const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
-        if (qy >= H || qx >= W) continue;
-        const float m = pick4(o, qi) * pick4(inv_sum, qi);
-        const uint32_t qpos = static_cast<uint32_t>(__mul24(qy, W) + qx);      // token within the map
-        if constexpr (!FINEST) {
-            float* mb = a.msg + (static_cast<size_t>(b) * N * a.heads + h) * D;  // uniform
-            mb[qpos * static_cast<uint32_t>(a.heads * D) + ch] = m;
-        } else {
-            const size_t qtok = static_cast<size_t>(b) * N + qpos;
-            const int L = a.levels;
-            const float wdef = 1.0f / L;
-            float out;
-            if (prefetch) {
-                out = (VA ? 1.0f : (a.w ? wq[u][0] : wdef)) * m;
-#pragma unroll
-                for (int lev = 1; lev <= kPre; ++lev) {
-                    if (lev >= L) break;
-                    out += (VA ? 1.0f : (a.w ? wq[u][lev] : wdef)) * anc[lev - 1];
-                }
-            } else {
-                const float* wrow = a.w ? a.w + (qtok * a.heads + h) * L : nullptr;
-                out = (VA ? 1.0f : (wrow ? wrow[0] : wdef)) * m;
-                for (int lev = 1; lev < L; ++lev) {
-                    const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
-                                      static_cast<size_t>(qy >> lev) * a.lvl_W[lev] + (qx >> lev);
-                    const float wl = VA ? 1.0f : (wrow ? wrow[lev] : wdef);
-                    out += wl * a.coarser_msg[lev][(an * a.heads + h) * D + ch];
-                }
-            }
-            void* ob = static_cast<unsigned char*>(a.out) + (static_cast<size_t>(b) * N * C + h * D) * TB;  // uniform
-            S::store1(ob, qpos * static_cast<uint32_t>(C) + ch, out);
-        }
-    }
+    const int nsp = (4 * a.K + 15) & ~15;
+    fine_item<T, D, NSP, VA, FINEST>(a, item, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
 }
 
 template <typename T, int D, int NSP, bool VA, bool FINEST>
