@@ -29,7 +29,12 @@
  *     further level) every candidate contributes;
  *   - temperature tau = 1/sqrt(d) (head dimension) at every level unless a scale is given;
  *   - w is used as given, [B][H*W][heads][L]; NULL means 1/L everywhere;
- *   - every head is an independent quadtree.
+ *   - every head is an independent quadtree;
+ *   - K may differ per level (the paper's matching setting keeps K = 8 at the finest selecting
+ *     level and doubles it at each coarser one, Sec. 4.1.1): K_l keys are kept by every query of
+ *     level l, and a query of level l-1 meets the 2x2 children of its parent's K_l keys;
+ *   - V's coarser levels may be supplied by the caller instead of pooled (the paper builds them
+ *     with a conv-norm-act layer for self-attention, Sec. 3.2); they are then used as given.
  *
  * Arithmetic: every dot product, softmax and message sum is in double, from the stored (already
  * rounded) pyramid values. Pyramids are computed in fp32 exactly as stated above.
@@ -55,18 +60,20 @@ typedef struct {
     const float* v;
     const float* w;               /* variant B only: [B][H*W][heads][L]; NULL means 1/L */
     int B, heads, H, W, d, L, K, variant, dtype;
+    const int* K_levels;          /* NULL (K at every level), or entry l in 1..L-1: K_l */
+    const float* const* v_levels; /* NULL (pooled V), or entry l in 1..L-1: V at level l, [B][H_l][W_l][C] */
     double scale;                 /* <= 0 means 1/sqrt(d) */
-    const int32_t* const* forced; /* NULL, or per level l in 1..L-1: [B][heads][N_l][K] */
+    const int32_t* const* forced; /* NULL, or per level l in 1..L-1: [B][heads][N_l][K_l] */
     /* outputs, all optional (NULL pointers or NULL entries are skipped) */
     double* out;                  /* [B][H][W][heads][d] */
     float* const* pyr_q;          /* per level l in 1..L-1: [B][H_l][W_l][C] */
     float* const* pyr_k;
     float* const* pyr_v;
     double* const* msg;           /* per level l in 0..L-1: [B][N_l][heads][d] */
-    int32_t* const* sel_idx;      /* per level l in 1..L-1: [B][heads][N_l][K], -1 padded */
+    int32_t* const* sel_idx;      /* per level l in 1..L-1: [B][heads][N_l][K_l], -1 padded */
     double* const* sel_key;       /* same shape; 0 where idx is -1 */
     int32_t* const* cand_idx;     /* per level l in 0..L-1: [B][heads][N_l][ncand_l] */
-    double* const* cand_key;      /*   ncand = N_{L-1} at the coarsest level, 4K elsewhere */
+    double* const* cand_key;      /*   ncand = N_{L-1} at the coarsest level, 4 K_{l+1} elsewhere */
 } qo_forward_args;
 
 /* ----------------------------------------------------------------------------------------- */
@@ -201,10 +208,20 @@ int qo_forward(const qo_forward_args* a)
     const int C = NH * d;
     const double tau = a->scale > 0.0 ? a->scale : 1.0 / sqrt((double)d);
     const int isB = a->variant == QO_B;
-    size_t Nl[QO_MAX_LEVELS];
+    size_t Nl[QO_MAX_LEVELS] = {0};
     for (int l = 0; l < L; ++l) Nl[l] = (size_t)Hl[l] * (size_t)Wl[l];
     const int Lc = L - 1;           /* coarsest level */
     const int nc_coarse = (int)Nl[Lc];
+    int Kl[QO_MAX_LEVELS];          /* keys kept per query at level l (l >= 1) */
+    int Kmax = 0;
+    for (int l = 0; l < L; ++l) {
+        Kl[l] = a->K_levels ? a->K_levels[l] : K;
+        if (l >= 1 && Kl[l] <= 0) return -1;
+        if (l >= 1 && Kl[l] > Kmax) Kmax = Kl[l];
+    }
+    if (a->v_levels)
+        for (int l = 1; l < L; ++l)
+            if (!a->v_levels[l]) return -1;
 
     int rc = 0;
     float* pq[QO_MAX_LEVELS] = {0};
@@ -213,12 +230,12 @@ int qo_forward(const qo_forward_args* a)
     double* msg[QO_MAX_LEVELS] = {0};
     int32_t* sel[QO_MAX_LEVELS] = {0};
     double* key[QO_MAX_LEVELS] = {0};
-    int ncand_max = nc_coarse > 4 * K ? nc_coarse : 4 * K;
+    int ncand_max = nc_coarse > 4 * Kmax ? nc_coarse : 4 * Kmax;
     double* ck = malloc(sizeof(double) * ncand_max);
     int* ci = malloc(sizeof(int) * ncand_max);
     int* cv = malloc(sizeof(int) * ncand_max);
     double* cx = malloc(sizeof(double) * ncand_max);
-    int* pos = malloc(sizeof(int) * (K + 1));
+    int* pos = malloc(sizeof(int) * (Kmax + 1));
     char* taken = malloc(ncand_max);
     char* in_sel = malloc(ncand_max);
     double* acc = malloc(sizeof(double) * d);
@@ -233,8 +250,8 @@ int qo_forward(const qo_forward_args* a)
         msg[l] = malloc(sizeof(double) * (size_t)B * Nl[l] * NH * d);
         if (!pq[l] || !pk[l] || !pv[l] || !msg[l]) { rc = -3; goto done; }
         if (l >= 1) {
-            sel[l] = malloc(sizeof(int32_t) * (size_t)B * NH * Nl[l] * K);
-            key[l] = malloc(sizeof(double) * (size_t)B * NH * Nl[l] * K);
+            sel[l] = malloc(sizeof(int32_t) * (size_t)B * NH * Nl[l] * Kl[l]);
+            key[l] = malloc(sizeof(double) * (size_t)B * NH * Nl[l] * Kl[l]);
             if (!sel[l] || !key[l]) { rc = -3; goto done; }
         }
     }
@@ -246,7 +263,11 @@ int qo_forward(const qo_forward_args* a)
     for (int l = 1; l < L; ++l) {
         qo_pool_level(pq[l - 1], B, Hl[l - 1], Wl[l - 1], C, a->dtype, pq[l]);
         qo_pool_level(pk[l - 1], B, Hl[l - 1], Wl[l - 1], C, a->dtype, pk[l]);
-        qo_pool_level(pv[l - 1], B, Hl[l - 1], Wl[l - 1], C, a->dtype, pv[l]);
+        if (a->v_levels) {
+            for (size_t i = 0; i < (size_t)B * Nl[l] * C; ++i) pv[l][i] = round_to_dtype(a->v_levels[l][i], a->dtype);
+        } else {
+            qo_pool_level(pv[l - 1], B, Hl[l - 1], Wl[l - 1], C, a->dtype, pv[l]);
+        }
     }
 
     for (int b = 0; b < B; ++b)
@@ -268,21 +289,22 @@ int qo_forward(const qo_forward_args* a)
                     for (size_t j = 0; j < N; ++j) { ck[j] /= den; ci[j] = (int)j; cv[j] = 1; in_sel[j] = 0; }
 
                     if (L > 1) {
+                        const int Ks = Kl[l];
                         int kept;
-                        int32_t* srow = sel[l] + (((size_t)b * NH + h) * N + i) * K;
-                        double* krow = key[l] + (((size_t)b * NH + h) * N + i) * K;
+                        int32_t* srow = sel[l] + (((size_t)b * NH + h) * N + i) * Ks;
+                        double* krow = key[l] + (((size_t)b * NH + h) * N + i) * Ks;
                         if (a->forced && a->forced[l]) {
-                            const int32_t* frow = a->forced[l] + (((size_t)b * NH + h) * N + i) * K;
+                            const int32_t* frow = a->forced[l] + (((size_t)b * NH + h) * N + i) * Ks;
                             kept = 0;
-                            for (int r = 0; r < K; ++r) {
+                            for (int r = 0; r < Ks; ++r) {
                                 if (frow[r] < 0) break;
                                 if (frow[r] >= (int32_t)N) { rc = -2; goto done; }
                                 pos[kept++] = frow[r];
                             }
                         } else {
-                            kept = select_top_k(ck, ci, cv, (int)N, K, pos, taken);
+                            kept = select_top_k(ck, ci, cv, (int)N, Ks, pos, taken);
                         }
-                        for (int r = 0; r < K; ++r) {
+                        for (int r = 0; r < Ks; ++r) {
                             srow[r] = r < kept ? ci[pos[r]] : -1;
                             krow[r] = r < kept ? ck[pos[r]] : 0.0;
                         }
@@ -314,17 +336,18 @@ int qo_forward(const qo_forward_args* a)
             for (int l = Lc - 1; l >= 0; --l) {
                 const size_t N = Nl[l], Np = Nl[l + 1];
                 const int Hh = Hl[l], Ww = Wl[l], Wp = Wl[l + 1];
-                const int ncand = 4 * K;
+                const int Kp = Kl[l + 1];      /* the parent's kept keys */
+                const int ncand = 4 * Kp;
                 for (int y = 0; y < Hh; ++y)
                     for (int x = 0; x < Ww; ++x) {
                         const size_t i = (size_t)y * Ww + x;
                         const size_t P = (size_t)(y >> 1) * Wp + (size_t)(x >> 1);
-                        const int32_t* psel = sel[l + 1] + (((size_t)b * NH + h) * Np + P) * K;
-                        const double* pkey = key[l + 1] + (((size_t)b * NH + h) * Np + P) * K;
+                        const int32_t* psel = sel[l + 1] + (((size_t)b * NH + h) * Np + P) * Kp;
+                        const double* pkey = key[l + 1] + (((size_t)b * NH + h) * Np + P) * Kp;
                         const float* qi = pq[l] + ((size_t)b * N + i) * C + (size_t)h * d;
                         /* candidate slot 4r+c: child c (order (0,0),(0,1),(1,0),(1,1)) of the parent's
                          * r-th kept key; slots of missing keys or off-map children are invalid */
-                        for (int r = 0; r < K; ++r) {
+                        for (int r = 0; r < Kp; ++r) {
                             const int J = psel[r];
                             for (int c = 0; c < 4; ++c) {
                                 const int s = 4 * r + c;
@@ -350,7 +373,7 @@ int qo_forward(const qo_forward_args* a)
                             for (int s = 0; s < ncand; ++s) if (cv[s]) ck[s] /= den;
                         } else {
                             /* Eq. (4): s = s_parent * t, t a softmax over the children of one kept key */
-                            for (int r = 0; r < K; ++r) {
+                            for (int r = 0; r < Kp; ++r) {
                                 double mx = -INFINITY, den = 0.0;
                                 for (int c = 0; c < 4; ++c) { const int s = 4 * r + c; if (cv[s] && cx[s] > mx) mx = cx[s]; }
                                 for (int c = 0; c < 4; ++c) { const int s = 4 * r + c; if (cv[s]) { ck[s] = exp(cx[s] - mx); den += ck[s]; } }
@@ -358,13 +381,14 @@ int qo_forward(const qo_forward_args* a)
                             }
                         }
                         if (l >= 1) {
+                            const int Ks = Kl[l];
                             int kept;
-                            int32_t* srow = sel[l] + (((size_t)b * NH + h) * N + i) * K;
-                            double* krow = key[l] + (((size_t)b * NH + h) * N + i) * K;
+                            int32_t* srow = sel[l] + (((size_t)b * NH + h) * N + i) * Ks;
+                            double* krow = key[l] + (((size_t)b * NH + h) * N + i) * Ks;
                             if (a->forced && a->forced[l]) {
-                                const int32_t* frow = a->forced[l] + (((size_t)b * NH + h) * N + i) * K;
+                                const int32_t* frow = a->forced[l] + (((size_t)b * NH + h) * N + i) * Ks;
                                 kept = 0;
-                                for (int r = 0; r < K; ++r) {
+                                for (int r = 0; r < Ks; ++r) {
                                     if (frow[r] < 0) break;
                                     int found = -1;
                                     for (int s = 0; s < ncand; ++s) if (cv[s] && ci[s] == frow[r]) found = s;
@@ -372,9 +396,9 @@ int qo_forward(const qo_forward_args* a)
                                     pos[kept++] = found;
                                 }
                             } else {
-                                kept = select_top_k(ck, ci, cv, ncand, K, pos, taken);
+                                kept = select_top_k(ck, ci, cv, ncand, Ks, pos, taken);
                             }
-                            for (int r = 0; r < K; ++r) {
+                            for (int r = 0; r < Ks; ++r) {
                                 srow[r] = r < kept ? ci[pos[r]] : -1;
                                 krow[r] = r < kept ? ck[pos[r]] : 0.0;
                             }
@@ -428,8 +452,8 @@ int qo_forward(const qo_forward_args* a)
             if (a->pyr_q && a->pyr_q[l]) memcpy(a->pyr_q[l], pq[l], sizeof(float) * n);
             if (a->pyr_k && a->pyr_k[l]) memcpy(a->pyr_k[l], pk[l], sizeof(float) * n);
             if (a->pyr_v && a->pyr_v[l]) memcpy(a->pyr_v[l], pv[l], sizeof(float) * n);
-            if (a->sel_idx && a->sel_idx[l]) memcpy(a->sel_idx[l], sel[l], sizeof(int32_t) * (size_t)B * NH * Nl[l] * K);
-            if (a->sel_key && a->sel_key[l]) memcpy(a->sel_key[l], key[l], sizeof(double) * (size_t)B * NH * Nl[l] * K);
+            if (a->sel_idx && a->sel_idx[l]) memcpy(a->sel_idx[l], sel[l], sizeof(int32_t) * (size_t)B * NH * Nl[l] * Kl[l]);
+            if (a->sel_key && a->sel_key[l]) memcpy(a->sel_key[l], key[l], sizeof(double) * (size_t)B * NH * Nl[l] * Kl[l]);
         }
         if (a->msg && a->msg[l]) memcpy(a->msg[l], msg[l], sizeof(double) * (size_t)B * Nl[l] * NH * d);
     }

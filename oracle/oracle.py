@@ -38,7 +38,8 @@ class _Args(ctypes.Structure):
         ("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("w", ctypes.c_void_p),
         ("B", ctypes.c_int), ("heads", ctypes.c_int), ("H", ctypes.c_int), ("W", ctypes.c_int),
         ("d", ctypes.c_int), ("L", ctypes.c_int), ("K", ctypes.c_int), ("variant", ctypes.c_int),
-        ("dtype", ctypes.c_int), ("scale", ctypes.c_double),
+        ("dtype", ctypes.c_int), ("K_levels", ctypes.c_void_p), ("v_levels", ctypes.c_void_p),
+        ("scale", ctypes.c_double),
         ("forced", ctypes.c_void_p),
         ("out", ctypes.c_void_p),
         ("pyr_q", ctypes.c_void_p), ("pyr_k", ctypes.c_void_p), ("pyr_v", ctypes.c_void_p),
@@ -94,12 +95,16 @@ def _ptr_table(arrays):
     return tbl
 
 
-def forward(q, k, v, *, levels: int, K: int, variant: str, dtype: str = "f32", w=None, scale=None,
-            forced=None, want_candidates: bool = False, want_pyramids: bool = False) -> dict:
+def forward(q, k, v, *, levels: int, K, variant: str, dtype: str = "f32", w=None, scale=None,
+            forced=None, want_candidates: bool = False, want_pyramids: bool = False, v_levels=None) -> dict:
     """Run the oracle. ``q, k, v``: float32 ``[B, H, W, heads, d]`` (values representable in dtype).
 
+    ``K``: one count for every level, or a sequence indexed by level whose entry l (1 <= l < levels)
+    is the number of keys kept at level l (entry 0 is ignored).
+    ``v_levels``: optional list indexed by level; entry l (1 <= l < levels) is V at level l,
+    ``[B, H_l, W_l, heads, d]``, used instead of pooling V.
     ``forced``: optional list indexed by level; entry l (1 <= l < levels) is an int32
-    ``[B, heads, N_l, K]`` selection that replaces the oracle's own choice at that level.
+    ``[B, heads, N_l, K_l]`` selection that replaces the oracle's own choice at that level.
     Returns a dict with ``out`` ``[B,H,W,heads,d]`` and per-level lists ``msg`` ``[B,N_l,heads,d]``,
     ``sel_idx``/``sel_key`` ``[B,heads,N_l,K]`` (None at level 0) and, on request,
     ``cand_idx``/``cand_key`` ``[B,heads,N_l,ncand]`` and the pyramids ``pyr_q/k/v`` ``[B,H_l,W_l,C]``.
@@ -117,11 +122,27 @@ def forward(q, k, v, *, levels: int, K: int, variant: str, dtype: str = "f32", w
     if w is not None:
         wts = np.ascontiguousarray(w, dtype=np.float32)
         assert wts.shape == (B, H * W, NH, L), wts.shape
+    if np.ndim(K) == 0:
+        Kl = [int(K)] * L
+    else:
+        Kl = [int(x) for x in K]
+        assert len(Kl) == L, "one K per level (entry 0 ignored)"
+        Kl[0] = Kl[1] if L > 1 else max(Kl[0], 1)
+    K_tbl = (ctypes.c_int * MAX_LEVELS)(*Kl)
+    v_tbl = None
+    v_keep = []
+    if v_levels is not None:
+        v_tbl = (ctypes.c_void_p * MAX_LEVELS)()
+        for l in range(1, L):
+            vl = np.ascontiguousarray(v_levels[l], dtype=np.float32)
+            assert vl.size == B * N[l] * C, (vl.shape, (B, dims[l][0], dims[l][1], NH, d))
+            v_keep.append(vl)
+            v_tbl[l] = vl.ctypes.data
     out = np.zeros((B, H, W, NH, d), np.float64)
     msg = [np.zeros((B, N[l], NH, d), np.float64) for l in range(L)]
-    sel_idx = [None] + [np.zeros((B, NH, N[l], K), np.int32) for l in range(1, L)]
-    sel_key = [None] + [np.zeros((B, NH, N[l], K), np.float64) for l in range(1, L)]
-    ncand = [4 * K] * (L - 1) + [N[L - 1]]
+    sel_idx = [None] + [np.zeros((B, NH, N[l], Kl[l]), np.int32) for l in range(1, L)]
+    sel_key = [None] + [np.zeros((B, NH, N[l], Kl[l]), np.float64) for l in range(1, L)]
+    ncand = [4 * Kl[l + 1] for l in range(L - 1)] + [N[L - 1]]
     cand_idx = cand_key = None
     if want_candidates:
         cand_idx = [np.zeros((B, NH, N[l], ncand[l]), np.int32) for l in range(L)]
@@ -136,7 +157,7 @@ def forward(q, k, v, *, levels: int, K: int, variant: str, dtype: str = "f32", w
         for l in range(1, L):
             if forced[l] is not None:
                 f = np.ascontiguousarray(forced[l], dtype=np.int32)
-                assert f.shape == (B, NH, N[l], K), (f.shape, (B, NH, N[l], K))
+                assert f.shape == (B, NH, N[l], Kl[l]), (f.shape, (B, NH, N[l], Kl[l]))
                 forced_arrays[l] = f
 
     tables = {}
@@ -156,7 +177,9 @@ def forward(q, k, v, *, levels: int, K: int, variant: str, dtype: str = "f32", w
     args.q, args.k, args.v = q.ctypes.data, k.ctypes.data, v.ctypes.data
     args.w = wts.ctypes.data if wts is not None else None
     args.B, args.heads, args.H, args.W, args.d = B, NH, H, W, d
-    args.L, args.K, args.variant, args.dtype = L, K, VARIANTS[variant], DTYPES[dtype]
+    args.L, args.K, args.variant, args.dtype = L, Kl[1] if L > 1 else Kl[0], VARIANTS[variant], DTYPES[dtype]
+    args.K_levels = ctypes.addressof(K_tbl)
+    args.v_levels = ctypes.addressof(v_tbl) if v_tbl is not None else None
     args.scale = float(scale) if scale is not None else 0.0
     args.out = out.ctypes.data
     for name, tbl in tables.items():

@@ -71,17 +71,24 @@ def _top(keys: dict, K: int) -> list:
     return [t for t, _ in order[:K]]
 
 
-def brute_quadtree(q, k, v, L: int, K: int, variant: str, tau: float, w=None) -> np.ndarray:
+def brute_quadtree(q, k, v, L: int, K, variant: str, tau: float, w=None, v_levels=None) -> np.ndarray:
     """Output [B, H, W, heads, d] of QuadTree attention, query by query, with explicit regions.
 
     q, k, v: [B, H, W, heads, d]; w (variant B): [B, H*W, heads, L] or None (=> 1/L).
+    K: one count, or a list whose entry l is the number of keys kept at level l (l >= 1).
+    v_levels: None (V pooled like Q and K) or a list whose entry l (l >= 1) is V at level l,
+    [B, H_l, W_l, heads, d].
     """
+    Kl = [K] * L if np.ndim(K) == 0 else list(K)
     q = np.asarray(q, np.float64)
     k = np.asarray(k, np.float64)
     v = np.asarray(v, np.float64)
     B, H, W, NH, d = q.shape
     flat = lambda t: t.reshape(t.shape[0], t.shape[1], t.shape[2], NH * d)
     PQ, PK, PV = pyramid(flat(q), L), pyramid(flat(k), L), pyramid(flat(v), L)
+    if v_levels is not None:
+        for l in range(1, L):
+            PV[l] = flat(np.asarray(v_levels[l], np.float64))
     out = np.zeros((B, H, W, NH, d))
     for b in range(B):
         for h in range(NH):
@@ -108,7 +115,7 @@ def brute_quadtree(q, k, v, L: int, K: int, variant: str, tau: float, w=None) ->
                                 t_ = _softmax(np.array([logit[t] for t in kids]))
                                 for t, tv in zip(kids, t_):
                                     score[t] = sp * tv
-                        kept = _top(score, K) if lvl > 0 else []
+                        kept = _top(score, Kl[lvl]) if lvl > 0 else []
                         if variant == "B":
                             m = sum(score[t] * PV[lvl][b, t[0], t[1], sl] for t in score)
                             wl = (1.0 / L) if w is None else float(w[b, y * W + x, h, lvl])

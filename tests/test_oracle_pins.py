@@ -343,3 +343,76 @@ def test_p14_deterministic():
     a = O.forward(q, k, v, levels=4, K=2, variant="A")["out"]
     b = O.forward(q, k, v, levels=4, K=2, variant="A")["out"]
     assert a.tobytes() == b.tobytes()
+
+
+# ------------------------------------- per-level K and caller-supplied V levels ---------------
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+@pytest.mark.parametrize("H,W,Ks", [(8, 8, [0, 1, 3]), (7, 9, [0, 2, 4]), (10, 6, [0, 3, 2]), (16, 16, [0, 2, 4, 8])])
+def test_k_schedule_matches_brute_force_regions(variant, H, W, Ks):
+    """A different K per level (the feature-matching setting, Sec. 4.1.1: K doubled at each coarser
+    level): the oracle equals the explicit-region formulation with K_l keys kept at level l and
+    the children of the parent's K_{l+1} keys as a level's candidates."""
+    L = len(Ks)
+    rng = np.random.default_rng(30 + H * W + sum(Ks))
+    q, k, v = (dyadic(rng, (1, H, W, 2, 4)) for _ in range(3))
+    w = rng.random((1, H * W, 2, L)).astype(np.float32)
+    tau = 1 / np.sqrt(4)
+    r = O.forward(q, k, v, levels=L, K=Ks, variant=variant, w=w if variant == "B" else None)
+    ref = brute.brute_quadtree(q, k, v, L, Ks, variant, tau, w if variant == "B" else None)
+    np.testing.assert_allclose(r["out"], ref, rtol=0, atol=1e-12)
+    for l in range(1, L):
+        assert r["sel_idx"][l].shape[-1] == Ks[l]
+
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+@pytest.mark.parametrize("H,W,L,K", [(8, 8, 3, 2), (7, 9, 3, [0, 2, 3]), (6, 10, 4, 1)])
+def test_supplied_v_levels_match_brute_force_regions(variant, H, W, L, K):
+    """V levels given by the caller (the conv-norm-act V pyramid of self-attention, Sec. 3.2):
+    the oracle equals the explicit-region formulation reading V^l from the given maps."""
+    rng = np.random.default_rng(40 + H * W + L)
+    q, k, v = (dyadic(rng, (1, H, W, 2, 4)) for _ in range(3))
+    dims = O.level_dims(H, W, L)
+    vl = [None] + [dyadic(rng, (1, dims[l][0], dims[l][1], 2, 4)) for l in range(1, L)]
+    w = rng.random((1, H * W, 2, L)).astype(np.float32)
+    tau = 1 / np.sqrt(4)
+    r = O.forward(q, k, v, levels=L, K=K, variant=variant, w=w if variant == "B" else None, v_levels=vl)
+    ref = brute.brute_quadtree(q, k, v, L, K, variant, tau, w if variant == "B" else None, v_levels=vl)
+    np.testing.assert_allclose(r["out"], ref, rtol=0, atol=1e-12)
+
+
+def test_supplied_pooled_v_levels_reproduce_the_default():
+    """Supplying exactly the average-pooled V levels changes nothing, bit for bit."""
+    rng = np.random.default_rng(50)
+    q, k, v = (rand(rng, (2, 13, 11, 2, 8)) for _ in range(3))
+    for variant in "AB":
+        base = O.forward(q, k, v, levels=4, K=[0, 2, 3, 5], variant=variant, want_pyramids=True)
+        vl = [None] + [base["pyr_v"][l].reshape(2, *base["dims"][l], 2, 8) for l in range(1, 4)]
+        again = O.forward(q, k, v, levels=4, K=[0, 2, 3, 5], variant=variant, v_levels=vl)
+        assert np.array_equal(base["out"], again["out"])
+
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+def test_constant_supplied_v_levels(variant):
+    """Every V level constant c_l. A: the partition weights sum to 1 at every finest query, so with
+    c_l = c at every level out = c (mass conservation, Sec. 3.2). B with every key kept (K_l >= N_l):
+    each level's message is its constant, out = sum_l w_l c_l (Eq. 5)."""
+    rng = np.random.default_rng(51)
+    H, W, L = 12, 10, 3
+    q, k = (rand(rng, (1, H, W, 1, 8)) for _ in range(2))
+    dims = O.level_dims(H, W, L)
+    if variant == "A":
+        c = rand(rng, (8,))
+        v = np.broadcast_to(c, (1, H, W, 1, 8)).copy()
+        vl = [None] + [np.broadcast_to(c, (1, dims[l][0], dims[l][1], 1, 8)).copy() for l in range(1, L)]
+        r = O.forward(q, k, v, levels=L, K=[0, 2, 3], variant="A", v_levels=vl)
+        np.testing.assert_allclose(r["out"], np.broadcast_to(c, r["out"].shape), atol=1e-12)
+    else:
+        cs = [rand(rng, (8,)) for _ in range(L)]
+        v = np.broadcast_to(cs[0], (1, H, W, 1, 8)).copy()
+        vl = [None] + [np.broadcast_to(cs[l], (1, dims[l][0], dims[l][1], 1, 8)).copy() for l in range(1, L)]
+        w = rng.random((1, H * W, 1, L)).astype(np.float32)
+        Ks = [0] + [dims[l][0] * dims[l][1] for l in range(1, L)]
+        r = O.forward(q, k, v, levels=L, K=Ks, variant="B", w=w, v_levels=vl)
+        expect = sum(w[0, :, 0, l][:, None] * cs[l][None, :].astype(np.float64) for l in range(L))
+        np.testing.assert_allclose(r["out"].reshape(H * W, 8), expect, atol=1e-12)
