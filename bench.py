@@ -47,10 +47,11 @@ def finest_kernel_bytes(wl) -> dict:
     n1 = dims[1][0] * dims[1][1]
     b = 2 if wl.dtype == "bf16" else 4
     sigma = 4 if wl.variant == "B" else 8
+    K1 = P.k_levels(wl.K, wl.levels)[1]       # keys each level-1 parent kept
     parts = {
         "queries": n0 * wl.d * b,
-        "parent_selections": n1 * wl.K * sigma,
-        "gather": n1 * 4 * wl.K * 2 * wl.d * b,
+        "parent_selections": n1 * K1 * sigma,
+        "gather": n1 * 4 * K1 * 2 * wl.d * b,
         "ancestor_messages": n1 * (wl.levels - 1) * wl.d * 4,
         "level_weights": n0 * wl.levels * 4 if wl.variant == "B" else 0,
         "output": n0 * wl.d * b,
@@ -79,14 +80,15 @@ def measured_traffic(workload: str):
 
 def cpu_baseline(wl, seconds: float) -> dict:
     """The oracle as it stands, single-threaded on the host, on whole layers of the workload."""
-    from paper_2201_02767_amd.inputs import make_level_weights, make_qkv
+    from paper_2201_02767_amd.inputs import make_level_weights, make_qkv, make_v_levels
     from oracle import oracle
 
     q, k, v = make_qkv(wl)
     w = make_level_weights(wl) if wl.variant == "B" else None
+    vl = make_v_levels(wl) if wl.v_given else None
     runs, t0 = 0, time.perf_counter()
     while True:
-        oracle.forward(q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w)
+        oracle.forward(q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w, v_levels=vl)
         runs += 1
         el = time.perf_counter() - t0
         if el >= seconds:
@@ -130,7 +132,7 @@ def main() -> int:
         return 0
 
     import paper_2201_02767_amd as P
-    from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_qkv
+    from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_qkv, make_v_levels
 
     if args.workload not in WORKLOADS:
         print(f"unknown workload {args.workload}; choose from {sorted(WORKLOADS)}", file=sys.stderr)
@@ -140,9 +142,12 @@ def main() -> int:
     tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     q, k, v = (torch.from_numpy(x).to(dev).to(tdt).contiguous() for x in make_qkv(wl))
     w = torch.from_numpy(make_level_weights(wl)).to(dev) if wl.variant == "B" else None
+    vl = None
+    if wl.v_given:
+        vl = [None] + [torch.from_numpy(x).to(dev).to(tdt).contiguous() for x in make_v_levels(wl)[1:]]
     plan = P.Plan(wl.B, wl.H, wl.W, wl.heads, wl.d, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=tdt,
-                  device=dev)
-    step = plan.prepare(q, k, v, w)
+                  device=dev, v_supplied=wl.v_given)
+    step = plan.prepare(q, k, v, w, v_levels=vl)
     log(f"bench: {wl} on {torch.cuda.get_device_name(0)}")
 
     for _ in range(args.warmup):
@@ -197,7 +202,8 @@ def main() -> int:
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32" if wl.dtype == "f32" else "bf16", "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "W": wl.W, "heads": wl.heads, "d": wl.d,
-                   "levels": wl.levels, "K": wl.K, "variant": wl.variant, "global_batch": wl.B,
+                   "levels": wl.levels, "K": wl.K if isinstance(wl.K, int) else list(wl.K)[1:],
+                   "v_levels": "given" if wl.v_given else "pooled", "variant": wl.variant, "global_batch": wl.B,
                    "seq_len": wl.H * wl.W, "parallelism": "none (1 GPU)"},
         "roofline": roof, "cpu_baseline": cpu,
     }

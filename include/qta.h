@@ -81,6 +81,7 @@ typedef struct {
     int H[QTA_MAX_LEVELS];
     int W[QTA_MAX_LEVELS];
     int blocked[QTA_MAX_LEVELS];    /* 1: pyramid level l is parent-blocked, 0: NHWC         */
+    int K[QTA_MAX_LEVELS];          /* keys kept per query at level l >= 1 (0 at level 0)     */
     size_t q[QTA_MAX_LEVELS];       /* pyramid level l >= 1, dtype                          */
     size_t k[QTA_MAX_LEVELS];
     size_t v[QTA_MAX_LEVELS];
@@ -105,6 +106,14 @@ qta_status qta_get_workspace_layout(int B, int heads, int H, int W, int d, int l
  * are invalid or unsupported. */
 size_t qta_workspace_bytes(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype);
 
+/* The same for qta_forward_levels: K_levels and v_supplied as there (v_supplied != 0 when V's
+ * coarser levels come from the caller; the workspace then holds no V levels). */
+qta_status qta_get_workspace_layout_levels(int B, int heads, int H, int W, int d, int levels,
+                                           const int* K_levels, int v_supplied, qta_dtype dtype,
+                                           qta_workspace_layout* layout);
+size_t qta_workspace_bytes_levels(int B, int heads, int H, int W, int d, int levels, const int* K_levels,
+                                  int v_supplied, qta_dtype dtype);
+
 /*
  * qta_forward - the whole QuadTree attention forward (Sec. 3.2, Eqs. 1-6).
  *   q, k, v    [B][H][W][heads][d] dtype. Query and key maps have the same H x W.
@@ -122,6 +131,26 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
                        int B, int heads, int H, int W, int d, int levels, int K,
                        qta_variant variant, qta_dtype dtype, float scale,
                        void* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * qta_forward_levels - qta_forward with a K per level and, optionally, the caller's V pyramid.
+ *   K_levels   host array; entry l (1 <= l <= levels-1) is the number of keys every query of level
+ *              l keeps (1..QTA_MAX_K); entry 0 is not read. Level l-1's candidates are the 2x2
+ *              children of the parent's K_levels[l] keys. The feature-matching setting of the
+ *              paper keeps 8 at the finest selecting level and doubles K at each coarser level
+ *              (Sec. 4.1.1). NULL is allowed only with levels == 1.
+ *   v_levels   NULL: V's coarser levels are average-pooled like Q's and K's. Otherwise a host
+ *              array of device pointers; entry l (1 <= l <= levels-1) is V at level l,
+ *              [B][H_l][W_l][heads][d] dtype, 16-byte aligned, used as given (the paper builds V's
+ *              levels with a stride-2 conv-norm-act layer for self-attention, Sec. 3.2; that layer
+ *              is the caller's). Entry 0 is not read: level 0 is `v`. Every level is then stored
+ *              NHWC in the workspace.
+ * Everything else as qta_forward, which is this call with K_levels[l] = K and v_levels = NULL.
+ */
+qta_status qta_forward_levels(const void* q, const void* k, const void* v, const void* const* v_levels,
+                              const float* w, int B, int heads, int H, int W, int d, int levels,
+                              const int* K_levels, qta_variant variant, qta_dtype dtype, float scale,
+                              void* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * qta_build_pyramid - step 1: levels 1..levels-1 of one token map by 2x2 average pooling

@@ -20,14 +20,14 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     const int item = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, gridDim.x) * wpb + wave);
     if (item >= nitems) return;            // whole wave leaves; only wave-level syncs follow
     extern __shared__ __align__(16) unsigned char smem[];
-    const int nsp = (4 * a.K + 15) & ~15;
+    const int nsp = (4 * a.Kp + 15) & ~15;
     fine_item<T, D, NSP, VA, FINEST>(a, item, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
 }
 
 template <typename T, int D, int NSP, bool VA, bool FINEST>
 hipError_t launch_one(const FineArgs& a, hipStream_t stream)
 {
-    const int nsp = (4 * a.K + 15) & ~15;
+    const int nsp = (4 * a.Kp + 15) & ~15;
     const size_t wave_bytes = wave_lds<T, D>(nsp).total;
     const int wpb = 4;
     if (wpb * wave_bytes > device_max_lds()) return hipErrorInvalidValue;
@@ -50,7 +50,7 @@ hipError_t launch_one(const FineArgs& a, hipStream_t stream)
 template <typename T, int D, bool VA, bool FINEST>
 hipError_t launch_nsp(const FineArgs& a, hipStream_t stream)
 {
-    const int nslot = 4 * a.K;
+    const int nslot = 4 * a.Kp;
     if (nslot <= 16) return launch_one<T, D, 16, VA, FINEST>(a, stream);
     if (nslot <= 32) return launch_one<T, D, 32, VA, FINEST>(a, stream);
     return launch_one<T, D, 64, VA, FINEST>(a, stream);
@@ -67,7 +67,7 @@ hipError_t launch_td(const FineArgs& a, bool variant_a, bool finest, hipStream_t
 
 hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool bf16_in, bool finest, hipStream_t stream)
 {
-    if (4 * a.K > kMaxSlots) return launch_fine_attn_wide(a, d, variant_a, bf16_in, finest, stream);
+    if (4 * a.Kp > kMaxSlots) return launch_fine_attn_wide(a, d, variant_a, bf16_in, finest, stream);
     FineArgs b = a;
     b.div_Wp = make_fastdiv(a.Wp);
     if (bf16_in) {

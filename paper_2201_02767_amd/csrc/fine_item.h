@@ -100,7 +100,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
     const int P = bp % Np;
     const int b = bp / Np;
     const int Py = P / a.Wp, Px = P - Py * a.Wp;
-    const int H = a.H, W = a.W, C = a.C, K = a.K;
+    const int H = a.H, W = a.W, C = a.C, K = a.Kp, Ks = a.Ks;
     const int N = H * W;
     const int nslot = 4 * K;
     const int nsp = (nslot + 15) & ~15;                // <= NSP
@@ -302,7 +302,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
     // ---- 4. this level's selection (levels above the finest) ----
     if constexpr (!FINEST) {
         const int nvalid = __popcll(__ballot(ok));
-        const int keff = K < nvalid ? K : nvalid;
+        const int keff = Ks < nvalid ? Ks : nvalid;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int qy = 2 * Py + (r >> 1), qx = 2 * Px + (r & 1);
@@ -312,14 +312,14 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
             bool kept[1];
             wave_select_top<1>(key, name, keff, kept);
             const uint64_t mask = __ballot(kept[0]);
-            const size_t orow = ((static_cast<size_t>(b) * a.heads + h) * N + qy * W + qx) * K;
+            const size_t orow = ((static_cast<size_t>(b) * a.heads + h) * N + qy * W + qx) * Ks;
             if (kept[0]) {
                 const int pos = lanes_below(mask);
                 a.sel_idx[orow + pos] = flat;
                 a.sel_key[orow + pos] = VA ? wgt[r] : wgt[r] * inv_sum[r];
                 if constexpr (VA) wgt[r] = 0.f;               // refined at the next level (Omega)
             }
-            if (lane >= keff && lane < K) {
+            if (lane >= keff && lane < Ks) {
                 a.sel_idx[orow + lane] = -1;
                 a.sel_key[orow + lane] = 0.f;
             }

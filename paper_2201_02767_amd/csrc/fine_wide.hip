@@ -105,7 +105,7 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     const int P = static_cast<int>(bp % Np);
     const int b = static_cast<int>(bp / Np);
     const int Py = P / a.Wp, Px = P - Py * a.Wp;
-    const int H = a.H, W = a.W, C = a.C, K = a.K;
+    const int H = a.H, W = a.W, C = a.C, K = a.Kp, Ksel = a.Ks;
     const int N = H * W;
     const int nslot = 4 * K;
 
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
         int nvalid = 0;
 #pragma unroll
         for (int t = 0; t < NT; ++t) nvalid += __popcll(__ballot(ok[t]));
-        const int keff = K < nvalid ? K : nvalid;
+        const int keff = Ksel < nvalid ? Ksel : nvalid;
 #pragma unroll
         for (int qi = 0; qi < 4; ++qi) {
             const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
@@ -266,11 +266,11 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
 #pragma unroll
             for (int t = 0; t < NT; ++t) word[t] = ok[t] ? rank_word(VA ? wgt[t][qi] : x[t][qi], flat[t]) : 0ull;
             wave_bitonic_sort_desc<NT>(word);
-            const size_t orow = ((static_cast<size_t>(b) * a.heads + h) * N + qy * W + qx) * K;
+            const size_t orow = ((static_cast<size_t>(b) * a.heads + h) * N + qy * W + qx) * Ksel;
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const int r = kWave * t + lane;
-                if (r < K) {
+                if (r < Ksel) {
                     const uint64_t wd = word[t];
                     int32_t idx = -1;
                     float key = 0.f;
@@ -374,7 +374,7 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
 template <typename T, int D, bool VA, bool FINEST, int NT>
 hipError_t launch_one(const FineArgs& a, hipStream_t stream)
 {
-    const int nslot = 4 * a.K;
+    const int nslot = 4 * a.Kp;
     const size_t wave_bytes = fine_wave_bytes(nslot, D, sizeof(T));
     const size_t kLdsMax = device_max_lds();
     int wpb = 4;
@@ -398,7 +398,7 @@ hipError_t launch_one(const FineArgs& a, hipStream_t stream)
 template <typename T, int D, bool VA, bool FINEST>
 hipError_t launch_nt(const FineArgs& a, hipStream_t stream)
 {
-    const int nslot = 4 * a.K;
+    const int nslot = 4 * a.Kp;
     if (nslot <= 64) return launch_one<T, D, VA, FINEST, 1>(a, stream);
     if (nslot <= 128) return launch_one<T, D, VA, FINEST, 2>(a, stream);
     if (nslot <= 256) return launch_one<T, D, VA, FINEST, 4>(a, stream);

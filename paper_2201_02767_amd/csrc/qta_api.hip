@@ -60,14 +60,32 @@ qta_status map_ok(int H, int W, int heads, int d, qta_dtype dtype)
     return QTA_OK;
 }
 
-// Intermediate levels (produced by the pyramid, gathered by the next finer level) are stored
-// parent-blocked when the fine kernels take the blocked path (4K <= 64). The input level stays
-// NHWC: a blocked copy of it would cost a write and a read of k and v for no gain in the gathers.
-bool use_blocked(int K, int levels) { return levels > 2 && 4 * K <= 64; }
-
-qta_status layout(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype, qta_workspace_layout* L)
+// Keys kept per query at every selecting level: entry l (1 <= l <= levels-1) in [1, QTA_MAX_K].
+qta_status check_k_levels(const int* Kl, int levels)
 {
-    qta_status st = check_problem(B, heads, d, K, QTA_VARIANT_B, dtype);
+    if (levels > 1 && !Kl) return QTA_ERR_INVALID;
+    for (int l = 1; l < levels; ++l) {
+        if (Kl[l] <= 0) return QTA_ERR_INVALID;
+        if (Kl[l] > QTA_MAX_K) return QTA_ERR_UNSUPPORTED;
+    }
+    return QTA_OK;
+}
+
+// Intermediate level l (produced by the pyramid, gathered by level l's attention, whose parents
+// kept K_{l+1} keys) is stored parent-blocked when that kernel takes the blocked path
+// (4*K_{l+1} <= 64) and V comes from the pyramid. The input level stays NHWC: a blocked copy of
+// it would cost a write and a read of k and v for no gain in the gathers.
+bool use_blocked(const int* Kl, int l, int levels, bool v_supplied)
+{
+    return !v_supplied && l >= 1 && l <= levels - 2 && 4 * Kl[l + 1] <= 64;
+}
+
+qta_status layout(int B, int heads, int H, int W, int d, int levels, const int* Kl, bool v_supplied, qta_dtype dtype,
+                  qta_workspace_layout* L)
+{
+    qta_status st = check_problem(B, heads, d, 1, QTA_VARIANT_B, dtype);
+    if (st != QTA_OK) return st;
+    st = check_k_levels(Kl, levels);
     if (st != QTA_OK) return st;
     int Hl[QTA_MAX_LEVELS], Wl[QTA_MAX_LEVELS];
     st = dims(H, W, levels, Hl, Wl);
@@ -79,12 +97,12 @@ qta_status layout(int B, int heads, int H, int W, int d, int levels, int K, qta_
     L->levels = levels;
     const int C = heads * d;
     const int tb = static_cast<int>(dtype_bytes(dtype));
-    const bool blk = use_blocked(K, levels);
     size_t off = 0;
     for (int l = 0; l < levels; ++l) {
         L->H[l] = Hl[l];
         L->W[l] = Wl[l];
-        L->blocked[l] = (blk && l >= 1 && l <= levels - 2) ? 1 : 0;
+        L->K[l] = l >= 1 ? Kl[l] : 0;
+        L->blocked[l] = use_blocked(Kl, l, levels, v_supplied) ? 1 : 0;
     }
     for (int l = 1; l < levels; ++l) {
         const size_t N = static_cast<size_t>(Hl[l]) * Wl[l];
@@ -93,14 +111,16 @@ qta_status layout(int B, int heads, int H, int W, int d, int levels, int K, qta_
         off = align_up(off + tok);
         L->k[l] = off;
         off = align_up(off + tok);
-        L->v[l] = off;
-        off = align_up(off + tok);
+        if (!v_supplied) {
+            L->v[l] = off;
+            off = align_up(off + tok);
+        }
         L->msg[l] = off;
         off = align_up(off + static_cast<size_t>(B) * N * C * sizeof(float));
         L->sel_idx[l] = off;
-        off = align_up(off + static_cast<size_t>(B) * heads * N * K * sizeof(int32_t));
+        off = align_up(off + static_cast<size_t>(B) * heads * N * Kl[l] * sizeof(int32_t));
         L->sel_key[l] = off;
-        off = align_up(off + static_cast<size_t>(B) * heads * N * K * sizeof(float));
+        off = align_up(off + static_cast<size_t>(B) * heads * N * Kl[l] * sizeof(float));
     }
     L->total = off > kAlign ? off : kAlign;   // nonzero for every valid problem
     return QTA_OK;
@@ -164,17 +184,35 @@ qta_status qta_level_dims(int H, int W, int levels, int* Hl, int* Wl)
     return dims(H, W, levels, Hl, Wl);
 }
 
+qta_status qta_get_workspace_layout_levels(int B, int heads, int H, int W, int d, int levels, const int* K_levels,
+                                           int v_supplied, qta_dtype dtype, qta_workspace_layout* out)
+{
+    if (!out) return QTA_ERR_INVALID;
+    return layout(B, heads, H, W, d, levels, K_levels, v_supplied != 0, dtype, out);
+}
+
+size_t qta_workspace_bytes_levels(int B, int heads, int H, int W, int d, int levels, const int* K_levels,
+                                  int v_supplied, qta_dtype dtype)
+{
+    qta_workspace_layout L;
+    if (layout(B, heads, H, W, d, levels, K_levels, v_supplied != 0, dtype, &L) != QTA_OK) return 0;
+    return L.total;
+}
+
 qta_status qta_get_workspace_layout(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype,
                                     qta_workspace_layout* out)
 {
     if (!out) return QTA_ERR_INVALID;
-    return layout(B, heads, H, W, d, levels, K, dtype, out);
+    if (K <= 0) return QTA_ERR_INVALID;
+    int Kl[QTA_MAX_LEVELS];
+    for (int l = 0; l < QTA_MAX_LEVELS; ++l) Kl[l] = K;
+    return layout(B, heads, H, W, d, levels, Kl, false, dtype, out);
 }
 
 size_t qta_workspace_bytes(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype)
 {
     qta_workspace_layout L;
-    if (layout(B, heads, H, W, d, levels, K, dtype, &L) != QTA_OK) return 0;
+    if (qta_get_workspace_layout(B, heads, H, W, d, levels, K, dtype, &L) != QTA_OK) return 0;
     return L.total;
 }
 
@@ -263,7 +301,8 @@ qta_status qta_fine_attn(const void* ql, const void* kl, const void* vl, int B, 
     a.Hp = (Hl + 1) / 2;
     a.Wp = (Wl + 1) / 2;
     a.C = heads * d;
-    a.K = K;
+    a.Kp = K;
+    a.Ks = K;
     a.scale = resolve_scale(scale, d);
     a.parent_idx = parent_idx;
     a.parent_key = parent_key;
@@ -301,7 +340,8 @@ qta_status qta_finest_attn(const void* q0, const void* k0, const void* v0, int B
     a.Hp = Hl[1];
     a.Wp = Wl[1];
     a.C = heads * d;
-    a.K = K;
+    a.Kp = K;
+    a.Ks = 0;
     a.scale = resolve_scale(scale, d);
     a.parent_idx = parent_idx;
     a.parent_key = parent_key;
@@ -318,17 +358,23 @@ qta_status qta_finest_attn(const void* q0, const void* k0, const void* v0, int B
                                           static_cast<hipStream_t>(stream)));
 }
 
-qta_status qta_forward(const void* q, const void* k, const void* v, const float* w, int B, int heads, int H, int W,
-                       int d, int levels, int K, qta_variant variant, qta_dtype dtype, float scale, void* out,
-                       void* workspace, size_t workspace_bytes, void* stream)
+qta_status qta_forward_levels(const void* q, const void* k, const void* v, const void* const* v_levels, const float* w,
+                              int B, int heads, int H, int W, int d, int levels, const int* K_levels,
+                              qta_variant variant, qta_dtype dtype, float scale, void* out, void* workspace,
+                              size_t workspace_bytes, void* stream)
 {
-    qta_status st = check_problem(B, heads, d, K, variant, dtype);
+    qta_status st = check_problem(B, heads, d, 1, variant, dtype);
     if (st != QTA_OK) return st;
     if (!q || !k || !v || !out) return QTA_ERR_INVALID;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return QTA_ERR_INVALID;
+    const bool v_supplied = v_levels != nullptr;
+    if (v_supplied)
+        for (int l = 1; l < levels && l < QTA_MAX_LEVELS; ++l)
+            if (!v_levels[l] || !aligned16(v_levels[l])) return QTA_ERR_INVALID;
     qta_workspace_layout L;
-    st = layout(B, heads, H, W, d, levels, K, dtype, &L);
+    st = layout(B, heads, H, W, d, levels, K_levels, v_supplied, dtype, &L);
     if (st != QTA_OK) return st;
+    const int* Kl = K_levels;
     if (levels > 1) {
         if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return QTA_ERR_INVALID;
         if (workspace_bytes < L.total) return QTA_ERR_WORKSPACE;
@@ -347,8 +393,10 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
     for (int l = 1; l < levels; ++l) {
         pyr[0][l] = ws + L.q[l];
         pyr[1][l] = ws + L.k[l];
-        pyr[2][l] = ws + L.v[l];
-        for (int t = 0; t < 3; ++t) lv[t][l] = pyr[t][l];
+        pyr[2][l] = v_supplied ? nullptr : ws + L.v[l];
+        lv[0][l] = pyr[0][l];
+        lv[1][l] = pyr[1][l];
+        lv[2][l] = v_supplied ? v_levels[l] : pyr[2][l];
     }
     auto msg = [&](int l) { return reinterpret_cast<float*>(ws + L.msg[l]); };
     auto sidx = [&](int l) { return reinterpret_cast<int32_t*>(ws + L.sel_idx[l]); };
@@ -359,7 +407,7 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
         const void* src[3] = {q, k, v};
         const int chunks = static_cast<int>(static_cast<size_t>(C) * dtype_bytes(dtype) / 16);
         const int head_chunks = static_cast<int>(static_cast<size_t>(d) * dtype_bytes(dtype) / 16);
-        hipError_t e = run_pyramid(src, pyr, 3, B, L.H, L.W, L.blocked, levels, chunks,
+        hipError_t e = run_pyramid(src, pyr, v_supplied ? 2 : 3, B, L.H, L.W, L.blocked, levels, chunks,
                                    head_chunks, use_bf16, s);
         if (e != hipSuccess) return QTA_ERR_HIP;
     }
@@ -382,7 +430,7 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
             a.out = out;
             a.w = w;
         } else {
-            a.K = K;
+            a.K = Kl[c];
             a.msg = msg(c);
             a.sel_idx = sidx(c);
             a.sel_key = skey(c);
@@ -407,7 +455,8 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
         a.Hp = L.H[l + 1];
         a.Wp = L.W[l + 1];
         a.C = C;
-        a.K = K;
+        a.Kp = Kl[l + 1];
+        a.Ks = Kl[l];
         a.scale = tau;
         a.parent_idx = sidx(l + 1);
         a.parent_key = skey(l + 1);
@@ -433,7 +482,8 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
         a.Hp = L.H[1];
         a.Wp = L.W[1];
         a.C = C;
-        a.K = K;
+        a.Kp = Kl[1];
+        a.Ks = 0;
         a.scale = tau;
         a.parent_idx = sidx(1);
         a.parent_key = skey(1);
@@ -449,6 +499,18 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
         if (e != hipSuccess) return QTA_ERR_HIP;
     }
     return QTA_OK;
+}
+
+qta_status qta_forward(const void* q, const void* k, const void* v, const float* w, int B, int heads, int H, int W,
+                       int d, int levels, int K, qta_variant variant, qta_dtype dtype, float scale, void* out,
+                       void* workspace, size_t workspace_bytes, void* stream)
+{
+    if (K <= 0) return QTA_ERR_INVALID;
+    if (K > QTA_MAX_K) return QTA_ERR_UNSUPPORTED;
+    int Kl[QTA_MAX_LEVELS];
+    for (int l = 0; l < QTA_MAX_LEVELS; ++l) Kl[l] = K;
+    return qta_forward_levels(q, k, v, nullptr, w, B, heads, H, W, d, levels, Kl, variant, dtype, scale, out, workspace,
+                              workspace_bytes, stream);
 }
 
 }  // extern "C"

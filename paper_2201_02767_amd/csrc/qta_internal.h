@@ -98,7 +98,9 @@ struct FineArgs {
     const void* v;
     bool q_blocked;             // queries of this level stored blocked (else NHWC)
     bool kv_blocked;            // keys and values of this level stored blocked (else NHWC)
-    int B, heads, H, W, Hp, Wp, C, K;
+    int B, heads, H, W, Hp, Wp, C;
+    int Kp;                     // keys each parent query kept: 4*Kp candidate slots per sibling group
+    int Ks;                     // keys this level keeps per query (levels above the finest)
     FastDiv div_Wp;             // division by Wp (flat parent index -> row)
     float scale;
     const int32_t* parent_idx;

@@ -16,8 +16,14 @@ not used):
              q, k, v are random linear maps of Gaussian-blurred (sigma 2 tokens) N(0,1) features.
   highres  - 2 x 200x336 (800x1333 image at 1/4), 2 heads x 32, bf16, 5 levels, K=16, QuadTree-B;
              generated like backbone. Its coarsest level (13x21) comes from ceil pooling.
+  matching_ksched - matching with the paper's K schedule for feature matching (Sec. 4.1.1): K = 8
+             at the finest selecting level, doubled at each coarser level (16 at the coarsest).
+  backbone_vgiven - backbone with V's coarser levels given as inputs, as in self-attention where a
+             stride-2 conv-norm-act layer builds them (Sec. 3.2); each level is an independent
+             N(0,1) map standing in for that layer's normalised output.
 
-Seeds: numpy PCG64 with seed = 1000 * config_number + tensor id (q=1, k=2, v=3, w=4, aux=5).
+Seeds: numpy PCG64 with seed = 1000 * config_number + tensor id (q=1, k=2, v=3, w=4, aux=5, and
+10 + l for the given V level l).
 All arrays are float32 ``[B, H, W, heads, d]``; for bf16 workloads the values are rounded to the
 nearest bfloat16 (ties to even), so they are exactly representable in bf16.
 """
@@ -38,10 +44,11 @@ class Workload:
     heads: int
     d: int
     levels: int
-    K: int
+    K: object         # one count for every level, or a tuple with one entry per level (entry 0 unused)
     variant: str      # "A" or "B"
     dtype: str        # "f32" or "bf16"
     kind: str         # generator: "iid_scaled", "shift", "disparity", "smooth"
+    v_given: bool = False   # V's coarser levels are inputs (make_v_levels) instead of pooled
 
     @property
     def tokens(self) -> int:
@@ -57,6 +64,8 @@ WORKLOADS = {
     "stereo": Workload("stereo", 3, 2, 120, 160, 8, 32, 4, 8, "B", "bf16", "disparity"),
     "backbone": Workload("backbone", 4, 32, 56, 56, 1, 64, 3, 8, "B", "bf16", "smooth"),
     "highres": Workload("highres", 5, 2, 200, 336, 2, 32, 5, 16, "B", "bf16", "smooth"),
+    "matching_ksched": Workload("matching_ksched", 2, 1, 60, 80, 8, 32, 3, (0, 8, 16), "B", "f32", "shift"),
+    "backbone_vgiven": Workload("backbone_vgiven", 4, 32, 56, 56, 1, 64, 3, 8, "B", "bf16", "smooth", True),
 }
 
 
@@ -140,3 +149,15 @@ def make_level_weights(wl: Workload, seed_offset: int = 0) -> np.ndarray:
     g = _rng(wl, 4, seed_offset).standard_normal((wl.B, wl.H * wl.W, wl.heads, wl.levels))
     e = np.exp(g - g.max(axis=-1, keepdims=True))
     return (e / e.sum(axis=-1, keepdims=True)).astype(np.float32)
+
+
+def make_v_levels(wl: Workload, seed_offset: int = 0) -> list:
+    """Given V levels for a workload with ``v_given``: entry l (1 <= l < levels) is float32
+    ``[B, H_l, W_l, heads, d]`` with H_l, W_l by ceil halving; entry 0 is None (level 0 is v)."""
+    out = [None]
+    H, W = wl.H, wl.W
+    for l in range(1, wl.levels):
+        H, W = (H + 1) // 2, (W + 1) // 2
+        x = _rng(wl, 10 + l, seed_offset).standard_normal((wl.B, H, W, wl.heads, wl.d), dtype=np.float32)
+        out.append(round_bf16(x) if wl.dtype == "bf16" else x)
+    return out

@@ -33,6 +33,7 @@ class WorkspaceLayout(ctypes.Structure):
         ("H", ctypes.c_int * MAX_LEVELS),
         ("W", ctypes.c_int * MAX_LEVELS),
         ("blocked", ctypes.c_int * MAX_LEVELS),
+        ("K", ctypes.c_int * MAX_LEVELS),
         ("q", ctypes.c_size_t * MAX_LEVELS),
         ("k", ctypes.c_size_t * MAX_LEVELS),
         ("v", ctypes.c_size_t * MAX_LEVELS),
@@ -52,7 +53,11 @@ _SIGS = {
     "qta_level_dims": ([_I, _I, _I, _P, _P], _I),
     "qta_get_workspace_layout": ([_I, _I, _I, _I, _I, _I, _I, _I, ctypes.POINTER(WorkspaceLayout)], _I),
     "qta_workspace_bytes": ([_I, _I, _I, _I, _I, _I, _I, _I], ctypes.c_size_t),
+    "qta_get_workspace_layout_levels": ([_I, _I, _I, _I, _I, _I, _P, _I, _I, ctypes.POINTER(WorkspaceLayout)], _I),
+    "qta_workspace_bytes_levels": ([_I, _I, _I, _I, _I, _I, _P, _I, _I], ctypes.c_size_t),
     "qta_forward": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, ctypes.c_size_t, _P], _I),
+    "qta_forward_levels": ([_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _F, _P, _P, ctypes.c_size_t, _P],
+                           _I),
     "qta_build_pyramid": ([_P, _P, _I, _I, _I, _I, _I, _I, _P], _I),
     "qta_coarse_attn": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P], _I),
     "qta_topk": ([_P, _P, _I, _I, _I, _P, _P, _P], _I),
@@ -123,15 +128,35 @@ def level_dims(H: int, W: int, levels: int) -> list[tuple[int, int]]:
     return [(hl[i], wl[i]) for i in range(levels)]
 
 
-def workspace_layout(B, heads, H, W, d, levels, K, dtype: torch.dtype) -> WorkspaceLayout:
+def k_levels(K, levels: int) -> list[int]:
+    """One K for every level, or a sequence whose entry l (1 <= l < levels) is level l's K (entry 0
+    unused), as the list the library reads."""
+    if isinstance(K, int):
+        return [K] * levels
+    Kl = [int(x) for x in K]
+    if len(Kl) != levels:
+        raise ValueError(f"K needs one entry per level ({levels}), got {len(Kl)}")
+    Kl[0] = 0
+    return Kl
+
+
+def _k_table(Kl):
+    return (ctypes.c_int * MAX_LEVELS)(*Kl)
+
+
+def workspace_layout(B, heads, H, W, d, levels, K, dtype: torch.dtype, v_supplied: bool = False) -> WorkspaceLayout:
     lay = WorkspaceLayout()
-    _check("qta_get_workspace_layout",
-           lib().qta_get_workspace_layout(B, heads, H, W, d, levels, K, _DTYPES[dtype], ctypes.byref(lay)))
+    tbl = _k_table(k_levels(K, levels))
+    _check("qta_get_workspace_layout_levels",
+           lib().qta_get_workspace_layout_levels(B, heads, H, W, d, levels, ctypes.addressof(tbl), int(v_supplied),
+                                                 _DTYPES[dtype], ctypes.byref(lay)))
     return lay
 
 
-def workspace_bytes(B, heads, H, W, d, levels, K, dtype: torch.dtype) -> int:
-    return int(lib().qta_workspace_bytes(B, heads, H, W, d, levels, K, _DTYPES[dtype]))
+def workspace_bytes(B, heads, H, W, d, levels, K, dtype: torch.dtype, v_supplied: bool = False) -> int:
+    tbl = _k_table(k_levels(K, levels))
+    return int(lib().qta_workspace_bytes_levels(B, heads, H, W, d, levels, ctypes.addressof(tbl), int(v_supplied),
+                                                _DTYPES[dtype]))
 
 
 # ------------------------------------------------------------------------------------------------
@@ -139,19 +164,27 @@ def workspace_bytes(B, heads, H, W, d, levels, K, dtype: torch.dtype) -> int:
 # ------------------------------------------------------------------------------------------------
 
 class Plan:
-    """Pre-allocated output and workspace for repeated forwards of one problem shape."""
+    """Pre-allocated output and workspace for repeated forwards of one problem shape.
 
-    def __init__(self, B, H, W, heads, d, *, levels, K, variant, dtype, device, scale=None):
+    ``K``: one count for every level, or one entry per level (entry l is level l's K, entry 0
+    unused). ``v_supplied``: V's coarser levels come from the caller (``v_levels`` of run/prepare).
+    """
+
+    def __init__(self, B, H, W, heads, d, *, levels, K, variant, dtype, device, scale=None, v_supplied=False):
         self.B, self.H, self.W, self.heads, self.d = B, H, W, heads, d
-        self.levels, self.K, self.variant, self.dtype = levels, K, variant, dtype
+        self.levels, self.variant, self.dtype = levels, variant, dtype
+        self.K_levels = k_levels(K, levels)
+        self.K = K if isinstance(K, int) else self.K_levels
         self.scale = scale
+        self.v_supplied = bool(v_supplied)
         self.device = torch.device(device)
-        self.layout = workspace_layout(B, heads, H, W, d, levels, K, dtype)
+        self.layout = workspace_layout(B, heads, H, W, d, levels, K, dtype, self.v_supplied)
+        self._k_tbl = _k_table(self.K_levels)
         nbytes = max(int(self.layout.total), 256)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
         self.out = torch.empty((B, H, W, heads, d), dtype=dtype, device=self.device)
 
-    def run(self, q, k, v, w=None, stream=None):
+    def _args(self, q, k, v, w, v_levels):
         for name, t in (("q", q), ("k", k), ("v", v)):
             _require(t, name, self.dtype, 5)
             if tuple(t.shape) != (self.B, self.H, self.W, self.heads, self.d):
@@ -160,32 +193,43 @@ class Plan:
             _require(w, "w", torch.float32, 4)
             if tuple(w.shape) != (self.B, self.H * self.W, self.heads, self.levels):
                 raise ValueError(f"w has shape {tuple(w.shape)}")
+        if (v_levels is not None) != self.v_supplied:
+            raise ValueError("v_levels must be given exactly when the plan was made with v_supplied=True")
+        vtbl = None
+        if v_levels is not None:
+            vtbl = (ctypes.c_void_p * MAX_LEVELS)()
+            for l in range(1, self.levels):
+                t = v_levels[l]
+                _require(t, f"v_levels[{l}]", self.dtype, 5)
+                if tuple(t.shape) != (self.B, self.layout.H[l], self.layout.W[l], self.heads, self.d):
+                    raise ValueError(f"v_levels[{l}] has shape {tuple(t.shape)}")
+                vtbl[l] = t.data_ptr()
+        return vtbl
+
+    def run(self, q, k, v, w=None, stream=None, v_levels=None):
+        vtbl = self._args(q, k, v, w, v_levels)
         s = _stream(self.device) if stream is None else ctypes.c_void_p(stream)
-        _check("qta_forward", lib().qta_forward(
-            _ptr(q), _ptr(k), _ptr(v), _ptr(w), self.B, self.heads, self.H, self.W, self.d, self.levels, self.K,
-            _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), _ptr(self.out),
-            _ptr(self.workspace), self.workspace.numel(), s))
+        _check("qta_forward_levels", lib().qta_forward_levels(
+            _ptr(q), _ptr(k), _ptr(v), ctypes.addressof(vtbl) if vtbl is not None else None, _ptr(w), self.B,
+            self.heads, self.H, self.W, self.d, self.levels, ctypes.addressof(self._k_tbl), _VARIANTS[self.variant],
+            _DTYPES[self.dtype], _scale(self.scale), _ptr(self.out), _ptr(self.workspace), self.workspace.numel(), s))
         return self.out
 
-    def prepare(self, q, k, v, w=None):
+    def prepare(self, q, k, v, w=None, v_levels=None):
         """Validate once and return a zero-argument callable that re-issues this forward on the
         current stream (for timing loops and graph capture: no per-call Python checks)."""
-        for name, t in (("q", q), ("k", k), ("v", v)):
-            _require(t, name, self.dtype, 5)
-            if tuple(t.shape) != (self.B, self.H, self.W, self.heads, self.d):
-                raise ValueError(f"{name} has shape {tuple(t.shape)}")
-        if w is not None:
-            _require(w, "w", torch.float32, 4)
-        fn = lib().qta_forward
-        args = (_ptr(q), _ptr(k), _ptr(v), _ptr(w), self.B, self.heads, self.H, self.W, self.d, self.levels, self.K,
+        vtbl = self._args(q, k, v, w, v_levels)
+        fn = lib().qta_forward_levels
+        args = (_ptr(q), _ptr(k), _ptr(v), ctypes.addressof(vtbl) if vtbl is not None else None, _ptr(w), self.B,
+                self.heads, self.H, self.W, self.d, self.levels, ctypes.addressof(self._k_tbl),
                 _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), _ptr(self.out),
                 _ptr(self.workspace), self.workspace.numel(), _stream(self.device))
-        keep = (q, k, v, w)
+        keep = (q, k, v, w, vtbl, v_levels)
 
         def call():
             st = fn(*args)
             if st != 0:
-                _check("qta_forward", st)
+                _check("qta_forward_levels", st)
             return keep
         return call
 
@@ -199,7 +243,7 @@ class Plan:
         sidx, skey = self.selection(1)
         msgs = [self.message(j) for j in range(1, self.levels)]
         table = (ctypes.c_void_p * (self.levels - 1))(*[m.data_ptr() for m in msgs])
-        args = (_ptr(q), _ptr(k), _ptr(v), self.B, self.heads, self.H, self.W, self.d, self.K,
+        args = (_ptr(q), _ptr(k), _ptr(v), self.B, self.heads, self.H, self.W, self.d, self.K_levels[1],
                 _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), _ptr(sidx), _ptr(skey),
                 self.levels, ctypes.addressof(table), _ptr(w), _ptr(self.out), _stream(self.device))
         keep = (q, k, v, w, table, msgs)
@@ -241,18 +285,20 @@ class Plan:
 
     def selection(self, level: int):
         lay = self.layout
-        shape = (self.B, self.heads, lay.H[level] * lay.W[level], self.K)
+        shape = (self.B, self.heads, lay.H[level] * lay.W[level], lay.K[level])
         return (self._view(lay.sel_idx[level], shape, torch.int32),
                 self._view(lay.sel_key[level], shape, torch.float32))
 
 
-def forward(q, k, v, *, levels: int, K: int, variant: str, w=None, scale=None) -> torch.Tensor:
-    """QuadTree attention forward; returns ``out`` [B, H, W, heads, d] in q's dtype."""
+def forward(q, k, v, *, levels: int, K, variant: str, w=None, scale=None, v_levels=None) -> torch.Tensor:
+    """QuadTree attention forward; returns ``out`` [B, H, W, heads, d] in q's dtype. ``K``: one count
+    or one per level (entry 0 unused); ``v_levels``: None, or a list whose entry l (l >= 1) is V at
+    level l, [B, H_l, W_l, heads, d]."""
     _require(q, "q", None, 5)
     B, H, W, heads, d = q.shape
     plan = Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=q.dtype, device=q.device,
-                scale=scale)
-    return plan.run(q, k, v, w)
+                scale=scale, v_supplied=v_levels is not None)
+    return plan.run(q, k, v, w, v_levels=v_levels)
 
 
 # ------------------------------------------------------------------------------------------------

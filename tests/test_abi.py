@@ -183,3 +183,50 @@ def test_fast_division_parameters_are_exact(d):
     q = (hi + n) >> np.uint64(s)
     assert np.all(hi + n < (1 << 32))
     assert np.array_equal(q, n // np.uint64(d))
+
+
+def _klv(*vals):
+    t = (ctypes.c_int * 16)()
+    for i, x in enumerate(vals):
+        t[i] = x
+    return t
+
+
+def test_layout_with_k_schedule_and_supplied_v():
+    """Selections are sized by each level's K; a level is blocked only when the kernel that gathers
+    it takes the blocked path (4*K of its parents <= 64); with V supplied no V level is stored and
+    nothing is blocked."""
+    lib = P.lib()
+    B, heads, H, W, d, L = 2, 2, 60, 80, 32, 4
+    for Ks, blocked in (([0, 4, 16, 8], [0, 1, 1, 0]), ([0, 8, 20, 8], [0, 0, 1, 0])):
+        lay = P.workspace_layout(B, heads, H, W, d, L, Ks, torch.float32)
+        assert [lay.blocked[l] for l in range(L)] == blocked
+        assert [lay.K[l] for l in range(1, L)] == Ks[1:]
+        for l in range(1, L):
+            N = lay.H[l] * lay.W[l]
+            assert lay.sel_key[l] - lay.sel_idx[l] >= B * heads * N * Ks[l] * 4
+        assert P.workspace_bytes(B, heads, H, W, d, L, Ks, torch.float32) == lay.total
+    lay_v = P.workspace_layout(B, heads, H, W, d, L, [0, 4, 16, 8], torch.float32, v_supplied=True)
+    assert all(lay_v.v[l] == 0 and lay_v.blocked[l] == 0 for l in range(L))
+    assert lay_v.total < P.workspace_layout(B, heads, H, W, d, L, [0, 4, 16, 8], torch.float32).total
+
+
+def test_forward_levels_validation():
+    lib = P.lib()
+
+    def fwd(Kl, vtbl=None, L=3):
+        return lib.qta_forward_levels(FAKE, FAKE, FAKE, vtbl, None, 1, 1, 16, 16, 32, L, Kl, VA, F32, 0.0, FAKE,
+                                      FAKE, 0, None)
+    assert fwd(ctypes.addressof(_klv(0, 4, 8))) == WORKSPACE               # valid shape, zero workspace
+    assert fwd(None) == INVALID                                            # K table required for L > 1
+    assert fwd(ctypes.addressof(_klv(0, 4, 0))) == INVALID
+    assert fwd(ctypes.addressof(_klv(0, 65, 4))) == UNSUPPORTED
+    assert fwd(ctypes.addressof(_klv(9, 4, 8))) == WORKSPACE               # entry 0 is not read
+    vt = (ctypes.c_void_p * 16)()
+    vt[1] = FAKE
+    assert fwd(ctypes.addressof(_klv(0, 4, 8)), ctypes.addressof(vt)) == INVALID       # level 2 missing
+    vt[2] = FAKE + 8
+    assert fwd(ctypes.addressof(_klv(0, 4, 8)), ctypes.addressof(vt)) == INVALID       # misaligned
+    vt[2] = FAKE
+    assert fwd(ctypes.addressof(_klv(0, 4, 8)), ctypes.addressof(vt)) == WORKSPACE
+    assert lib.qta_workspace_bytes_levels(1, 1, 16, 16, 32, 3, ctypes.addressof(_klv(0, 4, 65)), 0, F32) == 0

@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import paper_2201_02767_amd as P
-from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_qkv, round_bf16
+from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_qkv, make_v_levels, round_bf16
 from oracle import oracle as O
 from tests import brute
 from tests.parity import TOL, check_selection, rel_err, to_np
@@ -51,24 +51,30 @@ def dev_t(x, dtype, dev):
 # end-to-end protocol
 # ------------------------------------------------------------------------------------------------
 
-def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=None, label=""):
-    """GPU forward vs teacher-forced oracle; returns a dict of the measured agreement."""
+def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=None, label="", v_levels=None):
+    """GPU forward vs teacher-forced oracle; returns a dict of the measured agreement. ``K``: one
+    count or one per level; ``v_levels``: None or the caller's V levels (numpy, entry l >= 1)."""
     B, H, W, heads, d = q.shape
-    announce(f"forward {label} B={B} H={H} W={W} heads={heads} d={d} L={levels} K={K} {variant} {dtype}")
-    plan = P.Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=TDT[dtype], device=dev, scale=scale)
+    announce(f"forward {label} B={B} H={H} W={W} heads={heads} d={d} L={levels} K={K} {variant} {dtype}"
+             f"{' V levels given' if v_levels is not None else ''}")
+    plan = P.Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=TDT[dtype], device=dev, scale=scale,
+                  v_supplied=v_levels is not None)
+    Kl = P.k_levels(K, levels)
     wt = None if w is None else torch.from_numpy(w).to(dev)
-    out = plan.run(dev_t(q, dtype, dev), dev_t(k, dtype, dev), dev_t(v, dtype, dev), wt)
+    vl = None if v_levels is None else [None] + [dev_t(v_levels[l], dtype, dev) for l in range(1, levels)]
+    out = plan.run(dev_t(q, dtype, dev), dev_t(k, dtype, dev), dev_t(v, dtype, dev), wt, v_levels=vl)
     torch.cuda.synchronize()
     g_out = to_np(out)
     g_sel = [None] + [to_np(plan.selection(l)[0]) for l in range(1, levels)]
     ref = O.forward(q, k, v, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale,
-                    forced=g_sel, want_candidates=True, want_pyramids=True)
+                    forced=g_sel, want_candidates=True, want_pyramids=True, v_levels=v_levels)
     res = {"sel": {}, "msg": {}}
     for l in range(1, levels):
-        for name in "qkv":
+        for name in ("qk" if v_levels is not None else "qkv"):
             gp = to_np(plan.pyramid(name, l)).reshape(ref["pyr_" + name][l].shape)
             assert np.array_equal(gp, ref["pyr_" + name][l]), f"pyramid {name} level {l} differs"
-        chk = check_selection(g_sel[l], ref["cand_idx"][l], ref["cand_key"][l], K)
+        assert g_sel[l].shape[-1] == Kl[l]
+        chk = check_selection(g_sel[l], ref["cand_idx"][l], ref["cand_key"][l], Kl[l])
         assert chk["bad"] == 0, f"level {l} selection: {chk}"
         res["sel"][l] = chk
         e = rel_err(to_np(plan.message(l)), ref["msg"][l])
@@ -286,16 +292,18 @@ def test_explicit_scale(dev):
 
 
 # ------------------------------------------------------------------------------------------------
-# the five workloads at full size
+# the workloads at full size
 # ------------------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["tiny", "matching", "stereo", "backbone", "highres"])
+@pytest.mark.parametrize("name", ["tiny", "matching", "stereo", "backbone", "highres", "matching_ksched",
+                                  "backbone_vgiven"])
 def test_workload_full_size(dev, name):
     wl = WORKLOADS[name]
     q, k, v = make_qkv(wl)
     w = make_level_weights(wl) if wl.variant == "B" else None
+    vl = make_v_levels(wl) if wl.v_given else None
     res, _, _ = run_and_compare(dev, q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w,
-                                label=name)
+                                label=name, v_levels=vl)
     announce(f"{name}: out err {res['out']:.2e}; msg err {res['msg']}; selections {res['sel']}")
 
 
@@ -315,3 +323,54 @@ def test_tiny_every_key_kept_matches_closed_forms(dev, variant):
     q, k, v = make_qkv(wl)
     w = make_level_weights(wl) if variant == "B" else None
     run_and_compare(dev, q, k, v, levels=wl.levels, K=64, variant=variant, dtype="f32", w=w, label="tiny K=64")
+
+
+# ------------------------------------------------------------------------------------------------
+# per-level K (Sec. 4.1.1 schedule) and caller-supplied V levels (Sec. 3.2)
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant,dtype,B,H,W,heads,d,Ks", [
+    ("B", "f32", 1, 60, 80, 8, 32, [0, 8, 16]),        # the feature-matching schedule at full size
+    ("A", "f32", 2, 37, 29, 2, 32, [0, 4, 8, 16]),     # doubling over 4 levels, ragged map
+    ("B", "bf16", 1, 45, 38, 3, 64, [0, 16, 8, 4]),    # shrinking K going up
+    ("A", "bf16", 1, 33, 47, 1, 32, [0, 2, 20, 5]),    # 4K_l above 64 at one level: wide kernel there
+    ("B", "f32", 2, 16, 16, 1, 32, [0, 16, 64]),       # every coarse key kept, 64 candidates below
+])
+def test_forward_k_schedule(dev, variant, dtype, B, H, W, heads, d, Ks):
+    L = len(Ks)
+    q, k, v = rand_qkv(500 + sum(Ks) + H, B, H, W, heads, d, dtype)
+    w = np.random.default_rng(9).random((B, H * W, heads, L)).astype(np.float32) if variant == "B" else None
+    run_and_compare(dev, q, k, v, levels=L, K=Ks, variant=variant, dtype=dtype, w=w, label=f"K schedule {Ks}")
+
+
+@pytest.mark.parametrize("variant,dtype,B,H,W,heads,d,L,K", [
+    ("B", "bf16", 4, 56, 56, 1, 64, 3, 8),             # backbone-like self-attention, V levels given
+    ("A", "f32", 2, 37, 29, 2, 32, 4, 4),
+    ("B", "f32", 1, 25, 31, 2, 32, 3, [0, 4, 8]),
+])
+def test_forward_supplied_v_levels(dev, variant, dtype, B, H, W, heads, d, L, K):
+    q, k, v = rand_qkv(600 + H * W + L, B, H, W, heads, d, dtype)
+    dims = O.level_dims(H, W, L)
+    rng = np.random.default_rng(77)
+    vl = [None]
+    for l in range(1, L):
+        x = rng.standard_normal((B, dims[l][0], dims[l][1], heads, d)).astype(np.float32)
+        vl.append(round_bf16(x) if dtype == "bf16" else x)
+    w = np.random.default_rng(9).random((B, H * W, heads, L)).astype(np.float32) if variant == "B" else None
+    run_and_compare(dev, q, k, v, levels=L, K=K, variant=variant, dtype=dtype, w=w, v_levels=vl,
+                    label="V levels given")
+
+
+def test_supplied_pooled_v_levels_reproduce_default(dev):
+    """Handing the library its own pooled V levels gives the default forward's output bit for bit."""
+    B, H, W, heads, d, L, K = 1, 30, 22, 2, 32, 3, 8
+    q, k, v = rand_qkv(700, B, H, W, heads, d, "f32")
+    announce("V levels given = pooled V")
+    plan = P.Plan(B, H, W, heads, d, levels=L, K=K, variant="B", dtype=torch.float32, device=dev)
+    tq, tk, tv = (dev_t(x, "f32", dev) for x in (q, k, v))
+    ref = plan.run(tq, tk, tv).clone()
+    vl = [None] + [plan.pyramid("v", l).contiguous() for l in range(1, L)]
+    plan2 = P.Plan(B, H, W, heads, d, levels=L, K=K, variant="B", dtype=torch.float32, device=dev, v_supplied=True)
+    out = plan2.run(tq, tk, tv, v_levels=vl)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
