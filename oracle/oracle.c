@@ -34,7 +34,11 @@
  *     level and doubles it at each coarser one, Sec. 4.1.1): K_l keys are kept by every query of
  *     level l, and a query of level l-1 meets the 2x2 children of its parent's K_l keys;
  *   - V's coarser levels may be supplied by the caller instead of pooled (the paper builds them
- *     with a conv-norm-act layer for self-attention, Sec. 3.2); they are then used as given.
+ *     with a conv-norm-act layer for self-attention, Sec. 3.2); they are then used as given;
+ *   - multiscale position encoding (Sec. 3.2, after the locally-enhanced positional encoding it
+ *     cites): an unshared 3x3 depth-wise convolution of V^l (zero padding, optional bias) at each
+ *     level, added to level l's message at the query's own position before the levels are
+ *     combined.
  *
  * Arithmetic: every dot product, softmax and message sum is in double, from the stored (already
  * rounded) pyramid values. Pyramids are computed in fp32 exactly as stated above.
@@ -62,6 +66,8 @@ typedef struct {
     int B, heads, H, W, d, L, K, variant, dtype;
     const int* K_levels;          /* NULL (K at every level), or entry l in 1..L-1: K_l */
     const float* const* v_levels; /* NULL (pooled V), or entry l in 1..L-1: V at level l, [B][H_l][W_l][C] */
+    const float* pe_weight;       /* NULL (no position encoding), or [L][C][3][3] depth-wise kernels */
+    const float* pe_bias;         /* NULL (no bias), or [L][C]; used only with pe_weight */
     double scale;                 /* <= 0 means 1/sqrt(d) */
     const int32_t* const* forced; /* NULL, or per level l in 1..L-1: [B][heads][N_l][K_l] */
     /* outputs, all optional (NULL pointers or NULL entries are skipped) */
@@ -424,6 +430,28 @@ int qo_forward(const qo_forward_args* a)
                     }
             }
         }
+
+    /* ---- multiscale position encoding: m^l_i += sum over the 3x3 window of w_l[c] * V^l[c] (+ b_l[c]),
+     * zero outside the map, for every level and channel ---- */
+    if (a->pe_weight) {
+        for (int l = 0; l < L; ++l) {
+            const int Hh = Hl[l], Ww = Wl[l];
+            for (int b = 0; b < B; ++b)
+                for (int y = 0; y < Hh; ++y)
+                    for (int x = 0; x < Ww; ++x)
+                        for (int c = 0; c < C; ++c) {
+                            const float* kw = a->pe_weight + ((size_t)l * C + c) * 9;
+                            double acc2 = a->pe_bias ? (double)a->pe_bias[(size_t)l * C + c] : 0.0;
+                            for (int ky = 0; ky < 3; ++ky)
+                                for (int kx = 0; kx < 3; ++kx) {
+                                    const int yy = y + ky - 1, xx = x + kx - 1;
+                                    if (yy < 0 || yy >= Hh || xx < 0 || xx >= Ww) continue;
+                                    acc2 += (double)kw[ky * 3 + kx] * (double)pv[l][(((size_t)b * Hh + yy) * Ww + xx) * C + c];
+                                }
+                            msg[l][((size_t)b * Nl[l] + (size_t)y * Ww + x) * C + c] += acc2;
+                        }
+        }
+    }
 
     /* ---- combination: Eq. (2) for A, Eq. (5) for B; a finest query takes the message of its
      * ancestor at every level, since sub-patches share their parent's coarse messages ---- */

@@ -39,6 +39,7 @@ class _Args(ctypes.Structure):
         ("B", ctypes.c_int), ("heads", ctypes.c_int), ("H", ctypes.c_int), ("W", ctypes.c_int),
         ("d", ctypes.c_int), ("L", ctypes.c_int), ("K", ctypes.c_int), ("variant", ctypes.c_int),
         ("dtype", ctypes.c_int), ("K_levels", ctypes.c_void_p), ("v_levels", ctypes.c_void_p),
+        ("pe_weight", ctypes.c_void_p), ("pe_bias", ctypes.c_void_p),
         ("scale", ctypes.c_double),
         ("forced", ctypes.c_void_p),
         ("out", ctypes.c_void_p),
@@ -96,13 +97,16 @@ def _ptr_table(arrays):
 
 
 def forward(q, k, v, *, levels: int, K, variant: str, dtype: str = "f32", w=None, scale=None,
-            forced=None, want_candidates: bool = False, want_pyramids: bool = False, v_levels=None) -> dict:
+            forced=None, want_candidates: bool = False, want_pyramids: bool = False, v_levels=None,
+            pe_weight=None, pe_bias=None) -> dict:
     """Run the oracle. ``q, k, v``: float32 ``[B, H, W, heads, d]`` (values representable in dtype).
 
     ``K``: one count for every level, or a sequence indexed by level whose entry l (1 <= l < levels)
     is the number of keys kept at level l (entry 0 is ignored).
     ``v_levels``: optional list indexed by level; entry l (1 <= l < levels) is V at level l,
     ``[B, H_l, W_l, heads, d]``, used instead of pooling V.
+    ``pe_weight``: optional float32 ``[levels, heads*d, 3, 3]`` depth-wise kernels of the multiscale
+    position encoding; ``pe_bias``: optional float32 ``[levels, heads*d]``.
     ``forced``: optional list indexed by level; entry l (1 <= l < levels) is an int32
     ``[B, heads, N_l, K_l]`` selection that replaces the oracle's own choice at that level.
     Returns a dict with ``out`` ``[B,H,W,heads,d]`` and per-level lists ``msg`` ``[B,N_l,heads,d]``,
@@ -179,6 +183,17 @@ def forward(q, k, v, *, levels: int, K, variant: str, dtype: str = "f32", w=None
     args.B, args.heads, args.H, args.W, args.d = B, NH, H, W, d
     args.L, args.K, args.variant, args.dtype = L, Kl[1] if L > 1 else Kl[0], VARIANTS[variant], DTYPES[dtype]
     args.K_levels = ctypes.addressof(K_tbl)
+    pe_keep = []
+    if pe_weight is not None:
+        pw = np.ascontiguousarray(pe_weight, dtype=np.float32)
+        assert pw.shape == (L, C, 3, 3), pw.shape
+        pe_keep.append(pw)
+        args.pe_weight = pw.ctypes.data
+        if pe_bias is not None:
+            pb = np.ascontiguousarray(pe_bias, dtype=np.float32)
+            assert pb.shape == (L, C), pb.shape
+            pe_keep.append(pb)
+            args.pe_bias = pb.ctypes.data
     args.v_levels = ctypes.addressof(v_tbl) if v_tbl is not None else None
     args.scale = float(scale) if scale is not None else 0.0
     args.out = out.ctypes.data

@@ -71,13 +71,30 @@ def _top(keys: dict, K: int) -> list:
     return [t for t, _ in order[:K]]
 
 
-def brute_quadtree(q, k, v, L: int, K, variant: str, tau: float, w=None, v_levels=None) -> np.ndarray:
+def depthwise3x3(x: np.ndarray, kern: np.ndarray, bias=None) -> np.ndarray:
+    """[B,H,W,C] -> [B,H,W,C]: 3x3 depth-wise cross-correlation with zero padding, kern [C,3,3]."""
+    B, H, W, C = x.shape
+    xp = np.zeros((B, H + 2, W + 2, C))
+    xp[:, 1:-1, 1:-1] = x
+    out = np.zeros((B, H, W, C))
+    for ky in range(3):
+        for kx in range(3):
+            out += xp[:, ky:ky + H, kx:kx + W] * np.asarray(kern, np.float64)[:, ky, kx]
+    if bias is not None:
+        out += np.asarray(bias, np.float64)
+    return out
+
+
+def brute_quadtree(q, k, v, L: int, K, variant: str, tau: float, w=None, v_levels=None, pe_weight=None,
+                   pe_bias=None) -> np.ndarray:
     """Output [B, H, W, heads, d] of QuadTree attention, query by query, with explicit regions.
 
     q, k, v: [B, H, W, heads, d]; w (variant B): [B, H*W, heads, L] or None (=> 1/L).
     K: one count, or a list whose entry l is the number of keys kept at level l (l >= 1).
     v_levels: None (V pooled like Q and K) or a list whose entry l (l >= 1) is V at level l,
     [B, H_l, W_l, heads, d].
+    pe_weight [L, C, 3, 3] / pe_bias [L, C]: multiscale position encoding, a depth-wise 3x3 conv of
+    V^l added to level l's message at the query's position.
     """
     Kl = [K] * L if np.ndim(K) == 0 else list(K)
     q = np.asarray(q, np.float64)
@@ -89,6 +106,9 @@ def brute_quadtree(q, k, v, L: int, K, variant: str, tau: float, w=None, v_level
     if v_levels is not None:
         for l in range(1, L):
             PV[l] = flat(np.asarray(v_levels[l], np.float64))
+    PE = None
+    if pe_weight is not None:
+        PE = [depthwise3x3(PV[l], pe_weight[l], None if pe_bias is None else pe_bias[l]) for l in range(L)]
     out = np.zeros((B, H, W, NH, d))
     for b in range(B):
         for h in range(NH):
@@ -116,14 +136,16 @@ def brute_quadtree(q, k, v, L: int, K, variant: str, tau: float, w=None, v_level
                                 for t, tv in zip(kids, t_):
                                     score[t] = sp * tv
                         kept = _top(score, Kl[lvl]) if lvl > 0 else []
+                        pe = 0.0 if PE is None else PE[lvl][b, y >> lvl, x >> lvl, sl]
                         if variant == "B":
                             m = sum(score[t] * PV[lvl][b, t[0], t[1], sl] for t in score)
                             wl = (1.0 / L) if w is None else float(w[b, y * W + x, h, lvl])
-                            total = total + wl * m
+                            total = total + wl * (m + pe)
                         else:
                             rest = [t for t in score if t not in kept]
                             if rest:
                                 total = total + sum(score[t] * PV[lvl][b, t[0], t[1], sl] for t in rest)
+                            total = total + pe
                         if lvl > 0:
                             Hn, Wn = PK[lvl - 1].shape[1:3]
                             region = [(2 * t[0] + dy, 2 * t[1] + dx) for t in kept for dy in (0, 1) for dx in (0, 1)

@@ -416,3 +416,64 @@ def test_constant_supplied_v_levels(variant):
         r = O.forward(q, k, v, levels=L, K=Ks, variant="B", w=w, v_levels=vl)
         expect = sum(w[0, :, 0, l][:, None] * cs[l][None, :].astype(np.float64) for l in range(L))
         np.testing.assert_allclose(r["out"].reshape(H * W, 8), expect, atol=1e-12)
+
+
+# ----------------------------------------------------------- multiscale position encoding ------
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+@pytest.mark.parametrize("H,W,L,K,given_v", [(8, 8, 3, 2, False), (7, 9, 3, [0, 2, 3], False), (6, 10, 4, 1, True)])
+def test_position_encoding_matches_brute_force(variant, H, W, L, K, given_v):
+    """Multiscale position encoding (Sec. 3.2): the oracle equals the explicit-region formulation
+    with a depth-wise 3x3 convolution of V^l (zero padding, bias) added to each level's message."""
+    rng = np.random.default_rng(60 + H * W + L)
+    q, k, v = (dyadic(rng, (1, H, W, 2, 4)) for _ in range(3))
+    dims = O.level_dims(H, W, L)
+    vl = [None] + [dyadic(rng, (1, dims[l][0], dims[l][1], 2, 4)) for l in range(1, L)] if given_v else None
+    pw = dyadic(rng, (L, 8, 3, 3))
+    pb = dyadic(rng, (L, 8))
+    w = rng.random((1, H * W, 2, L)).astype(np.float32)
+    tau = 1 / np.sqrt(4)
+    r = O.forward(q, k, v, levels=L, K=K, variant=variant, w=w if variant == "B" else None, v_levels=vl,
+                  pe_weight=pw, pe_bias=pb)
+    ref = brute.brute_quadtree(q, k, v, L, K, variant, tau, w if variant == "B" else None, v_levels=vl,
+                               pe_weight=pw, pe_bias=pb)
+    np.testing.assert_allclose(r["out"], ref, rtol=0, atol=1e-12)
+
+
+def test_position_encoding_identity_kernel_adds_v():
+    """A kernel that is 1 at its centre makes each level's encoding V^l itself: with every key kept
+    (B, P7) level l's message becomes dense attention plus V^l at the query's own token."""
+    rng = np.random.default_rng(61)
+    L, H = 3, 8
+    q, k, v = (dyadic(rng, (1, H, H, 2, 4)) for _ in range(3))
+    pw = np.zeros((L, 8, 3, 3), np.float32)
+    pw[:, :, 1, 1] = 1.0
+    r = O.forward(q, k, v, levels=L, K=H * H, variant="B", pe_weight=pw, want_pyramids=True, scale=0.5)
+    PQ = brute.pyramid(q.reshape(1, H, H, 8), L)
+    PK = brute.pyramid(k.reshape(1, H, H, 8), L)
+    PV = brute.pyramid(v.reshape(1, H, H, 8), L)
+    for l in range(L):
+        n = PQ[l].shape[1] * PQ[l].shape[2]
+        dense = brute.dense_attention(PQ[l].reshape(1, n, 2, 4), PK[l].reshape(1, n, 2, 4),
+                                      PV[l].reshape(1, n, 2, 4), 0.5)
+        np.testing.assert_allclose(r["msg"][l], dense + PV[l].reshape(1, n, 2, 4), atol=1e-12)
+
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+def test_position_encoding_bias_only_shifts_output(variant):
+    """A zero kernel with bias b_l adds b_l to every message of level l, so the output moves by
+    sum_l b_l (A, Eq. 2) or sum_l w_l b_l (B, Eq. 5)."""
+    rng = np.random.default_rng(62)
+    H, W, L, K = 11, 13, 3, 2
+    q, k, v = (rand(rng, (1, H, W, 1, 8)) for _ in range(3))
+    w = rng.random((1, H * W, 1, L)).astype(np.float32) if variant == "B" else None
+    pb = rand(rng, (L, 8))
+    base = O.forward(q, k, v, levels=L, K=K, variant=variant, w=w)
+    r = O.forward(q, k, v, levels=L, K=K, variant=variant, w=w, pe_weight=np.zeros((L, 8, 3, 3), np.float32),
+                  pe_bias=pb)
+    if variant == "A":
+        shift = pb.astype(np.float64).sum(0)[None, :]
+    else:
+        shift = sum(w[0, :, 0, l][:, None] * pb[l][None, :].astype(np.float64) for l in range(L))
+    np.testing.assert_allclose(r["out"].reshape(H * W, 8) - base["out"].reshape(H * W, 8),
+                               np.broadcast_to(shift, (H * W, 8)), atol=1e-12)
