@@ -80,15 +80,17 @@ def measured_traffic(workload: str):
 
 def cpu_baseline(wl, seconds: float) -> dict:
     """The oracle as it stands, single-threaded on the host, on whole layers of the workload."""
-    from paper_2201_02767_amd.inputs import make_level_weights, make_qkv, make_v_levels
+    from paper_2201_02767_amd.inputs import make_level_weights, make_pe, make_qkv, make_v_levels
     from oracle import oracle
 
     q, k, v = make_qkv(wl)
     w = make_level_weights(wl) if wl.variant == "B" else None
     vl = make_v_levels(wl) if wl.v_given else None
+    pw, pb = make_pe(wl) if wl.pe else (None, None)
     runs, t0 = 0, time.perf_counter()
     while True:
-        oracle.forward(q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w, v_levels=vl)
+        oracle.forward(q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w, v_levels=vl,
+                       pe_weight=pw, pe_bias=pb)
         runs += 1
         el = time.perf_counter() - t0
         if el >= seconds:
@@ -132,7 +134,7 @@ def main() -> int:
         return 0
 
     import paper_2201_02767_amd as P
-    from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_qkv, make_v_levels
+    from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_pe, make_qkv, make_v_levels
 
     if args.workload not in WORKLOADS:
         print(f"unknown workload {args.workload}; choose from {sorted(WORKLOADS)}", file=sys.stderr)
@@ -145,9 +147,12 @@ def main() -> int:
     vl = None
     if wl.v_given:
         vl = [None] + [torch.from_numpy(x).to(dev).to(tdt).contiguous() for x in make_v_levels(wl)[1:]]
+    pw = pb = None
+    if wl.pe:
+        pw, pb = (torch.from_numpy(x).to(dev) for x in make_pe(wl))
     plan = P.Plan(wl.B, wl.H, wl.W, wl.heads, wl.d, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=tdt,
-                  device=dev, v_supplied=wl.v_given)
-    step = plan.prepare(q, k, v, w, v_levels=vl)
+                  device=dev, v_supplied=wl.v_given, pe=wl.pe)
+    step = plan.prepare(q, k, v, w, v_levels=vl, pe_weight=pw, pe_bias=pb)
     log(f"bench: {wl} on {torch.cuda.get_device_name(0)}")
 
     for _ in range(args.warmup):
@@ -203,7 +208,8 @@ def main() -> int:
         "vs_baseline": None, "dtype": "f32" if wl.dtype == "f32" else "bf16", "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "W": wl.W, "heads": wl.heads, "d": wl.d,
                    "levels": wl.levels, "K": wl.K if isinstance(wl.K, int) else list(wl.K)[1:],
-                   "v_levels": "given" if wl.v_given else "pooled", "variant": wl.variant, "global_batch": wl.B,
+                   "v_levels": "given" if wl.v_given else "pooled", "position_encoding": wl.pe,
+                   "variant": wl.variant, "global_batch": wl.B,
                    "seq_len": wl.H * wl.W, "parallelism": "none (1 GPU)"},
         "roofline": roof, "cpu_baseline": cpu,
     }

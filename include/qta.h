@@ -86,8 +86,9 @@ typedef struct {
     size_t k[QTA_MAX_LEVELS];
     size_t v[QTA_MAX_LEVELS];
     size_t msg[QTA_MAX_LEVELS];     /* level l >= 1, fp32 [B][N_l][heads][d]                 */
-    size_t sel_idx[QTA_MAX_LEVELS]; /* level l >= 1, int32 [B][heads][N_l][K]                */
-    size_t sel_key[QTA_MAX_LEVELS]; /* level l >= 1, fp32  [B][heads][N_l][K]                */
+    size_t sel_idx[QTA_MAX_LEVELS]; /* level l >= 1, int32 [B][heads][N_l][K_l]              */
+    size_t sel_key[QTA_MAX_LEVELS]; /* level l >= 1, fp32  [B][heads][N_l][K_l]              */
+    size_t pe0;                     /* with a position encoding: level 0's, fp32 [B][N][heads][d] */
     size_t total;                   /* bytes; every region starts on a 256-byte boundary     */
 } qta_workspace_layout;
 
@@ -106,51 +107,55 @@ qta_status qta_get_workspace_layout(int B, int heads, int H, int W, int d, int l
  * are invalid or unsupported. */
 size_t qta_workspace_bytes(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype);
 
-/* The same for qta_forward_levels: K_levels and v_supplied as there (v_supplied != 0 when V's
- * coarser levels come from the caller; the workspace then holds no V levels). */
-qta_status qta_get_workspace_layout_levels(int B, int heads, int H, int W, int d, int levels,
-                                           const int* K_levels, int v_supplied, qta_dtype dtype,
-                                           qta_workspace_layout* layout);
-size_t qta_workspace_bytes_levels(int B, int heads, int H, int W, int d, int levels, const int* K_levels,
-                                  int v_supplied, qta_dtype dtype);
-
-/*
- * qta_forward - the whole QuadTree attention forward (Sec. 3.2, Eqs. 1-6).
- *   q, k, v    [B][H][W][heads][d] dtype. Query and key maps have the same H x W.
- *   w          QuadTree-B level weights, fp32 [B][H*W][heads][levels] (level 0 = finest), used as
- *              given; NULL means 1/levels for every weight. Ignored by QuadTree-A.
- *   out        [B][H][W][heads][d] dtype: out_i = sum_l m^l of the ancestor of i at level l (A) or
- *              sum_l w_{i,l} m^l (B). With levels == 1 this is plain attention, Eq. (1) (times w for B).
- *   workspace  device buffer of at least qta_workspace_bytes(...) bytes, 256-byte aligned; after
- *              the call it holds the pyramids, messages and selections at the offsets that
- *              qta_get_workspace_layout reports.
- * Launches ceil((L-1)/2) pyramid passes, one coarse-attention kernel and one fine-attention
- * kernel per finer level, in stream order.
- */
 qta_status qta_forward(const void* q, const void* k, const void* v, const float* w,
                        int B, int heads, int H, int W, int d, int levels, int K,
                        qta_variant variant, qta_dtype dtype, float scale,
                        void* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * qta_forward_levels - qta_forward with a K per level and, optionally, the caller's V pyramid.
+ * Options of the *_ex calls. A NULL pointer to this struct, or NULL members, select the defaults.
  *   K_levels   host array; entry l (1 <= l <= levels-1) is the number of keys every query of level
  *              l keeps (1..QTA_MAX_K); entry 0 is not read. Level l-1's candidates are the 2x2
  *              children of the parent's K_levels[l] keys. The feature-matching setting of the
  *              paper keeps 8 at the finest selecting level and doubles K at each coarser level
- *              (Sec. 4.1.1). NULL is allowed only with levels == 1.
- *   v_levels   NULL: V's coarser levels are average-pooled like Q's and K's. Otherwise a host
- *              array of device pointers; entry l (1 <= l <= levels-1) is V at level l,
+ *              (Sec. 4.1.1). NULL: the call's K at every level.
+ *   v_levels   host array of device pointers; entry l (1 <= l <= levels-1) is V at level l,
  *              [B][H_l][W_l][heads][d] dtype, 16-byte aligned, used as given (the paper builds V's
  *              levels with a stride-2 conv-norm-act layer for self-attention, Sec. 3.2; that layer
  *              is the caller's). Entry 0 is not read: level 0 is `v`. Every level is then stored
- *              NHWC in the workspace.
- * Everything else as qta_forward, which is this call with K_levels[l] = K and v_levels = NULL.
+ *              NHWC in the workspace. NULL: V's levels are average-pooled like Q's and K's.
+ *   pe_weight  device fp32 [levels][heads*d][3][3], 16-byte aligned: the multiscale position
+ *              encoding (Sec. 3.2, the locally-enhanced positional encoding applied at every
+ *              level): level l's message at a query gets the 3x3 depth-wise cross-correlation of
+ *              V^l around the query's token (zero outside the map), channel by channel, before the
+ *              levels are combined. NULL: no position encoding.
+ *   pe_bias    device fp32 [levels][heads*d], 16-byte aligned, added with it; NULL: none.
+ *              Requires pe_weight.
  */
-qta_status qta_forward_levels(const void* q, const void* k, const void* v, const void* const* v_levels,
-                              const float* w, int B, int heads, int H, int W, int d, int levels,
-                              const int* K_levels, qta_variant variant, qta_dtype dtype, float scale,
-                              void* out, void* workspace, size_t workspace_bytes, void* stream);
+typedef struct {
+    const int* K_levels;
+    const void* const* v_levels;
+    const float* pe_weight;
+    const float* pe_bias;
+} qta_options;
+
+/* Workspace of qta_forward_ex with these options (layout and byte count as for qta_forward; with a
+ * position encoding the workspace also holds level 0's encoding, fp32 [B][H*W][heads][d], at
+ * layout.pe0). */
+qta_status qta_get_workspace_layout_ex(int B, int heads, int H, int W, int d, int levels, int K,
+                                       qta_dtype dtype, const qta_options* opt, qta_workspace_layout* layout);
+size_t qta_workspace_bytes_ex(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype,
+                              const qta_options* opt);
+
+/*
+ * qta_forward_ex - qta_forward with the options above (NULL opt: exactly qta_forward). K is read
+ * only where opt->K_levels is NULL. With a position encoding the workspace is needed also for a
+ * single level.
+ */
+qta_status qta_forward_ex(const void* q, const void* k, const void* v, const float* w, int B, int heads,
+                          int H, int W, int d, int levels, int K, qta_variant variant, qta_dtype dtype,
+                          float scale, const qta_options* opt, void* out, void* workspace,
+                          size_t workspace_bytes, void* stream);
 
 /*
  * qta_build_pyramid - step 1: levels 1..levels-1 of one token map by 2x2 average pooling

@@ -227,7 +227,8 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
         if (a.out) {
             float wl = 1.0f;
             if (!VA) wl = a.w ? a.w[((tok0 + qi) * a.heads + h) * a.levels] : 1.0f / a.levels;
-            S::store1(a.out, (tok0 + qi) * C + hoff + ch, wl * s);
+            const float pe = a.pe0 ? a.pe0[((tok0 + qi) * a.heads + h) * D + ch] : 0.f;
+            S::store1(a.out, (tok0 + qi) * C + hoff + ch, wl * (s + pe));
         } else {
             a.msg[((tok0 + qi) * a.heads + h) * D + ch] = s;
         }

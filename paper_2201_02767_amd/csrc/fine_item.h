@@ -244,6 +244,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
     constexpr int kPre = FINEST ? kPrefetchLevels : 1;
     float anc[kPre];
     float wq[FINEST ? QPL : 1][kPre + 1];
+    float peq[FINEST ? QPL : 1] = {};
     const bool prefetch = FINEST && a.levels <= kPre + 1;
     // the finest level's combination inputs, requested once the gathered registers are free; their
     // latency overlaps the softmax and the messages
@@ -257,6 +258,15 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
                 const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
                                   static_cast<size_t>((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev);
                 anc[lev - 1] = (a.coarser_msg[lev] + (an * a.heads + h) * D)[ch];
+            }
+            if (a.pe0) {                                     // uniform
+                const float* pb = a.pe0 + (static_cast<size_t>(b) * N * a.heads + h) * D + ch;
+#pragma unroll
+                for (int u = 0; u < QPL; ++u) {
+                    const int qi = (NH == 2 ? hh * QPL : 0) + u;
+                    const int py = min(2 * Py + (qi >> 1), H - 1), px = min(2 * Px + (qi & 1), W - 1);
+                    peq[u] = pb[static_cast<uint32_t>(__mul24(py, W) + px) * static_cast<uint32_t>(a.heads * D)];
+                }
             }
             if (!VA && a.w) {                                // uniform
                 const float* wb = a.w + (static_cast<size_t>(b) * N * a.heads + h) * L;
@@ -381,7 +391,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
             const float wdef = 1.0f / L;
             float out;
             if (prefetch) {
-                out = (VA ? 1.0f : (a.w ? wq[u][0] : wdef)) * m;
+                out = (VA ? 1.0f : (a.w ? wq[u][0] : wdef)) * (m + peq[u]);
 #pragma unroll
                 for (int lev = 1; lev <= kPre; ++lev) {
                     if (lev >= L) break;
@@ -389,7 +399,8 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
                 }
             } else {
                 const float* wrow = a.w ? a.w + (qtok * a.heads + h) * L : nullptr;
-                out = (VA ? 1.0f : (wrow ? wrow[0] : wdef)) * m;
+                const float pe = a.pe0 ? a.pe0[(qtok * a.heads + h) * D + ch] : 0.f;
+                out = (VA ? 1.0f : (wrow ? wrow[0] : wdef)) * (m + pe);
                 for (int lev = 1; lev < L; ++lev) {
                     const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
                                       static_cast<size_t>(qy >> lev) * a.lvl_W[lev] + (qx >> lev);

@@ -345,8 +345,9 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
         const float wdef = 1.0f / L;
         float o[CPL];
         const float w0 = VA ? 1.0f : (wrow ? wrow[0] : wdef);
+        const float* pe = a.pe0 ? a.pe0 + (qtok * a.heads + h) * D + cg * CPL : nullptr;
 #pragma unroll
-        for (int e = 0; e < CPL; ++e) o[e] = w0 * acc[e];
+        for (int e = 0; e < CPL; ++e) o[e] = w0 * (acc[e] + (pe ? pe[e] : 0.f));
         for (int lev = 1; lev < L; ++lev) {
             const size_t anc = static_cast<size_t>(b) * a.lvl_N[lev] + static_cast<size_t>(qy >> lev) * a.lvl_W[lev] +
                                (qx >> lev);

@@ -80,8 +80,8 @@ bool use_blocked(const int* Kl, int l, int levels, bool v_supplied)
     return !v_supplied && l >= 1 && l <= levels - 2 && 4 * Kl[l + 1] <= 64;
 }
 
-qta_status layout(int B, int heads, int H, int W, int d, int levels, const int* Kl, bool v_supplied, qta_dtype dtype,
-                  qta_workspace_layout* L)
+qta_status layout(int B, int heads, int H, int W, int d, int levels, const int* Kl, bool v_supplied, bool pe,
+                  qta_dtype dtype, qta_workspace_layout* L)
 {
     qta_status st = check_problem(B, heads, d, 1, QTA_VARIANT_B, dtype);
     if (st != QTA_OK) return st;
@@ -122,7 +122,37 @@ qta_status layout(int B, int heads, int H, int W, int d, int levels, const int* 
         L->sel_key[l] = off;
         off = align_up(off + static_cast<size_t>(B) * heads * N * Kl[l] * sizeof(float));
     }
+    if (pe) {
+        L->pe0 = off;
+        off = align_up(off + static_cast<size_t>(B) * Hl[0] * Wl[0] * C * sizeof(float));
+    }
     L->total = off > kAlign ? off : kAlign;   // nonzero for every valid problem
+    return QTA_OK;
+}
+
+// The options of qta_forward_ex with K filled in where K_levels is NULL.
+struct Options {
+    int Kl[QTA_MAX_LEVELS];
+    const void* const* v_levels;
+    const float* pe_weight;
+    const float* pe_bias;
+};
+
+qta_status read_options(int K, int levels, const qta_options* opt, Options* o)
+{
+    o->v_levels = opt ? opt->v_levels : nullptr;
+    o->pe_weight = opt ? opt->pe_weight : nullptr;
+    o->pe_bias = opt ? opt->pe_bias : nullptr;
+    const int* src = opt ? opt->K_levels : nullptr;
+    if (levels <= 0 || levels > QTA_MAX_LEVELS) return QTA_ERR_INVALID;
+    if (!src && K <= 0) return QTA_ERR_INVALID;
+    if (!src && K > QTA_MAX_K) return QTA_ERR_UNSUPPORTED;
+    for (int l = 0; l < QTA_MAX_LEVELS; ++l) o->Kl[l] = K;
+    if (src)
+        for (int l = 1; l < levels; ++l) o->Kl[l] = src[l];
+    if (o->pe_bias && !o->pe_weight) return QTA_ERR_INVALID;
+    const uintptr_t pw = reinterpret_cast<uintptr_t>(o->pe_weight), pb = reinterpret_cast<uintptr_t>(o->pe_bias);
+    if ((pw & 15u) != 0 || (pb & 15u) != 0) return QTA_ERR_INVALID;
     return QTA_OK;
 }
 
@@ -184,36 +214,33 @@ qta_status qta_level_dims(int H, int W, int levels, int* Hl, int* Wl)
     return dims(H, W, levels, Hl, Wl);
 }
 
-qta_status qta_get_workspace_layout_levels(int B, int heads, int H, int W, int d, int levels, const int* K_levels,
-                                           int v_supplied, qta_dtype dtype, qta_workspace_layout* out)
+qta_status qta_get_workspace_layout_ex(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype,
+                                       const qta_options* opt, qta_workspace_layout* out)
 {
     if (!out) return QTA_ERR_INVALID;
-    return layout(B, heads, H, W, d, levels, K_levels, v_supplied != 0, dtype, out);
+    Options o;
+    qta_status st = read_options(K, levels, opt, &o);
+    if (st != QTA_OK) return st;
+    return layout(B, heads, H, W, d, levels, o.Kl, o.v_levels != nullptr, o.pe_weight != nullptr, dtype, out);
 }
 
-size_t qta_workspace_bytes_levels(int B, int heads, int H, int W, int d, int levels, const int* K_levels,
-                                  int v_supplied, qta_dtype dtype)
+size_t qta_workspace_bytes_ex(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype,
+                              const qta_options* opt)
 {
     qta_workspace_layout L;
-    if (layout(B, heads, H, W, d, levels, K_levels, v_supplied != 0, dtype, &L) != QTA_OK) return 0;
+    if (qta_get_workspace_layout_ex(B, heads, H, W, d, levels, K, dtype, opt, &L) != QTA_OK) return 0;
     return L.total;
 }
 
 qta_status qta_get_workspace_layout(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype,
                                     qta_workspace_layout* out)
 {
-    if (!out) return QTA_ERR_INVALID;
-    if (K <= 0) return QTA_ERR_INVALID;
-    int Kl[QTA_MAX_LEVELS];
-    for (int l = 0; l < QTA_MAX_LEVELS; ++l) Kl[l] = K;
-    return layout(B, heads, H, W, d, levels, Kl, false, dtype, out);
+    return qta_get_workspace_layout_ex(B, heads, H, W, d, levels, K, dtype, nullptr, out);
 }
 
 size_t qta_workspace_bytes(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype)
 {
-    qta_workspace_layout L;
-    if (qta_get_workspace_layout(B, heads, H, W, d, levels, K, dtype, &L) != QTA_OK) return 0;
-    return L.total;
+    return qta_workspace_bytes_ex(B, heads, H, W, d, levels, K, dtype, nullptr);
 }
 
 qta_status qta_build_pyramid(const void* x, void* levels_out, int B, int H, int W, int C, int levels, qta_dtype dtype,
@@ -358,24 +385,28 @@ qta_status qta_finest_attn(const void* q0, const void* k0, const void* v0, int B
                                           static_cast<hipStream_t>(stream)));
 }
 
-qta_status qta_forward_levels(const void* q, const void* k, const void* v, const void* const* v_levels, const float* w,
-                              int B, int heads, int H, int W, int d, int levels, const int* K_levels,
-                              qta_variant variant, qta_dtype dtype, float scale, void* out, void* workspace,
-                              size_t workspace_bytes, void* stream)
+qta_status qta_forward_ex(const void* q, const void* k, const void* v, const float* w, int B, int heads, int H, int W,
+                          int d, int levels, int K, qta_variant variant, qta_dtype dtype, float scale,
+                          const qta_options* opt, void* out, void* workspace, size_t workspace_bytes, void* stream)
 {
     qta_status st = check_problem(B, heads, d, 1, variant, dtype);
     if (st != QTA_OK) return st;
     if (!q || !k || !v || !out) return QTA_ERR_INVALID;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return QTA_ERR_INVALID;
+    Options o;
+    st = read_options(K, levels, opt, &o);
+    if (st != QTA_OK) return st;
+    const void* const* v_levels = o.v_levels;
     const bool v_supplied = v_levels != nullptr;
+    const bool pe = o.pe_weight != nullptr;
     if (v_supplied)
         for (int l = 1; l < levels && l < QTA_MAX_LEVELS; ++l)
             if (!v_levels[l] || !aligned16(v_levels[l])) return QTA_ERR_INVALID;
     qta_workspace_layout L;
-    st = layout(B, heads, H, W, d, levels, K_levels, v_supplied, dtype, &L);
+    st = layout(B, heads, H, W, d, levels, o.Kl, v_supplied, pe, dtype, &L);
     if (st != QTA_OK) return st;
-    const int* Kl = K_levels;
-    if (levels > 1) {
+    const int* Kl = o.Kl;
+    if (levels > 1 || pe) {
         if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return QTA_ERR_INVALID;
         if (workspace_bytes < L.total) return QTA_ERR_WORKSPACE;
     }
@@ -412,6 +443,29 @@ qta_status qta_forward_levels(const void* q, const void* k, const void* v, const
         if (e != hipSuccess) return QTA_ERR_HIP;
     }
 
+    // multiscale position encoding: levels above 0 add it to their messages in place, level 0
+    // writes it to the workspace for the kernel that forms the output (launched right before it)
+    float* pe0 = pe ? reinterpret_cast<float*>(ws + L.pe0) : nullptr;
+    auto posenc = [&]() -> hipError_t {
+        PosEncArgs p{};
+        p.nlev = levels;
+        p.B = B;
+        p.heads = heads;
+        p.d = d;
+        for (int l = 0; l < levels; ++l) {
+            PosEncLevel& e = p.lv[l];
+            e.v = l == 0 ? v : lv[2][l];
+            e.blocked = l == 0 ? 0 : L.blocked[l];
+            e.H = L.H[l];
+            e.W = L.W[l];
+            e.dst = l == 0 ? pe0 : msg(l);
+            e.accumulate = l == 0 ? 0 : 1;
+            e.weight = o.pe_weight + static_cast<size_t>(l) * C * 9;
+            e.bias = o.pe_bias ? o.pe_bias + static_cast<size_t>(l) * C : nullptr;
+        }
+        return launch_posenc(p, use_bf16, s);
+    };
+
     // 2-3. coarsest level
     const int c = levels - 1;
     {
@@ -429,6 +483,11 @@ qta_status qta_forward_levels(const void* q, const void* k, const void* v, const
             a.K = 0;
             a.out = out;
             a.w = w;
+            if (pe) {
+                hipError_t e = posenc();
+                if (e != hipSuccess) return QTA_ERR_HIP;
+                a.pe0 = pe0;
+            }
         } else {
             a.K = Kl[c];
             a.msg = msg(c);
@@ -468,6 +527,10 @@ qta_status qta_forward_levels(const void* q, const void* k, const void* v, const
     }
 
     // 4-5. finest level with the combination fused in
+    if (pe) {
+        hipError_t e = posenc();
+        if (e != hipSuccess) return QTA_ERR_HIP;
+    }
     {
         FineArgs a{};
         a.q = q;
@@ -489,6 +552,7 @@ qta_status qta_forward_levels(const void* q, const void* k, const void* v, const
         a.parent_key = skey(1);
         a.out = out;
         a.w = w;
+        a.pe0 = pe0;
         a.levels = levels;
         for (int l = 1; l < levels; ++l) {
             a.coarser_msg[l] = msg(l);
@@ -505,12 +569,8 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
                        int d, int levels, int K, qta_variant variant, qta_dtype dtype, float scale, void* out,
                        void* workspace, size_t workspace_bytes, void* stream)
 {
-    if (K <= 0) return QTA_ERR_INVALID;
-    if (K > QTA_MAX_K) return QTA_ERR_UNSUPPORTED;
-    int Kl[QTA_MAX_LEVELS];
-    for (int l = 0; l < QTA_MAX_LEVELS; ++l) Kl[l] = K;
-    return qta_forward_levels(q, k, v, nullptr, w, B, heads, H, W, d, levels, Kl, variant, dtype, scale, out, workspace,
-                              workspace_bytes, stream);
+    return qta_forward_ex(q, k, v, w, B, heads, H, W, d, levels, K, variant, dtype, scale, nullptr, out, workspace,
+                          workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -63,6 +63,7 @@ struct CoarseArgs {
     float* sel_key;
     void* out;                  // single-level problem: write out = w0 * m (B) or m (A) in dtype
     const float* w;
+    const float* pe0;           // single-level problem: position encoding added to m, or NULL
     int levels;
 };
 
@@ -112,10 +113,31 @@ struct FineArgs {
     // finest level: fused combination
     void* out;
     const float* w;
+    const float* pe0;           // level 0's position encoding, fp32 [B][N][heads][d], added to m0; or NULL
     int levels;
     const float* coarser_msg[QTA_MAX_LEVELS];   // entry j: message of level j (j >= 1)
     int lvl_W[QTA_MAX_LEVELS];                  // map width of level j
     int lvl_N[QTA_MAX_LEVELS];                  // tokens of level j
+};
+
+// Multiscale position encoding of one level: dst += (or =, for level 0) the 3x3 depth-wise
+// convolution of V at that level with zero padding, plus the bias.
+struct PosEncLevel {
+    const void* v;              // V at this level (storage type), NHWC or parent-blocked
+    int blocked;
+    int H, W;
+    float* dst;                 // fp32 [B][H*W][heads][d]
+    int accumulate;             // 1: dst += encoding (a level's message), 0: dst = encoding
+    const float* weight;        // fp32 [C][3][3] for this level
+    const float* bias;          // fp32 [C], or NULL
+};
+
+struct PosEncArgs {
+    PosEncLevel lv[QTA_MAX_LEVELS];
+    long long start[QTA_MAX_LEVELS + 1];    // first work item of each level (set by the launcher)
+    long long level_end[QTA_MAX_LEVELS];     // one past the last work item of each level
+    int nlev;
+    int B, heads, d;
 };
 
 struct TopkArgs {
@@ -143,6 +165,7 @@ inline size_t device_max_lds()
 
 hipError_t launch_pyramid_pass(const PyramidPassArgs& a, int nlev, int ntensors, bool use_bf16, hipStream_t stream);
 hipError_t launch_coarse_attn(const CoarseArgs& a, int d, bool variant_a, bool use_bf16, hipStream_t stream);
+hipError_t launch_posenc(const PosEncArgs& a, bool use_bf16, hipStream_t stream);
 hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest, hipStream_t stream);
 hipError_t launch_fine_attn_wide(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
                                  hipStream_t stream);

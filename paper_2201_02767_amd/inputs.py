@@ -21,9 +21,11 @@ not used):
   backbone_vgiven - backbone with V's coarser levels given as inputs, as in self-attention where a
              stride-2 conv-norm-act layer builds them (Sec. 3.2); each level is an independent
              N(0,1) map standing in for that layer's normalised output.
+  backbone_pe - backbone with the multiscale position encoding (Sec. 3.2): 3x3 depth-wise kernels
+             N(0, 0.3^2) and biases N(0, 0.1^2) per level and channel (random-init weights).
 
-Seeds: numpy PCG64 with seed = 1000 * config_number + tensor id (q=1, k=2, v=3, w=4, aux=5, and
-10 + l for the given V level l).
+Seeds: numpy PCG64 with seed = 1000 * config_number + tensor id (q=1, k=2, v=3, w=4, aux=5,
+10 + l for the given V level l, 20 and 21 for the position-encoding weights and biases).
 All arrays are float32 ``[B, H, W, heads, d]``; for bf16 workloads the values are rounded to the
 nearest bfloat16 (ties to even), so they are exactly representable in bf16.
 """
@@ -49,6 +51,7 @@ class Workload:
     dtype: str        # "f32" or "bf16"
     kind: str         # generator: "iid_scaled", "shift", "disparity", "smooth"
     v_given: bool = False   # V's coarser levels are inputs (make_v_levels) instead of pooled
+    pe: bool = False        # multiscale position encoding (make_pe)
 
     @property
     def tokens(self) -> int:
@@ -66,6 +69,7 @@ WORKLOADS = {
     "highres": Workload("highres", 5, 2, 200, 336, 2, 32, 5, 16, "B", "bf16", "smooth"),
     "matching_ksched": Workload("matching_ksched", 2, 1, 60, 80, 8, 32, 3, (0, 8, 16), "B", "f32", "shift"),
     "backbone_vgiven": Workload("backbone_vgiven", 4, 32, 56, 56, 1, 64, 3, 8, "B", "bf16", "smooth", True),
+    "backbone_pe": Workload("backbone_pe", 4, 32, 56, 56, 1, 64, 3, 8, "B", "bf16", "smooth", False, True),
 }
 
 
@@ -161,3 +165,11 @@ def make_v_levels(wl: Workload, seed_offset: int = 0) -> list:
         x = _rng(wl, 10 + l, seed_offset).standard_normal((wl.B, H, W, wl.heads, wl.d), dtype=np.float32)
         out.append(round_bf16(x) if wl.dtype == "bf16" else x)
     return out
+
+
+def make_pe(wl: Workload, seed_offset: int = 0):
+    """Position-encoding weights fp32 [levels, heads*d, 3, 3] and biases fp32 [levels, heads*d]."""
+    C = wl.heads * wl.d
+    wgt = (_rng(wl, 20, seed_offset).standard_normal((wl.levels, C, 3, 3)) * 0.3).astype(np.float32)
+    bias = (_rng(wl, 21, seed_offset).standard_normal((wl.levels, C)) * 0.1).astype(np.float32)
+    return wgt, bias

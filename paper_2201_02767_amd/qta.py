@@ -40,7 +40,17 @@ class WorkspaceLayout(ctypes.Structure):
         ("msg", ctypes.c_size_t * MAX_LEVELS),
         ("sel_idx", ctypes.c_size_t * MAX_LEVELS),
         ("sel_key", ctypes.c_size_t * MAX_LEVELS),
+        ("pe0", ctypes.c_size_t),
         ("total", ctypes.c_size_t),
+    ]
+
+
+class Options(ctypes.Structure):
+    _fields_ = [
+        ("K_levels", ctypes.c_void_p),
+        ("v_levels", ctypes.c_void_p),
+        ("pe_weight", ctypes.c_void_p),
+        ("pe_bias", ctypes.c_void_p),
     ]
 
 
@@ -53,11 +63,10 @@ _SIGS = {
     "qta_level_dims": ([_I, _I, _I, _P, _P], _I),
     "qta_get_workspace_layout": ([_I, _I, _I, _I, _I, _I, _I, _I, ctypes.POINTER(WorkspaceLayout)], _I),
     "qta_workspace_bytes": ([_I, _I, _I, _I, _I, _I, _I, _I], ctypes.c_size_t),
-    "qta_get_workspace_layout_levels": ([_I, _I, _I, _I, _I, _I, _P, _I, _I, ctypes.POINTER(WorkspaceLayout)], _I),
-    "qta_workspace_bytes_levels": ([_I, _I, _I, _I, _I, _I, _P, _I, _I], ctypes.c_size_t),
+    "qta_get_workspace_layout_ex": ([_I, _I, _I, _I, _I, _I, _I, _I, _P, ctypes.POINTER(WorkspaceLayout)], _I),
+    "qta_workspace_bytes_ex": ([_I, _I, _I, _I, _I, _I, _I, _I, _P], ctypes.c_size_t),
     "qta_forward": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, ctypes.c_size_t, _P], _I),
-    "qta_forward_levels": ([_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _F, _P, _P, ctypes.c_size_t, _P],
-                           _I),
+    "qta_forward_ex": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, ctypes.c_size_t, _P], _I),
     "qta_build_pyramid": ([_P, _P, _I, _I, _I, _I, _I, _I, _P], _I),
     "qta_coarse_attn": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P], _I),
     "qta_topk": ([_P, _P, _I, _I, _I, _P, _P, _P], _I),
@@ -144,19 +153,37 @@ def _k_table(Kl):
     return (ctypes.c_int * MAX_LEVELS)(*Kl)
 
 
-def workspace_layout(B, heads, H, W, d, levels, K, dtype: torch.dtype, v_supplied: bool = False) -> WorkspaceLayout:
-    lay = WorkspaceLayout()
+_FAKE_PTR = 256      # a non-NULL, aligned, never-dereferenced device address (layout queries only)
+
+
+def _layout_options(K, levels, v_supplied, pe):
+    """Options for a layout query (only which options are present matters there)."""
     tbl = _k_table(k_levels(K, levels))
-    _check("qta_get_workspace_layout_levels",
-           lib().qta_get_workspace_layout_levels(B, heads, H, W, d, levels, ctypes.addressof(tbl), int(v_supplied),
-                                                 _DTYPES[dtype], ctypes.byref(lay)))
+    opt = Options()
+    opt.K_levels = ctypes.addressof(tbl)
+    vt = None
+    if v_supplied:
+        vt = (ctypes.c_void_p * MAX_LEVELS)(*([_FAKE_PTR] * MAX_LEVELS))
+        opt.v_levels = ctypes.addressof(vt)
+    if pe:
+        opt.pe_weight = _FAKE_PTR
+    return opt, (tbl, vt)
+
+
+def workspace_layout(B, heads, H, W, d, levels, K, dtype: torch.dtype, v_supplied: bool = False,
+                     pe: bool = False) -> WorkspaceLayout:
+    lay = WorkspaceLayout()
+    opt, keep = _layout_options(K, levels, v_supplied, pe)
+    _check("qta_get_workspace_layout_ex",
+           lib().qta_get_workspace_layout_ex(B, heads, H, W, d, levels, 1, _DTYPES[dtype], ctypes.byref(opt),
+                                             ctypes.byref(lay)))
     return lay
 
 
-def workspace_bytes(B, heads, H, W, d, levels, K, dtype: torch.dtype, v_supplied: bool = False) -> int:
-    tbl = _k_table(k_levels(K, levels))
-    return int(lib().qta_workspace_bytes_levels(B, heads, H, W, d, levels, ctypes.addressof(tbl), int(v_supplied),
-                                                _DTYPES[dtype]))
+def workspace_bytes(B, heads, H, W, d, levels, K, dtype: torch.dtype, v_supplied: bool = False,
+                    pe: bool = False) -> int:
+    opt, keep = _layout_options(K, levels, v_supplied, pe)
+    return int(lib().qta_workspace_bytes_ex(B, heads, H, W, d, levels, 1, _DTYPES[dtype], ctypes.byref(opt)))
 
 
 # ------------------------------------------------------------------------------------------------
@@ -168,23 +195,26 @@ class Plan:
 
     ``K``: one count for every level, or one entry per level (entry l is level l's K, entry 0
     unused). ``v_supplied``: V's coarser levels come from the caller (``v_levels`` of run/prepare).
+    ``pe``: a multiscale position encoding is applied (``pe_weight``/``pe_bias`` of run/prepare).
     """
 
-    def __init__(self, B, H, W, heads, d, *, levels, K, variant, dtype, device, scale=None, v_supplied=False):
+    def __init__(self, B, H, W, heads, d, *, levels, K, variant, dtype, device, scale=None, v_supplied=False,
+                 pe=False):
         self.B, self.H, self.W, self.heads, self.d = B, H, W, heads, d
         self.levels, self.variant, self.dtype = levels, variant, dtype
         self.K_levels = k_levels(K, levels)
         self.K = K if isinstance(K, int) else self.K_levels
         self.scale = scale
         self.v_supplied = bool(v_supplied)
+        self.pe = bool(pe)
         self.device = torch.device(device)
-        self.layout = workspace_layout(B, heads, H, W, d, levels, K, dtype, self.v_supplied)
+        self.layout = workspace_layout(B, heads, H, W, d, levels, K, dtype, self.v_supplied, self.pe)
         self._k_tbl = _k_table(self.K_levels)
         nbytes = max(int(self.layout.total), 256)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
         self.out = torch.empty((B, H, W, heads, d), dtype=dtype, device=self.device)
 
-    def _args(self, q, k, v, w, v_levels):
+    def _args(self, q, k, v, w, v_levels, pe_weight, pe_bias):
         for name, t in (("q", q), ("k", k), ("v", v)):
             _require(t, name, self.dtype, 5)
             if tuple(t.shape) != (self.B, self.H, self.W, self.heads, self.d):
@@ -204,32 +234,50 @@ class Plan:
                 if tuple(t.shape) != (self.B, self.layout.H[l], self.layout.W[l], self.heads, self.d):
                     raise ValueError(f"v_levels[{l}] has shape {tuple(t.shape)}")
                 vtbl[l] = t.data_ptr()
-        return vtbl
+        if (pe_weight is not None) != self.pe:
+            raise ValueError("pe_weight must be given exactly when the plan was made with pe=True")
+        C = self.heads * self.d
+        if pe_weight is not None:
+            _require(pe_weight, "pe_weight", torch.float32)
+            if tuple(pe_weight.shape) != (self.levels, C, 3, 3):
+                raise ValueError(f"pe_weight has shape {tuple(pe_weight.shape)}")
+            if pe_bias is not None:
+                _require(pe_bias, "pe_bias", torch.float32)
+                if tuple(pe_bias.shape) != (self.levels, C):
+                    raise ValueError(f"pe_bias has shape {tuple(pe_bias.shape)}")
+        elif pe_bias is not None:
+            raise ValueError("pe_bias needs pe_weight")
+        opt = Options()
+        opt.K_levels = ctypes.addressof(self._k_tbl)
+        opt.v_levels = ctypes.addressof(vtbl) if vtbl is not None else None
+        opt.pe_weight = pe_weight.data_ptr() if pe_weight is not None else None
+        opt.pe_bias = pe_bias.data_ptr() if pe_bias is not None else None
+        return opt, vtbl
 
-    def run(self, q, k, v, w=None, stream=None, v_levels=None):
-        vtbl = self._args(q, k, v, w, v_levels)
+    def _call_args(self, q, k, v, w, opt, stream):
+        return (_ptr(q), _ptr(k), _ptr(v), _ptr(w), self.B, self.heads, self.H, self.W, self.d, self.levels,
+                self.K_levels[1] if self.levels > 1 else max(self.K_levels[0], 1), _VARIANTS[self.variant],
+                _DTYPES[self.dtype], _scale(self.scale), ctypes.byref(opt), _ptr(self.out), _ptr(self.workspace),
+                self.workspace.numel(), stream)
+
+    def run(self, q, k, v, w=None, stream=None, v_levels=None, pe_weight=None, pe_bias=None):
+        opt, vtbl = self._args(q, k, v, w, v_levels, pe_weight, pe_bias)
         s = _stream(self.device) if stream is None else ctypes.c_void_p(stream)
-        _check("qta_forward_levels", lib().qta_forward_levels(
-            _ptr(q), _ptr(k), _ptr(v), ctypes.addressof(vtbl) if vtbl is not None else None, _ptr(w), self.B,
-            self.heads, self.H, self.W, self.d, self.levels, ctypes.addressof(self._k_tbl), _VARIANTS[self.variant],
-            _DTYPES[self.dtype], _scale(self.scale), _ptr(self.out), _ptr(self.workspace), self.workspace.numel(), s))
+        _check("qta_forward_ex", lib().qta_forward_ex(*self._call_args(q, k, v, w, opt, s)))
         return self.out
 
-    def prepare(self, q, k, v, w=None, v_levels=None):
+    def prepare(self, q, k, v, w=None, v_levels=None, pe_weight=None, pe_bias=None):
         """Validate once and return a zero-argument callable that re-issues this forward on the
         current stream (for timing loops and graph capture: no per-call Python checks)."""
-        vtbl = self._args(q, k, v, w, v_levels)
-        fn = lib().qta_forward_levels
-        args = (_ptr(q), _ptr(k), _ptr(v), ctypes.addressof(vtbl) if vtbl is not None else None, _ptr(w), self.B,
-                self.heads, self.H, self.W, self.d, self.levels, ctypes.addressof(self._k_tbl),
-                _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), _ptr(self.out),
-                _ptr(self.workspace), self.workspace.numel(), _stream(self.device))
-        keep = (q, k, v, w, vtbl, v_levels)
+        opt, vtbl = self._args(q, k, v, w, v_levels, pe_weight, pe_bias)
+        fn = lib().qta_forward_ex
+        args = self._call_args(q, k, v, w, opt, _stream(self.device))
+        keep = (q, k, v, w, vtbl, v_levels, opt, pe_weight, pe_bias)
 
         def call():
             st = fn(*args)
             if st != 0:
-                _check("qta_forward_levels", st)
+                _check("qta_forward_ex", st)
             return keep
         return call
 
@@ -290,15 +338,17 @@ class Plan:
                 self._view(lay.sel_key[level], shape, torch.float32))
 
 
-def forward(q, k, v, *, levels: int, K, variant: str, w=None, scale=None, v_levels=None) -> torch.Tensor:
+def forward(q, k, v, *, levels: int, K, variant: str, w=None, scale=None, v_levels=None, pe_weight=None,
+            pe_bias=None) -> torch.Tensor:
     """QuadTree attention forward; returns ``out`` [B, H, W, heads, d] in q's dtype. ``K``: one count
     or one per level (entry 0 unused); ``v_levels``: None, or a list whose entry l (l >= 1) is V at
-    level l, [B, H_l, W_l, heads, d]."""
+    level l, [B, H_l, W_l, heads, d]; ``pe_weight`` fp32 [levels, heads*d, 3, 3] and ``pe_bias`` fp32
+    [levels, heads*d]: the multiscale position encoding."""
     _require(q, "q", None, 5)
     B, H, W, heads, d = q.shape
     plan = Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=q.dtype, device=q.device,
-                scale=scale, v_supplied=v_levels is not None)
-    return plan.run(q, k, v, w, v_levels=v_levels)
+                scale=scale, v_supplied=v_levels is not None, pe=pe_weight is not None)
+    return plan.run(q, k, v, w, v_levels=v_levels, pe_weight=pe_weight, pe_bias=pe_bias)
 
 
 # ------------------------------------------------------------------------------------------------

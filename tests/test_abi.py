@@ -211,22 +211,44 @@ def test_layout_with_k_schedule_and_supplied_v():
     assert lay_v.total < P.workspace_layout(B, heads, H, W, d, L, [0, 4, 16, 8], torch.float32).total
 
 
-def test_forward_levels_validation():
+def test_forward_ex_validation():
     lib = P.lib()
 
-    def fwd(Kl, vtbl=None, L=3):
-        return lib.qta_forward_levels(FAKE, FAKE, FAKE, vtbl, None, 1, 1, 16, 16, 32, L, Kl, VA, F32, 0.0, FAKE,
-                                      FAKE, 0, None)
+    def fwd(Kl=None, vtbl=None, pw=None, pb=None, L=3, wsb=0):
+        opt = P.qta.Options()
+        opt.K_levels = Kl
+        opt.v_levels = vtbl
+        opt.pe_weight = pw
+        opt.pe_bias = pb
+        return lib.qta_forward_ex(FAKE, FAKE, FAKE, None, 1, 1, 16, 16, 32, L, 4, VA, F32, 0.0, ctypes.byref(opt),
+                                  FAKE, FAKE, wsb, None)
+    assert lib.qta_forward_ex(FAKE, FAKE, FAKE, None, 1, 1, 16, 16, 32, 3, 4, VA, F32, 0.0, None, FAKE, FAKE, 0,
+                              None) == WORKSPACE                           # NULL options: plain qta_forward
     assert fwd(ctypes.addressof(_klv(0, 4, 8))) == WORKSPACE               # valid shape, zero workspace
-    assert fwd(None) == INVALID                                            # K table required for L > 1
     assert fwd(ctypes.addressof(_klv(0, 4, 0))) == INVALID
     assert fwd(ctypes.addressof(_klv(0, 65, 4))) == UNSUPPORTED
     assert fwd(ctypes.addressof(_klv(9, 4, 8))) == WORKSPACE               # entry 0 is not read
     vt = (ctypes.c_void_p * 16)()
     vt[1] = FAKE
-    assert fwd(ctypes.addressof(_klv(0, 4, 8)), ctypes.addressof(vt)) == INVALID       # level 2 missing
+    assert fwd(None, ctypes.addressof(vt)) == INVALID                      # level 2 missing
     vt[2] = FAKE + 8
-    assert fwd(ctypes.addressof(_klv(0, 4, 8)), ctypes.addressof(vt)) == INVALID       # misaligned
+    assert fwd(None, ctypes.addressof(vt)) == INVALID                      # misaligned
     vt[2] = FAKE
-    assert fwd(ctypes.addressof(_klv(0, 4, 8)), ctypes.addressof(vt)) == WORKSPACE
-    assert lib.qta_workspace_bytes_levels(1, 1, 16, 16, 32, 3, ctypes.addressof(_klv(0, 4, 65)), 0, F32) == 0
+    assert fwd(None, ctypes.addressof(vt)) == WORKSPACE
+    assert fwd(pb=FAKE) == INVALID                                         # a bias needs weights
+    assert fwd(pw=FAKE + 4) == INVALID                                     # weights not 16-byte aligned
+    assert fwd(pw=FAKE, pb=FAKE) == WORKSPACE
+    assert fwd(pw=FAKE, L=1) == WORKSPACE                                  # one level with an encoding needs it
+    opt = P.qta.Options()
+    opt.K_levels = ctypes.addressof(_klv(0, 4, 65))
+    assert lib.qta_workspace_bytes_ex(1, 1, 16, 16, 32, 3, 4, F32, ctypes.byref(opt)) == 0
+
+
+def test_position_encoding_workspace():
+    """With an encoding the workspace adds level 0's fp32 encoding after everything else."""
+    base = P.workspace_layout(2, 2, 40, 30, 32, 3, 8, torch.bfloat16)
+    lay = P.workspace_layout(2, 2, 40, 30, 32, 3, 8, torch.bfloat16, pe=True)
+    assert lay.pe0 >= base.total - 256 and lay.pe0 % 256 == 0
+    assert lay.total >= lay.pe0 + 2 * 40 * 30 * 64 * 4
+    single = P.workspace_layout(1, 1, 16, 16, 32, 1, 4, torch.float32, pe=True)
+    assert single.total >= 16 * 16 * 32 * 4

@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import paper_2201_02767_amd as P
-from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_qkv, make_v_levels, round_bf16
+from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_pe, make_qkv, make_v_levels, round_bf16
 from oracle import oracle as O
 from tests import brute
 from tests.parity import TOL, check_selection, rel_err, to_np
@@ -51,23 +51,28 @@ def dev_t(x, dtype, dev):
 # end-to-end protocol
 # ------------------------------------------------------------------------------------------------
 
-def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=None, label="", v_levels=None):
+def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=None, label="", v_levels=None,
+                    pe_weight=None, pe_bias=None):
     """GPU forward vs teacher-forced oracle; returns a dict of the measured agreement. ``K``: one
     count or one per level; ``v_levels``: None or the caller's V levels (numpy, entry l >= 1)."""
     B, H, W, heads, d = q.shape
     announce(f"forward {label} B={B} H={H} W={W} heads={heads} d={d} L={levels} K={K} {variant} {dtype}"
              f"{' V levels given' if v_levels is not None else ''}")
     plan = P.Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=TDT[dtype], device=dev, scale=scale,
-                  v_supplied=v_levels is not None)
+                  v_supplied=v_levels is not None, pe=pe_weight is not None)
     Kl = P.k_levels(K, levels)
     wt = None if w is None else torch.from_numpy(w).to(dev)
     vl = None if v_levels is None else [None] + [dev_t(v_levels[l], dtype, dev) for l in range(1, levels)]
-    out = plan.run(dev_t(q, dtype, dev), dev_t(k, dtype, dev), dev_t(v, dtype, dev), wt, v_levels=vl)
+    pw = None if pe_weight is None else torch.from_numpy(np.ascontiguousarray(pe_weight)).to(dev)
+    pb = None if pe_bias is None else torch.from_numpy(np.ascontiguousarray(pe_bias)).to(dev)
+    out = plan.run(dev_t(q, dtype, dev), dev_t(k, dtype, dev), dev_t(v, dtype, dev), wt, v_levels=vl, pe_weight=pw,
+                   pe_bias=pb)
     torch.cuda.synchronize()
     g_out = to_np(out)
     g_sel = [None] + [to_np(plan.selection(l)[0]) for l in range(1, levels)]
     ref = O.forward(q, k, v, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale,
-                    forced=g_sel, want_candidates=True, want_pyramids=True, v_levels=v_levels)
+                    forced=g_sel, want_candidates=True, want_pyramids=True, v_levels=v_levels, pe_weight=pe_weight,
+                    pe_bias=pe_bias)
     res = {"sel": {}, "msg": {}}
     for l in range(1, levels):
         for name in ("qk" if v_levels is not None else "qkv"):
@@ -296,14 +301,15 @@ def test_explicit_scale(dev):
 # ------------------------------------------------------------------------------------------------
 
 @pytest.mark.parametrize("name", ["tiny", "matching", "stereo", "backbone", "highres", "matching_ksched",
-                                  "backbone_vgiven"])
+                                  "backbone_vgiven", "backbone_pe"])
 def test_workload_full_size(dev, name):
     wl = WORKLOADS[name]
     q, k, v = make_qkv(wl)
     w = make_level_weights(wl) if wl.variant == "B" else None
     vl = make_v_levels(wl) if wl.v_given else None
+    pw, pb = make_pe(wl) if wl.pe else (None, None)
     res, _, _ = run_and_compare(dev, q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w,
-                                label=name, v_levels=vl)
+                                label=name, v_levels=vl, pe_weight=pw, pe_bias=pb)
     announce(f"{name}: out err {res['out']:.2e}; msg err {res['msg']}; selections {res['sel']}")
 
 
@@ -374,3 +380,42 @@ def test_supplied_pooled_v_levels_reproduce_default(dev):
     out = plan2.run(tq, tk, tv, v_levels=vl)
     torch.cuda.synchronize()
     assert torch.equal(out, ref)
+
+
+# ------------------------------------------------------------------------------------------------
+# multiscale position encoding (Sec. 3.2)
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant,dtype,B,H,W,heads,d,L,K,given_v", [
+    ("B", "f32", 1, 60, 80, 8, 32, 3, 8, False),       # matching shape, blocked intermediate level
+    ("A", "bf16", 2, 37, 29, 2, 64, 4, 4, False),      # ragged map, d = 64
+    ("B", "bf16", 1, 33, 47, 1, 32, 3, 20, False),     # 80 candidates: the wide kernel at both levels
+    ("A", "f32", 1, 25, 31, 2, 32, 3, [0, 4, 8], True),    # with a K schedule and given V levels
+    ("B", "f32", 2, 12, 9, 2, 32, 1, 4, False),        # single level: the coarse kernel forms the output
+])
+def test_forward_position_encoding(dev, variant, dtype, B, H, W, heads, d, L, K, given_v):
+    q, k, v = rand_qkv(800 + H * W + L, B, H, W, heads, d, dtype)
+    rng = np.random.default_rng(88)
+    C = heads * d
+    pw = (rng.standard_normal((L, C, 3, 3)) * 0.3).astype(np.float32)
+    pb = (rng.standard_normal((L, C)) * 0.1).astype(np.float32)
+    vl = None
+    if given_v:
+        dims = O.level_dims(H, W, L)
+        vl = [None] + [rng.standard_normal((B, dims[l][0], dims[l][1], heads, d)).astype(np.float32)
+                       for l in range(1, L)]
+        if dtype == "bf16":
+            vl = [None] + [round_bf16(x) for x in vl[1:]]
+    w = np.random.default_rng(9).random((B, H * W, heads, L)).astype(np.float32) if variant == "B" else None
+    if L == 1:
+        announce(f"position encoding, single level {variant} {dtype}")
+        plan = P.Plan(B, H, W, heads, d, levels=1, K=K, variant=variant, dtype=TDT[dtype], device=dev, pe=True)
+        out = plan.run(dev_t(q, dtype, dev), dev_t(k, dtype, dev), dev_t(v, dtype, dev),
+                       None if w is None else torch.from_numpy(w).to(dev),
+                       pe_weight=torch.from_numpy(pw).to(dev), pe_bias=torch.from_numpy(pb).to(dev))
+        torch.cuda.synchronize()
+        ref = O.forward(q, k, v, levels=1, K=K, variant=variant, dtype=dtype, w=w, pe_weight=pw, pe_bias=pb)
+        assert rel_err(to_np(out), ref["out"]) <= TOL[dtype]
+        return
+    run_and_compare(dev, q, k, v, levels=L, K=K, variant=variant, dtype=dtype, w=w, v_levels=vl, pe_weight=pw,
+                    pe_bias=pb, label="position encoding")
