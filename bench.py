@@ -36,13 +36,14 @@ def finest_kernel_bytes(wl) -> dict:
     fused combination), counting every tensor once plus one gather of each sibling group's
     candidate key and value rows:
       per (batch, head):  N0*d*b (queries) + N1*K*sigma (parent selections; sigma = 4 B for B, 8 B
-      for A, which also reads the scores) + N1*4K*2*d*b (gathered key/value rows, four children per
-      kept key) + N1*(L-1)*d*4 (the ancestors' fp32 messages, once per sibling group)
-      + [B] N0*L*4 (level weights) + N0*d*b (output)."""
+      for A, which also reads the scores) + N1*c*K*2*d*b (gathered key/value rows, c = 4 children
+      per kept key, 2 on one-row maps) + N1*(L-1)*d*4 (the ancestors' fp32 messages, once per
+      sibling group) + [B] N0*L*4 (level weights) + N0*d*b (output)."""
     from paper_2201_02767_amd.inputs import Workload  # noqa: F401  (type only)
     import paper_2201_02767_amd as P
 
-    dims = P.level_dims(wl.H, wl.W, wl.levels)
+    mB, mH = (wl.B * wl.H, 1) if wl.epipolar else (wl.B, wl.H)      # the maps the library works on
+    dims = P.level_dims(mH, wl.W, wl.levels)
     n0 = dims[0][0] * dims[0][1]
     n1 = dims[1][0] * dims[1][1]
     b = 2 if wl.dtype == "bf16" else 4
@@ -51,12 +52,12 @@ def finest_kernel_bytes(wl) -> dict:
     parts = {
         "queries": n0 * wl.d * b,
         "parent_selections": n1 * K1 * sigma,
-        "gather": n1 * 4 * K1 * 2 * wl.d * b,
+        "gather": n1 * (2 if mH == 1 else 4) * K1 * 2 * wl.d * b,
         "ancestor_messages": n1 * (wl.levels - 1) * wl.d * 4,
         "level_weights": n0 * wl.levels * 4 if wl.variant == "B" else 0,
         "output": n0 * wl.d * b,
     }
-    units = wl.B * wl.heads
+    units = mB * wl.heads
     return {k: v * units for k, v in parts.items()}
 
 
@@ -87,6 +88,9 @@ def cpu_baseline(wl, seconds: float) -> dict:
     w = make_level_weights(wl) if wl.variant == "B" else None
     vl = make_v_levels(wl) if wl.v_given else None
     pw, pb = make_pe(wl) if wl.pe else (None, None)
+    if wl.epipolar:     # every row its own 1 x W map
+        q, k, v = (x.reshape(wl.B * wl.H, 1, wl.W, wl.heads, wl.d) for x in (q, k, v))
+        w = None if w is None else w.reshape(wl.B * wl.H, wl.W, wl.heads, wl.levels)
     runs, t0 = 0, time.perf_counter()
     while True:
         oracle.forward(q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w, v_levels=vl,
@@ -151,7 +155,7 @@ def main() -> int:
     if wl.pe:
         pw, pb = (torch.from_numpy(x).to(dev) for x in make_pe(wl))
     plan = P.Plan(wl.B, wl.H, wl.W, wl.heads, wl.d, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=tdt,
-                  device=dev, v_supplied=wl.v_given, pe=wl.pe)
+                  device=dev, v_supplied=wl.v_given, pe=wl.pe, epipolar=wl.epipolar)
     step = plan.prepare(q, k, v, w, v_levels=vl, pe_weight=pw, pe_bias=pb)
     log(f"bench: {wl} on {torch.cuda.get_device_name(0)}")
 
@@ -209,6 +213,7 @@ def main() -> int:
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "W": wl.W, "heads": wl.heads, "d": wl.d,
                    "levels": wl.levels, "K": wl.K if isinstance(wl.K, int) else list(wl.K)[1:],
                    "v_levels": "given" if wl.v_given else "pooled", "position_encoding": wl.pe,
+                   "attention": "epipolar rows" if wl.epipolar else "2-D",
                    "variant": wl.variant, "global_batch": wl.B,
                    "seq_len": wl.H * wl.W, "parallelism": "none (1 GPU)"},
         "roofline": roof, "cpu_baseline": cpu,

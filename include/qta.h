@@ -131,12 +131,20 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
  *              levels are combined. NULL: no position encoding.
  *   pe_bias    device fp32 [levels][heads*d], 16-byte aligned, added with it; NULL: none.
  *              Requires pe_weight.
+ *   epipolar   nonzero: attention along the rows only, as in stereo matching where both self- and
+ *              cross attention stay on epipolar lines (Sec. 4.1.2). Every row of every batch
+ *              element is then an independent 1 x W map: the pyramids pool pairs along the row
+ *              (the quadtree becomes a binary tree) and a query meets the 2 children of each kept
+ *              key. Shapes, layouts and w are unchanged; the result is the call on B*H maps of
+ *              1 x W, which is also how the workspace and v_levels are laid out
+ *              ([B*H][1][W_l][heads][d]) and how `levels` is validated (by W alone).
  */
 typedef struct {
     const int* K_levels;
     const void* const* v_levels;
     const float* pe_weight;
     const float* pe_bias;
+    int epipolar;
 } qta_options;
 
 /* Workspace of qta_forward_ex with these options (layout and byte count as for qta_forward; with a

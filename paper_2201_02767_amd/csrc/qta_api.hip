@@ -214,10 +214,24 @@ qta_status qta_level_dims(int H, int W, int levels, int* Hl, int* Wl)
     return dims(H, W, levels, Hl, Wl);
 }
 
+// Epipolar attention is the same layer on every row as its own 1 x W map (B*H maps of 1 x W).
+qta_status rows_as_maps(const qta_options* opt, int* B, int* H)
+{
+    if (!opt || !opt->epipolar) return QTA_OK;
+    if (*B <= 0 || *H <= 0) return QTA_ERR_INVALID;
+    const long long rows = static_cast<long long>(*B) * *H;
+    if (rows > 0x7FFFFFFFLL) return QTA_ERR_UNSUPPORTED;
+    *B = static_cast<int>(rows);
+    *H = 1;
+    return QTA_OK;
+}
+
 qta_status qta_get_workspace_layout_ex(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype,
                                        const qta_options* opt, qta_workspace_layout* out)
 {
     if (!out) return QTA_ERR_INVALID;
+    qta_status rs = rows_as_maps(opt, &B, &H);
+    if (rs != QTA_OK) return rs;
     Options o;
     qta_status st = read_options(K, levels, opt, &o);
     if (st != QTA_OK) return st;
@@ -393,6 +407,8 @@ qta_status qta_forward_ex(const void* q, const void* k, const void* v, const flo
     if (st != QTA_OK) return st;
     if (!q || !k || !v || !out) return QTA_ERR_INVALID;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return QTA_ERR_INVALID;
+    st = rows_as_maps(opt, &B, &H);
+    if (st != QTA_OK) return st;
     Options o;
     st = read_options(K, levels, opt, &o);
     if (st != QTA_OK) return st;

@@ -23,6 +23,8 @@ not used):
              N(0,1) map standing in for that layer's normalised output.
   backbone_pe - backbone with the multiscale position encoding (Sec. 3.2): 3x3 depth-wise kernels
              N(0, 0.3^2) and biases N(0, 0.1^2) per level and channel (random-init weights).
+  stereo_epipolar - stereo with attention along the epipolar lines only (Sec. 4.1.2): each of the
+             2 x 120 rows of 160 tokens is its own binary tree of 4 levels.
 
 Seeds: numpy PCG64 with seed = 1000 * config_number + tensor id (q=1, k=2, v=3, w=4, aux=5,
 10 + l for the given V level l, 20 and 21 for the position-encoding weights and biases).
@@ -52,6 +54,7 @@ class Workload:
     kind: str         # generator: "iid_scaled", "shift", "disparity", "smooth"
     v_given: bool = False   # V's coarser levels are inputs (make_v_levels) instead of pooled
     pe: bool = False        # multiscale position encoding (make_pe)
+    epipolar: bool = False  # attention along rows only
 
     @property
     def tokens(self) -> int:
@@ -70,6 +73,8 @@ WORKLOADS = {
     "matching_ksched": Workload("matching_ksched", 2, 1, 60, 80, 8, 32, 3, (0, 8, 16), "B", "f32", "shift"),
     "backbone_vgiven": Workload("backbone_vgiven", 4, 32, 56, 56, 1, 64, 3, 8, "B", "bf16", "smooth", True),
     "backbone_pe": Workload("backbone_pe", 4, 32, 56, 56, 1, 64, 3, 8, "B", "bf16", "smooth", False, True),
+    "stereo_epipolar": Workload("stereo_epipolar", 3, 2, 120, 160, 8, 32, 4, 8, "B", "bf16", "disparity",
+                                epipolar=True),
 }
 
 

@@ -51,6 +51,7 @@ class Options(ctypes.Structure):
         ("v_levels", ctypes.c_void_p),
         ("pe_weight", ctypes.c_void_p),
         ("pe_bias", ctypes.c_void_p),
+        ("epipolar", ctypes.c_int),
     ]
 
 
@@ -156,11 +157,12 @@ def _k_table(Kl):
 _FAKE_PTR = 256      # a non-NULL, aligned, never-dereferenced device address (layout queries only)
 
 
-def _layout_options(K, levels, v_supplied, pe):
+def _layout_options(K, levels, v_supplied, pe, epipolar=False):
     """Options for a layout query (only which options are present matters there)."""
     tbl = _k_table(k_levels(K, levels))
     opt = Options()
     opt.K_levels = ctypes.addressof(tbl)
+    opt.epipolar = int(bool(epipolar))
     vt = None
     if v_supplied:
         vt = (ctypes.c_void_p * MAX_LEVELS)(*([_FAKE_PTR] * MAX_LEVELS))
@@ -171,9 +173,9 @@ def _layout_options(K, levels, v_supplied, pe):
 
 
 def workspace_layout(B, heads, H, W, d, levels, K, dtype: torch.dtype, v_supplied: bool = False,
-                     pe: bool = False) -> WorkspaceLayout:
+                     pe: bool = False, epipolar: bool = False) -> WorkspaceLayout:
     lay = WorkspaceLayout()
-    opt, keep = _layout_options(K, levels, v_supplied, pe)
+    opt, keep = _layout_options(K, levels, v_supplied, pe, epipolar)
     _check("qta_get_workspace_layout_ex",
            lib().qta_get_workspace_layout_ex(B, heads, H, W, d, levels, 1, _DTYPES[dtype], ctypes.byref(opt),
                                              ctypes.byref(lay)))
@@ -181,8 +183,8 @@ def workspace_layout(B, heads, H, W, d, levels, K, dtype: torch.dtype, v_supplie
 
 
 def workspace_bytes(B, heads, H, W, d, levels, K, dtype: torch.dtype, v_supplied: bool = False,
-                    pe: bool = False) -> int:
-    opt, keep = _layout_options(K, levels, v_supplied, pe)
+                    pe: bool = False, epipolar: bool = False) -> int:
+    opt, keep = _layout_options(K, levels, v_supplied, pe, epipolar)
     return int(lib().qta_workspace_bytes_ex(B, heads, H, W, d, levels, 1, _DTYPES[dtype], ctypes.byref(opt)))
 
 
@@ -196,10 +198,12 @@ class Plan:
     ``K``: one count for every level, or one entry per level (entry l is level l's K, entry 0
     unused). ``v_supplied``: V's coarser levels come from the caller (``v_levels`` of run/prepare).
     ``pe``: a multiscale position encoding is applied (``pe_weight``/``pe_bias`` of run/prepare).
+    ``epipolar``: attention along rows only (every row an independent 1 x W map; levels, workspace
+    views and ``v_levels`` then follow the B*H maps of 1 x W).
     """
 
     def __init__(self, B, H, W, heads, d, *, levels, K, variant, dtype, device, scale=None, v_supplied=False,
-                 pe=False):
+                 pe=False, epipolar=False):
         self.B, self.H, self.W, self.heads, self.d = B, H, W, heads, d
         self.levels, self.variant, self.dtype = levels, variant, dtype
         self.K_levels = k_levels(K, levels)
@@ -207,8 +211,11 @@ class Plan:
         self.scale = scale
         self.v_supplied = bool(v_supplied)
         self.pe = bool(pe)
+        self.epipolar = bool(epipolar)
+        # the maps the library works on: B*H rows of 1 x W for epipolar attention
+        self.mB, self.mH = (B * H, 1) if self.epipolar else (B, H)
         self.device = torch.device(device)
-        self.layout = workspace_layout(B, heads, H, W, d, levels, K, dtype, self.v_supplied, self.pe)
+        self.layout = workspace_layout(B, heads, H, W, d, levels, K, dtype, self.v_supplied, self.pe, self.epipolar)
         self._k_tbl = _k_table(self.K_levels)
         nbytes = max(int(self.layout.total), 256)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
@@ -231,7 +238,7 @@ class Plan:
             for l in range(1, self.levels):
                 t = v_levels[l]
                 _require(t, f"v_levels[{l}]", self.dtype, 5)
-                if tuple(t.shape) != (self.B, self.layout.H[l], self.layout.W[l], self.heads, self.d):
+                if tuple(t.shape) != (self.mB, self.layout.H[l], self.layout.W[l], self.heads, self.d):
                     raise ValueError(f"v_levels[{l}] has shape {tuple(t.shape)}")
                 vtbl[l] = t.data_ptr()
         if (pe_weight is not None) != self.pe:
@@ -252,6 +259,7 @@ class Plan:
         opt.v_levels = ctypes.addressof(vtbl) if vtbl is not None else None
         opt.pe_weight = pe_weight.data_ptr() if pe_weight is not None else None
         opt.pe_bias = pe_bias.data_ptr() if pe_bias is not None else None
+        opt.epipolar = int(self.epipolar)
         return opt, vtbl
 
     def _call_args(self, q, k, v, w, opt, stream):
@@ -291,7 +299,7 @@ class Plan:
         sidx, skey = self.selection(1)
         msgs = [self.message(j) for j in range(1, self.levels)]
         table = (ctypes.c_void_p * (self.levels - 1))(*[m.data_ptr() for m in msgs])
-        args = (_ptr(q), _ptr(k), _ptr(v), self.B, self.heads, self.H, self.W, self.d, self.K_levels[1],
+        args = (_ptr(q), _ptr(k), _ptr(v), self.mB, self.heads, self.mH, self.W, self.d, self.K_levels[1],
                 _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), _ptr(sidx), _ptr(skey),
                 self.levels, ctypes.addressof(table), _ptr(w), _ptr(self.out), _stream(self.device))
         keep = (q, k, v, w, table, msgs)
@@ -312,42 +320,42 @@ class Plan:
         return self.workspace[off:off + nbytes].view(dtype).view(shape)
 
     def pyramid(self, which: str, level: int):
-        """Pyramid level `level` (>= 1) of q, k or v as [B, H_l, W_l, heads, d]; blocked storage is
-        unpacked into a new tensor."""
+        """Pyramid level `level` (>= 1) of q, k or v as [B, H_l, W_l, heads, d] (B*H maps of one row
+        for epipolar attention); blocked storage is unpacked into a new tensor."""
         lay = self.layout
         off = getattr(lay, which)[level]
         H, W = lay.H[level], lay.W[level]
         if not lay.blocked[level]:
-            return self._view(off, (self.B, H, W, self.heads, self.d), self.dtype)
+            return self._view(off, (self.mB, H, W, self.heads, self.d), self.dtype)
         return self._unblock(off, H, W)
 
     def _unblock(self, off, H, W):
         Hp, Wp = (H + 1) // 2, (W + 1) // 2
-        t = self._view(off, (self.B, self.heads, Hp, Wp, 2, 2, self.d), self.dtype)
-        t = t.permute(0, 2, 4, 3, 5, 1, 6).reshape(self.B, 2 * Hp, 2 * Wp, self.heads, self.d)
+        t = self._view(off, (self.mB, self.heads, Hp, Wp, 2, 2, self.d), self.dtype)
+        t = t.permute(0, 2, 4, 3, 5, 1, 6).reshape(self.mB, 2 * Hp, 2 * Wp, self.heads, self.d)
         return t[:, :H, :W].contiguous()
 
     def message(self, level: int):
         lay = self.layout
-        return self._view(lay.msg[level], (self.B, lay.H[level] * lay.W[level], self.heads, self.d), torch.float32)
+        return self._view(lay.msg[level], (self.mB, lay.H[level] * lay.W[level], self.heads, self.d), torch.float32)
 
     def selection(self, level: int):
         lay = self.layout
-        shape = (self.B, self.heads, lay.H[level] * lay.W[level], lay.K[level])
+        shape = (self.mB, self.heads, lay.H[level] * lay.W[level], lay.K[level])
         return (self._view(lay.sel_idx[level], shape, torch.int32),
                 self._view(lay.sel_key[level], shape, torch.float32))
 
 
 def forward(q, k, v, *, levels: int, K, variant: str, w=None, scale=None, v_levels=None, pe_weight=None,
-            pe_bias=None) -> torch.Tensor:
+            pe_bias=None, epipolar: bool = False) -> torch.Tensor:
     """QuadTree attention forward; returns ``out`` [B, H, W, heads, d] in q's dtype. ``K``: one count
     or one per level (entry 0 unused); ``v_levels``: None, or a list whose entry l (l >= 1) is V at
     level l, [B, H_l, W_l, heads, d]; ``pe_weight`` fp32 [levels, heads*d, 3, 3] and ``pe_bias`` fp32
-    [levels, heads*d]: the multiscale position encoding."""
+    [levels, heads*d]: the multiscale position encoding; ``epipolar``: attention along rows only."""
     _require(q, "q", None, 5)
     B, H, W, heads, d = q.shape
     plan = Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=q.dtype, device=q.device,
-                scale=scale, v_supplied=v_levels is not None, pe=pe_weight is not None)
+                scale=scale, v_supplied=v_levels is not None, pe=pe_weight is not None, epipolar=epipolar)
     return plan.run(q, k, v, w, v_levels=v_levels, pe_weight=pe_weight, pe_bias=pe_bias)
 
 

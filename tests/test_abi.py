@@ -252,3 +252,22 @@ def test_position_encoding_workspace():
     assert lay.total >= lay.pe0 + 2 * 40 * 30 * 64 * 4
     single = P.workspace_layout(1, 1, 16, 16, 32, 1, 4, torch.float32, pe=True)
     assert single.total >= 16 * 16 * 32 * 4
+
+
+def test_epipolar_layout_is_that_of_one_row_maps():
+    """Attention along rows works on B*H maps of one row: the same workspace as that problem."""
+    for dt in (torch.float32, torch.bfloat16):
+        for pe in (False, True):
+            a = P.workspace_layout(2, 8, 120, 160, 32, 4, 8, dt, pe=pe, epipolar=True)
+            b = P.workspace_layout(240, 8, 1, 160, 32, 4, 8, dt, pe=pe)
+            assert a.total == b.total and a.pe0 == b.pe0
+            for f in ("H", "W", "blocked", "K", "q", "k", "v", "msg", "sel_idx", "sel_key"):
+                assert list(getattr(a, f)) == list(getattr(b, f)), f
+    lay = P.workspace_layout(3, 1, 7, 37, 32, 3, [0, 2, 4], torch.float32, epipolar=True)
+    assert list(lay.H)[:3] == [1, 1, 1] and list(lay.W)[:3] == [37, 19, 10]
+
+
+def test_epipolar_row_count_limit():
+    """B*H rows must fit the map count; a count past 2^31 - 1 is rejected, not wrapped."""
+    with pytest.raises(P.QtaError):
+        P.workspace_layout(1 << 16, 1, 1 << 16, 8, 32, 2, 4, torch.float32, epipolar=True)

@@ -52,14 +52,15 @@ def dev_t(x, dtype, dev):
 # ------------------------------------------------------------------------------------------------
 
 def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=None, label="", v_levels=None,
-                    pe_weight=None, pe_bias=None):
+                    pe_weight=None, pe_bias=None, epipolar=False):
     """GPU forward vs teacher-forced oracle; returns a dict of the measured agreement. ``K``: one
-    count or one per level; ``v_levels``: None or the caller's V levels (numpy, entry l >= 1)."""
+    count or one per level; ``v_levels``: None or the caller's V levels (numpy, entry l >= 1);
+    ``epipolar``: attention along rows, checked against the oracle on the B*H one-row maps."""
     B, H, W, heads, d = q.shape
     announce(f"forward {label} B={B} H={H} W={W} heads={heads} d={d} L={levels} K={K} {variant} {dtype}"
-             f"{' V levels given' if v_levels is not None else ''}")
+             f"{' V levels given' if v_levels is not None else ''}{' epipolar' if epipolar else ''}")
     plan = P.Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=TDT[dtype], device=dev, scale=scale,
-                  v_supplied=v_levels is not None, pe=pe_weight is not None)
+                  v_supplied=v_levels is not None, pe=pe_weight is not None, epipolar=epipolar)
     Kl = P.k_levels(K, levels)
     wt = None if w is None else torch.from_numpy(w).to(dev)
     vl = None if v_levels is None else [None] + [dev_t(v_levels[l], dtype, dev) for l in range(1, levels)]
@@ -70,6 +71,10 @@ def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=No
     torch.cuda.synchronize()
     g_out = to_np(out)
     g_sel = [None] + [to_np(plan.selection(l)[0]) for l in range(1, levels)]
+    if epipolar:        # the oracle sees what the library computes: B*H maps of one row
+        q, k, v = (x.reshape(B * H, 1, W, heads, d) for x in (q, k, v))
+        w = None if w is None else w.reshape(B * H, W, heads, levels)
+        g_out = g_out.reshape(B * H, 1, W, heads, d)
     ref = O.forward(q, k, v, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale,
                     forced=g_sel, want_candidates=True, want_pyramids=True, v_levels=v_levels, pe_weight=pe_weight,
                     pe_bias=pe_bias)
@@ -301,7 +306,7 @@ def test_explicit_scale(dev):
 # ------------------------------------------------------------------------------------------------
 
 @pytest.mark.parametrize("name", ["tiny", "matching", "stereo", "backbone", "highres", "matching_ksched",
-                                  "backbone_vgiven", "backbone_pe"])
+                                  "backbone_vgiven", "backbone_pe", "stereo_epipolar"])
 def test_workload_full_size(dev, name):
     wl = WORKLOADS[name]
     q, k, v = make_qkv(wl)
@@ -309,7 +314,7 @@ def test_workload_full_size(dev, name):
     vl = make_v_levels(wl) if wl.v_given else None
     pw, pb = make_pe(wl) if wl.pe else (None, None)
     res, _, _ = run_and_compare(dev, q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w,
-                                label=name, v_levels=vl, pe_weight=pw, pe_bias=pb)
+                                label=name, v_levels=vl, pe_weight=pw, pe_bias=pb, epipolar=wl.epipolar)
     announce(f"{name}: out err {res['out']:.2e}; msg err {res['msg']}; selections {res['sel']}")
 
 
@@ -419,3 +424,52 @@ def test_forward_position_encoding(dev, variant, dtype, B, H, W, heads, d, L, K,
         return
     run_and_compare(dev, q, k, v, levels=L, K=K, variant=variant, dtype=dtype, w=w, v_levels=vl, pe_weight=pw,
                     pe_bias=pb, label="position encoding")
+
+
+# ------------------------------------------------------------------------------------------------
+# attention along epipolar lines (Sec. 4.1.2): every row its own one-row map, a binary tree
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant,dtype,B,H,W,heads,d,L,K,given_v,pe", [
+    ("B", "bf16", 2, 7, 160, 8, 32, 4, 8, False, False),    # stereo-like rows
+    ("A", "f32", 1, 5, 37, 2, 32, 3, 4, False, False),      # ragged rows
+    ("A", "bf16", 2, 3, 93, 1, 64, 5, [0, 2, 4, 8, 16], False, False),   # K schedule; 4 levels of pairs
+    ("B", "f32", 1, 4, 50, 2, 32, 3, 20, False, False),     # 40 candidates per query
+    ("B", "bf16", 1, 6, 41, 2, 32, 3, 4, True, True),       # given V levels and the position encoding
+])
+def test_forward_epipolar(dev, variant, dtype, B, H, W, heads, d, L, K, given_v, pe):
+    q, k, v = rand_qkv(900 + H * W + L, B, H, W, heads, d, dtype)
+    rng = np.random.default_rng(91)
+    w = rng.random((B, H * W, heads, L)).astype(np.float32) if variant == "B" else None
+    vl = None
+    if given_v:
+        dims = O.level_dims(1, W, L)
+        vl = [None] + [rng.standard_normal((B * H, 1, dims[l][1], heads, d)).astype(np.float32)
+                       for l in range(1, L)]
+        if dtype == "bf16":
+            vl = [None] + [round_bf16(x) for x in vl[1:]]
+    pw = (rng.standard_normal((L, heads * d, 3, 3)) * 0.3).astype(np.float32) if pe else None
+    pb = (rng.standard_normal((L, heads * d)) * 0.1).astype(np.float32) if pe else None
+    run_and_compare(dev, q, k, v, levels=L, K=K, variant=variant, dtype=dtype, w=w, v_levels=vl, pe_weight=pw,
+                    pe_bias=pb, epipolar=True, label="epipolar")
+
+
+def test_epipolar_rows_are_independent_at_full_size(dev):
+    """On the full stereo workload, sampled rows run alone (as a 1 x 160 map) give the same output as
+    in the epipolar run over all 240 rows, bit for bit: the rows do not interact."""
+    wl = WORKLOADS["stereo_epipolar"]
+    announce("epipolar rows independent, stereo 2 x 120 x 160")
+    q, k, v = make_qkv(wl)
+    w = make_level_weights(wl)
+    plan = P.Plan(wl.B, wl.H, wl.W, wl.heads, wl.d, levels=wl.levels, K=wl.K, variant="B", dtype=torch.bfloat16,
+                  device=dev, epipolar=True)
+    out = to_np(plan.run(dev_t(q, "bf16", dev), dev_t(k, "bf16", dev), dev_t(v, "bf16", dev),
+                         torch.from_numpy(w).to(dev)))
+    one = P.Plan(1, 1, wl.W, wl.heads, wl.d, levels=wl.levels, K=wl.K, variant="B", dtype=torch.bfloat16, device=dev)
+    w_rows = w.reshape(wl.B, wl.H, wl.W, wl.heads, wl.levels)
+    for b, y in [(0, 0), (0, 57), (1, 119), (1, 3)]:
+        row = [dev_t(np.ascontiguousarray(x[b:b + 1, y:y + 1]), "bf16", dev) for x in (q, k, v)]
+        o = to_np(one.run(*row, torch.from_numpy(np.ascontiguousarray(w_rows[b, y])).reshape(1, wl.W, wl.heads,
+                                                                                               wl.levels).to(dev)))
+        torch.cuda.synchronize()
+        assert np.array_equal(o[0, 0], out[b, y]), f"row {b},{y} differs from its run alone"

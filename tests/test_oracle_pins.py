@@ -477,3 +477,42 @@ def test_position_encoding_bias_only_shifts_output(variant):
         shift = sum(w[0, :, 0, l][:, None] * pb[l][None, :].astype(np.float64) for l in range(L))
     np.testing.assert_allclose(r["out"].reshape(H * W, 8) - base["out"].reshape(H * W, 8),
                                np.broadcast_to(shift, (H * W, 8)), atol=1e-12)
+
+
+# ------------------------------------------------------- attention along rows (binary tree) ----
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+@pytest.mark.parametrize("W,L,K", [(16, 4, 2), (13, 3, 3), (40, 5, [0, 2, 4, 4, 8])])
+def test_one_row_maps_match_brute_force(variant, W, L, K):
+    """Stereo attention stays on epipolar lines (Sec. 4.1.2): on a map of one row the pyramid pools
+    pairs and a query meets the two children of each kept key (a binary tree). The oracle equals
+    the explicit-region formulation on such maps."""
+    rng = np.random.default_rng(70 + W + L)
+    q, k, v = (dyadic(rng, (3, 1, W, 2, 4)) for _ in range(3))
+    w = rng.random((3, W, 2, L)).astype(np.float32)
+    r = O.forward(q, k, v, levels=L, K=K, variant=variant, w=w if variant == "B" else None, want_candidates=True)
+    ref = brute.brute_quadtree(q, k, v, L, K, variant, 0.5, w if variant == "B" else None)
+    np.testing.assert_allclose(r["out"], ref, rtol=0, atol=1e-12)
+    # every candidate set of a fine level holds the 2 children of each kept parent key, never more
+    Kl = [K] * L if np.ndim(K) == 0 else K
+    for l in range(L - 1):
+        valid = (r["cand_idx"][l] >= 0).sum(-1)
+        assert valid.max() <= 2 * Kl[l + 1]
+
+
+def test_one_row_b_with_all_keys_kept_is_dense_along_the_row():
+    """P7 on one-row maps: keeping every key, each level's message is dense attention along the row
+    of that level (pairs pooled), combined with w."""
+    rng = np.random.default_rng(71)
+    W, L = 16, 3
+    q, k, v = (dyadic(rng, (2, 1, W, 1, 4)) for _ in range(3))
+    w = rng.random((2, W, 1, L)).astype(np.float32)
+    r = O.forward(q, k, v, levels=L, K=W, variant="B", w=w, scale=0.5)
+    PQ = brute.pyramid(q.reshape(2, 1, W, 4), L)
+    PK = brute.pyramid(k.reshape(2, 1, W, 4), L)
+    PV = brute.pyramid(v.reshape(2, 1, W, 4), L)
+    for l in range(L):
+        n = PQ[l].shape[2]
+        dense = brute.dense_attention(PQ[l].reshape(2, n, 1, 4), PK[l].reshape(2, n, 1, 4),
+                                      PV[l].reshape(2, n, 1, 4), 0.5)
+        np.testing.assert_allclose(r["msg"][l], dense, atol=1e-12)
