@@ -493,3 +493,338 @@ done:
     free(ck); free(ci); free(cv); free(cx); free(pos); free(taken); free(in_sel); free(acc);
     return rc;
 }
+
+/* ----------------------------------------------------------------------------------------- */
+/* backward                                                                                   */
+/* ----------------------------------------------------------------------------------------- */
+
+/*
+ * Gradients of the layer output with respect to q, k, v and (QuadTree-B) w, for an upstream
+ * gradient dout = dLoss/dout. The kept-key sets are held fixed: they are the forward's (or the
+ * forced ones), and the gradient flows through everything computed from them. The chain rule is
+ * taken step by step through the forward above:
+ *   - combination (Eqs. 2 and 5): dm^l at a level-l token is the sum over its finest descendants i
+ *     of w_{i,l} dout_i (1 for A); dw_{i,l} = <dout_i, m^l of the ancestor>;
+ *   - QuadTree-B at a level (Eq. 6): m = sum_j p_j v_j with p a softmax over the candidates, so
+ *     dv_j += p_j dm, g_j = <dm, v_j>, dlogit_j = p_j (g_j - sum_j' p_j' g_j');
+ *   - QuadTree-A at a level (Eqs. 3-4): m = sum over Omega of s_j v_j with s_j = sigma_r t_j, t a
+ *     softmax over the children of kept key r and sigma_r that key's score at the parent level. The
+ *     gradient of s_j is <dm, v_j> on Omega and, for a key this query keeps, the gradient of its
+ *     score that the next finer level sends back (its children's s are sigma times their t). Then
+ *     dsigma_r = sum over r's children of t_j ds_j goes up to the parent, dt_j = sigma_r ds_j, and
+ *     dlogit_j = t_j (dt_j - sum over r's children of t_j' dt_j');
+ *   - logits tau <q, k_j>: dq += tau dlogit_j k_j, dk_j += tau dlogit_j q;
+ *   - pyramid (Sec. 3.2): a pooled token is the mean of its n valid children, so each child
+ *     receives 1/n of the pooled token's gradient (the storage rounding of pooled values is taken
+ *     as the identity).
+ * The levels are processed finest first, so that QuadTree-A's score gradients reach the coarser
+ * level that produced the scores. Caller-supplied V levels and the position encoding are not
+ * covered (return -1).
+ *
+ * Return codes as qo_forward.
+ */
+typedef struct {
+    qo_forward_args fwd;          /* the forward problem; its output pointers are ignored        */
+    const float* dout;            /* [B][H][W][heads*d]                                           */
+    double* dq;                   /* [B][H][W][heads*d] each                                      */
+    double* dk;
+    double* dv;
+    double* dw;                   /* B with w given: [B][H*W][heads][L]; otherwise not written    */
+} qo_backward_args;
+
+int qo_backward(const qo_backward_args* ba)
+{
+    if (!ba || !ba->dout || !ba->dq || !ba->dk || !ba->dv) return -1;
+    const qo_forward_args* a = &ba->fwd;
+    if (a->v_levels || a->pe_weight) return -1;
+    const int B = a->B, NH = a->heads, H = a->H, W = a->W, d = a->d, L = a->L, K = a->K;
+    if (B <= 0 || NH <= 0 || d <= 0 || K <= 0) return -1;
+    int Hl[QO_MAX_LEVELS], Wl[QO_MAX_LEVELS];
+    if (qo_level_dims(H, W, L, Hl, Wl) != 0) return -1;
+    const int C = NH * d;
+    const double tau = a->scale > 0.0 ? a->scale : 1.0 / sqrt((double)d);
+    const int isB = a->variant == QO_B;
+    size_t Nl[QO_MAX_LEVELS] = {0};
+    int Kl[QO_MAX_LEVELS] = {0};
+    int Kmax = 1;
+    for (int l = 0; l < L; ++l) {
+        Nl[l] = (size_t)Hl[l] * (size_t)Wl[l];
+        Kl[l] = a->K_levels ? a->K_levels[l] : K;
+        if (l >= 1 && Kl[l] > Kmax) Kmax = Kl[l];
+    }
+    const int Lc = L - 1;
+
+    int rc = 0;
+    float* pq[QO_MAX_LEVELS] = {0};
+    float* pk[QO_MAX_LEVELS] = {0};
+    float* pv[QO_MAX_LEVELS] = {0};
+    double* msg[QO_MAX_LEVELS] = {0};
+    int32_t* sel[QO_MAX_LEVELS] = {0};
+    double* key[QO_MAX_LEVELS] = {0};
+    double* dm[QO_MAX_LEVELS] = {0};     /* dLoss/dm^l, [B][N_l][heads][d] */
+    double* dQ[QO_MAX_LEVELS] = {0};     /* gradients at each level, [B][N_l][C] */
+    double* dK[QO_MAX_LEVELS] = {0};
+    double* dV[QO_MAX_LEVELS] = {0};
+    double* dsig[QO_MAX_LEVELS] = {0};   /* A: dLoss/d(kept score), [B][heads][N_l][K_l] */
+    const int ncand_max = (int)Nl[Lc] > 4 * Kmax ? (int)Nl[Lc] : 4 * Kmax;
+    double* cx = malloc(sizeof(double) * ncand_max);   /* logits */
+    double* cp = malloc(sizeof(double) * ncand_max);   /* B: p; A: t */
+    double* cs = malloc(sizeof(double) * ncand_max);   /* A: s = sigma t */
+    double* cg = malloc(sizeof(double) * ncand_max);   /* dLoss/d(weight) */
+    double* cd = malloc(sizeof(double) * ncand_max);   /* dLoss/d(logit) */
+    int* ci = malloc(sizeof(int) * ncand_max);
+    int* cv = malloc(sizeof(int) * ncand_max);
+    int* kpos = malloc(sizeof(int) * ncand_max);       /* position in the query's own kept list, or -1 */
+    if (!cx || !cp || !cs || !cg || !cd || !ci || !cv || !kpos) { rc = -3; goto done; }
+
+    for (int l = 0; l < L; ++l) {
+        const size_t n = (size_t)B * Nl[l] * C;
+        pq[l] = malloc(sizeof(float) * n);
+        pk[l] = malloc(sizeof(float) * n);
+        pv[l] = malloc(sizeof(float) * n);
+        msg[l] = malloc(sizeof(double) * n);
+        dm[l] = calloc(n, sizeof(double));
+        dQ[l] = calloc(n, sizeof(double));
+        dK[l] = calloc(n, sizeof(double));
+        dV[l] = calloc(n, sizeof(double));
+        if (!pq[l] || !pk[l] || !pv[l] || !msg[l] || !dm[l] || !dQ[l] || !dK[l] || !dV[l]) { rc = -3; goto done; }
+        if (l >= 1) {
+            const size_t ns = (size_t)B * NH * Nl[l] * Kl[l];
+            sel[l] = malloc(sizeof(int32_t) * ns);
+            key[l] = malloc(sizeof(double) * ns);
+            dsig[l] = calloc(ns, sizeof(double));
+            if (!sel[l] || !key[l] || !dsig[l]) { rc = -3; goto done; }
+        }
+    }
+
+    /* the forward, for its pyramids, messages, kept keys and their scores */
+    {
+        qo_forward_args f = *a;
+        f.out = NULL;
+        f.pyr_q = pq;
+        f.pyr_k = pk;
+        f.pyr_v = pv;
+        f.msg = msg;
+        f.sel_idx = sel;
+        f.sel_key = key;
+        f.cand_idx = NULL;
+        f.cand_key = NULL;
+        rc = qo_forward(&f);
+        if (rc != 0) goto done;
+        for (size_t i = 0; i < (size_t)B * Nl[0] * C; ++i) {
+            pq[0][i] = round_to_dtype(a->q[i], a->dtype);
+            pk[0][i] = round_to_dtype(a->k[i], a->dtype);
+            pv[0][i] = round_to_dtype(a->v[i], a->dtype);
+        }
+    }
+
+    /* combination: dm^l and dw */
+    for (int b = 0; b < B; ++b)
+        for (int y = 0; y < H; ++y)
+            for (int x = 0; x < W; ++x)
+                for (int h = 0; h < NH; ++h) {
+                    const size_t i = (size_t)y * W + x;
+                    const float* go = ba->dout + ((size_t)b * Nl[0] + i) * C + (size_t)h * d;
+                    for (int l = 0; l < L; ++l) {
+                        const size_t anc = (size_t)(y >> l) * Wl[l] + (size_t)(x >> l);
+                        const size_t widx = (((size_t)b * Nl[0] + i) * NH + h) * L + l;
+                        double wl = 1.0;
+                        if (isB) wl = a->w ? (double)a->w[widx] : 1.0 / L;
+                        double* g = dm[l] + (((size_t)b * Nl[l] + anc) * NH + h) * d;
+                        const double* m = msg[l] + (((size_t)b * Nl[l] + anc) * NH + h) * d;
+                        double dot = 0.0;
+                        for (int c = 0; c < d; ++c) {
+                            g[c] += wl * (double)go[c];
+                            dot += (double)go[c] * m[c];
+                        }
+                        if (isB && a->w && ba->dw) ba->dw[widx] = dot;
+                    }
+                }
+
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < NH; ++h) {
+            /* ---- finer levels, finest first ---- */
+            for (int l = 0; l < Lc; ++l) {
+                const size_t N = Nl[l], Np = Nl[l + 1];
+                const int Hh = Hl[l], Ww = Wl[l], Wp = Wl[l + 1];
+                const int Kp = Kl[l + 1];
+                const int ncand = 4 * Kp;
+                for (int y = 0; y < Hh; ++y)
+                    for (int x = 0; x < Ww; ++x) {
+                        const size_t i = (size_t)y * Ww + x;
+                        const size_t P = (size_t)(y >> 1) * Wp + (size_t)(x >> 1);
+                        const size_t prow = ((size_t)b * NH + h) * Np + P;
+                        const int32_t* psel = sel[l + 1] + prow * Kp;
+                        const double* pkey = key[l + 1] + prow * Kp;
+                        double* pdsig = dsig[l + 1] + prow * Kp;
+                        const float* qi = pq[l] + ((size_t)b * N + i) * C + (size_t)h * d;
+                        const double* gm = dm[l] + (((size_t)b * N + i) * NH + h) * d;
+                        /* candidates as in the forward: slot 4r+c is child c of kept key r */
+                        for (int r = 0; r < Kp; ++r)
+                            for (int c = 0; c < 4; ++c) {
+                                const int s = 4 * r + c;
+                                cv[s] = 0;
+                                ci[s] = -1;
+                                kpos[s] = -1;
+                                const int J = psel[r];
+                                if (J < 0) continue;
+                                const int cy = 2 * (J / Wp) + (c >> 1), cxx = 2 * (J % Wp) + (c & 1);
+                                if (cy >= Hh || cxx >= Ww) continue;
+                                cv[s] = 1;
+                                ci[s] = cy * Ww + cxx;
+                                cx[s] = tau * dot_head(qi, pk[l] + ((size_t)b * N + ci[s]) * C + (size_t)h * d, d);
+                            }
+                        /* the keys this query keeps (A: their score gradients come from level l-1) */
+                        if (l >= 1) {
+                            const int32_t* srow = sel[l] + (((size_t)b * NH + h) * N + i) * Kl[l];
+                            for (int r = 0; r < Kl[l]; ++r) {
+                                if (srow[r] < 0) continue;
+                                for (int s = 0; s < ncand; ++s)
+                                    if (cv[s] && ci[s] == srow[r]) kpos[s] = r;
+                            }
+                        }
+                        /* forward weights */
+                        if (isB) {
+                            double mx = -INFINITY, den = 0.0;
+                            for (int s = 0; s < ncand; ++s) if (cv[s] && cx[s] > mx) mx = cx[s];
+                            for (int s = 0; s < ncand; ++s) if (cv[s]) { cp[s] = exp(cx[s] - mx); den += cp[s]; }
+                            for (int s = 0; s < ncand; ++s) if (cv[s]) cp[s] /= den;
+                        } else {
+                            for (int r = 0; r < Kp; ++r) {
+                                double mx = -INFINITY, den = 0.0;
+                                for (int c = 0; c < 4; ++c) { const int s = 4 * r + c; if (cv[s] && cx[s] > mx) mx = cx[s]; }
+                                for (int c = 0; c < 4; ++c) { const int s = 4 * r + c; if (cv[s]) { cp[s] = exp(cx[s] - mx); den += cp[s]; } }
+                                for (int c = 0; c < 4; ++c) { const int s = 4 * r + c; if (cv[s]) { cp[s] /= den; cs[s] = pkey[r] * cp[s]; } }
+                            }
+                        }
+                        /* gradient of each weight, and the values' gradients */
+                        for (int s = 0; s < ncand; ++s) {
+                            if (!cv[s]) continue;
+                            const float* vj = pv[l] + ((size_t)b * N + ci[s]) * C + (size_t)h * d;
+                            double* dvj = dV[l] + ((size_t)b * N + ci[s]) * C + (size_t)h * d;
+                            const int in_omega = isB || l == 0 || kpos[s] < 0;
+                            if (in_omega) {
+                                double g = 0.0;
+                                for (int c = 0; c < d; ++c) g += gm[c] * (double)vj[c];
+                                cg[s] = g;
+                                const double wgt = isB ? cp[s] : cs[s];
+                                for (int c = 0; c < d; ++c) dvj[c] += wgt * gm[c];
+                            } else {
+                                cg[s] = dsig[l][(((size_t)b * NH + h) * N + i) * Kl[l] + kpos[s]];
+                            }
+                        }
+                        /* logit gradients */
+                        if (isB) {
+                            double D = 0.0;
+                            for (int s = 0; s < ncand; ++s) if (cv[s]) D += cp[s] * cg[s];
+                            for (int s = 0; s < ncand; ++s) if (cv[s]) cd[s] = cp[s] * (cg[s] - D);
+                        } else {
+                            for (int r = 0; r < Kp; ++r) {
+                                double dsr = 0.0, D = 0.0;
+                                for (int c = 0; c < 4; ++c) {
+                                    const int s = 4 * r + c;
+                                    if (!cv[s]) continue;
+                                    dsr += cp[s] * cg[s];            /* d sigma_r */
+                                    D += cp[s] * (pkey[r] * cg[s]);  /* sum t dt */
+                                }
+                                if (psel[r] >= 0) pdsig[r] += dsr;
+                                for (int c = 0; c < 4; ++c) {
+                                    const int s = 4 * r + c;
+                                    if (cv[s]) cd[s] = cp[s] * (pkey[r] * cg[s] - D);
+                                }
+                            }
+                        }
+                        /* through the logits */
+                        double* dqi = dQ[l] + ((size_t)b * N + i) * C + (size_t)h * d;
+                        for (int s = 0; s < ncand; ++s) {
+                            if (!cv[s]) continue;
+                            const float* kj = pk[l] + ((size_t)b * N + ci[s]) * C + (size_t)h * d;
+                            double* dkj = dK[l] + ((size_t)b * N + ci[s]) * C + (size_t)h * d;
+                            for (int c = 0; c < d; ++c) {
+                                dqi[c] += tau * cd[s] * (double)kj[c];
+                                dkj[c] += tau * cd[s] * (double)qi[c];
+                            }
+                        }
+                    }
+            }
+
+            /* ---- coarsest level: every key (Eq. 1) ---- */
+            {
+                const int l = Lc;
+                const size_t N = Nl[l];
+                for (size_t i = 0; i < N; ++i) {
+                    const float* qi = pq[l] + ((size_t)b * N + i) * C + (size_t)h * d;
+                    const double* gm = dm[l] + (((size_t)b * N + i) * NH + h) * d;
+                    double mx = -INFINITY, den = 0.0;
+                    for (size_t j = 0; j < N; ++j) {
+                        cx[j] = tau * dot_head(qi, pk[l] + ((size_t)b * N + j) * C + (size_t)h * d, d);
+                        if (cx[j] > mx) mx = cx[j];
+                        kpos[j] = -1;
+                    }
+                    for (size_t j = 0; j < N; ++j) { cp[j] = exp(cx[j] - mx); den += cp[j]; }
+                    for (size_t j = 0; j < N; ++j) cp[j] /= den;
+                    if (L > 1 && !isB) {
+                        const int32_t* srow = sel[l] + (((size_t)b * NH + h) * N + i) * Kl[l];
+                        for (int r = 0; r < Kl[l]; ++r)
+                            if (srow[r] >= 0) kpos[srow[r]] = r;
+                    }
+                    double D = 0.0;
+                    for (size_t j = 0; j < N; ++j) {
+                        const float* vj = pv[l] + ((size_t)b * N + j) * C + (size_t)h * d;
+                        double* dvj = dV[l] + ((size_t)b * N + j) * C + (size_t)h * d;
+                        if (kpos[j] < 0) {
+                            double g = 0.0;
+                            for (int c = 0; c < d; ++c) g += gm[c] * (double)vj[c];
+                            cg[j] = g;
+                            for (int c = 0; c < d; ++c) dvj[c] += cp[j] * gm[c];
+                        } else {
+                            cg[j] = dsig[l][(((size_t)b * NH + h) * N + i) * Kl[l] + kpos[j]];
+                        }
+                        D += cp[j] * cg[j];
+                    }
+                    double* dqi = dQ[l] + ((size_t)b * N + i) * C + (size_t)h * d;
+                    for (size_t j = 0; j < N; ++j) {
+                        const double dl = cp[j] * (cg[j] - D);
+                        const float* kj = pk[l] + ((size_t)b * N + j) * C + (size_t)h * d;
+                        double* dkj = dK[l] + ((size_t)b * N + j) * C + (size_t)h * d;
+                        for (int c = 0; c < d; ++c) {
+                            dqi[c] += tau * dl * (double)kj[c];
+                            dkj[c] += tau * dl * (double)qi[c];
+                        }
+                    }
+                }
+            }
+        }
+
+    /* pyramid: each pooled token hands 1/n of its gradient to each of its n valid children */
+    for (int l = Lc; l >= 1; --l) {
+        const int Hs = Hl[l - 1], Ws = Wl[l - 1];
+        for (int b = 0; b < B; ++b)
+            for (int y = 0; y < Hl[l]; ++y)
+                for (int x = 0; x < Wl[l]; ++x) {
+                    const int ny = (2 * y + 1 < Hs) ? 2 : 1, nx = (2 * x + 1 < Ws) ? 2 : 1;
+                    const double inv_n = 1.0 / (double)(ny * nx);
+                    const size_t src = ((size_t)b * Nl[l] + (size_t)y * Wl[l] + x) * C;
+                    for (int cy = 0; cy < ny; ++cy)
+                        for (int cxx = 0; cxx < nx; ++cxx) {
+                            const size_t dst = ((size_t)b * Nl[l - 1] + (size_t)(2 * y + cy) * Ws + (2 * x + cxx)) * C;
+                            for (int c = 0; c < C; ++c) {
+                                dQ[l - 1][dst + c] += dQ[l][src + c] * inv_n;
+                                dK[l - 1][dst + c] += dK[l][src + c] * inv_n;
+                                dV[l - 1][dst + c] += dV[l][src + c] * inv_n;
+                            }
+                        }
+                }
+    }
+    memcpy(ba->dq, dQ[0], sizeof(double) * (size_t)B * Nl[0] * C);
+    memcpy(ba->dk, dK[0], sizeof(double) * (size_t)B * Nl[0] * C);
+    memcpy(ba->dv, dV[0], sizeof(double) * (size_t)B * Nl[0] * C);
+
+done:
+    for (int l = 0; l < QO_MAX_LEVELS; ++l) {
+        free(pq[l]); free(pk[l]); free(pv[l]); free(msg[l]); free(sel[l]); free(key[l]);
+        free(dm[l]); free(dQ[l]); free(dK[l]); free(dV[l]); free(dsig[l]);
+    }
+    free(cx); free(cp); free(cs); free(cg); free(cd); free(ci); free(cv); free(kpos);
+    return rc;
+}

@@ -50,6 +50,14 @@ class _Args(ctypes.Structure):
     ]
 
 
+class _BwdArgs(ctypes.Structure):
+    _fields_ = [
+        ("fwd", _Args),
+        ("dout", ctypes.c_void_p),
+        ("dq", ctypes.c_void_p), ("dk", ctypes.c_void_p), ("dv", ctypes.c_void_p), ("dw", ctypes.c_void_p),
+    ]
+
+
 _lib = None
 
 
@@ -61,6 +69,8 @@ def _load():
         lib = ctypes.CDLL(_LIB_PATH)
         lib.qo_forward.argtypes = [ctypes.POINTER(_Args)]
         lib.qo_forward.restype = ctypes.c_int
+        lib.qo_backward.argtypes = [ctypes.POINTER(_BwdArgs)]
+        lib.qo_backward.restype = ctypes.c_int
         lib.qo_pool_level.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                       ctypes.c_int, ctypes.c_void_p]
         lib.qo_pool_level.restype = ctypes.c_int
@@ -208,3 +218,59 @@ def forward(q, k, v, *, levels: int, K, variant: str, dtype: str = "f32", w=None
     if want_pyramids:
         res["pyr_q"], res["pyr_k"], res["pyr_v"] = pyr["q"], pyr["k"], pyr["v"]
     return res
+
+
+def backward(q, k, v, dout, *, levels: int, K, variant: str, dtype: str = "f32", w=None, scale=None,
+             forced=None) -> dict:
+    """Gradients of ``sum(dout * out)`` with the kept-key sets held fixed (the oracle's own, or
+    ``forced`` as in ``forward``). ``dout``: float32 ``[B, H, W, heads, d]``. Returns float64
+    ``dq``, ``dk``, ``dv`` ``[B, H, W, heads, d]`` and, for QuadTree-B with ``w`` given, ``dw``
+    ``[B, H*W, heads, levels]`` (else None)."""
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    k = np.ascontiguousarray(k, dtype=np.float32)
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    g = np.ascontiguousarray(dout, dtype=np.float32)
+    B, H, W, NH, d = q.shape
+    assert k.shape == q.shape and v.shape == q.shape and g.shape == q.shape
+    L = levels
+    dims = level_dims(H, W, L)
+    N = [h * w_ for h, w_ in dims]
+    if np.ndim(K) == 0:
+        Kl = [int(K)] * L
+    else:
+        Kl = [int(x) for x in K]
+        assert len(Kl) == L, "one K per level (entry 0 ignored)"
+        Kl[0] = Kl[1] if L > 1 else max(Kl[0], 1)
+    K_tbl = (ctypes.c_int * MAX_LEVELS)(*Kl)
+    wts = None
+    if w is not None:
+        wts = np.ascontiguousarray(w, dtype=np.float32)
+        assert wts.shape == (B, H * W, NH, L), wts.shape
+    forced_arrays = None
+    if forced is not None:
+        forced_arrays = [None] * L
+        for l in range(1, L):
+            if forced[l] is not None:
+                f = np.ascontiguousarray(forced[l], dtype=np.int32)
+                assert f.shape == (B, NH, N[l], Kl[l]), (f.shape, (B, NH, N[l], Kl[l]))
+                forced_arrays[l] = f
+        forced_tbl = _ptr_table(forced_arrays)
+    dq, dk, dv = (np.zeros((B, H, W, NH, d), np.float64) for _ in range(3))
+    dw = np.zeros((B, H * W, NH, L), np.float64) if (variant == "B" and wts is not None) else None
+    args = _BwdArgs()
+    f = args.fwd
+    f.q, f.k, f.v = q.ctypes.data, k.ctypes.data, v.ctypes.data
+    f.w = wts.ctypes.data if wts is not None else None
+    f.B, f.heads, f.H, f.W, f.d = B, NH, H, W, d
+    f.L, f.K, f.variant, f.dtype = L, Kl[1] if L > 1 else Kl[0], VARIANTS[variant], DTYPES[dtype]
+    f.K_levels = ctypes.addressof(K_tbl)
+    f.scale = float(scale) if scale is not None else 0.0
+    if forced_arrays is not None:
+        f.forced = ctypes.addressof(forced_tbl)
+    args.dout = g.ctypes.data
+    args.dq, args.dk, args.dv = dq.ctypes.data, dk.ctypes.data, dv.ctypes.data
+    args.dw = dw.ctypes.data if dw is not None else None
+    rc = _load().qo_backward(ctypes.byref(args))
+    if rc != 0:
+        raise RuntimeError(f"oracle backward failed with code {rc}")
+    return {"dq": dq, "dk": dk, "dv": dv, "dw": dw}
