@@ -166,6 +166,35 @@ qta_status qta_forward_ex(const void* q, const void* k, const void* v, const flo
                           size_t workspace_bytes, void* stream);
 
 /*
+ * qta_backward_ex - gradients of the layer for training (the paper trains every model with it,
+ * Sec. 4): given dout = dLoss/dout, the gradients of q, k, v and, for QuadTree-B with w, of w. The
+ * kept-key sets are those the forward chose and are held fixed: top-K is a selection and has no
+ * gradient; everything computed from the kept keys is differentiated, including QuadTree-A's
+ * scores s = s_parent * t (Eq. 4), whose gradient flows back to the level that produced
+ * s_parent. Pyramid levels are means of their valid children, so each child receives 1/n of a
+ * pooled token's gradient (the rounding of pooled values to the storage type is taken as exact).
+ *   q, k, v, w   the forward's inputs, unchanged since qta_forward_ex.
+ *   workspace    the workspace that qta_forward_ex filled for these inputs and options, unchanged
+ *                (read only: pyramids, messages, kept keys and their scores).
+ *   dout         [B][H][W][heads][d] dtype.
+ *   dq, dk, dv   fp32 [B][H][W][heads][d], overwritten.
+ *   dw           fp32 [B][H*W][heads][levels], overwritten for QuadTree-B when w is given (NULL:
+ *                not computed); not touched otherwise.
+ *   bwd_workspace  device memory of qta_backward_workspace_bytes_ex bytes, 256-byte aligned; its
+ *                contents need not be preserved between calls.
+ * Unsupported (QTA_ERR_UNSUPPORTED): caller-supplied V levels, the position encoding, and K_l with
+ * 4*K_l > 64 at any level. The gradients of k and v (and internal sums) are accumulated with fp32
+ * atomics, so their last bits may vary between runs. Options as in qta_forward_ex.
+ */
+size_t qta_backward_workspace_bytes_ex(int B, int heads, int H, int W, int d, int levels, int K,
+                                       qta_variant variant, qta_dtype dtype, const qta_options* opt);
+qta_status qta_backward_ex(const void* q, const void* k, const void* v, const float* w, const void* dout,
+                           int B, int heads, int H, int W, int d, int levels, int K, qta_variant variant,
+                           qta_dtype dtype, float scale, const qta_options* opt, const void* workspace,
+                           size_t workspace_bytes, float* dq, float* dk, float* dv, float* dw,
+                           void* bwd_workspace, size_t bwd_workspace_bytes, void* stream);
+
+/*
  * qta_build_pyramid - step 1: levels 1..levels-1 of one token map by 2x2 average pooling
  * (Sec. 3.2). Each level is pooled from the stored level below it: the valid children are summed
  * in fp32 as ((c00 + c01) + (c10 + c11)), missing children left out, multiplied by 1/count and

@@ -192,6 +192,58 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], in
     return hipSuccess;
 }
 
+// Workspace of the backward pass: per level l >= 1 the gradient of the message (dm) and the
+// level's q, k, v gradients (fp32 [B][N_l][C]); QuadTree-A's gradients of the kept scores
+// ([B][heads][N_l][K_l]); the coarse softmax statistics ([B][heads][N_c][4]). The buffers that
+// are accumulated with atomics (dm at levels >= 2, the k and v gradients of levels 1..L-2) form
+// one contiguous region, cleared at the start of every call.
+struct BwdLayout {
+    size_t dm[QTA_MAX_LEVELS], gq[QTA_MAX_LEVELS], gk[QTA_MAX_LEVELS], gv[QTA_MAX_LEVELS];
+    size_t dsig[QTA_MAX_LEVELS];
+    size_t zero_begin, zero_end;
+    size_t stats, total;
+};
+
+void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int levels, const int* Kl, bool va,
+                BwdLayout* L)
+{
+    *L = BwdLayout{};
+    const int c = levels - 1;
+    auto fbytes = [&](int l) { return static_cast<size_t>(B) * Hl[l] * Wl[l] * C * sizeof(float); };
+    size_t off = 0;
+    L->zero_begin = off;
+    for (int l = 2; l <= c; ++l) {
+        L->dm[l] = off;
+        off = align_up(off + fbytes(l));
+    }
+    for (int l = 1; l < c; ++l) {
+        L->gk[l] = off;
+        off = align_up(off + fbytes(l));
+        L->gv[l] = off;
+        off = align_up(off + fbytes(l));
+    }
+    L->zero_end = off;
+    if (c >= 1) {
+        L->dm[1] = off;
+        off = align_up(off + fbytes(1));
+        L->gk[c] = off;
+        off = align_up(off + fbytes(c));
+        L->gv[c] = off;
+        off = align_up(off + fbytes(c));
+    }
+    for (int l = 1; l <= c; ++l) {
+        L->gq[l] = off;
+        off = align_up(off + fbytes(l));
+        if (va) {
+            L->dsig[l] = off;
+            off = align_up(off + static_cast<size_t>(B) * heads * Hl[l] * Wl[l] * Kl[l] * sizeof(float));
+        }
+    }
+    L->stats = off;
+    off = align_up(off + static_cast<size_t>(B) * heads * Hl[c] * Wl[c] * 4 * sizeof(float));
+    L->total = off;
+}
+
 }  // namespace
 
 extern "C" {
@@ -587,6 +639,201 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
 {
     return qta_forward_ex(q, k, v, w, B, heads, H, W, d, levels, K, variant, dtype, scale, nullptr, out, workspace,
                           workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+extern "C" {
+
+size_t qta_backward_workspace_bytes_ex(int B, int heads, int H, int W, int d, int levels, int K, qta_variant variant,
+                                       qta_dtype dtype, const qta_options* opt)
+{
+    if (rows_as_maps(opt, &B, &H) != QTA_OK) return 0;
+    if (!variant_ok(variant)) return 0;
+    Options o;
+    if (read_options(K, levels, opt, &o) != QTA_OK) return 0;
+    qta_workspace_layout L;
+    if (layout(B, heads, H, W, d, levels, o.Kl, o.v_levels != nullptr, o.pe_weight != nullptr, dtype, &L) != QTA_OK)
+        return 0;
+    BwdLayout G;
+    bwd_layout(B, heads, L.H, L.W, heads * d, levels, o.Kl, variant == QTA_VARIANT_A, &G);
+    return G.total;
+}
+
+qta_status qta_backward_ex(const void* q, const void* k, const void* v, const float* w, const void* dout, int B,
+                           int heads, int H, int W, int d, int levels, int K, qta_variant variant, qta_dtype dtype,
+                           float scale, const qta_options* opt, const void* workspace, size_t workspace_bytes,
+                           float* dq, float* dk, float* dv, float* dw, void* bwd_workspace,
+                           size_t bwd_workspace_bytes, void* stream)
+{
+    qta_status st = check_problem(B, heads, d, 1, variant, dtype);
+    if (st != QTA_OK) return st;
+    if (!q || !k || !v || !dout || !dq || !dk || !dv) return QTA_ERR_INVALID;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(dq) || !aligned16(dk) ||
+        !aligned16(dv))
+        return QTA_ERR_INVALID;
+    st = rows_as_maps(opt, &B, &H);
+    if (st != QTA_OK) return st;
+    Options o;
+    st = read_options(K, levels, opt, &o);
+    if (st != QTA_OK) return st;
+    if (o.v_levels || o.pe_weight) return QTA_ERR_UNSUPPORTED;
+    qta_workspace_layout L;
+    st = layout(B, heads, H, W, d, levels, o.Kl, false, false, dtype, &L);
+    if (st != QTA_OK) return st;
+    const int* Kl = o.Kl;
+    for (int l = 1; l < levels; ++l)
+        if (4 * Kl[l] > 64) return QTA_ERR_UNSUPPORTED;
+    if (levels > 1) {
+        if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return QTA_ERR_INVALID;
+        if (workspace_bytes < L.total) return QTA_ERR_WORKSPACE;
+    }
+    const bool va = variant == QTA_VARIANT_A;
+    const int C = heads * d;
+    BwdLayout G;
+    bwd_layout(B, heads, L.H, L.W, C, levels, Kl, va, &G);
+    if (!bwd_workspace || (reinterpret_cast<uintptr_t>(bwd_workspace) & (kAlign - 1)) != 0) return QTA_ERR_INVALID;
+    if (bwd_workspace_bytes < G.total) return QTA_ERR_WORKSPACE;
+    float* dw_out = (!va && w) ? dw : nullptr;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool use_bf16 = dtype == QTA_BF16;
+    const float tau = resolve_scale(scale, d);
+    const char* ws = static_cast<const char*>(workspace);
+    char* gws = static_cast<char*>(bwd_workspace);
+    auto fptr = [&](size_t off) { return reinterpret_cast<float*>(gws + off); };
+    auto sidx = [&](int l) { return reinterpret_cast<const int32_t*>(ws + L.sel_idx[l]); };
+    auto skey = [&](int l) { return reinterpret_cast<const float*>(ws + L.sel_key[l]); };
+    const int c = levels - 1;
+
+    if (levels > 1) {
+        // clear what is accumulated: dm of levels >= 2, the k and v gradients of levels 0..L-2
+        FillRange r[3];
+        r[0] = FillRange{fptr(G.zero_begin), (G.zero_end - G.zero_begin) / sizeof(float)};
+        r[1] = FillRange{dk, static_cast<size_t>(B) * H * W * C};
+        r[2] = FillRange{dv, static_cast<size_t>(B) * H * W * C};
+        if (launch_fill_zero(r, 3, s) != hipSuccess) return QTA_ERR_HIP;
+
+        // 1. combination
+        BwdCombineArgs cb{};
+        cb.dout = dout;
+        cb.w = va ? nullptr : w;
+        cb.variant_b = va ? 0 : 1;
+        cb.B = B;
+        cb.heads = heads;
+        cb.d = d;
+        cb.C = C;
+        cb.L = levels;
+        for (int l = 0; l < levels; ++l) {
+            cb.H[l] = L.H[l];
+            cb.W[l] = L.W[l];
+            if (l >= 1) {
+                cb.msg[l] = reinterpret_cast<const float*>(ws + L.msg[l]);
+                cb.dm[l] = fptr(G.dm[l]);
+            }
+        }
+        cb.dw = dw_out;
+        if (launch_bwd_combine(cb, use_bf16, s) != hipSuccess) return QTA_ERR_HIP;
+
+        // 2. finer levels, finest first (QuadTree-A's score gradients go up one level each)
+        for (int l = 0; l < c; ++l) {
+            BwdLevelArgs a{};
+            if (l == 0) {
+                a.q = q;
+                a.k = k;
+                a.v = v;
+                a.blocked = false;
+                a.dout = dout;
+                a.w = va ? nullptr : w;
+                a.dq = dq;
+                a.dk = dk;
+                a.dv = dv;
+                a.dw = dw_out;
+            } else {
+                a.q = ws + L.q[l];
+                a.k = ws + L.k[l];
+                a.v = ws + L.v[l];
+                a.blocked = L.blocked[l] != 0;
+                a.sel_idx = sidx(l);
+                a.dsig_in = va ? fptr(G.dsig[l]) : nullptr;
+                a.dm = fptr(G.dm[l]);
+                a.dq = fptr(G.gq[l]);
+                a.dk = fptr(G.gk[l]);
+                a.dv = fptr(G.gv[l]);
+            }
+            a.B = B;
+            a.heads = heads;
+            a.H = L.H[l];
+            a.W = L.W[l];
+            a.Hp = L.H[l + 1];
+            a.Wp = L.W[l + 1];
+            a.C = C;
+            a.Kp = Kl[l + 1];
+            a.Ks = l >= 1 ? Kl[l] : 0;
+            a.scale = tau;
+            a.parent_idx = sidx(l + 1);
+            a.parent_key = skey(l + 1);
+            a.dsig_out = va ? fptr(G.dsig[l + 1]) : nullptr;
+            a.levels = levels;
+            if (launch_bwd_level(a, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
+        }
+    }
+
+    // 3. coarsest level
+    {
+        BwdCoarseArgs a{};
+        a.B = B;
+        a.heads = heads;
+        a.N = L.H[c] * L.W[c];
+        a.C = C;
+        a.scale = tau;
+        a.variant_b = va ? 0 : 1;
+        a.stats = fptr(G.stats);
+        if (levels == 1) {
+            a.q = q;
+            a.k = k;
+            a.v = v;
+            a.K = 0;
+            a.dout = dout;
+            a.w = va ? nullptr : w;
+            a.dq = dq;
+            a.dk = dk;
+            a.dv = dv;
+            a.dw = dw_out;
+        } else {
+            a.q = ws + L.q[c];
+            a.k = ws + L.k[c];
+            a.v = ws + L.v[c];
+            a.K = Kl[c];
+            a.sel_idx = sidx(c);
+            a.dsig = va ? fptr(G.dsig[c]) : nullptr;
+            a.dm = fptr(G.dm[c]);
+            a.dq = fptr(G.gq[c]);
+            a.dk = fptr(G.gk[c]);
+            a.dv = fptr(G.gv[c]);
+        }
+        if (launch_bwd_coarse(a, d, va, use_bf16, s) != hipSuccess) return QTA_ERR_HIP;
+    }
+    if (levels == 1) return QTA_OK;
+
+    // 4. pyramids
+    BwdUnpoolArgs u{};
+    u.B = B;
+    u.C = C;
+    u.L = levels;
+    for (int l = 0; l < levels; ++l) {
+        u.H[l] = L.H[l];
+        u.W[l] = L.W[l];
+        if (l >= 1) {
+            u.gq[l] = fptr(G.gq[l]);
+            u.gk[l] = fptr(G.gk[l]);
+            u.gv[l] = fptr(G.gv[l]);
+        }
+    }
+    u.dq = dq;
+    u.dk = dk;
+    u.dv = dv;
+    return launch_bwd_unpool(u, s) == hipSuccess ? QTA_OK : QTA_ERR_HIP;
 }
 
 }  // extern "C"

@@ -140,6 +140,86 @@ struct PosEncArgs {
     int B, heads, d;
 };
 
+// ---- backward pass (gradients with the kept-key sets held fixed) ----
+
+// dLoss/dm^l of every level l >= 1 from the upstream gradient: dm^l at a level-l token sums
+// w_{i,l} dout_i over its finest descendants i (w = 1 for QuadTree-A); and dw_{i,l} = <dout_i, m^l
+// of i's ancestor> for l >= 1. One thread per (batch, level-1 token, channel).
+struct BwdCombineArgs {
+    const void* dout;           // [B][N0][C] storage type
+    const float* w;             // QuadTree-B: [B][N0][heads][L] or NULL (1/L); NULL for A
+    int variant_b;
+    int B, heads, d, C, L;
+    int H[QTA_MAX_LEVELS], W[QTA_MAX_LEVELS];
+    const float* msg[QTA_MAX_LEVELS];   // forward messages of levels >= 1 (for dw)
+    float* dm[QTA_MAX_LEVELS];          // level 1 written, levels >= 2 accumulated (zeroed first)
+    float* dw;                          // QuadTree-B with w: entries l >= 1 written; or NULL
+};
+
+// Backward of one finer level l (0 <= l < L-1): one wave per (parent query at l+1, head).
+struct BwdLevelArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    bool blocked;               // q, k, v of this level parent-blocked (else NHWC)
+    int B, heads, H, W, Hp, Wp, C;
+    int Kp;                     // keys each parent kept (4*Kp candidate slots, at most 64)
+    int Ks;                     // keys this level keeps (l >= 1)
+    FastDiv div_Wp;
+    float scale;
+    const int32_t* parent_idx;  // [B][heads][Np][Kp]
+    const float* parent_key;    // QuadTree-A: the parents' scores sigma
+    const int32_t* sel_idx;     // QuadTree-A, l >= 1: this level's kept keys [B][heads][N][Ks]
+    const float* dsig_in;       // QuadTree-A, l >= 1: dLoss/d(score of each kept key) [B][heads][N][Ks]
+    float* dsig_out;            // QuadTree-A: dLoss/d(parent's kept-key scores) [B][heads][Np][Kp]
+    const float* dm;            // l >= 1: dLoss/dm^l fp32 [B][N][C]
+    const void* dout;           // l == 0: upstream gradient, storage type [B][N][C]
+    const float* w;             // l == 0, QuadTree-B: [B][N][heads][L] or NULL (1/L)
+    int levels;
+    float* dq;                  // fp32 [B][N][C], written
+    float* dk;                  // fp32 [B][N][C], accumulated with atomics
+    float* dv;
+    float* dw;                  // l == 0, QuadTree-B with w: entry 0 written; or NULL
+};
+
+// Backward of the coarsest level (Eq. 1 over all N keys), in two passes: per query (dq and the
+// softmax statistics) and per key (dk, dv), both without atomics.
+struct BwdCoarseArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    int B, heads, N, C, K;      // K: keys kept per coarse query (0 for a single level)
+    float scale;
+    const int32_t* sel_idx;     // QuadTree-A with levels > 1
+    const float* dsig;          // QuadTree-A with levels > 1: dLoss/d(kept scores)
+    const float* dm;            // levels > 1: dLoss/dm fp32 [B][N][C]
+    const void* dout;           // single level: upstream gradient (storage type)
+    const float* w;             // single level, QuadTree-B: [B][N][heads][1] or NULL
+    int variant_b;
+    float* stats;               // [B][heads][N][4]: row max, row sum, sum_j p_j ds_j
+    float* dq;                  // fp32 [B][N][C], written
+    float* dk;
+    float* dv;
+    float* dw;                  // single level, QuadTree-B with w
+};
+
+// Adds to the level-0 gradients every coarser level's, split evenly among valid children.
+struct BwdUnpoolArgs {
+    int B, C, L;
+    int H[QTA_MAX_LEVELS], W[QTA_MAX_LEVELS];
+    const float* gq[QTA_MAX_LEVELS];
+    const float* gk[QTA_MAX_LEVELS];
+    const float* gv[QTA_MAX_LEVELS];
+    float* dq;
+    float* dk;
+    float* dv;
+};
+
+struct FillRange {
+    float* p;
+    size_t n;                   // floats, a multiple of 4, p 16-byte aligned
+};
+
 struct TopkArgs {
     const float* keys;
     const int32_t* cand_idx;
@@ -170,5 +250,11 @@ hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool use_b
 hipError_t launch_fine_attn_wide(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
                                  hipStream_t stream);
 hipError_t launch_topk(const TopkArgs& a, hipStream_t stream);
+hipError_t launch_fill_zero(const FillRange* r, int n, hipStream_t stream);
+hipError_t launch_bwd_combine(const BwdCombineArgs& a, bool use_bf16, hipStream_t stream);
+hipError_t launch_bwd_level(const BwdLevelArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
+                            hipStream_t stream);
+hipError_t launch_bwd_coarse(const BwdCoarseArgs& a, int d, bool variant_a, bool use_bf16, hipStream_t stream);
+hipError_t launch_bwd_unpool(const BwdUnpoolArgs& a, hipStream_t stream);
 
 }  // namespace qta

@@ -27,7 +27,8 @@ not used):
              2 x 120 rows of 160 tokens is its own binary tree of 4 levels.
 
 Seeds: numpy PCG64 with seed = 1000 * config_number + tensor id (q=1, k=2, v=3, w=4, aux=5,
-10 + l for the given V level l, 20 and 21 for the position-encoding weights and biases).
+10 + l for the given V level l, 20 and 21 for the position-encoding weights and biases, 30 for the
+upstream gradient of the backward pass).
 All arrays are float32 ``[B, H, W, heads, d]``; for bf16 workloads the values are rounded to the
 nearest bfloat16 (ties to even), so they are exactly representable in bf16.
 """
@@ -178,3 +179,10 @@ def make_pe(wl: Workload, seed_offset: int = 0):
     wgt = (_rng(wl, 20, seed_offset).standard_normal((wl.levels, C, 3, 3)) * 0.3).astype(np.float32)
     bias = (_rng(wl, 21, seed_offset).standard_normal((wl.levels, C)) * 0.1).astype(np.float32)
     return wgt, bias
+
+
+def make_dout(wl: Workload, seed_offset: int = 0) -> np.ndarray:
+    """Upstream gradient of the layer output for the backward pass: N(0,1) float32
+    ``[B, H, W, heads, d]`` (rounded to bf16 for bf16 workloads)."""
+    g = _rng(wl, 30, seed_offset).standard_normal((wl.B, wl.H, wl.W, wl.heads, wl.d), dtype=np.float32)
+    return round_bf16(g) if wl.dtype == "bf16" else g

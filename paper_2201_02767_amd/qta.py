@@ -68,6 +68,9 @@ _SIGS = {
     "qta_workspace_bytes_ex": ([_I, _I, _I, _I, _I, _I, _I, _I, _P], ctypes.c_size_t),
     "qta_forward": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, ctypes.c_size_t, _P], _I),
     "qta_forward_ex": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, ctypes.c_size_t, _P], _I),
+    "qta_backward_workspace_bytes_ex": ([_I, _I, _I, _I, _I, _I, _I, _I, _I, _P], ctypes.c_size_t),
+    "qta_backward_ex": ([_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, ctypes.c_size_t,
+                         _P, _P, _P, _P, _P, ctypes.c_size_t, _P], _I),
     "qta_build_pyramid": ([_P, _P, _I, _I, _I, _I, _I, _I, _P], _I),
     "qta_coarse_attn": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P], _I),
     "qta_topk": ([_P, _P, _I, _I, _I, _P, _P, _P], _I),
@@ -311,6 +314,69 @@ class Plan:
             return keep
         return call
 
+    # ---- backward ----
+    def _bwd_buffers(self, want_dw):
+        if getattr(self, "_grads", None) is None:
+            opt = Options()
+            opt.K_levels = ctypes.addressof(self._k_tbl)
+            opt.epipolar = int(self.epipolar)
+            nbytes = lib().qta_backward_workspace_bytes_ex(
+                self.B, self.heads, self.H, self.W, self.d, self.levels,
+                self.K_levels[1] if self.levels > 1 else max(self.K_levels[0], 1), _VARIANTS[self.variant],
+                _DTYPES[self.dtype], ctypes.byref(opt))
+            if nbytes == 0:
+                raise ValueError("unsupported problem for the backward pass")
+            shape = (self.B, self.H, self.W, self.heads, self.d)
+            self.bwd_workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+            self._grads = [torch.empty(shape, dtype=torch.float32, device=self.device) for _ in range(3)]
+            self._dw = None
+        if want_dw and self._dw is None:
+            self._dw = torch.empty((self.B, self.H * self.W, self.heads, self.levels), dtype=torch.float32,
+                                   device=self.device)
+        return self._grads, (self._dw if want_dw else None)
+
+    def _bwd_args(self, q, k, v, w, dout, stream):
+        if self.v_supplied or self.pe:
+            raise ValueError("the backward pass covers pooled V levels without a position encoding")
+        self._args(q, k, v, w, None, None, None)
+        _require(dout, "dout", self.dtype, 5)
+        if tuple(dout.shape) != (self.B, self.H, self.W, self.heads, self.d):
+            raise ValueError(f"dout has shape {tuple(dout.shape)}")
+        want_dw = self.variant == "B" and w is not None
+        (dq, dk, dv), dw = self._bwd_buffers(want_dw)
+        opt = Options()
+        opt.K_levels = ctypes.addressof(self._k_tbl)
+        opt.epipolar = int(self.epipolar)
+        args = (_ptr(q), _ptr(k), _ptr(v), _ptr(w), _ptr(dout), self.B, self.heads, self.H, self.W, self.d,
+                self.levels, self.K_levels[1] if self.levels > 1 else max(self.K_levels[0], 1),
+                _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), ctypes.byref(opt),
+                _ptr(self.workspace), self.workspace.numel(), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dw),
+                _ptr(self.bwd_workspace), self.bwd_workspace.numel(), stream)
+        return args, opt, (dq, dk, dv, dw)
+
+    def backward(self, q, k, v, dout, w=None, stream=None):
+        """Gradients (dq, dk, dv, dw) in fp32 of the last ``run`` on the same inputs, for the upstream
+        gradient ``dout`` (the kept keys of that run held fixed). ``dw`` is None unless QuadTree-B
+        with ``w``. The returned tensors are the plan's own buffers, overwritten by the next call."""
+        s = _stream(self.device) if stream is None else ctypes.c_void_p(stream)
+        args, opt, grads = self._bwd_args(q, k, v, w, dout, s)
+        _check("qta_backward_ex", lib().qta_backward_ex(*args))
+        return grads
+
+    def prepare_backward(self, q, k, v, dout, w=None):
+        """Validate once and return a zero-argument callable that re-issues this backward on the
+        current stream."""
+        args, opt, grads = self._bwd_args(q, k, v, w, dout, _stream(self.device))
+        fn = lib().qta_backward_ex
+        keep = (q, k, v, w, dout, opt, grads)
+
+        def call():
+            st = fn(*args)
+            if st != 0:
+                _check("qta_backward_ex", st)
+            return keep
+        return call
+
     # views into the workspace after run()
     def _view(self, off, shape, dtype):
         n = 1
@@ -357,6 +423,41 @@ def forward(q, k, v, *, levels: int, K, variant: str, w=None, scale=None, v_leve
     plan = Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=q.dtype, device=q.device,
                 scale=scale, v_supplied=v_levels is not None, pe=pe_weight is not None, epipolar=epipolar)
     return plan.run(q, k, v, w, v_levels=v_levels, pe_weight=pe_weight, pe_bias=pe_bias)
+
+
+class _QuadTreeAttention(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, q, k, v, w, plan):
+        out = plan.run(q, k, v, w).clone()
+        ctx.plan = plan
+        if w is not None:
+            ctx.save_for_backward(q, k, v, w)
+        else:
+            ctx.save_for_backward(q, k, v)
+        return out
+
+    @staticmethod
+    def backward(ctx, dout):
+        saved = ctx.saved_tensors
+        q, k, v = saved[:3]
+        w = saved[3] if len(saved) > 3 else None
+        dq, dk, dv, dw = ctx.plan.backward(q, k, v, dout.to(q.dtype).contiguous(), w)
+        cast = lambda t: None if t is None else t.to(q.dtype)
+        return cast(dq), cast(dk), cast(dv), (dw.clone() if dw is not None else None), None
+
+
+def attention(q, k, v, *, levels: int, K, variant: str, w=None, scale=None, epipolar: bool = False,
+              plan: "Plan | None" = None) -> torch.Tensor:
+    """Differentiable QuadTree attention (autograd): the forward of ``forward`` and, on backward,
+    the gradients of q, k, v (in q's dtype) and w (fp32) from ``qta_backward_ex``, with the kept keys
+    of the forward held fixed. Pass a ``plan`` to reuse its buffers; a plan's workspace holds one
+    forward at a time, so a plan must not be shared by two layers awaiting their backward."""
+    _require(q, "q", None, 5)
+    B, H, W, heads, d = q.shape
+    if plan is None:
+        plan = Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=q.dtype, device=q.device,
+                    scale=scale, epipolar=epipolar)
+    return _QuadTreeAttention.apply(q, k, v, w, plan)
 
 
 # ------------------------------------------------------------------------------------------------

@@ -271,3 +271,33 @@ def test_epipolar_row_count_limit():
     """B*H rows must fit the map count; a count past 2^31 - 1 is rejected, not wrapped."""
     with pytest.raises(P.QtaError):
         P.workspace_layout(1 << 16, 1, 1 << 16, 8, 32, 2, 4, torch.float32, epipolar=True)
+
+
+def test_backward_validation():
+    """qta_backward_ex rejects before any launch: what it does not cover, missing pointers, small
+    workspaces."""
+    lib = P.lib()
+
+    def bwd(L=3, K=4, Kl=None, vtbl=None, pw=None, dout=FAKE, wsb=1 << 40, gwsb=1 << 40, variant=VA):
+        opt = P.qta.Options()
+        opt.K_levels = Kl
+        opt.v_levels = vtbl
+        opt.pe_weight = pw
+        return lib.qta_backward_ex(FAKE, FAKE, FAKE, None, dout, 1, 1, 16, 16, 32, L, K, variant, F32, 0.0,
+                                   ctypes.byref(opt), FAKE, wsb, FAKE, FAKE, FAKE, None, FAKE, gwsb, None)
+    assert bwd(dout=None) == INVALID
+    assert bwd(dout=FAKE + 4) == INVALID                                    # not 16-byte aligned
+    assert bwd(K=17) == UNSUPPORTED                                         # 68 candidates per group
+    assert bwd(Kl=ctypes.addressof(_klv(0, 4, 20))) == UNSUPPORTED
+    vt = (ctypes.c_void_p * 16)()
+    vt[1] = vt[2] = FAKE
+    assert bwd(vtbl=ctypes.addressof(vt)) == UNSUPPORTED                    # given V levels
+    assert bwd(pw=FAKE) == UNSUPPORTED                                      # position encoding
+    assert bwd(wsb=0) == WORKSPACE                                          # the forward's workspace
+    assert bwd(gwsb=0) == WORKSPACE
+    assert bwd(L=1, gwsb=0) == WORKSPACE                                    # one level still needs statistics
+    need_a = lib.qta_backward_workspace_bytes_ex(1, 1, 16, 16, 32, 3, 4, VA, F32, None)
+    need_b = lib.qta_backward_workspace_bytes_ex(1, 1, 16, 16, 32, 3, 4, VB, F32, None)
+    assert need_a > need_b > 0                                              # A adds the score gradients
+    assert bwd(gwsb=need_a - 1) == WORKSPACE
+    assert lib.qta_backward_workspace_bytes_ex(1, 1, 16, 16, 32, 3, 4, 7, F32, None) == 0

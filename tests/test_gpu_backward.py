@@ -1,0 +1,159 @@
+"""GPU parity of the backward pass (gradients of q, k, v and w with the kept keys held fixed)
+against the CPU oracle's backward, teacher-forced with the GPU forward's selections.
+
+Error measure per gradient tensor: max |gpu - oracle| / max |oracle|. Every gradient is computed in
+fp32 from inputs that are exact in the storage type (bf16 inputs are bf16 values), with sums of at
+most a few thousand terms (the coarse level's 1024 keys), so 1e-4 leaves an order of magnitude over
+fp32 accumulation; the same bound holds for bf16 inputs because nothing is rounded to bf16 on the
+way. The one exception is dw at levels >= 1: dw_{i,l} = <dout_i, m^l> uses the forward's stored
+messages, which for bf16 inputs carry the forward's bf16 rounding of the attention weights, so dw is
+held to the forward's message tolerance.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2201_02767_amd as P
+from paper_2201_02767_amd.inputs import WORKLOADS, make_dout, make_level_weights, make_qkv, round_bf16
+from oracle import oracle as O
+from tests.parity import TOL, to_np
+
+pytestmark = pytest.mark.gpu
+
+TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
+TOL_GRAD = 1e-4
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    P.lib()
+    return torch.device("cuda:0")
+
+
+def announce(msg: str) -> None:
+    print(f"[gpu case] {msg}", file=sys.stderr, flush=True)
+
+
+def dev_t(x, dtype, dev):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dev).to(TDT[dtype])
+
+
+def rand(seed, shape, dtype):
+    x = np.random.default_rng(seed).standard_normal(shape).astype(np.float32)
+    return round_bf16(x) if dtype == "bf16" else x
+
+
+def grad_err(g, r):
+    return float(np.abs(g - r).max() / max(np.abs(r).max(), 1e-30))
+
+
+def run_backward(dev, q, k, v, g, *, levels, K, variant, dtype, w=None, scale=None, epipolar=False, label=""):
+    B, H, W, heads, d = q.shape
+    announce(f"backward {label} B={B} H={H} W={W} heads={heads} d={d} L={levels} K={K} {variant} {dtype}"
+             f"{' epipolar' if epipolar else ''}")
+    plan = P.Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=TDT[dtype], device=dev, scale=scale,
+                  epipolar=epipolar)
+    tq, tk, tv, tg = (dev_t(x, dtype, dev) for x in (q, k, v, g))
+    tw = None if w is None else torch.from_numpy(w).to(dev)
+    plan.run(tq, tk, tv, tw)
+    dq, dk, dv, dw = plan.backward(tq, tk, tv, tg, tw)
+    torch.cuda.synchronize()
+    sel = [None] + [to_np(plan.selection(l)[0]) for l in range(1, levels)]
+    if epipolar:
+        q, k, v, g = (x.reshape(B * H, 1, W, heads, d) for x in (q, k, v, g))
+        w = None if w is None else w.reshape(B * H, W, heads, levels)
+    ref = O.backward(q, k, v, g, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale, forced=sel)
+    errs = {}
+    for name, t in (("dq", dq), ("dk", dk), ("dv", dv), ("dw", dw)):
+        if ref[name] is None:
+            assert t is None
+            continue
+        errs[name] = grad_err(to_np(t).reshape(ref[name].shape), ref[name])
+    announce(f"  gradient errors {errs}")
+    for name, e in errs.items():
+        assert e <= (TOL[dtype] if name == "dw" else TOL_GRAD), f"{name} error {e}"
+    return plan, (dq, dk, dv, dw), errs
+
+
+@pytest.mark.parametrize("variant,dtype,B,H,W,heads,d,L,K,with_w", [
+    ("A", "f32", 1, 16, 16, 1, 32, 3, 4, False),        # the tiny workload's shape
+    ("B", "f32", 1, 16, 16, 1, 32, 3, 4, True),
+    ("B", "f32", 2, 13, 11, 2, 32, 3, 3, False),       # ragged maps, w = 1/L
+    ("A", "bf16", 2, 25, 19, 2, 32, 4, 4, False),      # ragged over four levels
+    ("B", "bf16", 1, 31, 22, 3, 64, 3, 8, True),       # d = 64, odd head count
+    ("A", "f32", 1, 20, 24, 2, 64, 3, 16, False),      # 64 candidates per sibling group
+    ("B", "bf16", 1, 9, 7, 1, 32, 2, 2, True),         # two levels: the finest parents are coarse
+    ("A", "f32", 2, 7, 9, 2, 32, 1, 4, False),         # one level: dense attention
+    ("B", "bf16", 1, 5, 40, 2, 32, 1, 4, True),
+    ("B", "f32", 1, 40, 41, 1, 32, 2, 4, True),        # 420 coarse tokens: 7 key chunks per lane
+    ("A", "bf16", 1, 27, 33, 2, 32, 3, [0, 2, 16], False),   # K schedule, blocked level 1
+    ("B", "f32", 1, 33, 29, 2, 32, 4, [0, 8, 4, 2], True),
+])
+def test_backward_matches_oracle(dev, variant, dtype, B, H, W, heads, d, L, K, with_w):
+    seed = 300 + H * W + L
+    q, k, v, g = (rand(seed + i, (B, H, W, heads, d), dtype) for i in range(4))
+    w = np.random.default_rng(seed).random((B, H * W, heads, L)).astype(np.float32) if with_w else None
+    run_backward(dev, q, k, v, g, levels=L, K=K, variant=variant, dtype=dtype, w=w, label="case")
+
+
+@pytest.mark.parametrize("variant,dtype", [("A", "bf16"), ("B", "f32")])
+def test_backward_epipolar(dev, variant, dtype):
+    q, k, v, g = (rand(400 + i, (2, 5, 37, 2, 32), dtype) for i in range(4))
+    w = np.random.default_rng(4).random((2, 5 * 37, 2, 4)).astype(np.float32) if variant == "B" else None
+    run_backward(dev, q, k, v, g, levels=4, K=3, variant=variant, dtype=dtype, w=w, epipolar=True, label="rows")
+
+
+@pytest.mark.parametrize("name", ["tiny", "matching", "matching_ksched", "stereo", "backbone", "highres",
+                                  "stereo_epipolar"])
+def test_backward_workload_full_size(dev, name):
+    wl = WORKLOADS[name]
+    q, k, v = make_qkv(wl)
+    g = make_dout(wl)
+    w = make_level_weights(wl) if wl.variant == "B" else None
+    run_backward(dev, q, k, v, g, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w,
+                 epipolar=wl.epipolar, label=name)
+
+
+def test_backward_repeated_calls(dev):
+    """Repeated calls agree: dw has one writer per element (identical bits); dk, dv and the
+    messages' gradients at levels >= 2 (hence dq too) are summed with atomics, so only the order of
+    their additions may change."""
+    wl = WORKLOADS["matching"]
+    announce("backward repeated calls, matching")
+    q, k, v = (dev_t(x, "f32", dev) for x in make_qkv(wl))
+    g = dev_t(make_dout(wl), "f32", dev)
+    w = torch.from_numpy(make_level_weights(wl)).to(dev)
+    plan = P.Plan(wl.B, wl.H, wl.W, wl.heads, wl.d, levels=wl.levels, K=wl.K, variant="B", dtype=torch.float32,
+                  device=dev)
+    plan.run(q, k, v, w)
+    first = [t.clone() for t in plan.backward(q, k, v, g, w)]
+    for _ in range(2):
+        again = plan.backward(q, k, v, g, w)
+        torch.cuda.synchronize()
+        assert torch.equal(again[3], first[3])
+        for a, b in zip(again[:3], first[:3]):
+            assert grad_err(to_np(a), to_np(b)) <= 1e-6
+
+
+def test_autograd_function(dev):
+    """attention() under autograd gives the gradients of the plan's backward, in q's dtype."""
+    announce("autograd function, 2 x 24 x 20, bf16, B")
+    B, H, W, heads, d, L = 2, 24, 20, 2, 32, 3
+    q, k, v = (dev_t(rand(500 + i, (B, H, W, heads, d), "bf16"), "bf16", dev).requires_grad_() for i in range(3))
+    w = torch.rand((B, H * W, heads, L), device=dev).requires_grad_()
+    out = P.attention(q, k, v, levels=L, K=4, variant="B", w=w)
+    g = dev_t(rand(504, (B, H, W, heads, d), "bf16"), "bf16", dev)
+    (out.float() * g.float()).sum().backward()
+    plan = P.Plan(B, H, W, heads, d, levels=L, K=4, variant="B", dtype=torch.bfloat16, device=dev)
+    plan.run(q.detach(), k.detach(), v.detach(), w.detach())
+    dq, dk, dv, dw = plan.backward(q.detach(), k.detach(), v.detach(), g, w.detach())
+    torch.cuda.synchronize()
+    assert q.grad.dtype == torch.bfloat16 and w.grad.dtype == torch.float32
+    assert torch.equal(q.grad, dq.to(torch.bfloat16))
+    assert grad_err(to_np(k.grad.float()), to_np(dk)) <= 1e-2
+    assert grad_err(to_np(v.grad.float()), to_np(dv)) <= 1e-2
+    assert torch.equal(w.grad, dw)
