@@ -6,7 +6,11 @@ workload is the feature-matching layer (1 x 60x80 tokens, 8 heads x 32, fp32, 3 
 QuadTree-B). Prints one JSON line with the throughput, the finest-level kernel's HBM roofline
 fraction (timed with HIP events on its own stream) and the CPU oracle timed on the host.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+With --backward a step is one whole backward pass instead (the gradients of q, k, v and w for an
+upstream gradient, the kept keys of one preceding forward held fixed), and the roofline kernel is
+the finest level's backward.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--backward]
 """
 from __future__ import annotations
 
@@ -22,9 +26,14 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "query tokens/sec per QuadTree attention layer + % of HBM/MFMA roofline, 1 GPU"
+METRIC_BWD = ("query tokens/sec per QuadTree attention layer, backward pass (gradients of q, k, v, w) + % of HBM "
+              "roofline, 1 GPU")
 HBM_PEAK_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
-FINE_SRC = os.path.join(ROOT, "paper_2201_02767_amd", "csrc", "fine.hip")
+_CSRC = os.path.join(ROOT, "paper_2201_02767_amd", "csrc")
+# every source compiled into the roofline kernel: its counters are stale once one of them changes
+FINE_SRC = [os.path.join(_CSRC, f) for f in ("fine.hip", "fine_item.h", "qta_device.h", "qta_internal.h")]
+BWD_SRC = [os.path.join(_CSRC, f) for f in ("backward.hip", "qta_device.h", "qta_internal.h")]
 
 
 def log(msg: str) -> None:
@@ -61,27 +70,64 @@ def finest_kernel_bytes(wl) -> dict:
     return {k: v * units for k, v in parts.items()}
 
 
-def kernel_source_hash() -> str:
-    with open(FINE_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def finest_backward_kernel_bytes(wl) -> dict:
+    """Algorithmic HBM bytes of one launch of the finest level's backward kernel, every tensor once:
+      per (batch, head):  N0*d*b (queries) + N0*d*b (upstream gradient) + [B with w] N0*4 (w_0 read)
+      + N1*K*sigma (parent selections) + N1*c*K*2*d*b (gathered key/value rows, c = 4 children per
+      kept key, 2 on one-row maps) + N0*d*4 (dq) + N1*c*K*2*d*4 (the gathered rows' fp32 gradient
+      contributions to dk and dv, one per sibling group) + [B with w] N0*4 (dw_0) + [A] N1*K*4 (the
+      parents' score gradients)."""
+    import paper_2201_02767_amd as P
+
+    mB, mH = (wl.B * wl.H, 1) if wl.epipolar else (wl.B, wl.H)
+    dims = P.level_dims(mH, wl.W, wl.levels)
+    n0 = dims[0][0] * dims[0][1]
+    n1 = dims[1][0] * dims[1][1]
+    b = 2 if wl.dtype == "bf16" else 4
+    sigma = 4 if wl.variant == "B" else 8
+    K1 = P.k_levels(wl.K, wl.levels)[1]
+    c = 2 if mH == 1 else 4
+    B_w = wl.variant == "B"
+    parts = {
+        "queries": n0 * wl.d * b,
+        "upstream_gradient": n0 * wl.d * b,
+        "level_weights": n0 * 4 if B_w else 0,
+        "parent_selections": n1 * K1 * sigma,
+        "gather": n1 * c * K1 * 2 * wl.d * b,
+        "dq": n0 * wl.d * 4,
+        "dk_dv_scatter": n1 * c * K1 * 2 * wl.d * 4,
+        "dw": n0 * 4 if B_w else 0,
+        "score_gradients": 0 if B_w else n1 * K1 * 4,
+    }
+    units = mB * wl.heads
+    return {k: v * units for k, v in parts.items()}
 
 
-def measured_traffic(workload: str):
+def kernel_source_hash(srcs=FINE_SRC) -> str:
+    h = hashlib.sha256()
+    for src in srcs:
+        with open(src, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, kernel: str = "fine_attn_finest", src=FINE_SRC):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken on the
     current kernel source; None otherwise."""
-    path = os.path.join(PROFILES, f"fine_attn_finest_{workload}_traffic.json")
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash(src):
         return None
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, seconds: float) -> dict:
-    """The oracle as it stands, single-threaded on the host, on whole layers of the workload."""
-    from paper_2201_02767_amd.inputs import make_level_weights, make_pe, make_qkv, make_v_levels
+def cpu_baseline(wl, seconds: float, backward: bool = False) -> dict:
+    """The oracle as it stands, single-threaded on the host, on whole layers of the workload (its
+    backward, which also runs the forward it differentiates, with --backward)."""
+    from paper_2201_02767_amd.inputs import make_dout, make_level_weights, make_pe, make_qkv, make_v_levels
     from oracle import oracle
 
     q, k, v = make_qkv(wl)
@@ -91,17 +137,21 @@ def cpu_baseline(wl, seconds: float) -> dict:
     if wl.epipolar:     # every row its own 1 x W map
         q, k, v = (x.reshape(wl.B * wl.H, 1, wl.W, wl.heads, wl.d) for x in (q, k, v))
         w = None if w is None else w.reshape(wl.B * wl.H, wl.W, wl.heads, wl.levels)
+    g = make_dout(wl).reshape(q.shape) if backward else None
     runs, t0 = 0, time.perf_counter()
     while True:
-        oracle.forward(q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w, v_levels=vl,
-                       pe_weight=pw, pe_bias=pb)
+        if backward:
+            oracle.backward(q, k, v, g, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w)
+        else:
+            oracle.forward(q, k, v, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w,
+                           v_levels=vl, pe_weight=pw, pe_bias=pb)
         runs += 1
         el = time.perf_counter() - t0
         if el >= seconds:
             break
     return {"value": wl.tokens * runs / el, "unit": "query tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{runs} whole {wl.name} layer(s) ({wl.B}x{wl.H}x{wl.W}, {wl.heads}x{wl.d}, L={wl.levels}, "
-                      f"K={wl.K}) in {el:.1f} s, one thread"}
+            "sample": f"{runs} whole {wl.name} layer {'backward pass(es)' if backward else 'forward(s)'} "
+                      f"({wl.B}x{wl.H}x{wl.W}, {wl.heads}x{wl.d}, L={wl.levels}, K={wl.K}) in {el:.1f} s, one thread"}
 
 
 def main() -> int:
@@ -113,6 +163,7 @@ def main() -> int:
     ap.add_argument("--kernel-launches", type=int, default=500, help="launches timed for the roofline kernel")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--backward", action="store_true", help="time the backward pass instead of the forward")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run plain device copies of this many MiB (to scale HBM byte counters) and exit")
     args = ap.parse_args()
@@ -138,7 +189,7 @@ def main() -> int:
         return 0
 
     import paper_2201_02767_amd as P
-    from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_pe, make_qkv, make_v_levels
+    from paper_2201_02767_amd.inputs import WORKLOADS, make_dout, make_level_weights, make_pe, make_qkv, make_v_levels
 
     if args.workload not in WORKLOADS:
         print(f"unknown workload {args.workload}; choose from {sorted(WORKLOADS)}", file=sys.stderr)
@@ -158,6 +209,14 @@ def main() -> int:
                   device=dev, v_supplied=wl.v_given, pe=wl.pe, epipolar=wl.epipolar)
     step = plan.prepare(q, k, v, w, v_levels=vl, pe_weight=pw, pe_bias=pb)
     log(f"bench: {wl} on {torch.cuda.get_device_name(0)}")
+    if args.backward:
+        if wl.v_given or wl.pe:
+            print("the backward pass covers pooled V levels without a position encoding", file=sys.stderr)
+            return 2
+        g = torch.from_numpy(make_dout(wl)).to(dev).to(tdt).contiguous()
+        step()                                   # the forward whose kept keys the backward holds fixed
+        step = plan.prepare_backward(q, k, v, g, w)
+        log("bench: timing the backward pass")
 
     for _ in range(args.warmup):
         step()
@@ -179,7 +238,28 @@ def main() -> int:
 
     # the dominant kernel alone, on the same stream, on the selections the forward left behind
     roof = None
-    if wl.levels >= 2:
+    if wl.levels >= 2 and args.backward:
+        finest = plan.prepare_backward(q, k, v, g, w, finest_only=True)
+        for _ in range(10):
+            finest()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.kernel_launches):
+            finest()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        k_us = e0.elapsed_time(e1) * 1e3 / args.kernel_launches
+        parts = finest_backward_kernel_bytes(wl)
+        algo = sum(parts.values())
+        achieved = algo / (k_us * 1e-6) / 1e9
+        traffic = measured_traffic(wl.name, "bwd_level_finest", BWD_SRC)
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": "bwd_level_kernel (finest level backward)", "kernel_us": round(k_us, 3),
+                "algorithmic_bytes": algo}
+        log(f"bench: finest-level backward kernel {k_us:.2f} us/launch, {algo / 1e6:.1f} MB algorithmic -> "
+            f"{achieved:.0f} GB/s ({100 * achieved / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f})")
+    elif wl.levels >= 2:
         finest = plan.prepare_finest(q, k, v, w)
         for _ in range(10):
             finest()
@@ -203,17 +283,18 @@ def main() -> int:
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, args.cpu_seconds)
+        cpu = cpu_baseline(wl, args.cpu_seconds, args.backward)
         log(f"bench: oracle {cpu['value']:.4g} query tokens/s ({cpu['sample']})")
 
     rec = {
-        "metric": METRIC, "value": round(value, 1), "unit": "query tokens/s", "n_gpus": 1, "steps": args.steps,
+        "metric": METRIC_BWD if args.backward else METRIC, "value": round(value, 1), "unit": "query tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32" if wl.dtype == "f32" else "bf16", "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "W": wl.W, "heads": wl.heads, "d": wl.d,
                    "levels": wl.levels, "K": wl.K if isinstance(wl.K, int) else list(wl.K)[1:],
                    "v_levels": "given" if wl.v_given else "pooled", "position_encoding": wl.pe,
                    "attention": "epipolar rows" if wl.epipolar else "2-D",
+                   "pass": "backward" if args.backward else "forward",
                    "variant": wl.variant, "global_batch": wl.B,
                    "seq_len": wl.H * wl.W, "parallelism": "none (1 GPU)"},
         "roofline": roof, "cpu_baseline": cpu,

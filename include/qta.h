@@ -195,6 +195,19 @@ qta_status qta_backward_ex(const void* q, const void* k, const void* v, const fl
                            void* bwd_workspace, size_t bwd_workspace_bytes, void* stream);
 
 /*
+ * qta_backward_finest_ex - the level-0 step of qta_backward_ex alone (the attention backward at the
+ * finest level), for timing it: same arguments, and the workspaces a qta_backward_ex call on the same
+ * inputs left behind. It overwrites dq and, for QuadTree-B with w, dw[..][0] with that step's values
+ * and adds that step's contributions to dk and dv again, so the gradients are no longer those of
+ * the layer afterwards. levels >= 2.
+ */
+qta_status qta_backward_finest_ex(const void* q, const void* k, const void* v, const float* w, const void* dout,
+                                  int B, int heads, int H, int W, int d, int levels, int K, qta_variant variant,
+                                  qta_dtype dtype, float scale, const qta_options* opt, const void* workspace,
+                                  size_t workspace_bytes, float* dq, float* dk, float* dv, float* dw,
+                                  void* bwd_workspace, size_t bwd_workspace_bytes, void* stream);
+
+/*
  * qta_build_pyramid - step 1: levels 1..levels-1 of one token map by 2x2 average pooling
  * (Sec. 3.2). Each level is pooled from the stored level below it: the valid children are summed
  * in fp32 as ((c00 + c01) + (c10 + c11)), missing children left out, multiplied by 1/count and

@@ -660,11 +660,16 @@ size_t qta_backward_workspace_bytes_ex(int B, int heads, int H, int W, int d, in
     return G.total;
 }
 
-qta_status qta_backward_ex(const void* q, const void* k, const void* v, const float* w, const void* dout, int B,
-                           int heads, int H, int W, int d, int levels, int K, qta_variant variant, qta_dtype dtype,
-                           float scale, const qta_options* opt, const void* workspace, size_t workspace_bytes,
-                           float* dq, float* dk, float* dv, float* dw, void* bwd_workspace,
-                           size_t bwd_workspace_bytes, void* stream)
+}  // extern "C"
+
+namespace {
+
+// The backward pass; with only_finest, just the level-0 kernel (for profiling it alone).
+qta_status backward_impl(const void* q, const void* k, const void* v, const float* w, const void* dout, int B,
+                         int heads, int H, int W, int d, int levels, int K, qta_variant variant, qta_dtype dtype,
+                         float scale, const qta_options* opt, const void* workspace, size_t workspace_bytes,
+                         float* dq, float* dk, float* dv, float* dw, void* bwd_workspace, size_t bwd_workspace_bytes,
+                         void* stream, bool only_finest)
 {
     qta_status st = check_problem(B, heads, d, 1, variant, dtype);
     if (st != QTA_OK) return st;
@@ -705,8 +710,9 @@ qta_status qta_backward_ex(const void* q, const void* k, const void* v, const fl
     auto sidx = [&](int l) { return reinterpret_cast<const int32_t*>(ws + L.sel_idx[l]); };
     auto skey = [&](int l) { return reinterpret_cast<const float*>(ws + L.sel_key[l]); };
     const int c = levels - 1;
+    if (only_finest && levels < 2) return QTA_ERR_INVALID;
 
-    if (levels > 1) {
+    if (levels > 1 && !only_finest) {
         // clear what is accumulated: dm of levels >= 2, the k and v gradients of levels 0..L-2
         FillRange r[3];
         r[0] = FillRange{fptr(G.zero_begin), (G.zero_end - G.zero_begin) / sizeof(float)};
@@ -734,9 +740,10 @@ qta_status qta_backward_ex(const void* q, const void* k, const void* v, const fl
         }
         cb.dw = dw_out;
         if (launch_bwd_combine(cb, use_bf16, s) != hipSuccess) return QTA_ERR_HIP;
-
+    }
+    if (levels > 1) {
         // 2. finer levels, finest first (QuadTree-A's score gradients go up one level each)
-        for (int l = 0; l < c; ++l) {
+        for (int l = 0; l < (only_finest ? 1 : c); ++l) {
             BwdLevelArgs a{};
             if (l == 0) {
                 a.q = q;
@@ -778,6 +785,7 @@ qta_status qta_backward_ex(const void* q, const void* k, const void* v, const fl
             if (launch_bwd_level(a, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
         }
     }
+    if (only_finest) return QTA_OK;
 
     // 3. coarsest level
     {
@@ -834,6 +842,30 @@ qta_status qta_backward_ex(const void* q, const void* k, const void* v, const fl
     u.dk = dk;
     u.dv = dv;
     return launch_bwd_unpool(u, s) == hipSuccess ? QTA_OK : QTA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+qta_status qta_backward_ex(const void* q, const void* k, const void* v, const float* w, const void* dout, int B,
+                           int heads, int H, int W, int d, int levels, int K, qta_variant variant, qta_dtype dtype,
+                           float scale, const qta_options* opt, const void* workspace, size_t workspace_bytes,
+                           float* dq, float* dk, float* dv, float* dw, void* bwd_workspace,
+                           size_t bwd_workspace_bytes, void* stream)
+{
+    return backward_impl(q, k, v, w, dout, B, heads, H, W, d, levels, K, variant, dtype, scale, opt, workspace,
+                         workspace_bytes, dq, dk, dv, dw, bwd_workspace, bwd_workspace_bytes, stream, false);
+}
+
+qta_status qta_backward_finest_ex(const void* q, const void* k, const void* v, const float* w, const void* dout,
+                                  int B, int heads, int H, int W, int d, int levels, int K, qta_variant variant,
+                                  qta_dtype dtype, float scale, const qta_options* opt, const void* workspace,
+                                  size_t workspace_bytes, float* dq, float* dk, float* dv, float* dw,
+                                  void* bwd_workspace, size_t bwd_workspace_bytes, void* stream)
+{
+    return backward_impl(q, k, v, w, dout, B, heads, H, W, d, levels, K, variant, dtype, scale, opt, workspace,
+                         workspace_bytes, dq, dk, dv, dw, bwd_workspace, bwd_workspace_bytes, stream, true);
 }
 
 }  // extern "C"

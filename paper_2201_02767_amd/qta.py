@@ -71,6 +71,8 @@ _SIGS = {
     "qta_backward_workspace_bytes_ex": ([_I, _I, _I, _I, _I, _I, _I, _I, _I, _P], ctypes.c_size_t),
     "qta_backward_ex": ([_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, ctypes.c_size_t,
                          _P, _P, _P, _P, _P, ctypes.c_size_t, _P], _I),
+    "qta_backward_finest_ex": ([_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, ctypes.c_size_t,
+                                _P, _P, _P, _P, _P, ctypes.c_size_t, _P], _I),
     "qta_build_pyramid": ([_P, _P, _I, _I, _I, _I, _I, _I, _P], _I),
     "qta_coarse_attn": ([_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, _P], _I),
     "qta_topk": ([_P, _P, _I, _I, _I, _P, _P, _P], _I),
@@ -363,11 +365,12 @@ class Plan:
         _check("qta_backward_ex", lib().qta_backward_ex(*args))
         return grads
 
-    def prepare_backward(self, q, k, v, dout, w=None):
+    def prepare_backward(self, q, k, v, dout, w=None, finest_only=False):
         """Validate once and return a zero-argument callable that re-issues this backward on the
-        current stream."""
+        current stream (``finest_only``: just its level-0 kernel, for timing it; the gradients are
+        then no longer the layer's)."""
         args, opt, grads = self._bwd_args(q, k, v, w, dout, _stream(self.device))
-        fn = lib().qta_backward_ex
+        fn = lib().qta_backward_finest_ex if finest_only else lib().qta_backward_ex
         keep = (q, k, v, w, dout, opt, grads)
 
         def call():
