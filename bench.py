@@ -71,12 +71,16 @@ def finest_kernel_bytes(wl) -> dict:
 
 
 def finest_backward_kernel_bytes(wl) -> dict:
-    """Algorithmic HBM bytes of one launch of the finest level's backward kernel, every tensor once:
-      per (batch, head):  N0*d*b (queries) + N0*d*b (upstream gradient) + [B with w] N0*4 (w_0 read)
-      + N1*K*sigma (parent selections) + N1*c*K*2*d*b (gathered key/value rows, c = 4 children per
-      kept key, 2 on one-row maps) + N0*d*4 (dq) + N1*c*K*2*d*4 (the gathered rows' fp32 gradient
-      contributions to dk and dv, one per sibling group) + [B with w] N0*4 (dw_0) + [A] N1*K*4 (the
-      parents' score gradients)."""
+    """Algorithmic HBM bytes of the finest level's backward step (its query pass, the counting sort
+    of the kept pairs, its key pass), every tensor once, per (batch, head), with c = 4 children per
+    kept key (2 on one-row maps) and M = N1*K kept (parent, key) pairs:
+      query pass:  N0*d*b (q) + N0*d*b (dout) + [B with w] 4*N0*L (w) + M*sigma (parent selections)
+                   + M*c*2*d*b (gathered key/value rows) + 4*N0*d (dq) + 8*N0 (statistics; A: 8*N0*K)
+                   + [B with w] 4*N0*L (dw) + 4*N1*d*(L-1) (message gradients of the coarser levels,
+                   one row per sibling group and level) + [A] 4*M (score gradients) + 4*M (counts)
+      sort:        4*M (the pairs, grouped by key)
+      key pass:    4*M (the pairs) + M*c*(2*d*b + 8) (the parents' children: q and dout rows,
+                   statistics) + N1*c*2*d*b (the keys' k and v rows) + 2*4*N0*d (dk, dv)."""
     import paper_2201_02767_amd as P
 
     mB, mH = (wl.B * wl.H, 1) if wl.epipolar else (wl.B, wl.H)
@@ -87,17 +91,24 @@ def finest_backward_kernel_bytes(wl) -> dict:
     sigma = 4 if wl.variant == "B" else 8
     K1 = P.k_levels(wl.K, wl.levels)[1]
     c = 2 if mH == 1 else 4
+    d, L = wl.d, wl.levels
     B_w = wl.variant == "B"
+    M = n1 * K1
     parts = {
-        "queries": n0 * wl.d * b,
-        "upstream_gradient": n0 * wl.d * b,
-        "level_weights": n0 * 4 if B_w else 0,
-        "parent_selections": n1 * K1 * sigma,
-        "gather": n1 * c * K1 * 2 * wl.d * b,
-        "dq": n0 * wl.d * 4,
-        "dk_dv_scatter": n1 * c * K1 * 2 * wl.d * 4,
-        "dw": n0 * 4 if B_w else 0,
-        "score_gradients": 0 if B_w else n1 * K1 * 4,
+        "queries": n0 * d * b,
+        "upstream_gradient": n0 * d * b,
+        "level_weights": 4 * n0 * L if B_w else 0,
+        "parent_selections": M * sigma,
+        "gather": M * c * 2 * d * b,
+        "dq": 4 * n0 * d,
+        "statistics": 8 * n0 * (1 if B_w else K1),
+        "dw": 4 * n0 * L if B_w else 0,
+        "message_gradients": 4 * n1 * d * (L - 1),
+        "score_gradients": 0 if B_w else 4 * M,
+        "counts_and_pairs": 4 * M * 3,
+        "key_pass_queries": M * c * (2 * d * b + 8),
+        "key_pass_keys": n1 * c * 2 * d * b,
+        "dk_dv": 2 * 4 * n0 * d,
     }
     units = mB * wl.heads
     return {k: v * units for k, v in parts.items()}
@@ -255,9 +266,10 @@ def main() -> int:
         traffic = measured_traffic(wl.name, "bwd_level_finest", BWD_SRC)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "bwd_level_kernel (finest level backward)", "kernel_us": round(k_us, 3),
+                "kernel": "finest-level backward step (query pass, counting sort, key pass; 6 launches)",
+                "kernel_us": round(k_us, 3),
                 "algorithmic_bytes": algo}
-        log(f"bench: finest-level backward kernel {k_us:.2f} us/launch, {algo / 1e6:.1f} MB algorithmic -> "
+        log(f"bench: finest-level backward step {k_us:.2f} us/launch, {algo / 1e6:.1f} MB algorithmic -> "
             f"{achieved:.0f} GB/s ({100 * achieved / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f})")
     elif wl.levels >= 2:
         finest = plan.prepare_finest(q, k, v, w)

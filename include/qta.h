@@ -183,8 +183,9 @@ qta_status qta_forward_ex(const void* q, const void* k, const void* v, const flo
  *   bwd_workspace  device memory of qta_backward_workspace_bytes_ex bytes, 256-byte aligned; its
  *                contents need not be preserved between calls.
  * Unsupported (QTA_ERR_UNSUPPORTED): caller-supplied V levels, the position encoding, and K_l with
- * 4*K_l > 64 at any level. The gradients of k and v (and internal sums) are accumulated with fp32
- * atomics, so their last bits may vary between runs. Options as in qta_forward_ex.
+ * 4*K_l > 64 at any level. Some sums (the message gradients of levels >= 2, and each key's list of
+ * the parents that kept it) are ordered by atomics, so the last bits may vary between runs. Options
+ * as in qta_forward_ex.
  */
 size_t qta_backward_workspace_bytes_ex(int B, int heads, int H, int W, int d, int levels, int K,
                                        qta_variant variant, qta_dtype dtype, const qta_options* opt);
@@ -196,10 +197,10 @@ qta_status qta_backward_ex(const void* q, const void* k, const void* v, const fl
 
 /*
  * qta_backward_finest_ex - the level-0 step of qta_backward_ex alone (the attention backward at the
- * finest level), for timing it: same arguments, and the workspaces a qta_backward_ex call on the same
- * inputs left behind. It overwrites dq and, for QuadTree-B with w, dw[..][0] with that step's values
- * and adds that step's contributions to dk and dv again, so the gradients are no longer those of
- * the layer afterwards. levels >= 2.
+ * finest level: its query pass and its key pass), for timing it: same arguments, and the workspaces a
+ * qta_backward_ex call on the same inputs left behind. It overwrites dq, dk, dv and, for QuadTree-B
+ * with w, dw[..][0] with that step's values, so the gradients are no longer those of the layer
+ * afterwards. levels >= 2.
  */
 qta_status qta_backward_finest_ex(const void* q, const void* k, const void* v, const float* w, const void* dout,
                                   int B, int heads, int H, int W, int d, int levels, int K, qta_variant variant,

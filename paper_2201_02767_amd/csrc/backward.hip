@@ -1,19 +1,27 @@
 // Backward pass of QuadTree attention: gradients of q, k, v (and QuadTree-B's w) for an upstream
 // gradient of the output, with the kept-key sets of the forward held fixed (top-K is a selection,
 // not differentiated). The chain rule runs through the forward's steps in reverse (Sec. 3.2):
-//   1. combination (Eqs. 2, 5): dm^l of a level-l token sums w_{i,l} dout_i over its finest
-//      descendants; dw_{i,l} = <dout_i, m^l of the ancestor>            (bwd_combine_kernel)
-//   2. each finer level, finest first, one wave per sibling group as in the forward: the logits
-//      and <dm, v> of every candidate on MFMA, then the softmax gradient (B: over the candidates,
-//      Eq. 6; A: over each kept key's children with s = sigma t, Eq. 4, sending d sigma back to the
-//      parent level), dq on MFMA, and dk, dv scattered to the gathered keys with fp32 atomics
+//   1. combination (Eqs. 2, 5), inside the finest level's query pass: dm^l of a level-l token sums
+//      w_{i,l} dout_i over its finest descendants (each sibling group adds its four queries' share
+//      to its ancestors); dw_{i,l} = <dout_i, m^l of the ancestor>
+//   2. each finer level, finest first, in two passes:
+//      query pass, one wave per sibling group as in the forward: the logits and <dm, v> of every
+//      candidate on MFMA, the softmax gradient (B: over the candidates, Eq. 6; A: over each kept
+//      key's children with s = sigma t, Eq. 4, sending d sigma back to the parent level), dq on
+//      MFMA; it keeps each query's softmax statistics and counts how many parents kept each key
 //                                                                        (bwd_level_kernel)
+//      key pass: the parents are sorted by the key they kept (a counting sort: the counts, a scan,
+//      a fill), and one wave per chunk of up to kKeyChunk parents of one kept key gathers those
+//      parents' four children and forms dk and dv of the key's four children from the recomputed
+//      probabilities; a key's rows are written once (summed over its chunks when it has several)
+//                                                   (bwd_scan_*, bwd_fill, bwd_key, bwd_key_reduce)
 //   3. the coarsest level (Eq. 1): a pass per query (dq, softmax statistics) and a pass per key
 //      (dk, dv) that recomputes the probabilities, so neither needs atomics (bwd_coarse_*)
 //   4. pyramids: a pooled token hands 1/n of its gradient to each of its n valid children; the
 //      level-0 gradients add every ancestor's, scaled along the chain      (bwd_unpool_kernel)
-// All gradients are fp32. The order in which the atomics land varies from run to run, so dk and
-// dv (and dm at levels >= 2) may differ in the last bits between runs.
+// All gradients are fp32. The message gradients of levels >= 2 are summed with atomics and the
+// parents within one kept key's list come in the order the fill's atomics hand out, so the last bits
+// of the gradients may differ between runs.
 #include "qta_device.h"
 #include "qta_internal.h"
 
@@ -45,93 +53,13 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(FillArgs a)
 }
 
 // ---------------------------------------------------------------------------------------------
-// 1. combination backward
-// ---------------------------------------------------------------------------------------------
-
-// Sum over the d lanes of one head (d = 32 or 64 consecutive lanes, aligned).
-__device__ __forceinline__ float head_sum(float x, int d)
-{
-    x += xchg_f32<1>(x);
-    x += xchg_f32<2>(x);
-    x += xchg_f32<4>(x);
-    x += xchg_f32<8>(x);
-    x += xchg_f32<16>(x);
-    if (d == 64) x += xchg_f32<32>(x);
-    return x;
-}
-
-template <typename T>
-__global__ __launch_bounds__(256) void bwd_combine_kernel(BwdCombineArgs a)
-{
-    using S = Storage<T>;
-    const int C = a.C, L = a.L;
-    const int H1 = a.H[1], W1 = a.W[1], H0 = a.H[0], W0 = a.W[0];
-    const long long total = static_cast<long long>(a.B) * H1 * W1 * C;
-    const long long tid = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
-    // threads past the end run on clamped indices (the head sums need every lane) and store nothing
-    const bool active = tid < total;
-    const long long t = active ? tid : total - 1;
-    const int c = static_cast<int>(t % C);
-    const long long pt = t / C;
-    const int P = static_cast<int>(pt % (static_cast<long long>(H1) * W1));
-    const int b = static_cast<int>(pt / (static_cast<long long>(H1) * W1));
-    const int h = c / a.d;
-    const int Py = P / W1, Px = P - Py * W1;
-    const bool want_dw = a.variant_b && a.w && a.dw;
-    // the ancestors' messages at this channel (shared by the 2x2 children of P)
-    float manc[QTA_MAX_LEVELS];
-#pragma unroll
-    for (int l = 1; l < QTA_MAX_LEVELS; ++l) {
-        manc[l] = 0.f;
-        if (l < L && want_dw) {
-            const size_t anc = static_cast<size_t>(b) * a.H[l] * a.W[l] +
-                               static_cast<size_t>((2 * Py) >> l) * a.W[l] + ((2 * Px) >> l);
-            manc[l] = a.msg[l][anc * C + c];
-        }
-    }
-    float acc[QTA_MAX_LEVELS];
-#pragma unroll
-    for (int l = 0; l < QTA_MAX_LEVELS; ++l) acc[l] = 0.f;
-    const float wdef = a.variant_b ? 1.0f / L : 1.0f;
-#pragma unroll
-    for (int ci = 0; ci < 4; ++ci) {
-        const int y = 2 * Py + (ci >> 1), x = 2 * Px + (ci & 1);
-        const bool valid = y < H0 && x < W0;           // the same for every lane of a head
-        const size_t tok = static_cast<size_t>(b) * H0 * W0 + static_cast<size_t>(valid ? y : 2 * Py) * W0 +
-                           (valid ? x : 2 * Px);
-        const float g = valid ? S::load1(a.dout, tok * C + c) : 0.f;
-        const float* wrow = a.w ? a.w + (tok * a.heads + h) * L : nullptr;
-#pragma unroll
-        for (int l = 1; l < QTA_MAX_LEVELS; ++l) {
-            if (l >= L) break;
-            const float wl = (a.variant_b && wrow) ? wrow[l] : wdef;
-            acc[l] += wl * g;
-            if (want_dw) {
-                const float dot = head_sum(g * manc[l], a.d);
-                if (active && valid && (c % a.d) == 0) a.dw[(tok * a.heads + h) * L + l] = dot;
-            }
-        }
-    }
-    if (!active) return;
-    a.dm[1][(static_cast<size_t>(b) * H1 * W1 + P) * C + c] = acc[1];
-#pragma unroll
-    for (int l = 2; l < QTA_MAX_LEVELS; ++l) {
-        if (l >= L) break;
-        const size_t anc = static_cast<size_t>(b) * a.H[l] * a.W[l] + static_cast<size_t>(Py >> (l - 1)) * a.W[l] +
-                           (Px >> (l - 1));
-        atomicAddNoRet(a.dm[l] + anc * C + c, acc[l]);
-    }
-}
-
-// ---------------------------------------------------------------------------------------------
 // 2. finer levels
 // ---------------------------------------------------------------------------------------------
 
 // Byte layout of one wave's LDS region for nsp padded slots: the gathered key rows in fp32 (B
-// operand of dq), per slot the four queries' logit gradients and value weights, per channel the
-// four queries' q and dm, and the slots' flat key indices.
+// operand of dq) and per slot the four queries' logit gradients.
 struct BwdLds {
-    int ks, dx, vw, q, dm, flat, total;
+    int ks, dx, total;
     int kpitch;     // floats per key row
 };
 
@@ -142,11 +70,7 @@ __host__ __device__ inline BwdLds bwd_lds(int nsp)
     L.kpitch = D + 4;
     L.ks = 0;
     L.dx = L.ks + nsp * L.kpitch * 4;
-    L.vw = L.dx + nsp * 16;
-    L.q = L.vw + nsp * 16;
-    L.dm = L.q + D * 16;
-    L.flat = L.dm + D * 16;
-    L.total = (L.flat + nsp * 4 + 15) / 16 * 16;
+    L.total = L.dx + nsp * 16;
     return L;
 }
 
@@ -185,10 +109,6 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
     const BwdLds lay = bwd_lds<D>(nsp);
     float* Ks = reinterpret_cast<float*>(base + lay.ks);
     float* dxs = reinterpret_cast<float*>(base + lay.dx);      // [slot][4]
-    float* vws = reinterpret_cast<float*>(base + lay.vw);      // [slot][4]
-    float* q4 = reinterpret_cast<float*>(base + lay.q);        // [channel][4]
-    float* dm4 = reinterpret_cast<float*>(base + lay.dm);      // [channel][4]
-    int* flat_l = reinterpret_cast<int*>(base + lay.flat);
 
     const size_t prow_off = (static_cast<size_t>(b) * a.heads + h) * Np + P;
     const int32_t* prow = a.parent_idx + prow_off * K;
@@ -265,28 +185,10 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             w0[r] = a.w ? a.w[((static_cast<size_t>(b) * N + rt) * a.heads + h) * a.levels] : 1.0f / a.levels;
         }
     }
-    // q and dm of the four queries per channel, fp32, for dk and dv (lanes n16 < 4 hold query n16)
-    if (n16 < 4) {
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            float qf[E];
-            S::unpack(qa[j], qf);
-            float gf[E];
-            if constexpr (FINEST) {
-                S::unpack(da[j], gf);
-#pragma unroll
-                for (int e = 0; e < E; ++e) gf[e] *= pick4(float4_t{w0[0], w0[1], w0[2], w0[3]}, n16);
-            } else {
-#pragma unroll
-                for (int e = 0; e < E; ++e) gf[e] = dmA[j][e];
-            }
-            const int c0 = (g + 4 * j) * E;
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                q4[(c0 + e) * 4 + n16] = qf[e];
-                dm4[(c0 + e) * 4 + n16] = gf[e];
-            }
-        }
+    // how many parents kept each key of level l+1 (for the key pass's counting sort)
+    {
+        const int Jr = prow[min(lane, last_sel)];
+        if (lane < K && Jr >= 0) atomicAdd(a.count + (static_cast<size_t>(b) * a.heads + h) * Np + Jr, 1);
     }
 
     // ---- gathers, logits and <dm, v> on MFMA, key rows to LDS, one tile of 16 slots at a time ----
@@ -355,7 +257,6 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             acc_g[r] = g == t ? ag[r] : acc_g[r];
         }
     }
-    if (lane < nsp) flat_l[lane] = flat;
 
     // ---- softmax gradients of slot `lane` for the four queries ----
     float x[4], gsl[4];
@@ -364,16 +265,23 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
         x[r] = ok ? acc_x[r] * a.scale : -INFINITY;
         gsl[r] = FINEST ? w0[r] * acc_g[r] : acc_g[r];      // dLoss/d(weight) on Omega
     }
-    float dxr[4], vwr[4];
+    float dxr[4];
+    const size_t bh = static_cast<size_t>(b) * a.heads + h;
     if constexpr (!VA) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const float m = wave_max_fast(x[r]);
             const float e = ok ? __expf(x[r] - m) : 0.f;
-            const float p = e / wave_sum_fast(e);
+            const float sum = wave_sum_fast(e);
+            const float p = e / sum;
             const float Dr = wave_sum_fast(p * gsl[r]);
             dxr[r] = qv[r] ? p * (gsl[r] - Dr) : 0.f;
-            vwr[r] = qv[r] ? p : 0.f;
+            // the key pass recomputes p = exp(x - lse) and needs D
+            if (lane == 0 && qv[r]) {
+                const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
+                *reinterpret_cast<float2*>(a.stats + (bh * N + __mul24(ry, W) + rx) * 2) =
+                    make_float2(m + __logf(sum), Dr);
+            }
             if constexpr (FINEST) {
                 if (a.w && a.dw) {                            // uniform
                     const float dw0 = wave_sum_fast(p * acc_g[r]);
@@ -396,33 +304,29 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             const float tt = ok ? e / sum : 0.f;
             const float sc = pkey * tt;
             float ds = gsl[r];
-            bool kept = false;
             if constexpr (!FINEST) {
                 // a key this query keeps is refined at level l-1: its score's gradient comes from there
                 const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
                 const size_t srow = ((static_cast<size_t>(b) * a.heads + h) * N + __mul24(min(ry, H - 1), W) +
                                      min(rx, W - 1)) * a.Ks;
-                for (int mm = 0; mm < a.Ks; ++mm) {
-                    const int32_t j = a.sel_idx[srow + mm];
-                    if (ok && j == flat) {
-                        kept = true;
-                        ds = a.dsig_in[srow + mm];
-                    }
-                }
+                for (int mm = 0; mm < a.Ks; ++mm)
+                    if (ok && a.sel_idx[srow + mm] == flat) ds = a.dsig_in[srow + mm];
             }
             float dsq = tt * ds;                              // this query's d sigma of the kept key
             dsq += xchg_f32<1>(dsq);
             dsq += xchg_f32<2>(dsq);
             dxr[r] = qv[r] ? sc * (ds - dsq) : 0.f;
-            vwr[r] = (qv[r] && !kept) ? sc : 0.f;
             dsig_acc += qv[r] ? dsq : 0.f;
+            // the key pass recomputes t = exp(x - lse) per kept parent key and needs sum t ds
+            if ((lane & 3) == 0 && (lane >> 2) < K && qv[r]) {
+                const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
+                *reinterpret_cast<float2*>(a.stats + ((bh * N + __mul24(ry, W) + rx) * K + (lane >> 2)) * 2) =
+                    make_float2(m + __logf(sum), dsq);
+            }
         }
         if ((lane & 3) == 0 && (lane >> 2) < K) a.dsig_out[prow_off * K + (lane >> 2)] = dsig_acc;
     }
-    if (lane < nsp) {
-        *reinterpret_cast<float4*>(dxs + lane * 4) = make_float4(dxr[0], dxr[1], dxr[2], dxr[3]);
-        *reinterpret_cast<float4*>(vws + lane * 4) = make_float4(vwr[0], vwr[1], vwr[2], vwr[3]);
-    }
+    if (lane < nsp) *reinterpret_cast<float4*>(dxs + lane * 4) = make_float4(dxr[0], dxr[1], dxr[2], dxr[3]);
     wave_lds_sync();
 
     // ---- dq = scale * sum_s dx_s k_s on the 4x4 MFMA (blocks over 4-channel groups, slot halves) ----
@@ -450,20 +354,60 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
         }
     }
 
-    // ---- dk and dv of the gathered keys: lanes over (slot, channel), coalesced atomics ----
-    for (int idx = lane; idx < nslot * D; idx += kWave) {
-        const int s = idx / D, c = idx - s * D;
-        const int f = flat_l[s];
-        if (f < 0) continue;
-        const float4 dx4 = *reinterpret_cast<const float4*>(dxs + s * 4);
-        const float4 vw4 = *reinterpret_cast<const float4*>(vws + s * 4);
-        const float4 qc = *reinterpret_cast<const float4*>(q4 + c * 4);
-        const float4 gc = *reinterpret_cast<const float4*>(dm4 + c * 4);
-        const float dkv = a.scale * (dx4.x * qc.x + dx4.y * qc.y + dx4.z * qc.z + dx4.w * qc.w);
-        const float dvv = vw4.x * gc.x + vw4.y * gc.y + vw4.z * gc.z + vw4.w * gc.w;
-        const size_t row = (static_cast<size_t>(b) * N + f) * C + h * D + c;
-        atomicAddNoRet(a.dk + row, dkv);
-        atomicAddNoRet(a.dv + row, dvv);
+    // ---- level 0: the combination's backward for the coarser levels. The four queries are the
+    //      children of P, so at every level j >= 1 they share one ancestor: dm^j of that ancestor
+    //      receives sum_r w_{r,j} dout_r (written at j = 1, where the ancestor is P itself, and
+    //      added with atomics above), and dw_{r,j} = <dout_r, m^j of the ancestor>. ----
+    if constexpr (FINEST) {
+        const int L = a.levels;
+        const bool want_dw = !VA && a.w && a.dw;
+        const size_t wrow = ((static_cast<size_t>(b) * N + qtok) * a.heads + h) * L;    // query n16 & 3
+        float gv[NJ][E];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) S::unpack(da[j], gv[j]);                    // zero off the map
+        for (int lv = 1; lv < L; ++lv) {
+            const float wl = VA ? 1.0f : (a.w ? a.w[wrow + lv] : 1.0f / L);
+            const size_t anc = static_cast<size_t>(b) * a.lvl_N[lv] +
+                               static_cast<size_t>((2 * Py) >> lv) * a.lvl_W[lv] + ((2 * Px) >> lv);
+            const size_t arow = (anc * a.heads + h) * D;
+            float part = 0.f;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const int c0 = (g + 4 * j) * E;
+                float sv[E];
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    sv[e] = wl * gv[j][e];
+                    sv[e] += xchg_f32<1>(sv[e]);                                  // the four queries
+                    sv[e] += xchg_f32<2>(sv[e]);
+                }
+                if (want_dw) {
+                    const float* m = a.msg_fwd[lv] + arow + c0;
+#pragma unroll
+                    for (int e4 = 0; e4 < E; e4 += 4) {
+                        const float4 m4 = *reinterpret_cast<const float4*>(m + e4);
+                        part += gv[j][e4] * m4.x + gv[j][e4 + 1] * m4.y + gv[j][e4 + 2] * m4.z + gv[j][e4 + 3] * m4.w;
+                    }
+                }
+                // every lane of group g holds the sums of chunk g + 4j: lane 16g + e stores element e,
+                // so one instruction covers the head's channels contiguously
+                float mine = sv[0];
+#pragma unroll
+                for (int e = 1; e < E; ++e) mine = n16 == e ? sv[e] : mine;
+                if (n16 < E) {
+                    float* dst = a.dm_out[lv] + arow + c0 + n16;
+                    if (lv == 1)
+                        *dst = mine;
+                    else
+                        atomicAddNoRet(dst, mine);
+                }
+            }
+            if (want_dw) {
+                part += xchg_f32<16>(part);
+                part += xchg_f32<32>(part);
+                if (g == 0 && n16 < 4 && q_ok) a.dw[wrow + lv] = part;
+            }
+        }
     }
 }
 
@@ -519,6 +463,525 @@ hipError_t launch_level_td(const BwdLevelArgs& a, bool variant_a, bool finest, h
     if (variant_a)
         return finest ? launch_level_nsp<T, D, true, true>(a, stream) : launch_level_nsp<T, D, true, false>(a, stream);
     return finest ? launch_level_nsp<T, D, false, true>(a, stream) : launch_level_nsp<T, D, false, false>(a, stream);
+}
+
+// ---- counting sort of the parents by the key they kept ----
+
+// Block-wide exclusive scan of two counters per element over 256 threads x 4 elements; returns
+// the block total in `total` (all threads).
+__device__ __forceinline__ void block_scan_256x4(int2 (&v)[4], int2& total)
+{
+    __shared__ int2 wsum[4];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int2 run = make_int2(0, 0);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int2 t = v[e];
+        v[e] = run;
+        run.x += t.x;
+        run.y += t.y;
+    }
+    // inclusive scan of the thread sums over the wave
+    int2 inc = run;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int ux = __shfl_up(inc.x, o, kWave), uy = __shfl_up(inc.y, o, kWave);
+        if (lane >= o) {
+            inc.x += ux;
+            inc.y += uy;
+        }
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int2 before = make_int2(inc.x - run.x, inc.y - run.y);
+    total = make_int2(0, 0);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const int2 t = wsum[w];
+        if (w < wave) {
+            before.x += t.x;
+            before.y += t.y;
+        }
+        total.x += t.x;
+        total.y += t.y;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        v[e].x += before.x;
+        v[e].y += before.y;
+    }
+}
+
+__device__ __forceinline__ int chunks_of(int n) { return n > 0 ? (n + kKeyChunk - 1) / kKeyChunk : 1; }
+
+// Per block of 1024 kept-key slots: the sums of the counts and of the chunk counts.
+__global__ __launch_bounds__(256) void bwd_scan_reduce_kernel(BwdScanArgs a)
+{
+    int2 v[4];
+    const int base = blockIdx.x * 1024 + threadIdx.x * 4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int i = base + e;
+        const int c = i < a.n ? a.count[i] : 0;
+        v[e] = i < a.n ? make_int2(c, chunks_of(c)) : make_int2(0, 0);
+    }
+    int2 total;
+    block_scan_256x4(v, total);
+    if (threadIdx.x == 0) {
+        a.block_sums[2 * blockIdx.x] = total.x;
+        a.block_sums[2 * blockIdx.x + 1] = total.y;
+    }
+}
+
+// One block: exclusive scan of the block sums, in place.
+__global__ __launch_bounds__(256) void bwd_scan_blocks_kernel(BwdScanArgs a)
+{
+    int2 carry = make_int2(0, 0);
+    for (int t0 = 0; t0 < a.nblocks; t0 += 1024) {
+        int2 v[4];
+        const int base = t0 + threadIdx.x * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int i = base + e;
+            v[e] = i < a.nblocks ? make_int2(a.block_sums[2 * i], a.block_sums[2 * i + 1]) : make_int2(0, 0);
+        }
+        int2 total;
+        block_scan_256x4(v, total);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int i = base + e;
+            if (i < a.nblocks) {
+                a.block_sums[2 * i] = v[e].x + carry.x;
+                a.block_sums[2 * i + 1] = v[e].y + carry.y;
+            }
+        }
+        carry.x += total.x;
+        carry.y += total.y;
+    }
+    if (threadIdx.x == 0) {
+        a.off[a.n] = carry.x;
+        a.coff[a.n] = carry.y;
+    }
+}
+
+// Per block: the exclusive scans of the counts (list offsets) and of the chunk counts, and the
+// kept key of every chunk.
+__global__ __launch_bounds__(256) void bwd_scan_write_kernel(BwdScanArgs a)
+{
+    int2 v[4], c[4];
+    const int base = blockIdx.x * 1024 + threadIdx.x * 4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int i = base + e;
+        const int cnt = i < a.n ? a.count[i] : 0;
+        c[e] = i < a.n ? make_int2(cnt, chunks_of(cnt)) : make_int2(0, 0);
+        v[e] = c[e];
+    }
+    int2 total;
+    block_scan_256x4(v, total);
+    const int2 bo = make_int2(a.block_sums[2 * blockIdx.x], a.block_sums[2 * blockIdx.x + 1]);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int i = base + e;
+        if (i >= a.n) continue;
+        a.off[i] = bo.x + v[e].x;
+        a.coff[i] = bo.y + v[e].y;
+        for (int t = 0; t < c[e].y; ++t) a.chunk_key[bo.y + v[e].y + t] = i;
+    }
+}
+
+// Every kept (parent, rank) pair into the list of the key it kept; the counts return to zero.
+__global__ __launch_bounds__(256) void bwd_fill_kernel(BwdFillArgs a)
+{
+    const long long tid = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (tid >= a.nentries) return;
+    const int J = a.parent_idx[tid];
+    if (J < 0) return;
+    const int row = static_cast<int>(tid / a.Kp);          // bh * Np + P
+    const int r = static_cast<int>(tid - static_cast<long long>(row) * a.Kp);
+    const int bh = row / a.Np, P = row - bh * a.Np;
+    const int key = bh * a.Np + J;
+    const int pos = a.off[key] + atomicSub(a.count + key, 1) - 1;
+    a.entries[pos] = P * a.Kp + r;
+}
+
+// Key pass: one wave per chunk of one kept key J's parent list (up to kKeyChunk = 16 parents, so
+// 64 query slots s = 4e + child). It mirrors the forward's fine kernel with the roles of queries and
+// keys exchanged: the four children of J (keys) are the MFMA operand repeated over the rows, the
+// slots' query rows are gathered 16 at a time (lane 16g + n takes chunks g, g+4, ... of slot n of a
+// tile), lane s keeps tile s/16 of the products and so ends with slot s's logits and <dm, v> for
+// the four keys. The weights dx and vw go to LDS, and dk = scale * dx^T Q, then dv = vw^T dM, run on
+// the 4x4 MFMA from the slots' q rows, then their dm rows, in fp32 in one LDS buffer. Only the
+// tiles that hold parents are gathered. A key whose list spans several chunks has each chunk store
+// its partial rows, and bwd_key_reduce_kernel adds them up. (Letting the last chunk add them, with a
+// counter and device-scope fences, was ten times slower: every such fence writes back the L2.)
+struct KeyLds {
+    int rows, dx, vw, total;
+    int pitch;      // floats per row
+};
+
+template <int D>
+__host__ __device__ inline KeyLds key_lds()
+{
+    KeyLds L;
+    L.pitch = D + 4;
+    L.rows = 0;
+    L.dx = L.rows + 4 * kKeyChunk * L.pitch * 4;
+    L.vw = L.dx + 4 * kKeyChunk * 16;
+    L.total = L.vw + 4 * kKeyChunk * 16;
+    return L;
+}
+
+template <typename T, int D, bool VA, bool FINEST>
+__global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
+{
+    using S = Storage<T>;
+    constexpr bool kBf16 = sizeof(T) == 2;
+    constexpr int TB = sizeof(T);
+    constexpr int RB = D * TB;               // bytes of one head's row (storage)
+    constexpr int E = S::kPer16B;            // storage elements per 16-byte chunk
+    constexpr int NJ = RB / 64;              // storage chunks per lane and row
+    constexpr int NJF = D / 16;              // fp32 4-channel chunks per lane and row
+    constexpr int NT = 4 * kKeyChunk / 16;   // tiles of 16 slots
+    constexpr int NCG = D / 4;
+    constexpr int NH = 16 / NCG;
+    constexpr int QPL = 4 / NH;
+    static_assert(kKeyChunk == 16, "one wave holds the 64 query slots of a chunk");
+
+    const int lane = threadIdx.x & 63;
+    const int Np = a.Hp * a.Wp;
+    const int n = a.B * a.heads * Np;
+    const int chunk = __builtin_amdgcn_readfirstlane(static_cast<int>(blockIdx.x));
+    if (chunk >= a.coff[n]) return;          // whole wave
+    extern __shared__ __align__(16) unsigned char smem[];
+    const KeyLds lay = key_lds<D>();
+    float* Rs = reinterpret_cast<float*>(smem + lay.rows);    // q rows, then dm rows
+    float* dxs = reinterpret_cast<float*>(smem + lay.dx);     // [slot][4 keys]
+    float* vws = reinterpret_cast<float*>(smem + lay.vw);
+
+    const int key = a.chunk_key[chunk];      // bh * Np + J
+    const int bh = key / Np, J = key - bh * Np;
+    const int h = bh % a.heads, b = bh / a.heads;
+    const int H = a.H, W = a.W, C = a.C, N = H * W, K = a.Kp;
+    const int first = a.coff[key], nch = a.coff[key + 1] - first;
+    const int beg = a.off[key] + (chunk - first) * kKeyChunk;
+    const int nent = min(a.off[key + 1] - beg, kKeyChunk);
+    const int Jy = J / a.Wp, Jx = J - Jy * a.Wp;
+    const int n16 = lane & 15, g = lane >> 4;
+    const bool kvb = a.blocked;
+    const unsigned char* qbase = static_cast<const unsigned char*>(a.q);
+
+    // the four keys (children of J); rows n16 of the A operand hold key n16 & 3
+    bool jv[4];
+    int jtok[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int y = 2 * Jy + (c >> 1), x = 2 * Jx + (c & 1);
+        jv[c] = y < H && x < W;
+        jtok[c] = jv[c] ? y * W + x : 0;
+    }
+    const int kc = n16 & 3;
+    const bool kc_ok = kc == 0 ? jv[0] : kc == 1 ? jv[1] : kc == 2 ? jv[2] : jv[3];
+    const int kc_tok = kc == 0 ? jtok[0] : kc == 1 ? jtok[1] : kc == 2 ? jtok[2] : jtok[3];
+    const size_t krow = kvb ? (static_cast<size_t>(key) * 4 + kc) * RB
+                            : ((static_cast<size_t>(b) * N + kc_tok) * C + h * D) * TB;
+    uint4 kA[NJ], vA[NJ];
+    float vAf[NJF][4];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const uint4 kr = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.k) + krow + (g + 4 * j) * 16);
+        const uint4 vr = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.v) + krow + (g + 4 * j) * 16);
+        kA[j] = kc_ok ? kr : make_uint4(0, 0, 0, 0);
+        vA[j] = kc_ok ? vr : make_uint4(0, 0, 0, 0);
+    }
+    if constexpr (!FINEST) {
+        // V in 4-channel chunks g, g+4, ... to meet the fp32 dm rows channel for channel
+#pragma unroll
+        for (int j = 0; j < NJF; ++j) {
+            const int c0 = (g + 4 * j) * 4;
+            if constexpr (kBf16) {
+                const uint2 vr = *reinterpret_cast<const uint2*>(static_cast<const unsigned char*>(a.v) + krow + c0 * 2);
+                vAf[j][0] = bf16_bits_to_f32(vr.x & 0xFFFFu);
+                vAf[j][1] = bf16_bits_to_f32(vr.x >> 16);
+                vAf[j][2] = bf16_bits_to_f32(vr.y & 0xFFFFu);
+                vAf[j][3] = bf16_bits_to_f32(vr.y >> 16);
+            } else {
+                const float4 vr = *reinterpret_cast<const float4*>(static_cast<const unsigned char*>(a.v) + krow + c0 * 4);
+                vAf[j][0] = vr.x;
+                vAf[j][1] = vr.y;
+                vAf[j][2] = vr.z;
+                vAf[j][3] = vr.w;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) vAf[j][e] = kc_ok ? vAf[j][e] : 0.f;
+        }
+    }
+
+    // the chunk's parents: lane e < nent holds entry e
+    const int ent_lane = nent > 0 ? a.entries[beg + min(lane, nent - 1)] : 0;   // an empty list reads nothing
+    // where slot s's query lives: entry s >> 2, child s & 3
+    auto slot_query = [&](int s, int ent, int& P, int& r, int& qtok, bool& qv) {
+        P = ent / K;
+        r = ent - P * K;
+        const int Py = P / a.Wp, Px = P - Py * a.Wp;
+        const int qi = s & 3;
+        const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
+        qv = (s >> 2) < nent && qy < H && qx < W;
+        qtok = min(qy, H - 1) * W + min(qx, W - 1);
+    };
+
+    const int ntile = (nent + 3) / 4;                         // tiles that hold parents
+    const int nsp = 16 * ntile;
+    float acc_x[4] = {0.f, 0.f, 0.f, 0.f}, acc_g[4] = {0.f, 0.f, 0.f, 0.f};
+    // each tile's dm chunks (level 0: w_0 dout), kept for dv
+    float mreg[NT][FINEST ? NJ * E : NJF * 4];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        if (t >= ntile) break;                                // uniform
+        const int s = 16 * t + n16;
+        const int ent = __shfl(ent_lane, s >> 2, kWave);
+        int P, r, qtok;
+        bool qv;
+        slot_query(s, ent, P, r, qtok, qv);
+        const size_t qrow = kvb ? ((static_cast<size_t>(bh) * Np + P) * 4 + (s & 3)) * RB
+                                : ((static_cast<size_t>(b) * N + qtok) * C + h * D) * TB;
+        const size_t grow = (static_cast<size_t>(b) * N + qtok) * C + h * D;      // elements
+        uint4 qB[NJ];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const uint4 raw = *reinterpret_cast<const uint4*>(qbase + qrow + (g + 4 * j) * 16);
+            qB[j] = qv ? raw : make_uint4(0, 0, 0, 0);
+        }
+        float w0 = 1.0f;
+        if constexpr (FINEST && !VA)
+            w0 = a.w ? a.w[((static_cast<size_t>(b) * N + qtok) * a.heads + h) * a.levels] : 1.0f / a.levels;
+        float4_t ax = {0.f, 0.f, 0.f, 0.f}, ag = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            if constexpr (kBf16) {
+                ax = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kA[j]),
+                                                             __builtin_bit_cast(bf16x8_t, qB[j]), ax, 0, 0, 0);
+            } else {
+                ax = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kA[j].x), __uint_as_float(qB[j].x), ax, 0, 0, 0);
+                ax = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kA[j].y), __uint_as_float(qB[j].y), ax, 0, 0, 0);
+                ax = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kA[j].z), __uint_as_float(qB[j].z), ax, 0, 0, 0);
+                ax = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kA[j].w), __uint_as_float(qB[j].w), ax, 0, 0, 0);
+            }
+            // the query row in fp32 for dk
+            float qf[E];
+            S::unpack(qB[j], qf);
+            float* qd = Rs + s * lay.pitch + (g + 4 * j) * E;
+#pragma unroll
+            for (int e4 = 0; e4 < E; e4 += 4)
+                *reinterpret_cast<float4*>(qd + e4) = make_float4(qf[e4], qf[e4 + 1], qf[e4 + 2], qf[e4 + 3]);
+        }
+        if constexpr (FINEST) {
+            // <dout, v> on the storage type (times w_0 below), and w_0 dout in fp32 for dv
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const uint4 raw = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.dout) +
+                                                                  (grow + (g + 4 * j) * E) * TB);
+                const uint4 dd = qv ? raw : make_uint4(0, 0, 0, 0);
+                if constexpr (kBf16) {
+                    ag = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vA[j]),
+                                                                 __builtin_bit_cast(bf16x8_t, dd), ag, 0, 0, 0);
+                } else {
+                    ag = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vA[j].x), __uint_as_float(dd.x), ag, 0, 0, 0);
+                    ag = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vA[j].y), __uint_as_float(dd.y), ag, 0, 0, 0);
+                    ag = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vA[j].z), __uint_as_float(dd.z), ag, 0, 0, 0);
+                    ag = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vA[j].w), __uint_as_float(dd.w), ag, 0, 0, 0);
+                }
+                float gf[E];
+                S::unpack(dd, gf);
+#pragma unroll
+                for (int e = 0; e < E; ++e) mreg[t][j * E + e] = w0 * gf[e];
+            }
+        } else {
+            // <dm, v> with dm in fp32, 4-channel chunks g, g+4, ...
+#pragma unroll
+            for (int j = 0; j < NJF; ++j) {
+                const float4 raw = *reinterpret_cast<const float4*>(a.dm + grow + (g + 4 * j) * 4);
+                const float4 dm4 = qv ? raw : make_float4(0.f, 0.f, 0.f, 0.f);
+                ag = __builtin_amdgcn_mfma_f32_16x16x4f32(vAf[j][0], dm4.x, ag, 0, 0, 0);
+                ag = __builtin_amdgcn_mfma_f32_16x16x4f32(vAf[j][1], dm4.y, ag, 0, 0, 0);
+                ag = __builtin_amdgcn_mfma_f32_16x16x4f32(vAf[j][2], dm4.z, ag, 0, 0, 0);
+                ag = __builtin_amdgcn_mfma_f32_16x16x4f32(vAf[j][3], dm4.w, ag, 0, 0, 0);
+                mreg[t][4 * j] = dm4.x;
+                mreg[t][4 * j + 1] = dm4.y;
+                mreg[t][4 * j + 2] = dm4.z;
+                mreg[t][4 * j + 3] = dm4.w;
+            }
+        }
+        // rows 4g + c of the products are key c for every g: lane 16g + n keeps tile g
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            acc_x[c] = g == t ? ax[c] : acc_x[c];
+            acc_g[c] = g == t ? ag[c] : acc_g[c];
+        }
+    }
+
+    // ---- slot `lane`: its query's statistics and the weights of the four keys ----
+    {
+        const int s = lane;
+        int P, r, qtok;
+        bool qv;
+        slot_query(s, __shfl(ent_lane, s >> 2, kWave), P, r, qtok, qv);
+        const size_t qrow = static_cast<size_t>(bh) * N + qtok;
+        const float2 st = VA ? *reinterpret_cast<const float2*>(a.stats + (qrow * K + r) * 2)
+                             : *reinterpret_cast<const float2*>(a.stats + qrow * 2);
+        const float sigma = VA ? a.parent_key[(static_cast<size_t>(bh) * Np + P) * K + r] : 1.0f;
+        float w0 = 1.0f;
+        if constexpr (FINEST && !VA)
+            w0 = a.w ? a.w[((static_cast<size_t>(b) * N + qtok) * a.heads + h) * a.levels] : 1.0f / a.levels;
+        float dx[4], vw[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const bool valid = qv && jv[c];
+            const float pr = valid ? __expf(acc_x[c] * a.scale - st.x) : 0.f;   // B: p; A: t
+            const float gsv = FINEST ? w0 * acc_g[c] : acc_g[c];
+            if constexpr (!VA) {
+                dx[c] = pr * (gsv - st.y);
+                vw[c] = pr;
+            } else {
+                const float sc = sigma * pr;
+                float ds = gsv;
+                bool kept = false;
+                if constexpr (!FINEST) {
+                    const size_t srow = qrow * a.Ks;
+                    for (int mm = 0; mm < a.Ks; ++mm)
+                        if (valid && a.sel_idx[srow + mm] == jtok[c]) {
+                            kept = true;
+                            ds = a.dsig_in[srow + mm];
+                        }
+                }
+                dx[c] = sc * (ds - st.y);
+                vw[c] = kept ? 0.f : sc;
+            }
+        }
+        *reinterpret_cast<float4*>(dxs + s * 4) = make_float4(dx[0], dx[1], dx[2], dx[3]);
+        *reinterpret_cast<float4*>(vws + s * 4) = make_float4(vw[0], vw[1], vw[2], vw[3]);
+    }
+    wave_lds_sync();
+
+    // ---- dk = dx^T Q, then dv = vw^T dM, on the 4x4 MFMA (blocks over 4-channel groups, slot halves) ----
+    const int blk = lane >> 2, t4 = lane & 3;
+    const int cg = blk / NH, hh = blk % NH;
+    const int ch = 4 * cg + t4;
+    const int sph = nsp / NH;
+    float4_t ok_ = {0.f, 0.f, 0.f, 0.f}, ov = {0.f, 0.f, 0.f, 0.f};
+    for (int st = 0; st < sph; ++st) {
+        const int sl = hh * sph + st;
+        ok_ = __builtin_amdgcn_mfma_f32_4x4x1f32(dxs[sl * 4 + t4], Rs[sl * lay.pitch + ch], ok_, 0, 0, 0);
+    }
+    wave_lds_sync();
+    // the dm rows into the same buffer (lane 16g + n holds slot 16t + n's chunks g, g+4, ...)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        if (t >= ntile) break;                                // uniform
+        const int s = 16 * t + n16;
+        if constexpr (FINEST) {
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                float* md = Rs + s * lay.pitch + (g + 4 * j) * E;
+#pragma unroll
+                for (int e4 = 0; e4 < E; e4 += 4)
+                    *reinterpret_cast<float4*>(md + e4) = make_float4(mreg[t][j * E + e4], mreg[t][j * E + e4 + 1],
+                                                                      mreg[t][j * E + e4 + 2], mreg[t][j * E + e4 + 3]);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < NJF; ++j)
+                *reinterpret_cast<float4*>(Rs + s * lay.pitch + (g + 4 * j) * 4) =
+                    make_float4(mreg[t][4 * j], mreg[t][4 * j + 1], mreg[t][4 * j + 2], mreg[t][4 * j + 3]);
+        }
+    }
+    wave_lds_sync();
+    for (int st = 0; st < sph; ++st) {
+        const int sl = hh * sph + st;
+        ov = __builtin_amdgcn_mfma_f32_4x4x1f32(vws[sl * 4 + t4], Rs[sl * lay.pitch + ch], ov, 0, 0, 0);
+    }
+    if constexpr (NH == 2) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            ok_[c] += xchg_f32<4>(ok_[c]);
+            ov[c] += xchg_f32<4>(ov[c]);
+        }
+    }
+    if (nch > 1) {
+        // this chunk's rows; bwd_key_reduce_kernel adds up the key's chunks
+#pragma unroll
+        for (int u = 0; u < QPL; ++u) {
+            const int c = (NH == 2 ? hh * QPL : 0) + u;
+            float* pk = a.partial + ((static_cast<size_t>(chunk) * 4 + c) * 2) * D + ch;
+            pk[0] = pick4(ok_, c);
+            pk[D] = pick4(ov, c);
+        }
+        return;
+    }
+#pragma unroll
+    for (int u = 0; u < QPL; ++u) {
+        const int c = (NH == 2 ? hh * QPL : 0) + u;
+        const bool cv = c == 0 ? jv[0] : c == 1 ? jv[1] : c == 2 ? jv[2] : jv[3];
+        const int ct = c == 0 ? jtok[0] : c == 1 ? jtok[1] : c == 2 ? jtok[2] : jtok[3];
+        if (!cv) continue;
+        const size_t row = (static_cast<size_t>(b) * N + ct) * C + h * D + ch;
+        a.dk[row] = a.scale * pick4(ok_, c);
+        a.dv[row] = pick4(ov, c);
+    }
+}
+
+// Keys whose list spans several chunks: the sum of the chunks' partial rows. One thread per
+// (kept-key slot, child, 4 channels).
+__global__ __launch_bounds__(256) void bwd_key_reduce_kernel(BwdLevelArgs a, int d)
+{
+    const int Np = a.Hp * a.Wp;
+    const long long n = static_cast<long long>(a.B) * a.heads * Np;
+    const int q4n = d / 4;
+    const long long tid = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (tid >= n * 4 * q4n) return;
+    const int qd = static_cast<int>(tid % q4n);
+    const int c = static_cast<int>((tid / q4n) % 4);
+    const int key = static_cast<int>(tid / (4LL * q4n));
+    const int first = a.coff[key], nch = a.coff[key + 1] - first;
+    if (nch <= 1) return;
+    const int bh = key / Np, J = key - bh * Np;
+    const int h = bh % a.heads, b = bh / a.heads;
+    const int Jy = J / a.Wp, Jx = J - Jy * a.Wp;
+    const int y = 2 * Jy + (c >> 1), x = 2 * Jx + (c & 1);
+    if (y >= a.H || x >= a.W) return;
+    float4 sk = make_float4(0.f, 0.f, 0.f, 0.f), sv = sk;
+    for (int t = 0; t < nch; ++t) {
+        const float* pk = a.partial + ((static_cast<size_t>(first + t) * 4 + c) * 2) * d + 4 * qd;
+        const float4 k4 = *reinterpret_cast<const float4*>(pk);
+        const float4 v4 = *reinterpret_cast<const float4*>(pk + d);
+        sk.x += k4.x; sk.y += k4.y; sk.z += k4.z; sk.w += k4.w;
+        sv.x += v4.x; sv.y += v4.y; sv.z += v4.z; sv.w += v4.w;
+    }
+    const size_t row = (static_cast<size_t>(b) * a.H * a.W + y * a.W + x) * a.C + h * d + 4 * qd;
+    *reinterpret_cast<float4*>(a.dk + row) = make_float4(a.scale * sk.x, a.scale * sk.y, a.scale * sk.z, a.scale * sk.w);
+    *reinterpret_cast<float4*>(a.dv + row) = sv;
+}
+
+template <typename T, int D, bool VA, bool FINEST>
+hipError_t launch_key_tdv(const BwdLevelArgs& a, long long max_chunks, hipStream_t stream)
+{
+    if (max_chunks >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    const size_t lds = key_lds<D>().total;
+    if (lds > device_max_lds()) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((bwd_key_kernel<T, D, VA, FINEST>), dim3(static_cast<unsigned>(max_chunks)), dim3(kWave), lds,
+                       stream, a);
+    return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t launch_key_td(const BwdLevelArgs& a, bool variant_a, bool finest, long long max_chunks, hipStream_t stream)
+{
+    if (variant_a)
+        return finest ? launch_key_tdv<T, D, true, true>(a, max_chunks, stream)
+                      : launch_key_tdv<T, D, true, false>(a, max_chunks, stream);
+    return finest ? launch_key_tdv<T, D, false, true>(a, max_chunks, stream)
+                  : launch_key_tdv<T, D, false, false>(a, max_chunks, stream);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -824,18 +1287,6 @@ hipError_t launch_fill_zero(const FillRange* r, int n, hipStream_t stream)
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_combine(const BwdCombineArgs& a, bool use_bf16, hipStream_t stream)
-{
-    const long long total = static_cast<long long>(a.B) * a.H[1] * a.W[1] * a.C;
-    const long long blocks = (total + 255) / 256;
-    if (blocks >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    if (use_bf16)
-        hipLaunchKernelGGL(bwd_combine_kernel<bf16>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, a);
-    else
-        hipLaunchKernelGGL(bwd_combine_kernel<float>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, a);
-    return hipGetLastError();
-}
-
 hipError_t launch_bwd_level(const BwdLevelArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
                             hipStream_t stream)
 {
@@ -850,6 +1301,40 @@ hipError_t launch_bwd_level(const BwdLevelArgs& a, int d, bool variant_a, bool u
         if (d == 64) return launch_level_td<float, 64>(b, variant_a, finest, stream);
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_bwd_keys(const BwdLevelArgs& a, const BwdScanArgs& sc, int d, bool variant_a, bool use_bf16,
+                           bool finest, hipStream_t stream)
+{
+    if (sc.n <= 0) return hipErrorInvalidValue;
+    const unsigned nb = static_cast<unsigned>(sc.nblocks);
+    hipLaunchKernelGGL(bwd_scan_reduce_kernel, dim3(nb), dim3(256), 0, stream, sc);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(bwd_scan_blocks_kernel, dim3(1), dim3(256), 0, stream, sc);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(bwd_scan_write_kernel, dim3(nb), dim3(256), 0, stream, sc);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    BwdFillArgs f{a.parent_idx, static_cast<long long>(sc.n) * a.Kp, a.Kp, a.Hp * a.Wp, sc.count, sc.off, a.entries};
+    const long long fb = (f.nentries + 255) / 256;
+    if (fb >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(bwd_fill_kernel, dim3(static_cast<unsigned>(fb)), dim3(256), 0, stream, f);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const long long max_chunks = static_cast<long long>(sc.n) + (static_cast<long long>(sc.n) * a.Kp + kKeyChunk - 1) / kKeyChunk;
+    if (use_bf16) {
+        if (d == 32) e = launch_key_td<bf16, 32>(a, variant_a, finest, max_chunks, stream);
+        else if (d == 64) e = launch_key_td<bf16, 64>(a, variant_a, finest, max_chunks, stream);
+        else return hipErrorInvalidValue;
+    } else {
+        if (d == 32) e = launch_key_td<float, 32>(a, variant_a, finest, max_chunks, stream);
+        else if (d == 64) e = launch_key_td<float, 64>(a, variant_a, finest, max_chunks, stream);
+        else return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
+    const long long rb = (static_cast<long long>(sc.n) * 4 * (d / 4) + 255) / 256;
+    if (rb >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(bwd_key_reduce_kernel, dim3(static_cast<unsigned>(rb)), dim3(256), 0, stream, a, d);
+    return hipGetLastError();
 }
 
 hipError_t launch_bwd_coarse(const BwdCoarseArgs& a, int d, bool variant_a, bool use_bf16, hipStream_t stream)

@@ -194,44 +194,56 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], in
 
 // Workspace of the backward pass: per level l >= 1 the gradient of the message (dm) and the
 // level's q, k, v gradients (fp32 [B][N_l][C]); QuadTree-A's gradients of the kept scores
-// ([B][heads][N_l][K_l]); the coarse softmax statistics ([B][heads][N_c][4]). The buffers that
-// are accumulated with atomics (dm at levels >= 2, the k and v gradients of levels 1..L-2) form
-// one contiguous region, cleared at the start of every call.
+// ([B][heads][N_l][K_l]); the coarse softmax statistics ([B][heads][N_c][4]); and, reused level by
+// level, the finer levels' query statistics and the counting sort of the kept pairs (counts, list
+// and chunk offsets, block sums, lists, chunk keys, per-chunk partial rows). What is summed with
+// atomics (dm at levels >= 2, the counts) forms one contiguous region, cleared at the start of
+// every call; the counts return to zero after each level's sort.
 struct BwdLayout {
     size_t dm[QTA_MAX_LEVELS], gq[QTA_MAX_LEVELS], gk[QTA_MAX_LEVELS], gv[QTA_MAX_LEVELS];
     size_t dsig[QTA_MAX_LEVELS];
     size_t zero_begin, zero_end;
     size_t stats, total;
+    size_t count, off, coff, block_sums, entries, chunk_key, partial, qstats;
+    long long nslots_max;           // B*heads*N_{l+1} over the finer levels
 };
 
-void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int levels, const int* Kl, bool va,
+void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int d, int levels, const int* Kl, bool va,
                 BwdLayout* L)
 {
     *L = BwdLayout{};
     const int c = levels - 1;
     auto fbytes = [&](int l) { return static_cast<size_t>(B) * Hl[l] * Wl[l] * C * sizeof(float); };
+    long long nmax = 0, emax = 0, cmax = 0, smax = 0;
+    for (int l = 0; l < c; ++l) {
+        const long long n = static_cast<long long>(B) * heads * Hl[l + 1] * Wl[l + 1];
+        const long long e = n * Kl[l + 1];
+        const long long ch = n + (e + kKeyChunk - 1) / kKeyChunk;
+        const long long st = static_cast<long long>(B) * heads * Hl[l] * Wl[l] * 2 * (va ? Kl[l + 1] : 1);
+        nmax = n > nmax ? n : nmax;
+        emax = e > emax ? e : emax;
+        cmax = ch > cmax ? ch : cmax;
+        smax = st > smax ? st : smax;
+    }
+    L->nslots_max = nmax;
     size_t off = 0;
     L->zero_begin = off;
     for (int l = 2; l <= c; ++l) {
         L->dm[l] = off;
         off = align_up(off + fbytes(l));
     }
-    for (int l = 1; l < c; ++l) {
-        L->gk[l] = off;
-        off = align_up(off + fbytes(l));
-        L->gv[l] = off;
-        off = align_up(off + fbytes(l));
-    }
+    L->count = off;
+    off = align_up(off + static_cast<size_t>(nmax) * sizeof(int32_t));
     L->zero_end = off;
     if (c >= 1) {
         L->dm[1] = off;
         off = align_up(off + fbytes(1));
-        L->gk[c] = off;
-        off = align_up(off + fbytes(c));
-        L->gv[c] = off;
-        off = align_up(off + fbytes(c));
     }
     for (int l = 1; l <= c; ++l) {
+        L->gk[l] = off;
+        off = align_up(off + fbytes(l));
+        L->gv[l] = off;
+        off = align_up(off + fbytes(l));
         L->gq[l] = off;
         off = align_up(off + fbytes(l));
         if (va) {
@@ -241,6 +253,22 @@ void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int level
     }
     L->stats = off;
     off = align_up(off + static_cast<size_t>(B) * heads * Hl[c] * Wl[c] * 4 * sizeof(float));
+    if (c >= 1) {
+        L->off = off;
+        off = align_up(off + static_cast<size_t>(nmax + 1) * sizeof(int32_t));
+        L->coff = off;
+        off = align_up(off + static_cast<size_t>(nmax + 1) * sizeof(int32_t));
+        L->block_sums = off;
+        off = align_up(off + static_cast<size_t>(2 * ((nmax + 1023) / 1024)) * sizeof(int32_t));
+        L->entries = off;
+        off = align_up(off + static_cast<size_t>(emax) * sizeof(int32_t));
+        L->chunk_key = off;
+        off = align_up(off + static_cast<size_t>(cmax) * sizeof(int32_t));
+        L->partial = off;
+        off = align_up(off + static_cast<size_t>(cmax) * 8 * d * sizeof(float));
+        L->qstats = off;
+        off = align_up(off + static_cast<size_t>(smax) * sizeof(float));
+    }
     L->total = off;
 }
 
@@ -656,7 +684,7 @@ size_t qta_backward_workspace_bytes_ex(int B, int heads, int H, int W, int d, in
     if (layout(B, heads, H, W, d, levels, o.Kl, o.v_levels != nullptr, o.pe_weight != nullptr, dtype, &L) != QTA_OK)
         return 0;
     BwdLayout G;
-    bwd_layout(B, heads, L.H, L.W, heads * d, levels, o.Kl, variant == QTA_VARIANT_A, &G);
+    bwd_layout(B, heads, L.H, L.W, heads * d, d, levels, o.Kl, variant == QTA_VARIANT_A, &G);
     return G.total;
 }
 
@@ -696,7 +724,8 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     const bool va = variant == QTA_VARIANT_A;
     const int C = heads * d;
     BwdLayout G;
-    bwd_layout(B, heads, L.H, L.W, C, levels, Kl, va, &G);
+    bwd_layout(B, heads, L.H, L.W, C, d, levels, Kl, va, &G);
+    if (G.nslots_max >= 0x7FFFFFFFLL / 64) return QTA_ERR_UNSUPPORTED;     // sort indices are int
     if (!bwd_workspace || (reinterpret_cast<uintptr_t>(bwd_workspace) & (kAlign - 1)) != 0) return QTA_ERR_INVALID;
     if (bwd_workspace_bytes < G.total) return QTA_ERR_WORKSPACE;
     float* dw_out = (!va && w) ? dw : nullptr;
@@ -713,33 +742,12 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     if (only_finest && levels < 2) return QTA_ERR_INVALID;
 
     if (levels > 1 && !only_finest) {
-        // clear what is accumulated: dm of levels >= 2, the k and v gradients of levels 0..L-2
-        FillRange r[3];
+        // clear what is accumulated: dm of levels >= 2 and the kept-by counts
+        FillRange r[1];
         r[0] = FillRange{fptr(G.zero_begin), (G.zero_end - G.zero_begin) / sizeof(float)};
-        r[1] = FillRange{dk, static_cast<size_t>(B) * H * W * C};
-        r[2] = FillRange{dv, static_cast<size_t>(B) * H * W * C};
-        if (launch_fill_zero(r, 3, s) != hipSuccess) return QTA_ERR_HIP;
+        if (launch_fill_zero(r, 1, s) != hipSuccess) return QTA_ERR_HIP;
 
-        // 1. combination
-        BwdCombineArgs cb{};
-        cb.dout = dout;
-        cb.w = va ? nullptr : w;
-        cb.variant_b = va ? 0 : 1;
-        cb.B = B;
-        cb.heads = heads;
-        cb.d = d;
-        cb.C = C;
-        cb.L = levels;
-        for (int l = 0; l < levels; ++l) {
-            cb.H[l] = L.H[l];
-            cb.W[l] = L.W[l];
-            if (l >= 1) {
-                cb.msg[l] = reinterpret_cast<const float*>(ws + L.msg[l]);
-                cb.dm[l] = fptr(G.dm[l]);
-            }
-        }
-        cb.dw = dw_out;
-        if (launch_bwd_combine(cb, use_bf16, s) != hipSuccess) return QTA_ERR_HIP;
+
     }
     if (levels > 1) {
         // 2. finer levels, finest first (QuadTree-A's score gradients go up one level each)
@@ -756,6 +764,12 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
                 a.dk = dk;
                 a.dv = dv;
                 a.dw = dw_out;
+                for (int j = 1; j < levels; ++j) {      // 1. the combination's backward
+                    a.dm_out[j] = fptr(G.dm[j]);
+                    a.msg_fwd[j] = reinterpret_cast<const float*>(ws + L.msg[j]);
+                    a.lvl_W[j] = L.W[j];
+                    a.lvl_N[j] = L.H[j] * L.W[j];
+                }
             } else {
                 a.q = ws + L.q[l];
                 a.k = ws + L.k[l];
@@ -782,7 +796,23 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
             a.parent_key = skey(l + 1);
             a.dsig_out = va ? fptr(G.dsig[l + 1]) : nullptr;
             a.levels = levels;
+            a.stats = fptr(G.qstats);
+            a.count = reinterpret_cast<int32_t*>(gws + G.count);
+            a.off = reinterpret_cast<const int32_t*>(gws + G.off);
+            a.coff = reinterpret_cast<const int32_t*>(gws + G.coff);
+            a.chunk_key = reinterpret_cast<const int32_t*>(gws + G.chunk_key);
+            a.entries = reinterpret_cast<int32_t*>(gws + G.entries);
+            a.partial = fptr(G.partial);
             if (launch_bwd_level(a, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
+            BwdScanArgs sc{};
+            sc.n = B * heads * L.H[l + 1] * L.W[l + 1];
+            sc.nblocks = (sc.n + 1023) / 1024;
+            sc.count = a.count;
+            sc.off = reinterpret_cast<int32_t*>(gws + G.off);
+            sc.coff = reinterpret_cast<int32_t*>(gws + G.coff);
+            sc.chunk_key = reinterpret_cast<int32_t*>(gws + G.chunk_key);
+            sc.block_sums = reinterpret_cast<int32_t*>(gws + G.block_sums);
+            if (launch_bwd_keys(a, sc, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
         }
     }
     if (only_finest) return QTA_OK;

@@ -142,21 +142,13 @@ struct PosEncArgs {
 
 // ---- backward pass (gradients with the kept-key sets held fixed) ----
 
-// dLoss/dm^l of every level l >= 1 from the upstream gradient: dm^l at a level-l token sums
-// w_{i,l} dout_i over its finest descendants i (w = 1 for QuadTree-A); and dw_{i,l} = <dout_i, m^l
-// of i's ancestor> for l >= 1. One thread per (batch, level-1 token, channel).
-struct BwdCombineArgs {
-    const void* dout;           // [B][N0][C] storage type
-    const float* w;             // QuadTree-B: [B][N0][heads][L] or NULL (1/L); NULL for A
-    int variant_b;
-    int B, heads, d, C, L;
-    int H[QTA_MAX_LEVELS], W[QTA_MAX_LEVELS];
-    const float* msg[QTA_MAX_LEVELS];   // forward messages of levels >= 1 (for dw)
-    float* dm[QTA_MAX_LEVELS];          // level 1 written, levels >= 2 accumulated (zeroed first)
-    float* dw;                          // QuadTree-B with w: entries l >= 1 written; or NULL
-};
+// Backward of one finer level l (0 <= l < L-1), in two passes. Query pass: one wave per (parent
+// query at l+1, head): dq, each query's softmax statistics, QuadTree-A's parent-score gradients and
+// dw_0, and for every key of level l+1 the number of parents that kept it. Key pass: the kept
+// (parent, rank) pairs sorted by key, then one wave per chunk of one key's list: dk and dv of the
+// key's four children at level l, each row written once.
+constexpr int kKeyChunk = 16;       // parents per key-pass chunk
 
-// Backward of one finer level l (0 <= l < L-1): one wave per (parent query at l+1, head).
 struct BwdLevelArgs {
     const void* q;
     const void* k;
@@ -177,9 +169,41 @@ struct BwdLevelArgs {
     const float* w;             // l == 0, QuadTree-B: [B][N][heads][L] or NULL (1/L)
     int levels;
     float* dq;                  // fp32 [B][N][C], written
-    float* dk;                  // fp32 [B][N][C], accumulated with atomics
+    float* dk;                  // fp32 [B][N][C], written by the key pass
     float* dv;
     float* dw;                  // l == 0, QuadTree-B with w: entry 0 written; or NULL
+    float* stats;               // B: [B][heads][N][2] (log-sum-exp, sum p ds); A: [B][heads][N][Kp][2]
+    int32_t* count;             // [B*heads*Np] parents that kept each key (zero before the query pass;
+                                //   the fill returns it to zero)
+    const int32_t* off;         // [B*heads*Np + 1] start of each key's list in `entries`
+    const int32_t* coff;        // [B*heads*Np + 1] first chunk of each key; coff[B*heads*Np] = chunks
+    const int32_t* chunk_key;   // [chunks] the key (b*heads + h)*Np + J of each chunk
+    int32_t* entries;           // [B*heads*Np*Kp] P*Kp + r of every kept pair, grouped by key
+    float* partial;             // [chunks][4][2][d] per-chunk sums of keys with several chunks
+    // l == 0: the combination's backward for the coarser levels j >= 1
+    float* dm_out[QTA_MAX_LEVELS];          // dLoss/dm^j: j = 1 written, j >= 2 accumulated (zeroed first)
+    const float* msg_fwd[QTA_MAX_LEVELS];   // the forward's messages m^j (for dw)
+    int lvl_W[QTA_MAX_LEVELS];
+    int lvl_N[QTA_MAX_LEVELS];
+};
+
+// Scans of the kept-by counts of one level (n = B*heads*Np key slots, blocks of 1024).
+struct BwdScanArgs {
+    int n, nblocks;
+    int32_t* count;
+    int32_t* off;
+    int32_t* coff;
+    int32_t* chunk_key;
+    int32_t* block_sums;        // [2 * nblocks]
+};
+
+struct BwdFillArgs {
+    const int32_t* parent_idx;  // [n][Kp]
+    long long nentries;         // n * Kp
+    int Kp, Np;
+    int32_t* count;
+    const int32_t* off;
+    int32_t* entries;
 };
 
 // Backward of the coarsest level (Eq. 1 over all N keys), in two passes: per query (dq and the
@@ -251,9 +275,10 @@ hipError_t launch_fine_attn_wide(const FineArgs& a, int d, bool variant_a, bool 
                                  hipStream_t stream);
 hipError_t launch_topk(const TopkArgs& a, hipStream_t stream);
 hipError_t launch_fill_zero(const FillRange* r, int n, hipStream_t stream);
-hipError_t launch_bwd_combine(const BwdCombineArgs& a, bool use_bf16, hipStream_t stream);
 hipError_t launch_bwd_level(const BwdLevelArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
                             hipStream_t stream);
+hipError_t launch_bwd_keys(const BwdLevelArgs& a, const BwdScanArgs& sc, int d, bool variant_a, bool use_bf16,
+                           bool finest, hipStream_t stream);
 hipError_t launch_bwd_coarse(const BwdCoarseArgs& a, int d, bool variant_a, bool use_bf16, hipStream_t stream);
 hipError_t launch_bwd_unpool(const BwdUnpoolArgs& a, hipStream_t stream);
 
