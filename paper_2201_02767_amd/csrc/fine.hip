@@ -1,7 +1,8 @@
-// Gathered fine attention at the finer levels: one wave per (parent query, head) work item; the
-// per-item work (gather, MFMA logits, softmax, top-K, messages, the finest level's combination) is
-// fine_item in fine_item.h. A workgroup holds four independent waves; nothing synchronises across
-// waves. Candidate sets of more than 64 slots run the kernel of fine_wide.hip.
+// Gathered fine attention at the finer levels: one wave per (parent query, head) work item, or per
+// pair of neighbouring parents on maps of one row; the per-item work (gather, MFMA logits, softmax,
+// top-K, messages, the finest level's combination) is fine_item in fine_item.h. A workgroup holds
+// four independent waves; nothing synchronises across waves. Candidate sets of more than 64 slots
+// run the kernel of fine_wide.hip.
 #include "fine_item.h"
 
 namespace qta {
@@ -10,21 +11,22 @@ namespace {
 
 using namespace fine;
 
-template <typename T, int D, int NSP, bool VA, bool FINEST>
+template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW>
 __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
 {
     const int wave = threadIdx.x >> 6;
     const int wpb = blockDim.x >> 6;
-    const long long nitems = static_cast<long long>(a.B) * a.heads * a.Hp * a.Wp;
+    const int np = a.Hp * a.Wp;
+    const long long nitems = static_cast<long long>(a.B) * a.heads * (ROW ? (np + 1) / 2 : np);
     // the work item is the same for the whole wave: keep it (and all that derives from it) scalar
     const int item = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, gridDim.x) * wpb + wave);
     if (item >= nitems) return;            // whole wave leaves; only wave-level syncs follow
     extern __shared__ __align__(16) unsigned char smem[];
     const int nsp = (4 * a.Kp + 15) & ~15;
-    fine_item<T, D, NSP, VA, FINEST>(a, item, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
+    fine_item<T, D, NSP, VA, FINEST, ROW>(a, item, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
 }
 
-template <typename T, int D, int NSP, bool VA, bool FINEST>
+template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW>
 hipError_t launch_one(const FineArgs& a, hipStream_t stream)
 {
     const int nsp = (4 * a.Kp + 15) & ~15;
@@ -33,27 +35,36 @@ hipError_t launch_one(const FineArgs& a, hipStream_t stream)
     if (wpb * wave_bytes > device_max_lds()) return hipErrorInvalidValue;
     static bool configured = false;
     if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, NSP, VA, FINEST>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, NSP, VA, FINEST, ROW>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            static_cast<int>(device_max_lds()));
         if (e != hipSuccess) return e;
         configured = true;
     }
-    const long long items = static_cast<long long>(a.B) * a.heads * a.Hp * a.Wp;
+    const long long np = static_cast<long long>(a.Hp) * a.Wp;
+    const long long items = static_cast<long long>(a.B) * a.heads * (ROW ? (np + 1) / 2 : np);
     const long long blocks = (items + wpb - 1) / wpb;
     if (blocks * wpb >= 0x7FFFFFFFLL) return hipErrorInvalidValue;     // work items are int
-    hipLaunchKernelGGL((fine_attn_kernel<T, D, NSP, VA, FINEST>), dim3(static_cast<unsigned>(blocks)),
+    hipLaunchKernelGGL((fine_attn_kernel<T, D, NSP, VA, FINEST, ROW>), dim3(static_cast<unsigned>(blocks)),
                        dim3(wpb * kWave), wpb * wave_bytes, stream, a);
     return hipGetLastError();
 }
 
+template <typename T, int D, bool VA, bool FINEST, bool ROW>
+hipError_t launch_nsp_row(const FineArgs& a, hipStream_t stream)
+{
+    const int nslot = 4 * a.Kp;
+    if (nslot <= 16) return launch_one<T, D, 16, VA, FINEST, ROW>(a, stream);
+    if (nslot <= 32) return launch_one<T, D, 32, VA, FINEST, ROW>(a, stream);
+    return launch_one<T, D, 64, VA, FINEST, ROW>(a, stream);
+}
+
+// Maps of one row (attention along epipolar lines) pack two parents into one item.
 template <typename T, int D, bool VA, bool FINEST>
 hipError_t launch_nsp(const FineArgs& a, hipStream_t stream)
 {
-    const int nslot = 4 * a.Kp;
-    if (nslot <= 16) return launch_one<T, D, 16, VA, FINEST>(a, stream);
-    if (nslot <= 32) return launch_one<T, D, 32, VA, FINEST>(a, stream);
-    return launch_one<T, D, 64, VA, FINEST>(a, stream);
+    if (a.H == 1 && a.Hp == 1) return launch_nsp_row<T, D, VA, FINEST, true>(a, stream);
+    return launch_nsp_row<T, D, VA, FINEST, false>(a, stream);
 }
 
 template <typename T, int D>

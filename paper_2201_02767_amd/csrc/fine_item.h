@@ -78,7 +78,12 @@ __device__ __forceinline__ float pick4(const float (&v)[4], int i)
 // One work item (parent query P at level l+1, head h; item = (b*Np + P)*heads + h) on the calling
 // wave, whose private LDS region of wave_lds<T, D>(nsp).total bytes starts at `base`. The whole
 // wave must call it with the same item.
-template <typename T, int D, int NSP, bool VA, bool FINEST>
+// ROW: maps of one row (attention along epipolar lines). A parent there has only two children and
+// its kept keys two children each, so one item takes two neighbouring parents P0 = 2p, P1 = 2p + 1
+// (item = (b*ceil(Np/2) + p)*heads + h): its four queries are tokens 4p .. 4p+3, candidate slot
+// s = 2*(half*K + r) + c is child c of kept key r of parent `half`, and query q uses the slots of
+// half q >> 1 only.
+template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW = false>
 __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, unsigned char* const base)
 {
     using S = Storage<T>;
@@ -97,9 +102,11 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
     const int Np = a.Hp * a.Wp;
     const int h = item % a.heads;
     const int bp = item / a.heads;
-    const int P = bp % Np;
-    const int b = bp / Np;
-    const int Py = P / a.Wp, Px = P - Py * a.Wp;
+    const int NI = ROW ? (Np + 1) / 2 : Np;               // items per (batch, head)
+    const int P = ROW ? 2 * (bp % NI) : bp % NI;          // ROW: the pair's first parent
+    const int b = bp / NI;
+    const int Py = ROW ? 0 : P / a.Wp, Px = ROW ? P : P - Py * a.Wp;
+    const bool pair2 = ROW && P + 1 < Np;                 // ROW: the second parent exists
     const int H = a.H, W = a.W, C = a.C, K = a.Kp, Ks = a.Ks;
     const int N = H * W;
     const int nslot = 4 * K;
@@ -111,12 +118,27 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
 
     const int32_t* prow = a.parent_idx + ((static_cast<size_t>(b) * a.heads + h) * Np + P) * K;
     // flat index at level l of child (s & 3) of kept key J (a level l+1 index), or -1. Map sizes are
-    // below 2^24 tokens, so coordinate products fit the 24-bit multiplier.
+    // below 2^24 tokens, so coordinate products fit the 24-bit multiplier. ROW: child s & 1 of J.
     auto child_of_slot_J = [&](int J, int s) -> int {
         if (s >= nslot || J < 0) return -1;
+        if constexpr (ROW) {
+            if (!pair2 && s >= 2 * K) return -1;
+            const int cx = 2 * J + (s & 1);
+            return cx < W ? cx : -1;
+        }
         const int Jy = fast_div(J, a.div_Wp), Jx = J - __mul24(Jy, a.Wp);
         const int cy = 2 * Jy + ((s >> 1) & 1), cx = 2 * Jx + (s & 1);
         return (cy < H && cx < W) ? __mul24(cy, W) + cx : -1;
+    };
+    // query r of the item: its map coordinates
+    auto query_yx = [&](int r, int& qy, int& qx) {
+        if constexpr (ROW) {
+            qy = 0;
+            qx = 2 * P + r;
+        } else {
+            qy = 2 * Py + (r >> 1);
+            qx = 2 * Px + (r & 1);
+        }
     };
 
     // ---- 1. loads. Vector memory counters drain in order, and a load inside a divergent branch
@@ -127,28 +149,35 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
     const int ntile = nsp / 16;
     // phase A: the parents' kept keys (own slot and this lane's gather slot of each tile), the
     // parents' scores (A) and the query chunks (A operand: row n16 holds query n16 & 3)
-    const int last_sel = K - 1;
+    // the kept-key entry of slot s: s >> 2 (ROW: s >> 1, the pair's two rows being contiguous)
+    constexpr int kSlotShift = ROW ? 1 : 2;
+    const int last_sel = (ROW && pair2 ? 2 * K : K) - 1;
     int J_g[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) J_g[t] = prow[min(4 * t + (n16 >> 2), last_sel)];
-    // lane = slot 16g + n16 belongs to kept key 4g + (n16 >> 2): tile g's gather key
+    for (int t = 0; t < NT; ++t) J_g[t] = prow[min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)];
+    // lane = slot 16g + n16: tile g's gather key
     int J_own_raw = -1;
 #pragma unroll
     for (int t = 0; t < NT; ++t) J_own_raw = g == t ? J_g[t] : J_own_raw;
     float pkey = 0.f;
-    if constexpr (VA) pkey = a.parent_key[((static_cast<size_t>(b) * a.heads + h) * Np + P) * K + min(lane >> 2, last_sel)];
+    if constexpr (VA)
+        pkey = a.parent_key[((static_cast<size_t>(b) * a.heads + h) * Np + P) * K + min(lane >> kSlotShift, last_sel)];
     uint4 qa[NJ];
     bool q_ok;
     {
         const int qi = n16 & 3;
-        const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
+        int qy, qx;
+        query_yx(qi, qy, qx);
         q_ok = qy < H && qx < W;
         const int qyc = qy < H ? qy : H - 1, qxc = qx < W ? qx : W - 1;
-        // uniform base of this (batch, head) plus a 32-bit per-lane offset
+        // uniform base of this (batch, head) plus a 32-bit per-lane offset. ROW, blocked: query 4p + qi
+        // is child qi & 1 of parent 2p + (qi >> 1)
         const unsigned char* qbase = static_cast<const unsigned char*>(a.q) +
             (a.q_blocked ? ((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 * RB
                          : (static_cast<size_t>(b) * N * C + h * D) * TB);
-        const uint32_t qoff = a.q_blocked ? static_cast<uint32_t>(qi * RB)
+        // (a query off the map may belong to a parent past the last one: read the first block instead)
+        const int qblk = ROW ? (q_ok ? (qi >> 1) * 4 + (qi & 1) : 0) : qi;
+        const uint32_t qoff = a.q_blocked ? static_cast<uint32_t>(qblk * RB)
                                           : static_cast<uint32_t>(__mul24(qyc, W) + qxc) * static_cast<uint32_t>(C * TB);
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
@@ -172,7 +201,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
             const int f = child_of_slot_J(J_g[t], s);
             gok[t] = f >= 0;
             // 32-bit byte offset within this (batch, head)'s map (below 2^31 by the host's checks)
-            const uint32_t goff = (!gok[t] ? 0u : (kvb ? static_cast<uint32_t>(J_g[t] * 4 + (s & 3)) * RB
+            const uint32_t goff = (!gok[t] ? 0u : (kvb ? static_cast<uint32_t>(J_g[t] * 4 + (ROW ? (s & 1) : (s & 3))) * RB
                                                         : static_cast<uint32_t>(f) * tok_bytes)) + g * 16;
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
@@ -242,7 +271,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
     const int cg = blk / NH, hh = blk % NH;
     const int ch = 4 * cg + t4;
     constexpr int kPre = FINEST ? kPrefetchLevels : 1;
-    float anc[kPre];
+    float anc[ROW ? QPL : 1][kPre];     // ROW: the two parents of a pair have different ancestors
     float wq[FINEST ? QPL : 1][kPre + 1];
     float peq[FINEST ? QPL : 1] = {};
     const bool prefetch = FINEST && a.levels <= kPre + 1;
@@ -254,17 +283,30 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
 #pragma unroll
             for (int lev = 1; lev <= kPre; ++lev) {
                 if (lev >= L) break;                         // uniform
-                // the ancestor is shared by the four siblings: a uniform address plus the channel
-                const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
-                                  static_cast<size_t>((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev);
-                anc[lev - 1] = (a.coarser_msg[lev] + (an * a.heads + h) * D)[ch];
+                if constexpr (ROW) {
+#pragma unroll
+                    for (int u = 0; u < QPL; ++u) {
+                        const int qi = (NH == 2 ? hh * QPL : 0) + u;
+                        // clamped: a query off the map may lie past the last ancestor
+                        const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] + min((2 * P + qi) >> lev, a.lvl_W[lev] - 1);
+                        anc[u][lev - 1] = (a.coarser_msg[lev] + (an * a.heads + h) * D)[ch];
+                    }
+                } else {
+                    // the ancestor is shared by the four siblings: a uniform address plus the channel
+                    const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
+                                      static_cast<size_t>((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev);
+                    anc[0][lev - 1] = (a.coarser_msg[lev] + (an * a.heads + h) * D)[ch];
+                }
             }
             if (a.pe0) {                                     // uniform
                 const float* pb = a.pe0 + (static_cast<size_t>(b) * N * a.heads + h) * D + ch;
 #pragma unroll
                 for (int u = 0; u < QPL; ++u) {
                     const int qi = (NH == 2 ? hh * QPL : 0) + u;
-                    const int py = min(2 * Py + (qi >> 1), H - 1), px = min(2 * Px + (qi & 1), W - 1);
+                    int py, px;
+                    query_yx(qi, py, px);
+                    py = min(py, H - 1);
+                    px = min(px, W - 1);
                     peq[u] = pb[static_cast<uint32_t>(__mul24(py, W) + px) * static_cast<uint32_t>(a.heads * D)];
                 }
             }
@@ -273,7 +315,10 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
 #pragma unroll
                 for (int u = 0; u < QPL; ++u) {
                     const int qi = (NH == 2 ? hh * QPL : 0) + u;
-                    const int wy = min(2 * Py + (qi >> 1), H - 1), wx = min(2 * Px + (qi & 1), W - 1);
+                    int wy, wx;
+                    query_yx(qi, wy, wx);
+                    wy = min(wy, H - 1);
+                    wx = min(wx, W - 1);
                     const float* wrow = wb + static_cast<uint32_t>(__mul24(wy, W) + wx) * static_cast<uint32_t>(a.heads * L);
 #pragma unroll
                     for (int lev = 0; lev <= kPre; ++lev) {
@@ -284,9 +329,13 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
             }
         }
     }
+    // the slots of query r (ROW: only those of its own parent, half r >> 1)
+    bool okr[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) okr[r] = ROW ? ok && ((lane >> 1) >= K) == ((r >> 1) != 0) : ok;
     float x[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) x[r] = ok ? acc_own[r] * a.scale : -INFINITY;
+    for (int r = 0; r < 4; ++r) x[r] = okr[r] ? acc_own[r] * a.scale : -INFINITY;
 
     // ---- 3. weights ----
     float wgt[4], inv_sum[4] = {1.f, 1.f, 1.f, 1.f};
@@ -294,30 +343,32 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const float m = wave_max_fast(x[r]);
-            wgt[r] = ok ? __expf(x[r] - m) : 0.f;
+            wgt[r] = okr[r] ? __expf(x[r] - m) : 0.f;
             inv_sum[r] = 1.0f / wave_sum_fast(wgt[r]);
         }
     } else {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
+            // t: a softmax over the children of one kept key (a lane quad; ROW: a lane pair)
             float m = fmaxf(x[r], xchg_f32<1>(x[r]));
-            m = fmaxf(m, xchg_f32<2>(m));
-            const float e = ok ? __expf(x[r] - m) : 0.f;
+            if constexpr (!ROW) m = fmaxf(m, xchg_f32<2>(m));
+            const float e = okr[r] ? __expf(x[r] - m) : 0.f;
             float s = e + xchg_f32<1>(e);
-            s += xchg_f32<2>(s);
-            wgt[r] = ok ? pkey * (e / s) : 0.f;
+            if constexpr (!ROW) s += xchg_f32<2>(s);
+            wgt[r] = okr[r] ? pkey * (e / s) : 0.f;
         }
     }
 
     // ---- 4. this level's selection (levels above the finest) ----
     if constexpr (!FINEST) {
-        const int nvalid = __popcll(__ballot(ok));
-        const int keff = Ks < nvalid ? Ks : nvalid;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int qy = 2 * Py + (r >> 1), qx = 2 * Px + (r & 1);
+            int qy, qx;
+            query_yx(r, qy, qx);
             if (qy >= H || qx >= W) continue;                 // uniform across the wave
-            const uint32_t key[1] = {ok ? ordered_bits(VA ? wgt[r] : x[r]) : 0u};
+            const int nvalid = __popcll(__ballot(okr[r]));
+            const int keff = Ks < nvalid ? Ks : nvalid;
+            const uint32_t key[1] = {okr[r] ? ordered_bits(VA ? wgt[r] : x[r]) : 0u};
             const uint32_t name[1] = {static_cast<uint32_t>(flat)};
             bool kept[1];
             wave_select_top<1>(key, name, keff, kept);
@@ -378,7 +429,8 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
 #pragma unroll
     for (int u = 0; u < QPL; ++u) {
         const int qi = (NH == 2 ? hh * QPL : 0) + u;
-        const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
+        int qy, qx;
+        query_yx(qi, qy, qx);
         if (qy >= H || qx >= W) continue;
         const float m = pick4(o, qi) * pick4(inv_sum, qi);
         const uint32_t qpos = static_cast<uint32_t>(__mul24(qy, W) + qx);      // token within the map
@@ -395,7 +447,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
 #pragma unroll
                 for (int lev = 1; lev <= kPre; ++lev) {
                     if (lev >= L) break;
-                    out += (VA ? 1.0f : (a.w ? wq[u][lev] : wdef)) * anc[lev - 1];
+                    out += (VA ? 1.0f : (a.w ? wq[u][lev] : wdef)) * anc[ROW ? u : 0][lev - 1];
                 }
             } else {
                 const float* wrow = a.w ? a.w + (qtok * a.heads + h) * L : nullptr;
