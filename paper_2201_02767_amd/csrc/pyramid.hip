@@ -115,11 +115,13 @@ __global__ __launch_bounds__(256) void pyramid_pass_kernel(PyramidPassArgs a)
 }
 
 // Two-level pass, workgroup = tpb top tokens x 4 children x `chunks` chunks (at most 256 threads).
-template <typename T>
+// ROW (maps of one row): a token has two children, so tpb top tokens x 2 children x `chunks`.
+template <typename T, bool ROW>
 __global__ __launch_bounds__(256) void pyramid_pass2_kernel(PyramidPassArgs a, int tpb)
 {
     using S = Storage<T>;
     constexpr int E = S::kPer16B;
+    constexpr int NC = ROW ? 2 : 4;                    // children of a token
     __shared__ uint4 stage[256];
     const int tensor = blockIdx.y;
     const char* __restrict__ src = static_cast<const char*>(a.src[tensor]);
@@ -128,8 +130,8 @@ __global__ __launch_bounds__(256) void pyramid_pass2_kernel(PyramidPassArgs a, i
     const int chunks = a.chunks;
     const int li = threadIdx.x;
     const int ch = li % chunks;
-    const int q = (li / chunks) & 3;
-    const int t = li / (4 * chunks);
+    const int q = (li / chunks) % NC;
+    const int t = li / (NC * chunks);
     const long long ntop = static_cast<long long>(a.B) * a.H2 * a.W2;
     const long long top = static_cast<long long>(blockIdx.x) * tpb + t;
     const bool active = top < ntop;                    // inactive threads still reach the barrier
@@ -138,11 +140,16 @@ __global__ __launch_bounds__(256) void pyramid_pass2_kernel(PyramidPassArgs a, i
     const int Y = static_cast<int>((topc / a.W2) % a.H2);
     const int b = static_cast<int>(topc / (static_cast<long long>(a.W2) * a.H2));
 
-    const int y1 = 2 * Y + (q >> 1), x1 = 2 * X + (q & 1);
+    const int y1 = ROW ? 0 : 2 * Y + (q >> 1), x1 = 2 * X + (q & 1);
     const bool mid_ok = y1 < a.H1 && x1 < a.W1;
     uint4 raw[2][2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
+        if (ROW && i == 1) {                               // no row below
+            raw[1][0] = raw[0][0];
+            raw[1][1] = raw[0][1];
+            break;
+        }
         const int y = min(2 * y1 + i, a.Hs - 1);
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
@@ -166,12 +173,12 @@ __global__ __launch_bounds__(256) void pyramid_pass2_kernel(PyramidPassArgs a, i
     stage[li] = packed;
     __syncthreads();
     if (!active || q != 0) return;
-    const int base = t * 4 * chunks + ch;
+    const int base = t * NC * chunks + ch;
     float m0[E], m1[E], m2[E], m3[E], o[E];
     S::unpack(stage[base], m0);
     S::unpack(stage[base + chunks], m1);
-    S::unpack(stage[base + 2 * chunks], m2);
-    S::unpack(stage[base + 3 * chunks], m3);
+    S::unpack(stage[base + (ROW ? 0 : 2) * chunks], m2);   // ROW: unused (no row below)
+    S::unpack(stage[base + (ROW ? 1 : 3) * chunks], m3);
     pool_children<E>(m0, m1, m2, m3, 2 * X + 1 < a.W1, 2 * Y + 1 < a.H1, o);
 #pragma unroll
     for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
@@ -184,14 +191,21 @@ __global__ __launch_bounds__(256) void pyramid_pass2_kernel(PyramidPassArgs a, i
 hipError_t launch_pyramid_pass(const PyramidPassArgs& a, int nlev, int ntensors, bool use_bf16, hipStream_t stream)
 {
     if (nlev == 2 && 4 * a.chunks <= 256) {
-        const int tpb = 256 / (4 * a.chunks);
+        const bool row = a.Hs == 1;                       // maps of one row: two children per token
+        const int nc = row ? 2 : 4;
+        const int tpb = 256 / (nc * a.chunks);
         const long long ntop = static_cast<long long>(a.B) * a.H2 * a.W2;
         const long long blocks = (ntop + tpb - 1) / tpb;
         if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
         dim3 grid(static_cast<unsigned>(blocks), ntensors);
-        const dim3 block(tpb * 4 * a.chunks);
-        if (use_bf16) hipLaunchKernelGGL((pyramid_pass2_kernel<bf16>), grid, block, 0, stream, a, tpb);
-        else hipLaunchKernelGGL((pyramid_pass2_kernel<float>), grid, block, 0, stream, a, tpb);
+        const dim3 block(tpb * nc * a.chunks);
+        if (use_bf16) {
+            if (row) hipLaunchKernelGGL((pyramid_pass2_kernel<bf16, true>), grid, block, 0, stream, a, tpb);
+            else hipLaunchKernelGGL((pyramid_pass2_kernel<bf16, false>), grid, block, 0, stream, a, tpb);
+        } else {
+            if (row) hipLaunchKernelGGL((pyramid_pass2_kernel<float, true>), grid, block, 0, stream, a, tpb);
+            else hipLaunchKernelGGL((pyramid_pass2_kernel<float, false>), grid, block, 0, stream, a, tpb);
+        }
         return hipGetLastError();
     }
     const int Ht = nlev == 2 ? a.H2 : a.H1, Wt = nlev == 2 ? a.W2 : a.W1;
