@@ -15,8 +15,9 @@
 //      parents' four children and forms dk and dv of the key's four children from the recomputed
 //      probabilities; a key's rows are written once (summed over its chunks when it has several)
 //                                                   (bwd_scan_*, bwd_fill, bwd_key, bwd_key_reduce)
-//   3. the coarsest level (Eq. 1): a pass per query (dq, softmax statistics) and a pass per key
-//      (dk, dv) that recomputes the probabilities, so neither needs atomics (bwd_coarse_*)
+//   3. the coarsest level (Eq. 1), in coarse_bwd.hip: a pass over query tiles (dq, softmax
+//      statistics) and a pass over key tiles (dk, dv) that recomputes the probabilities, both on
+//      MFMA and without atomics
 //   4. pyramids: a pooled token hands 1/n of its gradient to each of its n valid children; the
 //      level-0 gradients add every ancestor's, scaled along the chain      (bwd_unpool_kernel)
 // All gradients are fp32. The message gradients of levels >= 2 are summed with atomics and the
@@ -984,246 +985,7 @@ hipError_t launch_key_td(const BwdLevelArgs& a, bool variant_a, bool finest, lon
                   : launch_key_tdv<T, D, false, false>(a, max_chunks, stream);
 }
 
-// ---------------------------------------------------------------------------------------------
-// 3. coarsest level
-// ---------------------------------------------------------------------------------------------
-
-constexpr int kCoarseChunks = QTA_MAX_COARSE / kWave;   // keys (or queries) per lane, at most
-
-// <x, row> over one head's D channels: x fp32 in LDS (broadcast reads), row in the storage type
-// (or fp32) in HBM, streamed 16 bytes at a time.
-template <typename T, int D>
-__device__ __forceinline__ float dot_row(const float* x, const void* base, size_t elem)
-{
-    using S = Storage<T>;
-    constexpr int E = S::kPer16B;
-    const uint4* p = reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(base) + elem * sizeof(T));
-    float acc = 0.f;
-#pragma unroll
-    for (int cc = 0; cc < D / E; ++cc) {
-        float f[E];
-        S::unpack(p[cc], f);
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc += x[cc * E + e] * f[e];
-    }
-    return acc;
-}
-
-// acc[c] += s * row[c] over one head's D channels.
-template <typename T, int D>
-__device__ __forceinline__ void axpy_row(float s, const void* base, size_t elem, float* acc)
-{
-    using S = Storage<T>;
-    constexpr int E = S::kPer16B;
-    const uint4* p = reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(base) + elem * sizeof(T));
-#pragma unroll
-    for (int cc = 0; cc < D / E; ++cc) {
-        float f[E];
-        S::unpack(p[cc], f);
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[cc * E + e] += s * f[e];
-    }
-}
-
-// Sum over the wave of each acc[c]; lane c < D receives the total of channel c.
-template <int D>
-__device__ __forceinline__ float wave_sum_to_lane(const float* acc)
-{
-    const int lane = threadIdx.x & 63;
-    float mine = 0.f;
-#pragma unroll
-    for (int c = 0; c < D; ++c) {
-        const float s = wave_sum_fast(acc[c]);
-        if (lane == c) mine = s;
-    }
-    return mine;
-}
-
-// The gradient of coarse message row `tok` at channel c: dm^c when there are finer levels,
-// otherwise w_0 dout (QuadTree-B) or dout (A).
-template <typename T>
-__device__ __forceinline__ float dm_elem(const BwdCoarseArgs& a, size_t tok, int h, int D, int c)
-{
-    if (a.dm) return a.dm[tok * a.C + h * D + c];
-    const float w0 = (a.variant_b && a.w) ? a.w[tok * a.heads + h] : 1.0f;
-    return w0 * Storage<T>::load1(a.dout, tok * a.C + h * D + c);
-}
-
-// Per query (one wave per (b, h, i), lanes over keys): softmax statistics, dq and, for a single
-// QuadTree-B level with w, dw. The query's q, dm (and dout) rows sit in the wave's LDS.
-template <typename T, int D, bool VA>
-__global__ __launch_bounds__(256) void bwd_coarse_query_kernel(BwdCoarseArgs a)
-{
-    const int lane = threadIdx.x & 63;
-    const long long nitems = static_cast<long long>(a.B) * a.heads * a.N;
-    const long long item = static_cast<long long>(blockIdx.x) * (blockDim.x >> 6) + (threadIdx.x >> 6);
-    if (item >= nitems) return;                              // whole wave
-    __shared__ __align__(16) float rows[4][3][D];
-    float* qs = rows[threadIdx.x >> 6][0];
-    float* gs_row = rows[threadIdx.x >> 6][1];
-    float* go = rows[threadIdx.x >> 6][2];
-    const int N = a.N;
-    const int i = static_cast<int>(item % N);
-    const int bh = static_cast<int>(item / N);
-    const int h = bh % a.heads, b = bh / a.heads;
-    const size_t qtok = static_cast<size_t>(b) * N + i;
-    const bool want_dw = !a.dm && a.variant_b && a.w && a.dw;
-    if (lane < D) {
-        qs[lane] = Storage<T>::load1(a.q, qtok * a.C + h * D + lane);
-        gs_row[lane] = dm_elem<T>(a, qtok, h, D, lane);
-        go[lane] = want_dw ? Storage<T>::load1(a.dout, qtok * a.C + h * D + lane) : 0.f;
-    }
-    wave_lds_sync();
-    float x[kCoarseChunks], gg[kCoarseChunks], g0[kCoarseChunks];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int ch = 0; ch < kCoarseChunks; ++ch) {
-        x[ch] = -INFINITY;
-        gg[ch] = 0.f;
-        g0[ch] = 0.f;
-        if (ch * kWave >= N) continue;                        // uniform
-        const int j = ch * kWave + lane;
-        const size_t krow = (static_cast<size_t>(b) * N + min(j, N - 1)) * a.C + h * D;
-        const float xs = dot_row<T, D>(qs, a.k, krow);
-        gg[ch] = dot_row<T, D>(gs_row, a.v, krow);
-        if (want_dw) g0[ch] = dot_row<T, D>(go, a.v, krow);
-        x[ch] = j < N ? xs * a.scale : -INFINITY;
-        mx = fmaxf(mx, x[ch]);
-    }
-    mx = wave_max_fast(mx);
-    float sum = 0.f;
-#pragma unroll
-    for (int ch = 0; ch < kCoarseChunks; ++ch) {
-        x[ch] = __expf(x[ch] - mx);                           // 0 for missing keys
-        sum += x[ch];
-    }
-    sum = wave_sum_fast(sum);
-    const float inv = 1.0f / sum;
-    // QuadTree-A's kept keys: their score's gradient comes from the level below
-    if (VA && a.K > 0) {
-        const size_t srow = (static_cast<size_t>(bh) * N + i) * a.K;
-        for (int mm = 0; mm < a.K; ++mm) {
-            const int32_t j = a.sel_idx[srow + mm];
-            if (j < 0) continue;
-            const float dsv = a.dsig[srow + mm];
-#pragma unroll
-            for (int ch = 0; ch < kCoarseChunks; ++ch)
-                if (j == ch * kWave + lane) gg[ch] = dsv;
-        }
-    }
-    float Dsum = 0.f, dwsum = 0.f;
-#pragma unroll
-    for (int ch = 0; ch < kCoarseChunks; ++ch) {
-        x[ch] *= inv;                                         // p
-        Dsum += x[ch] * gg[ch];
-        dwsum += x[ch] * g0[ch];
-    }
-    Dsum = wave_sum_fast(Dsum);
-    float dq[D];
-#pragma unroll
-    for (int c = 0; c < D; ++c) dq[c] = 0.f;
-#pragma unroll
-    for (int ch = 0; ch < kCoarseChunks; ++ch) {
-        if (ch * kWave >= N) continue;                        // uniform
-        const int j = ch * kWave + lane;
-        const float dx = x[ch] * (gg[ch] - Dsum);             // 0 for missing keys (p = 0)
-        axpy_row<T, D>(dx, a.k, (static_cast<size_t>(b) * N + min(j, N - 1)) * a.C + h * D, dq);
-    }
-    const float mine = wave_sum_to_lane<D>(dq);
-    if (lane < D) a.dq[qtok * a.C + h * D + lane] = a.scale * mine;
-    if (lane == 0)
-        *reinterpret_cast<float4*>(a.stats + (static_cast<size_t>(bh) * N + i) * 4) = make_float4(mx, sum, Dsum, 0.f);
-    if (want_dw) {
-        dwsum = wave_sum_fast(dwsum);
-        if (lane == 0) a.dw[qtok * a.heads + h] = dwsum;
-    }
-}
-
-// Per key (one wave per (b, h, j), lanes over queries): dk and dv from the recomputed probabilities.
-template <typename T, int D, bool VA>
-__global__ __launch_bounds__(256) void bwd_coarse_key_kernel(BwdCoarseArgs a)
-{
-    const int lane = threadIdx.x & 63;
-    const long long nitems = static_cast<long long>(a.B) * a.heads * a.N;
-    const long long item = static_cast<long long>(blockIdx.x) * (blockDim.x >> 6) + (threadIdx.x >> 6);
-    if (item >= nitems) return;                              // whole wave
-    __shared__ __align__(16) float rows[4][2][D];
-    float* ks = rows[threadIdx.x >> 6][0];
-    float* vs = rows[threadIdx.x >> 6][1];
-    const int N = a.N;
-    const int j = static_cast<int>(item % N);
-    const int bh = static_cast<int>(item / N);
-    const int h = bh % a.heads, b = bh / a.heads;
-    const size_t ktok = static_cast<size_t>(b) * N + j;
-    if (lane < D) {
-        ks[lane] = Storage<T>::load1(a.k, ktok * a.C + h * D + lane);
-        vs[lane] = Storage<T>::load1(a.v, ktok * a.C + h * D + lane);
-    }
-    wave_lds_sync();
-    float dk[D], dv[D];
-#pragma unroll
-    for (int c = 0; c < D; ++c) {
-        dk[c] = 0.f;
-        dv[c] = 0.f;
-    }
-    for (int ch = 0; ch < kCoarseChunks; ++ch) {
-        if (ch * kWave >= N) break;                           // uniform
-        const int i = ch * kWave + lane;
-        const int ic = min(i, N - 1);
-        const size_t qtok = static_cast<size_t>(b) * N + ic;
-        const size_t qrow = qtok * a.C + h * D;
-        const float4 st = *reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(bh) * N + ic) * 4);
-        const float xs = dot_row<T, D>(ks, a.q, qrow);
-        // <dm_i, v_j>: dm^c rows are fp32; for a single level, w_0 dout in the storage type
-        float w0 = 1.0f, gsv;
-        if (a.dm) {
-            gsv = dot_row<float, D>(vs, a.dm, qrow);
-        } else {
-            if (a.variant_b && a.w) w0 = a.w[qtok * a.heads + h];
-            gsv = w0 * dot_row<T, D>(vs, a.dout, qrow);
-        }
-        const float p = i < N ? __expf(xs * a.scale - st.x) / st.y : 0.f;
-        float ds = gsv;
-        bool kept = false;
-        if (VA && a.K > 0) {
-            const size_t srow = (static_cast<size_t>(bh) * N + ic) * a.K;
-            for (int mm = 0; mm < a.K; ++mm)
-                if (a.sel_idx[srow + mm] == j) {
-                    kept = true;
-                    ds = a.dsig[srow + mm];
-                }
-        }
-        const float dx = p * (ds - st.z);
-        const float vw = kept ? 0.f : p;
-        axpy_row<T, D>(dx, a.q, qrow, dk);
-        if (a.dm)
-            axpy_row<float, D>(vw, a.dm, qrow, dv);
-        else
-            axpy_row<T, D>(vw * w0, a.dout, qrow, dv);
-    }
-    const float mk = wave_sum_to_lane<D>(dk);
-    const float mv = wave_sum_to_lane<D>(dv);
-    if (lane < D) {
-        a.dk[ktok * a.C + h * D + lane] = a.scale * mk;
-        a.dv[ktok * a.C + h * D + lane] = mv;
-    }
-}
-
-template <typename T, int D, bool VA>
-hipError_t launch_coarse_tdv(const BwdCoarseArgs& a, hipStream_t stream)
-{
-    const long long items = static_cast<long long>(a.B) * a.heads * a.N;
-    const int wpb = 4;
-    const long long blocks = (items + wpb - 1) / wpb;
-    if (blocks >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((bwd_coarse_query_kernel<T, D, VA>), dim3(static_cast<unsigned>(blocks)), dim3(wpb * kWave), 0,
-                       stream, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((bwd_coarse_key_kernel<T, D, VA>), dim3(static_cast<unsigned>(blocks)), dim3(wpb * kWave), 0,
-                       stream, a);
-    return hipGetLastError();
-}
+// 3. the coarsest level: coarse_bwd.hip
 
 // ---------------------------------------------------------------------------------------------
 // 4. pyramids
@@ -1335,19 +1097,6 @@ hipError_t launch_bwd_keys(const BwdLevelArgs& a, const BwdScanArgs& sc, int d, 
     if (rb >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
     hipLaunchKernelGGL(bwd_key_reduce_kernel, dim3(static_cast<unsigned>(rb)), dim3(256), 0, stream, a, d);
     return hipGetLastError();
-}
-
-hipError_t launch_bwd_coarse(const BwdCoarseArgs& a, int d, bool variant_a, bool use_bf16, hipStream_t stream)
-{
-    if (a.N > QTA_MAX_COARSE) return hipErrorInvalidValue;
-    if (use_bf16) {
-        if (d == 32) return variant_a ? launch_coarse_tdv<bf16, 32, true>(a, stream) : launch_coarse_tdv<bf16, 32, false>(a, stream);
-        if (d == 64) return variant_a ? launch_coarse_tdv<bf16, 64, true>(a, stream) : launch_coarse_tdv<bf16, 64, false>(a, stream);
-    } else {
-        if (d == 32) return variant_a ? launch_coarse_tdv<float, 32, true>(a, stream) : launch_coarse_tdv<float, 32, false>(a, stream);
-        if (d == 64) return variant_a ? launch_coarse_tdv<float, 64, true>(a, stream) : launch_coarse_tdv<float, 64, false>(a, stream);
-    }
-    return hipErrorInvalidValue;
 }
 
 hipError_t launch_bwd_unpool(const BwdUnpoolArgs& a, hipStream_t stream)
