@@ -12,6 +12,7 @@
 //            LDS and written as fp32 messages (or, for a single-level problem, straight to the
 //            output in the storage type).
 // The coarsest map holds at most QTA_MAX_COARSE tokens, so a row fits in 16 registers per lane.
+// Maps of at most 64 tokens take coarse_small_kernel instead (one wave per query row).
 #include "qta_device.h"
 #include "qta_internal.h"
 
@@ -235,6 +236,89 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     }
 }
 
+// Small coarsest maps (N <= 64, e.g. the many short maps of attention along epipolar lines): one
+// wave per query row, lane j holding key j. The logits are per-lane dot products, the softmax and the
+// selection are wave reductions and a ballot radix select, and lane c then forms channel c of the
+// message from the weights in LDS, four value rows in flight at a time.
+template <typename T, int D, bool VA>
+__global__ __launch_bounds__(256) void coarse_small_kernel(CoarseArgs a)
+{
+    using S = Storage<T>;
+    constexpr int E = S::kPer16B;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int N = a.N, C = a.C;
+    const long long rows = static_cast<long long>(a.B) * a.heads * N;
+    const long long row = static_cast<long long>(blockIdx.x) * (blockDim.x >> 6) + wave;
+    if (row >= rows) return;                                  // whole wave
+    const int qi = static_cast<int>(row % N);
+    const int bh = static_cast<int>(row / N);
+    const int h = bh % a.heads, b = bh / a.heads;
+    const size_t tok0 = static_cast<size_t>(b) * N;
+    const size_t hoff = static_cast<size_t>(h) * D;
+    const int j = min(lane, N - 1);
+    const bool valid = lane < N;
+    // the query row (the same address on every lane) and key row j
+    const uint4* qp = reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.q) + ((tok0 + qi) * C + hoff) * sizeof(T));
+    const uint4* kp = reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.k) + ((tok0 + j) * C + hoff) * sizeof(T));
+    __shared__ float pw[4][kWave];
+    float x = 0.f;
+#pragma unroll
+    for (int cc = 0; cc < D / E; ++cc) {
+        float qf[E], kf[E];
+        S::unpack(qp[cc], qf);
+        S::unpack(kp[cc], kf);
+#pragma unroll
+        for (int e = 0; e < E; ++e) x += qf[e] * kf[e];
+    }
+    x = valid ? x * a.scale : -INFINITY;
+    const float mx = wave_max_fast(x);
+    float p = valid ? __expf(x - mx) : 0.f;
+    p *= 1.0f / wave_sum_fast(p);
+    if (a.K > 0) {
+        const uint32_t key[1] = {valid ? ordered_bits(x) : 0u};
+        const uint32_t name[1] = {static_cast<uint32_t>(lane)};
+        bool kept[1];
+        const int keff = a.K < N ? a.K : N;
+        wave_select_top<1>(key, name, keff, kept);
+        const size_t orow = (static_cast<size_t>(bh) * N + qi) * a.K;
+        const uint64_t mask = __ballot(kept[0]);
+        if (kept[0]) {
+            const int pos = lanes_below(mask);
+            a.sel_idx[orow + pos] = lane;
+            a.sel_key[orow + pos] = p;
+            if constexpr (VA) p = 0.f;                        // refined at the next level (Omega)
+        }
+        if (lane >= keff && lane < a.K) {
+            a.sel_idx[orow + lane] = -1;
+            a.sel_key[orow + lane] = 0.f;
+        }
+    }
+    pw[wave][lane] = p;
+    wave_lds_sync();
+    if (lane >= D) return;
+    float m = 0.f;
+#pragma unroll 4
+    for (int jj = 0; jj < N; ++jj) m += pw[wave][jj] * S::load1(a.v, (tok0 + jj) * C + hoff + lane);
+    if (a.out) {
+        float wl = 1.0f;
+        if (!VA) wl = a.w ? a.w[((tok0 + qi) * a.heads + h) * a.levels] : 1.0f / a.levels;
+        const float pe = a.pe0 ? a.pe0[((tok0 + qi) * a.heads + h) * D + lane] : 0.f;
+        S::store1(a.out, (tok0 + qi) * C + hoff + lane, wl * (m + pe));
+    } else {
+        a.msg[((tok0 + qi) * a.heads + h) * D + lane] = m;
+    }
+}
+
+template <typename T, int D, bool VA>
+hipError_t launch_small(const CoarseArgs& a, hipStream_t stream)
+{
+    const long long rows = static_cast<long long>(a.B) * a.heads * a.N;
+    const long long blocks = (rows + 3) / 4;
+    if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((coarse_small_kernel<T, D, VA>), dim3(static_cast<unsigned>(blocks)), dim3(4 * kWave), 0, stream, a);
+    return hipGetLastError();
+}
+
 template <typename T, int D, bool VA, int kPerLane>
 hipError_t launch_one(const CoarseArgs& a, hipStream_t stream)
 {
@@ -259,6 +343,7 @@ hipError_t launch_one(const CoarseArgs& a, hipStream_t stream)
 template <typename T, int D, bool VA>
 hipError_t launch_per_lane(const CoarseArgs& a, hipStream_t stream)
 {
+    if (a.N <= kWave) return launch_small<T, D, VA>(a, stream);
     switch (coarse_per_lane(a.N)) {
     case 1: return launch_one<T, D, VA, 1>(a, stream);
     case 2: return launch_one<T, D, VA, 2>(a, stream);
