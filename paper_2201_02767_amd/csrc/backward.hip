@@ -10,9 +10,10 @@
 //      key's children with s = sigma t, Eq. 4, sending d sigma back to the parent level), dq on
 //      MFMA; it keeps each query's softmax statistics and counts how many parents kept each key
 //                                                                        (bwd_level_kernel)
-//      key pass: the parents are sorted by the key they kept (a counting sort: the counts, a scan,
-//      a fill), and one wave per chunk of up to kKeyChunk parents of one kept key gathers those
-//      parents' four children and forms dk and dv of the key's four children from the recomputed
+//      key pass: the parents are sorted by the key they kept (a counting sort: the query pass's
+//      count atomics also give each pair its place in its key's list; a scan, a fill), and one
+//      wave per chunk of up to kKeyChunk parents of one kept key gathers those parents' four
+//      children and forms dk and dv of the key's four children from the recomputed
 //      probabilities; a key's rows are written once (summed over its chunks when it has several)
 //                                                   (bwd_scan_*, bwd_fill, bwd_key, bwd_key_reduce)
 //   3. the coarsest level (Eq. 1), in coarse_bwd.hip: a pass over query tiles (dq, softmax
@@ -21,8 +22,8 @@
 //   4. pyramids: a pooled token hands 1/n of its gradient to each of its n valid children; the
 //      level-0 gradients add every ancestor's, scaled along the chain      (bwd_unpool_kernel)
 // All gradients are fp32. The message gradients of levels >= 2 are summed with atomics and the
-// parents within one kept key's list come in the order the fill's atomics hand out, so the last bits
-// of the gradients may differ between runs.
+// parents within one kept key's list come in the order the query pass's count atomics hand out, so
+// the last bits of the gradients may differ between runs.
 #include "qta_device.h"
 #include "qta_internal.h"
 
@@ -186,10 +187,11 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             w0[r] = a.w ? a.w[((static_cast<size_t>(b) * N + rt) * a.heads + h) * a.levels] : 1.0f / a.levels;
         }
     }
-    // how many parents kept each key of level l+1 (for the key pass's counting sort)
-    {
+    // how many parents kept each key of level l+1 (for the key pass's counting sort); the count a
+    // pair finds is its place in the key's list
+    if (lane < K) {
         const int Jr = prow[min(lane, last_sel)];
-        if (lane < K && Jr >= 0) atomicAdd(a.count + (static_cast<size_t>(b) * a.heads + h) * Np + Jr, 1);
+        if (Jr >= 0) a.slot[prow_off * K + lane] = atomicAdd(a.count + (static_cast<size_t>(b) * a.heads + h) * Np + Jr, 1);
     }
 
     // ---- gathers, logits and <dm, v> on MFMA, key rows to LDS, one tile of 16 slots at a time ----
@@ -516,17 +518,39 @@ __device__ __forceinline__ void block_scan_256x4(int2 (&v)[4], int2& total)
 
 __device__ __forceinline__ int chunks_of(int n) { return n > 0 ? (n + kKeyChunk - 1) / kKeyChunk : 1; }
 
+// (count, chunk count) of the key slots i0 .. i0+3 (i0 a multiple of 4) from one 16-byte load, and
+// (0, 0) past the last slot. The count array is padded to a multiple of four slots, so the load
+// (clamped to the last quad) stays inside it; it is unconditional and masked rather than selected,
+// so that the compiler keeps every such load of a thread in flight at once.
+__device__ __forceinline__ void quad_counts(const int32_t* count, int i0, int n, int2 (&c)[4])
+{
+    const int4 r = *reinterpret_cast<const int4*>(count + min(i0, (n - 1) & ~3));
+    const int v[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int valid = i0 + e < n;
+        const int x = v[e] & -valid;
+        c[e] = make_int2(x, chunks_of(x) & -valid);
+    }
+}
+
+// Elements i0 .. i0+3 of p below n: one 16-byte store for a full quad (i0 a multiple of 4).
+__device__ __forceinline__ void store_quad(int32_t* p, int i0, int n, int x, int y, int z, int w)
+{
+    if (i0 + 3 < n) {
+        *reinterpret_cast<int4*>(p + i0) = make_int4(x, y, z, w);
+    } else {
+        if (i0 < n) p[i0] = x;
+        if (i0 + 1 < n) p[i0 + 1] = y;
+        if (i0 + 2 < n) p[i0 + 2] = z;
+    }
+}
+
 // Per block of 1024 kept-key slots: the sums of the counts and of the chunk counts.
 __global__ __launch_bounds__(256) void bwd_scan_reduce_kernel(BwdScanArgs a)
 {
     int2 v[4];
-    const int base = blockIdx.x * 1024 + threadIdx.x * 4;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int i = base + e;
-        const int c = i < a.n ? a.count[i] : 0;
-        v[e] = i < a.n ? make_int2(c, chunks_of(c)) : make_int2(0, 0);
-    }
+    quad_counts(a.count, blockIdx.x * 1024 + threadIdx.x * 4, a.n, v);
     int2 total;
     block_scan_256x4(v, total);
     if (threadIdx.x == 0) {
@@ -545,7 +569,9 @@ __global__ __launch_bounds__(256) void bwd_scan_blocks_kernel(BwdScanArgs a)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int i = base + e;
-            v[e] = i < a.nblocks ? make_int2(a.block_sums[2 * i], a.block_sums[2 * i + 1]) : make_int2(0, 0);
+            const int j = 2 * min(i, a.nblocks - 1);
+            const int2 b = make_int2(a.block_sums[j], a.block_sums[j + 1]);
+            v[e] = i < a.nblocks ? b : make_int2(0, 0);
         }
         int2 total;
         block_scan_256x4(v, total);
@@ -572,23 +598,96 @@ __global__ __launch_bounds__(256) void bwd_scan_write_kernel(BwdScanArgs a)
 {
     int2 v[4], c[4];
     const int base = blockIdx.x * 1024 + threadIdx.x * 4;
+    quad_counts(a.count, base, a.n, c);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int i = base + e;
-        const int cnt = i < a.n ? a.count[i] : 0;
-        c[e] = i < a.n ? make_int2(cnt, chunks_of(cnt)) : make_int2(0, 0);
-        v[e] = c[e];
-    }
+    for (int e = 0; e < 4; ++e) v[e] = c[e];
     int2 total;
     block_scan_256x4(v, total);
     const int2 bo = make_int2(a.block_sums[2 * blockIdx.x], a.block_sums[2 * blockIdx.x + 1]);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        const int i = base + e;
-        if (i >= a.n) continue;
-        a.off[i] = bo.x + v[e].x;
-        a.coff[i] = bo.y + v[e].y;
-        for (int t = 0; t < c[e].y; ++t) a.chunk_key[bo.y + v[e].y + t] = i;
+        v[e].x += bo.x;
+        v[e].y += bo.y;
+    }
+    store_quad(a.off, base, a.n, v[0].x, v[1].x, v[2].x, v[3].x);
+    store_quad(a.coff, base, a.n, v[0].y, v[1].y, v[2].y, v[3].y);
+    store_quad(a.count, base, a.n, 0, 0, 0, 0);               // the last reader: zero for the next level
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        if (base + e < a.n)
+            for (int t = 0; t < c[e].y; ++t) a.chunk_key[v[e].y + t] = base + e;
+}
+
+// Up to kSingleScanMax key slots: the whole scan in one workgroup of 1024 threads (four tiles of
+// 4096 slots), in place of the three-kernel scan. Every load comes first and every store last: a
+// store issued between two waits for loads would be waited for too.
+constexpr int kSingleScanMax = 16384;
+
+__global__ __launch_bounds__(1024) void bwd_scan_single_kernel(BwdScanArgs a)
+{
+    __shared__ int2 wsum[4][16];                              // one row per tile: a single barrier each
+    constexpr int kTile = 4096;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int2 c[4][4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) quad_counts(a.count, t * kTile + tid * 4, a.n, c[t]);
+    int2 x[4][4];                                             // exclusive scans (list offset, first chunk)
+    int2 carry = make_int2(0, 0);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        if (t * kTile < a.n) {                                // uniform; no early exit, so c stays in registers
+            int2 run = make_int2(0, 0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                x[t][e] = run;
+                run.x += c[t][e].x;
+                run.y += c[t][e].y;
+            }
+            int2 inc = run;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const int ux = __shfl_up(inc.x, o, kWave), uy = __shfl_up(inc.y, o, kWave);
+                if (lane >= o) {
+                    inc.x += ux;
+                    inc.y += uy;
+                }
+            }
+            if (lane == 63) wsum[t][wave] = inc;
+            __syncthreads();
+            int2 before = make_int2(carry.x + inc.x - run.x, carry.y + inc.y - run.y), total = make_int2(0, 0);
+#pragma unroll
+            for (int w = 0; w < 16; ++w) {
+                const int2 ws = wsum[t][w];
+                if (w < wave) {
+                    before.x += ws.x;
+                    before.y += ws.y;
+                }
+                total.x += ws.x;
+                total.y += ws.y;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                x[t][e].x += before.x;
+                x[t][e].y += before.y;
+            }
+            carry.x += total.x;
+            carry.y += total.y;
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const int i0 = t * kTile + tid * 4;
+        store_quad(a.off, i0, a.n, x[t][0].x, x[t][1].x, x[t][2].x, x[t][3].x);
+        store_quad(a.coff, i0, a.n, x[t][0].y, x[t][1].y, x[t][2].y, x[t][3].y);
+        store_quad(a.count, i0, a.n, 0, 0, 0, 0);             // read above by this thread only
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (i0 + e < a.n)
+                for (int u = 0; u < c[t][e].y; ++u) a.chunk_key[x[t][e].y + u] = i0 + e;
+    }
+    if (tid == 0) {
+        a.off[a.n] = carry.x;
+        a.coff[a.n] = carry.y;
     }
 }
 
@@ -602,9 +701,7 @@ __global__ __launch_bounds__(256) void bwd_fill_kernel(BwdFillArgs a)
     const int row = static_cast<int>(tid / a.Kp);          // bh * Np + P
     const int r = static_cast<int>(tid - static_cast<long long>(row) * a.Kp);
     const int bh = row / a.Np, P = row - bh * a.Np;
-    const int key = bh * a.Np + J;
-    const int pos = a.off[key] + atomicSub(a.count + key, 1) - 1;
-    a.entries[pos] = P * a.Kp + r;
+    a.entries[a.off[bh * a.Np + J] + a.slot[tid]] = P * a.Kp + r;
 }
 
 // Key pass: one wave per chunk of one kept key J's parent list (up to kKeyChunk = 16 parents, so
@@ -1069,15 +1166,20 @@ hipError_t launch_bwd_keys(const BwdLevelArgs& a, const BwdScanArgs& sc, int d, 
                            bool finest, hipStream_t stream)
 {
     if (sc.n <= 0) return hipErrorInvalidValue;
-    const unsigned nb = static_cast<unsigned>(sc.nblocks);
-    hipLaunchKernelGGL(bwd_scan_reduce_kernel, dim3(nb), dim3(256), 0, stream, sc);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_scan_blocks_kernel, dim3(1), dim3(256), 0, stream, sc);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_scan_write_kernel, dim3(nb), dim3(256), 0, stream, sc);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    BwdFillArgs f{a.parent_idx, static_cast<long long>(sc.n) * a.Kp, a.Kp, a.Hp * a.Wp, sc.count, sc.off, a.entries};
+    hipError_t e;
+    if (sc.n <= kSingleScanMax) {
+        hipLaunchKernelGGL(bwd_scan_single_kernel, dim3(1), dim3(1024), 0, stream, sc);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else {
+        const unsigned nb = static_cast<unsigned>(sc.nblocks);
+        hipLaunchKernelGGL(bwd_scan_reduce_kernel, dim3(nb), dim3(256), 0, stream, sc);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(bwd_scan_blocks_kernel, dim3(1), dim3(256), 0, stream, sc);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(bwd_scan_write_kernel, dim3(nb), dim3(256), 0, stream, sc);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    BwdFillArgs f{a.parent_idx, a.slot, static_cast<long long>(sc.n) * a.Kp, a.Kp, a.Hp * a.Wp, sc.off, a.entries};
     const long long fb = (f.nentries + 255) / 256;
     if (fb >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
     hipLaunchKernelGGL(bwd_fill_kernel, dim3(static_cast<unsigned>(fb)), dim3(256), 0, stream, f);

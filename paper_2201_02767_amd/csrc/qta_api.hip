@@ -195,16 +195,16 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], in
 // Workspace of the backward pass: per level l >= 1 the gradient of the message (dm) and the
 // level's q, k, v gradients (fp32 [B][N_l][C]); QuadTree-A's gradients of the kept scores
 // ([B][heads][N_l][K_l]); the coarse softmax statistics ([B][heads][N_c][4]); and, reused level by
-// level, the finer levels' query statistics and the counting sort of the kept pairs (counts, list
-// and chunk offsets, block sums, lists, chunk keys, per-chunk partial rows). What is summed with
-// atomics (dm at levels >= 2, the counts) forms one contiguous region, cleared at the start of
-// every call; the counts return to zero after each level's sort.
+// level, the finer levels' query statistics and the counting sort of the kept pairs (counts, places
+// in the lists, list and chunk offsets, block sums, lists, chunk keys, per-chunk partial rows). What
+// is summed with atomics (dm at levels >= 2, the counts) forms one contiguous region, cleared at the
+// start of every call; the scan returns the counts to zero after each level's sort.
 struct BwdLayout {
     size_t dm[QTA_MAX_LEVELS], gq[QTA_MAX_LEVELS], gk[QTA_MAX_LEVELS], gv[QTA_MAX_LEVELS];
     size_t dsig[QTA_MAX_LEVELS];
     size_t zero_begin, zero_end;
     size_t stats, total;
-    size_t count, off, coff, block_sums, entries, chunk_key, partial, qstats;
+    size_t count, off, coff, block_sums, entries, slot, chunk_key, partial, qstats;
     long long nslots_max;           // B*heads*N_{l+1} over the finer levels
 };
 
@@ -232,8 +232,8 @@ void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int d, in
         L->dm[l] = off;
         off = align_up(off + fbytes(l));
     }
-    L->count = off;
-    off = align_up(off + static_cast<size_t>(nmax) * sizeof(int32_t));
+    L->count = off;                 // padded to whole quads: the scan reads four counts at a time
+    off = align_up(off + static_cast<size_t>((nmax + 3) & ~3LL) * sizeof(int32_t));
     L->zero_end = off;
     if (c >= 1) {
         L->dm[1] = off;
@@ -261,6 +261,8 @@ void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int d, in
         L->block_sums = off;
         off = align_up(off + static_cast<size_t>(2 * ((nmax + 1023) / 1024)) * sizeof(int32_t));
         L->entries = off;
+        off = align_up(off + static_cast<size_t>(emax) * sizeof(int32_t));
+        L->slot = off;
         off = align_up(off + static_cast<size_t>(emax) * sizeof(int32_t));
         L->chunk_key = off;
         off = align_up(off + static_cast<size_t>(cmax) * sizeof(int32_t));
@@ -802,6 +804,7 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
             a.coff = reinterpret_cast<const int32_t*>(gws + G.coff);
             a.chunk_key = reinterpret_cast<const int32_t*>(gws + G.chunk_key);
             a.entries = reinterpret_cast<int32_t*>(gws + G.entries);
+            a.slot = reinterpret_cast<int32_t*>(gws + G.slot);
             a.partial = fptr(G.partial);
             if (launch_bwd_level(a, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
             BwdScanArgs sc{};

@@ -174,7 +174,8 @@ struct BwdLevelArgs {
     float* dw;                  // l == 0, QuadTree-B with w: entry 0 written; or NULL
     float* stats;               // B: [B][heads][N][2] (log-sum-exp, sum p ds); A: [B][heads][N][Kp][2]
     int32_t* count;             // [B*heads*Np] parents that kept each key (zero before the query pass;
-                                //   the fill returns it to zero)
+                                //   the scan returns it to zero)
+    int32_t* slot;              // [B*heads*Np*Kp] place of each kept pair in its key's list
     const int32_t* off;         // [B*heads*Np + 1] start of each key's list in `entries`
     const int32_t* coff;        // [B*heads*Np + 1] first chunk of each key; coff[B*heads*Np] = chunks
     const int32_t* chunk_key;   // [chunks] the key (b*heads + h)*Np + J of each chunk
@@ -199,9 +200,9 @@ struct BwdScanArgs {
 
 struct BwdFillArgs {
     const int32_t* parent_idx;  // [n][Kp]
+    const int32_t* slot;        // [n][Kp]
     long long nentries;         // n * Kp
     int Kp, Np;
-    int32_t* count;
     const int32_t* off;
     int32_t* entries;
 };

@@ -140,7 +140,10 @@ def test_backward_repeated_calls(dev):
 
 
 def test_autograd_function(dev):
-    """attention() under autograd gives the gradients of the plan's backward, in q's dtype."""
+    """attention() under autograd gives the gradients of the plan's backward, in q's dtype. dw has
+    one writer per element (identical bits); dq, dk and dv take sums made with atomics (the
+    message gradients at levels >= 2, the key lists' order), so they are compared to the bf16
+    rounding of the plan's gradients."""
     announce("autograd function, 2 x 24 x 20, bf16, B")
     B, H, W, heads, d, L = 2, 24, 20, 2, 32, 3
     q, k, v = (dev_t(rand(500 + i, (B, H, W, heads, d), "bf16"), "bf16", dev).requires_grad_() for i in range(3))
@@ -153,7 +156,7 @@ def test_autograd_function(dev):
     dq, dk, dv, dw = plan.backward(q.detach(), k.detach(), v.detach(), g, w.detach())
     torch.cuda.synchronize()
     assert q.grad.dtype == torch.bfloat16 and w.grad.dtype == torch.float32
-    assert torch.equal(q.grad, dq.to(torch.bfloat16))
+    assert grad_err(to_np(q.grad.float()), to_np(dq)) <= 1e-2
     assert grad_err(to_np(k.grad.float()), to_np(dk)) <= 1e-2
     assert grad_err(to_np(v.grad.float()), to_np(dv)) <= 1e-2
     assert torch.equal(w.grad, dw)
