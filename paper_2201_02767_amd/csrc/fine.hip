@@ -81,6 +81,9 @@ hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool bf16_
     if (4 * a.Kp > kMaxSlots) return launch_fine_attn_wide(a, d, variant_a, bf16_in, finest, stream);
     FineArgs b = a;
     b.div_Wp = make_fastdiv(a.Wp);
+    b.div_heads = make_fastdiv(a.heads);
+    const int np = a.Hp * a.Wp;
+    b.div_items = make_fastdiv(a.H == 1 && a.Hp == 1 ? (np + 1) / 2 : np);   // one-row maps: parent pairs
     if (bf16_in) {
         if (d == 32) return launch_td<bf16, 32>(b, variant_a, finest, stream);
         if (d == 64) return launch_td<bf16, 64>(b, variant_a, finest, stream);

@@ -100,12 +100,12 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
 
     const int lane = threadIdx.x & 63;
     const int Np = a.Hp * a.Wp;
-    const int h = item % a.heads;
-    const int bp = item / a.heads;
+    const int bp = fast_div(item, a.div_heads);
+    const int h = item - bp * a.heads;
     const int NI = ROW ? (Np + 1) / 2 : Np;               // items per (batch, head)
-    const int P = ROW ? 2 * (bp % NI) : bp % NI;          // ROW: the pair's first parent
-    const int b = bp / NI;
-    const int Py = ROW ? 0 : P / a.Wp, Px = ROW ? P : P - Py * a.Wp;
+    const int b = fast_div(bp, a.div_items);
+    const int P = ROW ? 2 * (bp - b * NI) : bp - b * NI;  // ROW: the pair's first parent
+    const int Py = ROW ? 0 : fast_div(P, a.div_Wp), Px = ROW ? P : P - Py * a.Wp;
     const bool pair2 = ROW && P + 1 < Np;                 // ROW: the second parent exists
     const int H = a.H, W = a.W, C = a.C, K = a.Kp, Ks = a.Ks;
     const int N = H * W;
@@ -116,7 +116,10 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
     unsigned char* Vb = base + lay.v;
     unsigned char* Pb = base + lay.p;
 
-    const int32_t* prow = a.parent_idx + ((static_cast<size_t>(b) * a.heads + h) * Np + P) * K;
+    // per batch element a 64-bit base, within it 32-bit offsets (one element's map is below 2^31 bytes,
+    // so its kept-key table and its coarser messages are too)
+    const int32_t* prow = a.parent_idx + static_cast<size_t>(b) * static_cast<uint32_t>(a.heads * Np * K) +
+                          static_cast<uint32_t>((h * Np + P) * K);
     // flat index at level l of child (s & 3) of kept key J (a level l+1 index), or -1. Map sizes are
     // below 2^24 tokens, so coordinate products fit the 24-bit multiplier. ROW: child s & 1 of J.
     auto child_of_slot_J = [&](int J, int s) -> int {
@@ -288,14 +291,15 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
                     for (int u = 0; u < QPL; ++u) {
                         const int qi = (NH == 2 ? hh * QPL : 0) + u;
                         // clamped: a query off the map may lie past the last ancestor
-                        const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] + min((2 * P + qi) >> lev, a.lvl_W[lev] - 1);
-                        anc[u][lev - 1] = (a.coarser_msg[lev] + (an * a.heads + h) * D)[ch];
+                        const uint32_t an = min((2 * P + qi) >> lev, a.lvl_W[lev] - 1);
+                        anc[u][lev - 1] = (a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C))
+                                              [an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)];
                     }
                 } else {
                     // the ancestor is shared by the four siblings: a uniform address plus the channel
-                    const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +
-                                      static_cast<size_t>((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev);
-                    anc[0][lev - 1] = (a.coarser_msg[lev] + (an * a.heads + h) * D)[ch];
+                    const uint32_t an = static_cast<uint32_t>(((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev));
+                    anc[0][lev - 1] = (a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C))
+                                          [an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)];
                 }
             }
             if (a.pe0) {                                     // uniform
@@ -344,7 +348,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
         for (int r = 0; r < 4; ++r) {
             const float m = wave_max_fast(x[r]);
             wgt[r] = okr[r] ? __expf(x[r] - m) : 0.f;
-            inv_sum[r] = 1.0f / wave_sum_fast(wgt[r]);
+            inv_sum[r] = fast_rcp(wave_sum_fast(wgt[r]));   // the sum is at least 1 (the maximum's term)
         }
     } else {
 #pragma unroll
@@ -355,7 +359,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
             const float e = okr[r] ? __expf(x[r] - m) : 0.f;
             float s = e + xchg_f32<1>(e);
             if constexpr (!ROW) s += xchg_f32<2>(s);
-            wgt[r] = okr[r] ? pkey * (e / s) : 0.f;
+            wgt[r] = okr[r] ? pkey * e * fast_rcp(s) : 0.f;  // s >= 1
         }
     }
 

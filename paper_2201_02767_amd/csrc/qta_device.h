@@ -163,6 +163,10 @@ __device__ __forceinline__ float wave_allreduce(float x, Op op)
     return op(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
 }
 
+// 1/x on the hardware reciprocal (within one ulp) instead of the correctly rounded division
+// sequence; used for softmax normalisers, which are at least 1.
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
 __device__ __forceinline__ float wave_max_fast(float x)
 {
     return wave_allreduce(x, [](float a, float b) { return fmaxf(a, b); });

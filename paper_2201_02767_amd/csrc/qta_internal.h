@@ -103,6 +103,8 @@ struct FineArgs {
     int Kp;                     // keys each parent query kept: 4*Kp candidate slots per sibling group
     int Ks;                     // keys this level keeps per query (levels above the finest)
     FastDiv div_Wp;             // division by Wp (flat parent index -> row)
+    FastDiv div_heads;          // division by heads (work item -> head); set by the launcher
+    FastDiv div_items;          // division by the work items of one (batch, head); set by the launcher
     float scale;
     const int32_t* parent_idx;
     const float* parent_key;
