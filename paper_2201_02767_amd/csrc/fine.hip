@@ -1,8 +1,8 @@
 // Gathered fine attention at the finer levels: one wave per (parent query, head) work item, or per
-// pair of neighbouring parents on maps of one row; the per-item work (gather, MFMA logits, softmax,
-// top-K, messages, the finest level's combination) is fine_item in fine_item.h. A workgroup holds
-// four independent waves; nothing synchronises across waves. Candidate sets of more than 64 slots
-// run the kernel of fine_wide.hip.
+// pair of neighbouring parents on maps of one row; the per-item work (its independent loads in
+// item_head, then gather, MFMA logits, softmax, top-K, messages, the finest level's combination in
+// fine_item, both in fine_item.h). A workgroup holds four independent waves; nothing synchronises
+// across waves. Candidate sets of more than 64 slots run the kernel of fine_wide.hip.
 #include "fine_item.h"
 
 namespace qta {
@@ -17,13 +17,15 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     const int wave = threadIdx.x >> 6;
     const int wpb = blockDim.x >> 6;
     const int np = a.Hp * a.Wp;
-    const long long nitems = static_cast<long long>(a.B) * a.heads * (ROW ? (np + 1) / 2 : np);
+    const int nitems = a.B * a.heads * (ROW ? (np + 1) / 2 : np);   // below 2^31 (checked by the launcher)
     // the work item is the same for the whole wave: keep it (and all that derives from it) scalar
     const int item = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, gridDim.x) * wpb + wave);
     if (item >= nitems) return;            // whole wave leaves; only wave-level syncs follow
     extern __shared__ __align__(16) unsigned char smem[];
     const int nsp = (4 * a.Kp + 15) & ~15;
-    fine_item<T, D, NSP, VA, FINEST, ROW>(a, item, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
+    ItemHead<T, D, NSP, ROW> hd;
+    item_head<T, D, NSP, VA, ROW>(a, item, hd);
+    fine_item<T, D, NSP, VA, FINEST, ROW>(a, hd, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
 }
 
 template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW>

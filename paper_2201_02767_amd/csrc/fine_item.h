@@ -75,8 +75,78 @@ __device__ __forceinline__ float pick4(const float (&v)[4], int i)
     return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
 }
 
-// One work item (parent query P at level l+1, head h; item = (b*Np + P)*heads + h) on the calling
-// wave, whose private LDS region of wave_lds<T, D>(nsp).total bytes starts at `base`. The whole
+// The loads of a work item that need no other load, with the item's coordinates: its parents' kept
+// keys (each lane's gather key of every slot tile), their scores (QuadTree-A) and the query rows
+// (MFMA A operand: row n16 holds query n16 & 3). Vector memory counters drain in order, and a load
+// inside a divergent branch makes the compiler wait for it at the join, so every load here is
+// unconditional, at a clamped address that is always in bounds, with validity applied when the
+// value is used.
+template <typename T, int D, int NSP, bool ROW>
+struct ItemHead {
+    int b, h, P, Py, Px;
+    bool pair2;                 // ROW: the second parent exists
+    bool q_ok;                  // this lane's query (n16 & 3) lies on the map
+    int J_g[NSP / 16];
+    float pkey;
+    uint4 qa[D * sizeof(T) / 64];
+};
+
+template <typename T, int D, int NSP, bool VA, bool ROW>
+__device__ __forceinline__ void item_head(const FineArgs& a, const int item, ItemHead<T, D, NSP, ROW>& hd)
+{
+    constexpr int TB = sizeof(T);
+    constexpr int RB = D * TB;
+    constexpr int NJ = RB / 64;
+    constexpr int NT = NSP / 16;
+    const int lane = threadIdx.x & 63;
+    const int n16 = lane & 15, g = lane >> 4;
+    const int Np = a.Hp * a.Wp;
+    const int bp = fast_div(item, a.div_heads);
+    const int h = item - bp * a.heads;
+    const int NI = ROW ? (Np + 1) / 2 : Np;               // items per (batch, head)
+    const int b = fast_div(bp, a.div_items);
+    const int P = ROW ? 2 * (bp - b * NI) : bp - b * NI;  // ROW: the pair's first parent
+    const int Py = ROW ? 0 : fast_div(P, a.div_Wp), Px = ROW ? P : P - Py * a.Wp;
+    const bool pair2 = ROW && P + 1 < Np;
+    const int H = a.H, W = a.W, C = a.C, K = a.Kp;
+    hd.b = b;
+    hd.h = h;
+    hd.P = P;
+    hd.Py = Py;
+    hd.Px = Px;
+    hd.pair2 = pair2;
+    // per batch element a 64-bit base, within it 32-bit offsets (one element's map is below 2^31 bytes,
+    // so its kept-key table and its coarser messages are too)
+    const int32_t* prow = a.parent_idx + static_cast<size_t>(b) * static_cast<uint32_t>(a.heads * Np * K) +
+                          static_cast<uint32_t>((h * Np + P) * K);
+    // the kept-key entry of slot s: s >> 2 (ROW: s >> 1, the pair's two rows being contiguous)
+    constexpr int kSlotShift = ROW ? 1 : 2;
+    const int last_sel = (ROW && pair2 ? 2 * K : K) - 1;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) hd.J_g[t] = prow[min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)];
+    hd.pkey = 0.f;
+    if constexpr (VA)
+        hd.pkey = a.parent_key[((static_cast<size_t>(b) * a.heads + h) * Np + P) * K + min(lane >> kSlotShift, last_sel)];
+    const int qi = n16 & 3;
+    const int qy = ROW ? 0 : 2 * Py + (qi >> 1), qx = ROW ? 2 * P + qi : 2 * Px + (qi & 1);
+    hd.q_ok = qy < H && qx < W;
+    const int qyc = qy < H ? qy : H - 1, qxc = qx < W ? qx : W - 1;
+    // uniform base of this (batch, head) plus a 32-bit per-lane offset. ROW, blocked: query 4p + qi
+    // is child qi & 1 of parent 2p + (qi >> 1)
+    const unsigned char* qbase = static_cast<const unsigned char*>(a.q) +
+        (a.q_blocked ? ((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 * RB
+                     : (static_cast<size_t>(b) * H * W * C + h * D) * TB);
+    // (a query off the map may belong to a parent past the last one: read the first block instead)
+    const int qblk = ROW ? (hd.q_ok ? (qi >> 1) * 4 + (qi & 1) : 0) : qi;
+    const uint32_t qoff = a.q_blocked ? static_cast<uint32_t>(qblk * RB)
+                                      : static_cast<uint32_t>(__mul24(qyc, W) + qxc) * static_cast<uint32_t>(C * TB);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+        hd.qa[j] = *reinterpret_cast<const uint4*>(qbase + (qoff + static_cast<uint32_t>((g + 4 * j) * 16)));
+}
+
+// One work item (parent query P at level l+1, head h; item = (b*Np + P)*heads + h), whose
+// independent loads item_head has issued, on the calling wave, whose private LDS region of wave_lds<T, D>(nsp).total bytes starts at `base`. The whole
 // wave must call it with the same item.
 // ROW: maps of one row (attention along epipolar lines). A parent there has only two children and
 // its kept keys two children each, so one item takes two neighbouring parents P0 = 2p, P1 = 2p + 1
@@ -84,7 +154,7 @@ __device__ __forceinline__ float pick4(const float (&v)[4], int i)
 // s = 2*(half*K + r) + c is child c of kept key r of parent `half`, and query q uses the slots of
 // half q >> 1 only.
 template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW = false>
-__device__ __forceinline__ void fine_item(const FineArgs& a, const int item, unsigned char* const base)
+__device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D, NSP, ROW>& hd, unsigned char* const base)
 {
     using S = Storage<T>;
     constexpr bool kBf16 = sizeof(T) == 2;
@@ -100,13 +170,8 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
 
     const int lane = threadIdx.x & 63;
     const int Np = a.Hp * a.Wp;
-    const int bp = fast_div(item, a.div_heads);
-    const int h = item - bp * a.heads;
-    const int NI = ROW ? (Np + 1) / 2 : Np;               // items per (batch, head)
-    const int b = fast_div(bp, a.div_items);
-    const int P = ROW ? 2 * (bp - b * NI) : bp - b * NI;  // ROW: the pair's first parent
-    const int Py = ROW ? 0 : fast_div(P, a.div_Wp), Px = ROW ? P : P - Py * a.Wp;
-    const bool pair2 = ROW && P + 1 < Np;                 // ROW: the second parent exists
+    const int b = hd.b, h = hd.h, P = hd.P, Py = hd.Py, Px = hd.Px;
+    const bool pair2 = hd.pair2;
     const int H = a.H, W = a.W, C = a.C, K = a.Kp, Ks = a.Ks;
     const int N = H * W;
     const int nslot = 4 * K;
@@ -116,10 +181,6 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
     unsigned char* Vb = base + lay.v;
     unsigned char* Pb = base + lay.p;
 
-    // per batch element a 64-bit base, within it 32-bit offsets (one element's map is below 2^31 bytes,
-    // so its kept-key table and its coarser messages are too)
-    const int32_t* prow = a.parent_idx + static_cast<size_t>(b) * static_cast<uint32_t>(a.heads * Np * K) +
-                          static_cast<uint32_t>((h * Np + P) * K);
     // flat index at level l of child (s & 3) of kept key J (a level l+1 index), or -1. Map sizes are
     // below 2^24 tokens, so coordinate products fit the 24-bit multiplier. ROW: child s & 1 of J.
     auto child_of_slot_J = [&](int J, int s) -> int {
@@ -144,48 +205,18 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const int item, uns
         }
     };
 
-    // ---- 1. loads. Vector memory counters drain in order, and a load inside a divergent branch
-    //      makes the compiler wait for it at the join, so every load below is unconditional, at a
-    //      clamped address that is always in bounds, with validity applied when the value is used.
-    //      Phase A holds every load that needs no other load; phase B the gathers. ----
+    // ---- 1. loads: item_head issued the phase A loads (kept keys, scores, query rows); phase B,
+    //      the gathers, needs the kept keys ----
     const int n16 = lane & 15, g = lane >> 4;
     const int ntile = nsp / 16;
-    // phase A: the parents' kept keys (own slot and this lane's gather slot of each tile), the
-    // parents' scores (A) and the query chunks (A operand: row n16 holds query n16 & 3)
-    // the kept-key entry of slot s: s >> 2 (ROW: s >> 1, the pair's two rows being contiguous)
-    constexpr int kSlotShift = ROW ? 1 : 2;
-    const int last_sel = (ROW && pair2 ? 2 * K : K) - 1;
-    int J_g[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) J_g[t] = prow[min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)];
+    const int (&J_g)[NT] = hd.J_g;
     // lane = slot 16g + n16: tile g's gather key
     int J_own_raw = -1;
 #pragma unroll
     for (int t = 0; t < NT; ++t) J_own_raw = g == t ? J_g[t] : J_own_raw;
-    float pkey = 0.f;
-    if constexpr (VA)
-        pkey = a.parent_key[((static_cast<size_t>(b) * a.heads + h) * Np + P) * K + min(lane >> kSlotShift, last_sel)];
-    uint4 qa[NJ];
-    bool q_ok;
-    {
-        const int qi = n16 & 3;
-        int qy, qx;
-        query_yx(qi, qy, qx);
-        q_ok = qy < H && qx < W;
-        const int qyc = qy < H ? qy : H - 1, qxc = qx < W ? qx : W - 1;
-        // uniform base of this (batch, head) plus a 32-bit per-lane offset. ROW, blocked: query 4p + qi
-        // is child qi & 1 of parent 2p + (qi >> 1)
-        const unsigned char* qbase = static_cast<const unsigned char*>(a.q) +
-            (a.q_blocked ? ((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 * RB
-                         : (static_cast<size_t>(b) * N * C + h * D) * TB);
-        // (a query off the map may belong to a parent past the last one: read the first block instead)
-        const int qblk = ROW ? (q_ok ? (qi >> 1) * 4 + (qi & 1) : 0) : qi;
-        const uint32_t qoff = a.q_blocked ? static_cast<uint32_t>(qblk * RB)
-                                          : static_cast<uint32_t>(__mul24(qyc, W) + qxc) * static_cast<uint32_t>(C * TB);
-#pragma unroll
-        for (int j = 0; j < NJ; ++j)
-            qa[j] = *reinterpret_cast<const uint4*>(qbase + (qoff + static_cast<uint32_t>((g + 4 * j) * 16)));
-    }
+    const float pkey = hd.pkey;
+    const uint4 (&qa)[NJ] = hd.qa;
+    const bool q_ok = hd.q_ok;
     // phase B: the gathers. NHWC: child f of this head at kg + f*C*TB. Blocked: the four children
     // of kept key J are the 4*RB bytes at kg + J*4*RB (this (batch, head)'s blocks start at kg).
     const bool kvb = a.kv_blocked;
