@@ -99,11 +99,11 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
 
     const int lane = threadIdx.x & 63;
     const int Np = a.Hp * a.Wp;
-    const int h = item % a.heads;
-    const int bp = item / a.heads;
-    const int P = bp % Np;
-    const int b = bp / Np;
-    const int Py = P / a.Wp, Px = P - Py * a.Wp;
+    const int bp = fast_div(item, a.div_heads);
+    const int h = item - bp * a.heads;
+    const int b = fast_div(bp, a.div_Np);
+    const int P = bp - b * Np;
+    const int Py = fast_div(P, a.div_Wp), Px = P - Py * a.Wp;
     const int H = a.H, W = a.W, C = a.C, K = a.Kp;
     const int N = H * W;
     const int nslot = 4 * K;
@@ -175,7 +175,12 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             }
         }
     }
-    // level 0: w_{r,0} of the four queries (QuadTree-B; 1/L without w; 1 for A)
+    // level 0: w_{r,0} of the four queries (QuadTree-B; 1/L without w; 1 for A). Per batch element a
+    // 64-bit base, within it 32-bit offsets (one element's map is below 2^31 bytes, and so are its
+    // level weights and softmax statistics)
+    const size_t wq_off = static_cast<size_t>(b) * static_cast<uint32_t>(N * a.heads * a.levels);
+    const float* wq_b = a.w + wq_off;
+    float* const st_b = a.stats + static_cast<size_t>(b * a.heads + h) * static_cast<uint32_t>(N * 2 * (VA ? K : 1));
     float w0[4] = {1.f, 1.f, 1.f, 1.f};
     bool qv[4];
 #pragma unroll
@@ -184,7 +189,7 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
         qv[r] = ry < H && rx < W;
         if constexpr (FINEST && !VA) {
             const uint32_t rt = static_cast<uint32_t>(__mul24(min(ry, H - 1), W) + min(rx, W - 1));
-            w0[r] = a.w ? a.w[((static_cast<size_t>(b) * N + rt) * a.heads + h) * a.levels] : 1.0f / a.levels;
+            w0[r] = a.w ? wq_b[(rt * a.heads + h) * a.levels] : 1.0f / a.levels;
         }
     }
     // how many parents kept each key of level l+1 (for the key pass's counting sort); the count a
@@ -276,21 +281,21 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             const float m = wave_max_fast(x[r]);
             const float e = ok ? __expf(x[r] - m) : 0.f;
             const float sum = wave_sum_fast(e);
-            const float p = e / sum;
+            const float p = e * fast_rcp(sum);                // sum >= 1 (the maximum's term)
             const float Dr = wave_sum_fast(p * gsl[r]);
             dxr[r] = qv[r] ? p * (gsl[r] - Dr) : 0.f;
             // the key pass recomputes p = exp(x - lse) and needs D
             if (lane == 0 && qv[r]) {
                 const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
-                *reinterpret_cast<float2*>(a.stats + (bh * N + __mul24(ry, W) + rx) * 2) =
-                    make_float2(m + __logf(sum), Dr);
+                *reinterpret_cast<float2*>(st_b + static_cast<uint32_t>(__mul24(ry, W) + rx) * 2) =
+                    make_float2(m + fast_ln(sum), Dr);
             }
             if constexpr (FINEST) {
                 if (a.w && a.dw) {                            // uniform
                     const float dw0 = wave_sum_fast(p * acc_g[r]);
                     if (lane == 0 && qv[r]) {
                         const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
-                        a.dw[((static_cast<size_t>(b) * N + ry * W + rx) * a.heads + h) * a.levels] = dw0;
+                        a.dw[wq_off + static_cast<uint32_t>(((ry * W + rx) * a.heads + h) * a.levels)] = dw0;
                     }
                 }
             }
@@ -304,7 +309,7 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             const float e = ok ? __expf(x[r] - m) : 0.f;
             float sum = e + xchg_f32<1>(e);
             sum += xchg_f32<2>(sum);
-            const float tt = ok ? e / sum : 0.f;
+            const float tt = ok ? e * fast_rcp(sum) : 0.f;   // sum >= 1
             const float sc = pkey * tt;
             float ds = gsl[r];
             if constexpr (!FINEST) {
@@ -323,8 +328,8 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             // the key pass recomputes t = exp(x - lse) per kept parent key and needs sum t ds
             if ((lane & 3) == 0 && (lane >> 2) < K && qv[r]) {
                 const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
-                *reinterpret_cast<float2*>(a.stats + ((bh * N + __mul24(ry, W) + rx) * K + (lane >> 2)) * 2) =
-                    make_float2(m + __logf(sum), dsq);
+                *reinterpret_cast<float2*>(st_b + static_cast<uint32_t>((__mul24(ry, W) + rx) * K + (lane >> 2)) * 2) =
+                    make_float2(m + fast_ln(sum), dsq);
             }
         }
         if ((lane & 3) == 0 && (lane >> 2) < K) a.dsig_out[prow_off * K + (lane >> 2)] = dsig_acc;
@@ -759,13 +764,13 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     float* vws = reinterpret_cast<float*>(smem + lay.vw);
 
     const int key = a.chunk_key[chunk];      // bh * Np + J
-    const int bh = key / Np, J = key - bh * Np;
-    const int h = bh % a.heads, b = bh / a.heads;
+    const int bh = fast_div(key, a.div_Np), J = key - bh * Np;
+    const int b = fast_div(bh, a.div_heads), h = bh - b * a.heads;
     const int H = a.H, W = a.W, C = a.C, N = H * W, K = a.Kp;
     const int first = a.coff[key], nch = a.coff[key + 1] - first;
     const int beg = a.off[key] + (chunk - first) * kKeyChunk;
     const int nent = min(a.off[key + 1] - beg, kKeyChunk);
-    const int Jy = J / a.Wp, Jx = J - Jy * a.Wp;
+    const int Jy = fast_div(J, a.div_Wp), Jx = J - Jy * a.Wp;
     const int n16 = lane & 15, g = lane >> 4;
     const bool kvb = a.blocked;
     const unsigned char* qbase = static_cast<const unsigned char*>(a.q);
@@ -820,9 +825,9 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     const int ent_lane = nent > 0 ? a.entries[beg + min(lane, nent - 1)] : 0;   // an empty list reads nothing
     // where slot s's query lives: entry s >> 2, child s & 3
     auto slot_query = [&](int s, int ent, int& P, int& r, int& qtok, bool& qv) {
-        P = ent / K;
+        P = fast_div(ent, a.div_Kp);
         r = ent - P * K;
-        const int Py = P / a.Wp, Px = P - Py * a.Wp;
+        const int Py = fast_div(P, a.div_Wp), Px = P - Py * a.Wp;
         const int qi = s & 3;
         const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
         qv = (s >> 2) < nent && qy < H && qx < W;
@@ -1043,9 +1048,9 @@ __global__ __launch_bounds__(256) void bwd_key_reduce_kernel(BwdLevelArgs a, int
     const int key = static_cast<int>(tid / (4LL * q4n));
     const int first = a.coff[key], nch = a.coff[key + 1] - first;
     if (nch <= 1) return;
-    const int bh = key / Np, J = key - bh * Np;
-    const int h = bh % a.heads, b = bh / a.heads;
-    const int Jy = J / a.Wp, Jx = J - Jy * a.Wp;
+    const int bh = fast_div(key, a.div_Np), J = key - bh * Np;
+    const int b = fast_div(bh, a.div_heads), h = bh - b * a.heads;
+    const int Jy = fast_div(J, a.div_Wp), Jx = J - Jy * a.Wp;
     const int y = 2 * Jy + (c >> 1), x = 2 * Jx + (c & 1);
     if (y >= a.H || x >= a.W) return;
     float4 sk = make_float4(0.f, 0.f, 0.f, 0.f), sv = sk;
@@ -1146,12 +1151,22 @@ hipError_t launch_fill_zero(const FillRange* r, int n, hipStream_t stream)
     return hipGetLastError();
 }
 
+// The multiply-high constants of the divisions the level kernels make by the map sizes.
+BwdLevelArgs with_divisors(const BwdLevelArgs& a)
+{
+    BwdLevelArgs b = a;
+    b.div_Wp = make_fastdiv(a.Wp);
+    b.div_Np = make_fastdiv(a.Hp * a.Wp);
+    b.div_heads = make_fastdiv(a.heads);
+    b.div_Kp = make_fastdiv(a.Kp);
+    return b;
+}
+
 hipError_t launch_bwd_level(const BwdLevelArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
                             hipStream_t stream)
 {
     if (4 * a.Kp > 64) return hipErrorInvalidValue;
-    BwdLevelArgs b = a;
-    b.div_Wp = make_fastdiv(a.Wp);
+    const BwdLevelArgs b = with_divisors(a);
     if (use_bf16) {
         if (d == 32) return launch_level_td<bf16, 32>(b, variant_a, finest, stream);
         if (d == 64) return launch_level_td<bf16, 64>(b, variant_a, finest, stream);
@@ -1185,19 +1200,20 @@ hipError_t launch_bwd_keys(const BwdLevelArgs& a, const BwdScanArgs& sc, int d, 
     hipLaunchKernelGGL(bwd_fill_kernel, dim3(static_cast<unsigned>(fb)), dim3(256), 0, stream, f);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const long long max_chunks = static_cast<long long>(sc.n) + (static_cast<long long>(sc.n) * a.Kp + kKeyChunk - 1) / kKeyChunk;
+    const BwdLevelArgs k = with_divisors(a);
     if (use_bf16) {
-        if (d == 32) e = launch_key_td<bf16, 32>(a, variant_a, finest, max_chunks, stream);
-        else if (d == 64) e = launch_key_td<bf16, 64>(a, variant_a, finest, max_chunks, stream);
+        if (d == 32) e = launch_key_td<bf16, 32>(k, variant_a, finest, max_chunks, stream);
+        else if (d == 64) e = launch_key_td<bf16, 64>(k, variant_a, finest, max_chunks, stream);
         else return hipErrorInvalidValue;
     } else {
-        if (d == 32) e = launch_key_td<float, 32>(a, variant_a, finest, max_chunks, stream);
-        else if (d == 64) e = launch_key_td<float, 64>(a, variant_a, finest, max_chunks, stream);
+        if (d == 32) e = launch_key_td<float, 32>(k, variant_a, finest, max_chunks, stream);
+        else if (d == 64) e = launch_key_td<float, 64>(k, variant_a, finest, max_chunks, stream);
         else return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
     const long long rb = (static_cast<long long>(sc.n) * 4 * (d / 4) + 255) / 256;
     if (rb >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(bwd_key_reduce_kernel, dim3(static_cast<unsigned>(rb)), dim3(256), 0, stream, a, d);
+    hipLaunchKernelGGL(bwd_key_reduce_kernel, dim3(static_cast<unsigned>(rb)), dim3(256), 0, stream, k, d);
     return hipGetLastError();
 }
 

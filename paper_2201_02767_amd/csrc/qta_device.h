@@ -167,6 +167,10 @@ __device__ __forceinline__ float wave_allreduce(float x, Op op)
 // sequence; used for softmax normalisers, which are at least 1.
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
+// Natural logarithm from the hardware base-2 logarithm (about one ulp of log2 x); used for the
+// log-sum-exp of softmax sums, which are at least 1.
+__device__ __forceinline__ float fast_ln(float x) { return __builtin_amdgcn_logf(x) * 0.69314718056f; }
+
 __device__ __forceinline__ float wave_max_fast(float x)
 {
     return wave_allreduce(x, [](float a, float b) { return fmaxf(a, b); });

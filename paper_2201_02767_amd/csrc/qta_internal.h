@@ -159,7 +159,7 @@ struct BwdLevelArgs {
     int B, heads, H, W, Hp, Wp, C;
     int Kp;                     // keys each parent kept (4*Kp candidate slots, at most 64)
     int Ks;                     // keys this level keeps (l >= 1)
-    FastDiv div_Wp;
+    FastDiv div_Wp, div_Np, div_heads, div_Kp;   // divisions by Wp, Hp*Wp, heads, Kp; set by the launchers
     float scale;
     const int32_t* parent_idx;  // [B][heads][Np][Kp]
     const float* parent_key;    // QuadTree-A: the parents' scores sigma
