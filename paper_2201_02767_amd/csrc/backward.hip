@@ -62,16 +62,17 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(FillArgs a)
 // operand of dq) and per slot the four queries' logit gradients.
 struct BwdLds {
     int ks, dx, total;
-    int kpitch;     // floats per key row
+    int kpitch;     // elements per key row (bf16 rows stay bf16: exact, and half the LDS per wave)
 };
 
-template <int D>
+template <typename T, int D>
 __host__ __device__ inline BwdLds bwd_lds(int nsp)
 {
+    constexpr int TB = sizeof(T);
     BwdLds L;
-    L.kpitch = D + 4;
+    L.kpitch = TB == 2 ? D + 8 : D + 4;     // rows of 16-byte multiples
     L.ks = 0;
-    L.dx = L.ks + nsp * L.kpitch * 4;
+    L.dx = L.ks + nsp * L.kpitch * TB;
     L.total = L.dx + nsp * 16;
     return L;
 }
@@ -108,7 +109,7 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
     const int N = H * W;
     const int nslot = 4 * K;
     const int nsp = (nslot + 15) & ~15;
-    const BwdLds lay = bwd_lds<D>(nsp);
+    const BwdLds lay = bwd_lds<T, D>(nsp);
     float* Ks = reinterpret_cast<float*>(base + lay.ks);
     float* dxs = reinterpret_cast<float*>(base + lay.dx);      // [slot][4]
 
@@ -250,13 +251,12 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
                 for (int e = 0; e < E; ++e)
                     ag = __builtin_amdgcn_mfma_f32_16x16x4f32(dmA[j][e], vf[e], ag, 0, 0, 0);
             }
-            // the key row in fp32 (zeros for missing candidates)
-            float kf[E];
-            S::unpack(kk, kf);
-            float* krow = Ks + s * lay.kpitch + (g + 4 * j) * E;
-#pragma unroll
-            for (int e4 = 0; e4 < E; e4 += 4)
-                *reinterpret_cast<float4*>(krow + e4) = make_float4(kf[e4], kf[e4 + 1], kf[e4 + 2], kf[e4 + 3]);
+            // the key row in the storage type (zeros for missing candidates)
+            if constexpr (kBf16) {
+                *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(Ks) + s * lay.kpitch + (g + 4 * j) * E) = kk;
+            } else {
+                *reinterpret_cast<uint4*>(Ks + s * lay.kpitch + (g + 4 * j) * E) = kk;
+            }
         }
         // rows 4g + r of the products are query r for every g: lane 16g + n keeps tile g
 #pragma unroll
@@ -344,10 +344,14 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
         const int ch = 4 * cg + t4;
         const int sph = nsp / NH;
         float4_t o = {0.f, 0.f, 0.f, 0.f};
-        const float* kcol = Ks + 4 * cg + t4;
         for (int st = 0; st < sph; ++st) {
             const int sl = hh * sph + st;
-            o = __builtin_amdgcn_mfma_f32_4x4x1f32(dxs[sl * 4 + t4], kcol[sl * lay.kpitch], o, 0, 0, 0);
+            float kv;
+            if constexpr (kBf16)
+                kv = bf16_bits_to_f32(reinterpret_cast<const uint16_t*>(Ks)[sl * lay.kpitch + 4 * cg + t4]);
+            else
+                kv = Ks[sl * lay.kpitch + 4 * cg + t4];
+            o = __builtin_amdgcn_mfma_f32_4x4x1f32(dxs[sl * 4 + t4], kv, o, 0, 0, 0);
         }
         if constexpr (NH == 2) {
 #pragma unroll
@@ -429,14 +433,14 @@ __global__ __launch_bounds__(256) void bwd_level_kernel(BwdLevelArgs a)
     if (item >= nitems) return;            // whole wave leaves; only wave-level syncs follow
     extern __shared__ __align__(16) unsigned char smem[];
     const int nsp = (4 * a.Kp + 15) & ~15;
-    bwd_item<T, D, NSP, VA, FINEST>(a, item, smem + static_cast<size_t>(wave) * bwd_lds<D>(nsp).total);
+    bwd_item<T, D, NSP, VA, FINEST>(a, item, smem + static_cast<size_t>(wave) * bwd_lds<T, D>(nsp).total);
 }
 
 template <typename T, int D, int NSP, bool VA, bool FINEST>
 hipError_t launch_level_one(const BwdLevelArgs& a, hipStream_t stream)
 {
     const int nsp = (4 * a.Kp + 15) & ~15;
-    const size_t wave_bytes = bwd_lds<D>(nsp).total;
+    const size_t wave_bytes = bwd_lds<T, D>(nsp).total;
     int wpb = 4;
     while (wpb > 1 && wpb * wave_bytes > 64 * 1024) --wpb;
     if (wpb * wave_bytes > device_max_lds()) return hipErrorInvalidValue;
