@@ -700,7 +700,8 @@ __global__ __launch_bounds__(1024) void bwd_scan_single_kernel(BwdScanArgs a)
     }
 }
 
-// Every kept (parent, rank) pair into the list of the key it kept; the counts return to zero.
+// Every kept (parent, rank) pair into the list of the key it kept, at the place its count atomic
+// handed out in the query pass.
 __global__ __launch_bounds__(256) void bwd_fill_kernel(BwdFillArgs a)
 {
     const long long tid = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -725,16 +726,20 @@ __global__ __launch_bounds__(256) void bwd_fill_kernel(BwdFillArgs a)
 // counter and device-scope fences, was ten times slower: every such fence writes back the L2.)
 struct KeyLds {
     int rows, dx, vw, total;
-    int pitch;      // floats per row
+    int pitch;      // elements per row
 };
 
-template <int D>
+// The finest level's rows (the queries, then dout, whose w_0 the weights vw take instead) are bf16
+// values for bf16 inputs and stay bf16: exact, and half the LDS per wave. Coarser levels' dm rows
+// are fp32.
+template <typename T, int D, bool FINEST>
 __host__ __device__ inline KeyLds key_lds()
 {
+    constexpr int RB = sizeof(T) == 2 && FINEST ? 2 : 4;     // bytes per row element
     KeyLds L;
-    L.pitch = D + 4;
+    L.pitch = RB == 2 ? D + 8 : D + 4;                     // rows of 16-byte multiples
     L.rows = 0;
-    L.dx = L.rows + 4 * kKeyChunk * L.pitch * 4;
+    L.dx = L.rows + 4 * kKeyChunk * L.pitch * RB;
     L.vw = L.dx + 4 * kKeyChunk * 16;
     L.total = L.vw + 4 * kKeyChunk * 16;
     return L;
@@ -762,7 +767,13 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     const int chunk = __builtin_amdgcn_readfirstlane(static_cast<int>(blockIdx.x));
     if (chunk >= a.coff[n]) return;          // whole wave
     extern __shared__ __align__(16) unsigned char smem[];
-    const KeyLds lay = key_lds<D>();
+    const KeyLds lay = key_lds<T, D, FINEST>();
+    constexpr bool kRows16 = kBf16 && FINEST;                // rows kept as bf16
+    uint16_t* const Rs16 = reinterpret_cast<uint16_t*>(smem + lay.rows);
+    auto row_elem = [&](int sl, int c) -> float {
+        if constexpr (kRows16) return bf16_bits_to_f32(Rs16[sl * lay.pitch + c]);
+        else return reinterpret_cast<const float*>(smem + lay.rows)[sl * lay.pitch + c];
+    };
     float* Rs = reinterpret_cast<float*>(smem + lay.rows);    // q rows, then dm rows
     float* dxs = reinterpret_cast<float*>(smem + lay.dx);     // [slot][4 keys]
     float* vws = reinterpret_cast<float*>(smem + lay.vw);
@@ -841,8 +852,9 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     const int ntile = (nent + 3) / 4;                         // tiles that hold parents
     const int nsp = 16 * ntile;
     float acc_x[4] = {0.f, 0.f, 0.f, 0.f}, acc_g[4] = {0.f, 0.f, 0.f, 0.f};
-    // each tile's dm chunks (level 0: w_0 dout), kept for dv
-    float mreg[NT][FINEST ? NJ * E : NJF * 4];
+    // each tile's dm chunks (level 0: w_0 dout; bf16: dout as stored), kept for dv
+    float mreg[NT][kRows16 ? 1 : (FINEST ? NJ * E : NJF * 4)];
+    uint4 dreg[kRows16 ? NT : 1][kRows16 ? NJ : 1];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         if (t >= ntile) break;                                // uniform
@@ -875,13 +887,17 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
                 ax = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kA[j].z), __uint_as_float(qB[j].z), ax, 0, 0, 0);
                 ax = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kA[j].w), __uint_as_float(qB[j].w), ax, 0, 0, 0);
             }
-            // the query row in fp32 for dk
-            float qf[E];
-            S::unpack(qB[j], qf);
-            float* qd = Rs + s * lay.pitch + (g + 4 * j) * E;
+            // the query row for dk (fp32, or bf16 as stored)
+            if constexpr (kRows16) {
+                *reinterpret_cast<uint4*>(Rs16 + s * lay.pitch + (g + 4 * j) * E) = qB[j];
+            } else {
+                float qf[E];
+                S::unpack(qB[j], qf);
+                float* qd = Rs + s * lay.pitch + (g + 4 * j) * E;
 #pragma unroll
-            for (int e4 = 0; e4 < E; e4 += 4)
-                *reinterpret_cast<float4*>(qd + e4) = make_float4(qf[e4], qf[e4 + 1], qf[e4 + 2], qf[e4 + 3]);
+                for (int e4 = 0; e4 < E; e4 += 4)
+                    *reinterpret_cast<float4*>(qd + e4) = make_float4(qf[e4], qf[e4 + 1], qf[e4 + 2], qf[e4 + 3]);
+            }
         }
         if constexpr (FINEST) {
             // <dout, v> on the storage type (times w_0 below), and w_0 dout in fp32 for dv
@@ -899,10 +915,14 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
                     ag = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vA[j].z), __uint_as_float(dd.z), ag, 0, 0, 0);
                     ag = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(vA[j].w), __uint_as_float(dd.w), ag, 0, 0, 0);
                 }
-                float gf[E];
-                S::unpack(dd, gf);
+                if constexpr (kRows16) {
+                    dreg[t][j] = dd;
+                } else {
+                    float gf[E];
+                    S::unpack(dd, gf);
 #pragma unroll
-                for (int e = 0; e < E; ++e) mreg[t][j * E + e] = w0 * gf[e];
+                    for (int e = 0; e < E; ++e) mreg[t][j * E + e] = w0 * gf[e];
+                }
             }
         } else {
             // <dm, v> with dm in fp32, 4-channel chunks g, g+4, ...
@@ -966,6 +986,10 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
                 vw[c] = kept ? 0.f : sc;
             }
         }
+        if constexpr (kRows16) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) vw[c] *= w0;         // the dout rows are stored without w_0
+        }
         *reinterpret_cast<float4*>(dxs + s * 4) = make_float4(dx[0], dx[1], dx[2], dx[3]);
         *reinterpret_cast<float4*>(vws + s * 4) = make_float4(vw[0], vw[1], vw[2], vw[3]);
     }
@@ -979,7 +1003,7 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     float4_t ok_ = {0.f, 0.f, 0.f, 0.f}, ov = {0.f, 0.f, 0.f, 0.f};
     for (int st = 0; st < sph; ++st) {
         const int sl = hh * sph + st;
-        ok_ = __builtin_amdgcn_mfma_f32_4x4x1f32(dxs[sl * 4 + t4], Rs[sl * lay.pitch + ch], ok_, 0, 0, 0);
+        ok_ = __builtin_amdgcn_mfma_f32_4x4x1f32(dxs[sl * 4 + t4], row_elem(sl, ch), ok_, 0, 0, 0);
     }
     wave_lds_sync();
     // the dm rows into the same buffer (lane 16g + n holds slot 16t + n's chunks g, g+4, ...)
@@ -987,7 +1011,10 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     for (int t = 0; t < NT; ++t) {
         if (t >= ntile) break;                                // uniform
         const int s = 16 * t + n16;
-        if constexpr (FINEST) {
+        if constexpr (kRows16) {
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) *reinterpret_cast<uint4*>(Rs16 + s * lay.pitch + (g + 4 * j) * E) = dreg[t][j];
+        } else if constexpr (FINEST) {
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
                 float* md = Rs + s * lay.pitch + (g + 4 * j) * E;
@@ -1006,7 +1033,7 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     wave_lds_sync();
     for (int st = 0; st < sph; ++st) {
         const int sl = hh * sph + st;
-        ov = __builtin_amdgcn_mfma_f32_4x4x1f32(vws[sl * 4 + t4], Rs[sl * lay.pitch + ch], ov, 0, 0, 0);
+        ov = __builtin_amdgcn_mfma_f32_4x4x1f32(vws[sl * 4 + t4], row_elem(sl, ch), ov, 0, 0, 0);
     }
     if constexpr (NH == 2) {
 #pragma unroll
@@ -1074,7 +1101,7 @@ template <typename T, int D, bool VA, bool FINEST>
 hipError_t launch_key_tdv(const BwdLevelArgs& a, long long max_chunks, hipStream_t stream)
 {
     if (max_chunks >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    const size_t lds = key_lds<D>().total;
+    const size_t lds = key_lds<T, D, FINEST>().total;
     if (lds > device_max_lds()) return hipErrorInvalidValue;
     hipLaunchKernelGGL((bwd_key_kernel<T, D, VA, FINEST>), dim3(static_cast<unsigned>(max_chunks)), dim3(kWave), lds,
                        stream, a);
