@@ -720,26 +720,34 @@ __global__ __launch_bounds__(256) void bwd_fill_kernel(BwdFillArgs a)
 // slots' query rows are gathered 16 at a time (lane 16g + n takes chunks g, g+4, ... of slot n of a
 // tile), lane s keeps tile s/16 of the products and so ends with slot s's logits and <dm, v> for
 // the four keys. The weights dx and vw go to LDS, and dk = scale * dx^T Q, then dv = vw^T dM, run on
-// the 4x4 MFMA from the slots' q rows, then their dm rows, in fp32 in one LDS buffer. Only the
-// tiles that hold parents are gathered. A key whose list spans several chunks has each chunk store
-// its partial rows, and bwd_key_reduce_kernel adds them up. (Letting the last chunk add them, with a
-// counter and device-scope fences, was ten times slower: every such fence writes back the L2.)
+// the 4x4 MFMA from the slots' q rows, then their dm rows, in one LDS buffer (layout in key_lds).
+// Only the tiles that hold parents are gathered. A key whose list spans several chunks has each
+// chunk store its partial rows, and bwd_key_reduce_kernel adds them up. (Letting the last chunk add
+// them, with a counter and device-scope fences, was ten times slower: every such fence writes back
+// the L2.)
 struct KeyLds {
     int rows, dx, vw, total;
-    int pitch;      // elements per row
+    int qpitch;     // elements per query row
+    int mpitch;     // elements per dm row
+    int mslots;     // dm rows the buffer holds at once (all 64, or 32 per pass)
 };
 
-// The finest level's rows (the queries, then dout, whose w_0 the weights vw take instead) are bf16
-// values for bf16 inputs and stay bf16: exact, and half the LDS per wave. Coarser levels' dm rows
-// are fp32.
+// With bf16 inputs the query rows are bf16 values and stay bf16 (exact, half the LDS). So do the
+// finest level's dm rows, which are dout (its w_0 moves into the weights vw). The coarser levels'
+// dm rows are fp32 and go through the buffer 32 slots at a time, so that it stays at the size of
+// the bf16 query rows.
 template <typename T, int D, bool FINEST>
 __host__ __device__ inline KeyLds key_lds()
 {
-    constexpr int RB = sizeof(T) == 2 && FINEST ? 2 : 4;     // bytes per row element
+    constexpr bool bf = sizeof(T) == 2;
     KeyLds L;
-    L.pitch = RB == 2 ? D + 8 : D + 4;                     // rows of 16-byte multiples
+    L.qpitch = bf ? D + 8 : D + 4;                         // rows of 16-byte multiples
+    L.mpitch = bf && FINEST ? D + 8 : D + 4;
+    L.mslots = bf && !FINEST ? 2 * kKeyChunk : 4 * kKeyChunk;
+    const int qbytes = 4 * kKeyChunk * L.qpitch * (bf ? 2 : 4);
+    const int mbytes = L.mslots * L.mpitch * (bf && FINEST ? 2 : 4);
     L.rows = 0;
-    L.dx = L.rows + 4 * kKeyChunk * L.pitch * RB;
+    L.dx = L.rows + (qbytes > mbytes ? qbytes : mbytes);
     L.vw = L.dx + 4 * kKeyChunk * 16;
     L.total = L.vw + 4 * kKeyChunk * 16;
     return L;
@@ -768,11 +776,16 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     if (chunk >= a.coff[n]) return;          // whole wave
     extern __shared__ __align__(16) unsigned char smem[];
     const KeyLds lay = key_lds<T, D, FINEST>();
-    constexpr bool kRows16 = kBf16 && FINEST;                // rows kept as bf16
+    constexpr bool kRows16 = kBf16 && FINEST;                // query and dm rows kept as bf16
+    constexpr bool kSplit = kBf16 && !FINEST;                // bf16 query rows, fp32 dm rows in two passes
     uint16_t* const Rs16 = reinterpret_cast<uint16_t*>(smem + lay.rows);
-    auto row_elem = [&](int sl, int c) -> float {
-        if constexpr (kRows16) return bf16_bits_to_f32(Rs16[sl * lay.pitch + c]);
-        else return reinterpret_cast<const float*>(smem + lay.rows)[sl * lay.pitch + c];
+    auto q_elem = [&](int sl, int c) -> float {
+        if constexpr (kBf16) return bf16_bits_to_f32(Rs16[sl * lay.qpitch + c]);
+        else return reinterpret_cast<const float*>(smem + lay.rows)[sl * lay.qpitch + c];
+    };
+    auto m_elem = [&](int sl, int c) -> float {
+        if constexpr (kRows16) return bf16_bits_to_f32(Rs16[sl * lay.mpitch + c]);
+        else return reinterpret_cast<const float*>(smem + lay.rows)[sl * lay.mpitch + c];
     };
     float* Rs = reinterpret_cast<float*>(smem + lay.rows);    // q rows, then dm rows
     float* dxs = reinterpret_cast<float*>(smem + lay.dx);     // [slot][4 keys]
@@ -888,12 +901,12 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
                 ax = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kA[j].w), __uint_as_float(qB[j].w), ax, 0, 0, 0);
             }
             // the query row for dk (fp32, or bf16 as stored)
-            if constexpr (kRows16) {
-                *reinterpret_cast<uint4*>(Rs16 + s * lay.pitch + (g + 4 * j) * E) = qB[j];
+            if constexpr (kBf16) {
+                *reinterpret_cast<uint4*>(Rs16 + s * lay.qpitch + (g + 4 * j) * E) = qB[j];
             } else {
                 float qf[E];
                 S::unpack(qB[j], qf);
-                float* qd = Rs + s * lay.pitch + (g + 4 * j) * E;
+                float* qd = Rs + s * lay.qpitch + (g + 4 * j) * E;
 #pragma unroll
                 for (int e4 = 0; e4 < E; e4 += 4)
                     *reinterpret_cast<float4*>(qd + e4) = make_float4(qf[e4], qf[e4 + 1], qf[e4 + 2], qf[e4 + 3]);
@@ -1003,37 +1016,47 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     float4_t ok_ = {0.f, 0.f, 0.f, 0.f}, ov = {0.f, 0.f, 0.f, 0.f};
     for (int st = 0; st < sph; ++st) {
         const int sl = hh * sph + st;
-        ok_ = __builtin_amdgcn_mfma_f32_4x4x1f32(dxs[sl * 4 + t4], row_elem(sl, ch), ok_, 0, 0, 0);
+        ok_ = __builtin_amdgcn_mfma_f32_4x4x1f32(dxs[sl * 4 + t4], q_elem(sl, ch), ok_, 0, 0, 0);
     }
-    wave_lds_sync();
-    // the dm rows into the same buffer (lane 16g + n holds slot 16t + n's chunks g, g+4, ...)
+    // the dm rows into the same buffer (lane 16g + n holds slot 16t + n's chunks g, g+4, ...), all
+    // slots at once or (kSplit) 32 at a time; slot sl of a pass is row sl - first
+    constexpr int kPasses = kSplit ? 2 : 1;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        if (t >= ntile) break;                                // uniform
-        const int s = 16 * t + n16;
-        if constexpr (kRows16) {
+    for (int pass = 0; pass < kPasses; ++pass) {
+        const int first = pass * lay.mslots;
+        if (first >= nsp) break;                              // uniform
+        wave_lds_sync();
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) *reinterpret_cast<uint4*>(Rs16 + s * lay.pitch + (g + 4 * j) * E) = dreg[t][j];
-        } else if constexpr (FINEST) {
+        for (int t = 0; t < NT; ++t) {
+            if (t >= ntile) break;                            // uniform
+            if (16 * t < first || 16 * t >= first + lay.mslots) continue;   // uniform
+            const int s = 16 * t + n16 - first;
+            if constexpr (kRows16) {
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                float* md = Rs + s * lay.pitch + (g + 4 * j) * E;
+                for (int j = 0; j < NJ; ++j) *reinterpret_cast<uint4*>(Rs16 + s * lay.mpitch + (g + 4 * j) * E) = dreg[t][j];
+            } else if constexpr (FINEST) {
 #pragma unroll
-                for (int e4 = 0; e4 < E; e4 += 4)
-                    *reinterpret_cast<float4*>(md + e4) = make_float4(mreg[t][j * E + e4], mreg[t][j * E + e4 + 1],
-                                                                      mreg[t][j * E + e4 + 2], mreg[t][j * E + e4 + 3]);
+                for (int j = 0; j < NJ; ++j) {
+                    float* md = Rs + s * lay.mpitch + (g + 4 * j) * E;
+#pragma unroll
+                    for (int e4 = 0; e4 < E; e4 += 4)
+                        *reinterpret_cast<float4*>(md + e4) = make_float4(mreg[t][j * E + e4], mreg[t][j * E + e4 + 1],
+                                                                          mreg[t][j * E + e4 + 2], mreg[t][j * E + e4 + 3]);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < NJF; ++j)
+                    *reinterpret_cast<float4*>(Rs + s * lay.mpitch + (g + 4 * j) * 4) =
+                        make_float4(mreg[t][4 * j], mreg[t][4 * j + 1], mreg[t][4 * j + 2], mreg[t][4 * j + 3]);
             }
-        } else {
-#pragma unroll
-            for (int j = 0; j < NJF; ++j)
-                *reinterpret_cast<float4*>(Rs + s * lay.pitch + (g + 4 * j) * 4) =
-                    make_float4(mreg[t][4 * j], mreg[t][4 * j + 1], mreg[t][4 * j + 2], mreg[t][4 * j + 3]);
         }
-    }
-    wave_lds_sync();
-    for (int st = 0; st < sph; ++st) {
-        const int sl = hh * sph + st;
-        ov = __builtin_amdgcn_mfma_f32_4x4x1f32(vws[sl * 4 + t4], row_elem(sl, ch), ov, 0, 0, 0);
+        wave_lds_sync();
+        const int cnt = min(nsp - first, lay.mslots);         // a multiple of 16
+        const int sphp = cnt / NH;
+        for (int st = 0; st < sphp; ++st) {
+            const int sl = hh * sphp + st;
+            ov = __builtin_amdgcn_mfma_f32_4x4x1f32(vws[(first + sl) * 4 + t4], m_elem(sl, ch), ov, 0, 0, 0);
+        }
     }
     if constexpr (NH == 2) {
 #pragma unroll
