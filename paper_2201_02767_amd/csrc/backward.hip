@@ -1147,43 +1147,53 @@ hipError_t launch_key_td(const BwdLevelArgs& a, bool variant_a, bool finest, lon
 // 4. pyramids
 // ---------------------------------------------------------------------------------------------
 
+template <int LMAX>
 __global__ __launch_bounds__(256) void bwd_unpool_kernel(BwdUnpoolArgs a)
 {
+    // one thread per 4 channels of a level-0 token; a batch element takes a.bpb consecutive blocks
+    // (its map is below 2^31 bytes, so its chunk index fits 32 bits)
     const int cpt = a.C / 4;
-    const long long N0 = static_cast<long long>(a.H[0]) * a.W[0];
-    const long long total = a.B * N0 * cpt;
-    const long long tid = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (tid >= total) return;
-    const int ch = static_cast<int>(tid % cpt);
-    const long long tok = tid / cpt;
-    const int i = static_cast<int>(tok % N0);
-    const int b = static_cast<int>(tok / N0);
-    const int y = i / a.W[0], x = i - y * a.W[0];
-    float4 aq = make_float4(0.f, 0.f, 0.f, 0.f), ak = aq, av = aq;
-    float f = 1.0f;
-    for (int l = 1; l < a.L; ++l) {
+    const int n0 = a.H[0] * a.W[0] * cpt;
+    const int b = static_cast<int>(blockIdx.x) / a.bpb;
+    const int t = (static_cast<int>(blockIdx.x) - b * a.bpb) * blockDim.x + threadIdx.x;
+    if (t >= n0) return;
+    const int i = fast_div(t, a.div_cpt);
+    const int ch = t - i * cpt;
+    const int y = fast_div(i, a.div_W0), x = i - y * a.W[0];
+    // every load first (the ancestors' rows at each level, then this token's rows), then the sums
+    float4 g[LMAX][3];
+    float f[LMAX];
+    float fl = 1.0f;
+#pragma unroll
+    for (int l = 1; l < LMAX; ++l) {
+        if (l >= a.L) break;                                  // uniform
         const int yl = y >> l, xl = x >> l;
         const int ny = (2 * yl + 1 < a.H[l - 1]) ? 2 : 1, nx = (2 * xl + 1 < a.W[l - 1]) ? 2 : 1;
-        f *= 1.0f / static_cast<float>(ny * nx);
-        const size_t off = ((static_cast<size_t>(b) * a.H[l] + yl) * a.W[l] + xl) * a.C + 4 * ch;
-        const float4 gq = *reinterpret_cast<const float4*>(a.gq[l] + off);
-        const float4 gk = *reinterpret_cast<const float4*>(a.gk[l] + off);
-        const float4 gv = *reinterpret_cast<const float4*>(a.gv[l] + off);
-        aq.x += f * gq.x; aq.y += f * gq.y; aq.z += f * gq.z; aq.w += f * gq.w;
-        ak.x += f * gk.x; ak.y += f * gk.y; ak.z += f * gk.z; ak.w += f * gk.w;
-        av.x += f * gv.x; av.y += f * gv.y; av.z += f * gv.z; av.w += f * gv.w;
+        fl *= 1.0f / static_cast<float>(ny * nx);
+        f[l] = fl;
+        const size_t off = static_cast<size_t>(b) * static_cast<uint32_t>(a.H[l] * a.W[l] * a.C) +
+                           static_cast<uint32_t>((yl * a.W[l] + xl) * a.C + 4 * ch);
+        g[l][0] = *reinterpret_cast<const float4*>(a.gq[l] + off);
+        g[l][1] = *reinterpret_cast<const float4*>(a.gk[l] + off);
+        g[l][2] = *reinterpret_cast<const float4*>(a.gv[l] + off);
     }
-    const size_t o = static_cast<size_t>(tok) * a.C + 4 * ch;
-    float4* pq = reinterpret_cast<float4*>(a.dq + o);
-    float4* pk = reinterpret_cast<float4*>(a.dk + o);
-    float4* pv = reinterpret_cast<float4*>(a.dv + o);
-    float4 q = *pq, k = *pk, v = *pv;
-    q.x += aq.x; q.y += aq.y; q.z += aq.z; q.w += aq.w;
-    k.x += ak.x; k.y += ak.y; k.z += ak.z; k.w += ak.w;
-    v.x += av.x; v.y += av.y; v.z += av.z; v.w += av.w;
-    *pq = q;
-    *pk = k;
-    *pv = v;
+    const size_t o = static_cast<size_t>(b) * static_cast<uint32_t>(n0) * 4 + static_cast<uint32_t>(t) * 4;
+    float4* const p[3] = {reinterpret_cast<float4*>(a.dq + o), reinterpret_cast<float4*>(a.dk + o),
+                          reinterpret_cast<float4*>(a.dv + o)};
+    float4 r[3] = {*p[0], *p[1], *p[2]};
+#pragma unroll
+    for (int l = 1; l < LMAX; ++l) {
+        if (l >= a.L) break;                                  // uniform
+#pragma unroll
+        for (int m = 0; m < 3; ++m) {
+            r[m].x += f[l] * g[l][m].x;
+            r[m].y += f[l] * g[l][m].y;
+            r[m].z += f[l] * g[l][m].z;
+            r[m].w += f[l] * g[l][m].w;
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < 3; ++m) *p[m] = r[m];
 }
 
 }  // namespace
@@ -1273,10 +1283,17 @@ hipError_t launch_bwd_keys(const BwdLevelArgs& a, const BwdScanArgs& sc, int d, 
 
 hipError_t launch_bwd_unpool(const BwdUnpoolArgs& a, hipStream_t stream)
 {
-    const long long total = static_cast<long long>(a.B) * a.H[0] * a.W[0] * (a.C / 4);
-    const long long blocks = (total + 255) / 256;
-    if (blocks >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(bwd_unpool_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, a);
+    const long long n0 = static_cast<long long>(a.H[0]) * a.W[0] * (a.C / 4);
+    const long long bpb = (n0 + 255) / 256;
+    if (n0 >= 0x7FFFFFFFLL || bpb * a.B >= 0x7FFFFFFFLL || a.L < 2) return hipErrorInvalidValue;
+    BwdUnpoolArgs u = a;
+    u.div_cpt = make_fastdiv(a.C / 4);
+    u.div_W0 = make_fastdiv(a.W[0]);
+    u.bpb = static_cast<int>(bpb);
+    const dim3 grid(static_cast<unsigned>(bpb * a.B));
+    if (a.L <= 4) hipLaunchKernelGGL(bwd_unpool_kernel<4>, grid, dim3(256), 0, stream, u);
+    else if (a.L <= 8) hipLaunchKernelGGL(bwd_unpool_kernel<8>, grid, dim3(256), 0, stream, u);
+    else hipLaunchKernelGGL(bwd_unpool_kernel<QTA_MAX_LEVELS>, grid, dim3(256), 0, stream, u);
     return hipGetLastError();
 }
 
