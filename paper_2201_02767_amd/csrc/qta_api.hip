@@ -194,17 +194,20 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], in
 
 // Workspace of the backward pass: per level l >= 1 the gradient of the message (dm) and the
 // level's q, k, v gradients (fp32 [B][N_l][C]); QuadTree-A's gradients of the kept scores
-// ([B][heads][N_l][K_l]); the coarse softmax statistics ([B][heads][N_c][4]); and, reused level by
-// level, the finer levels' query statistics and the counting sort of the kept pairs (counts, places
-// in the lists, list and chunk offsets, block sums, lists, chunk keys, per-chunk partial rows). What
-// is summed with atomics (dm at levels >= 2, the counts) forms one contiguous region, cleared at the
-// start of every call; the scan returns the counts to zero after each level's sort.
+// ([B][heads][N_l][K_l]); the coarse softmax statistics ([B][heads][N_c][4]); and per finer level
+// its query statistics and the counting sort of its kept pairs (counts, places in the lists, list
+// and chunk offsets, block sums, lists, chunk keys, per-chunk partial rows), separate per level so
+// that one level's sort and key pass may run beside the next level's query pass. What is summed
+// with atomics (dm at levels >= 2, the counts) forms one contiguous region, cleared at the start of
+// every call; each level's scan returns its counts to zero.
 struct BwdLayout {
     size_t dm[QTA_MAX_LEVELS], gq[QTA_MAX_LEVELS], gk[QTA_MAX_LEVELS], gv[QTA_MAX_LEVELS];
     size_t dsig[QTA_MAX_LEVELS];
     size_t zero_begin, zero_end;
     size_t stats, total;
-    size_t count, off, coff, block_sums, entries, slot, chunk_key, partial, qstats;
+    size_t count[QTA_MAX_LEVELS], off[QTA_MAX_LEVELS], coff[QTA_MAX_LEVELS], block_sums[QTA_MAX_LEVELS];
+    size_t entries[QTA_MAX_LEVELS], slot[QTA_MAX_LEVELS], chunk_key[QTA_MAX_LEVELS], partial[QTA_MAX_LEVELS];
+    size_t qstats[QTA_MAX_LEVELS];
     long long nslots_max;           // B*heads*N_{l+1} over the finer levels
 };
 
@@ -214,26 +217,18 @@ void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int d, in
     *L = BwdLayout{};
     const int c = levels - 1;
     auto fbytes = [&](int l) { return static_cast<size_t>(B) * Hl[l] * Wl[l] * C * sizeof(float); };
-    long long nmax = 0, emax = 0, cmax = 0, smax = 0;
-    for (int l = 0; l < c; ++l) {
-        const long long n = static_cast<long long>(B) * heads * Hl[l + 1] * Wl[l + 1];
-        const long long e = n * Kl[l + 1];
-        const long long ch = n + (e + kKeyChunk - 1) / kKeyChunk;
-        const long long st = static_cast<long long>(B) * heads * Hl[l] * Wl[l] * 2 * (va ? Kl[l + 1] : 1);
-        nmax = n > nmax ? n : nmax;
-        emax = e > emax ? e : emax;
-        cmax = ch > cmax ? ch : cmax;
-        smax = st > smax ? st : smax;
-    }
-    L->nslots_max = nmax;
+    auto nslots = [&](int l) { return static_cast<long long>(B) * heads * Hl[l + 1] * Wl[l + 1]; };
+    for (int l = 0; l < c; ++l) L->nslots_max = nslots(l) > L->nslots_max ? nslots(l) : L->nslots_max;
     size_t off = 0;
     L->zero_begin = off;
     for (int l = 2; l <= c; ++l) {
         L->dm[l] = off;
         off = align_up(off + fbytes(l));
     }
-    L->count = off;                 // padded to whole quads: the scan reads four counts at a time
-    off = align_up(off + static_cast<size_t>((nmax + 3) & ~3LL) * sizeof(int32_t));
+    for (int l = 0; l < c; ++l) {       // padded to whole quads: the scan reads four counts at a time
+        L->count[l] = off;
+        off = align_up(off + static_cast<size_t>((nslots(l) + 3) & ~3LL) * sizeof(int32_t));
+    }
     L->zero_end = off;
     if (c >= 1) {
         L->dm[1] = off;
@@ -253,23 +248,27 @@ void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int d, in
     }
     L->stats = off;
     off = align_up(off + static_cast<size_t>(B) * heads * Hl[c] * Wl[c] * 4 * sizeof(float));
-    if (c >= 1) {
-        L->off = off;
-        off = align_up(off + static_cast<size_t>(nmax + 1) * sizeof(int32_t));
-        L->coff = off;
-        off = align_up(off + static_cast<size_t>(nmax + 1) * sizeof(int32_t));
-        L->block_sums = off;
-        off = align_up(off + static_cast<size_t>(2 * ((nmax + 1023) / 1024)) * sizeof(int32_t));
-        L->entries = off;
-        off = align_up(off + static_cast<size_t>(emax) * sizeof(int32_t));
-        L->slot = off;
-        off = align_up(off + static_cast<size_t>(emax) * sizeof(int32_t));
-        L->chunk_key = off;
-        off = align_up(off + static_cast<size_t>(cmax) * sizeof(int32_t));
-        L->partial = off;
-        off = align_up(off + static_cast<size_t>(cmax) * 8 * d * sizeof(float));
-        L->qstats = off;
-        off = align_up(off + static_cast<size_t>(smax) * sizeof(float));
+    for (int l = 0; l < c; ++l) {
+        const long long n = nslots(l);
+        const long long e = n * Kl[l + 1];
+        const long long ch = n + (e + kKeyChunk - 1) / kKeyChunk;
+        const long long st = static_cast<long long>(B) * heads * Hl[l] * Wl[l] * 2 * (va ? Kl[l + 1] : 1);
+        L->off[l] = off;
+        off = align_up(off + static_cast<size_t>(n + 1) * sizeof(int32_t));
+        L->coff[l] = off;
+        off = align_up(off + static_cast<size_t>(n + 1) * sizeof(int32_t));
+        L->block_sums[l] = off;
+        off = align_up(off + static_cast<size_t>(2 * ((n + 1023) / 1024)) * sizeof(int32_t));
+        L->entries[l] = off;
+        off = align_up(off + static_cast<size_t>(e) * sizeof(int32_t));
+        L->slot[l] = off;
+        off = align_up(off + static_cast<size_t>(e) * sizeof(int32_t));
+        L->chunk_key[l] = off;
+        off = align_up(off + static_cast<size_t>(ch) * sizeof(int32_t));
+        L->partial[l] = off;
+        off = align_up(off + static_cast<size_t>(ch) * 8 * d * sizeof(float));
+        L->qstats[l] = off;
+        off = align_up(off + static_cast<size_t>(st) * sizeof(float));
     }
     L->total = off;
 }
@@ -733,6 +732,15 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     float* dw_out = (!va && w) ? dw : nullptr;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
+    // the counting sorts and key passes go to the auxiliary stream when there is one (not for the
+    // finest step alone); `after(x, y)` orders later work on y after the work issued so far on x
+    hipStream_t s2 = (opt && opt->aux_stream && !only_finest && levels > 1) ? static_cast<hipStream_t>(opt->aux_stream) : s;
+    auto after = [](hipStream_t x, hipStream_t y) {
+        hipEvent_t e;
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return false;
+        const bool ok = hipEventRecord(e, x) == hipSuccess && hipStreamWaitEvent(y, e, 0) == hipSuccess;
+        return hipEventDestroy(e) == hipSuccess && ok;
+    };
     const bool use_bf16 = dtype == QTA_BF16;
     const float tau = resolve_scale(scale, d);
     const char* ws = static_cast<const char*>(workspace);
@@ -798,24 +806,25 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
             a.parent_key = skey(l + 1);
             a.dsig_out = va ? fptr(G.dsig[l + 1]) : nullptr;
             a.levels = levels;
-            a.stats = fptr(G.qstats);
-            a.count = reinterpret_cast<int32_t*>(gws + G.count);
-            a.off = reinterpret_cast<const int32_t*>(gws + G.off);
-            a.coff = reinterpret_cast<const int32_t*>(gws + G.coff);
-            a.chunk_key = reinterpret_cast<const int32_t*>(gws + G.chunk_key);
-            a.entries = reinterpret_cast<int32_t*>(gws + G.entries);
-            a.slot = reinterpret_cast<int32_t*>(gws + G.slot);
-            a.partial = fptr(G.partial);
+            a.stats = fptr(G.qstats[l]);
+            a.count = reinterpret_cast<int32_t*>(gws + G.count[l]);
+            a.off = reinterpret_cast<const int32_t*>(gws + G.off[l]);
+            a.coff = reinterpret_cast<const int32_t*>(gws + G.coff[l]);
+            a.chunk_key = reinterpret_cast<const int32_t*>(gws + G.chunk_key[l]);
+            a.entries = reinterpret_cast<int32_t*>(gws + G.entries[l]);
+            a.slot = reinterpret_cast<int32_t*>(gws + G.slot[l]);
+            a.partial = fptr(G.partial[l]);
             if (launch_bwd_level(a, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
+            if (s2 != s && !after(s, s2)) return QTA_ERR_HIP;   // the sort and key pass need this query pass
             BwdScanArgs sc{};
             sc.n = B * heads * L.H[l + 1] * L.W[l + 1];
             sc.nblocks = (sc.n + 1023) / 1024;
             sc.count = a.count;
-            sc.off = reinterpret_cast<int32_t*>(gws + G.off);
-            sc.coff = reinterpret_cast<int32_t*>(gws + G.coff);
-            sc.chunk_key = reinterpret_cast<int32_t*>(gws + G.chunk_key);
-            sc.block_sums = reinterpret_cast<int32_t*>(gws + G.block_sums);
-            if (launch_bwd_keys(a, sc, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
+            sc.off = reinterpret_cast<int32_t*>(gws + G.off[l]);
+            sc.coff = reinterpret_cast<int32_t*>(gws + G.coff[l]);
+            sc.chunk_key = reinterpret_cast<int32_t*>(gws + G.chunk_key[l]);
+            sc.block_sums = reinterpret_cast<int32_t*>(gws + G.block_sums[l]);
+            if (launch_bwd_keys(a, sc, d, va, use_bf16, l == 0, s2) != hipSuccess) return QTA_ERR_HIP;
         }
     }
     if (only_finest) return QTA_OK;
@@ -856,6 +865,7 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
         if (launch_bwd_coarse(a, d, va, use_bf16, s) != hipSuccess) return QTA_ERR_HIP;
     }
     if (levels == 1) return QTA_OK;
+    if (s2 != s && !after(s2, s)) return QTA_ERR_HIP;       // every key pass before the unpooling
 
     // 4. pyramids
     BwdUnpoolArgs u{};

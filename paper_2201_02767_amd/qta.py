@@ -52,6 +52,7 @@ class Options(ctypes.Structure):
         ("pe_weight", ctypes.c_void_p),
         ("pe_bias", ctypes.c_void_p),
         ("epipolar", ctypes.c_int),
+        ("aux_stream", ctypes.c_void_p),
     ]
 
 
@@ -337,7 +338,7 @@ class Plan:
                                    device=self.device)
         return self._grads, (self._dw if want_dw else None)
 
-    def _bwd_args(self, q, k, v, w, dout, stream):
+    def _bwd_args(self, q, k, v, w, dout, stream, overlap=True):
         if self.v_supplied or self.pe:
             raise ValueError("the backward pass covers pooled V levels without a position encoding")
         self._args(q, k, v, w, None, None, None)
@@ -349,6 +350,11 @@ class Plan:
         opt = Options()
         opt.K_levels = ctypes.addressof(self._k_tbl)
         opt.epipolar = int(self.epipolar)
+        if overlap:
+            # a second stream of the plan's own for the sorts and key passes (ordered by the library)
+            if getattr(self, "_aux", None) is None:
+                self._aux = torch.cuda.Stream(device=self.device)
+            opt.aux_stream = self._aux.cuda_stream
         args = (_ptr(q), _ptr(k), _ptr(v), _ptr(w), _ptr(dout), self.B, self.heads, self.H, self.W, self.d,
                 self.levels, self.K_levels[1] if self.levels > 1 else max(self.K_levels[0], 1),
                 _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), ctypes.byref(opt),
@@ -356,12 +362,14 @@ class Plan:
                 _ptr(self.bwd_workspace), self.bwd_workspace.numel(), stream)
         return args, opt, (dq, dk, dv, dw)
 
-    def backward(self, q, k, v, dout, w=None, stream=None):
+    def backward(self, q, k, v, dout, w=None, stream=None, overlap=True):
         """Gradients (dq, dk, dv, dw) in fp32 of the last ``run`` on the same inputs, for the upstream
         gradient ``dout`` (the kept keys of that run held fixed). ``dw`` is None unless QuadTree-B
-        with ``w``. The returned tensors are the plan's own buffers, overwritten by the next call."""
+        with ``w``. The returned tensors are the plan's own buffers, overwritten by the next call.
+        ``overlap``: run each level's sort and key pass on a second stream of the plan's own, beside
+        the next level's query pass (False: everything on the one stream)."""
         s = _stream(self.device) if stream is None else ctypes.c_void_p(stream)
-        args, opt, grads = self._bwd_args(q, k, v, w, dout, s)
+        args, opt, grads = self._bwd_args(q, k, v, w, dout, s, overlap)
         _check("qta_backward_ex", lib().qta_backward_ex(*args))
         return grads
 
