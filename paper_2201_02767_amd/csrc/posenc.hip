@@ -7,6 +7,8 @@
 // of one level and reads their 3x6 window once (8- or 16-byte loads; neighbouring threads take the
 // other channels of the same tokens), so the encoding costs about one pass over each V level and
 // one read-modify-write of each message.
+#include <type_traits>
+
 #include "qta_device.h"
 #include "qta_internal.h"
 
@@ -51,15 +53,34 @@ __global__ __launch_bounds__(kThreads) void posenc_kernel(PosEncArgs a)
     const PosEncLevel& L = a.lv[l];
     const int C = a.heads * a.d, groups = C / 4;
     const int xtiles = (L.W + kTX - 1) / kTX;
-    long long r = item - a.start[l];
-    const int g = static_cast<int>(r % groups);
+    // within a level the item index fits 32 bits (the launcher checks)
+    int r = static_cast<int>(item - a.start[l]);
+    const int g = r % groups;
     r /= groups;
-    const int x0 = static_cast<int>(r % xtiles) * kTX;
+    const int x0 = (r % xtiles) * kTX;
     r /= xtiles;
-    const int y = static_cast<int>(r % L.H);
-    const int b = static_cast<int>(r / L.H);
+    const int y = r % L.H;
+    const int b = r / L.H;
     const int c0 = 4 * g, h = c0 / a.d, c = c0 - h * a.d;
-    // the 36 weights of these four channels are contiguous ([C][3][3]): nine 16-byte loads
+    // every load first: the 3 x (kTX+2) window at clamped (in-bounds) positions, masked when used,
+    // so that they are all in flight at once; then the 36 weights of these four channels
+    // (contiguous, [C][3][3])
+    using Raw = typename std::conditional<sizeof(T) == 4, float4, uint2>::type;
+    Raw win[3][kTX + 2];
+    bool ok[3][kTX + 2];
+#pragma unroll
+    for (int ky = 0; ky < 3; ++ky) {
+        const int yy = y + ky - 1;
+        const int yc = min(max(yy, 0), L.H - 1);
+#pragma unroll
+        for (int j = 0; j < kTX + 2; ++j) {
+            const int xx = x0 + j - 1;
+            const int xc = min(max(xx, 0), L.W - 1);
+            ok[ky][j] = yy >= 0 && yy < L.H && xx >= 0 && xx < L.W;
+            win[ky][j] = *reinterpret_cast<const Raw*>(static_cast<const T*>(L.v) +
+                                                       elem_offset(L.blocked != 0, b, yc, xc, L.H, L.W, h, c, a.heads, a.d));
+        }
+    }
     float wk[36];
     const float4* wp = reinterpret_cast<const float4*>(L.weight + static_cast<size_t>(c0) * 9);
 #pragma unroll
@@ -74,16 +95,20 @@ __global__ __launch_bounds__(kThreads) void posenc_kernel(PosEncArgs a)
     float4 acc[kTX];
 #pragma unroll
     for (int t = 0; t < kTX; ++t) acc[t] = bias;
-    // window columns x0-1 .. x0+kTX; each column is loaded once and feeds up to three outputs
+    // window column j feeds outputs x0 + t with t = j - kx for the three kernel columns kx
 #pragma unroll
     for (int ky = 0; ky < 3; ++ky) {
-        const int yy = y + ky - 1;
-        if (yy < 0 || yy >= L.H) continue;
 #pragma unroll
         for (int j = 0; j < kTX + 2; ++j) {
-            const int xx = x0 + j - 1;
-            if (xx < 0 || xx >= L.W) continue;
-            const float4 vv = load4<T>(L.v, elem_offset(L.blocked != 0, b, yy, xx, L.H, L.W, h, c, a.heads, a.d));
+            float4 vv;
+            if constexpr (sizeof(T) == 4) {
+                vv = win[ky][j];
+            } else {
+                const uint2 u = win[ky][j];
+                vv = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                                 __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+            }
+            if (!ok[ky][j]) vv = make_float4(0.f, 0.f, 0.f, 0.f);   // zero outside the map
 #pragma unroll
             for (int kx = 0; kx < 3; ++kx) {
                 const int t = j - kx;                      // output x0 + t uses column x0 + t + kx - 1
@@ -96,20 +121,22 @@ __global__ __launch_bounds__(kThreads) void posenc_kernel(PosEncArgs a)
             }
         }
     }
+    float* const row = L.dst + (static_cast<size_t>(b) * L.H + y) * L.W * C + c0;
+    if (L.accumulate) {                                   // uniform: a level's message, read first
+        float4 m[kTX];
 #pragma unroll
-    for (int t = 0; t < kTX; ++t) {
-        if (x0 + t >= L.W) break;
-        float4* dst = reinterpret_cast<float4*>(L.dst + ((static_cast<size_t>(b) * L.H + y) * L.W + x0 + t) * C + c0);
-        float4 o = acc[t];
-        if (L.accumulate) {
-            const float4 m = *dst;
-            o.x += m.x;
-            o.y += m.y;
-            o.z += m.z;
-            o.w += m.w;
+        for (int t = 0; t < kTX; ++t) m[t] = *reinterpret_cast<const float4*>(row + static_cast<size_t>(min(x0 + t, L.W - 1)) * C);
+#pragma unroll
+        for (int t = 0; t < kTX; ++t) {
+            acc[t].x += m[t].x;
+            acc[t].y += m[t].y;
+            acc[t].z += m[t].z;
+            acc[t].w += m[t].w;
         }
-        *dst = o;
     }
+#pragma unroll
+    for (int t = 0; t < kTX; ++t)
+        if (x0 + t < L.W) *reinterpret_cast<float4*>(row + static_cast<size_t>(x0 + t) * C) = acc[t];
 }
 
 }  // namespace
@@ -124,6 +151,7 @@ hipError_t launch_posenc(const PosEncArgs& a, bool use_bf16, hipStream_t stream)
     p.start[0] = 0;
     for (int l = 0; l < a.nlev; ++l) {
         const long long n = static_cast<long long>(a.B) * a.lv[l].H * ((a.lv[l].W + kTX - 1) / kTX) * (C / cpt);
+        if (n >= 0x7FFFFFFFLL) return hipErrorInvalidValue;           // items within a level are int
         p.level_end[l] = p.start[l] + n;
         p.start[l + 1] = (p.level_end[l] + kThreads - 1) / kThreads * kThreads;
     }
