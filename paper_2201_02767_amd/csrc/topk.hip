@@ -20,17 +20,21 @@ __global__ __launch_bounds__(256) void topk_kernel(TopkArgs a)
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= a.rows) return;                  // whole wave leaves; no workgroup barriers below
     const size_t base = static_cast<size_t>(row) * a.n;
+    // every load unconditional (clamped into the row) so that all are in flight at once; slots
+    // past the row and negative names are masked to 0 (no candidate)
     uint64_t word[NPER];
+    float key[NPER];
+    int32_t name[NPER];
 #pragma unroll
     for (int e = 0; e < NPER; ++e) {
-        const int j = lane + kWave * e;
-        word[e] = 0ull;
-        if (j < a.n) {
-            const int32_t name = a.cand_idx ? a.cand_idx[base + j] : j;
-            if (name >= 0) {
-                word[e] = rank_word(a.keys[base + j], name);
-            }
-        }
+        const int j = min(lane + kWave * e, a.n - 1);
+        key[e] = a.keys[base + j];
+        name[e] = a.cand_idx ? a.cand_idx[base + j] : j;
+    }
+#pragma unroll
+    for (int e = 0; e < NPER; ++e) {
+        const bool live = lane + kWave * e < a.n && name[e] >= 0;
+        word[e] = live ? rank_word(key[e], name[e]) : 0ull;
     }
     const size_t orow = static_cast<size_t>(row) * a.K;
     for (int r = 0; r < a.K; ++r) {
