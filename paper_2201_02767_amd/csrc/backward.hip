@@ -377,47 +377,70 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
         float gv[NJ][E];
 #pragma unroll
         for (int j = 0; j < NJ; ++j) S::unpack(da[j], gv[j]);                    // zero off the map
-        for (int lv = 1; lv < L; ++lv) {
-            const float wl = VA ? 1.0f : (a.w ? a.w[wrow + lv] : 1.0f / L);
-            const size_t anc = static_cast<size_t>(b) * a.lvl_N[lv] +
-                               static_cast<size_t>((2 * Py) >> lv) * a.lvl_W[lv] + ((2 * Px) >> lv);
-            const size_t arow = (anc * a.heads + h) * D;
-            float part = 0.f;
+        // the coarser levels in blocks: each block's weights and forward messages are all requested
+        // before any is used, so their latencies overlap. Blocks of four need about 20 more VGPRs,
+        // which costs occupancy unless the LDS already caps it (64 candidate slots)
+        constexpr int kBlk = NSP == 64 ? 4 : 1;
+        for (int lv0 = 1; lv0 < L; lv0 += kBlk) {
+            float wl[kBlk];
+            float4 mq[kBlk][NJ * E / 4];
+            size_t arow[kBlk];
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                const int c0 = (g + 4 * j) * E;
-                float sv[E];
+            for (int i = 0; i < kBlk; ++i) {
+                const int lv = min(lv0 + i, L - 1);                               // clamped: unused past L-1
+                wl[i] = VA ? 1.0f : (a.w ? a.w[wrow + lv] : 1.0f / L);
+                const size_t anc = static_cast<size_t>(b) * a.lvl_N[lv] +
+                                   static_cast<size_t>((2 * Py) >> lv) * a.lvl_W[lv] + ((2 * Px) >> lv);
+                arow[i] = (anc * a.heads + h) * D;
+                if (want_dw) {                                                    // uniform
 #pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    sv[e] = wl * gv[j][e];
-                    sv[e] += xchg_f32<1>(sv[e]);                                  // the four queries
-                    sv[e] += xchg_f32<2>(sv[e]);
-                }
-                if (want_dw) {
-                    const float* m = a.msg_fwd[lv] + arow + c0;
+                    for (int j = 0; j < NJ; ++j)
 #pragma unroll
-                    for (int e4 = 0; e4 < E; e4 += 4) {
-                        const float4 m4 = *reinterpret_cast<const float4*>(m + e4);
-                        part += gv[j][e4] * m4.x + gv[j][e4 + 1] * m4.y + gv[j][e4 + 2] * m4.z + gv[j][e4 + 3] * m4.w;
-                    }
-                }
-                // every lane of group g holds the sums of chunk g + 4j: lane 16g + e stores element e,
-                // so one instruction covers the head's channels contiguously
-                float mine = sv[0];
-#pragma unroll
-                for (int e = 1; e < E; ++e) mine = n16 == e ? sv[e] : mine;
-                if (n16 < E) {
-                    float* dst = a.dm_out[lv] + arow + c0 + n16;
-                    if (lv == 1)
-                        *dst = mine;
-                    else
-                        atomicAddNoRet(dst, mine);
+                        for (int e4 = 0; e4 < E; e4 += 4)
+                            mq[i][(j * E + e4) / 4] =
+                                *reinterpret_cast<const float4*>(a.msg_fwd[lv] + arow[i] + (g + 4 * j) * E + e4);
                 }
             }
-            if (want_dw) {
-                part += xchg_f32<16>(part);
-                part += xchg_f32<32>(part);
-                if (g == 0 && n16 < 4 && q_ok) a.dw[wrow + lv] = part;
+#pragma unroll
+            for (int i = 0; i < kBlk; ++i) {
+                const int lv = lv0 + i;
+                if (lv >= L) break;                                               // uniform
+                float part = 0.f;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const int c0 = (g + 4 * j) * E;
+                    float sv[E];
+#pragma unroll
+                    for (int e = 0; e < E; ++e) {
+                        sv[e] = wl[i] * gv[j][e];
+                        sv[e] += xchg_f32<1>(sv[e]);                              // the four queries
+                        sv[e] += xchg_f32<2>(sv[e]);
+                    }
+                    if (want_dw) {
+#pragma unroll
+                        for (int e4 = 0; e4 < E; e4 += 4) {
+                            const float4 m4 = mq[i][(j * E + e4) / 4];
+                            part += gv[j][e4] * m4.x + gv[j][e4 + 1] * m4.y + gv[j][e4 + 2] * m4.z + gv[j][e4 + 3] * m4.w;
+                        }
+                    }
+                    // every lane of group g holds the sums of chunk g + 4j: lane 16g + e stores
+                    // element e, so one instruction covers the head's channels contiguously
+                    float mine = sv[0];
+#pragma unroll
+                    for (int e = 1; e < E; ++e) mine = n16 == e ? sv[e] : mine;
+                    if (n16 < E) {
+                        float* dst = a.dm_out[lv] + arow[i] + c0 + n16;
+                        if (lv == 1)
+                            *dst = mine;
+                        else
+                            atomicAddNoRet(dst, mine);
+                    }
+                }
+                if (want_dw) {
+                    part += xchg_f32<16>(part);
+                    part += xchg_f32<32>(part);
+                    if (g == 0 && n16 < 4 && q_ok) a.dw[wrow + lv] = part;
+                }
             }
         }
     }
