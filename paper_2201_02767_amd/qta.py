@@ -82,6 +82,20 @@ _SIGS = {
 }
 
 
+_AUX = {}
+
+
+def _aux_stream(device) -> "torch.cuda.Stream":
+    """One auxiliary stream per device for the whole process, shared by every plan: each new stream
+    takes the next hardware queue, and one shared stream keeps the backward's two streams on
+    distinct queues however many plans exist."""
+    dev = torch.device(device)
+    idx = dev.index if dev.index is not None else torch.cuda.current_device()
+    if idx not in _AUX:
+        _AUX[idx] = torch.cuda.Stream(device=idx)
+    return _AUX[idx]
+
+
 def lib() -> ctypes.CDLL:
     """Load ``libqta.so`` (raises if it has not been built)."""
     global _lib
@@ -351,10 +365,9 @@ class Plan:
         opt.K_levels = ctypes.addressof(self._k_tbl)
         opt.epipolar = int(self.epipolar)
         if overlap:
-            # a second stream of the plan's own for the sorts and key passes (ordered by the library)
-            if getattr(self, "_aux", None) is None:
-                self._aux = torch.cuda.Stream(device=self.device)
-            opt.aux_stream = self._aux.cuda_stream
+            # the process's second stream on this device for the sorts and key passes (the library
+            # orders it against the caller's stream)
+            opt.aux_stream = _aux_stream(self.device).cuda_stream
         args = (_ptr(q), _ptr(k), _ptr(v), _ptr(w), _ptr(dout), self.B, self.heads, self.H, self.W, self.d,
                 self.levels, self.K_levels[1] if self.levels > 1 else max(self.K_levels[0], 1),
                 _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), ctypes.byref(opt),
@@ -366,8 +379,8 @@ class Plan:
         """Gradients (dq, dk, dv, dw) in fp32 of the last ``run`` on the same inputs, for the upstream
         gradient ``dout`` (the kept keys of that run held fixed). ``dw`` is None unless QuadTree-B
         with ``w``. The returned tensors are the plan's own buffers, overwritten by the next call.
-        ``overlap``: run each level's sort and key pass on a second stream of the plan's own, beside
-        the next level's query pass (False: everything on the one stream)."""
+        ``overlap``: run each level's sort and key pass on a second stream (one per device for the
+        process), beside the next level's query pass (False: everything on the one stream)."""
         s = _stream(self.device) if stream is None else ctypes.c_void_p(stream)
         args, opt, grads = self._bwd_args(q, k, v, w, dout, s, overlap)
         _check("qta_backward_ex", lib().qta_backward_ex(*args))
