@@ -139,8 +139,8 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
  *              1 x W, which is also how the workspace and v_levels are laid out
  *              ([B*H][1][W_l][heads][d]) and how `levels` is validated (by W alone).
  *   aux_stream a second hipStream_t (caller-owned, default priority) on which qta_backward_ex may
- *              run the work that does not feed the next level: each level's counting sort and
- *              key pass overlap the coarser levels' query passes, which stay on `stream`. The
+ *              run work that does not feed the next level: the finest level's counting sort and
+ *              key pass overlap the coarser levels' work, which stays on `stream`. The
  *              call orders both streams itself (events recorded on one and waited for on the
  *              other); when it returns, all its work is ordered before later work on `stream`,
  *              and nothing later on aux_stream depends on it. NULL: everything on `stream`. The

@@ -732,8 +732,9 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     float* dw_out = (!va && w) ? dw : nullptr;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // the counting sorts and key passes go to the auxiliary stream when there is one (not for the
-    // finest step alone); `after(x, y)` orders later work on y after the work issued so far on x
+    // the finest level's counting sort and key pass go to the auxiliary stream when there is one
+    // (not for the finest step alone); `after(x, y)` orders later work on y after the work issued
+    // so far on x
     hipStream_t s2 = (opt && opt->aux_stream && !only_finest && levels > 1) ? static_cast<hipStream_t>(opt->aux_stream) : s;
     auto after = [](hipStream_t x, hipStream_t y) {
         hipEvent_t e;
@@ -741,6 +742,15 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
         const bool ok = hipEventRecord(e, x) == hipSuccess && hipStreamWaitEvent(y, e, 0) == hipSuccess;
         return hipEventDestroy(e) == hipSuccess && ok;
     };
+    struct DeferredKeys {
+        BwdLevelArgs a;
+        BwdScanArgs sc;
+        int level;
+    };
+    DeferredKeys deferred[QTA_MAX_LEVELS];
+    int ndeferred = 0;
+    const long long coarse_tiles = static_cast<long long>(B) * heads * ((L.H[levels - 1] * L.W[levels - 1] + 15) / 16);
+    const bool defer_coarser = s2 != s && coarse_tiles < device_cu_count();
     const bool use_bf16 = dtype == QTA_BF16;
     const float tau = resolve_scale(scale, d);
     const char* ws = static_cast<const char*>(workspace);
@@ -762,6 +772,11 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     if (levels > 1) {
         // 2. finer levels, finest first (QuadTree-A's score gradients go up one level each)
         for (int l = 0; l < (only_finest ? 1 : c); ++l) {
+            // with two streams the finest level's sort and key pass (the largest) go to the
+            // auxiliary stream right after its query pass. When the coarse level's tile kernels
+            // leave compute units idle (fewer 16-row tiles than units), the coarser levels' sorts
+            // and key passes follow them on the caller's stream, so that the coarse level runs
+            // beside the finest key pass; otherwise they too go to the auxiliary stream
             BwdLevelArgs a{};
             if (l == 0) {
                 a.q = q;
@@ -815,7 +830,7 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
             a.slot = reinterpret_cast<int32_t*>(gws + G.slot[l]);
             a.partial = fptr(G.partial[l]);
             if (launch_bwd_level(a, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
-            if (s2 != s && !after(s, s2)) return QTA_ERR_HIP;   // the sort and key pass need this query pass
+            if (s2 != s && (l == 0 || !defer_coarser) && !after(s, s2)) return QTA_ERR_HIP;   // the sort and key pass need this query pass
             BwdScanArgs sc{};
             sc.n = B * heads * L.H[l + 1] * L.W[l + 1];
             sc.nblocks = (sc.n + 1023) / 1024;
@@ -824,6 +839,10 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
             sc.coff = reinterpret_cast<int32_t*>(gws + G.coff[l]);
             sc.chunk_key = reinterpret_cast<int32_t*>(gws + G.chunk_key[l]);
             sc.block_sums = reinterpret_cast<int32_t*>(gws + G.block_sums[l]);
+            if (s2 != s && l > 0 && defer_coarser) {
+                deferred[ndeferred++] = DeferredKeys{a, sc, l};
+                continue;
+            }
             if (launch_bwd_keys(a, sc, d, va, use_bf16, l == 0, s2) != hipSuccess) return QTA_ERR_HIP;
         }
     }
@@ -865,7 +884,9 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
         if (launch_bwd_coarse(a, d, va, use_bf16, s) != hipSuccess) return QTA_ERR_HIP;
     }
     if (levels == 1) return QTA_OK;
-    if (s2 != s && !after(s2, s)) return QTA_ERR_HIP;       // every key pass before the unpooling
+    for (int i = 0; i < ndeferred; ++i)
+        if (launch_bwd_keys(deferred[i].a, deferred[i].sc, d, va, use_bf16, false, s) != hipSuccess) return QTA_ERR_HIP;
+    if (s2 != s && !after(s2, s)) return QTA_ERR_HIP;       // the finest key pass before the unpooling
 
     // 4. pyramids
     BwdUnpoolArgs u{};

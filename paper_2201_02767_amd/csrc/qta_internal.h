@@ -272,6 +272,20 @@ inline size_t device_max_lds()
     return static_cast<size_t>(cached[dev]);
 }
 
+// Compute units of the current device (cached per device).
+inline int device_cu_count()
+{
+    static int cached[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cached[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+        cached[dev] = v;
+    }
+    return cached[dev];
+}
+
 hipError_t launch_pyramid_pass(const PyramidPassArgs& a, int nlev, int ntensors, bool use_bf16, hipStream_t stream);
 hipError_t launch_coarse_attn(const CoarseArgs& a, int d, bool variant_a, bool use_bf16, hipStream_t stream);
 hipError_t launch_posenc(const PosEncArgs& a, bool use_bf16, hipStream_t stream);
