@@ -139,17 +139,19 @@ def test_backward_repeated_calls(dev):
             assert grad_err(to_np(a), to_np(b)) <= 1e-6
 
 
-@pytest.mark.parametrize("variant,dtype,name", [("B", "f32", "matching"), ("A", "bf16", "backbone")])
+@pytest.mark.parametrize("variant,dtype,name", [("B", "f32", "matching"), ("A", "bf16", "backbone"),
+                                                ("A", "bf16", "highres"), ("B", "bf16", "stereo_epipolar")])
 def test_backward_overlap_matches_one_stream(dev, variant, dtype, name):
-    """The two-stream schedule (each level's sort and key pass beside the next level's query pass)
-    gives the one-stream gradients, up to the order of the atomic sums."""
+    """The two-stream schedule (the finest level's sort and key pass on a second stream; the coarser
+    levels' either there too or after the coarse level, depending on its size) gives the one-stream
+    gradients, up to the order of the atomic sums."""
     wl = WORKLOADS[name].with_(variant=variant, dtype=dtype)
     announce(f"backward overlap vs one stream, {name} {variant} {dtype}")
     q, k, v = (dev_t(x, dtype, dev) for x in make_qkv(wl))
     g = dev_t(make_dout(wl), dtype, dev)
     w = torch.from_numpy(make_level_weights(wl)).to(dev) if variant == "B" else None
     plan = P.Plan(wl.B, wl.H, wl.W, wl.heads, wl.d, levels=wl.levels, K=wl.K, variant=variant, dtype=TDT[dtype],
-                  device=dev)
+                  device=dev, epipolar=wl.epipolar)
     plan.run(q, k, v, w)
     one = [None if t is None else t.clone() for t in plan.backward(q, k, v, g, w, overlap=False)]
     two = plan.backward(q, k, v, g, w, overlap=True)
