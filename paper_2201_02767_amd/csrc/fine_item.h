@@ -374,7 +374,28 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
 
     // ---- 3. weights ----
     float wgt[4], inv_sum[4] = {1.f, 1.f, 1.f, 1.f};
-    if constexpr (!VA) {
+    // the finest level of B with 32 slots and d = 32: two queries per register (lanes 0..31 query
+    // 2p, lanes 32..63 query 2p+1, slot lane & 31), so that one reduction within each 32-lane half
+    // serves two queries; the weights stay packed for the P store below (with d = 64 the extra
+    // registers cost occupancy)
+    constexpr bool kPack = !VA && FINEST && NSP == 32 && !ROW && D == 32;
+    float wpk[2];
+    if constexpr (kPack) {
+        // (the cross-lane exchanges run with every lane active, before the per-half selects)
+        const bool upper = lane >= 32;
+        const uint32_t ok_hi = xchg_u32<32>(ok ? 1u : 0u);
+        const bool okp = upper ? ok_hi != 0u : ok;
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const float hi = xchg_f32<32>(x[2 * p + 1]);
+            const float y = upper ? hi : x[2 * p];
+            const float m = half_allreduce(y, [](float u, float v) { return fmaxf(u, v); });
+            wpk[p] = okp ? __expf(y - m) : 0.f;
+            const float inv = fast_rcp(half_allreduce(wpk[p], [](float u, float v) { return u + v; }));   // >= 1
+            inv_sum[2 * p] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(inv), 0));
+            inv_sum[2 * p + 1] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(inv), 32));
+        }
+    } else if constexpr (!VA) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const float m = wave_max_fast(x[r]);
@@ -423,7 +444,16 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     }
 
     // ---- 5. messages on MFMA ----
-    if (lane < nsp) {
+    if constexpr (kPack) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const int row = 2 * p + (lane >> 5);
+            if constexpr (kBf16)
+                reinterpret_cast<uint16_t*>(Pb)[row * nsp + (lane & 31)] = static_cast<uint16_t>(f32_to_bf16_bits(wpk[p]));
+            else
+                reinterpret_cast<float*>(Pb)[row * nsp + (lane & 31)] = wpk[p];
+        }
+    } else if (lane < nsp) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             if constexpr (kBf16)

@@ -171,6 +171,18 @@ __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcp
 // log-sum-exp of softmax sums, which are at least 1.
 __device__ __forceinline__ float fast_ln(float x) { return __builtin_amdgcn_logf(x) * 0.69314718056f; }
 
+// Butterfly all-reduce within each 32-lane half of the wave.
+template <typename Op>
+__device__ __forceinline__ float half_allreduce(float x, Op op)
+{
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppXor1, 0xF, 0xF, false)));
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppXor2, 0xF, 0xF, false)));
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppRowHalfMirror, 0xF, 0xF, false)));
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppRowMirror, 0xF, 0xF, false)));
+    const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return op(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+}
+
 __device__ __forceinline__ float wave_max_fast(float x)
 {
     return wave_allreduce(x, [](float a, float b) { return fmaxf(a, b); });
