@@ -186,10 +186,161 @@ __global__ __launch_bounds__(256) void pyramid_pass2_kernel(PyramidPassArgs a, i
         S::pack(o);
 }
 
+// Three-level pass, workgroup = tpb top tokens (level s+3). A unit is one 16-byte chunk of one
+// level-1 token under a top token (NC * NC level-1 tokens each); a thread takes units tid,
+// tid + 256, ... (at most R), loads the 2x2 source chunks of all of them before pooling any, writes
+// the level-1 tokens and stages them in LDS; after a barrier the threads pool the staged level-1
+// tokens into level 2 (written and staged again), and after a second barrier into the top tokens.
+// ROW (maps of one row): two children per token, as in the two-level pass.
+template <typename T, bool ROW, int R>
+__global__ __launch_bounds__(256) void pyramid_pass3_kernel(PyramidPassArgs a, int tpb)
+{
+    using S = Storage<T>;
+    constexpr int E = S::kPer16B;
+    constexpr int NC = ROW ? 2 : 4;
+    __shared__ uint4 stage1[256 * R];
+    __shared__ uint4 stage2[256 * R / NC];
+    const int tensor = blockIdx.y;
+    const char* __restrict__ src = static_cast<const char*>(a.src[tensor]);
+    char* __restrict__ dst1 = static_cast<char*>(a.dst1[tensor]);
+    char* __restrict__ dst2 = static_cast<char*>(a.dst2[tensor]);
+    char* __restrict__ dst3 = static_cast<char*>(a.dst3[tensor]);
+    const int chunks = a.chunks;
+    const int per2 = NC * chunks;                      // units of one level-2 token
+    const int U = NC * per2;                           // units of one top token
+    const int nunits = tpb * U;
+    const int ntop = a.B * a.H3 * a.W3;                // < 2^31, checked by the launcher
+    const int top0 = static_cast<int>(blockIdx.x) * tpb;
+    // (b, Y, X) of the workgroup's top token t, clamped onto the last one past the end
+    auto top_pos = [&](int t, int& b, int& Y, int& X) {
+        const int top = min(top0 + t, ntop - 1);
+        X = top % a.W3;
+        Y = (top / a.W3) % a.H3;
+        b = top / (a.W3 * a.H3);
+    };
+
+    int b1[R], y1[R], x1[R], ch1[R];
+    bool ok1[R];
+    uint4 raw[R][2][2];
+#pragma unroll
+    for (int it = 0; it < R; ++it) {
+        const int u0 = it * 256 + static_cast<int>(threadIdx.x);
+        const int u = min(u0, nunits - 1);
+        const int t = u / U, r = u - t * U;
+        const int l1 = r / chunks;
+        ch1[it] = r - l1 * chunks;
+        const int q2 = l1 / NC, q1 = l1 - q2 * NC;
+        int Y, X;
+        top_pos(t, b1[it], Y, X);
+        const int y2 = ROW ? 0 : 2 * Y + (q2 >> 1), x2 = 2 * X + (ROW ? q2 : (q2 & 1));
+        y1[it] = ROW ? 0 : 2 * y2 + (q1 >> 1);
+        x1[it] = 2 * x2 + (ROW ? q1 : (q1 & 1));
+        ok1[it] = u0 < nunits && top0 + t < ntop && y1[it] < a.H1 && x1[it] < a.W1;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            if (ROW && i == 1) {                           // no row below
+                raw[it][1][0] = raw[it][0][0];
+                raw[it][1][1] = raw[it][0][1];
+                break;
+            }
+            const int y = min(2 * y1[it] + i, a.Hs - 1);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int x = min(2 * x1[it] + j, a.Ws - 1);
+                raw[it][i][j] = *reinterpret_cast<const uint4*>(
+                    src + chunk_offset(a.src_blocked, b1[it], y, x, a.Hs, a.Ws, ch1[it], chunks, a.head_chunks));
+            }
+        }
+    }
+#pragma unroll
+    for (int it = 0; it < R; ++it) {
+        float c00[E], c01[E], c10[E], c11[E], mid[E];
+        S::unpack(raw[it][0][0], c00);
+        S::unpack(raw[it][0][1], c01);
+        S::unpack(raw[it][1][0], c10);
+        S::unpack(raw[it][1][1], c11);
+        pool_children<E>(c00, c01, c10, c11, 2 * x1[it] + 1 < a.Ws, !ROW && 2 * y1[it] + 1 < a.Hs, mid);
+#pragma unroll
+        for (int e = 0; e < E; ++e) mid[e] = S::round(mid[e]);
+        const uint4 packed = S::pack(mid);
+        if (ok1[it])
+            *reinterpret_cast<uint4*>(dst1 + chunk_offset(a.dst1_blocked, b1[it], y1[it], x1[it], a.H1, a.W1,
+                                                          ch1[it], chunks, a.head_chunks)) = packed;
+        stage1[it * 256 + threadIdx.x] = packed;
+    }
+    __syncthreads();
+
+    // level 2: one unit per (level-2 token, chunk); its children are staged at (q2 * NC + q1) * chunks
+    const int n2 = tpb * per2;
+    for (int u = threadIdx.x; u < n2; u += 256) {
+        const int t = u / per2, r = u - t * per2;
+        const int q2 = r / chunks, ch = r - q2 * chunks;
+        int b, Y, X;
+        top_pos(t, b, Y, X);
+        const int y2 = ROW ? 0 : 2 * Y + (q2 >> 1), x2 = 2 * X + (ROW ? q2 : (q2 & 1));
+        const int base = t * U + q2 * per2 + ch;
+        float m0[E], m1[E], m2[E], m3[E], o[E];
+        S::unpack(stage1[base], m0);
+        S::unpack(stage1[base + chunks], m1);
+        S::unpack(stage1[base + (ROW ? 0 : 2) * chunks], m2);   // ROW: unused (no row below)
+        S::unpack(stage1[base + (ROW ? 1 : 3) * chunks], m3);
+        pool_children<E>(m0, m1, m2, m3, 2 * x2 + 1 < a.W1, !ROW && 2 * y2 + 1 < a.H1, o);
+#pragma unroll
+        for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
+        const uint4 packed = S::pack(o);
+        if (top0 + t < ntop && y2 < a.H2 && x2 < a.W2)
+            *reinterpret_cast<uint4*>(dst2 + chunk_offset(a.dst2_blocked, b, y2, x2, a.H2, a.W2, ch, chunks,
+                                                          a.head_chunks)) = packed;
+        stage2[u] = packed;
+    }
+    __syncthreads();
+
+    // top level: one unit per (top token, chunk); its children are staged at q2 * chunks
+    const int n3 = tpb * chunks;
+    for (int u = threadIdx.x; u < n3; u += 256) {
+        const int t = u / chunks, ch = u - t * chunks;
+        if (top0 + t >= ntop) break;
+        int b, Y, X;
+        top_pos(t, b, Y, X);
+        const int base = t * per2 + ch;
+        float m0[E], m1[E], m2[E], m3[E], o[E];
+        S::unpack(stage2[base], m0);
+        S::unpack(stage2[base + chunks], m1);
+        S::unpack(stage2[base + (ROW ? 0 : 2) * chunks], m2);
+        S::unpack(stage2[base + (ROW ? 1 : 3) * chunks], m3);
+        pool_children<E>(m0, m1, m2, m3, 2 * X + 1 < a.W2, !ROW && 2 * Y + 1 < a.H2, o);
+#pragma unroll
+        for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
+        *reinterpret_cast<uint4*>(dst3 + chunk_offset(a.dst3_blocked, b, Y, X, a.H3, a.W3, ch, chunks,
+                                                      a.head_chunks)) = S::pack(o);
+    }
+}
+
 }  // namespace
+
+template <typename T, bool ROW>
+static hipError_t launch_pass3(const PyramidPassArgs& a, int ntensors, hipStream_t stream)
+{
+    const int U = (ROW ? 4 : 16) * a.chunks;
+    const int tpb = U >= 256 ? 1 : 256 / U;
+    const int R = (tpb * U + 255) / 256;
+    const long long ntop = static_cast<long long>(a.B) * a.H3 * a.W3;
+    if (ntop <= 0 || ntop > 0x7FFFFFFFLL || R > 4) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>((ntop + tpb - 1) / tpb), ntensors);
+    if (R == 1) hipLaunchKernelGGL((pyramid_pass3_kernel<T, ROW, 1>), grid, dim3(256), 0, stream, a, tpb);
+    else if (R == 2) hipLaunchKernelGGL((pyramid_pass3_kernel<T, ROW, 2>), grid, dim3(256), 0, stream, a, tpb);
+    else hipLaunchKernelGGL((pyramid_pass3_kernel<T, ROW, 4>), grid, dim3(256), 0, stream, a, tpb);
+    return hipGetLastError();
+}
 
 hipError_t launch_pyramid_pass(const PyramidPassArgs& a, int nlev, int ntensors, bool use_bf16, hipStream_t stream)
 {
+    if (nlev == 3) {
+        const bool row = a.Hs == 1;
+        if (!pyramid_pass3_fits(a.chunks, row)) return hipErrorInvalidValue;
+        if (use_bf16) return row ? launch_pass3<bf16, true>(a, ntensors, stream) : launch_pass3<bf16, false>(a, ntensors, stream);
+        return row ? launch_pass3<float, true>(a, ntensors, stream) : launch_pass3<float, false>(a, ntensors, stream);
+    }
     if (nlev == 2 && 4 * a.chunks <= 256) {
         const bool row = a.Hs == 1;                       // maps of one row: two children per token
         const int nc = row ? 2 : 4;

@@ -39,17 +39,22 @@ inline size_t level_bytes(bool blocked, int B, int H, int W, int C, int tb)
     return static_cast<size_t>(B) * ((H + 1) / 2) * ((W + 1) / 2) * 4 * C * tb;
 }
 
-// One pyramid pass over up to three token maps (q, k, v): from a source level produce one or two
-// coarser levels.
+// One pyramid pass over up to three token maps (q, k, v): from a source level produce one, two or
+// three coarser levels.
 struct PyramidPassArgs {
     const void* src[3];
     void* dst1[3];
     void* dst2[3];
-    int B, Hs, Ws, H1, W1, H2, W2;
+    void* dst3[3];
+    int B, Hs, Ws, H1, W1, H2, W2, H3, W3;
     int chunks;                 // 16-byte chunks per token (C * sizeof(dtype) / 16)
     int head_chunks;            // 16-byte chunks per head row (d * sizeof(dtype) / 16)
-    bool src_blocked, dst1_blocked, dst2_blocked;
+    bool src_blocked, dst1_blocked, dst2_blocked, dst3_blocked;
 };
+
+// Whether the three-level pass takes tokens of `chunks` 16-byte chunks (maps of one row when
+// `row`): a top token's level-1 children must fit 1024 chunks, four per thread.
+inline bool pyramid_pass3_fits(int chunks, bool row) { return (row ? 4 : 16) * chunks <= 1024; }
 
 struct CoarseArgs {
     const void* q;

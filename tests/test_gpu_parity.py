@@ -111,6 +111,9 @@ def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=No
     ("f32", 3, 37, 53, 96, 6), ("bf16", 2, 200, 336, 64, 5), ("f32", 1, 60, 80, 256, 3),
     # 16 top tokens per workgroup; tokens too wide for the staged pass (80 chunks, fp32 and bf16)
     ("bf16", 1, 33, 17, 32, 4), ("f32", 1, 19, 23, 320, 4), ("bf16", 2, 9, 11, 640, 3),
+    # three-level pass: 3 of 4 chunk slots per thread used; one-row maps with two level-2 rounds;
+    # 8 top tokens per workgroup
+    ("f32", 2, 21, 27, 160, 4), ("bf16", 3, 1, 45, 1600, 4), ("f32", 2, 9, 7, 8, 4),
 ])
 def test_pyramid_bit_exact(dev, dtype, B, H, W, C, L):
     rng = np.random.default_rng(H * W + C)
