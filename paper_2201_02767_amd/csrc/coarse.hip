@@ -13,6 +13,8 @@
 //            output in the storage type).
 // The coarsest map holds at most QTA_MAX_COARSE tokens, so a row fits in 16 registers per lane.
 // Maps of at most 64 tokens take coarse_small_kernel instead (one wave per query row).
+#include <type_traits>
+
 #include "qta_device.h"
 #include "qta_internal.h"
 
@@ -236,86 +238,217 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     }
 }
 
-// Small coarsest maps (N <= 64, e.g. the many short maps of attention along epipolar lines): one
-// wave per query row, lane j holding key j. The logits are per-lane dot products, the softmax and the
-// selection are wave reductions and a ballot radix select, and lane c then forms channel c of the
-// message from the weights in LDS, four value rows in flight at a time.
+// Sum over each aligned group of G consecutive lanes (G = 4, 8 or 16), the same bits in every lane of
+// a group (each step adds two partial sums that the two lanes hold in swapped roles).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v)
+{
+    return __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), CTRL, 0xF, 0xF, false));
+}
+
+template <int G>
+__device__ __forceinline__ float group_sum(float x)
+{
+    static_assert(G == 4 || G == 8 || G == 16, "group of 4, 8 or 16 lanes");
+    x += dpp_f32<kDppXor1>(x);
+    x += dpp_f32<kDppXor2>(x);
+    if constexpr (G >= 8) x += dpp_f32<kDppRowHalfMirror>(x);
+    if constexpr (G >= 16) x += dpp_f32<kDppRowMirror>(x);
+    return x;
+}
+
+// a.lo * b.lo + a.hi * b.hi + c for two packed bf16 pairs, fp32 accumulation
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c)
+{
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+// Small coarsest maps (N <= 64, e.g. the many short maps of attention along epipolar lines): a wave
+// takes `qpw` consecutive query rows of one (batch, head) map, lane j holding key j. Key row j and
+// the value chunks a lane needs are loaded once per wave; per query row the logits are per-lane dot
+// products, the softmax and the selection are wave reductions and a ballot radix select, and the
+// message is formed from the weights in LDS: lane (c, g) sums chunk c of value rows g, g + G, ...
+// and DPP sums over the G lanes of a chunk add the groups.
 template <typename T, int D, bool VA>
-__global__ __launch_bounds__(256) void coarse_small_kernel(CoarseArgs a)
+__global__ __launch_bounds__(256) void coarse_small_kernel(CoarseArgs a, int qpw)
 {
     using S = Storage<T>;
     constexpr int E = S::kPer16B;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int CH = D / E;                                 // chunks of a head row
+    constexpr int G = kWave / CH;                             // key groups of the message, >= E (D <= 64)
+    constexpr int NV = kWave / G;                             // value rows a lane covers (N <= 64)
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
     const int N = a.N, C = a.C;
-    const long long rows = static_cast<long long>(a.B) * a.heads * N;
-    const long long row = static_cast<long long>(blockIdx.x) * (blockDim.x >> 6) + wave;
-    if (row >= rows) return;                                  // whole wave
-    const int qi = static_cast<int>(row % N);
-    const int bh = static_cast<int>(row / N);
+    const int wpm = (N + qpw - 1) / qpw;                      // waves per map
+    const int gw = static_cast<int>(blockIdx.x) * 4 + wave;   // < 2^31, checked by the launcher
+    if (gw >= a.B * a.heads * wpm) return;                    // whole wave
+    const int bh = gw / wpm;
+    const int q0 = (gw - bh * wpm) * qpw, qend = min(q0 + qpw, N);
     const int h = bh % a.heads, b = bh / a.heads;
     const size_t tok0 = static_cast<size_t>(b) * N;
     const size_t hoff = static_cast<size_t>(h) * D;
-    const int j = min(lane, N - 1);
     const bool valid = lane < N;
-    // the query row (the same address on every lane) and key row j
-    const uint4* qp = reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.q) + ((tok0 + qi) * C + hoff) * sizeof(T));
-    const uint4* kp = reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.k) + ((tok0 + j) * C + hoff) * sizeof(T));
+    const unsigned char* qb = static_cast<const unsigned char*>(a.q) + (tok0 * C + hoff) * sizeof(T);
+    // key row j (clamped onto the map) and value chunk c of rows g, g + G, ...
+    const int c = lane / G, g = lane % G;
+    // bf16 keys stay packed (products of pairs with the query's packed pairs); fp32 keys as floats
+    constexpr bool kDot2 = std::is_same<T, bf16>::value;
+    uint4 kraw[CH];
+    float kf[kDot2 ? 1 : D];
+    uint4 vraw[NV];
+    {
+        const uint4* kp = reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.k) +
+                                                         ((tok0 + min(lane, N - 1)) * C + hoff) * sizeof(T));
+        const unsigned char* vb = static_cast<const unsigned char*>(a.v) + (tok0 * C + hoff) * sizeof(T) + c * 16;
+#pragma unroll
+        for (int cc = 0; cc < CH; ++cc) kraw[cc] = kp[cc];
+#pragma unroll
+        for (int u = 0; u < NV; ++u)
+            vraw[u] = *reinterpret_cast<const uint4*>(vb + static_cast<size_t>(min(g + u * G, N - 1)) * C * sizeof(T));
+        if constexpr (!kDot2) {
+#pragma unroll
+            for (int cc = 0; cc < CH; ++cc) S::unpack(kraw[cc], kf + cc * E);
+        }
+    }
     __shared__ float pw[4][kWave];
-    float x = 0.f;
+    __shared__ int sidx[4][kWave];
+    __shared__ float skey[4][kWave];
+    // the query row: lanes c * G, ... hold its chunk c, read by every lane with readlane; the next
+    // row is in flight while this one is used
+    auto qchunk = [&](int qi) {
+        return reinterpret_cast<const uint4*>(qb + static_cast<size_t>(qi) * C * sizeof(T))[c];
+    };
+    uint4 qv = qchunk(q0);
+    // the previous row's selection and message, stored once this row's query has arrived so that
+    // the wait for the query never waits for them
+    size_t sel_at = 0, msg_at = 0;
+    int sel_i = 0;
+    float sel_k = 0.f, msg_v = 0.f;
+    bool sel_pending = false, msg_pending = false;
+    for (int qi = q0; qi < qend; ++qi) {
+        float x = 0.f;
 #pragma unroll
-    for (int cc = 0; cc < D / E; ++cc) {
-        float qf[E], kf[E];
-        S::unpack(qp[cc], qf);
-        S::unpack(kp[cc], kf);
+        for (int cc = 0; cc < CH; ++cc) {
+            uint4 t;
+            t.x = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(qv.x), cc * G));
+            t.y = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(qv.y), cc * G));
+            t.z = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(qv.z), cc * G));
+            t.w = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(qv.w), cc * G));
+            if constexpr (kDot2) {
+                x = dot2_bf16(t.x, kraw[cc].x, x);
+                x = dot2_bf16(t.y, kraw[cc].y, x);
+                x = dot2_bf16(t.z, kraw[cc].z, x);
+                x = dot2_bf16(t.w, kraw[cc].w, x);
+            } else {
+                float qf[E];
+                S::unpack(t, qf);
 #pragma unroll
-        for (int e = 0; e < E; ++e) x += qf[e] * kf[e];
-    }
-    x = valid ? x * a.scale : -INFINITY;
-    const float mx = wave_max_fast(x);
-    float p = valid ? __expf(x - mx) : 0.f;
-    p *= 1.0f / wave_sum_fast(p);
-    if (a.K > 0) {
-        const uint32_t key[1] = {valid ? ordered_bits(x) : 0u};
-        const uint32_t name[1] = {static_cast<uint32_t>(lane)};
-        bool kept[1];
-        const int keff = a.K < N ? a.K : N;
-        wave_select_top<1>(key, name, keff, kept);
-        const size_t orow = (static_cast<size_t>(bh) * N + qi) * a.K;
-        const uint64_t mask = __ballot(kept[0]);
-        if (kept[0]) {
-            const int pos = lanes_below(mask);
-            a.sel_idx[orow + pos] = lane;
-            a.sel_key[orow + pos] = p;
-            if constexpr (VA) p = 0.f;                        // refined at the next level (Omega)
+                for (int e = 0; e < E; ++e) x += qf[e] * kf[cc * E + e];
+            }
         }
-        if (lane >= keff && lane < a.K) {
-            a.sel_idx[orow + lane] = -1;
-            a.sel_key[orow + lane] = 0.f;
+        qv = qchunk(min(qi + 1, qend - 1));
+        if (sel_pending) {
+            a.sel_idx[sel_at] = sel_i;
+            a.sel_key[sel_at] = sel_k;
+        }
+        if (msg_pending) a.msg[msg_at] = msg_v;
+        x = valid ? x * a.scale : -INFINITY;
+        const float mx = wave_max_fast(x);
+        float p = valid ? __expf(x - mx) : 0.f;
+        p *= fast_rcp(wave_sum_fast(p));
+        if (a.K > 0) {
+            const uint32_t key[1] = {valid ? ordered_bits(x) : 0u};
+            const uint32_t name[1] = {static_cast<uint32_t>(lane)};
+            bool sel[1];
+            const int keff = a.K < N ? a.K : N;
+            wave_select_top<1>(key, name, keff, sel);
+            const bool kept = sel[0];
+            // listed in index order through LDS, then slot o = min(lane, K - 1) written by every lane
+            // (lanes past K repeat slot K - 1 with its own values)
+            if (kept) {
+                const int pos = lanes_below(__ballot(kept));
+                sidx[wave][pos] = lane;
+                skey[wave][pos] = p;
+                if constexpr (VA) p = 0.f;                    // refined at the next level (Omega)
+            }
+            wave_lds_sync();
+            const int o = min(lane, a.K - 1);
+            const size_t orow = (static_cast<size_t>(bh) * N + qi) * a.K;
+            const int oi = sidx[wave][min(o, kWave - 1)];
+            const float ok = skey[wave][min(o, kWave - 1)];
+            sel_at = orow + o;
+            sel_i = o < keff ? oi : -1;
+            sel_k = o < keff ? ok : 0.f;
+            sel_pending = true;
+        }
+        pw[wave][lane] = p;
+        wave_lds_sync();
+        float acc[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = 0.f;
+#pragma unroll
+        for (int u = 0; u < NV; ++u) {
+            const int jj = g + u * G;
+            float pj = pw[wave][jj];
+            pj = jj < N ? pj : 0.f;
+            float vf[E];
+            S::unpack(vraw[u], vf);
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc[e] += pj * vf[e];
+        }
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = group_sum<G>(acc[e]);
+        // every lane holds its chunk's sums: lane (g, c) writes channel c * E + g % E (lanes with
+        // g >= E repeat a channel with the same value)
+        const int ge = g % E;
+        float m = acc[0];
+#pragma unroll
+        for (int e = 1; e < E; ++e) m = ge == e ? acc[e] : m;
+        const int ch = c * E + ge;
+        if (a.out) {
+            float wl = 1.0f;
+            if (!VA) wl = a.w ? a.w[((tok0 + qi) * a.heads + h) * a.levels] : 1.0f / a.levels;
+            const float pe = a.pe0 ? a.pe0[((tok0 + qi) * a.heads + h) * D + ch] : 0.f;
+            S::store1(a.out, (tok0 + qi) * C + hoff + ch, wl * (m + pe));
+        } else {
+            msg_at = ((tok0 + qi) * a.heads + h) * D + ch;
+            msg_v = m;
+            msg_pending = true;
         }
     }
-    pw[wave][lane] = p;
-    wave_lds_sync();
-    if (lane >= D) return;
-    float m = 0.f;
-#pragma unroll 4
-    for (int jj = 0; jj < N; ++jj) m += pw[wave][jj] * S::load1(a.v, (tok0 + jj) * C + hoff + lane);
-    if (a.out) {
-        float wl = 1.0f;
-        if (!VA) wl = a.w ? a.w[((tok0 + qi) * a.heads + h) * a.levels] : 1.0f / a.levels;
-        const float pe = a.pe0 ? a.pe0[((tok0 + qi) * a.heads + h) * D + lane] : 0.f;
-        S::store1(a.out, (tok0 + qi) * C + hoff + lane, wl * (m + pe));
-    } else {
-        a.msg[((tok0 + qi) * a.heads + h) * D + lane] = m;
+    if (sel_pending) {
+        a.sel_idx[sel_at] = sel_i;
+        a.sel_key[sel_at] = sel_k;
     }
+    if (msg_pending) a.msg[msg_at] = msg_v;
 }
 
 template <typename T, int D, bool VA>
 hipError_t launch_small(const CoarseArgs& a, hipStream_t stream)
 {
-    const long long rows = static_cast<long long>(a.B) * a.heads * a.N;
-    const long long blocks = (rows + 3) / 4;
-    if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((coarse_small_kernel<T, D, VA>), dim3(static_cast<unsigned>(blocks)), dim3(4 * kWave), 0, stream, a);
+    // enough query rows per wave that the waves fit the chip's wave slots (at the kernel's
+    // occupancy) about once
+    static int blocks_per_cu = 0;
+    if (blocks_per_cu == 0) {
+        int n = 0;
+        hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &n, reinterpret_cast<const void*>(&coarse_small_kernel<T, D, VA>), 4 * kWave, 0);
+        if (e != hipSuccess) return e;
+        blocks_per_cu = n > 0 ? n : 1;
+    }
+    const long long maps = static_cast<long long>(a.B) * a.heads;
+    const long long slots = static_cast<long long>(device_cu_count()) * blocks_per_cu * 4;
+    long long qpw = std::min<long long>(a.N, std::max<long long>(1, (maps * a.N + slots - 1) / slots));
+    while (qpw < a.N && maps * ((a.N + qpw - 1) / qpw) > slots) ++qpw;   // no partial second round
+    const long long wpm = (a.N + qpw - 1) / qpw;
+    qpw = (a.N + wpm - 1) / wpm;                                          // the rows spread evenly
+    const long long waves = maps * wpm;
+    if (waves > 0x7FFFFFFFLL - 3) return hipErrorInvalidValue;
+    const long long blocks = (waves + 3) / 4;
+    hipLaunchKernelGGL((coarse_small_kernel<T, D, VA>), dim3(static_cast<unsigned>(blocks)), dim3(4 * kWave), 0, stream, a,
+                       static_cast<int>(qpw));
     return hipGetLastError();
 }
 
