@@ -1,7 +1,6 @@
 // The per-item body of the gathered fine attention (steps 3-5 at the finer levels; Sec. 3.2,
 // Fig. 1; QuadTree-A scores Eq. 4, QuadTree-B softmax Eq. 6; the finest level's combination,
-// Eqs. 2 and 5). Shared by the fine kernels and the coarse kernel, which runs the first finer
-// level's items of its own queries right after selecting their keys.
+// Eqs. 2 and 5), included by the fine kernels of every finer level.
 //
 // Work item = one parent query P at level l+1 and one head. Its four children at level l are
 // sibling queries with one shared candidate set: the 2x2 children of the K keys P kept (4K <= 64
