@@ -743,9 +743,11 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     // (not for the finest step alone); `after(x, y)` orders later work on y after the work issued
     // so far on x
     hipStream_t s2 = (opt && opt->aux_stream && !only_finest && levels > 1) ? static_cast<hipStream_t>(opt->aux_stream) : s;
+    // (both streams feed this device's kernels only: a device-scope release is enough, and the
+    // system-scope one would add a cache write-back on every hand-over)
     auto after = [](hipStream_t x, hipStream_t y) {
         hipEvent_t e;
-        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return false;
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming | hipEventDisableSystemFence) != hipSuccess) return false;
         const bool ok = hipEventRecord(e, x) == hipSuccess && hipStreamWaitEvent(y, e, 0) == hipSuccess;
         return hipEventDestroy(e) == hipSuccess && ok;
     };
