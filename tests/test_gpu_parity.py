@@ -228,6 +228,7 @@ def test_stages_teacher_forced(dev, variant, dtype, d, K):
     (1, 1, 40, 2, 32, 4, 3),        # single row
     (1, 12, 12, 1, 32, 3, 20),      # K above the candidate count (two slot chunks)
     (1, 20, 24, 2, 64, 3, 64),      # K = 64 (four slot chunks)
+    (1, 29, 32, 2, 64, 3, 8),       # coarse level of exactly 64 tokens (8 x 8), d = 64
 ])
 def test_forward_parity(dev, variant, dtype, B, H, W, heads, d, L, K):
     q, k, v = rand_qkv(B * H * W + L * K, B, H, W, heads, d, dtype)
@@ -439,6 +440,9 @@ def test_forward_position_encoding(dev, variant, dtype, B, H, W, heads, d, L, K,
     ("A", "bf16", 2, 3, 93, 1, 64, 5, [0, 2, 4, 8, 16], False, False),   # K schedule; 4 levels of pairs
     ("B", "f32", 1, 4, 50, 2, 32, 3, 20, False, False),     # 40 candidates per query
     ("B", "bf16", 1, 6, 41, 2, 32, 3, 4, True, True),       # given V levels and the position encoding
+    # 1200 coarse rows of 10 tokens, d = 64: several query rows per wave in the small-map coarse kernel
+    ("A", "f32", 1, 600, 40, 2, 64, 3, 8, False, False),
+    ("B", "bf16", 1, 600, 40, 2, 64, 3, 8, False, False),
 ])
 def test_forward_epipolar(dev, variant, dtype, B, H, W, heads, d, L, K, given_v, pe):
     q, k, v = rand_qkv(900 + H * W + L, B, H, W, heads, d, dtype)
