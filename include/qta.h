@@ -145,6 +145,11 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
  *              other); when it returns, all its work is ordered before later work on `stream`,
  *              and nothing later on aux_stream depends on it. NULL: everything on `stream`. The
  *              forward ignores it.
+ *   aux_stream2 a third hipStream_t (caller-owned, default priority, distinct from the other two),
+ *              used only with aux_stream: the coarser finer levels' counting sorts and key passes
+ *              run there, each right after its level's query pass, beside the finest key pass on
+ *              aux_stream and the coarse level on `stream`; ordered and joined like aux_stream.
+ *              NULL: those go to aux_stream or `stream`, whichever keeps the coarse level busier.
  */
 typedef struct {
     const int* K_levels;
@@ -153,6 +158,7 @@ typedef struct {
     const float* pe_bias;
     int epipolar;
     void* aux_stream;
+    void* aux_stream2;
 } qta_options;
 
 /* Workspace of qta_forward_ex with these options (layout and byte count as for qta_forward; with a

@@ -743,6 +743,8 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     // (not for the finest step alone); `after(x, y)` orders later work on y after the work issued
     // so far on x
     hipStream_t s2 = (opt && opt->aux_stream && !only_finest && levels > 1) ? static_cast<hipStream_t>(opt->aux_stream) : s;
+    // with a third stream the coarser finer levels' sorts and key passes go there
+    hipStream_t s3 = (s2 != s && opt->aux_stream2) ? static_cast<hipStream_t>(opt->aux_stream2) : s;
     // (both streams feed this device's kernels only: a device-scope release is enough, and the
     // system-scope one would add a cache write-back on every hand-over)
     auto after = [](hipStream_t x, hipStream_t y) {
@@ -759,7 +761,7 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     DeferredKeys deferred[QTA_MAX_LEVELS];
     int ndeferred = 0;
     const long long coarse_tiles = static_cast<long long>(B) * heads * ((L.H[levels - 1] * L.W[levels - 1] + 15) / 16);
-    const bool defer_coarser = s2 != s && coarse_tiles < device_cu_count();
+    const bool defer_coarser = s2 != s && s3 == s && coarse_tiles < device_cu_count();
     const bool use_bf16 = dtype == QTA_BF16;
     const float tau = resolve_scale(scale, d);
     const char* ws = static_cast<const char*>(workspace);
@@ -839,7 +841,9 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
             a.slot = reinterpret_cast<int32_t*>(gws + G.slot[l]);
             a.partial = fptr(G.partial[l]);
             if (launch_bwd_level(a, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
-            if (s2 != s && (l == 0 || !defer_coarser) && !after(s, s2)) return QTA_ERR_HIP;   // the sort and key pass need this query pass
+            // the stream of this level's sort and key pass, which need its query pass
+            const hipStream_t sk = l == 0 ? s2 : (s3 != s ? s3 : (defer_coarser ? s : s2));
+            if (sk != s && !after(s, sk)) return QTA_ERR_HIP;
             BwdScanArgs sc{};
             sc.n = B * heads * L.H[l + 1] * L.W[l + 1];
             sc.nblocks = (sc.n + 1023) / 1024;
@@ -852,7 +856,7 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
                 deferred[ndeferred++] = DeferredKeys{a, sc, l};
                 continue;
             }
-            if (launch_bwd_keys(a, sc, d, va, use_bf16, l == 0, s2) != hipSuccess) return QTA_ERR_HIP;
+            if (launch_bwd_keys(a, sc, d, va, use_bf16, l == 0, sk) != hipSuccess) return QTA_ERR_HIP;
         }
     }
     if (only_finest) return QTA_OK;
@@ -895,7 +899,8 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     if (levels == 1) return QTA_OK;
     for (int i = 0; i < ndeferred; ++i)
         if (launch_bwd_keys(deferred[i].a, deferred[i].sc, d, va, use_bf16, false, s) != hipSuccess) return QTA_ERR_HIP;
-    if (s2 != s && !after(s2, s)) return QTA_ERR_HIP;       // the finest key pass before the unpooling
+    if (s2 != s && !after(s2, s)) return QTA_ERR_HIP;       // the key passes before the unpooling
+    if (s3 != s && !after(s3, s)) return QTA_ERR_HIP;
 
     // 4. pyramids
     BwdUnpoolArgs u{};

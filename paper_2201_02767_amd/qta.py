@@ -53,6 +53,7 @@ class Options(ctypes.Structure):
         ("pe_bias", ctypes.c_void_p),
         ("epipolar", ctypes.c_int),
         ("aux_stream", ctypes.c_void_p),
+        ("aux_stream2", ctypes.c_void_p),
     ]
 
 
@@ -85,15 +86,15 @@ _SIGS = {
 _AUX = {}
 
 
-def _aux_stream(device) -> "torch.cuda.Stream":
-    """One auxiliary stream per device for the whole process, shared by every plan: each new stream
-    takes the next hardware queue, and one shared stream keeps the backward's two streams on
-    distinct queues however many plans exist."""
+def _aux_stream(device, which: int = 0) -> "torch.cuda.Stream":
+    """Auxiliary stream `which` (0 or 1) of a device, one each for the whole process and shared by
+    every plan: each new stream takes the next hardware queue, and shared streams keep the
+    backward's three streams on distinct queues however many plans exist."""
     dev = torch.device(device)
     idx = dev.index if dev.index is not None else torch.cuda.current_device()
     if idx not in _AUX:
-        _AUX[idx] = torch.cuda.Stream(device=idx)
-    return _AUX[idx]
+        _AUX[idx] = (torch.cuda.Stream(device=idx), torch.cuda.Stream(device=idx))
+    return _AUX[idx][which]
 
 
 def lib() -> ctypes.CDLL:
@@ -365,9 +366,10 @@ class Plan:
         opt.K_levels = ctypes.addressof(self._k_tbl)
         opt.epipolar = int(self.epipolar)
         if overlap:
-            # the process's second stream on this device for the sorts and key passes (the library
-            # orders it against the caller's stream)
-            opt.aux_stream = _aux_stream(self.device).cuda_stream
+            # the process's second and third streams on this device for the sorts and key passes
+            # (the library orders them against the caller's stream)
+            opt.aux_stream = _aux_stream(self.device, 0).cuda_stream
+            opt.aux_stream2 = _aux_stream(self.device, 1).cuda_stream
         args = (_ptr(q), _ptr(k), _ptr(v), _ptr(w), _ptr(dout), self.B, self.heads, self.H, self.W, self.d,
                 self.levels, self.K_levels[1] if self.levels > 1 else max(self.K_levels[0], 1),
                 _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), ctypes.byref(opt),
