@@ -1173,24 +1173,25 @@ hipError_t launch_key_td(const BwdLevelArgs& a, bool variant_a, bool finest, lon
 template <int LMAX>
 __global__ __launch_bounds__(256) void bwd_unpool_kernel(BwdUnpoolArgs a)
 {
-    // one thread per 4 channels of a level-0 token; a batch element takes a.bpb consecutive blocks
-    // (its map is below 2^31 bytes, so its chunk index fits 32 bits)
+    // one thread per 4 channels of the (up to) 2x2 level-0 tokens under one level-1 token, which
+    // share every ancestor: the ancestors' rows are loaded once for four tokens. A batch element
+    // takes a.bpb consecutive blocks (its maps are below 2^31 bytes, so chunk indices fit 32 bits)
     const int cpt = a.C / 4;
-    const int n0 = a.H[0] * a.W[0] * cpt;
+    const int n1 = a.H[1] * a.W[1] * cpt;
     const int b = static_cast<int>(blockIdx.x) / a.bpb;
     const int t = (static_cast<int>(blockIdx.x) - b * a.bpb) * blockDim.x + threadIdx.x;
-    if (t >= n0) return;
+    if (t >= n1) return;
     const int i = fast_div(t, a.div_cpt);
     const int ch = t - i * cpt;
-    const int y = fast_div(i, a.div_W0), x = i - y * a.W[0];
-    // every load first (the ancestors' rows at each level, then this token's rows), then the sums
+    const int y1 = fast_div(i, a.div_W1), x1 = i - y1 * a.W[1];
+    // every load first (the ancestors' rows at each level, then the four tokens' rows), then the sums
     float4 g[LMAX][3];
     float f[LMAX];
     float fl = 1.0f;
 #pragma unroll
     for (int l = 1; l < LMAX; ++l) {
         if (l >= a.L) break;                                  // uniform
-        const int yl = y >> l, xl = x >> l;
+        const int yl = y1 >> (l - 1), xl = x1 >> (l - 1);
         const int ny = (2 * yl + 1 < a.H[l - 1]) ? 2 : 1, nx = (2 * xl + 1 < a.W[l - 1]) ? 2 : 1;
         fl *= 1.0f / static_cast<float>(ny * nx);
         f[l] = fl;
@@ -1200,23 +1201,41 @@ __global__ __launch_bounds__(256) void bwd_unpool_kernel(BwdUnpoolArgs a)
         g[l][1] = *reinterpret_cast<const float4*>(a.gk[l] + off);
         g[l][2] = *reinterpret_cast<const float4*>(a.gv[l] + off);
     }
-    const size_t o = static_cast<size_t>(b) * static_cast<uint32_t>(n0) * 4 + static_cast<uint32_t>(t) * 4;
-    float4* const p[3] = {reinterpret_cast<float4*>(a.dq + o), reinterpret_cast<float4*>(a.dk + o),
-                          reinterpret_cast<float4*>(a.dv + o)};
-    float4 r[3] = {*p[0], *p[1], *p[2]};
+    const int H0 = a.H[0], W0 = a.W[0];
+    const size_t base = static_cast<size_t>(b) * static_cast<uint32_t>(H0 * W0 * a.C) + 4 * ch;
+    uint32_t tok[4];
+    bool ok[4];
+    float4 r[4][3];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int y = 2 * y1 + (c >> 1), x = 2 * x1 + (c & 1);
+        ok[c] = y < H0 && x < W0;
+        tok[c] = static_cast<uint32_t>((min(y, H0 - 1) * W0 + min(x, W0 - 1)) * a.C);   // clamped onto the map
+        r[c][0] = *reinterpret_cast<const float4*>(a.dq + base + tok[c]);
+        r[c][1] = *reinterpret_cast<const float4*>(a.dk + base + tok[c]);
+        r[c][2] = *reinterpret_cast<const float4*>(a.dv + base + tok[c]);
+    }
+    float4 s[3] = {};
 #pragma unroll
     for (int l = 1; l < LMAX; ++l) {
         if (l >= a.L) break;                                  // uniform
 #pragma unroll
         for (int m = 0; m < 3; ++m) {
-            r[m].x += f[l] * g[l][m].x;
-            r[m].y += f[l] * g[l][m].y;
-            r[m].z += f[l] * g[l][m].z;
-            r[m].w += f[l] * g[l][m].w;
+            s[m].x += f[l] * g[l][m].x;
+            s[m].y += f[l] * g[l][m].y;
+            s[m].z += f[l] * g[l][m].z;
+            s[m].w += f[l] * g[l][m].w;
         }
     }
+    float* const dst[3] = {a.dq, a.dk, a.dv};
 #pragma unroll
-    for (int m = 0; m < 3; ++m) *p[m] = r[m];
+    for (int c = 0; c < 4; ++c) {
+        if (!ok[c]) continue;
+#pragma unroll
+        for (int m = 0; m < 3; ++m)
+            *reinterpret_cast<float4*>(dst[m] + base + tok[c]) =
+                make_float4(r[c][m].x + s[m].x, r[c][m].y + s[m].y, r[c][m].z + s[m].z, r[c][m].w + s[m].w);
+    }
 }
 
 }  // namespace
@@ -1306,12 +1325,14 @@ hipError_t launch_bwd_keys(const BwdLevelArgs& a, const BwdScanArgs& sc, int d, 
 
 hipError_t launch_bwd_unpool(const BwdUnpoolArgs& a, hipStream_t stream)
 {
-    const long long n0 = static_cast<long long>(a.H[0]) * a.W[0] * (a.C / 4);
-    const long long bpb = (n0 + 255) / 256;
-    if (n0 >= 0x7FFFFFFFLL || bpb * a.B >= 0x7FFFFFFFLL || a.L < 2) return hipErrorInvalidValue;
+    if (a.L < 2) return hipErrorInvalidValue;
+    const long long n0 = static_cast<long long>(a.H[0]) * a.W[0] * a.C;          // floats of a level-0 map
+    const long long n1 = static_cast<long long>(a.H[1]) * a.W[1] * (a.C / 4);    // threads per batch element
+    const long long bpb = (n1 + 255) / 256;
+    if (n0 >= 0x7FFFFFFFLL || bpb * a.B >= 0x7FFFFFFFLL) return hipErrorInvalidValue;
     BwdUnpoolArgs u = a;
     u.div_cpt = make_fastdiv(a.C / 4);
-    u.div_W0 = make_fastdiv(a.W[0]);
+    u.div_W1 = make_fastdiv(a.W[1]);
     u.bpb = static_cast<int>(bpb);
     const dim3 grid(static_cast<unsigned>(bpb * a.B));
     if (a.L <= 4) hipLaunchKernelGGL(bwd_unpool_kernel<4>, grid, dim3(256), 0, stream, u);

@@ -239,7 +239,7 @@ struct BwdCoarseArgs {
 struct BwdUnpoolArgs {
     int B, C, L;
     int H[QTA_MAX_LEVELS], W[QTA_MAX_LEVELS];
-    FastDiv div_cpt, div_W0;    // divisions by C/4 and W[0]; set by the launcher
+    FastDiv div_cpt, div_W1;    // divisions by C/4 and W[1]; set by the launcher
     int bpb;                    // blocks per batch element; set by the launcher
     const float* gq[QTA_MAX_LEVELS];
     const float* gk[QTA_MAX_LEVELS];
