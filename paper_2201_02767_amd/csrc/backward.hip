@@ -795,8 +795,11 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     const int lane = threadIdx.x & 63;
     const int Np = a.Hp * a.Wp;
     const int n = a.B * a.heads * Np;
-    const int chunk = __builtin_amdgcn_readfirstlane(static_cast<int>(blockIdx.x));
-    if (chunk >= a.coff[n]) return;          // whole wave
+    // chunks of neighbouring keys (whose parents overlap) run on one XCD and share its L2: the
+    // workgroups that have a chunk (the grid is an upper bound) are remapped onto contiguous ranges
+    const int nchunks = a.coff[n];
+    if (static_cast<int>(blockIdx.x) >= nchunks) return;    // whole wave
+    const int chunk = __builtin_amdgcn_readfirstlane(xcd_remap(static_cast<int>(blockIdx.x), nchunks));
     extern __shared__ __align__(16) unsigned char smem[];
     const KeyLds lay = key_lds<T, D, FINEST>();
     constexpr bool kRows16 = kBf16 && FINEST;                // query and dm rows kept as bf16
