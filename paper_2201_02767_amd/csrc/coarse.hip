@@ -63,7 +63,7 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     const size_t tok0 = static_cast<size_t>(b) * N;           // first token of this batch element
     const size_t hoff = static_cast<size_t>(h) * D;
 
-    // V operands of phase 3's first key batch, requested now so that their latency overlaps the
+    // V operands of phase 3's first two key batches, requested now so that their latency overlaps the
     // logits and the selection (phase 3 layout: lane (kgrp, col) holds V[4*step + kgrp][16*ct + col])
     constexpr int NCT = D / 16;          // 16-wide column tiles of the messages
     constexpr int NKS = kWaves / NCT;    // key chunks
@@ -71,15 +71,16 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     const int p3_ct = wave % NCT, p3_ks = wave / NCT;
     const int p3_ch = p3_ct * 16 + (lane & 15);
     const int steps = (N + 3) / 4;
-    float vb[kVBatch];
-    auto load_v = [&](int st0) {
+    float vb[kVBatch], vb2[kVBatch];
+    auto load_v = [&](int st0, float (&dst)[kVBatch]) {
 #pragma unroll
         for (int u = 0; u < kVBatch; ++u) {
             const int cand = min((st0 + u * NKS) * 4 + (lane >> 4), N - 1);    // clamped; weight 0 beyond N
-            vb[u] = S::load1(a.v, (tok0 + cand) * C + hoff + p3_ch);
+            dst[u] = S::load1(a.v, (tok0 + cand) * C + hoff + p3_ch);
         }
     };
-    load_v(p3_ks);
+    load_v(p3_ks, vb);
+    load_v(p3_ks + NKS * kVBatch, vb2);      // and the second (together 512 keys at d = 32, 256 at d = 64)
 
     // ---- phase 1: logits on MFMA; a wave takes key tiles wave, wave+16, ... (at most 4) ----
     // The contraction over the d channels is taken in a permuted order so that each lane loads
@@ -206,13 +207,15 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     {
         const int arow = lane & 15, kgrp = lane >> 4;
         float4_t acc = {0.f, 0.f, 0.f, 0.f};
-        for (int st0 = p3_ks; st0 < steps; st0 += NKS * kVBatch) {
-            if (st0 != p3_ks) load_v(st0);                    // the first batch came in at the start
+        int it = 0;
+        for (int st0 = p3_ks; st0 < steps; st0 += NKS * kVBatch, ++it) {
+            if (it >= 2) load_v(st0, vb);                     // the first two batches came in at the start
 #pragma unroll
             for (int u = 0; u < kVBatch; ++u) {
                 const int st = st0 + u * NKS;
                 if (st >= steps) break;
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Sm[arow * pitch + st * 4 + kgrp], vb[u], acc, 0, 0, 0);
+                const float vu = it == 1 ? vb2[u] : vb[u];
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Sm[arow * pitch + st * 4 + kgrp], vu, acc, 0, 0, 0);
             }
         }
 #pragma unroll
