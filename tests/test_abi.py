@@ -301,3 +301,27 @@ def test_backward_validation():
     assert need_a > need_b > 0                                              # A adds the score gradients
     assert bwd(gwsb=need_a - 1) == WORKSPACE
     assert lib.qta_backward_workspace_bytes_ex(1, 1, 16, 16, 32, 3, 4, 7, F32, None) == 0
+
+
+def test_binding_structs_match_the_header(tmp_path):
+    """The ctypes mirrors of the header's structs have the C layout: size and every field's offset,
+    as a C compiler lays them out from include/qta.h."""
+    import subprocess
+
+    structs = {"qta_options": P.qta.Options, "qta_workspace_layout": P.qta.WorkspaceLayout}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "qta.h"', "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in cls._fields_:
+            lines.append(f'printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l.strip()}
+    for cname, cls in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(cls), cname
+        for fname, _ in cls._fields_:
+            assert got[(cname, fname)] == getattr(cls, fname).offset, f"{cname}.{fname}"
