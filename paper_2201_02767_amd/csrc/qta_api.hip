@@ -783,11 +783,12 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     if (levels > 1) {
         // 2. finer levels, finest first (QuadTree-A's score gradients go up one level each)
         for (int l = 0; l < (only_finest ? 1 : c); ++l) {
-            // with two streams the finest level's sort and key pass (the largest) go to the
-            // auxiliary stream right after its query pass. When the coarse level's tile kernels
-            // leave compute units idle (fewer 16-row tiles than units), the coarser levels' sorts
-            // and key passes follow them on the caller's stream, so that the coarse level runs
-            // beside the finest key pass; otherwise they too go to the auxiliary stream
+            // with an auxiliary stream the finest level's sort and key pass (the largest) go there
+            // right after its query pass. The coarser levels' sorts and key passes go to the third
+            // stream when there is one, each right after its level's query pass; with two streams
+            // only, when the coarse level's tile kernels leave compute units idle (fewer 16-row
+            // tiles than units) they follow those on the caller's stream, so that the coarse level
+            // runs beside the finest key pass, and otherwise they go to the auxiliary stream too
             BwdLevelArgs a{};
             if (l == 0) {
                 a.q = q;

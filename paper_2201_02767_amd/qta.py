@@ -381,8 +381,9 @@ class Plan:
         """Gradients (dq, dk, dv, dw) in fp32 of the last ``run`` on the same inputs, for the upstream
         gradient ``dout`` (the kept keys of that run held fixed). ``dw`` is None unless QuadTree-B
         with ``w``. The returned tensors are the plan's own buffers, overwritten by the next call.
-        ``overlap``: run each level's sort and key pass on a second stream (one per device for the
-        process), beside the next level's query pass (False: everything on the one stream)."""
+        ``overlap``: run the finest level's sort and key pass on a second stream and the coarser
+        levels' on a third (both one per device for the process), beside the query passes and the
+        coarse level (False: everything on the one stream)."""
         s = _stream(self.device) if stream is None else ctypes.c_void_p(stream)
         args, opt, grads = self._bwd_args(q, k, v, w, dout, s, overlap)
         _check("qta_backward_ex", lib().qta_backward_ex(*args))
