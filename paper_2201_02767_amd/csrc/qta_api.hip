@@ -762,6 +762,9 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     int ndeferred = 0;
     const long long coarse_tiles = static_cast<long long>(B) * heads * ((L.H[levels - 1] * L.W[levels - 1] + 15) / 16);
     const bool defer_coarser = s2 != s && s3 == s && coarse_tiles < device_cu_count();
+    // (measured: a gain where one intermediate level sits below a coarse level that fills the
+    // chip; with more intermediate levels, or a coarse level with idle units, a loss)
+    const bool qside = !va && s3 != s && levels == 3 && coarse_tiles >= device_cu_count();
     const bool use_bf16 = dtype == QTA_BF16;
     const float tau = resolve_scale(scale, d);
     const char* ws = static_cast<const char*>(workspace);
@@ -841,10 +844,15 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
             a.entries = reinterpret_cast<int32_t*>(gws + G.entries[l]);
             a.slot = reinterpret_cast<int32_t*>(gws + G.slot[l]);
             a.partial = fptr(G.partial[l]);
-            if (launch_bwd_level(a, d, va, use_bf16, l == 0, s) != hipSuccess) return QTA_ERR_HIP;
+            // QuadTree-B with three streams and one intermediate level (`qside`): that level's query
+            // pass needs only the finest query pass (every dm comes from it), so it runs on the
+            // third stream beside the coarse level
+            const hipStream_t sq = (l > 0 && qside) ? s3 : s;
+            if (launch_bwd_level(a, d, va, use_bf16, l == 0, sq) != hipSuccess) return QTA_ERR_HIP;
+            if (l == 0 && qside && !after(s, s3)) return QTA_ERR_HIP;
             // the stream of this level's sort and key pass, which need its query pass
             const hipStream_t sk = l == 0 ? s2 : (s3 != s ? s3 : (defer_coarser ? s : s2));
-            if (sk != s && !after(s, sk)) return QTA_ERR_HIP;
+            if (sk != sq && !after(sq, sk)) return QTA_ERR_HIP;
             BwdScanArgs sc{};
             sc.n = B * heads * L.H[l + 1] * L.W[l + 1];
             sc.nblocks = (sc.n + 1023) / 1024;
