@@ -140,10 +140,12 @@ def test_backward_repeated_calls(dev):
 
 
 @pytest.mark.parametrize("variant,dtype,name", [("B", "f32", "matching"), ("A", "bf16", "backbone"),
-                                                ("A", "bf16", "highres"), ("B", "bf16", "stereo_epipolar")])
+                                                ("B", "bf16", "backbone"), ("A", "bf16", "highres"),
+                                                ("B", "bf16", "stereo_epipolar")])
 def test_backward_overlap_matches_one_stream(dev, variant, dtype, name):
-    """The two-stream schedule (the finest level's sort and key pass on a second stream; the coarser
-    levels' either there too or after the coarse level, depending on its size) gives the one-stream
+    """The three-stream schedule (the finest level's sort and key pass on a second stream, the
+    coarser levels' on a third; with QuadTree-B, one intermediate level and a coarse level that fills
+    the chip, as for backbone, that level's query pass on the third stream too) gives the one-stream
     gradients, up to the order of the atomic sums."""
     wl = WORKLOADS[name].with_(variant=variant, dtype=dtype)
     announce(f"backward overlap vs one stream, {name} {variant} {dtype}")
