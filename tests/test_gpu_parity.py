@@ -443,6 +443,8 @@ def test_forward_position_encoding(dev, variant, dtype, B, H, W, heads, d, L, K,
     # 1200 coarse rows of 10 tokens, d = 64: several query rows per wave in the small-map coarse kernel
     ("A", "f32", 1, 600, 40, 2, 64, 3, 8, False, False),
     ("B", "bf16", 1, 600, 40, 2, 64, 3, 8, False, False),
+    # coarse rows of 5 tokens with K = 8: padded selections, several rows per wave
+    ("A", "bf16", 1, 600, 40, 2, 32, 4, 8, False, False),
 ])
 def test_forward_epipolar(dev, variant, dtype, B, H, W, heads, d, L, K, given_v, pe):
     q, k, v = rand_qkv(900 + H * W + L, B, H, W, heads, d, dtype)
