@@ -2,9 +2,11 @@
 
 A step is one whole forward (pyramids, coarse attention with top-K, every finer level, the fused
 combination) over one batch of synthetic input that is already resident in HBM. The default
-workload is the feature-matching layer (1 x 60x80 tokens, 8 heads x 32, fp32, 3 levels, K=8,
-QuadTree-B). Prints one JSON line with the throughput, the finest-level kernel's HBM roofline
-fraction (timed with HIP events on its own stream) and the CPU oracle timed on the host.
+workload is the largest one, dense-prediction high-resolution self-attention (2 x 200x336 tokens,
+2 heads x 32, bf16, 5 levels, K=16, QuadTree-B). Prints one JSON line with the throughput, the
+finest-level kernel's HBM roofline fraction (timed with HIP events on the stream it runs on, in
+algorithmic bytes and, from committed rocprofv3 counters, in measured bytes), the whole layer's
+fraction of its HBM roofline, the coarse level's MFMA figures, and the CPU oracle timed on the host.
 
 With --backward a step is one whole backward pass instead (the gradients of q, k, v and w for an
 upstream gradient, the kept keys of one preceding forward held fixed), and the roofline kernel is
@@ -29,11 +31,14 @@ METRIC = "query tokens/sec per QuadTree attention layer + % of HBM/MFMA roofline
 METRIC_BWD = ("query tokens/sec per QuadTree attention layer, backward pass (gradients of q, k, v, w) + % of HBM "
               "roofline, 1 GPU")
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}      # dense MFMA peaks of MI355X per input type
+COARSE_MFMA_TARGET = 0.40
 PROFILES = os.path.join(ROOT, "profiles")
 _CSRC = os.path.join(ROOT, "paper_2201_02767_amd", "csrc")
 # every source compiled into the roofline kernel: its counters are stale once one of them changes
 FINE_SRC = [os.path.join(_CSRC, f) for f in ("fine.hip", "fine_item.h", "qta_device.h", "qta_internal.h")]
 BWD_SRC = [os.path.join(_CSRC, f) for f in ("backward.hip", "qta_device.h", "qta_internal.h")]
+COARSE_SRC = [os.path.join(_CSRC, f) for f in ("coarse.hip", "qta_device.h", "qta_internal.h")]
 
 
 def log(msg: str) -> None:
@@ -135,20 +140,100 @@ def measured_traffic(workload: str, kernel: str = "fine_attn_finest", src=FINE_S
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, seconds: float, backward: bool = False) -> dict:
+def measured_mfma(workload: str):
+    """The coarse kernel's MFMA counters from the committed rocprofv3 summary
+    (profiles/coarse_mfma_<workload>.json), if taken on the current coarse source; None otherwise."""
+    path = os.path.join(PROFILES, f"coarse_mfma_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash(COARSE_SRC):
+        return None
+    return rec
+
+
+def _level_geometry(wl):
+    """Token counts per level of the maps the library works on (B*H one-row maps for epipolar
+    attention), the number of such (map, head) units, storage bytes, children per kept key, K per level."""
+    import paper_2201_02767_amd as P
+
+    mB, mH = (wl.B * wl.H, 1) if wl.epipolar else (wl.B, wl.H)
+    N = [h * w for h, w in P.level_dims(mH, wl.W, wl.levels)]
+    b = 2 if wl.dtype == "bf16" else 4
+    return N, mB * wl.heads, b, (2 if mH == 1 else 4), P.k_levels(wl.K, wl.levels)
+
+
+def layer_bytes(wl) -> dict:
+    """Algorithmic HBM bytes of one whole layer (every tensor streamed once, plus one gather of each
+    sibling group's candidate key and value rows), per (batch, head) with b storage bytes, sigma = 4 B
+    (B) or 8 B (A: index and score) per kept entry, c children per kept key, c = L-1 the coarsest level:
+      pyramid  read q, k, v at level 0 and write every coarser level: (2 or 3)*(N0 + sum_{l>=1} N_l)*d*b
+               (V's levels are the caller's when given);
+      coarse   3*Nc*d*b + 4*Nc*d (message) + Nc*Kc*sigma (selections);
+      level l  N_l*d*b (queries) + N_{l+1}*K_{l+1}*sigma (parents' selections)
+               + N_{l+1}*c*K_{l+1}*2*d*b (gathered key and value rows)
+               + [l >= 1] N_l*(4*d + K_l*sigma) (message, selections)
+               + [l = 0] N0*d*b (output) + N1*(L-1)*4*d (ancestors' messages) + [B] 4*N0*L (w);
+      position encoding (when used) sum_l N_l*d*b (V read once more at every level)."""
+    N, units, b, ch, Kl = _level_geometry(wl)
+    d, L = wl.d, wl.levels
+    sigma = 4 if wl.variant == "B" else 8
+    ntens = 2 if wl.v_given else 3
+    parts = {"pyramid": ntens * sum(N) * d * b if L > 1 else 0}
+    c = L - 1
+    if L == 1:
+        parts["coarse"] = 4 * N[0] * d * b
+    else:
+        parts["coarse"] = 3 * N[c] * d * b + 4 * N[c] * d + N[c] * Kl[c] * sigma
+    for l in range(L - 2, -1, -1):
+        x = N[l] * d * b + N[l + 1] * Kl[l + 1] * sigma + N[l + 1] * ch * Kl[l + 1] * 2 * d * b
+        if l >= 1:
+            x += N[l] * (4 * d + Kl[l] * sigma)
+        else:
+            x += N[0] * d * b + N[1] * (L - 1) * 4 * d + (4 * N[0] * L if wl.variant == "B" else 0)
+        parts[f"level{l}"] = x
+    if wl.pe:
+        parts["position_encoding"] = sum(N) * d * b
+    return {k: v * units for k, v in parts.items()}
+
+
+def coarse_flops(wl) -> int:
+    """QK^T and PV of the coarsest level at 2 flops per multiply-add: 4*d*Nc^2 per (batch, head)."""
+    N, units, _, _, _ = _level_geometry(wl)
+    return 4 * wl.d * N[-1] ** 2 * units
+
+
+def host_cpu() -> dict:
+    """Core count and model of the host the oracle runs on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = None
+    return {"host_cores": os.cpu_count(), "host_cores_usable": usable, "host_cpu": model}
+
+
+def cpu_baseline(wl, arrays, seconds: float, backward: bool = False) -> dict:
     """The oracle as it stands, single-threaded on the host, on whole layers of the workload (its
-    backward, which also runs the forward it differentiates, with --backward)."""
-    from paper_2201_02767_amd.inputs import make_dout, make_level_weights, make_pe, make_qkv, make_v_levels
+    backward, which also runs the forward it differentiates, with --backward). ``arrays``: the
+    numpy inputs the GPU run used."""
     from oracle import oracle
 
-    q, k, v = make_qkv(wl)
-    w = make_level_weights(wl) if wl.variant == "B" else None
-    vl = make_v_levels(wl) if wl.v_given else None
-    pw, pb = make_pe(wl) if wl.pe else (None, None)
+    q, k, v, w, vl, pw, pb, g = arrays
     if wl.epipolar:     # every row its own 1 x W map
         q, k, v = (x.reshape(wl.B * wl.H, 1, wl.W, wl.heads, wl.d) for x in (q, k, v))
         w = None if w is None else w.reshape(wl.B * wl.H, wl.W, wl.heads, wl.levels)
-    g = make_dout(wl).reshape(q.shape) if backward else None
+    if backward:
+        g = g.reshape(q.shape)
     runs, t0 = 0, time.perf_counter()
     while True:
         if backward:
@@ -160,9 +245,27 @@ def cpu_baseline(wl, seconds: float, backward: bool = False) -> dict:
         el = time.perf_counter() - t0
         if el >= seconds:
             break
-    return {"value": wl.tokens * runs / el, "unit": "query tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{runs} whole {wl.name} layer {'backward pass(es)' if backward else 'forward(s)'} "
-                      f"({wl.B}x{wl.H}x{wl.W}, {wl.heads}x{wl.d}, L={wl.levels}, K={wl.K}) in {el:.1f} s, one thread"}
+    rec = {"value": wl.tokens * runs / el, "unit": "query tokens/s", "cores": 1, "kind": "oracle",
+           "sample": f"{runs} whole {wl.name} layer {'backward pass(es)' if backward else 'forward(s)'} "
+                     f"({wl.B}x{wl.H}x{wl.W}, {wl.heads}x{wl.d}, L={wl.levels}, K={wl.K}) in {el:.1f} s, "
+                     "one thread (the oracle is single-threaded C, fp64)"}
+    rec.update(host_cpu())
+    return rec
+
+
+def _time_launches(fn, n, stream, e0, e1) -> float:
+    """Average microseconds per call of ``fn`` over ``n`` calls, HIP events on ``stream``."""
+    import torch
+
+    for _ in range(10):
+        fn()
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(n):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / n
 
 
 def main() -> int:
@@ -170,7 +273,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="matching")
+    ap.add_argument("--workload", default="highres")
     ap.add_argument("--kernel-launches", type=int, default=500, help="launches timed for the roofline kernel")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -206,25 +309,32 @@ def main() -> int:
         print(f"unknown workload {args.workload}; choose from {sorted(WORKLOADS)}", file=sys.stderr)
         return 2
     wl = WORKLOADS[args.workload]
+    if args.backward and (wl.v_given or wl.pe):
+        print("the backward pass covers pooled V levels without a position encoding", file=sys.stderr)
+        return 2
+    log(f"bench: generating the {wl.name} inputs")
+    qn, kn, vn = make_qkv(wl)
+    wn = make_level_weights(wl) if wl.variant == "B" else None
+    vln = make_v_levels(wl) if wl.v_given else None
+    pwn, pbn = make_pe(wl) if wl.pe else (None, None)
+    gn = make_dout(wl) if args.backward else None
+
     dev = torch.device("cuda:0")
     tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
-    q, k, v = (torch.from_numpy(x).to(dev).to(tdt).contiguous() for x in make_qkv(wl))
-    w = torch.from_numpy(make_level_weights(wl)).to(dev) if wl.variant == "B" else None
+    q, k, v = (torch.from_numpy(x).to(dev).to(tdt).contiguous() for x in (qn, kn, vn))
+    w = torch.from_numpy(wn).to(dev) if wn is not None else None
     vl = None
     if wl.v_given:
-        vl = [None] + [torch.from_numpy(x).to(dev).to(tdt).contiguous() for x in make_v_levels(wl)[1:]]
+        vl = [None] + [torch.from_numpy(x).to(dev).to(tdt).contiguous() for x in vln[1:]]
     pw = pb = None
     if wl.pe:
-        pw, pb = (torch.from_numpy(x).to(dev) for x in make_pe(wl))
+        pw, pb = torch.from_numpy(pwn).to(dev), torch.from_numpy(pbn).to(dev)
     plan = P.Plan(wl.B, wl.H, wl.W, wl.heads, wl.d, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=tdt,
                   device=dev, v_supplied=wl.v_given, pe=wl.pe, epipolar=wl.epipolar)
     step = plan.prepare(q, k, v, w, v_levels=vl, pe_weight=pw, pe_bias=pb)
     log(f"bench: {wl} on {torch.cuda.get_device_name(0)}")
     if args.backward:
-        if wl.v_given or wl.pe:
-            print("the backward pass covers pooled V levels without a position encoding", file=sys.stderr)
-            return 2
-        g = torch.from_numpy(make_dout(wl)).to(dev).to(tdt).contiguous()
+        g = torch.from_numpy(gn).to(dev).to(tdt).contiguous()
         step()                                   # the forward whose kept keys the backward holds fixed
         step = plan.prepare_backward(q, k, v, g, w)
         log("bench: timing the backward pass")
@@ -250,16 +360,8 @@ def main() -> int:
     # the dominant kernel alone, on the same stream, on the selections the forward left behind
     roof = None
     if wl.levels >= 2 and args.backward:
-        finest = plan.prepare_backward(q, k, v, g, w, finest_only=True)
-        for _ in range(10):
-            finest()
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(args.kernel_launches):
-            finest()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        k_us = e0.elapsed_time(e1) * 1e3 / args.kernel_launches
+        k_us = _time_launches(plan.prepare_backward(q, k, v, g, w, finest_only=True), args.kernel_launches,
+                              stream, e0, e1)
         parts = finest_backward_kernel_bytes(wl)
         algo = sum(parts.values())
         achieved = algo / (k_us * 1e-6) / 1e9
@@ -272,16 +374,7 @@ def main() -> int:
         log(f"bench: finest-level backward step {k_us:.2f} us/launch, {algo / 1e6:.1f} MB algorithmic -> "
             f"{achieved:.0f} GB/s ({100 * achieved / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f})")
     elif wl.levels >= 2:
-        finest = plan.prepare_finest(q, k, v, w)
-        for _ in range(10):
-            finest()
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(args.kernel_launches):
-            finest()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        k_us = e0.elapsed_time(e1) * 1e3 / args.kernel_launches
+        k_us = _time_launches(plan.prepare_finest(q, k, v, w), args.kernel_launches, stream, e0, e1)
         parts = finest_kernel_bytes(wl)
         algo = sum(parts.values())
         achieved = algo / (k_us * 1e-6) / 1e9
@@ -290,16 +383,51 @@ def main() -> int:
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": "fine_attn_kernel (finest level, fused combine)", "kernel_us": round(k_us, 3),
                 "algorithmic_bytes": algo}
+        if traffic:
+            # the same launch time against the bytes the counters saw cross the L2 (HBM or MALL)
+            roof["traffic_frac"] = round(traffic / (k_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
         log(f"bench: finest-level kernel {k_us:.2f} us/launch, {algo / 1e6:.1f} MB algorithmic -> "
-            f"{achieved:.0f} GB/s ({100 * achieved / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f})")
+            f"{achieved:.0f} GB/s ({100 * achieved / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f})"
+            + (f"; counters {traffic / 1e6:.1f} MB -> {100 * roof['traffic_frac']:.1f}%" if traffic else ""))
+
+        # the whole layer against its own HBM roofline (every tensor once, one gather per sibling group)
+        lparts = layer_bytes(wl)
+        lbytes = sum(lparts.values())
+        lach = lbytes / (ms_per_step * 1e-3) / 1e9
+        roof["layer"] = {"bound": "hbm", "algorithmic_bytes": lbytes, "us": round(ms_per_step * 1e3, 3),
+                         "achieved": round(lach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(lach / HBM_PEAK_GBS, 4),
+                         "roofline_us": round(lbytes / (HBM_PEAK_GBS * 1e9) * 1e6, 2)}
+        log(f"bench: whole layer {lbytes / 1e6:.1f} MB algorithmic in {ms_per_step * 1e3:.2f} us -> {lach:.0f} GB/s "
+            f"({100 * lach / HBM_PEAK_GBS:.1f}% of {HBM_PEAK_GBS:.0f})")
+
+        # the coarsest level on MFMA: device-wide flop rate, and the MFMA-busy share of the CUs it occupies
+        if not wl.v_given:
+            c_us = _time_launches(plan.prepare_coarse(), args.kernel_launches, stream, e0, e1)
+            fl = coarse_flops(wl)
+            tf = fl / (c_us * 1e-6) / 1e12
+            peak = MFMA_PEAK_TFLOPS[wl.dtype]
+            coarse = {"kernel": "coarse_attn_kernel (coarsest level with top-K)", "kernel_us": round(c_us, 3),
+                      "flops": fl, "achieved": round(tf, 3), "peak": peak, "unit": "TFLOP/s",
+                      "frac_device": round(tf / peak, 6), "target": COARSE_MFMA_TARGET,
+                      "compared_with_target": "mfma_busy_frac_occupied"}
+            mf = measured_mfma(wl.name)
+            coarse["mfma_busy_frac_occupied"] = mf.get("mfma_busy_frac_occupied") if mf else None
+            coarse["mfma_busy_frac_device"] = mf.get("mfma_busy_frac_device") if mf else None
+            roof["coarse"] = coarse
+            log(f"bench: coarse level {c_us:.2f} us/launch, {fl / 1e6:.1f} MFLOP -> {tf:.2f} TFLOP/s "
+                f"({100 * tf / peak:.3f}% of {peak:.0f}); MFMA busy on occupied CUs "
+                f"{coarse['mfma_busy_frac_occupied']}")
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, args.cpu_seconds, args.backward)
-        log(f"bench: oracle {cpu['value']:.4g} query tokens/s ({cpu['sample']})")
+        cpu = cpu_baseline(wl, (qn, kn, vn, wn, vln, pwn, pbn, gn), args.cpu_seconds, args.backward)
+        log(f"bench: oracle {cpu['value']:.4g} query tokens/s ({cpu['sample']}; host {cpu['host_cores']} cores, "
+            f"{cpu['host_cpu']})")
 
     rec = {
-        "metric": METRIC_BWD if args.backward else METRIC, "value": round(value, 1), "unit": "query tokens/s", "n_gpus": 1, "steps": args.steps,
+        "metric": METRIC_BWD if args.backward else METRIC, "value": round(value, 1), "unit": "query tokens/s",
+        "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32" if wl.dtype == "f32" else "bf16", "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "W": wl.W, "heads": wl.heads, "d": wl.d,

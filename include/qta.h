@@ -40,8 +40,10 @@
  *     1 <= L <= QTA_MAX_LEVELS with no level above a 1x1 map; token pointers 16-byte aligned;
  *     per batch element fewer than 2^24 tokens and 2^31 bytes in the token map (attention calls).
  *   - K larger than a query's candidate count is not an error: min(K, count) keys are kept.
- *   - Inputs must be finite; outputs must not alias inputs. Calls are re-entrant: the library
- *     holds no state.
+ *   - Inputs must be finite; outputs must not alias inputs. Calls are re-entrant and may come from
+ *     several host threads: the library keeps no data between calls. Its only process-wide state
+ *     is per-device caches (device attributes, and each kernel's raised LDS limit, set once per
+ *     device), filled with atomic operations on first use.
  */
 #ifndef QTA_H
 #define QTA_H

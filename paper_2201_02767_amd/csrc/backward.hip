@@ -467,14 +467,10 @@ hipError_t launch_level_one(const BwdLevelArgs& a, hipStream_t stream)
     int wpb = 4;
     while (wpb > 1 && wpb * wave_bytes > 64 * 1024) --wpb;
     if (wpb * wave_bytes > device_max_lds()) return hipErrorInvalidValue;
-    static bool configured = false;
-    if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_level_kernel<T, D, NSP, VA, FINEST>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           static_cast<int>(device_max_lds()));
-        if (e != hipSuccess) return e;
-        configured = true;
-    }
+    static std::atomic<unsigned long long> configured{0};     // devices whose LDS limit is raised
+    if (hipError_t e = set_max_lds_once(reinterpret_cast<const void*>(&bwd_level_kernel<T, D, NSP, VA, FINEST>), configured);
+        e != hipSuccess)
+        return e;
     const long long items = static_cast<long long>(a.B) * a.heads * a.Hp * a.Wp;
     const long long blocks = (items + wpb - 1) / wpb;
     if (blocks * wpb >= 0x7FFFFFFFLL) return hipErrorInvalidValue;

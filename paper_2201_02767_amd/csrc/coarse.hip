@@ -433,13 +433,16 @@ hipError_t launch_small(const CoarseArgs& a, hipStream_t stream)
 {
     // enough query rows per wave that the waves fit the chip's wave slots (at the kernel's
     // occupancy) about once
-    static int blocks_per_cu = 0;
+    // (the occupancy depends on the kernel and the architecture only; racing threads store the same value)
+    static std::atomic<int> occupancy{0};
+    int blocks_per_cu = occupancy.load(std::memory_order_relaxed);
     if (blocks_per_cu == 0) {
         int n = 0;
         hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
             &n, reinterpret_cast<const void*>(&coarse_small_kernel<T, D, VA>), 4 * kWave, 0);
         if (e != hipSuccess) return e;
         blocks_per_cu = n > 0 ? n : 1;
+        occupancy.store(blocks_per_cu, std::memory_order_relaxed);
     }
     const long long maps = static_cast<long long>(a.B) * a.heads;
     const long long slots = static_cast<long long>(device_cu_count()) * blocks_per_cu * 4;
@@ -460,14 +463,10 @@ hipError_t launch_one(const CoarseArgs& a, hipStream_t stream)
 {
     const size_t lds = (static_cast<size_t>(kRows) * coarse_pitch(a.N) + kWaves * 16 * 16) * sizeof(float);
     if (lds > device_max_lds()) return hipErrorInvalidValue;
-    static bool configured = false;
-    if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&coarse_attn_kernel<T, D, VA, kPerLane>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           static_cast<int>(device_max_lds()));
-        if (e != hipSuccess) return e;
-        configured = true;
-    }
+    static std::atomic<unsigned long long> configured{0};     // devices whose LDS limit is raised
+    if (hipError_t e = set_max_lds_once(reinterpret_cast<const void*>(&coarse_attn_kernel<T, D, VA, kPerLane>), configured);
+        e != hipSuccess)
+        return e;
     const int tiles = (a.N + kRows - 1) / kRows;
     const long long blocks = static_cast<long long>(a.B) * a.heads * tiles;
     if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;

@@ -262,14 +262,10 @@ hipError_t launch_tile(const BwdCoarseArgs& a, hipStream_t stream)
 {
     const size_t lds = (2 * static_cast<size_t>(kRows) * bwd_coarse_pitch(a.N) + kWaves * 16 * 16) * sizeof(float);
     if (lds > device_max_lds()) return hipErrorInvalidValue;
-    static bool configured = false;
-    if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_coarse_tile_kernel<T, D, VA, kPerLane, KEYS>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           static_cast<int>(device_max_lds()));
-        if (e != hipSuccess) return e;
-        configured = true;
-    }
+    static std::atomic<unsigned long long> configured{0};     // devices whose LDS limit is raised
+    if (hipError_t e = set_max_lds_once(reinterpret_cast<const void*>(&bwd_coarse_tile_kernel<T, D, VA, kPerLane, KEYS>), configured);
+        e != hipSuccess)
+        return e;
     const int tiles = (a.N + kRows - 1) / kRows;
     const long long blocks = static_cast<long long>(a.B) * a.heads * tiles;
     if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;

@@ -35,14 +35,10 @@ hipError_t launch_one(const FineArgs& a, hipStream_t stream)
     const size_t wave_bytes = wave_lds<T, D>(nsp).total;
     const int wpb = 4;
     if (wpb * wave_bytes > device_max_lds()) return hipErrorInvalidValue;
-    static bool configured = false;
-    if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, NSP, VA, FINEST, ROW>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           static_cast<int>(device_max_lds()));
-        if (e != hipSuccess) return e;
-        configured = true;
-    }
+    static std::atomic<unsigned long long> configured{0};     // devices whose LDS limit is raised
+    if (hipError_t e = set_max_lds_once(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, NSP, VA, FINEST, ROW>), configured);
+        e != hipSuccess)
+        return e;
     const long long np = static_cast<long long>(a.Hp) * a.Wp;
     const long long items = static_cast<long long>(a.B) * a.heads * (ROW ? (np + 1) / 2 : np);
     const long long blocks = (items + wpb - 1) / wpb;

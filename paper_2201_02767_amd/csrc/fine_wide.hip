@@ -381,13 +381,11 @@ hipError_t launch_one(const FineArgs& a, hipStream_t stream)
     int wpb = 4;
     while (wpb > 1 && wpb * wave_bytes > kLdsMax) --wpb;
     if (wave_bytes > kLdsMax) return hipErrorInvalidValue;
-    static bool configured = false;
-    if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, VA, FINEST, NT>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kLdsMax));
-        if (e != hipSuccess) return e;
-        configured = true;
-    }
+    static std::atomic<unsigned long long> configured{0};     // devices whose LDS limit is raised
+    if (hipError_t e = set_max_lds_once(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, VA, FINEST, NT>),
+                                        configured);
+        e != hipSuccess)
+        return e;
     const long long items = static_cast<long long>(a.B) * a.heads * a.Hp * a.Wp;
     const long long blocks = (items + wpb - 1) / wpb;
     if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;

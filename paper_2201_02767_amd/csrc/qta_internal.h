@@ -2,6 +2,8 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include <atomic>
 #include <stdint.h>
 
 #include "../../include/qta.h"
@@ -262,33 +264,47 @@ struct TopkArgs {
     float* key_out;
 };
 
-// Largest dynamic LDS a workgroup may use on the current device (cached per device).
-inline size_t device_max_lds()
+// Per-device caches: entry `dev` of a table of 64 atomics, filled on first use (several host threads
+// may race to fill an entry; they all store the same value).
+inline int cached_device_attribute(std::atomic<int> (&cache)[64], hipDeviceAttribute_t attr, int fallback)
 {
-    static int cached[64] = {};
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 64 * 1024;
-    if (cached[dev] == 0) {
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
-            v = 64 * 1024;
-        cached[dev] = v;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return fallback;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        if (hipDeviceGetAttribute(&v, attr, dev) != hipSuccess || v <= 0) v = fallback;
+        cache[dev].store(v, std::memory_order_relaxed);
     }
-    return static_cast<size_t>(cached[dev]);
+    return v;
 }
 
-// Compute units of the current device (cached per device).
+// Largest dynamic LDS a workgroup may use on the current device.
+inline size_t device_max_lds()
+{
+    static std::atomic<int> cache[64];
+    return static_cast<size_t>(cached_device_attribute(cache, hipDeviceAttributeMaxSharedMemoryPerBlock, 64 * 1024));
+}
+
+// Compute units of the current device.
 inline int device_cu_count()
 {
-    static int cached[64] = {};
+    static std::atomic<int> cache[64];
+    return cached_device_attribute(cache, hipDeviceAttributeMultiprocessorCount, 256);
+}
+
+// Raises kernel `fn`'s dynamic-LDS limit to the current device's maximum, once per device: `done` is
+// that kernel's set of devices already configured (bit `dev`). Racing threads may both set the
+// attribute, which is harmless.
+inline hipError_t set_max_lds_once(const void* fn, std::atomic<unsigned long long>& done)
+{
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cached[dev] == 0) {
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
-        cached[dev] = v;
-    }
-    return cached[dev];
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const unsigned long long bit = (dev >= 0 && dev < 64) ? 1ull << dev : 0ull;
+    if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(device_max_lds()));
+    if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_release);
+    return e;
 }
 
 hipError_t launch_pyramid_pass(const PyramidPassArgs& a, int nlev, int ntensors, bool use_bf16, hipStream_t stream);

@@ -332,6 +332,34 @@ class Plan:
             return keep
         return call
 
+    def prepare_coarse(self):
+        """A zero-argument callable that re-runs only the coarsest level (attention with its top-K,
+        through ``qta_coarse_attn``) on the coarsest pyramid level this plan's last run left in its
+        workspace, writing the same message and selections again."""
+        if self.levels < 2:
+            raise ValueError("a single-level problem has no separate coarse stage")
+        c = self.levels - 1
+        lay = self.layout
+        shape = (self.mB, lay.H[c], lay.W[c], self.heads, self.d)
+        qc, kc = self._view(lay.q[c], shape, self.dtype), self._view(lay.k[c], shape, self.dtype)
+        if self.v_supplied:
+            raise ValueError("the coarse stage alone is timed with pooled V levels")
+        vc = self._view(lay.v[c], shape, self.dtype)
+        sidx, skey = self.selection(c)
+        msg = self.message(c)
+        fn = lib().qta_coarse_attn
+        args = (_ptr(qc), _ptr(kc), _ptr(vc), self.mB, self.heads, lay.H[c], lay.W[c], self.d, self.K_levels[c],
+                _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), _ptr(msg), _ptr(sidx), _ptr(skey),
+                _stream(self.device))
+        keep = (qc, kc, vc, sidx, skey, msg)
+
+        def call():
+            st = fn(*args)
+            if st != 0:
+                _check("qta_coarse_attn", st)
+            return keep
+        return call
+
     # ---- backward ----
     def _bwd_buffers(self, want_dw):
         if getattr(self, "_grads", None) is None:

@@ -190,3 +190,25 @@ def hierarchical_weights(q, k, L: int, tau: float) -> np.ndarray:
                         wgt *= t[ay - sy, ax - sx]
                     Wt[b, h, i, j] = wgt
     return Wt
+
+
+def nearest_bf16(x: float) -> float:
+    """The bfloat16 value nearest to the finite float ``x``, ties to the even significand, written
+    from the format's definition (8 significand bits, exponents -126..127, subnormals spaced 2^-133,
+    IEEE overflow to infinity) with exact rational arithmetic: no bit manipulation."""
+    from fractions import Fraction
+    import math
+
+    if x == 0.0:
+        return x                                    # keeps the sign of zero
+    sign = -1.0 if x < 0 else 1.0
+    a = Fraction(abs(x))
+    e = math.frexp(abs(x))[1] - 1                   # 2^e <= |x| < 2^(e+1)
+    ulp = Fraction(2) ** (max(e, -126) - 7)         # spacing of bf16 values around |x|
+    lo = (a / ulp).__floor__()                      # |x| lies in [lo*ulp, (lo+1)*ulp]
+    below, above = a - lo * ulp, (lo + 1) * ulp - a
+    n = lo if below < above or (below == above and lo % 2 == 0) else lo + 1
+    r = n * ulp
+    if r >= Fraction(2) ** 128:                     # beyond the largest finite value (2 - 2^-7) * 2^127
+        return sign * math.inf
+    return sign * float(r)

@@ -129,6 +129,29 @@ def test_pyramid_bit_exact(dev, dtype, B, H, W, C, L):
         assert np.array_equal(to_np(levels[l]), ref), f"level {l}"
 
 
+@pytest.mark.parametrize("W", [2, 9, 130])
+def test_pyramid_bf16_rounding_ties(dev, W):
+    """Pooled bf16 tokens whose fp32 mean lands exactly halfway between two bf16 values: on a one-row
+    map each token averages a pair, here a bf16 value and the next one up (or the same value). The
+    kernels' nearest-even rounding must equal the oracle's, whose rounding is pinned to the format's
+    definition on the CPU; both tie directions occur (even kept significands round down, odd up)."""
+    rng = np.random.default_rng(77 + W)
+    C = 64
+    a = round_bf16((rng.standard_normal((1, 1, W, C)) * np.exp2(rng.integers(-60, 60, size=(1, 1, W, C))))
+                   .astype(np.float32))
+    x = a.copy()
+    up = rng.random((1, 1, W // 2, C)) < 0.8
+    x[:, :, 1::2] = (a[:, :, 0:W - 1:2].view(np.uint32) + np.where(up, 0x10000, 0).astype(np.uint32)).view(np.float32)
+    announce(f"pyramid bf16 rounding ties 1x1x{W}x{C}")
+    levels = P.build_pyramid(dev_t(x, "bf16", dev), 2)
+    torch.cuda.synchronize()
+    ref = O.pool_level(x, "bf16")
+    assert np.array_equal(to_np(levels[1]).view(np.uint32), ref.view(np.uint32))
+    m = ((x[:, :, 0:W - 1:2] + x[:, :, 1::2]) * np.float32(0.5)).astype(np.float32).view(np.uint32)
+    ties = (m & 0xFFFF) == 0x8000
+    assert ties.mean() > 0.5 and (ties & ((m >> 16) & 1 == 1)).any() and (ties & ((m >> 16) & 1 == 0)).any()
+
+
 # ------------------------------------------------------------------------------------------------
 # stage: top-K
 # ------------------------------------------------------------------------------------------------

@@ -95,6 +95,62 @@ def test_bf16_pyramid_rounds_each_level():
     assert np.array_equal(l2, round_bf16(brute.ceil_pool(l1).astype(np.float32)))
 
 
+def bf16_edge_values() -> np.ndarray:
+    """fp32 values at every kind of bf16 rounding decision: exact ties with an even and with an odd
+    kept significand, one unit of the dropped bits either side of a tie, both signs and zeros,
+    subnormals, the largest finite values (whose ties overflow to infinity) and random values over
+    the whole exponent range."""
+    rng = np.random.default_rng(11)
+    hi = np.concatenate([rng.integers(0, 0x7F80, size=400), [0, 1, 2, 0x007F, 0x0080, 0x3F80, 0x3F81,
+                                                             0x7F7E, 0x7F7F]]).astype(np.uint32)
+    lows = np.array([0x0000, 0x0001, 0x7FFF, 0x8000, 0x8001, 0xFFFF], np.uint32)
+    u = (hi[:, None] << 16 | lows[None, :]).ravel()
+    u = np.concatenate([u, u | 0x80000000, rng.integers(0, 0x7F800000, size=2000).astype(np.uint32)])
+    return u.view(np.float32)
+
+
+def test_bf16_rounding_matches_its_definition():
+    """The oracle's bf16 storage rounding (the last step of every pooled bf16 token, Sec. 3.2 with
+    the rounding reading of the pyramid) and the input generator's rounding both equal the nearest
+    bfloat16 value with ties to even, computed from the format's definition in exact rational
+    arithmetic and, independently, by torch's float32 -> bfloat16 conversion. Compared bit for bit,
+    so the sign of zero, a wrong tie bit or a wrong shift fails."""
+    import torch
+
+    x = bf16_edge_values()
+    ref = np.array([brute.nearest_bf16(float(t)) for t in x], np.float32)
+    by_torch = torch.from_numpy(x.copy()).to(torch.bfloat16).float().numpy()
+    # a 1 x 1 map pools to its single token (sum of one child times 1/1), so the oracle's pooling
+    # returns exactly its rounding of each value
+    pooled = O.pool_level(x.reshape(1, 1, 1, -1), "bf16").ravel()
+    gen = round_bf16(x)
+    for name, got in (("torch", by_torch), ("oracle", pooled), ("inputs.round_bf16", gen)):
+        bad = np.flatnonzero(got.view(np.uint32) != ref.view(np.uint32))
+        assert bad.size == 0, (name, [(hex(int(x.view(np.uint32)[i])), got[i], ref[i]) for i in bad[:5]])
+    # the ties really are there: halfway cases rounded both down (even) and up (odd)
+    ties = (x.view(np.uint32) & 0xFFFF) == 0x8000
+    up = ties & ((x.view(np.uint32) >> 16 & 1) == 1)
+    assert ties.sum() > 400 and up.sum() > 100
+
+
+def test_bf16_pooling_rounds_the_fp32_mean():
+    """A pooled bf16 token is the fp32 mean of its stored children rounded once to nearest-even:
+    children chosen so that the fp32 mean lands exactly on a tie, just off it, or needs no rounding."""
+    base = np.array([1.0, 1.0078125, -2.0, 3.0], np.float32)           # bf16 values 2^-7 apart near 1
+    half = np.float32(2.0 ** -8)                                        # half a bf16 unit at 1
+    # children (a, b) whose mean is a + half*{1, 0.5, 1.5}: a tie, below it, above it
+    cases = []
+    for a in base:
+        for frac in (1.0, 0.5, 1.5):
+            b = np.float32(a + np.float32(2 * frac) * half * np.float32(abs(a) if abs(a) >= 2 else 1))
+            cases.append((a, b))
+    x = np.array([[c[0], c[1]] for c in cases], np.float32).T.reshape(1, 1, 2, -1)
+    pooled = O.pool_level(x, "bf16").ravel()
+    means = ((x[0, 0, 0].astype(np.float32) + x[0, 0, 1]) * np.float32(0.5)).astype(np.float32)
+    ref = np.array([brute.nearest_bf16(float(m)) for m in means], np.float32)
+    assert np.array_equal(pooled.view(np.uint32), ref.view(np.uint32))
+
+
 # ---------------------------------------------------------------- attention --------------------
 
 @pytest.mark.parametrize("variant", ["A", "B"])
