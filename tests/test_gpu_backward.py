@@ -1,16 +1,21 @@
 """GPU parity of the backward pass (gradients of q, k, v and w with the kept keys held fixed)
 against the CPU oracle's backward, teacher-forced with the GPU forward's selections.
 
-Error measure: the forward's per-row measure (tests/parity.py ``rel_err``): for every row (batch,
-token, head) of a gradient tensor, max |gpu - oracle| over the row divided by max(max |oracle| over
-the row, 1e-3 * RMS of the whole tensor). Rows of dq, dk, dv hold the d channels of one token and
-head; rows of dw the L levels. Every gradient is computed in fp32 from inputs that are exact in the
-storage type (bf16 inputs are bf16 values), with sums of at most a few thousand terms (the coarse
-level's 1024 keys), so 1e-4 leaves an order of magnitude over fp32 accumulation; the same bound holds
-for bf16 inputs because nothing is rounded to bf16 on the way. The one exception is dw at levels
->= 1: dw_{i,l} = <dout_i, m^l> uses the forward's stored messages, which for bf16 inputs carry the
-forward's bf16 rounding of the attention weights, so dw is held to the forward's message tolerance.
-The tensor-wide measure max |gpu - oracle| / max |oracle| is printed beside it.
+Error measure for dq, dk, dv: the forward's per-row measure (tests/parity.py ``rel_err``): for
+every row (batch, token, head), max |gpu - oracle| over the d channels divided by max(max |oracle|
+over the row, 1e-3 * RMS of the whole tensor). Every such gradient is computed in fp32 from inputs
+that are exact in the storage type (bf16 inputs are bf16 values), with sums of at most a few thousand
+terms (the coarse level's 1024 keys), so 1e-4 leaves an order of magnitude over fp32 accumulation;
+the same bound holds for bf16 inputs because nothing is rounded to bf16 on the way.
+
+dw is the exception: dw_{i,l} = <dout_i, m^l> is a dot product with the forward's stored message of
+the query's level-l ancestor, and for bf16 inputs that message carries the forward's bf16 rounding of
+the attention weights (the forward's messages are held to 2e-2 of max |m| per row). The dot product
+can cancel to nearly zero, so a bound relative to |dw| itself does not follow from the message bar;
+what follows is |dw_gpu - dw_ref| <= tol * sum_c |dout_ic| * max_c |m^l_c| (the message error summed
+against dout). dw is checked element by element against that bound, tol being the forward's message
+tolerance (1e-4 fp32, 2e-2 bf16), with the oracle's messages in the bound.
+The tensor-wide measure max |gpu - oracle| / max |oracle| is printed beside both.
 """
 import sys
 
@@ -54,6 +59,21 @@ def grad_err(g, r):
     return float(np.abs(g - r).max() / max(np.abs(r).max(), 1e-30))
 
 
+def dw_err(g, r, dout, msgs):
+    """max over (map, token, head, level) of |g - r| / (sum_c |dout_c| * max_c |m^l_c| of the token's
+    level-l ancestor); g, r [B, H*W, heads, L], dout [B, H, W, heads, d], msgs[l] [B, N_l, heads, d]."""
+    B, H, W, heads, d = dout.shape
+    L = r.shape[-1]
+    l1 = np.abs(np.asarray(dout, np.float64)).sum(-1).reshape(B, H * W, heads)
+    yy, xx = np.divmod(np.arange(H * W), W)
+    norm = np.empty(r.shape)
+    for l in range(L):
+        Wl = -(-W // (1 << l))
+        anc = (yy >> l) * Wl + (xx >> l)
+        norm[..., l] = l1 * np.abs(msgs[l]).max(-1)[:, anc, :]
+    return float((np.abs(np.asarray(g, np.float64) - r) / np.maximum(norm, 1e-30)).max())
+
+
 def run_backward(dev, q, k, v, g, *, levels, K, variant, dtype, w=None, scale=None, epipolar=False, label=""):
     B, H, W, heads, d = q.shape
     announce(f"backward {label} B={B} H={H} W={W} heads={heads} d={d} L={levels} K={K} {variant} {dtype}"
@@ -76,9 +96,13 @@ def run_backward(dev, q, k, v, g, *, levels, K, variant, dtype, w=None, scale=No
             assert t is None
             continue
         g_ = to_np(t).reshape(ref[name].shape)
-        errs[name] = rel_err(g_, ref[name])
+        if name == "dw":
+            fwd = O.forward(q, k, v, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale, forced=sel)
+            errs[name] = dw_err(g_, ref[name], g, fwd["msg"])
+        else:
+            errs[name] = rel_err(g_, ref[name])
         wide[name] = grad_err(g_, ref[name])
-    announce(f"  gradient errors per row {errs}, tensor-wide {wide}")
+    announce(f"  gradient errors per row (dw: per element against the message bound) {errs}, tensor-wide {wide}")
     for name, e in errs.items():
         assert e <= (TOL[dtype] if name == "dw" else TOL_GRAD), f"{name} error {e}"
     return plan, (dq, dk, dv, dw), errs
