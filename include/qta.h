@@ -182,6 +182,27 @@ qta_status qta_forward_ex(const void* q, const void* k, const void* v, const flo
                           size_t workspace_bytes, void* stream);
 
 /*
+ * qta_forward_ex_noalloc - qta_forward_ex for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same computation and
+ * results, with the workspace taken from an array of QTA_NOALLOC_WORKSPACE_BYTES inside the library,
+ * one per device, which the runtime places in device memory when it loads the library's code on that
+ * device and which stays there until the process ends. The call allocates and frees nothing; its
+ * first call on a device looks the array's address up (hipGetSymbolAddress) with that device current.
+ *   Problems whose workspace (qta_workspace_bytes_ex with the same arguments) exceeds
+ *   QTA_NOALLOC_WORKSPACE_BYTES return QTA_ERR_WORKSPACE before any launch; other errors as in
+ *   qta_forward_ex.
+ *   Every call on one device uses that device's one array: calls that may run at the same time on
+ *   one device (different streams, or host threads without an order between their streams) race and
+ *   give wrong results; calls issued in order on one stream are safe. No part of the array needs to
+ *   start cleared (each call writes every region it reads), and its contents after a call are
+ *   unspecified.
+ */
+#define QTA_NOALLOC_WORKSPACE_BYTES ((size_t)64 << 20)
+qta_status qta_forward_ex_noalloc(const void* q, const void* k, const void* v, const float* w, int B, int heads,
+                                  int H, int W, int d, int levels, int K, qta_variant variant, qta_dtype dtype,
+                                  float scale, const qta_options* opt, void* out, void* stream);
+
+/*
  * qta_backward_ex - gradients of the layer for training (the paper trains every model with it,
  * Sec. 4): given dout = dLoss/dout, the gradients of q, k, v and, for QuadTree-B with w, of w. The
  * kept-key sets are those the forward chose and are held fixed: top-K is a selection and has no

@@ -679,6 +679,59 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
 
 }  // extern "C"
 
+// ---- the forward without a caller workspace ----
+// The workspace of qta_forward_ex_noalloc: one array per device, in the library's code object, so
+// that a call allocates nothing. In host code `scratch` names a host-side stand-in, never the device
+// memory: the device address is looked up per device (scratch_device_ptr) and only that is used.
+static __device__ __align__(256) unsigned char scratch[QTA_NOALLOC_WORKSPACE_BYTES];
+
+namespace {
+
+std::atomic<void*> scratch_address[64];      // per device: the device address of `scratch`
+
+// The device address of `scratch` on the current device, looked up on the first call on that device
+// (with that device current); racing threads store the same address.
+qta_status scratch_device_ptr(void** out)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return QTA_ERR_HIP;
+    if (dev < 0 || dev >= 64) return QTA_ERR_UNSUPPORTED;
+    void* p = scratch_address[dev].load(std::memory_order_acquire);
+    if (!p) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return QTA_ERR_HIP;
+        if ((reinterpret_cast<uintptr_t>(p) & (kAlign - 1)) != 0) return QTA_ERR_HIP;
+        scratch_address[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return QTA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+qta_status qta_forward_ex_noalloc(const void* q, const void* k, const void* v, const float* w, int B, int heads, int H,
+                                  int W, int d, int levels, int K, qta_variant variant, qta_dtype dtype, float scale,
+                                  const qta_options* opt, void* out, void* stream)
+{
+    // everything qta_forward_ex validates before it touches the workspace, so that a rejected call
+    // does not reach the device either
+    qta_status st = check_problem(B, heads, d, 1, variant, dtype);
+    if (st != QTA_OK) return st;
+    if (!q || !k || !v || !out) return QTA_ERR_INVALID;
+    qta_workspace_layout L;
+    st = qta_get_workspace_layout_ex(B, heads, H, W, d, levels, K, dtype, opt, &L);
+    if (st != QTA_OK) return st;
+    if (L.total > QTA_NOALLOC_WORKSPACE_BYTES) return QTA_ERR_WORKSPACE;
+    void* ws = nullptr;
+    st = scratch_device_ptr(&ws);
+    if (st != QTA_OK) return st;
+    return qta_forward_ex(q, k, v, w, B, heads, H, W, d, levels, K, variant, dtype, scale, opt, out, ws,
+                          QTA_NOALLOC_WORKSPACE_BYTES, stream);
+}
+
+}  // extern "C"
+
 extern "C" {
 
 size_t qta_backward_workspace_bytes_ex(int B, int heads, int H, int W, int d, int levels, int K, qta_variant variant,

@@ -70,6 +70,7 @@ _SIGS = {
     "qta_workspace_bytes_ex": ([_I, _I, _I, _I, _I, _I, _I, _I, _P], ctypes.c_size_t),
     "qta_forward": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, ctypes.c_size_t, _P], _I),
     "qta_forward_ex": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P, ctypes.c_size_t, _P], _I),
+    "qta_forward_ex_noalloc": ([_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, _P], _I),
     "qta_backward_workspace_bytes_ex": ([_I, _I, _I, _I, _I, _I, _I, _I, _I, _P], ctypes.c_size_t),
     "qta_backward_ex": ([_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _P, ctypes.c_size_t,
                          _P, _P, _P, _P, _P, ctypes.c_size_t, _P], _I),
@@ -478,6 +479,32 @@ def forward(q, k, v, *, levels: int, K, variant: str, w=None, scale=None, v_leve
     plan = Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=q.dtype, device=q.device,
                 scale=scale, v_supplied=v_levels is not None, pe=pe_weight is not None, epipolar=epipolar)
     return plan.run(q, k, v, w, v_levels=v_levels, pe_weight=pe_weight, pe_bias=pe_bias)
+
+
+NOALLOC_WORKSPACE_BYTES = 64 << 20      # QTA_NOALLOC_WORKSPACE_BYTES of include/qta.h
+
+
+def forward_noalloc(q, k, v, out, *, levels: int, K, variant: str, w=None, scale=None, epipolar: bool = False):
+    """``qta_forward_ex_noalloc``: the forward into the caller's ``out`` (same shape and dtype as q),
+    with the library's own per-device workspace array, so nothing is allocated (the binding allocates
+    nothing either). ``K``: one count or one per level (entry 0 unused). Calls on one device that can
+    overlap in time race on that array."""
+    for name, t in (("q", q), ("k", k), ("v", v), ("out", out)):
+        _require(t, name, q.dtype, 5)
+        if tuple(t.shape) != tuple(q.shape):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}")
+    B, H, W, heads, d = q.shape
+    if w is not None:
+        _require(w, "w", torch.float32, 4)
+    Kl = k_levels(K, levels)
+    tbl = _k_table(Kl)
+    opt = Options()
+    opt.K_levels = ctypes.addressof(tbl)
+    opt.epipolar = int(bool(epipolar))
+    _check("qta_forward_ex_noalloc", lib().qta_forward_ex_noalloc(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(w), B, heads, H, W, d, levels, Kl[1] if levels > 1 else max(Kl[0], 1),
+        _VARIANTS[variant], _dtype_code(q), _scale(scale), ctypes.byref(opt), _ptr(out), _stream(q.device)))
+    return out
 
 
 class _QuadTreeAttention(torch.autograd.Function):

@@ -325,3 +325,30 @@ def test_binding_structs_match_the_header(tmp_path):
         assert got[(cname, "size")] == ctypes.sizeof(cls), cname
         for fname, _ in cls._fields_:
             assert got[(cname, fname)] == getattr(cls, fname).offset, f"{cname}.{fname}"
+
+
+def test_noalloc_forward_rejects_problems_beyond_its_array():
+    """qta_forward_ex_noalloc: a problem whose workspace exceeds QTA_NOALLOC_WORKSPACE_BYTES is
+    rejected with QTA_ERR_WORKSPACE on the host (before the device array is looked up or any launch);
+    invalid arguments as in qta_forward_ex."""
+    lib = P.lib()
+    text = open(HEADER).read()
+    assert "#define QTA_NOALLOC_WORKSPACE_BYTES ((size_t)64 << 20)" in text
+    assert P.NOALLOC_WORKSPACE_BYTES == 64 << 20
+    # epipolar stereo-sized problem: 141 MiB of workspace
+    opt = P.Options()
+    opt.epipolar = 1
+    need = lib.qta_workspace_bytes_ex(2, 8, 120, 160, 32, 4, 8, BF16, ctypes.byref(opt))
+    assert need > 64 << 20
+    st = lib.qta_forward_ex_noalloc(FAKE, FAKE, FAKE, None, 2, 8, 120, 160, 32, 4, 8, VB, BF16, 0.0,
+                                    ctypes.byref(opt), FAKE, None)
+    assert st == WORKSPACE
+    # without a null pointer check failing first, a too-large plain problem is a workspace error too
+    assert lib.qta_workspace_bytes(64, 8, 120, 160, 32, 4, 8, F32) > 64 << 20
+    assert lib.qta_forward_ex_noalloc(FAKE, FAKE, FAKE, None, 64, 8, 120, 160, 32, 4, 8, VB, F32, 0.0, None,
+                                      FAKE, None) == WORKSPACE
+    # invalid arguments are still invalid
+    assert lib.qta_forward_ex_noalloc(None, FAKE, FAKE, None, 1, 1, 16, 16, 32, 3, 4, VA, F32, 0.0, None,
+                                      FAKE, None) == INVALID
+    assert lib.qta_forward_ex_noalloc(FAKE, FAKE, FAKE, None, 1, 1, 16, 16, 48, 3, 4, VA, F32, 0.0, None,
+                                      FAKE, None) == UNSUPPORTED
