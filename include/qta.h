@@ -21,10 +21,12 @@
  *     storage type `dtype` (fp32 or bf16). Pyramid levels use the same layout at their size.
  *   - Flat token index at level l: y*W_l + x.
  *   - Messages are fp32 [B][N_l][heads][d]. Selections are int32 [B][heads][N_l][K] holding the
- *     flat key indices of level l that a query keeps. They form a set: the first min(K, number of
- *     candidates) entries are the kept keys in an unspecified (but deterministic) order, the rest
- *     are -1. Scores are fp32 in the same shape, aligned with the indices (0 where the index is
- *     -1): QuadTree-B stores the softmax probability, QuadTree-A the recursive score s.
+ *     flat key indices of level l that a query keeps: the first min(K, number of candidates)
+ *     entries are the kept keys, the rest are -1. Scores are fp32 in the same shape, aligned with
+ *     the indices (0 where the index is -1): QuadTree-B stores the softmax probability, QuadTree-A
+ *     the recursive score s. The stage calls (qta_coarse_attn, qta_fine_attn) return every row
+ *     ordered by (score descending, index ascending); the selections qta_forward keeps in its
+ *     workspace are sets in an unspecified but deterministic order (no consumer needs them sorted).
  *   - Each head is an independent quadtree. Softmax temperature: `scale` if > 0, else 1/sqrt(d).
  *   - A query keeps the K candidates of highest score; ties at the cut go to the lower flat index.
  *
@@ -261,7 +263,8 @@ qta_status qta_build_pyramid(const void* x, void* levels_out, int B, int H, int 
  * qta_coarse_attn - steps 2-3 at the coarsest level (Eq. 1 over the whole Hc x Wc map).
  *   qc, kc, vc  coarsest pyramid level, [B][Hc][Wc][heads][d] dtype; Hc*Wc <= QTA_MAX_COARSE.
  *   msg         fp32 [B][Hc*Wc][heads][d].
- *   sel_idx, sel_key  [B][heads][Hc*Wc][K]: the min(K, Hc*Wc) keys of highest probability.
+ *   sel_idx, sel_key  [B][heads][Hc*Wc][K]: the min(K, Hc*Wc) keys of highest probability, each
+ *               row ordered by (probability descending, index ascending), then the -1 slots.
  *               Both NULL: no selection (a single-level problem) and msg is full attention for
  *               either variant. Otherwise both must be given; QuadTree-A's msg then leaves out
  *               the kept keys (they are refined at the next level, Omega = Gamma - Gamma'),
@@ -293,7 +296,8 @@ qta_status qta_topk(const float* keys, const int32_t* cand_idx, int rows, int n,
  *               A: s = s_parent * t with t a softmax over the 2x2 children of one kept key
  *               (Eq. 4); the message sums s*v over the candidates this query does not keep
  *               (Eq. 3 over Omega).
- *   sel_idx, sel_key  [B][heads][Hl*Wl][K]: this level's selections (B by probability, A by s).
+ *   sel_idx, sel_key  [B][heads][Hl*Wl][K]: this level's selections (B by probability, A by s),
+ *               each row ordered by (score descending, index ascending), then the -1 slots.
  */
 qta_status qta_fine_attn(const void* ql, const void* kl, const void* vl,
                          int B, int heads, int Hl, int Wl, int d, int K,

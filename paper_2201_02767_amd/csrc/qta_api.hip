@@ -393,8 +393,11 @@ qta_status qta_coarse_attn(const void* qc, const void* kc, const void* vc, int B
     a.sel_idx = sel_idx;
     a.sel_key = sel_key;
     a.levels = 1;
-    return launch_status(launch_coarse_attn(a, d, variant == QTA_VARIANT_A, dtype == QTA_BF16,
-                                            static_cast<hipStream_t>(stream)));
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (launch_coarse_attn(a, d, variant == QTA_VARIANT_A, dtype == QTA_BF16, s) != hipSuccess) return QTA_ERR_HIP;
+    // the stage call returns each row ordered (inside qta_forward a selection stays an unordered set)
+    if (!sel_idx) return QTA_OK;
+    return launch_status(launch_sort_rows(sel_idx, sel_key, static_cast<long long>(B) * heads * Hc * Wc, K, s));
 }
 
 qta_status qta_topk(const float* keys, const int32_t* cand_idx, int rows, int n, int K, int32_t* idx_out,
@@ -438,8 +441,10 @@ qta_status qta_fine_attn(const void* ql, const void* kl, const void* vl, int B, 
     a.msg = msg;
     a.sel_idx = sel_idx;
     a.sel_key = sel_key;
-    return launch_status(launch_fine_attn(a, d, variant == QTA_VARIANT_A, dtype == QTA_BF16, false,
-                                          static_cast<hipStream_t>(stream)));
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (launch_fine_attn(a, d, variant == QTA_VARIANT_A, dtype == QTA_BF16, false, s) != hipSuccess) return QTA_ERR_HIP;
+    // the stage call returns each row ordered (inside qta_forward a selection stays an unordered set)
+    return launch_status(launch_sort_rows(sel_idx, sel_key, static_cast<long long>(B) * heads * Hl * Wl, K, s));
 }
 
 qta_status qta_finest_attn(const void* q0, const void* k0, const void* v0, int B, int heads, int H, int W, int d, int K,

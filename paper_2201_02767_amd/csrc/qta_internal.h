@@ -314,6 +314,9 @@ hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool use_b
 hipError_t launch_fine_attn_wide(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
                                  hipStream_t stream);
 hipError_t launch_topk(const TopkArgs& a, hipStream_t stream);
+// Orders each of `rows` selection rows of K entries (idx int32, key fp32, in place) by (key descending,
+// index ascending), empty slots (index -1) last.
+hipError_t launch_sort_rows(int32_t* idx, float* key, long long rows, int K, hipStream_t stream);
 hipError_t launch_fill_zero(const FillRange* r, int n, hipStream_t stream);
 hipError_t launch_bwd_level(const BwdLevelArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
                             hipStream_t stream);

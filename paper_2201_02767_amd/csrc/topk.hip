@@ -67,7 +67,49 @@ __global__ __launch_bounds__(256) void topk_kernel(TopkArgs a)
     }
 }
 
+// In-place ordering of selection rows of K <= 64 entries (the stage calls' output contract): one
+// wave per row, lane i holds entry i as a ranking word (0 for an empty slot, index -1), counts the
+// entries ranked before it by reading every other lane's word, and writes itself to that place.
+// Empty slots follow the kept keys. Every load of the row completes before any store (the ranks
+// need all of them).
+__global__ __launch_bounds__(256) void sort_rows_kernel(int32_t* idx, float* key, int rows, int K)
+{
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;                    // whole wave leaves; no workgroup barriers below
+    const size_t base = static_cast<size_t>(row) * K;
+    const int e = min(lane, K - 1);
+    const int32_t my_idx = idx[base + e];
+    const float my_key = key[base + e];
+    const bool live = lane < K && my_idx >= 0;
+    const uint64_t word = live ? rank_word(my_key, my_idx) : 0ull;
+    int before = 0;
+    for (int j = 0; j < K; ++j) {               // uniform trip count
+        const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(word), j);
+        const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(word >> 32), j);
+        const uint64_t wj = (static_cast<uint64_t>(hi) << 32) | lo;
+        before += wj > word ? 1 : 0;
+    }
+    const uint64_t live_mask = __ballot(live);
+    const uint64_t dead_mask = __ballot(lane < K && !live);
+    const int nlive = __popcll(live_mask);
+    const int pos = live ? before : nlive + lanes_below(dead_mask);
+    if (lane < K) {
+        idx[base + pos] = live ? my_idx : -1;
+        key[base + pos] = live ? my_key : 0.f;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_sort_rows(int32_t* idx, float* key, long long rows, int K, hipStream_t stream)
+{
+    if (rows <= 0) return hipSuccess;
+    if (K < 1 || K > kWave || rows > 0x7FFFFFFFLL - 3) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(sort_rows_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, stream, idx, key,
+                       static_cast<int>(rows), K);
+    return hipGetLastError();
+}
 
 hipError_t launch_topk(const TopkArgs& a, hipStream_t stream)
 {

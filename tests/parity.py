@@ -88,3 +88,20 @@ def query_rows_mask(dims, level: int, B: int, heads: int) -> np.ndarray:
     """All queries of a level are real (no padding), so every row counts."""
     H, W = dims[level]
     return np.ones((B, heads, H * W), bool)
+
+
+def assert_rows_ordered(idx: np.ndarray, key: np.ndarray) -> None:
+    """Every selection row lists its kept keys by (score descending, index ascending), then the empty
+    slots (index -1, score 0): the order the stage calls return."""
+    idx = idx.reshape(-1, idx.shape[-1])
+    key = key.reshape(-1, key.shape[-1]).astype(np.float64)
+    live = idx >= 0
+    n = live.sum(axis=1)
+    # live entries first
+    assert (live == (np.arange(idx.shape[1])[None, :] < n[:, None])).all(), "empty slots before kept keys"
+    assert (key[~live] == 0).all()
+    a_i, a_k = idx[:, :-1], key[:, :-1]
+    b_i, b_k = idx[:, 1:], key[:, 1:]
+    both = live[:, :-1] & live[:, 1:]
+    ok = (a_k > b_k) | ((a_k == b_k) & (a_i < b_i))
+    assert ok[both].all(), "kept keys not ordered by (score desc, index asc)"

@@ -13,7 +13,7 @@ import paper_2201_02767_amd as P
 from paper_2201_02767_amd.inputs import WORKLOADS, make_level_weights, make_pe, make_qkv, make_v_levels, round_bf16
 from oracle import oracle as O
 from tests import brute
-from tests.parity import TOL, check_selection, rel_err, to_np
+from tests.parity import TOL, assert_rows_ordered, check_selection, rel_err, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -208,6 +208,7 @@ def test_stages_teacher_forced(dev, variant, dtype, d, K):
     torch.cuda.synchronize()
     chk = check_selection(to_np(sidx), ref["cand_idx"][c], ref["cand_key"][c], K)
     assert chk["bad"] == 0, chk
+    assert_rows_ordered(to_np(sidx), to_np(skey))
     forced = O.forward(q, k, v, levels=L, K=K, variant=variant, dtype=dtype, w=w,
                        forced=[None] * c + [to_np(sidx)])
     assert rel_err(to_np(msg), forced["msg"][c]) <= TOL[dtype]
@@ -220,6 +221,7 @@ def test_stages_teacher_forced(dev, variant, dtype, d, K):
         torch.cuda.synchronize()
         chk = check_selection(to_np(sidx), ref["cand_idx"][l], ref["cand_key"][l], K)
         assert chk["bad"] == 0, chk
+        assert_rows_ordered(to_np(sidx), to_np(skey))
         frc = [None] * L
         frc[l] = to_np(sidx)
         for j in range(l + 1, L):
@@ -235,6 +237,39 @@ def test_stages_teacher_forced(dev, variant, dtype, d, K):
                         variant=variant, w=None if w is None else torch.from_numpy(w).to(dev))
     torch.cuda.synchronize()
     assert rel_err(to_np(out), ref["out"]) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+def test_stage_selection_order_with_ties_and_empty_slots(dev, variant):
+    """The stage calls' row order on exact ties and padded rows: constant queries and keys make every
+    logit equal, so each row keeps the lowest indices, listed in ascending order; with more slots than
+    keys (K = 6 on a 2 x 2 coarsest map) the two empty slots come last as (-1, 0). The intermediate
+    stage gets parents whose candidate sets all tie in the same way."""
+    B, heads, d = 2, 2, 32
+    one = np.ones((B, 2, 2, heads, d), np.float32)
+    rng = np.random.default_rng(5)
+    vc = rng.standard_normal(one.shape).astype(np.float32)
+    announce(f"stage selection order {variant}")
+    msg, sidx, skey = P.coarse_attn(dev_t(one, "f32", dev), dev_t(one, "f32", dev), dev_t(vc, "f32", dev), K=6,
+                                    variant=variant)
+    torch.cuda.synchronize()
+    idx, key = to_np(sidx), to_np(skey)
+    assert_rows_ordered(idx, key)
+    assert (idx[..., :4] == np.arange(4)).all() and (idx[..., 4:] == -1).all()
+    np.testing.assert_allclose(key[..., :4], 0.25, rtol=1e-6)
+    # level 1 of a 4 x 6 map: parents (2 x 3 map) each kept keys 5, 0, 3 of the parent level
+    Hl, Wl, K = 4, 6, 3
+    ql = np.ones((B, Hl, Wl, heads, d), np.float32)
+    pidx = np.broadcast_to(np.array([5, 0, 3], np.int32), (B, heads, 6, K)).copy()
+    pkey = np.full((B, heads, 6, K), 1.0 / 3, np.float32)
+    msg, sidx, skey = P.fine_attn(dev_t(ql, "f32", dev), dev_t(ql, "f32", dev), dev_t(ql, "f32", dev),
+                                  torch.from_numpy(pidx).to(dev), torch.from_numpy(pkey).to(dev), K=K, variant=variant)
+    torch.cuda.synchronize()
+    idx, key = to_np(sidx), to_np(skey)
+    assert_rows_ordered(idx, key)
+    # candidates: children of parent keys 0, 3 and 5 (level-1 flat indices); equal scores keep the
+    # three lowest: 0, 1 and 6 (children (0,0), (0,1), (1,0) of parent key 0)
+    assert (idx == np.array([0, 1, 6], np.int32)).all()
 
 
 # ------------------------------------------------------------------------------------------------
