@@ -61,17 +61,20 @@ extern "C" {
 #define QTA_MAX_K 64
 #define QTA_MAX_COARSE 1024
 
+/* Each enum ends with a sentinel at INT_MAX so that its range covers every int: a caller may pass
+ * any int, and values other than the listed ones are rejected as QTA_ERR_INVALID. */
 typedef enum {
     QTA_OK = 0,
     QTA_ERR_INVALID = 1,
     QTA_ERR_UNSUPPORTED = 2,
     QTA_ERR_WORKSPACE = 3,
-    QTA_ERR_HIP = 4
+    QTA_ERR_HIP = 4,
+    QTA_STATUS_MAX_ENUM = 0x7FFFFFFF
 } qta_status;
 
-typedef enum { QTA_VARIANT_A = 0, QTA_VARIANT_B = 1 } qta_variant;
+typedef enum { QTA_VARIANT_A = 0, QTA_VARIANT_B = 1, QTA_VARIANT_MAX_ENUM = 0x7FFFFFFF } qta_variant;
 
-typedef enum { QTA_F32 = 0, QTA_BF16 = 1 } qta_dtype;
+typedef enum { QTA_F32 = 0, QTA_BF16 = 1, QTA_DTYPE_MAX_ENUM = 0x7FFFFFFF } qta_dtype;
 
 /* Byte offsets of the regions qta_forward keeps in its workspace. Entries for levels that do not
  * exist (and level 0 of q/k/v, msg, sel_idx, sel_key, which live outside it) are 0.

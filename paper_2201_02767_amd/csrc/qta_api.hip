@@ -292,6 +292,7 @@ const char* qta_status_str(qta_status status)
     case QTA_ERR_UNSUPPORTED: return "unsupported shape or type";
     case QTA_ERR_WORKSPACE: return "workspace too small";
     case QTA_ERR_HIP: return "HIP launch failed";
+    default: break;
     }
     return "unknown status";
 }
