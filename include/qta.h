@@ -95,7 +95,7 @@ typedef struct {
     size_t msg[QTA_MAX_LEVELS];     /* level l >= 1, fp32 [B][N_l][heads][d]                 */
     size_t sel_idx[QTA_MAX_LEVELS]; /* level l >= 1, int32 [B][heads][N_l][K_l]              */
     size_t sel_key[QTA_MAX_LEVELS]; /* level l >= 1, fp32  [B][heads][N_l][K_l]              */
-    size_t pe0;                     /* with a position encoding: level 0's, fp32 [B][N][heads][d] */
+    size_t pe0;                     /* level 0's position encoding when not fused, fp32 [B][N][heads][d] */
     size_t total;                   /* bytes; every region starts on a 256-byte boundary     */
 } qta_workspace_layout;
 
@@ -168,9 +168,10 @@ typedef struct {
     void* aux_stream2;
 } qta_options;
 
-/* Workspace of qta_forward_ex with these options (layout and byte count as for qta_forward; with a
- * position encoding the workspace also holds level 0's encoding, fp32 [B][H*W][heads][d], at
- * layout.pe0). */
+/* Workspace of qta_forward_ex with these options (layout and byte count as for qta_forward). With a
+ * position encoding, level 0's encoding is computed inside the finest level's kernel on maps of more
+ * than one row when 4*K_1 <= 64; otherwise (a single level, one-row maps or epipolar attention,
+ * 4*K_1 > 64) the workspace also holds it, fp32 [B][H*W][heads][d], at layout.pe0. */
 qta_status qta_get_workspace_layout_ex(int B, int heads, int H, int W, int d, int levels, int K,
                                        qta_dtype dtype, const qta_options* opt, qta_workspace_layout* layout);
 size_t qta_workspace_bytes_ex(int B, int heads, int H, int W, int d, int levels, int K, qta_dtype dtype,

@@ -230,6 +230,22 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
         for (int ks = 0; ks < NKS; ++ks) s += red[((ks * NCT + ct) * 16 + r) * 16 + col];
         const int qi = tile * kRows + r;
         if (qi >= N) continue;
+        if (a.pe_w) {                                    // uniform: the fused position encoding
+            // 3x3 depth-wise cross-correlation of v around token qi, zero outside the map, plus the bias
+            const int Wc = a.Wc, Hc = N / Wc;
+            const int qy = qi / Wc, qx = qi - qy * Wc;
+            const float* wk = a.pe_w + (static_cast<size_t>(h) * D + ch) * 9;
+            float pe = a.pe_b ? a.pe_b[h * D + ch] : 0.f;
+#pragma unroll
+            for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+                for (int kx = 0; kx < 3; ++kx) {
+                    const int yy = qy + ky - 1, xx = qx + kx - 1;
+                    if (yy < 0 || yy >= Hc || xx < 0 || xx >= Wc) continue;
+                    pe = fmaf(wk[ky * 3 + kx], S::load1(a.v, (tok0 + yy * Wc + xx) * C + hoff + ch), pe);
+                }
+            s += pe;
+        }
         if (a.out) {
             float wl = 1.0f;
             if (!VA) wl = a.w ? a.w[((tok0 + qi) * a.heads + h) * a.levels] : 1.0f / a.levels;
@@ -478,7 +494,10 @@ hipError_t launch_one(const CoarseArgs& a, hipStream_t stream)
 template <typename T, int D, bool VA>
 hipError_t launch_per_lane(const CoarseArgs& a, hipStream_t stream)
 {
-    if (a.N <= kWave) return launch_small<T, D, VA>(a, stream);
+    if (a.N <= kWave) {
+        if (a.pe_w) return hipErrorInvalidValue;       // the small-map kernel has no fused position encoding
+        return launch_small<T, D, VA>(a, stream);
+    }
     switch (coarse_per_lane(a.N)) {
     case 1: return launch_one<T, D, VA, 1>(a, stream);
     case 2: return launch_one<T, D, VA, 2>(a, stream);

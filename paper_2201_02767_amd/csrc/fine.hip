@@ -11,7 +11,7 @@ namespace {
 
 using namespace fine;
 
-template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW>
+template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW, bool PE>
 __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
 {
     const int wave = threadIdx.x >> 6;
@@ -25,36 +25,53 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     const int nsp = (4 * a.Kp + 15) & ~15;
     ItemHead<T, D, NSP, ROW> hd;
     item_head<T, D, NSP, VA, ROW>(a, item, hd);
-    fine_item<T, D, NSP, VA, FINEST, ROW>(a, hd, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
+    fine_item<T, D, NSP, VA, FINEST, ROW, PE>(a, hd, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
 }
 
-template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW>
+template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW, bool PE>
 hipError_t launch_one(const FineArgs& a, hipStream_t stream)
 {
     const int nsp = (4 * a.Kp + 15) & ~15;
-    const size_t wave_bytes = wave_lds<T, D>(nsp).total;
+    const WaveLds lay = wave_lds<T, D>(nsp);
+    const size_t wave_bytes = lay.total;
     const int wpb = 4;
     if (wpb * wave_bytes > device_max_lds()) return hipErrorInvalidValue;
+    // the fused position encoding stages a 4x4 token block of one head in the value-row region
+    if (PE && static_cast<size_t>(lay.p - lay.v) < static_cast<size_t>(D) * kPeTokenPitch * sizeof(T))
+        return hipErrorInvalidValue;
     static std::atomic<unsigned long long> configured{0};     // devices whose LDS limit is raised
-    if (hipError_t e = set_max_lds_once(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, NSP, VA, FINEST, ROW>), configured);
+    if (hipError_t e = set_max_lds_once(reinterpret_cast<const void*>(&fine_attn_kernel<T, D, NSP, VA, FINEST, ROW, PE>),
+                                        configured);
         e != hipSuccess)
         return e;
     const long long np = static_cast<long long>(a.Hp) * a.Wp;
     const long long items = static_cast<long long>(a.B) * a.heads * (ROW ? (np + 1) / 2 : np);
     const long long blocks = (items + wpb - 1) / wpb;
     if (blocks * wpb >= 0x7FFFFFFFLL) return hipErrorInvalidValue;     // work items are int
-    hipLaunchKernelGGL((fine_attn_kernel<T, D, NSP, VA, FINEST, ROW>), dim3(static_cast<unsigned>(blocks)),
+    hipLaunchKernelGGL((fine_attn_kernel<T, D, NSP, VA, FINEST, ROW, PE>), dim3(static_cast<unsigned>(blocks)),
                        dim3(wpb * kWave), wpb * wave_bytes, stream, a);
     return hipGetLastError();
 }
 
+template <typename T, int D, bool VA, bool FINEST, bool ROW, bool PE>
+hipError_t launch_nsp_pe(const FineArgs& a, hipStream_t stream)
+{
+    const int nslot = 4 * a.Kp;
+    if (nslot <= 16) return launch_one<T, D, 16, VA, FINEST, ROW, PE>(a, stream);
+    if (nslot <= 32) return launch_one<T, D, 32, VA, FINEST, ROW, PE>(a, stream);
+    return launch_one<T, D, 64, VA, FINEST, ROW, PE>(a, stream);
+}
+
+// Levels of maps with more than one row may fuse their position encoding (a.pe_w).
 template <typename T, int D, bool VA, bool FINEST, bool ROW>
 hipError_t launch_nsp_row(const FineArgs& a, hipStream_t stream)
 {
-    const int nslot = 4 * a.Kp;
-    if (nslot <= 16) return launch_one<T, D, 16, VA, FINEST, ROW>(a, stream);
-    if (nslot <= 32) return launch_one<T, D, 32, VA, FINEST, ROW>(a, stream);
-    return launch_one<T, D, 64, VA, FINEST, ROW>(a, stream);
+    if constexpr (!ROW) {
+        if (a.pe_w) return launch_nsp_pe<T, D, VA, FINEST, ROW, true>(a, stream);
+    } else {
+        if (a.pe_w) return hipErrorInvalidValue;
+    }
+    return launch_nsp_pe<T, D, VA, FINEST, ROW, false>(a, stream);
 }
 
 // Maps of one row (attention along epipolar lines) pack two parents into one item.
@@ -76,7 +93,10 @@ hipError_t launch_td(const FineArgs& a, bool variant_a, bool finest, hipStream_t
 
 hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool bf16_in, bool finest, hipStream_t stream)
 {
-    if (4 * a.Kp > kMaxSlots) return launch_fine_attn_wide(a, d, variant_a, bf16_in, finest, stream);
+    if (4 * a.Kp > kMaxSlots) {
+        if (a.pe_w) return hipErrorInvalidValue;        // the wide kernel has no fused position encoding
+        return launch_fine_attn_wide(a, d, variant_a, bf16_in, finest, stream);
+    }
     FineArgs b = a;
     b.div_Wp = make_fastdiv(a.Wp);
     b.div_heads = make_fastdiv(a.heads);

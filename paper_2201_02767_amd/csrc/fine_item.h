@@ -21,7 +21,10 @@
 //      ballots (ties at the cut to the lower flat index); A drops their weight from its message;
 //   5. messages m = P V on the 4x4 MFMA, blocks split over 4-channel groups (and slot halves);
 //   6. levels above 0 store m; level 0 adds the ancestors' messages (times w for B) and stores the
-//      output in the storage type.
+//      output in the storage type. With a fused position encoding (PE, maps of more than one row)
+//      every level first adds to m the 3x3 depth-wise cross-correlation of its own value map around
+//      each query (zero outside the map) plus the bias: the 4x4 tokens around the sibling block are
+//      read once per wave and passed through the wave's LDS.
 #ifndef QTA_FINE_ITEM_H
 #define QTA_FINE_ITEM_H
 
@@ -37,6 +40,9 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
 constexpr int kMaxSlots = 64;
 constexpr int kPrefetchLevels = 4;    // the finest level prefetches up to this many ancestors
+// LDS pitch (elements) of one channel's 16 tokens in the fused position encoding: 20 puts the four lane
+// groups' writes and neighbouring channels' row reads in different banks (16 would stack them)
+constexpr int kPeTokenPitch = 20;
 
 // Byte layout of one wave's LDS region for nsp padded slots (a multiple of 16): the value rows
 // and the weights P.
@@ -59,6 +65,8 @@ __host__ __device__ inline WaveLds wave_lds(int nsp)
         L.vpitch = D + 4;                   // Vs[slot][channel]
         vbytes = nsp * L.vpitch * 4;
     }
+    // (the fused position encoding stages 16 tokens of one head here, kPeTokenPitch elements per channel)
+    if (vbytes < D * kPeTokenPitch * TB) vbytes = D * kPeTokenPitch * TB;
     L.p = L.v + vbytes;
     L.total = (L.p + 4 * nsp * TB + 15) / 16 * 16;
     return L;
@@ -152,7 +160,7 @@ __device__ __forceinline__ void item_head(const FineArgs& a, const int item, Ite
 // (item = (b*ceil(Np/2) + p)*heads + h): its four queries are tokens 4p .. 4p+3, candidate slot
 // s = 2*(half*K + r) + c is child c of kept key r of parent `half`, and query q uses the slots of
 // half q >> 1 only.
-template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW = false>
+template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW = false, bool PE = false>
 __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D, NSP, ROW>& hd, unsigned char* const base)
 {
     using S = Storage<T>;
@@ -166,6 +174,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     constexpr int NCG = D / 4;             // PV: 4-channel groups
     constexpr int NH = 16 / NCG;           // PV: slot halves (2 for d = 32, 1 for d = 64)
     constexpr int QPL = 4 / NH;            // output queries per lane
+    static_assert(!PE || !ROW, "the fused position encoding is for maps of more than one row");
 
     const int lane = threadIdx.x & 63;
     const int Np = a.Hp * a.Wp;
@@ -304,6 +313,30 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     const int cg = blk / NH, hh = blk % NH;
     const int ch = 4 * cg + t4;
     constexpr int kPre = FINEST ? kPrefetchLevels : 1;
+    // fused position encoding: the 4x4 tokens (2Py-1 .. 2Py+2) x (2Px-1 .. 2Px+2) of v around the
+    // sibling block, token n16 = (by, bx), chunks g, g+4, ... of its row (as in the gathers; tokens off
+    // the map read a clamped row and count as zero), and this lane's channel's 3x3 kernel and bias,
+    // requested before the ancestors' rows so that their latency overlaps the weights and the messages
+    uint4 peb[PE ? NJ : 1];
+    float pek[PE ? 9 : 1];
+    float pebias = 0.f;
+    bool pe_ok = false;
+    if constexpr (PE) {
+        const int by = 2 * Py - 1 + (n16 >> 2), bx = 2 * Px - 1 + (n16 & 3);
+        pe_ok = by >= 0 && by < H && bx >= 0 && bx < W;
+        const int byc = min(max(by, 0), H - 1), bxc = min(max(bx, 0), W - 1);
+        // this (batch, head)'s value map as for the gathers: NHWC rows, or child (by & 1, bx & 1) of
+        // parent block (by >> 1, bx >> 1)
+        const uint32_t boff = (kvb ? static_cast<uint32_t>(((__mul24(byc >> 1, a.Wp) + (bxc >> 1)) * 4 + (byc & 1) * 2 +
+                                                            (bxc & 1)) * RB)
+                                   : static_cast<uint32_t>(__mul24(byc, W) + bxc) * tok_bytes) + g * 16;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) peb[j] = *reinterpret_cast<const uint4*>(vg + (boff + 64 * j));
+        const float* wp = a.pe_w + static_cast<uint32_t>(h * D + ch) * 9u;
+#pragma unroll
+        for (int i = 0; i < 9; ++i) pek[i] = wp[i];
+        pebias = a.pe_b ? a.pe_b[h * D + ch] : 0.f;
+    }
     float anc[ROW ? QPL : 1][kPre];     // ROW: the two parents of a pair have different ancestors
     float wq[FINEST ? QPL : 1][kPre + 1];
     float peq[FINEST ? QPL : 1] = {};
@@ -489,6 +522,72 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
         for (int r = 0; r < 4; ++r) o[r] += xchg_f32<4>(o[r]);
     }
 
+    float pe_f[PE ? QPL : 1] = {};
+    if constexpr (PE) {
+        // the block into the wave's LDS as [channel][16 tokens, pitch kPeTokenPitch] (the value rows are no
+        // longer read)
+        wave_lds_sync();
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const uint4 vv = pe_ok ? peb[j] : make_uint4(0, 0, 0, 0);   // zero outside the map
+            const int c0 = (g + 4 * j) * E;
+            if constexpr (kBf16) {
+                uint16_t* pt = reinterpret_cast<uint16_t*>(Vb);
+                const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    pt[(c0 + e) * kPeTokenPitch + n16] =
+                        static_cast<uint16_t>((e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xFFFFu));
+            } else {
+                float* pt = reinterpret_cast<float*>(Vb);
+                pt[(c0 + 0) * kPeTokenPitch + n16] = __uint_as_float(vv.x);
+                pt[(c0 + 1) * kPeTokenPitch + n16] = __uint_as_float(vv.y);
+                pt[(c0 + 2) * kPeTokenPitch + n16] = __uint_as_float(vv.z);
+                pt[(c0 + 3) * kPeTokenPitch + n16] = __uint_as_float(vv.w);
+            }
+        }
+        wave_lds_sync();
+        // this lane's channel over the 4x4 block (row r: four tokens), then each of its queries,
+        // which sits at block position (1 + (qi >> 1), 1 + (qi & 1))
+        float blkv[4][4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            if constexpr (kBf16) {
+                const uint2 u = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(Vb) + ch * kPeTokenPitch + r * 4);
+                blkv[r][0] = __uint_as_float(u.x << 16);
+                blkv[r][1] = __uint_as_float(u.x & 0xFFFF0000u);
+                blkv[r][2] = __uint_as_float(u.y << 16);
+                blkv[r][3] = __uint_as_float(u.y & 0xFFFF0000u);
+            } else {
+                const float4 u = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(Vb) + ch * kPeTokenPitch + r * 4);
+                blkv[r][0] = u.x;
+                blkv[r][1] = u.y;
+                blkv[r][2] = u.z;
+                blkv[r][3] = u.w;
+            }
+        }
+        // (with two lanes per channel, NH = 2, the lane's queries are row hh of the sibling block, so the
+        // window rows are hh .. hh + 2, chosen by a select between the two possible rows)
+#pragma unroll
+        for (int u = 0; u < QPL; ++u) {
+            const int rx = u & 1;                     // the window's left column in the block
+            const int ry = NH == 2 ? 0 : u >> 1;      // its top row (NH = 2: plus hh)
+            float acc = pebias;
+#pragma unroll
+            for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+                for (int kx = 0; kx < 3; ++kx) {
+                    float val;
+                    if constexpr (NH == 2)
+                        val = hh ? blkv[ky + 1][rx + kx] : blkv[ky][rx + kx];
+                    else
+                        val = blkv[ry + ky][rx + kx];
+                    acc = fmaf(pek[ky * 3 + kx], val, acc);
+                }
+            pe_f[u] = acc;
+        }
+    }
+
     // ---- 6. outputs ----
 #pragma unroll
     for (int u = 0; u < QPL; ++u) {
@@ -500,14 +599,14 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
         const uint32_t qpos = static_cast<uint32_t>(__mul24(qy, W) + qx);      // token within the map
         if constexpr (!FINEST) {
             float* mb = a.msg + (static_cast<size_t>(b) * N * a.heads + h) * D;  // uniform
-            mb[qpos * static_cast<uint32_t>(a.heads * D) + ch] = m;
+            mb[qpos * static_cast<uint32_t>(a.heads * D) + ch] = PE ? m + pe_f[PE ? u : 0] : m;
         } else {
             const size_t qtok = static_cast<size_t>(b) * N + qpos;
             const int L = a.levels;
             const float wdef = 1.0f / L;
             float out;
             if (prefetch) {
-                out = (VA ? 1.0f : (a.w ? wq[u][0] : wdef)) * (m + peq[u]);
+                out = (VA ? 1.0f : (a.w ? wq[u][0] : wdef)) * (m + (PE ? pe_f[PE ? u : 0] : peq[u]));
 #pragma unroll
                 for (int lev = 1; lev <= kPre; ++lev) {
                     if (lev >= L) break;
@@ -515,7 +614,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                 }
             } else {
                 const float* wrow = a.w ? a.w + (qtok * a.heads + h) * L : nullptr;
-                const float pe = a.pe0 ? a.pe0[(qtok * a.heads + h) * D + ch] : 0.f;
+                const float pe = PE ? pe_f[PE ? u : 0] : (a.pe0 ? a.pe0[(qtok * a.heads + h) * D + ch] : 0.f);
                 out = (VA ? 1.0f : (wrow ? wrow[0] : wdef)) * (m + pe);
                 for (int lev = 1; lev < L; ++lev) {
                     const size_t an = static_cast<size_t>(b) * a.lvl_N[lev] +

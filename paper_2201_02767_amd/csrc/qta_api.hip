@@ -80,6 +80,17 @@ bool use_blocked(const int* Kl, int l, int levels, bool v_supplied)
     return !v_supplied && l >= 1 && l <= levels - 2 && 4 * Kl[l + 1] <= 64;
 }
 
+// Whether level l's position encoding is computed inside that level's attention kernel: the coarsest
+// level when it takes the tiled coarse kernel (more than 64 tokens), a finer level when its kernel is
+// the one with at most 64 candidate slots and the level is not a one-row map (whose pairs of parents
+// that kernel packs). The other levels get the separate encoding pass (level 0 through a workspace
+// buffer, the others in place on their messages).
+bool pe_level_fused(int l, int levels, const int* Hl, const int* Wl, const int* Kl)
+{
+    if (l == levels - 1) return Hl[l] * Wl[l] > 64;
+    return !(Hl[l] == 1 && Hl[l + 1] == 1) && 4 * Kl[l + 1] <= 64;
+}
+
 qta_status layout(int B, int heads, int H, int W, int d, int levels, const int* Kl, bool v_supplied, bool pe,
                   qta_dtype dtype, qta_workspace_layout* L)
 {
@@ -122,7 +133,7 @@ qta_status layout(int B, int heads, int H, int W, int d, int levels, const int* 
         L->sel_key[l] = off;
         off = align_up(off + static_cast<size_t>(B) * heads * N * Kl[l] * sizeof(float));
     }
-    if (pe) {
+    if (pe && !pe_level_fused(0, levels, Hl, Wl, Kl)) {
         L->pe0 = off;
         off = align_up(off + static_cast<size_t>(B) * Hl[0] * Wl[0] * C * sizeof(float));
     }
@@ -553,17 +564,30 @@ qta_status qta_forward_ex(const void* q, const void* k, const void* v, const flo
         if (e != hipSuccess) return QTA_ERR_HIP;
     }
 
-    // multiscale position encoding: levels above 0 add it to their messages in place, level 0
-    // writes it to the workspace for the kernel that forms the output (launched right before it)
-    float* pe0 = pe ? reinterpret_cast<float*>(ws + L.pe0) : nullptr;
+    // multiscale position encoding: each level's attention kernel adds its own where it can
+    // (pe_level_fused); one separate pass covers the other levels, adding it in place to the messages
+    // of levels above 0 and writing level 0's to the workspace for the finest kernel (launched right
+    // before that kernel)
+    bool fused[QTA_MAX_LEVELS] = {};
+    int unfused = 0;
+    for (int l = 0; l < levels; ++l) {
+        fused[l] = pe && pe_level_fused(l, levels, L.H, L.W, o.Kl);
+        unfused += (pe && !fused[l]) ? 1 : 0;
+    }
+    auto pe_w = [&](int l) { return fused[l] ? o.pe_weight + static_cast<size_t>(l) * C * 9 : nullptr; };
+    auto pe_b = [&](int l) { return (fused[l] && o.pe_bias) ? o.pe_bias + static_cast<size_t>(l) * C : nullptr; };
+    float* pe0 = (pe && !fused[0]) ? reinterpret_cast<float*>(ws + L.pe0) : nullptr;
+    // the separate encoding pass over the levels whose kernel does not fuse it
     auto posenc = [&]() -> hipError_t {
+        if (unfused == 0) return hipSuccess;
         PosEncArgs p{};
-        p.nlev = levels;
+        p.nlev = 0;
         p.B = B;
         p.heads = heads;
         p.d = d;
         for (int l = 0; l < levels; ++l) {
-            PosEncLevel& e = p.lv[l];
+            if (fused[l]) continue;
+            PosEncLevel& e = p.lv[p.nlev++];
             e.v = l == 0 ? v : lv[2][l];
             e.blocked = l == 0 ? 0 : L.blocked[l];
             e.H = L.H[l];
@@ -589,6 +613,9 @@ qta_status qta_forward_ex(const void* q, const void* k, const void* v, const flo
         a.C = C;
         a.scale = tau;
         a.levels = levels;
+        a.pe_w = pe_w(c);
+        a.pe_b = pe_b(c);
+        a.Wc = L.W[c];
         if (levels == 1) {
             a.K = 0;
             a.out = out;
@@ -632,6 +659,8 @@ qta_status qta_forward_ex(const void* q, const void* k, const void* v, const flo
         a.msg = msg(l);
         a.sel_idx = sidx(l);
         a.sel_key = skey(l);
+        a.pe_w = pe_w(l);
+        a.pe_b = pe_b(l);
         hipError_t e = launch_fine_attn(a, d, va, use_bf16, false, s);
         if (e != hipSuccess) return QTA_ERR_HIP;
     }
@@ -663,6 +692,8 @@ qta_status qta_forward_ex(const void* q, const void* k, const void* v, const flo
         a.out = out;
         a.w = w;
         a.pe0 = pe0;
+        a.pe_w = pe_w(0);
+        a.pe_b = pe_b(0);
         a.levels = levels;
         for (int l = 1; l < levels; ++l) {
             a.coarser_msg[l] = msg(l);

@@ -71,6 +71,10 @@ struct CoarseArgs {
     void* out;                  // single-level problem: write out = w0 * m (B) or m (A) in dtype
     const float* w;
     const float* pe0;           // single-level problem: position encoding added to m, or NULL
+    const float* pe_w;          // or, fused (coarse_attn_kernel): this level's depth-wise kernels fp32 [C][3][3],
+                                // applied to v around each query (an Hc x Wc map) and added to m; or NULL
+    const float* pe_b;          // its bias fp32 [C], or NULL
+    int Wc;                     // map width (with pe_w)
     int levels;
 };
 
@@ -123,6 +127,9 @@ struct FineArgs {
     void* out;
     const float* w;
     const float* pe0;           // level 0's position encoding, fp32 [B][N][heads][d], added to m0; or NULL
+    const float* pe_w;          // or, fused (maps of more than one row): level 0's depth-wise kernels, fp32
+                                // [C][3][3], applied to v around each query and added to m0; or NULL
+    const float* pe_b;          // its bias, fp32 [C], or NULL
     int levels;
     const float* coarser_msg[QTA_MAX_LEVELS];   // entry j: message of level j (j >= 1)
     int lvl_W[QTA_MAX_LEVELS];                  // map width of level j

@@ -245,11 +245,16 @@ def test_forward_ex_validation():
 
 
 def test_position_encoding_workspace():
-    """With an encoding the workspace adds level 0's fp32 encoding after everything else."""
+    """Level 0's encoding is fused into the finest kernel on maps of more than one row when
+    4*K_1 <= 64 (no workspace buffer); otherwise the workspace adds it, fp32, after everything else."""
     base = P.workspace_layout(2, 2, 40, 30, 32, 3, 8, torch.bfloat16)
-    lay = P.workspace_layout(2, 2, 40, 30, 32, 3, 8, torch.bfloat16, pe=True)
-    assert lay.pe0 >= base.total - 256 and lay.pe0 % 256 == 0
-    assert lay.total >= lay.pe0 + 2 * 40 * 30 * 64 * 4
+    fused = P.workspace_layout(2, 2, 40, 30, 32, 3, 8, torch.bfloat16, pe=True)
+    assert fused.pe0 == 0 and fused.total == base.total
+    for K, H, L in ((20, 40, 3), (8, 1, 3), (8, 20, 1)):       # wide slots, one row, one level
+        base = P.workspace_layout(2, 2, H, 30, 32, L, K, torch.bfloat16)
+        lay = P.workspace_layout(2, 2, H, 30, 32, L, K, torch.bfloat16, pe=True)
+        assert lay.pe0 >= base.total - 256 and lay.pe0 % 256 == 0
+        assert lay.total >= lay.pe0 + 2 * H * 30 * 64 * 4
     single = P.workspace_layout(1, 1, 16, 16, 32, 1, 4, torch.float32, pe=True)
     assert single.total >= 16 * 16 * 32 * 4
 
