@@ -245,18 +245,21 @@ def test_forward_ex_validation():
 
 
 def test_position_encoding_workspace():
-    """Level 0's encoding is fused into the finest kernel on maps of more than one row when
-    4*K_1 <= 64 (no workspace buffer); otherwise the workspace adds it, fp32, after everything else."""
-    base = P.workspace_layout(2, 2, 40, 30, 32, 3, 8, torch.bfloat16)
-    fused = P.workspace_layout(2, 2, 40, 30, 32, 3, 8, torch.bfloat16, pe=True)
-    assert fused.pe0 == 0 and fused.total == base.total
-    for K, H, L in ((20, 40, 3), (8, 1, 3), (8, 20, 1)):       # wide slots, one row, one level
+    """Level 0's encoding is computed inside the kernel that produces level 0's message (no workspace
+    buffer) on maps of more than one row when 4*K_1 <= 64, and for a single level when the map takes
+    the tiled coarse kernel (more than 64 tokens); otherwise the workspace adds it, fp32, after
+    everything else."""
+    for H, L in ((40, 3), (20, 1)):
+        base = P.workspace_layout(2, 2, H, 30, 32, L, 8, torch.bfloat16)
+        fused = P.workspace_layout(2, 2, H, 30, 32, L, 8, torch.bfloat16, pe=True)
+        assert fused.pe0 == 0 and fused.total == base.total
+    for K, H, L in ((20, 40, 3), (8, 1, 3), (8, 2, 1)):       # wide slots, one row, one level of 60 tokens
         base = P.workspace_layout(2, 2, H, 30, 32, L, K, torch.bfloat16)
         lay = P.workspace_layout(2, 2, H, 30, 32, L, K, torch.bfloat16, pe=True)
         assert lay.pe0 >= base.total - 256 and lay.pe0 % 256 == 0
         assert lay.total >= lay.pe0 + 2 * H * 30 * 64 * 4
-    single = P.workspace_layout(1, 1, 16, 16, 32, 1, 4, torch.float32, pe=True)
-    assert single.total >= 16 * 16 * 32 * 4
+    single = P.workspace_layout(1, 1, 8, 8, 32, 1, 4, torch.float32, pe=True)       # 64 tokens: not fused
+    assert single.total >= 8 * 8 * 32 * 4
 
 
 def test_epipolar_layout_is_that_of_one_row_maps():
