@@ -517,9 +517,13 @@ done:
  *   - pyramid (Sec. 3.2): a pooled token is the mean of its n valid children, so each child
  *     receives 1/n of the pooled token's gradient (the storage rounding of pooled values is taken
  *     as the identity).
+ *   - multiscale position encoding (Sec. 3.2): each level's message received the 3x3 depth-wise
+ *     cross-correlation of V^l plus a bias, so its kernels and bias get the gradient dm^l correlated
+ *     with V^l (and summed), and V^l gets dm^l convolved with the kernels (the transposed stencil);
+ *   - caller-supplied V levels are inputs of their own: their gradients are returned per level and
+ *     do not flow down the V pyramid.
  * The levels are processed finest first, so that QuadTree-A's score gradients reach the coarser
- * level that produced the scores. Caller-supplied V levels and the position encoding are not
- * covered (return -1).
+ * level that produced the scores.
  *
  * Return codes as qo_forward.
  */
@@ -530,13 +534,16 @@ typedef struct {
     double* dk;
     double* dv;
     double* dw;                   /* B with w given: [B][H*W][heads][L]; otherwise not written    */
+    double* dpe_weight;           /* with a position encoding: [L][C][3][3], or NULL              */
+    double* dpe_bias;             /* with a position encoding: [L][C], or NULL                    */
+    double* const* dv_levels;     /* with given V levels: entry l in 1..L-1, [B][H_l][W_l][C]     */
 } qo_backward_args;
 
 int qo_backward(const qo_backward_args* ba)
 {
     if (!ba || !ba->dout || !ba->dq || !ba->dk || !ba->dv) return -1;
     const qo_forward_args* a = &ba->fwd;
-    if (a->v_levels || a->pe_weight) return -1;
+    if (a->v_levels && !ba->dv_levels) return -1;
     const int B = a->B, NH = a->heads, H = a->H, W = a->W, d = a->d, L = a->L, K = a->K;
     if (B <= 0 || NH <= 0 || d <= 0 || K <= 0) return -1;
     int Hl[QO_MAX_LEVELS], Wl[QO_MAX_LEVELS];
@@ -796,7 +803,37 @@ int qo_backward(const qo_backward_args* ba)
             }
         }
 
-    /* pyramid: each pooled token hands 1/n of its gradient to each of its n valid children */
+    /* multiscale position encoding: the message of every level-l token received
+     * e_i[c] = b[c] + sum over the window of w[c][tap] * V^l(i + tap)[c] (zero outside the map), so
+     * db[c] = sum_i dm_i[c], dw[c][tap] = sum_i dm_i[c] * V^l(i + tap)[c] and each window token
+     * receives w[c][tap] * dm_i[c] in its value gradient */
+    if (a->pe_weight) {
+        if (ba->dpe_weight) memset(ba->dpe_weight, 0, sizeof(double) * (size_t)L * C * 9);
+        if (ba->dpe_bias) memset(ba->dpe_bias, 0, sizeof(double) * (size_t)L * C);
+        for (int l = 0; l < L; ++l) {
+            const int Hh = Hl[l], Ww = Wl[l];
+            for (int b = 0; b < B; ++b)
+                for (int y = 0; y < Hh; ++y)
+                    for (int x = 0; x < Ww; ++x)
+                        for (int c = 0; c < C; ++c) {
+                            const double g = dm[l][((size_t)b * Nl[l] + (size_t)y * Ww + x) * C + c];
+                            const float* kw = a->pe_weight + ((size_t)l * C + c) * 9;
+                            if (ba->dpe_bias) ba->dpe_bias[(size_t)l * C + c] += g;
+                            for (int ky = 0; ky < 3; ++ky)
+                                for (int kx = 0; kx < 3; ++kx) {
+                                    const int yy = y + ky - 1, xx = x + kx - 1;
+                                    if (yy < 0 || yy >= Hh || xx < 0 || xx >= Ww) continue;
+                                    const size_t j = (((size_t)b * Hh + yy) * Ww + xx) * C + c;
+                                    if (ba->dpe_weight)
+                                        ba->dpe_weight[((size_t)l * C + c) * 9 + ky * 3 + kx] += g * (double)pv[l][j];
+                                    dV[l][j] += (double)kw[ky * 3 + kx] * g;
+                                }
+                        }
+        }
+    }
+
+    /* pyramid: each pooled token hands 1/n of its gradient to each of its n valid children (V only
+     * when its levels were pooled; given V levels keep their gradients) */
     for (int l = Lc; l >= 1; --l) {
         const int Hs = Hl[l - 1], Ws = Wl[l - 1];
         for (int b = 0; b < B; ++b)
@@ -811,7 +848,7 @@ int qo_backward(const qo_backward_args* ba)
                             for (int c = 0; c < C; ++c) {
                                 dQ[l - 1][dst + c] += dQ[l][src + c] * inv_n;
                                 dK[l - 1][dst + c] += dK[l][src + c] * inv_n;
-                                dV[l - 1][dst + c] += dV[l][src + c] * inv_n;
+                                if (!a->v_levels) dV[l - 1][dst + c] += dV[l][src + c] * inv_n;
                             }
                         }
                 }
@@ -819,6 +856,9 @@ int qo_backward(const qo_backward_args* ba)
     memcpy(ba->dq, dQ[0], sizeof(double) * (size_t)B * Nl[0] * C);
     memcpy(ba->dk, dK[0], sizeof(double) * (size_t)B * Nl[0] * C);
     memcpy(ba->dv, dV[0], sizeof(double) * (size_t)B * Nl[0] * C);
+    if (a->v_levels)
+        for (int l = 1; l < L; ++l)
+            if (ba->dv_levels[l]) memcpy(ba->dv_levels[l], dV[l], sizeof(double) * (size_t)B * Nl[l] * C);
 
 done:
     for (int l = 0; l < QO_MAX_LEVELS; ++l) {

@@ -55,6 +55,7 @@ class _BwdArgs(ctypes.Structure):
         ("fwd", _Args),
         ("dout", ctypes.c_void_p),
         ("dq", ctypes.c_void_p), ("dk", ctypes.c_void_p), ("dv", ctypes.c_void_p), ("dw", ctypes.c_void_p),
+        ("dpe_weight", ctypes.c_void_p), ("dpe_bias", ctypes.c_void_p), ("dv_levels", ctypes.c_void_p),
     ]
 
 
@@ -221,11 +222,14 @@ def forward(q, k, v, *, levels: int, K, variant: str, dtype: str = "f32", w=None
 
 
 def backward(q, k, v, dout, *, levels: int, K, variant: str, dtype: str = "f32", w=None, scale=None,
-             forced=None) -> dict:
+             forced=None, v_levels=None, pe_weight=None, pe_bias=None) -> dict:
     """Gradients of ``sum(dout * out)`` with the kept-key sets held fixed (the oracle's own, or
-    ``forced`` as in ``forward``). ``dout``: float32 ``[B, H, W, heads, d]``. Returns float64
-    ``dq``, ``dk``, ``dv`` ``[B, H, W, heads, d]`` and, for QuadTree-B with ``w`` given, ``dw``
-    ``[B, H*W, heads, levels]`` (else None)."""
+    ``forced`` as in ``forward``). ``dout``: float32 ``[B, H, W, heads, d]``. ``v_levels``,
+    ``pe_weight``, ``pe_bias``: as in ``forward``. Returns float64 ``dq``, ``dk``, ``dv``
+    ``[B, H, W, heads, d]``; for QuadTree-B with ``w`` given, ``dw`` ``[B, H*W, heads, levels]``
+    (else None); with a position encoding ``dpe_weight`` ``[levels, heads*d, 3, 3]`` and ``dpe_bias``
+    ``[levels, heads*d]`` (else None); with given V levels ``dv_levels``, a list whose entry l >= 1 is
+    ``[B, H_l, W_l, heads, d]`` (else None)."""
     q = np.ascontiguousarray(q, dtype=np.float32)
     k = np.ascontiguousarray(k, dtype=np.float32)
     v = np.ascontiguousarray(v, dtype=np.float32)
@@ -257,6 +261,32 @@ def backward(q, k, v, dout, *, levels: int, K, variant: str, dtype: str = "f32",
         forced_tbl = _ptr_table(forced_arrays)
     dq, dk, dv = (np.zeros((B, H, W, NH, d), np.float64) for _ in range(3))
     dw = np.zeros((B, H * W, NH, L), np.float64) if (variant == "B" and wts is not None) else None
+    C = NH * d
+    keep = []
+    v_tbl = dvl_tbl = None
+    dvl = None
+    if v_levels is not None:
+        v_tbl = (ctypes.c_void_p * MAX_LEVELS)()
+        dvl_tbl = (ctypes.c_void_p * MAX_LEVELS)()
+        dvl = [None] + [np.zeros((B, dims[l][0], dims[l][1], NH, d), np.float64) for l in range(1, L)]
+        for l in range(1, L):
+            vl = np.ascontiguousarray(v_levels[l], dtype=np.float32)
+            assert vl.size == B * N[l] * C, (vl.shape, (B, dims[l][0], dims[l][1], NH, d))
+            keep.append(vl)
+            v_tbl[l] = vl.ctypes.data
+            dvl_tbl[l] = dvl[l].ctypes.data
+    dpw = dpb = None
+    if pe_weight is not None:
+        pw = np.ascontiguousarray(pe_weight, dtype=np.float32)
+        assert pw.shape == (L, C, 3, 3), pw.shape
+        keep.append(pw)
+        dpw = np.zeros((L, C, 3, 3), np.float64)
+        dpb = np.zeros((L, C), np.float64)
+        pb = None
+        if pe_bias is not None:
+            pb = np.ascontiguousarray(pe_bias, dtype=np.float32)
+            assert pb.shape == (L, C), pb.shape
+            keep.append(pb)
     args = _BwdArgs()
     f = args.fwd
     f.q, f.k, f.v = q.ctypes.data, k.ctypes.data, v.ctypes.data
@@ -270,7 +300,16 @@ def backward(q, k, v, dout, *, levels: int, K, variant: str, dtype: str = "f32",
     args.dout = g.ctypes.data
     args.dq, args.dk, args.dv = dq.ctypes.data, dk.ctypes.data, dv.ctypes.data
     args.dw = dw.ctypes.data if dw is not None else None
+    if v_tbl is not None:
+        f.v_levels = ctypes.addressof(v_tbl)
+        args.dv_levels = ctypes.addressof(dvl_tbl)
+    if pe_weight is not None:
+        f.pe_weight = pw.ctypes.data
+        f.pe_bias = pb.ctypes.data if pb is not None else None
+        args.dpe_weight = dpw.ctypes.data
+        args.dpe_bias = dpb.ctypes.data
     rc = _load().qo_backward(ctypes.byref(args))
     if rc != 0:
         raise RuntimeError(f"oracle backward failed with code {rc}")
-    return {"dq": dq, "dk": dk, "dv": dv, "dw": dw}
+    return {"dq": dq, "dk": dk, "dv": dv, "dw": dw, "dpe_weight": dpw, "dpe_bias": dpb if pe_bias is not None else None,
+            "dv_levels": dvl}

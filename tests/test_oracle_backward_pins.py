@@ -198,3 +198,130 @@ def test_backward_forced_selection_is_the_oracle_choice():
         b = O.backward(q, k, v, g, levels=3, K=3, variant=variant, forced=f)
         for name in ("dq", "dk", "dv"):
             assert np.array_equal(a[name], b[name])
+
+
+# ---------------------------------------------------------------- position encoding and given V levels
+
+PE_CASES = [
+    # variant, B, H, W, heads, d, L, K, with_w, pe, vgiven
+    ("B", 1, 6, 7, 2, 4, 3, 2, True, True, False),
+    ("A", 1, 7, 6, 1, 4, 3, 2, False, True, False),
+    ("B", 1, 6, 7, 2, 4, 3, 2, True, False, True),
+    ("A", 2, 5, 6, 1, 4, 3, 2, False, False, True),
+    ("B", 1, 9, 8, 1, 4, 4, [0, 3, 1, 2], True, True, True),
+    ("A", 1, 4, 5, 2, 4, 1, 3, False, True, False),         # one level
+    ("B", 2, 1, 11, 1, 4, 3, 2, False, True, True),         # one-row maps
+]
+
+
+@pytest.mark.parametrize("variant,B,H,W,heads,d,L,K,with_w,pe,vgiven", PE_CASES)
+def test_backward_with_position_encoding_and_given_v_matches_finite_differences(variant, B, H, W, heads, d, L, K,
+                                                                                with_w, pe, vgiven):
+    """The gradients of the multiscale position encoding's kernels and bias, of caller-supplied V levels,
+    and of q, k, v, w with either present, against central differences of the forward (kept keys forced,
+    dyadic inputs, step 2^-12)."""
+    rng = np.random.default_rng(B * 1000 + H * 10 + W + L + 3 * pe + 7 * vgiven)
+    q, k, v, g = (dyadic(rng, (B, H, W, heads, d)) for _ in range(4))
+    C = heads * d
+    w = (rng.integers(1, 64, size=(B, H * W, heads, L)) / 64.0).astype(np.float32) if with_w else None
+    dims = O.level_dims(H, W, L)
+    vl = [None] + [dyadic(rng, (B, dims[l][0], dims[l][1], heads, d)) for l in range(1, L)] if vgiven else None
+    pw = dyadic(rng, (L, C, 3, 3), -32, 33) if pe else None
+    pb = dyadic(rng, (L, C), -32, 33) if pe else None
+    forced = O.forward(q, k, v, levels=L, K=K, variant=variant, w=w, v_levels=vl, pe_weight=pw,
+                       pe_bias=pb)["sel_idx"]
+    grads = O.backward(q, k, v, g, levels=L, K=K, variant=variant, w=w, forced=forced, v_levels=vl, pe_weight=pw,
+                       pe_bias=pb)
+    inputs = {"q": q, "k": k, "v": v, "w": w, "pw": pw, "pb": pb, "vl": vl}
+
+    def loss(args):
+        r = O.forward(args["q"], args["k"], args["v"], levels=L, K=K, variant=variant, w=args["w"], forced=forced,
+                      v_levels=args["vl"], pe_weight=args["pw"], pe_bias=args["pb"])
+        return float((r["out"] * g).sum())
+
+    tensors = [("q", None, q, grads["dq"]), ("k", None, k, grads["dk"]), ("v", None, v, grads["dv"])]
+    if with_w:
+        tensors.append(("w", None, w, grads["dw"]))
+    if pe:
+        tensors += [("pw", None, pw, grads["dpe_weight"]), ("pb", None, pb, grads["dpe_bias"])]
+    else:
+        assert grads["dpe_weight"] is None
+    if vgiven:
+        tensors += [("vl", l, vl[l], grads["dv_levels"][l]) for l in range(1, L)]
+    else:
+        assert grads["dv_levels"] is None
+
+    for name, lev, arr, grad in tensors:
+        assert grad is not None and grad.shape == arr.shape, name
+        scale_g = max(np.abs(grad).max(), 1e-3)
+
+        def at(delta):
+            args = dict(inputs)
+            if lev is None:
+                args[name] = (arr + delta).astype(np.float32)
+            else:
+                args["vl"] = list(vl)
+                args["vl"][lev] = (arr + delta).astype(np.float32)
+            return loss(args)
+
+        for _ in range(4):
+            idx = tuple(int(rng.integers(0, s)) for s in arr.shape)
+            e = np.zeros_like(arr)
+            e[idx] = EPS
+            fd = (at(e) - at(-e)) / (2 * EPS)
+            assert abs(fd - grad[idx]) <= 1e-7 * scale_g + 1e-9, (name, lev, idx, fd, grad[idx])
+        u = rng.integers(-1, 2, size=arr.shape).astype(np.float32)
+        fd = (at(EPS * u) - at(-EPS * u)) / (2 * EPS)
+        exact = float((grad * u).sum())
+        assert abs(fd - exact) <= 1e-6 * max(1.0, abs(exact)), (name, lev, fd, exact)
+
+
+def _torch_depthwise(x, wk, bias):
+    """[B,H,W,C] x [C,3,3] (+ [C]) -> the 3x3 depth-wise cross-correlation with zero padding, by torch."""
+    C = x.shape[-1]
+    y = torch.nn.functional.conv2d(x.permute(0, 3, 1, 2), wk.reshape(C, 1, 3, 3), bias=bias, padding=1, groups=C)
+    return y.permute(0, 2, 3, 1)
+
+
+@pytest.mark.parametrize("vgiven", [False, True])
+@pytest.mark.parametrize("H,W,L", [(8, 8, 3), (7, 10, 3)])
+def test_backward_b_every_key_kept_with_encoding_is_autograd_of_the_closed_form(vgiven, H, W, L):
+    """QuadTree-B keeping every key, with the position encoding and pooled or given V levels: out =
+    sum_l w_l * (dense attention of level l + depth-wise conv of V^l), broadcast to the finest tokens;
+    every gradient (q, k, v, w, the kernels, the bias, the given V levels) by torch autograd in float64
+    of that formula, with torch's own conv2d for the encoding."""
+    rng = np.random.default_rng(16 + vgiven)
+    B, NH, d = 1, 2, 4
+    C = NH * d
+    q, k, v, g = (dyadic(rng, (B, H, W, NH, d)) for _ in range(4))
+    w = rng.random((B, H * W, NH, L)).astype(np.float32)
+    dims = O.level_dims(H, W, L)
+    vl = [None] + [dyadic(rng, (B, dims[l][0], dims[l][1], NH, d)) for l in range(1, L)] if vgiven else None
+    pw = dyadic(rng, (L, C, 3, 3), -32, 33)
+    pb = dyadic(rng, (L, C), -32, 33)
+    tau = 0.5
+    leaves = [torch.tensor(x, dtype=torch.float64, requires_grad=True) for x in (q, k, v, w, pw, pb)]
+    tvl = [None] + [torch.tensor(vl[l], dtype=torch.float64, requires_grad=True) for l in range(1, L)] if vgiven else None
+    tq, tk, tv, tw, tpw, tpb = leaves
+    xq, xk, xv = (t.reshape(B, H, W, C) for t in (tq, tk, tv))
+    out = torch.zeros((B, H, W, NH, d), dtype=torch.float64)
+    ys, xs = torch.arange(H), torch.arange(W)
+    for l in range(L):
+        if l >= 1 and vgiven:
+            xv = tvl[l].reshape(B, dims[l][0], dims[l][1], C)
+        Hl, Wl = xq.shape[1], xq.shape[2]
+        m = _torch_dense(xq.reshape(B, Hl * Wl, NH, d), xk.reshape(B, Hl * Wl, NH, d),
+                         xv.reshape(B, Hl * Wl, NH, d), tau).reshape(B, Hl, Wl, NH, d)
+        m = m + _torch_depthwise(xv, tpw[l], tpb[l]).reshape(B, Hl, Wl, NH, d)
+        anc = m[:, (ys >> l)][:, :, (xs >> l)]
+        out = out + tw[..., l].reshape(B, H, W, NH, 1) * anc
+        xq, xk = _torch_pool(xq), _torch_pool(xk)
+        if not vgiven:
+            xv = _torch_pool(xv)
+    (out * torch.tensor(g, dtype=torch.float64)).sum().backward()
+    r = O.backward(q, k, v, g, levels=L, K=64, variant="B", w=w, scale=tau, v_levels=vl, pe_weight=pw, pe_bias=pb)
+    for name, t in (("dq", tq), ("dk", tk), ("dv", tv), ("dw", tw), ("dpe_weight", tpw), ("dpe_bias", tpb)):
+        np.testing.assert_allclose(r[name], t.grad.numpy(), atol=1e-11, rtol=0, err_msg=name)
+    if vgiven:
+        for l in range(1, L):
+            np.testing.assert_allclose(r["dv_levels"][l], tvl[l].grad.numpy(), atol=1e-11, rtol=0)
