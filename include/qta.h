@@ -157,6 +157,12 @@ qta_status qta_forward(const void* q, const void* k, const void* v, const float*
  *              run there, each right after its level's query pass, beside the finest key pass on
  *              aux_stream and the coarse level on `stream`; ordered and joined like aux_stream.
  *              NULL: those go to aux_stream or `stream`, whichever keeps the coarse level busier.
+ *   dpe_weight, dpe_bias, dv_levels  outputs of qta_backward_ex only (the forward ignores them): with
+ *              pe_weight, dpe_weight (device fp32 [levels][heads*d][3][3], 16-byte aligned) receives the
+ *              gradient of the encoding's kernels, and with pe_bias, dpe_bias (device fp32
+ *              [levels][heads*d]) that of its bias; with v_levels, dv_levels (host array of device
+ *              pointers, entry l >= 1 fp32 [B][H_l][W_l][heads][d], 16-byte aligned) receives the
+ *              gradient of each given V level. Required when their input is given; overwritten.
  */
 typedef struct {
     const int* K_levels;
@@ -166,6 +172,9 @@ typedef struct {
     int epipolar;
     void* aux_stream;
     void* aux_stream2;
+    float* dpe_weight;
+    float* dpe_bias;
+    float* const* dv_levels;
 } qta_options;
 
 /* Workspace of qta_forward_ex with these options (layout and byte count as for qta_forward). With a
@@ -225,10 +234,13 @@ qta_status qta_forward_ex_noalloc(const void* q, const void* k, const void* v, c
  *                not computed); not touched otherwise.
  *   bwd_workspace  device memory of qta_backward_workspace_bytes_ex bytes, 256-byte aligned; its
  *                contents need not be preserved between calls.
- * Unsupported (QTA_ERR_UNSUPPORTED): caller-supplied V levels, the position encoding, and K_l with
- * 4*K_l > 64 at any level. Some sums (the message gradients of levels >= 2, and each key's list of
- * the parents that kept it) are ordered by atomics, so the last bits may vary between runs. Options
- * as in qta_forward_ex.
+ * With caller-supplied V levels (opt->v_levels) their gradients go to opt->dv_levels and do not
+ * flow into dv; with the position encoding (opt->pe_weight, Sec. 3.2) V's gradient also receives the
+ * encoding's transposed stencil at every level, and opt->dpe_weight / opt->dpe_bias the gradients of
+ * its kernels and bias. Unsupported (QTA_ERR_UNSUPPORTED): K_l with 4*K_l > 64 at any level, and the
+ * encoding with heads*d > 1024. Some sums (the message gradients of levels >= 2, and each key's list
+ * of the parents that kept it) are ordered by atomics, so the last bits may vary between runs.
+ * Options as in qta_forward_ex.
  */
 size_t qta_backward_workspace_bytes_ex(int B, int heads, int H, int W, int d, int levels, int K,
                                        qta_variant variant, qta_dtype dtype, const qta_options* opt);

@@ -1198,7 +1198,8 @@ __global__ __launch_bounds__(256) void bwd_unpool_kernel(BwdUnpoolArgs a)
                            static_cast<uint32_t>((yl * a.W[l] + xl) * a.C + 4 * ch);
         g[l][0] = *reinterpret_cast<const float4*>(a.gq[l] + off);
         g[l][1] = *reinterpret_cast<const float4*>(a.gk[l] + off);
-        g[l][2] = *reinterpret_cast<const float4*>(a.gv[l] + off);
+        // given V levels are not pooled from v: their gradients are returned as they are
+        g[l][2] = a.v_pooled ? *reinterpret_cast<const float4*>(a.gv[l] + off) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     const int H0 = a.H[0], W0 = a.W[0];
     const size_t base = static_cast<size_t>(b) * static_cast<uint32_t>(H0 * W0 * a.C) + 4 * ch;

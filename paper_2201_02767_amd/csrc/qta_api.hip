@@ -226,11 +226,12 @@ struct BwdLayout {
     size_t count[QTA_MAX_LEVELS], off[QTA_MAX_LEVELS], coff[QTA_MAX_LEVELS], block_sums[QTA_MAX_LEVELS];
     size_t entries[QTA_MAX_LEVELS], slot[QTA_MAX_LEVELS], chunk_key[QTA_MAX_LEVELS], partial[QTA_MAX_LEVELS];
     size_t qstats[QTA_MAX_LEVELS];
+    size_t pe_part;                 // with the position encoding: the per-block partial sums of its gradients
     long long nslots_max;           // B*heads*N_{l+1} over the finer levels
 };
 
 void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int d, int levels, const int* Kl, bool va,
-                BwdLayout* L)
+                bool pe, BwdLayout* L)
 {
     *L = BwdLayout{};
     const int c = levels - 1;
@@ -288,7 +289,11 @@ void bwd_layout(int B, int heads, const int* Hl, const int* Wl, int C, int d, in
         L->qstats[l] = off;
         off = align_up(off + static_cast<size_t>(st) * sizeof(float));
     }
-    L->total = off;
+    if (pe) {
+        L->pe_part = off;
+        off = align_up(off + static_cast<size_t>(posenc_bwd_blocks(B, Hl, Wl, levels, C)) * C * 10 * sizeof(float));
+    }
+    L->total = off > kAlign ? off : kAlign;
 }
 
 }  // namespace
@@ -782,7 +787,7 @@ size_t qta_backward_workspace_bytes_ex(int B, int heads, int H, int W, int d, in
     if (layout(B, heads, H, W, d, levels, o.Kl, o.v_levels != nullptr, o.pe_weight != nullptr, dtype, &L) != QTA_OK)
         return 0;
     BwdLayout G;
-    bwd_layout(B, heads, L.H, L.W, heads * d, d, levels, o.Kl, variant == QTA_VARIANT_A, &G);
+    bwd_layout(B, heads, L.H, L.W, heads * d, d, levels, o.Kl, variant == QTA_VARIANT_A, o.pe_weight != nullptr, &G);
     return G.total;
 }
 
@@ -808,9 +813,21 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     Options o;
     st = read_options(K, levels, opt, &o);
     if (st != QTA_OK) return st;
-    if (o.v_levels || o.pe_weight) return QTA_ERR_UNSUPPORTED;
+    const bool v_supplied = o.v_levels != nullptr;
+    const bool pe = o.pe_weight != nullptr;
+    if (v_supplied) {
+        if (!opt->dv_levels) return QTA_ERR_INVALID;
+        for (int l = 1; l < levels && l < QTA_MAX_LEVELS; ++l)
+            if (!o.v_levels[l] || !aligned16(o.v_levels[l]) || !opt->dv_levels[l] || !aligned16(opt->dv_levels[l]))
+                return QTA_ERR_INVALID;
+    }
+    if (pe) {
+        if (!opt->dpe_weight || !aligned16(opt->dpe_weight)) return QTA_ERR_INVALID;
+        if (o.pe_bias && !opt->dpe_bias) return QTA_ERR_INVALID;
+        if (static_cast<long long>(heads) * d > 1024) return QTA_ERR_UNSUPPORTED;
+    }
     qta_workspace_layout L;
-    st = layout(B, heads, H, W, d, levels, o.Kl, false, false, dtype, &L);
+    st = layout(B, heads, H, W, d, levels, o.Kl, v_supplied, pe, dtype, &L);
     if (st != QTA_OK) return st;
     const int* Kl = o.Kl;
     for (int l = 1; l < levels; ++l)
@@ -822,7 +839,7 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     const bool va = variant == QTA_VARIANT_A;
     const int C = heads * d;
     BwdLayout G;
-    bwd_layout(B, heads, L.H, L.W, C, d, levels, Kl, va, &G);
+    bwd_layout(B, heads, L.H, L.W, C, d, levels, Kl, va, pe, &G);
     if (G.nslots_max >= 0x7FFFFFFFLL / 64) return QTA_ERR_UNSUPPORTED;     // sort indices are int
     if (!bwd_workspace || (reinterpret_cast<uintptr_t>(bwd_workspace) & (kAlign - 1)) != 0) return QTA_ERR_INVALID;
     if (bwd_workspace_bytes < G.total) return QTA_ERR_WORKSPACE;
@@ -862,6 +879,10 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     auto fptr = [&](size_t off) { return reinterpret_cast<float*>(gws + off); };
     auto sidx = [&](int l) { return reinterpret_cast<const int32_t*>(ws + L.sel_idx[l]); };
     auto skey = [&](int l) { return reinterpret_cast<const float*>(ws + L.sel_key[l]); };
+    // V at level l >= 1 (given levels are the caller's), and where its gradient goes (given levels:
+    // the caller's dv_levels, which the pyramid adjoint then leaves alone)
+    auto vlev = [&](int l) -> const void* { return v_supplied ? o.v_levels[l] : ws + L.v[l]; };
+    auto gvlev = [&](int l) -> float* { return v_supplied ? opt->dv_levels[l] : fptr(G.gv[l]); };
     const int c = levels - 1;
     if (only_finest && levels < 2) return QTA_ERR_INVALID;
 
@@ -903,14 +924,14 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
             } else {
                 a.q = ws + L.q[l];
                 a.k = ws + L.k[l];
-                a.v = ws + L.v[l];
+                a.v = vlev(l);
                 a.blocked = L.blocked[l] != 0;
                 a.sel_idx = sidx(l);
                 a.dsig_in = va ? fptr(G.dsig[l]) : nullptr;
                 a.dm = fptr(G.dm[l]);
                 a.dq = fptr(G.gq[l]);
                 a.dk = fptr(G.gk[l]);
-                a.dv = fptr(G.gv[l]);
+                a.dv = gvlev(l);
             }
             a.B = B;
             a.heads = heads;
@@ -984,25 +1005,55 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
         } else {
             a.q = ws + L.q[c];
             a.k = ws + L.k[c];
-            a.v = ws + L.v[c];
+            a.v = vlev(c);
             a.K = Kl[c];
             a.sel_idx = sidx(c);
             a.dsig = va ? fptr(G.dsig[c]) : nullptr;
             a.dm = fptr(G.dm[c]);
             a.dq = fptr(G.gq[c]);
             a.dk = fptr(G.gk[c]);
-            a.dv = fptr(G.gv[c]);
+            a.dv = gvlev(c);
         }
         if (launch_bwd_coarse(a, d, va, use_bf16, s) != hipSuccess) return QTA_ERR_HIP;
     }
-    if (levels == 1) return QTA_OK;
+    // the position encoding's backward (every level, once all of the level's v gradients are
+    // written; before the unpooling, which reads them)
+    auto posenc_bwd = [&]() -> hipError_t {
+        PosEncBwdArgs p{};
+        p.nlev = levels;
+        p.B = B;
+        p.heads = heads;
+        p.d = d;
+        p.variant_b = va ? 0 : 1;
+        p.dout = dout;
+        p.w = va ? nullptr : w;
+        p.part = fptr(G.pe_part);
+        p.dweight = opt->dpe_weight;
+        p.dbias = o.pe_bias ? opt->dpe_bias : nullptr;
+        p.bias0 = o.pe_bias;
+        p.dw = dw_out;
+        for (int l = 0; l < levels; ++l) {
+            PosEncBwdLevel& e = p.lv[l];
+            e.v = l == 0 ? v : vlev(l);
+            e.blocked = l == 0 ? 0 : L.blocked[l];
+            e.H = L.H[l];
+            e.W = L.W[l];
+            e.dm = l == 0 ? nullptr : fptr(G.dm[l]);
+            e.dv = l == 0 ? dv : gvlev(l);
+            e.weight = o.pe_weight + static_cast<size_t>(l) * C * 9;
+        }
+        return launch_posenc_bwd(p, use_bf16, s);
+    };
+    if (levels == 1) return (pe && posenc_bwd() != hipSuccess) ? QTA_ERR_HIP : QTA_OK;
     for (int i = 0; i < ndeferred; ++i)
         if (launch_bwd_keys(deferred[i].a, deferred[i].sc, d, va, use_bf16, false, s) != hipSuccess) return QTA_ERR_HIP;
     if (s2 != s && !after(s2, s)) return QTA_ERR_HIP;       // the key passes before the unpooling
     if (s3 != s && !after(s3, s)) return QTA_ERR_HIP;
+    if (pe && posenc_bwd() != hipSuccess) return QTA_ERR_HIP;
 
     // 4. pyramids
     BwdUnpoolArgs u{};
+    u.v_pooled = v_supplied ? 0 : 1;
     u.B = B;
     u.C = C;
     u.L = levels;
@@ -1012,7 +1063,7 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
         if (l >= 1) {
             u.gq[l] = fptr(G.gq[l]);
             u.gk[l] = fptr(G.gk[l]);
-            u.gv[l] = fptr(G.gv[l]);
+            u.gv[l] = v_supplied ? nullptr : fptr(G.gv[l]);
         }
     }
     u.dq = dq;

@@ -156,6 +156,49 @@ struct PosEncArgs {
     int B, heads, d;
 };
 
+// Backward of the multiscale position encoding, every level in one launch: with dm^l the gradient of
+// level l's message, V^l receives the transposed stencil of dm^l (added to dv), and the kernels and
+// bias the per-block partial sums of dm^l correlated with V^l (reduced by launch_posenc_bwd's
+// second kernel into dweight / dbias).
+struct PosEncBwdLevel {
+    const void* v;              // V^l (storage type), NHWC or parent-blocked
+    int blocked;
+    int H, W;
+    const float* dm;            // fp32 [B][H*W][heads][d]; NULL at level 0 (dout and w are used)
+    float* dv;                  // fp32 [B][H*W][heads][d]: += the transposed stencil of dm
+    const float* weight;        // fp32 [C][3][3] of this level
+};
+
+struct PosEncBwdArgs {
+    PosEncBwdLevel lv[QTA_MAX_LEVELS];
+    long long start[QTA_MAX_LEVELS + 1];    // first work item of each level (set by the launcher)
+    long long level_end[QTA_MAX_LEVELS];
+    int nlev, B, heads, d;
+    int variant_b;
+    const void* dout;           // level 0: dm^0 = w_{i,0} * dout_i (B with w), dout_i / L (B without), dout_i (A)
+    const float* w;             // fp32 [B][H*W][heads][L] or NULL
+    float* part;                // per block of the first kernel: [C][10] partial sums (9 taps, then the bias)
+    float* dweight;             // fp32 [L][C][3][3]
+    float* dbias;               // fp32 [L][C], or NULL
+    const float* bias0;         // level 0's bias fp32 [C], or NULL
+    float* dw;                  // B with w: fp32 [B][H*W][heads][L], += <dout_i, level 0's encoding at i>; or NULL
+};
+
+// Work items (4 channels of 4 neighbouring tokens of one row) of one level of the encoding passes,
+// and the 256-thread blocks of the backward's first kernel (every level starts on a block boundary).
+constexpr int kPosEncTokens = 4;
+constexpr int kPosEncThreads = 256;
+inline long long posenc_items(int B, int H, int W, int C)
+{
+    return static_cast<long long>(B) * H * ((W + kPosEncTokens - 1) / kPosEncTokens) * (C / 4);
+}
+inline long long posenc_bwd_blocks(int B, const int* Hl, const int* Wl, int levels, int C)
+{
+    long long n = 0;
+    for (int l = 0; l < levels; ++l) n += (posenc_items(B, Hl[l], Wl[l], C) + kPosEncThreads - 1) / kPosEncThreads;
+    return n;
+}
+
 // ---- backward pass (gradients with the kept-key sets held fixed) ----
 
 // Backward of one finer level l (0 <= l < L-1), in two passes. Query pass: one wave per (parent
@@ -246,6 +289,7 @@ struct BwdCoarseArgs {
 
 // Adds to the level-0 gradients every coarser level's, split evenly among valid children.
 struct BwdUnpoolArgs {
+    int v_pooled;               // 0: V's coarser levels were given (their gradients stay there)
     int B, C, L;
     int H[QTA_MAX_LEVELS], W[QTA_MAX_LEVELS];
     FastDiv div_cpt, div_W1;    // divisions by C/4 and W[1]; set by the launcher
@@ -317,6 +361,7 @@ inline hipError_t set_max_lds_once(const void* fn, std::atomic<unsigned long lon
 hipError_t launch_pyramid_pass(const PyramidPassArgs& a, int nlev, int ntensors, bool use_bf16, hipStream_t stream);
 hipError_t launch_coarse_attn(const CoarseArgs& a, int d, bool variant_a, bool use_bf16, hipStream_t stream);
 hipError_t launch_posenc(const PosEncArgs& a, bool use_bf16, hipStream_t stream);
+hipError_t launch_posenc_bwd(const PosEncBwdArgs& a, bool use_bf16, hipStream_t stream);
 hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest, hipStream_t stream);
 hipError_t launch_fine_attn_wide(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
                                  hipStream_t stream);

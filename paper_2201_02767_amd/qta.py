@@ -54,6 +54,9 @@ class Options(ctypes.Structure):
         ("epipolar", ctypes.c_int),
         ("aux_stream", ctypes.c_void_p),
         ("aux_stream2", ctypes.c_void_p),
+        ("dpe_weight", ctypes.c_void_p),
+        ("dpe_bias", ctypes.c_void_p),
+        ("dv_levels", ctypes.c_void_p),
     ]
 
 
@@ -364,9 +367,7 @@ class Plan:
     # ---- backward ----
     def _bwd_buffers(self, want_dw):
         if getattr(self, "_grads", None) is None:
-            opt = Options()
-            opt.K_levels = ctypes.addressof(self._k_tbl)
-            opt.epipolar = int(self.epipolar)
+            opt, keep = _layout_options(self.K_levels, self.levels, self.v_supplied, self.pe, self.epipolar)
             nbytes = lib().qta_backward_workspace_bytes_ex(
                 self.B, self.heads, self.H, self.W, self.d, self.levels,
                 self.K_levels[1] if self.levels > 1 else max(self.K_levels[0], 1), _VARIANTS[self.variant],
@@ -377,23 +378,39 @@ class Plan:
             self.bwd_workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
             self._grads = [torch.empty(shape, dtype=torch.float32, device=self.device) for _ in range(3)]
             self._dw = None
+            # the gradients of the position encoding and of given V levels (their own inputs)
+            C = self.heads * self.d
+            self.grad_extra = {}
+            if self.pe:
+                self.grad_extra["dpe_weight"] = torch.empty((self.levels, C, 3, 3), dtype=torch.float32,
+                                                            device=self.device)
+                self.grad_extra["dpe_bias"] = torch.empty((self.levels, C), dtype=torch.float32, device=self.device)
+            if self.v_supplied:
+                lay = self.layout
+                self.grad_extra["dv_levels"] = [None] + [
+                    torch.empty((self.mB, lay.H[l], lay.W[l], self.heads, self.d), dtype=torch.float32,
+                                device=self.device) for l in range(1, self.levels)]
         if want_dw and self._dw is None:
             self._dw = torch.empty((self.B, self.H * self.W, self.heads, self.levels), dtype=torch.float32,
                                    device=self.device)
         return self._grads, (self._dw if want_dw else None)
 
-    def _bwd_args(self, q, k, v, w, dout, stream, overlap=True):
-        if self.v_supplied or self.pe:
-            raise ValueError("the backward pass covers pooled V levels without a position encoding")
-        self._args(q, k, v, w, None, None, None)
+    def _bwd_args(self, q, k, v, w, dout, stream, overlap=True, v_levels=None, pe_weight=None, pe_bias=None):
+        opt, vtbl = self._args(q, k, v, w, v_levels, pe_weight, pe_bias)
         _require(dout, "dout", self.dtype, 5)
         if tuple(dout.shape) != (self.B, self.H, self.W, self.heads, self.d):
             raise ValueError(f"dout has shape {tuple(dout.shape)}")
         want_dw = self.variant == "B" and w is not None
         (dq, dk, dv), dw = self._bwd_buffers(want_dw)
-        opt = Options()
-        opt.K_levels = ctypes.addressof(self._k_tbl)
-        opt.epipolar = int(self.epipolar)
+        dvl_tbl = None
+        if self.pe:
+            opt.dpe_weight = self.grad_extra["dpe_weight"].data_ptr()
+            opt.dpe_bias = self.grad_extra["dpe_bias"].data_ptr()
+        if self.v_supplied:
+            dvl_tbl = (ctypes.c_void_p * MAX_LEVELS)()
+            for l in range(1, self.levels):
+                dvl_tbl[l] = self.grad_extra["dv_levels"][l].data_ptr()
+            opt.dv_levels = ctypes.addressof(dvl_tbl)
         if overlap:
             # the process's second and third streams on this device for the sorts and key passes
             # (the library orders them against the caller's stream)
@@ -404,25 +421,27 @@ class Plan:
                 _VARIANTS[self.variant], _DTYPES[self.dtype], _scale(self.scale), ctypes.byref(opt),
                 _ptr(self.workspace), self.workspace.numel(), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dw),
                 _ptr(self.bwd_workspace), self.bwd_workspace.numel(), stream)
-        return args, opt, (dq, dk, dv, dw)
+        return args, (opt, vtbl, dvl_tbl), (dq, dk, dv, dw)
 
-    def backward(self, q, k, v, dout, w=None, stream=None, overlap=True):
+    def backward(self, q, k, v, dout, w=None, stream=None, overlap=True, v_levels=None, pe_weight=None, pe_bias=None):
         """Gradients (dq, dk, dv, dw) in fp32 of the last ``run`` on the same inputs, for the upstream
         gradient ``dout`` (the kept keys of that run held fixed). ``dw`` is None unless QuadTree-B
-        with ``w``. The returned tensors are the plan's own buffers, overwritten by the next call.
-        ``overlap``: run the finest level's sort and key pass on a second stream and the coarser
-        levels' on a third (both one per device for the process), beside the query passes and the
-        coarse level (False: everything on the one stream)."""
+        with ``w``. With given V levels or a position encoding (pass the forward's ``v_levels``,
+        ``pe_weight``, ``pe_bias``), their gradients are in ``self.grad_extra``: ``dpe_weight``,
+        ``dpe_bias`` and ``dv_levels`` (entry l >= 1). The returned tensors are the plan's own
+        buffers, overwritten by the next call. ``overlap``: run the finest level's sort and key pass
+        on a second stream and the coarser levels' on a third (both one per device for the process),
+        beside the query passes and the coarse level (False: everything on the one stream)."""
         s = _stream(self.device) if stream is None else ctypes.c_void_p(stream)
-        args, opt, grads = self._bwd_args(q, k, v, w, dout, s, overlap)
+        args, opt, grads = self._bwd_args(q, k, v, w, dout, s, overlap, v_levels, pe_weight, pe_bias)
         _check("qta_backward_ex", lib().qta_backward_ex(*args))
         return grads
 
-    def prepare_backward(self, q, k, v, dout, w=None, finest_only=False):
+    def prepare_backward(self, q, k, v, dout, w=None, finest_only=False, v_levels=None, pe_weight=None, pe_bias=None):
         """Validate once and return a zero-argument callable that re-issues this backward on the
         current stream (``finest_only``: just its level-0 kernel, for timing it; the gradients are
         then no longer the layer's)."""
-        args, opt, grads = self._bwd_args(q, k, v, w, dout, _stream(self.device))
+        args, opt, grads = self._bwd_args(q, k, v, w, dout, _stream(self.device), True, v_levels, pe_weight, pe_bias)
         fn = lib().qta_backward_finest_ex if finest_only else lib().qta_backward_ex
         keep = (q, k, v, w, dout, opt, grads)
 

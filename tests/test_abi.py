@@ -299,8 +299,28 @@ def test_backward_validation():
     assert bwd(Kl=ctypes.addressof(_klv(0, 4, 20))) == UNSUPPORTED
     vt = (ctypes.c_void_p * 16)()
     vt[1] = vt[2] = FAKE
-    assert bwd(vtbl=ctypes.addressof(vt)) == UNSUPPORTED                    # given V levels
-    assert bwd(pw=FAKE) == UNSUPPORTED                                      # position encoding
+    # given V levels need somewhere to put their gradients, the encoding too
+    assert bwd(vtbl=ctypes.addressof(vt)) == INVALID                        # no dv_levels
+    assert bwd(pw=FAKE) == INVALID                                          # no dpe_weight
+    opt = P.qta.Options()
+    opt.v_levels = ctypes.addressof(vt)
+    dvl = (ctypes.c_void_p * 16)()
+    dvl[1] = FAKE
+    opt.dv_levels = ctypes.addressof(dvl)                                   # level 2's missing
+    assert lib.qta_backward_ex(FAKE, FAKE, FAKE, None, FAKE, 1, 1, 16, 16, 32, 3, 4, VA, F32, 0.0, ctypes.byref(opt),
+                               FAKE, 1 << 40, FAKE, FAKE, FAKE, None, FAKE, 1 << 40, None) == INVALID
+    opt = P.qta.Options()
+    opt.pe_weight = FAKE
+    opt.pe_bias = FAKE
+    opt.dpe_weight = FAKE                                                   # dpe_bias missing for a bias
+    assert lib.qta_backward_ex(FAKE, FAKE, FAKE, None, FAKE, 1, 1, 16, 16, 32, 3, 4, VA, F32, 0.0, ctypes.byref(opt),
+                               FAKE, 1 << 40, FAKE, FAKE, FAKE, None, FAKE, 1 << 40, None) == INVALID
+    opt.pe_bias = None
+    assert lib.qta_backward_ex(FAKE, FAKE, FAKE, None, FAKE, 1, 40, 16, 16, 32, 3, 4, VA, F32, 0.0,
+                               ctypes.byref(opt), FAKE, 1 << 40, FAKE, FAKE, FAKE, None, FAKE, 1 << 40,
+                               None) == UNSUPPORTED                         # the encoding with C > 1024
+    need_pe = lib.qta_backward_workspace_bytes_ex(1, 1, 16, 16, 32, 3, 4, VA, F32, ctypes.byref(opt))
+    assert need_pe > lib.qta_backward_workspace_bytes_ex(1, 1, 16, 16, 32, 3, 4, VA, F32, None)
     assert bwd(wsb=0) == WORKSPACE                                          # the forward's workspace
     assert bwd(gwsb=0) == WORKSPACE
     assert bwd(L=1, gwsb=0) == WORKSPACE                                    # one level still needs statistics

@@ -24,7 +24,8 @@ import pytest
 import torch
 
 import paper_2201_02767_amd as P
-from paper_2201_02767_amd.inputs import WORKLOADS, make_dout, make_level_weights, make_qkv, round_bf16
+from paper_2201_02767_amd.inputs import (WORKLOADS, make_dout, make_level_weights, make_pe, make_qkv, make_v_levels,
+                                         round_bf16)
 from oracle import oracle as O
 from tests.parity import TOL, rel_err, to_np
 
@@ -74,22 +75,31 @@ def dw_err(g, r, dout, msgs):
     return float((np.abs(np.asarray(g, np.float64) - r) / np.maximum(norm, 1e-30)).max())
 
 
-def run_backward(dev, q, k, v, g, *, levels, K, variant, dtype, w=None, scale=None, epipolar=False, label=""):
+def run_backward(dev, q, k, v, g, *, levels, K, variant, dtype, w=None, scale=None, epipolar=False, label="",
+                 v_levels=None, pe_weight=None, pe_bias=None):
+    """GPU backward against the oracle's, teacher-forced. ``v_levels`` (numpy list, entry l >= 1, in the
+    library's map layout: B*H one-row maps for epipolar attention), ``pe_weight``, ``pe_bias``: the
+    forward's given V levels and position encoding, whose gradients are compared too."""
     B, H, W, heads, d = q.shape
     announce(f"backward {label} B={B} H={H} W={W} heads={heads} d={d} L={levels} K={K} {variant} {dtype}"
-             f"{' epipolar' if epipolar else ''}")
+             f"{' epipolar' if epipolar else ''}{' V levels given' if v_levels is not None else ''}"
+             f"{' position encoding' if pe_weight is not None else ''}")
     plan = P.Plan(B, H, W, heads, d, levels=levels, K=K, variant=variant, dtype=TDT[dtype], device=dev, scale=scale,
-                  epipolar=epipolar)
+                  epipolar=epipolar, v_supplied=v_levels is not None, pe=pe_weight is not None)
     tq, tk, tv, tg = (dev_t(x, dtype, dev) for x in (q, k, v, g))
     tw = None if w is None else torch.from_numpy(w).to(dev)
-    plan.run(tq, tk, tv, tw)
-    dq, dk, dv, dw = plan.backward(tq, tk, tv, tg, tw)
+    tvl = None if v_levels is None else [None] + [dev_t(v_levels[l], dtype, dev) for l in range(1, levels)]
+    tpw = None if pe_weight is None else torch.from_numpy(np.ascontiguousarray(pe_weight)).to(dev)
+    tpb = None if pe_bias is None else torch.from_numpy(np.ascontiguousarray(pe_bias)).to(dev)
+    plan.run(tq, tk, tv, tw, v_levels=tvl, pe_weight=tpw, pe_bias=tpb)
+    dq, dk, dv, dw = plan.backward(tq, tk, tv, tg, tw, v_levels=tvl, pe_weight=tpw, pe_bias=tpb)
     torch.cuda.synchronize()
     sel = [None] + [to_np(plan.selection(l)[0]) for l in range(1, levels)]
     if epipolar:
         q, k, v, g = (x.reshape(B * H, 1, W, heads, d) for x in (q, k, v, g))
         w = None if w is None else w.reshape(B * H, W, heads, levels)
-    ref = O.backward(q, k, v, g, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale, forced=sel)
+    ref = O.backward(q, k, v, g, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale, forced=sel,
+                     v_levels=v_levels, pe_weight=pe_weight, pe_bias=pe_bias)
     errs, wide = {}, {}
     for name, t in (("dq", dq), ("dk", dk), ("dv", dv), ("dw", dw)):
         if ref[name] is None:
@@ -97,11 +107,23 @@ def run_backward(dev, q, k, v, g, *, levels, K, variant, dtype, w=None, scale=No
             continue
         g_ = to_np(t).reshape(ref[name].shape)
         if name == "dw":
-            fwd = O.forward(q, k, v, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale, forced=sel)
+            fwd = O.forward(q, k, v, levels=levels, K=K, variant=variant, dtype=dtype, w=w, scale=scale, forced=sel,
+                            v_levels=v_levels, pe_weight=pe_weight, pe_bias=pe_bias)
             errs[name] = dw_err(g_, ref[name], g, fwd["msg"])
         else:
             errs[name] = rel_err(g_, ref[name])
         wide[name] = grad_err(g_, ref[name])
+    # the position encoding's kernels (rows of 9 taps) and bias (rows of one level's channels), and the
+    # given V levels (rows of d channels), per row like dq, dk, dv
+    if pe_weight is not None:
+        L_, C_ = pe_weight.shape[:2]
+        errs["dpe_weight"] = rel_err(to_np(plan.grad_extra["dpe_weight"]).reshape(L_, C_, 9),
+                                     ref["dpe_weight"].reshape(L_, C_, 9))
+        if pe_bias is not None:
+            errs["dpe_bias"] = rel_err(to_np(plan.grad_extra["dpe_bias"]), ref["dpe_bias"])
+    if v_levels is not None:
+        errs["dv_levels"] = max(rel_err(to_np(plan.grad_extra["dv_levels"][l]).reshape(ref["dv_levels"][l].shape),
+                                        ref["dv_levels"][l]) for l in range(1, levels))
     announce(f"  gradient errors per row (dw: per element against the message bound) {errs}, tensor-wide {wide}")
     for name, e in errs.items():
         assert e <= (TOL[dtype] if name == "dw" else TOL_GRAD), f"{name} error {e}"
@@ -145,6 +167,55 @@ def test_backward_workload_full_size(dev, name):
     w = make_level_weights(wl) if wl.variant == "B" else None
     run_backward(dev, q, k, v, g, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w,
                  epipolar=wl.epipolar, label=name)
+
+
+@pytest.mark.parametrize("variant,dtype,B,H,W,heads,d,L,K,with_w,pe,vgiven", [
+    ("B", "f32", 1, 13, 11, 2, 32, 3, 3, True, True, False),
+    ("A", "bf16", 2, 25, 19, 2, 32, 4, 4, False, True, False),      # ragged, four levels, blocked levels
+    ("B", "bf16", 1, 31, 22, 3, 64, 3, 8, True, False, True),       # d = 64, given V levels
+    ("A", "f32", 1, 20, 24, 2, 32, 3, [0, 2, 16], False, True, True),
+    ("B", "bf16", 1, 9, 7, 1, 32, 2, 2, True, True, True),          # two levels
+    ("B", "f32", 2, 7, 9, 2, 32, 1, 4, True, True, False),          # one level
+    ("B", "f32", 1, 20, 21, 1, 32, 3, 4, False, True, False),       # B with w = 1/L
+])
+def test_backward_position_encoding_and_given_v(dev, variant, dtype, B, H, W, heads, d, L, K, with_w, pe, vgiven):
+    """Gradients of the multiscale position encoding's kernels and bias and of caller-supplied V levels,
+    with q, k, v, w, against the oracle's backward."""
+    seed = 500 + H * W + L
+    q, k, v, g = (rand(seed + i, (B, H, W, heads, d), dtype) for i in range(4))
+    rng = np.random.default_rng(seed)
+    w = rng.random((B, H * W, heads, L)).astype(np.float32) if with_w else None
+    dims = O.level_dims(H, W, L)
+    vl = [None] + [rand(seed + 10 + l, (B, dims[l][0], dims[l][1], heads, d), dtype) for l in range(1, L)] \
+        if vgiven else None
+    pw = (rng.standard_normal((L, heads * d, 3, 3)) * 0.3).astype(np.float32) if pe else None
+    pb = (rng.standard_normal((L, heads * d)) * 0.1).astype(np.float32) if pe else None
+    run_backward(dev, q, k, v, g, levels=L, K=K, variant=variant, dtype=dtype, w=w, label="pe/vgiven", v_levels=vl,
+                 pe_weight=pw, pe_bias=pb)
+
+
+@pytest.mark.parametrize("variant", ["A", "B"])
+def test_backward_position_encoding_epipolar(dev, variant):
+    """Attention along rows with the encoding (every level's pass runs separately on one-row maps)."""
+    q, k, v, g = (rand(600 + i, (2, 5, 37, 2, 32), "bf16") for i in range(4))
+    rng = np.random.default_rng(6)
+    w = rng.random((2, 5 * 37, 2, 4)).astype(np.float32) if variant == "B" else None
+    pw = (rng.standard_normal((4, 64, 3, 3)) * 0.3).astype(np.float32)
+    pb = (rng.standard_normal((4, 64)) * 0.1).astype(np.float32)
+    run_backward(dev, q, k, v, g, levels=4, K=3, variant=variant, dtype="bf16", w=w, epipolar=True, label="rows pe",
+                 pe_weight=pw, pe_bias=pb)
+
+
+@pytest.mark.parametrize("name", ["backbone_pe", "backbone_vgiven"])
+def test_backward_pe_and_vgiven_workloads_full_size(dev, name):
+    wl = WORKLOADS[name]
+    q, k, v = make_qkv(wl)
+    g = make_dout(wl)
+    w = make_level_weights(wl) if wl.variant == "B" else None
+    vl = make_v_levels(wl) if wl.v_given else None
+    pw, pb = make_pe(wl) if wl.pe else (None, None)
+    run_backward(dev, q, k, v, g, levels=wl.levels, K=wl.K, variant=wl.variant, dtype=wl.dtype, w=w, label=name,
+                 v_levels=vl, pe_weight=pw, pe_bias=pb)
 
 
 def test_backward_repeated_calls(dev):
