@@ -238,7 +238,7 @@ qta_status qta_forward_ex_noalloc(const void* q, const void* k, const void* v, c
  * flow into dv; with the position encoding (opt->pe_weight, Sec. 3.2) V's gradient also receives the
  * encoding's transposed stencil at every level, and opt->dpe_weight / opt->dpe_bias the gradients of
  * its kernels and bias. Unsupported (QTA_ERR_UNSUPPORTED): K_l with 4*K_l > 64 at any level, and the
- * encoding with heads*d > 1024. Some sums (the message gradients of levels >= 2, and each key's list
+ * encoding with heads*d > 256. Some sums (the message gradients of levels >= 2, and each key's list
  * of the parents that kept it) are ordered by atomics, so the last bits may vary between runs.
  * Options as in qta_forward_ex.
  */

@@ -139,203 +139,239 @@ __global__ __launch_bounds__(kThreads) void posenc_kernel(PosEncArgs a)
         if (x0 + t < L.W) *reinterpret_cast<float4*>(row + static_cast<size_t>(x0 + t) * C) = acc[t];
 }
 
-// Four consecutive channels of dm^0 = scale * dout at one token: scale is w_{i,0} (B with w), 1/L
-// (B without w) or 1 (A), one per head.
-template <typename T>
-__device__ __forceinline__ float4 dm0_load(const PosEncBwdArgs& a, int b, int tok, int N, int C, int c0, int h)
-{
-    float4 g = load4<T>(a.dout, (static_cast<size_t>(b) * N + tok) * C + c0);
-    float s = 1.0f;
-    if (a.variant_b) s = a.w ? a.w[((static_cast<size_t>(b) * N + tok) * a.heads + h) * a.nlev] : 1.0f / a.nlev;
-    return make_float4(s * g.x, s * g.y, s * g.z, s * g.w);
-}
+constexpr int kBwdRows = kPosEncBwdRows;      // rows one thread sweeps in the encoding's backward
 
-// One thread owns four channels of four neighbouring tokens of one row of one level (as in the
-// forward pass). It reads the 3 x 6 windows of dm^l and V^l once, adds to dV at its tokens
-// sum over the window of w[tap] * dm(token - tap) (the transposed stencil), and forms its share of the
-// kernels' gradient sum_token dm(token) * V(token + tap) and of the bias gradient sum_token dm(token).
-// The block then sums those shares per channel through LDS and writes one row of partial sums. At
-// level 0 of QuadTree-B with w it also adds <dout_i, encoding_i> to dw_{i,0}: the level-0 message
-// that dw_{i,0} multiplies includes the encoding (a head's d/4 threads are consecutive lanes).
-template <typename T>
-__global__ __launch_bounds__(kThreads) void posenc_bwd_kernel(PosEncBwdArgs a)
+// One thread owns one channel of kTX neighbouring tokens over kBwdRows consecutive rows of one level
+// (channel fastest, so a wave reads contiguous channels of a token). It slides a 3-row window of dm^l
+// and V^l down the rows (one new row of kTX + 2 values of each per step), adds to dV at its tokens
+// sum over the window of w[tap] * dm(token - tap) (the transposed stencil), and accumulates its share
+// of the kernel's gradient sum_token dm(token) * V(token + tap) and of the bias gradient
+// sum_token dm(token). The block sums those shares per channel through LDS and writes one row of
+// partial sums per channel. At level 0 of QuadTree-B with w it also adds <dout_i, encoding_i> to
+// dw_{i,0}: the level-0 message that dw_{i,0} multiplies includes the encoding (a head's channels are
+// d consecutive lanes).
+// One row of the sliding window: dm and V at (y, x0 - 1 .. x0 + kTX) (zero outside the map) and, at
+// level 0, dout at the row's own kTX tokens (for the dw term).
+struct BwdRow {
+    float gm[kTX + 2], vv[kTX + 2], go[kTX];
+};
+
+__device__ const float kUnitScale = 1.0f;   // stands in for w when QuadTree-B runs without it
+
+// All-ones if ok, else zero, in a form the compiler cannot see through. "ok ? load : 0" with a
+// visible condition is turned into a branch around the load, which then waits for it at once;
+// x & mask with an opaque mask keeps every load of a window row unconditional (their addresses
+// are clamped into the map) and in flight together.
+__device__ __forceinline__ unsigned opaque_mask(bool ok)
 {
-    constexpr int kPart = 4 * 10;                       // 4 channels x (9 taps + the bias)
-    __shared__ float red[kThreads][kPart + 1];
-    const long long item = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+    unsigned m = ok ? 0xFFFFFFFFu : 0u;
+    asm volatile("" : "+v"(m));
+    return m;
+}
+__device__ __forceinline__ float masked(float x, unsigned m) { return __uint_as_float(__float_as_uint(x) & m); }
+
+// The work of one block; LEVEL0: a block of level 0 (dm from dout and w), else of a coarser level.
+template <typename T, bool LEVEL0>
+__device__ __forceinline__ void posenc_bwd_block(const PosEncBwdArgs& a, const long long blk, float (*red)[11])
+{
+    constexpr int kPart = 10;                          // 9 taps, then the bias
+    const long long item = blk * blockDim.x + threadIdx.x;
     int l = 0;
-    while (l + 1 < a.nlev && item >= a.start[l + 1]) ++l;
+    if constexpr (!LEVEL0)
+        while (l + 1 < a.nlev && item >= a.start[l + 1]) ++l;
     const PosEncBwdLevel& L = a.lv[l];
-    const int C = a.heads * a.d, groups = C / 4;
+    const int C = a.heads * a.d;
     const bool live = item < a.level_end[l];
-    const int xtiles = (L.W + kTX - 1) / kTX;
-    const long long rel = item - a.start[l];
-    int r = live ? static_cast<int>(rel) : 0;
-    const int g = r % groups;
-    r /= groups;
+    const int xtiles = (L.W + kTX - 1) / kTX, ytiles = (L.H + kBwdRows - 1) / kBwdRows;
+    int r = live ? static_cast<int>(item - a.start[l]) : 0;
+    const int ch = r % C;
+    r /= C;
     const int x0 = (r % xtiles) * kTX;
     r /= xtiles;
-    const int y = r % L.H;
-    const int b = r / L.H;
-    const int c0 = 4 * g, h = c0 / a.d, c = c0 - h * a.d;
+    const int y0 = (r % ytiles) * kBwdRows;
+    const int b = r / ytiles;
+    const int h = ch / a.d, c = ch - h * a.d;
     const int N = L.H * L.W;
+    const bool want_dw = LEVEL0 && a.dw != nullptr;   // uniform
+    // Column offsets of the window (clamped into the map) and their validity, fixed for the thread:
+    // NHWC tensors step C per column; at level 0 w steps heads*L (V there is the caller's, NHWC);
+    // at the coarser levels V in the parent-blocked layout ([B][heads][H/2][W/2][2][2][d]) steps 4d
+    // per column pair and d within a pair.
+    int colc[kTX + 2], colx[kTX + 2];
+    unsigned colok[kTX + 2];
+    const int wstride = (a.variant_b && a.w) ? a.heads * a.nlev : 0;
+#pragma unroll
+    for (int j = 0; j < kTX + 2; ++j) {
+        const int xx = x0 + j - 1;
+        const int xc = min(max(xx, 0), L.W - 1);
+        colok[j] = opaque_mask(live && xx >= 0 && xx < L.W);
+        colc[j] = xc * C;
+        if constexpr (LEVEL0) colx[j] = xc * wstride;
+        else colx[j] = L.blocked ? ((xc >> 1) * 4 + (xc & 1)) * a.d : xc * C;
+    }
+    // level 0 of QuadTree-B scales dout by w_{i,0} (with w) or 1/L (without); QuadTree-A does not
+    const float* wsrc = wstride ? a.w + h * a.nlev : &kUnitScale;
+    const float sc = (a.variant_b && !a.w) ? 1.0f / a.nlev : 1.0f;
+    const int Hp = (L.H + 1) / 2, Wp = (L.W + 1) / 2;
+    const T* vbase = static_cast<const T*>(L.v);
+    auto load_row = [&](int yy, BwdRow& R) {
+        const int yc = min(max(yy, 0), L.H - 1);
+        const unsigned rowok = opaque_mask(yy >= 0 && yy < L.H);
+        const size_t tokrow = static_cast<size_t>(b) * N + static_cast<size_t>(yc) * L.W;   // token of (b, yc, 0)
+        const size_t vrow = (!LEVEL0 && L.blocked)
+            ? ((((static_cast<size_t>(b) * a.heads + h) * Hp + (yc >> 1)) * Wp) * 4 + (yc & 1) * 2) * a.d + c
+            : tokrow * C + ch;
+        const T* vp = vbase + vrow;
+        const int* colv = LEVEL0 ? colc : colx;
+        if constexpr (LEVEL0) {
+            const T* gp = static_cast<const T*>(a.dout) + tokrow * C + ch;
+            const float* wp = wsrc + (wstride ? tokrow * wstride : 0);
+#pragma unroll
+            for (int j = 0; j < kTX + 2; ++j) {
+                const float raw = Storage<T>::load1(gp, colc[j]);
+                const float g = sc * wp[colx[j]] * raw;
+                if (j >= 1 && j <= kTX) R.go[j - 1] = raw;
+                R.gm[j] = masked(g, rowok & colok[j]);
+            }
+        } else {
+            const float* gp = L.dm + tokrow * C + ch;
+#pragma unroll
+            for (int j = 0; j < kTX + 2; ++j) R.gm[j] = masked(gp[colc[j]], rowok & colok[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < kTX + 2; ++j) {
+            const float v = Storage<T>::load1(vp, colv[j]);
+            R.vv[j] = masked(v, rowok & colok[j]);
+        }
+    };
     float part[kPart];
 #pragma unroll
     for (int i = 0; i < kPart; ++i) part[i] = 0.f;
-    const bool want_dw = l == 0 && a.dw != nullptr;                   // uniform
-    float dwp[kTX] = {};
-    if (live) {
-        // the windows of dm and V (zero outside the map)
-        float4 dmw[3][kTX + 2], vw[3][kTX + 2];
+    float wk[9];
 #pragma unroll
-        for (int ky = 0; ky < 3; ++ky) {
-            const int yy = y + ky - 1;
-            const int yc = min(max(yy, 0), L.H - 1);
+    for (int i = 0; i < 9; ++i) wk[i] = L.weight[static_cast<size_t>(ch) * 9 + i];
+    const float bias0 = (want_dw && a.bias0) ? a.bias0[ch] : 0.f;
+    // Row y of the tile with its window rows above (U), at (M) and below (D): D is loaded here, with
+    // dV at the row's tokens, so that the two wait once.
+    auto step = [&](int y, const BwdRow& U, const BwdRow& M, BwdRow& D) {
+        const int yc = min(y, L.H - 1);
+        float* dvp = L.dv + (static_cast<size_t>(b) * N + static_cast<size_t>(yc) * L.W) * C + ch;
+        float dvo[kTX];
 #pragma unroll
-            for (int j = 0; j < kTX + 2; ++j) {
-                const int xx = x0 + j - 1;
-                const int xc = min(max(xx, 0), L.W - 1);
-                const bool ok = yy >= 0 && yy < L.H && xx >= 0 && xx < L.W;
-                const int tok = yc * L.W + xc;
-                float4 gm = l == 0 ? dm0_load<T>(a, b, tok, N, C, c0, h)
-                                   : *reinterpret_cast<const float4*>(L.dm + (static_cast<size_t>(b) * N + tok) * C + c0);
-                float4 vv = load4<T>(L.v, elem_offset(L.blocked != 0, b, yc, xc, L.H, L.W, h, c, a.heads, a.d));
-                if (!ok) {
-                    gm = make_float4(0.f, 0.f, 0.f, 0.f);
-                    vv = gm;
-                }
-                dmw[ky][j] = gm;
-                vw[ky][j] = vv;
-            }
-        }
-        float wk[36];
-        const float4* wp = reinterpret_cast<const float4*>(L.weight + static_cast<size_t>(c0) * 9);
-#pragma unroll
-        for (int i = 0; i < 9; ++i) {
-            const float4 t = wp[i];
-            wk[4 * i] = t.x;
-            wk[4 * i + 1] = t.y;
-            wk[4 * i + 2] = t.z;
-            wk[4 * i + 3] = t.w;
-        }
+        for (int t = 0; t < kTX; ++t) dvo[t] = dvp[colc[t + 1]];
+        load_row(y + 1, D);
+        const BwdRow* rows[3] = {&U, &M, &D};
+        float dwv[kTX];
 #pragma unroll
         for (int t = 0; t < kTX; ++t) {
-            if (x0 + t >= L.W) break;
-            const float4 g0 = dmw[1][t + 1];                  // dm at this thread's token (y, x0 + t)
-            // the bias and the kernels: dm(token) times V(token + tap)
-            part[36 + 0] += g0.x;
-            part[36 + 1] += g0.y;
-            part[36 + 2] += g0.z;
-            part[36 + 3] += g0.w;
-            float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+            // zero dm outside the map makes the partial sums of a token past the edge vanish; only
+            // the stores are masked
+            const float g0 = M.gm[t + 1];
+            part[9] += g0;
+            float acc = 0.f, e = bias0;
 #pragma unroll
             for (int ky = 0; ky < 3; ++ky)
 #pragma unroll
                 for (int kx = 0; kx < 3; ++kx) {
                     const int k = ky * 3 + kx;
-                    const float4 vv = vw[ky][t + kx];
-                    part[0 * 9 + k] += g0.x * vv.x;
-                    part[1 * 9 + k] += g0.y * vv.y;
-                    part[2 * 9 + k] += g0.z * vv.z;
-                    part[3 * 9 + k] += g0.w * vv.w;
+                    part[k] = fmaf(g0, rows[ky]->vv[t + kx], part[k]);
                     // V at this token fed the message of token - tap + (1, 1) through tap (ky, kx)
-                    const float4 gg = dmw[2 - ky][t + 2 - kx];
-                    acc.x = fmaf(wk[0 * 9 + k], gg.x, acc.x);
-                    acc.y = fmaf(wk[1 * 9 + k], gg.y, acc.y);
-                    acc.z = fmaf(wk[2 * 9 + k], gg.z, acc.z);
-                    acc.w = fmaf(wk[3 * 9 + k], gg.w, acc.w);
+                    acc = fmaf(wk[k], rows[2 - ky]->gm[t + 2 - kx], acc);
+                    if (want_dw) e = fmaf(wk[k], rows[ky]->vv[t + kx], e);
                 }
-            float4* dst = reinterpret_cast<float4*>(L.dv + (static_cast<size_t>(b) * N + y * L.W + x0 + t) * C + c0);
-            const float4 old = *dst;
-            *dst = make_float4(old.x + acc.x, old.y + acc.y, old.z + acc.z, old.w + acc.w);
-            if (want_dw) {
-                // the encoding at this token, against dout there
-                float4 e = a.bias0 ? *reinterpret_cast<const float4*>(a.bias0 + c0) : make_float4(0.f, 0.f, 0.f, 0.f);
+            if (live && y < L.H && x0 + t < L.W) dvp[colc[t + 1]] = dvo[t] + acc;
+            dwv[t] = want_dw ? M.go[t] * e : 0.f;   // the encoding against dout
+        }
+        if (want_dw) {
+            // summed over the head's d channels (d consecutive lanes: the whole wave for d = 64, each
+            // half for d = 32), with every lane taking part in the exchanges
 #pragma unroll
-                for (int ky = 0; ky < 3; ++ky)
-#pragma unroll
-                    for (int kx = 0; kx < 3; ++kx) {
-                        const int k = ky * 3 + kx;
-                        const float4 vv = vw[ky][t + kx];
-                        e.x = fmaf(wk[0 * 9 + k], vv.x, e.x);
-                        e.y = fmaf(wk[1 * 9 + k], vv.y, e.y);
-                        e.z = fmaf(wk[2 * 9 + k], vv.z, e.z);
-                        e.w = fmaf(wk[3 * 9 + k], vv.w, e.w);
-                    }
-                const float4 go = load4<T>(a.dout, (static_cast<size_t>(b) * N + y * L.W + x0 + t) * C + c0);
-                dwp[t] = go.x * e.x + go.y * e.y + go.z * e.z + go.w * e.w;
+            for (int t = 0; t < kTX; ++t) {
+                const float sum = a.d == 64 ? wave_allreduce(dwv[t], [](float u, float v) { return u + v; })
+                                            : half_allreduce(dwv[t], [](float u, float v) { return u + v; });
+                if (live && y < L.H && x0 + t < L.W && c == 0)
+                    a.dw[((static_cast<size_t>(b) * N + static_cast<size_t>(y) * L.W + x0 + t) * a.heads + h) * a.nlev] += sum;
             }
         }
-    }
-    if (want_dw) {
-        // sum over the head's d/4 threads (aligned groups of consecutive lanes, all of one level and
-        // either all live or all past its end), then the first of them adds it to dw_{i,0}
-        const int G = a.d / 4;
-#pragma unroll
-        for (int t = 0; t < kTX; ++t) {
-            float s = dwp[t];
-            for (int m = 1; m < G; m <<= 1) s += __shfl_xor(s, m, kWave);
-            if (live && (g % G) == 0 && x0 + t < L.W) {
-                float* dwd = a.dw + ((static_cast<size_t>(b) * N + y * L.W + x0 + t) * a.heads + h) * a.nlev;
-                *dwd += s;
-            }
-        }
+    };
+    // three window slots in rotation (the loop is unrolled by three so that no row is copied)
+    BwdRow r0, r1, r2;
+    load_row(y0 - 1, r0);
+    load_row(y0, r1);
+#pragma unroll 1
+    for (int dy = 0; dy < kBwdRows; dy += 3) {
+        step(y0 + dy, r0, r1, r2);
+        if (dy + 1 < kBwdRows) step(y0 + dy + 1, r1, r2, r0);
+        if (dy + 2 < kBwdRows) step(y0 + dy + 2, r2, r0, r1);
     }
 #pragma unroll
     for (int i = 0; i < kPart; ++i) red[threadIdx.x][i] = part[i];
     __syncthreads();
     // the block's items start at a multiple of the block size within the level: thread t holds
-    // channel group (b0 + t) % groups
-    const int b0 = static_cast<int>((static_cast<long long>(blockIdx.x) * blockDim.x - a.start[l]) % groups);
-    for (int j = threadIdx.x; j < groups; j += blockDim.x) {
-        float s[kPart];
+    // channel (b0 + t) % C; thread j < C sums the threads of channel (b0 + j) % C
+    const int b0 = static_cast<int>((blk * blockDim.x - a.start[l]) % C);
+    if (static_cast<int>(threadIdx.x) < min(C, kThreads)) {
+        const int j = threadIdx.x;
+        float sum[kPart];
 #pragma unroll
-        for (int i = 0; i < kPart; ++i) s[i] = 0.f;
-        for (int t = ((j - b0) % groups + groups) % groups; t < kThreads; t += groups)
+        for (int i = 0; i < kPart; ++i) sum[i] = 0.f;
+        for (int t = j; t < kThreads; t += C)
 #pragma unroll
-            for (int i = 0; i < kPart; ++i) s[i] += red[t][i];
-        float* dst = a.part + static_cast<size_t>(blockIdx.x) * C * 10 + static_cast<size_t>(4 * j) * 10;
+            for (int i = 0; i < kPart; ++i) sum[i] += red[t][i];
+        const int chj = (b0 + j) % C;
+        float* dst = a.part + (static_cast<size_t>(blk) * C + chj) * kPart;
 #pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-#pragma unroll
-            for (int k = 0; k < 9; ++k) dst[cc * 10 + k] = s[cc * 9 + k];
-            dst[cc * 10 + 9] = s[36 + cc];
-        }
+        for (int i = 0; i < kPart; ++i) dst[i] = sum[i];
     }
 }
 
-// Sums the partial rows of each level: one block per (level, channel group of four), its threads
-// taking the level's blocks in turn, then a tree over the threads in LDS.
-__global__ __launch_bounds__(kThreads) void posenc_bwd_reduce_kernel(PosEncBwdArgs a)
+// One launch for every level: level 0's blocks first (b0 of them), then the coarser levels', which
+// run beside them; the two kinds of block take separate code paths (a uniform branch), so neither
+// pays for the other's registers.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void posenc_bwd_kernel(PosEncBwdArgs a, int b0)
 {
-    constexpr int kPart = 40;
-    __shared__ float red[kThreads][kPart + 1];
-    const int C = a.heads * a.d, groups = C / 4;
-    const int l = blockIdx.x / groups, j = blockIdx.x - l * groups;
+    __shared__ float red[kThreads][11];
+    const long long blk = blockIdx.x;
+    if (blk < b0) posenc_bwd_block<T, true>(a, blk, red);
+    else posenc_bwd_block<T, false>(a, blk, red);
+}
+
+// Sums the partial rows of each level: one block per (level, 64 consecutive entries of the C*10
+// row), lane i owning entry i and the block's waves taking the level's blocks in turn (coalesced
+// reads), then a sum over the waves in LDS.
+constexpr int kReduceWaves = 16;
+__global__ __launch_bounds__(kReduceWaves * kWave) void posenc_bwd_reduce_kernel(PosEncBwdArgs a)
+{
+    __shared__ float red[kReduceWaves][kWave];
+    const int C = a.heads * a.d, row = C * 10;
+    const int chunks = (row + kWave - 1) / kWave;
+    const int l = blockIdx.x / chunks, o = (blockIdx.x - l * chunks) * kWave + (threadIdx.x & (kWave - 1));
+    const int wave = threadIdx.x / kWave;
     const long long first = a.start[l] / kThreads;
     const long long last = (a.level_end[l] + kThreads - 1) / kThreads;
-    float s[kPart];
+    constexpr int kInFlight = 8;                     // independent loads per lane per round
+    float s[kInFlight] = {};
+    if (o < row) {
+        long long blk = first + wave;
+        for (; blk + (kInFlight - 1) * kReduceWaves < last; blk += kInFlight * kReduceWaves)
 #pragma unroll
-    for (int i = 0; i < kPart; ++i) s[i] = 0.f;
-    for (long long blk = first + threadIdx.x; blk < last; blk += blockDim.x) {
-        const float* src = a.part + static_cast<size_t>(blk) * C * 10 + static_cast<size_t>(4 * j) * 10;
-#pragma unroll
-        for (int i = 0; i < kPart; ++i) s[i] += src[i];
+            for (int u = 0; u < kInFlight; ++u) s[u] += a.part[static_cast<size_t>(blk + u * kReduceWaves) * row + o];
+        for (; blk < last; blk += kReduceWaves) s[0] += a.part[static_cast<size_t>(blk) * row + o];
     }
+    float tot = 0.f;
 #pragma unroll
-    for (int i = 0; i < kPart; ++i) red[threadIdx.x][i] = s[i];
+    for (int u = 0; u < kInFlight; ++u) tot += s[u];
+    red[wave][threadIdx.x & (kWave - 1)] = tot;
     __syncthreads();
-    for (int half = kThreads / 2; half > 0; half >>= 1) {
-        if (static_cast<int>(threadIdx.x) < half)
+    if (wave == 0 && o < row) {
+        float s = 0.f;
 #pragma unroll
-            for (int i = 0; i < kPart; ++i) red[threadIdx.x][i] += red[threadIdx.x + half][i];
-        __syncthreads();
-    }
-    if (threadIdx.x < kPart) {
-        const int cc = threadIdx.x / 10, k = threadIdx.x - cc * 10;
-        const size_t ch = static_cast<size_t>(l) * C + 4 * j + cc;
-        if (k < 9) a.dweight[ch * 9 + k] = red[0][threadIdx.x];
-        else if (a.dbias) a.dbias[ch] = red[0][threadIdx.x];
+        for (int w = 0; w < kReduceWaves; ++w) s += red[w][threadIdx.x];
+        const int chn = o / 10, k = o - chn * 10;
+        const size_t cg = static_cast<size_t>(l) * C + chn;
+        if (k < 9) a.dweight[cg * 9 + k] = s;
+        else if (a.dbias) a.dbias[cg] = s;
     }
 }
 
@@ -372,10 +408,10 @@ hipError_t launch_posenc_bwd(const PosEncBwdArgs& a, bool use_bf16, hipStream_t 
 {
     PosEncBwdArgs p = a;
     const int C = a.heads * a.d;
-    if (C % 4 != 0 || C / 4 > kThreads) return hipErrorInvalidValue;
+    if (C > kThreads || (a.d != 32 && a.d != 64)) return hipErrorInvalidValue;
     p.start[0] = 0;
     for (int l = 0; l < a.nlev; ++l) {
-        const long long n = posenc_items(a.B, a.lv[l].H, a.lv[l].W, C);
+        const long long n = posenc_bwd_items(a.B, a.lv[l].H, a.lv[l].W, C);
         if (n >= 0x7FFFFFFFLL) return hipErrorInvalidValue;           // items within a level are int
         p.level_end[l] = p.start[l] + n;
         p.start[l + 1] = (p.level_end[l] + kThreads - 1) / kThreads * kThreads;
@@ -383,11 +419,14 @@ hipError_t launch_posenc_bwd(const PosEncBwdArgs& a, bool use_bf16, hipStream_t 
     const long long blocks = p.start[p.nlev] / kThreads;
     if (blocks <= 0) return hipSuccess;
     if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    if (use_bf16) hipLaunchKernelGGL((posenc_bwd_kernel<bf16>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream, p);
-    else hipLaunchKernelGGL((posenc_bwd_kernel<float>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream, p);
+    const int b0 = static_cast<int>(p.start[1] / kThreads);   // level 0's blocks, then the others
+    if (use_bf16) hipLaunchKernelGGL((posenc_bwd_kernel<bf16>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream, p, b0);
+    else hipLaunchKernelGGL((posenc_bwd_kernel<float>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream, p, b0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(posenc_bwd_reduce_kernel, dim3(static_cast<unsigned>(p.nlev * (C / 4))), dim3(kThreads), 0, stream, p);
+    const int chunks = (C * 10 + kWave - 1) / kWave;
+    hipLaunchKernelGGL(posenc_bwd_reduce_kernel, dim3(static_cast<unsigned>(p.nlev * chunks)), dim3(kReduceWaves * kWave),
+                       0, stream, p);
     return hipGetLastError();
 }
 

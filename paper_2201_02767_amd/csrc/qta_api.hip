@@ -824,7 +824,7 @@ qta_status backward_impl(const void* q, const void* k, const void* v, const floa
     if (pe) {
         if (!opt->dpe_weight || !aligned16(opt->dpe_weight)) return QTA_ERR_INVALID;
         if (o.pe_bias && !opt->dpe_bias) return QTA_ERR_INVALID;
-        if (static_cast<long long>(heads) * d > 1024) return QTA_ERR_UNSUPPORTED;
+        if (static_cast<long long>(heads) * d > 256) return QTA_ERR_UNSUPPORTED;
     }
     qta_workspace_layout L;
     st = layout(B, heads, H, W, d, levels, o.Kl, v_supplied, pe, dtype, &L);

@@ -184,18 +184,26 @@ struct PosEncBwdArgs {
     float* dw;                  // B with w: fp32 [B][H*W][heads][L], += <dout_i, level 0's encoding at i>; or NULL
 };
 
-// Work items (4 channels of 4 neighbouring tokens of one row) of one level of the encoding passes,
-// and the 256-thread blocks of the backward's first kernel (every level starts on a block boundary).
+// Work items of one level of the encoding's forward pass (4 channels of 4 neighbouring tokens of one
+// row), and the 256-thread blocks of the backward's first kernel (every level starts on a block
+// boundary).
 constexpr int kPosEncTokens = 4;
 constexpr int kPosEncThreads = 256;
 inline long long posenc_items(int B, int H, int W, int C)
 {
     return static_cast<long long>(B) * H * ((W + kPosEncTokens - 1) / kPosEncTokens) * (C / 4);
 }
+// The backward's items: one channel of kPosEncTokens tokens over kPosEncBwdRows rows.
+constexpr int kPosEncBwdRows = 8;
+inline long long posenc_bwd_items(int B, int H, int W, int C)
+{
+    return static_cast<long long>(B) * ((H + kPosEncBwdRows - 1) / kPosEncBwdRows) *
+           ((W + kPosEncTokens - 1) / kPosEncTokens) * C;
+}
 inline long long posenc_bwd_blocks(int B, const int* Hl, const int* Wl, int levels, int C)
 {
     long long n = 0;
-    for (int l = 0; l < levels; ++l) n += (posenc_items(B, Hl[l], Wl[l], C) + kPosEncThreads - 1) / kPosEncThreads;
+    for (int l = 0; l < levels; ++l) n += (posenc_bwd_items(B, Hl[l], Wl[l], C) + kPosEncThreads - 1) / kPosEncThreads;
     return n;
 }
 

@@ -318,7 +318,7 @@ def test_backward_validation():
     opt.pe_bias = None
     assert lib.qta_backward_ex(FAKE, FAKE, FAKE, None, FAKE, 1, 40, 16, 16, 32, 3, 4, VA, F32, 0.0,
                                ctypes.byref(opt), FAKE, 1 << 40, FAKE, FAKE, FAKE, None, FAKE, 1 << 40,
-                               None) == UNSUPPORTED                         # the encoding with C > 1024
+                               None) == UNSUPPORTED                         # the encoding with C > 256
     need_pe = lib.qta_backward_workspace_bytes_ex(1, 1, 16, 16, 32, 3, 4, VA, F32, ctypes.byref(opt))
     assert need_pe > lib.qta_backward_workspace_bytes_ex(1, 1, 16, 16, 32, 3, 4, VA, F32, None)
     assert bwd(wsb=0) == WORKSPACE                                          # the forward's workspace
