@@ -1,14 +1,16 @@
 // Steps 2-3 at the coarsest level: full softmax attention, Eq. (1), plus each query's top-K keys.
 //
-// One workgroup of 16 waves owns a 16-query tile of one (batch, head):
-//   phase 1  logits S = tau * Q_tile K^T on MFMA (16x16 output tiles, waves take key tiles in
-//            turn), kept in LDS as fp32 [16][N];
+// One workgroup of Q waves (Q = 8 or 16) owns a tile of Q queries of one (batch, head):
+//   phase 1  logits S = tau * Q_tile K^T on MFMA (16x16 output tiles whose rows repeat the Q
+//            queries when Q < 16; waves take key tiles in turn, a batch of loads at a time), kept
+//            in LDS as fp32 [Q][N];
 //   phase 2  wave r owns query row r: max, exp and sum over the row (register butterflies), then
 //            the K best keys by a bitwise radix select on wave ballots (ties at the cut go to the
 //            lower index), listed in index order; QuadTree-A zeroes the kept keys' weights (their
 //            mass is refined at the next level);
-//   phase 3  m = P V on fp32 MFMA (values widened to fp32 as they are loaded): waves split the d
-//            columns into 16-wide tiles and the keys into chunks; partial tiles are summed through
+//   phase 3  m = P V on fp32 MFMA (values widened to fp32 as they are loaded, two batches of
+//            loads in flight): waves split the d columns into 16-wide tiles and the keys into
+//            chunks; partial tiles are summed through
 //            LDS and written as fp32 messages (or, for a single-level problem, straight to the
 //            output in the storage type).
 // The coarsest map holds at most QTA_MAX_COARSE tokens, so a row fits in 16 registers per lane.
@@ -25,8 +27,6 @@ namespace {
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kRows = 16;                         // queries per workgroup
-constexpr int kWaves = 16;
 
 // LDS pitch of a logit row: whole 64-element groups plus 4 floats, so the 16 rows that one MFMA
 // operand read touches fall in different banks.
@@ -43,30 +43,34 @@ inline int coarse_per_lane(int N)
     return 0;
 }
 
-template <typename T, int D, bool VA, int kPerLane>
-__global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
+template <typename T, int D, bool VA, int kPerLane, int Q>
+__global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
 {
     using S = Storage<T>;
     constexpr bool kBf16 = sizeof(T) == 2;
-    constexpr int kMaxTilesPerWave = QTA_MAX_COARSE / 16 / kWaves;
+    constexpr int kWaves = Q;                      // one wave per query row in phase 2
+    static_assert(Q == 8 || Q == 16, "8 or 16 query rows per workgroup");
     extern __shared__ __align__(16) float smem[];
     const int N = a.N, C = a.C, pitch = coarse_pitch(N);
-    float* Sm = smem;                              // [16][pitch]
-    float* red = smem + kRows * pitch;             // [16 waves][16][16]
-    const int tiles = (N + kRows - 1) / kRows;
+    float* Sm = smem;                              // [Q][pitch]
+    float* red = smem + Q * pitch;                 // [waves][16][16]
+    const int tiles = (N + Q - 1) / Q;             // query tiles of this map
+    const int ktiles = (N + 15) / 16;              // 16-key tiles
     int blk = blockIdx.x;
     const int tile = blk % tiles;
     blk /= tiles;
     const int h = blk % a.heads;
     const int b = blk / a.heads;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6)), lane = threadIdx.x & 63;
     const size_t tok0 = static_cast<size_t>(b) * N;           // first token of this batch element
     const size_t hoff = static_cast<size_t>(h) * D;
 
-    // V operands of phase 3's first two key batches, requested now so that their latency overlaps the
-    // logits and the selection (phase 3 layout: lane (kgrp, col) holds V[4*step + kgrp][16*ct + col])
+    // V operands of phase 3's first two key batches, requested after the logits' operands so that
+    // their latency overlaps the logits and the selection (phase 3 layout: lane (kgrp, col) holds
+    // V[4*step + kgrp][16*ct + col])
     constexpr int NCT = D / 16;          // 16-wide column tiles of the messages
     constexpr int NKS = kWaves / NCT;    // key chunks
+    static_assert(NKS >= 1, "at least one wave per column tile");
     constexpr int kVBatch = 8;           // key steps per V batch
     const int p3_ct = wave % NCT, p3_ks = wave / NCT;
     const int p3_ch = p3_ct * 16 + (lane & 15);
@@ -79,62 +83,77 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
             dst[u] = S::load1(a.v, (tok0 + cand) * C + hoff + p3_ch);
         }
     };
-    load_v(p3_ks, vb);
-    load_v(p3_ks + NKS * kVBatch, vb2);      // and the second (together 512 keys at d = 32, 256 at d = 64)
 
-    // ---- phase 1: logits on MFMA; a wave takes key tiles wave, wave+16, ... (at most 4) ----
-    // The contraction over the d channels is taken in a permuted order so that each lane loads
-    // whole 16-byte chunks of its query or key row: lane (kgrp, r) loads chunks kgrp, kgrp+4, ...
-    // of row r and feeds their elements to consecutive k-steps; Q and K use the same permutation.
+    // ---- phase 1: logits on MFMA; a wave takes key tiles wave, wave + waves, ..., a batch at a time ----
+    // The 16 rows of an MFMA tile hold the workgroup's Q query rows (repeated when Q < 16; only the
+    // first Q are kept). The contraction over the d channels is taken in a permuted order so that each
+    // lane loads whole 16-byte chunks of its query or key row: lane (kgrp, r) loads chunks kgrp,
+    // kgrp+4, ... of row r and feeds their elements to consecutive k-steps; Q and K use the same
+    // permutation.
     {
         const int arow = lane & 15, kgrp = lane >> 4;
-        const int qi = min(tile * kRows + arow, N - 1);   // rows past N are computed and ignored
-        constexpr int NJ = D * static_cast<int>(sizeof(T)) / 64;    // 16-byte chunks per lane and row
-        uint4 qa[NJ], kb[kMaxTilesPerWave][NJ];
+        const int qi = min(tile * Q + (arow & (Q - 1)), N - 1);   // rows past N are computed and ignored
+        constexpr int NJ = D * static_cast<int>(sizeof(T)) / 64;   // 16-byte chunks per lane and row
+        constexpr int kTileBatch = 4;
+        uint4 qa[NJ];
         const unsigned char* qrow = static_cast<const unsigned char*>(a.q) + ((tok0 + qi) * C + hoff) * sizeof(T);
 #pragma unroll
         for (int jj = 0; jj < NJ; ++jj) qa[jj] = *reinterpret_cast<const uint4*>(qrow + (kgrp + 4 * jj) * 16);
+        bool first = true;
+        for (int t0 = wave; t0 < ktiles; t0 += kWaves * kTileBatch) {             // uniform
+            uint4 kb[kTileBatch][NJ];
 #pragma unroll
-        for (int it = 0; it < kMaxTilesPerWave; ++it) {
-            if (wave + kWaves * it >= tiles) break;                           // uniform
-            const int n = min((wave + kWaves * it) * 16 + arow, N - 1);       // columns past N set to -inf
-            const unsigned char* krow = static_cast<const unsigned char*>(a.k) + ((tok0 + n) * C + hoff) * sizeof(T);
+            for (int it = 0; it < kTileBatch; ++it) {
+                if (t0 + kWaves * it >= ktiles) break;                            // uniform
+                const int n = min((t0 + kWaves * it) * 16 + arow, N - 1);         // columns past N set to -inf
+                const unsigned char* krow = static_cast<const unsigned char*>(a.k) + ((tok0 + n) * C + hoff) * sizeof(T);
 #pragma unroll
-            for (int jj = 0; jj < NJ; ++jj) kb[it][jj] = *reinterpret_cast<const uint4*>(krow + (kgrp + 4 * jj) * 16);
-        }
-#pragma unroll
-        for (int it = 0; it < kMaxTilesPerWave; ++it) {
-            const int kt = wave + kWaves * it;
-            if (kt >= tiles) break;
-            float4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int jj = 0; jj < NJ; ++jj) {
-                if constexpr (kBf16) {
-                    // 8 bf16 per chunk: k-steps 2*jj and 2*jj+1, four channels each
-                    const uint4 qq = qa[jj], kk = kb[it][jj];
-                    short4_t a0, b0, a1, b1;
-                    a0[0] = static_cast<short>(qq.x); a0[1] = static_cast<short>(qq.x >> 16);
-                    a0[2] = static_cast<short>(qq.y); a0[3] = static_cast<short>(qq.y >> 16);
-                    a1[0] = static_cast<short>(qq.z); a1[1] = static_cast<short>(qq.z >> 16);
-                    a1[2] = static_cast<short>(qq.w); a1[3] = static_cast<short>(qq.w >> 16);
-                    b0[0] = static_cast<short>(kk.x); b0[1] = static_cast<short>(kk.x >> 16);
-                    b0[2] = static_cast<short>(kk.y); b0[3] = static_cast<short>(kk.y >> 16);
-                    b1[0] = static_cast<short>(kk.z); b1[1] = static_cast<short>(kk.z >> 16);
-                    b1[2] = static_cast<short>(kk.w); b1[3] = static_cast<short>(kk.w >> 16);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, b0, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, b1, acc, 0, 0, 0);
-                } else {
-                    // 4 floats per chunk: four k-steps
-                    const uint4 qq = qa[jj], kk = kb[it][jj];
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.x), __uint_as_float(kk.x), acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.y), __uint_as_float(kk.y), acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.z), __uint_as_float(kk.z), acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.w), __uint_as_float(kk.w), acc, 0, 0, 0);
-                }
+                for (int jj = 0; jj < NJ; ++jj) kb[it][jj] = *reinterpret_cast<const uint4*>(krow + (kgrp + 4 * jj) * 16);
             }
-            const int n = kt * 16 + (lane & 15);
+            if (first) {
+                load_v(p3_ks, vb);
+                load_v(p3_ks + NKS * kVBatch, vb2);
+                first = false;
+            }
 #pragma unroll
-            for (int jr = 0; jr < 4; ++jr) Sm[(4 * kgrp + jr) * pitch + n] = n < N ? acc[jr] * a.scale : -INFINITY;
+            for (int it = 0; it < kTileBatch; ++it) {
+                const int kt = t0 + kWaves * it;
+                if (kt >= ktiles) break;
+                float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int jj = 0; jj < NJ; ++jj) {
+                    if constexpr (kBf16) {
+                        // 8 bf16 per chunk: k-steps 2*jj and 2*jj+1, four channels each
+                        const uint4 qq = qa[jj], kk = kb[it][jj];
+                        short4_t a0, b0, a1, b1;
+                        a0[0] = static_cast<short>(qq.x); a0[1] = static_cast<short>(qq.x >> 16);
+                        a0[2] = static_cast<short>(qq.y); a0[3] = static_cast<short>(qq.y >> 16);
+                        a1[0] = static_cast<short>(qq.z); a1[1] = static_cast<short>(qq.z >> 16);
+                        a1[2] = static_cast<short>(qq.w); a1[3] = static_cast<short>(qq.w >> 16);
+                        b0[0] = static_cast<short>(kk.x); b0[1] = static_cast<short>(kk.x >> 16);
+                        b0[2] = static_cast<short>(kk.y); b0[3] = static_cast<short>(kk.y >> 16);
+                        b1[0] = static_cast<short>(kk.z); b1[1] = static_cast<short>(kk.z >> 16);
+                        b1[2] = static_cast<short>(kk.w); b1[3] = static_cast<short>(kk.w >> 16);
+                        acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, b0, acc, 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, b1, acc, 0, 0, 0);
+                    } else {
+                        // 4 floats per chunk: four k-steps
+                        const uint4 qq = qa[jj], kk = kb[it][jj];
+                        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.x), __uint_as_float(kk.x), acc, 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.y), __uint_as_float(kk.y), acc, 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.z), __uint_as_float(kk.z), acc, 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.w), __uint_as_float(kk.w), acc, 0, 0, 0);
+                    }
+                }
+                const int n = kt * 16 + (lane & 15);
+#pragma unroll
+                for (int jr = 0; jr < 4; ++jr)
+                    if (4 * kgrp + jr < Q) Sm[(4 * kgrp + jr) * pitch + n] = n < N ? acc[jr] * a.scale : -INFINITY;
+            }
+        }
+        if (first) {                     // a wave with no key tile (more waves than tiles)
+            load_v(p3_ks, vb);
+            load_v(p3_ks + NKS * kVBatch, vb2);
         }
     }
     __syncthreads();
@@ -142,7 +161,7 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     // ---- phase 2: softmax and selection, one wave per query row ----
     {
         const int r = wave;
-        const int qi = tile * kRows + r;
+        const int qi = tile * Q + r;
         float* row = Sm + r * pitch;
         float x[kPerLane];
         float mx = -INFINITY;
@@ -204,31 +223,38 @@ __global__ __launch_bounds__(1024) void coarse_attn_kernel(CoarseArgs a)
     __syncthreads();
 
     // ---- phase 3: messages m = P V on fp32 MFMA (values widened on load, so no transpose) ----
+    // A wave takes key steps p3_ks, p3_ks + NKS, ... in batches of kVBatch, two batches in flight.
     {
-        const int arow = lane & 15, kgrp = lane >> 4;
+        const int prow = (lane & 15) & (Q - 1), kgrp = lane >> 4;   // P rows past Q repeat (ignored)
+        const float* prw = Sm + prow * pitch + kgrp;
         float4_t acc = {0.f, 0.f, 0.f, 0.f};
-        int it = 0;
-        for (int st0 = p3_ks; st0 < steps; st0 += NKS * kVBatch, ++it) {
-            if (it >= 2) load_v(st0, vb);                     // the first two batches came in at the start
+        auto mma_batch = [&](int st0, const float (&vv)[kVBatch]) {
 #pragma unroll
             for (int u = 0; u < kVBatch; ++u) {
                 const int st = st0 + u * NKS;
                 if (st >= steps) break;
-                const float vu = it == 1 ? vb2[u] : vb[u];
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Sm[arow * pitch + st * 4 + kgrp], vu, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(prw[st * 4], vv[u], acc, 0, 0, 0);
             }
+        };
+        constexpr int kStride = NKS * kVBatch;
+        for (int st0 = p3_ks; st0 < steps; st0 += 2 * kStride) {
+            mma_batch(st0, vb);
+            if (st0 + 2 * kStride < steps) load_v(st0 + 2 * kStride, vb);
+            if (st0 + kStride >= steps) break;
+            mma_batch(st0 + kStride, vb2);
+            if (st0 + 3 * kStride < steps) load_v(st0 + 3 * kStride, vb2);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) red[(wave * 16 + 4 * kgrp + j) * 16 + (lane & 15)] = acc[j];
     }
     __syncthreads();
-    for (int t = threadIdx.x; t < kRows * D; t += blockDim.x) {
+    for (int t = threadIdx.x; t < Q * D; t += blockDim.x) {
         const int r = t / D, ch = t % D;
         const int ct = ch / 16, col = ch % 16;
         float s = 0.f;
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) s += red[((ks * NCT + ct) * 16 + r) * 16 + col];
-        const int qi = tile * kRows + r;
+        const int qi = tile * Q + r;
         if (qi >= N) continue;
         if (a.pe_w) {                                    // uniform: the fused position encoding
             // 3x3 depth-wise cross-correlation of v around token qi, zero outside the map, plus the bias
@@ -474,21 +500,39 @@ hipError_t launch_small(const CoarseArgs& a, hipStream_t stream)
     return hipGetLastError();
 }
 
+// Query rows per workgroup of the coarse kernel (its waves, one per row in the softmax and selection
+// phase). Fewer rows per workgroup spread a small map's rows over more compute units, so that the
+// selection's scalar work and each phase's latency are shared by fewer rows, at the price of more
+// passes over the map's keys and values (from L2) and of MFMA tiles only half filled. Measured on
+// MI355X, 8 rows pay where the MFMA phases are cheapest (bf16 with d = 32: one 16-byte chunk per key
+// row and k-step pair) and 16 rows elsewhere (fp32, or d = 64).
+template <typename T, int D>
+constexpr int coarse_rows()
+{
+    return (sizeof(T) == 2 && D == 32) ? 8 : 16;
+}
+
+template <typename T, int D, bool VA, int kPerLane, int Q>
+hipError_t launch_rows(const CoarseArgs& a, hipStream_t stream)
+{
+    const size_t lds = (static_cast<size_t>(Q) * coarse_pitch(a.N) + static_cast<size_t>(Q) * 16 * 16) * sizeof(float);
+    if (lds > device_max_lds()) return hipErrorInvalidValue;
+    static std::atomic<unsigned long long> configured{0};     // devices whose LDS limit is raised
+    if (hipError_t e = set_max_lds_once(reinterpret_cast<const void*>(&coarse_attn_kernel<T, D, VA, kPerLane, Q>), configured);
+        e != hipSuccess)
+        return e;
+    const int tiles = (a.N + Q - 1) / Q;
+    const long long blocks = static_cast<long long>(a.B) * a.heads * tiles;
+    if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((coarse_attn_kernel<T, D, VA, kPerLane, Q>), dim3(static_cast<unsigned>(blocks)), dim3(Q * kWave),
+                       lds, stream, a);
+    return hipGetLastError();
+}
+
 template <typename T, int D, bool VA, int kPerLane>
 hipError_t launch_one(const CoarseArgs& a, hipStream_t stream)
 {
-    const size_t lds = (static_cast<size_t>(kRows) * coarse_pitch(a.N) + kWaves * 16 * 16) * sizeof(float);
-    if (lds > device_max_lds()) return hipErrorInvalidValue;
-    static std::atomic<unsigned long long> configured{0};     // devices whose LDS limit is raised
-    if (hipError_t e = set_max_lds_once(reinterpret_cast<const void*>(&coarse_attn_kernel<T, D, VA, kPerLane>), configured);
-        e != hipSuccess)
-        return e;
-    const int tiles = (a.N + kRows - 1) / kRows;
-    const long long blocks = static_cast<long long>(a.B) * a.heads * tiles;
-    if (blocks > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((coarse_attn_kernel<T, D, VA, kPerLane>), dim3(static_cast<unsigned>(blocks)), dim3(kWaves * kWave),
-                       lds, stream, a);
-    return hipGetLastError();
+    return launch_rows<T, D, VA, kPerLane, coarse_rows<T, D>()>(a, stream);
 }
 
 template <typename T, int D, bool VA>

@@ -287,22 +287,39 @@ template <int NPER>
 __device__ __forceinline__ void wave_select_top(const uint32_t (&key)[NPER], const uint32_t (&name)[NPER], int keff,
                                                 bool (&kept)[NPER])
 {
+    keff = __builtin_amdgcn_readfirstlane(keff);
     uint32_t cut = 0;
-    bool exact = false;
-    for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t c = cut | (1u << bit);
-        int cnt = 0;
-#pragma unroll
-        for (int e = 0; e < NPER; ++e) cnt += __popcll(__ballot(key[e] >= c));
-        if (cnt >= keff) {
-            cut = c;
-            if (cnt == keff) {
-                exact = true;
-                break;
+    int cnt = 0;                                     // keys at or above the cut, once the search ends
+    if constexpr (NPER == 1) {
+        // one candidate per lane: a constant trip count with an early exit, which the compiler
+        // unrolls completely (a compare, a bit count and a test per bit)
+        for (int bit = 31; bit >= 0; --bit) {
+            const uint32_t c = cut | (1u << bit);
+            const int n = __popcll(__ballot(key[0] >= c));
+            if (n >= keff) {
+                cut = c;
+                if (n == keff) break;
             }
         }
+    } else {
+        // several candidates per lane: the loop stays rolled, so the cut and the bit under test
+        // are kept wave-uniform in scalar registers explicitly (one scalar unit serves all the waves
+        // of a compute unit, so the loop keeps its scalar work small); a bit that leaves exactly
+        // keff keys at or above the cut ends the search by clearing the bit under test
+        uint32_t bitv = 0x80000000u;
+        while (bitv != 0u) {
+            const uint32_t c = cut | bitv;
+            int n = 0;
+#pragma unroll
+            for (int e = 0; e < NPER; ++e) n += __popcll(__ballot(key[e] >= c));
+            n = __builtin_amdgcn_readfirstlane(n);
+            cut = n >= keff ? c : cut;
+            bitv = n == keff ? 0u : bitv >> 1;
+        }
     }
-    if (exact) {
+#pragma unroll
+    for (int e = 0; e < NPER; ++e) cnt += __popcll(__ballot(key[e] >= cut));
+    if (cnt == keff) {
 #pragma unroll
         for (int e = 0; e < NPER; ++e) kept[e] = key[e] >= cut;
         return;
