@@ -28,7 +28,7 @@ FLAGS = [
 # The attention kernels (forward and backward) never see a NaN (finite inputs; masked logits are
 # -inf and are selected away before use), so their max reductions may skip the NaN-quieting the
 # IEEE mode asks for, which lets each butterfly step fuse into one DPP max.
-NO_NAN_SOURCES = {"fine.hip", "fine_wide.hip", "coarse.hip", "backward.hip", "coarse_bwd.hip"}
+NO_NAN_SOURCES = {"fine.hip", "coarse.hip", "backward.hip", "coarse_bwd.hip"}
 
 
 def _compile(src: str) -> str:

@@ -1,8 +1,8 @@
 // Gathered fine attention at the finer levels: one wave per (parent query, head) work item, or per
 // pair of neighbouring parents on maps of one row; the per-item work (its independent loads in
 // item_head, then gather, MFMA logits, softmax, top-K, messages, the finest level's combination in
-// fine_item, both in fine_item.h). A workgroup holds four independent waves; nothing synchronises
-// across waves. Candidate sets of more than 64 slots run the kernel of fine_wide.hip.
+// fine_item, both in fine_item.h). A workgroup holds up to four independent waves (fewer when a
+// wave's LDS region is large: 256 fp32 slots of d = 64); nothing synchronises across waves.
 #include "fine_item.h"
 
 namespace qta {
@@ -34,8 +34,9 @@ hipError_t launch_one(const FineArgs& a, hipStream_t stream)
     const int nsp = (4 * a.Kp + 15) & ~15;
     const WaveLds lay = wave_lds<T, D>(nsp);
     const size_t wave_bytes = lay.total;
-    const int wpb = 4;
-    if (wpb * wave_bytes > device_max_lds()) return hipErrorInvalidValue;
+    int wpb = 4;
+    while (wpb > 1 && wpb * wave_bytes > device_max_lds()) --wpb;
+    if (wave_bytes > device_max_lds()) return hipErrorInvalidValue;
     // the fused position encoding stages a 4x4 token block of one head in the value-row region
     if (PE && static_cast<size_t>(lay.p - lay.v) < static_cast<size_t>(D) * kPeTokenPitch * sizeof(T))
         return hipErrorInvalidValue;
@@ -59,7 +60,12 @@ hipError_t launch_nsp_pe(const FineArgs& a, hipStream_t stream)
     const int nslot = 4 * a.Kp;
     if (nslot <= 16) return launch_one<T, D, 16, VA, FINEST, ROW, PE>(a, stream);
     if (nslot <= 32) return launch_one<T, D, 32, VA, FINEST, ROW, PE>(a, stream);
-    return launch_one<T, D, 64, VA, FINEST, ROW, PE>(a, stream);
+    if (nslot <= 64) return launch_one<T, D, 64, VA, FINEST, ROW, PE>(a, stream);
+    if constexpr (!PE) {
+        if (nslot <= 128) return launch_one<T, D, 128, VA, FINEST, ROW, PE>(a, stream);
+        if (nslot <= 256) return launch_one<T, D, 256, VA, FINEST, ROW, PE>(a, stream);
+    }
+    return hipErrorInvalidValue;
 }
 
 // Levels of maps with more than one row may fuse their position encoding (a.pe_w).
@@ -93,10 +99,8 @@ hipError_t launch_td(const FineArgs& a, bool variant_a, bool finest, hipStream_t
 
 hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool bf16_in, bool finest, hipStream_t stream)
 {
-    if (4 * a.Kp > kMaxSlots) {
-        if (a.pe_w) return hipErrorInvalidValue;        // the wide kernel has no fused position encoding
-        return launch_fine_attn_wide(a, d, variant_a, bf16_in, finest, stream);
-    }
+    const int nslot = 4 * a.Kp;
+    if (nslot > kMaxSlots || (a.pe_w && nslot > kMaxSlotsPe)) return hipErrorInvalidValue;
     FineArgs b = a;
     b.div_Wp = make_fastdiv(a.Wp);
     b.div_heads = make_fastdiv(a.heads);

@@ -3,9 +3,10 @@
 // Eqs. 2 and 5), included by the fine kernels of every finer level.
 //
 // Work item = one parent query P at level l+1 and one head. Its four children at level l are
-// sibling queries with one shared candidate set: the 2x2 children of the K keys P kept (4K <= 64
+// sibling queries with one shared candidate set: the 2x2 children of the K keys P kept (4K <= 256
 // candidates). One wave owns one item; candidate slot s = 4r + c is child c, in the order (0,0),
-// (0,1),(1,0),(1,1), of kept key r, and the slots are taken in tiles of 16:
+// (0,1),(1,0),(1,1), of kept key r; lane l owns slots l, l + 64, ... (up to four), and the slots
+// are taken in tiles of 16:
 //   1. the candidates' key and value rows of this head are gathered once for the four queries with
 //      16-byte loads: lane 16g + n loads chunks g, g+4, ... of the row of slot n of each tile, so
 //      one instruction reads 16 whole rows. The value rows go to wave-private LDS (transposed for
@@ -13,8 +14,8 @@
 //   2. logits on the 16x16 MFMA straight from those registers: the key chunks are the B operand,
 //      the four queries, repeated over the 16 rows, the A operand (the d channels are contracted in
 //      the order the chunks arrive, the same for both operands). Every lane group then holds all
-//      four logits of its slot column for every tile, and lane 16g + n keeps tile g, so lane s ends
-//      with the four logits of slot s;
+//      four logits of its slot column for every tile, and lane 16g + n keeps tiles g, g + 4, ...,
+//      so lane l ends with the four logits of each of its slots;
 //   3. B: a softmax per query over the wave (DPP and permlane butterflies, no LDS);
 //      A: a softmax over each lane quad (the children of one kept key) times the parent's score;
 //   4. levels above 0: the K best candidates of each query by a bitwise radix select on wave
@@ -38,7 +39,8 @@ typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
-constexpr int kMaxSlots = 64;
+constexpr int kMaxSlots = 256;         // candidate slots of one item: 4 K_l for K_l <= 64, up to four per lane
+constexpr int kMaxSlotsPe = 64;        // with a fused position encoding: one slot per lane
 constexpr int kPrefetchLevels = 4;    // the finest level prefetches up to this many ancestors
 // LDS pitch (elements) of one channel's 16 tokens in the fused position encoding: 20 puts the four lane
 // groups' writes and neighbouring channels' row reads in different banks (16 would stack them)
@@ -94,7 +96,7 @@ struct ItemHead {
     bool pair2;                 // ROW: the second parent exists
     bool q_ok;                  // this lane's query (n16 & 3) lies on the map
     int J_g[NSP / 16];
-    float pkey;
+    float pkey[NSP > 64 ? NSP / 64 : 1];   // QuadTree-A: the parent's score of each of the lane's slots
     uint4 qa[D * sizeof(T) / 64];
 };
 
@@ -131,9 +133,14 @@ __device__ __forceinline__ void item_head(const FineArgs& a, const int item, Ite
     const int last_sel = (ROW && pair2 ? 2 * K : K) - 1;
 #pragma unroll
     for (int t = 0; t < NT; ++t) hd.J_g[t] = prow[min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)];
-    hd.pkey = 0.f;
-    if constexpr (VA)
-        hd.pkey = a.parent_key[((static_cast<size_t>(b) * a.heads + h) * Np + P) * K + min(lane >> kSlotShift, last_sel)];
+    constexpr int SPL = NSP > 64 ? NSP / 64 : 1;
+#pragma unroll
+    for (int u = 0; u < SPL; ++u) {
+        hd.pkey[u] = 0.f;
+        if constexpr (VA)
+            hd.pkey[u] = a.parent_key[((static_cast<size_t>(b) * a.heads + h) * Np + P) * K +
+                                      min((64 * u + lane) >> kSlotShift, last_sel)];
+    }
     const int qi = n16 & 3;
     const int qy = ROW ? 0 : 2 * Py + (qi >> 1), qx = ROW ? 2 * P + qi : 2 * Px + (qi & 1);
     hd.q_ok = qy < H && qx < W;
@@ -174,7 +181,9 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     constexpr int NCG = D / 4;             // PV: 4-channel groups
     constexpr int NH = 16 / NCG;           // PV: slot halves (2 for d = 32, 1 for d = 64)
     constexpr int QPL = 4 / NH;            // output queries per lane
+    constexpr int SPL = NSP > 64 ? NSP / 64 : 1;   // candidate slots per lane: lane + 64u
     static_assert(!PE || !ROW, "the fused position encoding is for maps of more than one row");
+    static_assert(NSP <= kMaxSlotsPe || !PE, "a fused position encoding takes at most 64 slots");
 
     const int lane = threadIdx.x & 63;
     const int Np = a.Hp * a.Wp;
@@ -218,11 +227,13 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     const int n16 = lane & 15, g = lane >> 4;
     const int ntile = nsp / 16;
     const int (&J_g)[NT] = hd.J_g;
-    // lane = slot 16g + n16: tile g's gather key
-    int J_own_raw = -1;
+    // lane 16g + n16 owns slots 64u + 16g + n16: the gather keys of tiles g + 4u
+    int J_own[SPL];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) J_own_raw = g == t ? J_g[t] : J_own_raw;
-    const float pkey = hd.pkey;
+    for (int u = 0; u < SPL; ++u) J_own[u] = -1;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) J_own[t >> 2] = g == (t & 3) ? J_g[t] : J_own[t >> 2];
+    const float (&pkey)[SPL] = hd.pkey;
     const uint4 (&qa)[NJ] = hd.qa;
     const bool q_ok = hd.q_ok;
     // phase B: the gathers. NHWC: child f of this head at kg + f*C*TB. Blocked: the four children
@@ -253,11 +264,17 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
         }
     };
     load_tiles(0);
-    const int flat = child_of_slot_J(lane < nslot ? J_own_raw : -1, lane);
-    const bool ok = flat >= 0;
+    int flat[SPL];
+    bool ok[SPL];
+#pragma unroll
+    for (int u = 0; u < SPL; ++u) {
+        const int s = 64 * u + lane;
+        flat[u] = child_of_slot_J(s < nslot ? J_own[u] : -1, s);
+        ok[u] = flat[u] >= 0;
+    }
 
     // ---- 2. logits on MFMA and the value rows into LDS, one batch of tiles at a time ----
-    float acc_own[4] = {0.f, 0.f, 0.f, 0.f};
+    float acc_own[SPL][4] = {};
     auto consume_tiles = [&](int t0) {
 #pragma unroll
         for (int i = 0; i < kTB; ++i) {
@@ -278,9 +295,9 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.w), __uint_as_float(kk.w), acc, 0, 0, 0);
                 }
             }
-            // rows 4g + r of the product are query r for every g: lane 16g + n keeps tile g
+            // rows 4g + r of the product are query r for every g: lane 16g + n keeps tiles g + 4u
 #pragma unroll
-            for (int r = 0; r < 4; ++r) acc_own[r] = g == t ? acc[r] : acc_own[r];
+            for (int r = 0; r < 4; ++r) acc_own[t >> 2][r] = g == (t & 3) ? acc[r] : acc_own[t >> 2][r];
             // value rows (off-map or missing candidates as zeros)
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
@@ -397,15 +414,18 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
         }
     }
     // the slots of query r (ROW: only those of its own parent, half r >> 1)
-    bool okr[4];
+    bool okr[SPL][4];
+    float x[SPL][4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) okr[r] = ROW ? ok && ((lane >> 1) >= K) == ((r >> 1) != 0) : ok;
-    float x[4];
+    for (int u = 0; u < SPL; ++u)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) x[r] = okr[r] ? acc_own[r] * a.scale : -INFINITY;
+        for (int r = 0; r < 4; ++r) {
+            okr[u][r] = ROW ? ok[u] && (((64 * u + lane) >> 1) >= K) == ((r >> 1) != 0) : ok[u];
+            x[u][r] = okr[u][r] ? acc_own[u][r] * a.scale : -INFINITY;
+        }
 
     // ---- 3. weights ----
-    float wgt[4], inv_sum[4] = {1.f, 1.f, 1.f, 1.f};
+    float wgt[SPL][4], inv_sum[4] = {1.f, 1.f, 1.f, 1.f};
     // the finest level of B with 32 slots and d = 32: two queries per register (lanes 0..31 query
     // 2p, lanes 32..63 query 2p+1, slot lane & 31), so that one reduction within each 32-lane half
     // serves two queries; the weights stay packed for the P store below (with d = 64 the extra
@@ -415,12 +435,12 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     if constexpr (kPack) {
         // (the cross-lane exchanges run with every lane active, before the per-half selects)
         const bool upper = lane >= 32;
-        const uint32_t ok_hi = xchg_u32<32>(ok ? 1u : 0u);
-        const bool okp = upper ? ok_hi != 0u : ok;
+        const uint32_t ok_hi = xchg_u32<32>(ok[0] ? 1u : 0u);
+        const bool okp = upper ? ok_hi != 0u : ok[0];
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
-            const float hi = xchg_f32<32>(x[2 * p + 1]);
-            const float y = upper ? hi : x[2 * p];
+            const float hi = xchg_f32<32>(x[0][2 * p + 1]);
+            const float y = upper ? hi : x[0][2 * p];
             const float m = half_allreduce(y, [](float u, float v) { return fmaxf(u, v); });
             wpk[p] = okp ? __expf(y - m) : 0.f;
             const float inv = fast_rcp(half_allreduce(wpk[p], [](float u, float v) { return u + v; }));   // >= 1
@@ -430,21 +450,31 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     } else if constexpr (!VA) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const float m = wave_max_fast(x[r]);
-            wgt[r] = okr[r] ? __expf(x[r] - m) : 0.f;
-            inv_sum[r] = fast_rcp(wave_sum_fast(wgt[r]));   // the sum is at least 1 (the maximum's term)
+            float xm = x[0][r];
+#pragma unroll
+            for (int u = 1; u < SPL; ++u) xm = fmaxf(xm, x[u][r]);
+            const float m = wave_max_fast(xm);
+            float se = 0.f;
+#pragma unroll
+            for (int u = 0; u < SPL; ++u) {
+                wgt[u][r] = okr[u][r] ? __expf(x[u][r] - m) : 0.f;
+                se += wgt[u][r];
+            }
+            inv_sum[r] = fast_rcp(wave_sum_fast(se));   // the sum is at least 1 (the maximum's term)
         }
     } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            // t: a softmax over the children of one kept key (a lane quad; ROW: a lane pair)
-            float m = fmaxf(x[r], xchg_f32<1>(x[r]));
-            if constexpr (!ROW) m = fmaxf(m, xchg_f32<2>(m));
-            const float e = okr[r] ? __expf(x[r] - m) : 0.f;
-            float s = e + xchg_f32<1>(e);
-            if constexpr (!ROW) s += xchg_f32<2>(s);
-            wgt[r] = okr[r] ? pkey * e * fast_rcp(s) : 0.f;  // s >= 1
-        }
+        for (int u = 0; u < SPL; ++u)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                // t: a softmax over the children of one kept key (a lane quad; ROW: a lane pair)
+                float m = fmaxf(x[u][r], xchg_f32<1>(x[u][r]));
+                if constexpr (!ROW) m = fmaxf(m, xchg_f32<2>(m));
+                const float e = okr[u][r] ? __expf(x[u][r] - m) : 0.f;
+                float s = e + xchg_f32<1>(e);
+                if constexpr (!ROW) s += xchg_f32<2>(s);
+                wgt[u][r] = okr[u][r] ? pkey[u] * e * fast_rcp(s) : 0.f;  // s >= 1
+            }
     }
 
     // ---- 4. this level's selection (levels above the finest) ----
@@ -454,19 +484,30 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
             int qy, qx;
             query_yx(r, qy, qx);
             if (qy >= H || qx >= W) continue;                 // uniform across the wave
-            const int nvalid = __popcll(__ballot(okr[r]));
+            int nvalid = 0;
+#pragma unroll
+            for (int u = 0; u < SPL; ++u) nvalid += __popcll(__ballot(okr[u][r]));
             const int keff = Ks < nvalid ? Ks : nvalid;
-            const uint32_t key[1] = {okr[r] ? ordered_bits(VA ? wgt[r] : x[r]) : 0u};
-            const uint32_t name[1] = {static_cast<uint32_t>(flat)};
-            bool kept[1];
-            wave_select_top<1>(key, name, keff, kept);
-            const uint64_t mask = __ballot(kept[0]);
+            uint32_t key[SPL], name[SPL];
+#pragma unroll
+            for (int u = 0; u < SPL; ++u) {
+                key[u] = okr[u][r] ? ordered_bits(VA ? wgt[u][r] : x[u][r]) : 0u;
+                name[u] = static_cast<uint32_t>(flat[u]);
+            }
+            bool kept[SPL];
+            wave_select_top<SPL>(key, name, keff, kept);
             const size_t orow = ((static_cast<size_t>(b) * a.heads + h) * N + qy * W + qx) * Ks;
-            if (kept[0]) {
-                const int pos = lanes_below(mask);
-                a.sel_idx[orow + pos] = flat;
-                a.sel_key[orow + pos] = VA ? wgt[r] : wgt[r] * inv_sum[r];
-                if constexpr (VA) wgt[r] = 0.f;               // refined at the next level (Omega)
+            int before = 0;
+#pragma unroll
+            for (int u = 0; u < SPL; ++u) {
+                const uint64_t mask = __ballot(kept[u]);
+                if (kept[u]) {
+                    const int pos = before + lanes_below(mask);
+                    a.sel_idx[orow + pos] = flat[u];
+                    a.sel_key[orow + pos] = VA ? wgt[u][r] : wgt[u][r] * inv_sum[r];
+                    if constexpr (VA) wgt[u][r] = 0.f;        // refined at the next level (Omega)
+                }
+                before += __popcll(mask);
             }
             if (lane >= keff && lane < Ks) {
                 a.sel_idx[orow + lane] = -1;
@@ -485,13 +526,19 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
             else
                 reinterpret_cast<float*>(Pb)[row * nsp + (lane & 31)] = wpk[p];
         }
-    } else if (lane < nsp) {
+    } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            if constexpr (kBf16)
-                reinterpret_cast<uint16_t*>(Pb)[r * nsp + lane] = static_cast<uint16_t>(f32_to_bf16_bits(wgt[r]));
-            else
-                reinterpret_cast<float*>(Pb)[r * nsp + lane] = wgt[r];
+        for (int u = 0; u < SPL; ++u) {
+            const int s = 64 * u + lane;
+            if (s < nsp) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if constexpr (kBf16)
+                        reinterpret_cast<uint16_t*>(Pb)[r * nsp + s] = static_cast<uint16_t>(f32_to_bf16_bits(wgt[u][r]));
+                    else
+                        reinterpret_cast<float*>(Pb)[r * nsp + s] = wgt[u][r];
+                }
+            }
         }
     }
     wave_lds_sync();

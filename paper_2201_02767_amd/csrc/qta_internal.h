@@ -371,8 +371,6 @@ hipError_t launch_coarse_attn(const CoarseArgs& a, int d, bool variant_a, bool u
 hipError_t launch_posenc(const PosEncArgs& a, bool use_bf16, hipStream_t stream);
 hipError_t launch_posenc_bwd(const PosEncBwdArgs& a, bool use_bf16, hipStream_t stream);
 hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest, hipStream_t stream);
-hipError_t launch_fine_attn_wide(const FineArgs& a, int d, bool variant_a, bool use_bf16, bool finest,
-                                 hipStream_t stream);
 hipError_t launch_topk(const TopkArgs& a, hipStream_t stream);
 // Orders each of `rows` selection rows of K entries (idx int32, key fp32, in place) by (key descending,
 // index ascending), empty slots (index -1) last.

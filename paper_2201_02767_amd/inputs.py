@@ -16,6 +16,10 @@ not used):
              q, k, v are random linear maps of Gaussian-blurred (sigma 2 tokens) N(0,1) features.
   highres  - 2 x 200x336 (800x1333 image at 1/4), 2 heads x 32, bf16, 5 levels, K=16, QuadTree-B;
              generated like backbone. Its coarsest level (13x21) comes from ceil pooling.
+  detection - 2 x 200x334 (an 800x1333 detection input at stride 4: the first stage of a PVTv2-b0
+             backbone), 1 head x 32, bf16, 5 levels (coarsest 13x21), K=32 as the paper's detection
+             backbones use (Sec. 4.2, Table 4), QuadTree-B; generated like backbone. With 4K = 128
+             candidates per sibling group it takes the wide fine-level path.
   matching_ksched - matching with the paper's K schedule for feature matching (Sec. 4.1.1): K = 8
              at the finest selecting level, doubled at each coarser level (16 at the coarsest).
   backbone_vgiven - backbone with V's coarser levels given as inputs, as in self-attention where a
@@ -71,6 +75,7 @@ WORKLOADS = {
     "stereo": Workload("stereo", 3, 2, 120, 160, 8, 32, 4, 8, "B", "bf16", "disparity"),
     "backbone": Workload("backbone", 4, 32, 56, 56, 1, 64, 3, 8, "B", "bf16", "smooth"),
     "highres": Workload("highres", 5, 2, 200, 336, 2, 32, 5, 16, "B", "bf16", "smooth"),
+    "detection": Workload("detection", 6, 2, 200, 334, 1, 32, 5, 32, "B", "bf16", "smooth"),
     "matching_ksched": Workload("matching_ksched", 2, 1, 60, 80, 8, 32, 3, (0, 8, 16), "B", "f32", "shift"),
     "backbone_vgiven": Workload("backbone_vgiven", 4, 32, 56, 56, 1, 64, 3, 8, "B", "bf16", "smooth", True),
     "backbone_pe": Workload("backbone_pe", 4, 32, 56, 56, 1, 64, 3, 8, "B", "bf16", "smooth", False, True),

@@ -285,6 +285,8 @@ def test_stage_selection_order_with_ties_and_empty_slots(dev, variant):
     (1, 23, 19, 1, 32, 5, 1),       # K = 1, deep pyramid on an odd map
     (1, 1, 40, 2, 32, 4, 3),        # single row
     (1, 12, 12, 1, 32, 3, 20),      # K above the candidate count (two slot chunks)
+    (1, 30, 26, 2, 64, 3, 24),      # 96 candidates per sibling group, d = 64 (two slots per lane)
+    (2, 37, 53, 1, 32, 4, 32),      # 128 candidates, ragged map, four levels (detection's K)
     (1, 20, 24, 2, 64, 3, 64),      # K = 64 (four slot chunks)
     (1, 29, 32, 2, 64, 3, 8),       # coarse level of exactly 64 tokens (8 x 8), d = 64
 ])
@@ -367,7 +369,7 @@ def test_explicit_scale(dev):
 # the workloads at full size
 # ------------------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["tiny", "matching", "stereo", "backbone", "highres", "matching_ksched",
+@pytest.mark.parametrize("name", ["tiny", "matching", "stereo", "backbone", "highres", "detection", "matching_ksched",
                                   "backbone_vgiven", "backbone_pe", "stereo_epipolar"])
 def test_workload_full_size(dev, name):
     wl = WORKLOADS[name]
@@ -497,6 +499,7 @@ def test_forward_position_encoding(dev, variant, dtype, B, H, W, heads, d, L, K,
     ("A", "f32", 1, 5, 37, 2, 32, 3, 4, False, False),      # ragged rows
     ("A", "bf16", 2, 3, 93, 1, 64, 5, [0, 2, 4, 8, 16], False, False),   # K schedule; 4 levels of pairs
     ("B", "f32", 1, 4, 50, 2, 32, 3, 20, False, False),     # 40 candidates per query
+    ("A", "bf16", 2, 3, 333, 1, 64, 3, 40, False, False),   # 80 per query, 160 slots per item (four per lane)
     ("B", "bf16", 1, 6, 41, 2, 32, 3, 4, True, True),       # given V levels and the position encoding
     # 1200 coarse rows of 10 tokens, d = 64: several query rows per wave in the small-map coarse kernel
     ("A", "f32", 1, 600, 40, 2, 64, 3, 8, False, False),
