@@ -82,7 +82,8 @@ typedef enum { QTA_F32 = 0, QTA_BF16 = 1, QTA_DTYPE_MAX_ENUM = 0x7FFFFFFF } qta_
  * attention) are stored parent-blocked when blocked[l] is 1:
  * [B][heads][ceil(H_l/2)][ceil(W_l/2)][2][2][d], i.e. the 2x2 children of one parent position of
  * one head are 4*d contiguous elements (off-map children are unused padding). The input level 0
- * and the coarsest level are NHWC. Blocking is used when 4*K <= 64. */
+ * and the coarsest level are NHWC. Blocking is used unless V's coarser levels are the caller's
+ * (qta_options.v_levels). */
 typedef struct {
     int levels;
     int H[QTA_MAX_LEVELS];

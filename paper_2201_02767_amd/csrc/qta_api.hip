@@ -71,13 +71,13 @@ qta_status check_k_levels(const int* Kl, int levels)
     return QTA_OK;
 }
 
-// Intermediate level l (produced by the pyramid, gathered by level l's attention, whose parents
-// kept K_{l+1} keys) is stored parent-blocked when that kernel takes the blocked path
-// (4*K_{l+1} <= 64) and V comes from the pyramid. The input level stays NHWC: a blocked copy of
-// it would cost a write and a read of k and v for no gain in the gathers.
+// Intermediate level l (produced by the pyramid, gathered by level l's attention) is stored
+// parent-blocked when V comes from the pyramid. The input level stays NHWC: a blocked copy of it
+// would cost a write and a read of k and v for no gain in the gathers.
 bool use_blocked(const int* Kl, int l, int levels, bool v_supplied)
 {
-    return !v_supplied && l >= 1 && l <= levels - 2 && 4 * Kl[l + 1] <= 64;
+    (void)Kl;
+    return !v_supplied && l >= 1 && l <= levels - 2;
 }
 
 // Whether level l's position encoding is computed inside that level's attention kernel: the coarsest

@@ -63,7 +63,7 @@ def _tok_bytes(blocked, B, H, W, C, tb):
     return B * H * W * C * tb
 
 
-@pytest.mark.parametrize("K,expect_blocked", [(16, True), (20, False)])
+@pytest.mark.parametrize("K,expect_blocked", [(16, True), (20, True)])
 def test_workspace_layout_is_aligned_and_disjoint(K, expect_blocked):
     lay = P.workspace_layout(2, 2, 200, 336, 32, 5, K, torch.bfloat16)
     regions = []
@@ -79,6 +79,12 @@ def test_workspace_layout_is_aligned_and_disjoint(K, expect_blocked):
         assert o1 % 256 == 0 and o1 + n1 <= o2
     assert regions[-1][0] + regions[-1][1] <= lay.total
     assert P.workspace_bytes(2, 2, 200, 336, 32, 5, K, torch.bfloat16) == lay.total
+
+
+def test_workspace_layout_nhwc_with_given_v_levels():
+    """With V's coarser levels given by the caller, every pyramid level stays NHWC."""
+    lay = P.workspace_layout(2, 2, 200, 336, 32, 5, 16, torch.bfloat16, v_supplied=True)
+    assert all(lay.blocked[l] == 0 for l in range(5))
 
 
 def test_workspace_bytes_zero_on_bad_shapes():
@@ -193,12 +199,12 @@ def _klv(*vals):
 
 
 def test_layout_with_k_schedule_and_supplied_v():
-    """Selections are sized by each level's K; a level is blocked only when the kernel that gathers
-    it takes the blocked path (4*K of its parents <= 64); with V supplied no V level is stored and
-    nothing is blocked."""
+    """Selections are sized by each level's K; every intermediate level is blocked whatever its
+    parents' K (80 candidates included); with V supplied no V level is stored and nothing is
+    blocked."""
     lib = P.lib()
     B, heads, H, W, d, L = 2, 2, 60, 80, 32, 4
-    for Ks, blocked in (([0, 4, 16, 8], [0, 1, 1, 0]), ([0, 8, 20, 8], [0, 0, 1, 0])):
+    for Ks, blocked in (([0, 4, 16, 8], [0, 1, 1, 0]), ([0, 8, 20, 8], [0, 1, 1, 0])):
         lay = P.workspace_layout(B, heads, H, W, d, L, Ks, torch.float32)
         assert [lay.blocked[l] for l in range(L)] == blocked
         assert [lay.K[l] for l in range(1, L)] == Ks[1:]
