@@ -1172,9 +1172,14 @@ hipError_t launch_key_td(const BwdLevelArgs& a, bool variant_a, bool finest, lon
 template <int LMAX>
 __global__ __launch_bounds__(256) void bwd_unpool_kernel(BwdUnpoolArgs a)
 {
-    // one thread per 4 channels of the (up to) 2x2 level-0 tokens under one level-1 token, which
-    // share every ancestor: the ancestors' rows are loaded once for four tokens. A batch element
-    // takes a.bpb consecutive blocks (its maps are below 2^31 bytes, so chunk indices fit 32 bits)
+    // one thread per tensor (q, k or v: blockIdx.y) and 4 channels of the (up to) 2x2 level-0 tokens
+    // under one level-1 token, which share every ancestor: the ancestors' rows are loaded once for four
+    // tokens. A batch element takes a.bpb consecutive blocks (its maps are below 2^31 bytes, so chunk
+    // indices fit 32 bits)
+    const int m = blockIdx.y;
+    // given V levels are not pooled from v: their gradients are returned as they are, and v's level-0
+    // gradient receives nothing from them
+    if (m == 2 && !a.v_pooled) return;                        // whole block
     const int cpt = a.C / 4;
     const int n1 = a.H[1] * a.W[1] * cpt;
     const int b = static_cast<int>(blockIdx.x) / a.bpb;
@@ -1183,59 +1188,55 @@ __global__ __launch_bounds__(256) void bwd_unpool_kernel(BwdUnpoolArgs a)
     const int i = fast_div(t, a.div_cpt);
     const int ch = t - i * cpt;
     const int y1 = fast_div(i, a.div_W1), x1 = i - y1 * a.W[1];
-    // every load first (the ancestors' rows at each level, then the four tokens' rows), then the sums
-    float4 g[LMAX][3];
-    float f[LMAX];
-    float fl = 1.0f;
-#pragma unroll
-    for (int l = 1; l < LMAX; ++l) {
-        if (l >= a.L) break;                                  // uniform
-        const int yl = y1 >> (l - 1), xl = x1 >> (l - 1);
-        const int ny = (2 * yl + 1 < a.H[l - 1]) ? 2 : 1, nx = (2 * xl + 1 < a.W[l - 1]) ? 2 : 1;
-        fl *= 1.0f / static_cast<float>(ny * nx);
-        f[l] = fl;
-        const size_t off = static_cast<size_t>(b) * static_cast<uint32_t>(a.H[l] * a.W[l] * a.C) +
-                           static_cast<uint32_t>((yl * a.W[l] + xl) * a.C + 4 * ch);
-        g[l][0] = *reinterpret_cast<const float4*>(a.gq[l] + off);
-        g[l][1] = *reinterpret_cast<const float4*>(a.gk[l] + off);
-        // given V levels are not pooled from v: their gradients are returned as they are
-        g[l][2] = a.v_pooled ? *reinterpret_cast<const float4*>(a.gv[l] + off) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
+    float* const dst = m == 0 ? a.dq : m == 1 ? a.dk : a.dv;
+    // the four tokens' rows first (they are used last), then the ancestors' rows, then the sums
     const int H0 = a.H[0], W0 = a.W[0];
     const size_t base = static_cast<size_t>(b) * static_cast<uint32_t>(H0 * W0 * a.C) + 4 * ch;
     uint32_t tok[4];
     bool ok[4];
-    float4 r[4][3];
+    float4 r[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         const int y = 2 * y1 + (c >> 1), x = 2 * x1 + (c & 1);
         ok[c] = y < H0 && x < W0;
         tok[c] = static_cast<uint32_t>((min(y, H0 - 1) * W0 + min(x, W0 - 1)) * a.C);   // clamped onto the map
-        r[c][0] = *reinterpret_cast<const float4*>(a.dq + base + tok[c]);
-        r[c][1] = *reinterpret_cast<const float4*>(a.dk + base + tok[c]);
-        r[c][2] = *reinterpret_cast<const float4*>(a.dv + base + tok[c]);
+        r[c] = *reinterpret_cast<const float4*>(dst + base + tok[c]);
     }
-    float4 s[3] = {};
+    // (eight levels at a time: all of a group's loads before its sums)
+    constexpr int kGroup = 8;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    float fl = 1.0f;
 #pragma unroll
-    for (int l = 1; l < LMAX; ++l) {
-        if (l >= a.L) break;                                  // uniform
+    for (int l0 = 1; l0 < LMAX; l0 += kGroup) {
+        if (l0 >= a.L) break;                                 // uniform
+        float4 g[kGroup];
+        float f[kGroup];
 #pragma unroll
-        for (int m = 0; m < 3; ++m) {
-            s[m].x += f[l] * g[l][m].x;
-            s[m].y += f[l] * g[l][m].y;
-            s[m].z += f[l] * g[l][m].z;
-            s[m].w += f[l] * g[l][m].w;
+        for (int j = 0; j < kGroup; ++j) {
+            const int l = l0 + j;
+            if (l >= LMAX || l >= a.L) break;                 // uniform
+            const int yl = y1 >> (l - 1), xl = x1 >> (l - 1);
+            const int ny = (2 * yl + 1 < a.H[l - 1]) ? 2 : 1, nx = (2 * xl + 1 < a.W[l - 1]) ? 2 : 1;
+            fl *= 1.0f / static_cast<float>(ny * nx);
+            f[j] = fl;
+            const size_t off = static_cast<size_t>(b) * static_cast<uint32_t>(a.H[l] * a.W[l] * a.C) +
+                               static_cast<uint32_t>((yl * a.W[l] + xl) * a.C + 4 * ch);
+            const float* const gl = m == 0 ? a.gq[l] : m == 1 ? a.gk[l] : a.gv[l];
+            g[j] = *reinterpret_cast<const float4*>(gl + off);
+        }
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) {
+            if (l0 + j >= LMAX || l0 + j >= a.L) break;       // uniform
+            s.x += f[j] * g[j].x;
+            s.y += f[j] * g[j].y;
+            s.z += f[j] * g[j].z;
+            s.w += f[j] * g[j].w;
         }
     }
-    float* const dst[3] = {a.dq, a.dk, a.dv};
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        if (!ok[c]) continue;
-#pragma unroll
-        for (int m = 0; m < 3; ++m)
-            *reinterpret_cast<float4*>(dst[m] + base + tok[c]) =
-                make_float4(r[c][m].x + s[m].x, r[c][m].y + s[m].y, r[c][m].z + s[m].z, r[c][m].w + s[m].w);
-    }
+    for (int c = 0; c < 4; ++c)
+        if (ok[c])
+            *reinterpret_cast<float4*>(dst + base + tok[c]) = make_float4(r[c].x + s.x, r[c].y + s.y, r[c].z + s.z, r[c].w + s.w);
 }
 
 }  // namespace
@@ -1334,7 +1335,7 @@ hipError_t launch_bwd_unpool(const BwdUnpoolArgs& a, hipStream_t stream)
     u.div_cpt = make_fastdiv(a.C / 4);
     u.div_W1 = make_fastdiv(a.W[1]);
     u.bpb = static_cast<int>(bpb);
-    const dim3 grid(static_cast<unsigned>(bpb * a.B));
+    const dim3 grid(static_cast<unsigned>(bpb * a.B), 3);     // y: q, k, v
     if (a.L <= 4) hipLaunchKernelGGL(bwd_unpool_kernel<4>, grid, dim3(256), 0, stream, u);
     else if (a.L <= 8) hipLaunchKernelGGL(bwd_unpool_kernel<8>, grid, dim3(256), 0, stream, u);
     else hipLaunchKernelGGL(bwd_unpool_kernel<QTA_MAX_LEVELS>, grid, dim3(256), 0, stream, u);

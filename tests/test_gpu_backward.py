@@ -141,6 +141,8 @@ def run_backward(dev, q, k, v, g, *, levels, K, variant, dtype, w=None, scale=No
     ("A", "f32", 2, 7, 9, 2, 32, 1, 4, False),         # one level: dense attention
     ("B", "bf16", 1, 5, 40, 2, 32, 1, 4, True),
     ("B", "f32", 1, 40, 41, 1, 32, 2, 4, True),        # 420 coarse tokens: 7 key chunks per lane
+    ("A", "bf16", 1, 50, 37, 1, 32, 6, 3, False),      # six levels (the unpooling's 8-level kernel)
+    ("B", "f32", 1, 257, 200, 1, 32, 9, 2, True),      # nine levels, coarsest 2x1 (its 16-level kernel)
     ("A", "bf16", 1, 27, 33, 2, 32, 3, [0, 2, 16], False),   # K schedule, blocked level 1
     ("B", "f32", 1, 33, 29, 2, 32, 4, [0, 8, 4, 2], True),
 ])
