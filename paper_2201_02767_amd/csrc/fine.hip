@@ -23,7 +23,7 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     if (item >= nitems) return;            // whole wave leaves; only wave-level syncs follow
     extern __shared__ __align__(16) unsigned char smem[];
     const int nsp = (4 * a.Kp + 15) & ~15;
-    ItemHead<T, D, NSP, ROW> hd;
+    ItemHead<T, D, NSP, VA, ROW> hd;
     item_head<T, D, NSP, VA, ROW>(a, item, hd);
     fine_item<T, D, NSP, VA, FINEST, ROW, PE>(a, hd, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
 }

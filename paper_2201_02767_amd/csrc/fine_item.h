@@ -12,14 +12,15 @@
 //      one instruction reads 16 whole rows. The value rows go to wave-private LDS (transposed for
 //      bf16); the key rows stay in registers;
 //   2. logits on the 16x16 MFMA straight from those registers: the key chunks are the B operand,
-//      the four queries, repeated over the 16 rows, the A operand (the d channels are contracted in
-//      the order the chunks arrive, the same for both operands). Every lane group then holds all
-//      four logits of its slot column for every tile, and lane 16g + n keeps tiles g, g + 4, ...,
-//      so lane l ends with the four logits of each of its slots;
-//   3. B: a softmax per query over the wave (DPP and permlane butterflies, no LDS);
+//      the four queries the A operand, query g on rows 4g .. 4g+3 (the d channels are contracted in
+//      the order the chunks arrive, the same for both operands). Lane 16g + n then holds query g's
+//      logit of slot 16t + n from tile t: a lane keeps one query's logits over the tiles;
+//   3. B: a softmax per query over its 16-lane row (DPP butterflies) and the lane's tiles;
 //      A: a softmax over each lane quad (the children of one kept key) times the parent's score;
-//   4. levels above 0: the K best candidates of each query by a bitwise radix select on wave
-//      ballots (ties at the cut to the lower flat index); A drops their weight from its message;
+//   4. levels above 0: the ranking keys move to one slot per lane (lane l: slots l, l + 64, ...) by
+//      a 4x4 transpose across the wave's 16-lane rows per four tiles (row swaps, no LDS), then the
+//      K best candidates of each query by a bitwise radix select on wave ballots (ties at the cut to
+//      the lower flat index); A drops their weight from its message;
 //   5. messages m = P V on the 4x4 MFMA, blocks split over 4-channel groups (and slot halves);
 //   6. levels above 0 store m; level 0 adds the ancestors' messages (times w for B) and stores the
 //      output in the storage type. With a fused position encoding (PE, maps of more than one row)
@@ -86,22 +87,22 @@ __device__ __forceinline__ float pick4(const float (&v)[4], int i)
 
 // The loads of a work item that need no other load, with the item's coordinates: its parents' kept
 // keys (each lane's gather key of every slot tile), their scores (QuadTree-A) and the query rows
-// (MFMA A operand: row n16 holds query n16 & 3). Vector memory counters drain in order, and a load
+// (MFMA A operand: row n16 holds query n16 >> 2). Vector memory counters drain in order, and a load
 // inside a divergent branch makes the compiler wait for it at the join, so every load here is
 // unconditional, at a clamped address that is always in bounds, with validity applied when the
 // value is used.
-template <typename T, int D, int NSP, bool ROW>
+template <typename T, int D, int NSP, bool VA, bool ROW>
 struct ItemHead {
     int b, h, P, Py, Px;
     bool pair2;                 // ROW: the second parent exists
-    bool q_ok;                  // this lane's query (n16 & 3) lies on the map
+    bool q_ok;                  // this lane's query (n16 >> 2) lies on the map
     int J_g[NSP / 16];
-    float pkey[NSP > 64 ? NSP / 64 : 1];   // QuadTree-A: the parent's score of each of the lane's slots
+    float pkey[VA ? NSP / 16 : 1];   // QuadTree-A: the parent's score of the lane's slot in each tile
     uint4 qa[D * sizeof(T) / 64];
 };
 
 template <typename T, int D, int NSP, bool VA, bool ROW>
-__device__ __forceinline__ void item_head(const FineArgs& a, const int item, ItemHead<T, D, NSP, ROW>& hd)
+__device__ __forceinline__ void item_head(const FineArgs& a, const int item, ItemHead<T, D, NSP, VA, ROW>& hd)
 {
     constexpr int TB = sizeof(T);
     constexpr int RB = D * TB;
@@ -133,15 +134,14 @@ __device__ __forceinline__ void item_head(const FineArgs& a, const int item, Ite
     const int last_sel = (ROW && pair2 ? 2 * K : K) - 1;
 #pragma unroll
     for (int t = 0; t < NT; ++t) hd.J_g[t] = prow[min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)];
-    constexpr int SPL = NSP > 64 ? NSP / 64 : 1;
+    if constexpr (VA) {
+        const float* pk = a.parent_key + ((static_cast<size_t>(b) * a.heads + h) * Np + P) * K;
 #pragma unroll
-    for (int u = 0; u < SPL; ++u) {
-        hd.pkey[u] = 0.f;
-        if constexpr (VA)
-            hd.pkey[u] = a.parent_key[((static_cast<size_t>(b) * a.heads + h) * Np + P) * K +
-                                      min((64 * u + lane) >> kSlotShift, last_sel)];
+        for (int t = 0; t < NT; ++t) hd.pkey[t] = pk[min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)];
+    } else {
+        hd.pkey[0] = 0.f;
     }
-    const int qi = n16 & 3;
+    const int qi = n16 >> 2;
     const int qy = ROW ? 0 : 2 * Py + (qi >> 1), qx = ROW ? 2 * P + qi : 2 * Px + (qi & 1);
     hd.q_ok = qy < H && qx < W;
     const int qyc = qy < H ? qy : H - 1, qxc = qx < W ? qx : W - 1;
@@ -168,7 +168,7 @@ __device__ __forceinline__ void item_head(const FineArgs& a, const int item, Ite
 // s = 2*(half*K + r) + c is child c of kept key r of parent `half`, and query q uses the slots of
 // half q >> 1 only.
 template <typename T, int D, int NSP, bool VA, bool FINEST, bool ROW = false, bool PE = false>
-__device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D, NSP, ROW>& hd, unsigned char* const base)
+__device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D, NSP, VA, ROW>& hd, unsigned char* const base)
 {
     using S = Storage<T>;
     constexpr bool kBf16 = sizeof(T) == 2;
@@ -177,7 +177,8 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     constexpr int E = S::kPer16B;          // elements per 16-byte chunk
     constexpr int NJ = RB / 64;            // 16-byte chunks per lane and row (lane group g: g, g+4, ...)
     constexpr int NT = NSP / 16;           // slot tiles (upper bound)
-    constexpr int kTB = (8 / NJ) < NT ? (8 / NJ) : NT;   // tiles whose rows are in registers at once
+    // tiles whose rows are in registers at once (at most four: eight would cost occupancy with 128 slots)
+    constexpr int kTB = (8 / NJ) < 4 ? ((8 / NJ) < NT ? (8 / NJ) : NT) : (4 < NT ? 4 : NT);
     constexpr int NCG = D / 4;             // PV: 4-channel groups
     constexpr int NH = 16 / NCG;           // PV: slot halves (2 for d = 32, 1 for d = 64)
     constexpr int QPL = 4 / NH;            // output queries per lane
@@ -233,7 +234,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     for (int u = 0; u < SPL; ++u) J_own[u] = -1;
 #pragma unroll
     for (int t = 0; t < NT; ++t) J_own[t >> 2] = g == (t & 3) ? J_g[t] : J_own[t >> 2];
-    const float (&pkey)[SPL] = hd.pkey;
+    const float (&pkey)[VA ? NT : 1] = hd.pkey;
     const uint4 (&qa)[NJ] = hd.qa;
     // phase B: the gathers. NHWC: child f of this head at kg + f*C*TB. Blocked: the four children
     // of kept key J are the 4*RB bytes at kg + J*4*RB (this (batch, head)'s blocks start at kg).
@@ -244,6 +245,8 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base;
     const uint32_t tok_bytes = static_cast<uint32_t>(C * TB);
     bool gok[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) gok[t] = false;
     uint4 kc[kTB][NJ], vc[kTB][NJ];
     auto load_tiles = [&](int t0) {
 #pragma unroll
@@ -273,7 +276,10 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     }
 
     // ---- 2. logits on MFMA and the value rows into LDS, one batch of tiles at a time ----
-    float acc_own[SPL][4] = {};
+    // xs[t]: this lane's query's (g's) logit of slot 16t + n16 (unscaled)
+    float xs[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) xs[t] = 0.f;
     auto consume_tiles = [&](int t0) {
 #pragma unroll
         for (int i = 0; i < kTB; ++i) {
@@ -298,9 +304,8 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(qq.w), __uint_as_float(kk.w), acc, 0, 0, 0);
                 }
             }
-            // rows 4g + r of the product are query r for every g: lane 16g + n keeps tiles g + 4u
-#pragma unroll
-            for (int r = 0; r < 4; ++r) acc_own[t >> 2][r] = g == (t & 3) ? acc[r] : acc_own[t >> 2][r];
+            // rows 4g .. 4g+3 of the product are all query g
+            xs[t] = acc[0];
             // value rows
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
@@ -417,85 +422,106 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
             }
         }
     }
-    // the slots of query r (ROW: only those of its own parent, half r >> 1)
-    bool okr[SPL][4];
-    float x[SPL][4];
+    // this lane's query g and its slots 16t + n16 (ROW: only those of its own parent, half g >> 1)
+    bool okt[NT];
+    float xt[NT];
 #pragma unroll
-    for (int u = 0; u < SPL; ++u)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            okr[u][r] = ROW ? ok[u] && (((64 * u + lane) >> 1) >= K) == ((r >> 1) != 0) : ok[u];
-            x[u][r] = okr[u][r] ? acc_own[u][r] * a.scale : -INFINITY;
-        }
+    for (int t = 0; t < NT; ++t) {
+        const int s = 16 * t + n16;
+        okt[t] = t < ntile && gok[t] && (!ROW || ((s >> 1) >= K) == ((g >> 1) != 0));
+        xt[t] = okt[t] ? xs[t] * a.scale : -INFINITY;
+    }
 
-    // ---- 3. weights ----
-    float wgt[SPL][4], inv_sum[4] = {1.f, 1.f, 1.f, 1.f};
-    // the finest level of B with 32 slots and d = 32: two queries per register (lanes 0..31 query
-    // 2p, lanes 32..63 query 2p+1, slot lane & 31), so that one reduction within each 32-lane half
-    // serves two queries; the weights stay packed for the P store below (with d = 64 the extra
-    // registers cost occupancy)
-    constexpr bool kPack = !VA && FINEST && NSP == 32 && !ROW && D == 32;
-    float wpk[2];
-    if constexpr (kPack) {
-        // (the cross-lane exchanges run with every lane active, before the per-half selects)
-        const bool upper = lane >= 32;
-        const uint32_t ok_hi = xchg_u32<32>(ok[0] ? 1u : 0u);
-        const bool okp = upper ? ok_hi != 0u : ok[0];
+    // ---- 3. weights (unnormalised for B: exp(x - max); the 1/sum is applied to the message) ----
+    float wt[NT];
+    float inv_g = 1.f;                                       // B: 1/sum of this lane's query
+    if constexpr (!VA) {
+        float m = xt[0];
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-            const float hi = xchg_f32<32>(x[0][2 * p + 1]);
-            const float y = upper ? hi : x[0][2 * p];
-            const float m = half_allreduce(y, [](float u, float v) { return fmaxf(u, v); });
-            wpk[p] = okp ? __expf(y - m) : 0.f;
-            const float inv = fast_rcp(half_allreduce(wpk[p], [](float u, float v) { return u + v; }));   // >= 1
-            inv_sum[2 * p] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(inv), 0));
-            inv_sum[2 * p + 1] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(inv), 32));
+        for (int t = 1; t < NT; ++t) m = fmaxf(m, xt[t]);
+        m = row_allreduce(m, [](float u, float v) { return fmaxf(u, v); });
+        float se = 0.f;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            wt[t] = okt[t] ? __expf(xt[t] - m) : 0.f;
+            se += wt[t];
         }
-    } else if constexpr (!VA) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float xm = x[0][r];
-#pragma unroll
-            for (int u = 1; u < SPL; ++u) xm = fmaxf(xm, x[u][r]);
-            const float m = wave_max_fast(xm);
-            float se = 0.f;
-#pragma unroll
-            for (int u = 0; u < SPL; ++u) {
-                wgt[u][r] = okr[u][r] ? __expf(x[u][r] - m) : 0.f;
-                se += wgt[u][r];
-            }
-            inv_sum[r] = fast_rcp(wave_sum_fast(se));   // the sum is at least 1 (the maximum's term)
-        }
+        inv_g = fast_rcp(row_allreduce(se, [](float u, float v) { return u + v; }));   // >= 1: the maximum's term
     } else {
 #pragma unroll
-        for (int u = 0; u < SPL; ++u)
+        for (int t = 0; t < NT; ++t) {
+            // t: a softmax over the children of one kept key (a lane quad; ROW: a lane pair)
+            float m = fmaxf(xt[t], xchg_f32<1>(xt[t]));
+            if constexpr (!ROW) m = fmaxf(m, xchg_f32<2>(m));
+            const float e = okt[t] ? __expf(xt[t] - m) : 0.f;
+            float se = e + xchg_f32<1>(e);
+            if constexpr (!ROW) se += xchg_f32<2>(se);
+            wt[t] = okt[t] ? pkey[t] * e * fast_rcp(se) : 0.f;   // se >= 1
+        }
+    }
+    // the four queries' normalisers, wave-uniform
+    float inv_sum[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                // t: a softmax over the children of one kept key (a lane quad; ROW: a lane pair)
-                float m = fmaxf(x[u][r], xchg_f32<1>(x[u][r]));
-                if constexpr (!ROW) m = fmaxf(m, xchg_f32<2>(m));
-                const float e = okr[u][r] ? __expf(x[u][r] - m) : 0.f;
-                float s = e + xchg_f32<1>(e);
-                if constexpr (!ROW) s += xchg_f32<2>(s);
-                wgt[u][r] = okr[u][r] ? pkey[u] * e * fast_rcp(s) : 0.f;  // s >= 1
-            }
+    for (int r = 0; r < 4; ++r) inv_sum[r] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(inv_g), 16 * r));
+
+    // ---- 5a. the weights P into the wave's LDS, [query][slot] ----
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        if (t >= ntile) break;                               // uniform
+        const int s = 16 * t + n16;
+        if constexpr (kBf16)
+            reinterpret_cast<uint16_t*>(Pb)[g * nsp + s] = static_cast<uint16_t>(f32_to_bf16_bits(wt[t]));
+        else
+            reinterpret_cast<float*>(Pb)[g * nsp + s] = wt[t];
     }
 
     // ---- 4. this level's selection (levels above the finest) ----
     if constexpr (!FINEST) {
+        // the ranking keys (B: the logit, ordered as the probability; A: the score) to one slot per
+        // lane: tiles 4u .. 4u+3 of query row g become query r's keys of slots 64u + lane
+        float kvs[SPL][4];
+#pragma unroll
+        for (int u = 0; u < SPL; ++u) {
+            float c[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int t = 4 * u + j;
+                c[j] = t < NT ? (VA ? wt[t] : xt[t]) : (VA ? 0.f : -INFINITY);
+            }
+            rows_transpose4(c);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) kvs[u][r] = c[r];
+        }
+        // B: query r's maximum logit, for its kept keys' probabilities
+        float mx[4] = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (!VA) {
+            float m = xt[0];
+#pragma unroll
+            for (int t = 1; t < NT; ++t) m = fmaxf(m, xt[t]);
+            m = row_allreduce(m, [](float u, float v) { return fmaxf(u, v); });
+#pragma unroll
+            for (int r = 0; r < 4; ++r) mx[r] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m), 16 * r));
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             int qy, qx;
             query_yx(r, qy, qx);
             if (qy >= H || qx >= W) continue;                 // uniform across the wave
+            bool okr[SPL];
+            float kv[SPL];
             int nvalid = 0;
 #pragma unroll
-            for (int u = 0; u < SPL; ++u) nvalid += __popcll(__ballot(okr[u][r]));
+            for (int u = 0; u < SPL; ++u) {
+                const int s = 64 * u + lane;
+                okr[u] = ROW ? ok[u] && ((s >> 1) >= K) == ((r >> 1) != 0) : ok[u];
+                kv[u] = kvs[u][r];
+                nvalid += __popcll(__ballot(okr[u]));
+            }
             const int keff = Ks < nvalid ? Ks : nvalid;
             uint32_t key[SPL], name[SPL];
 #pragma unroll
             for (int u = 0; u < SPL; ++u) {
-                key[u] = okr[u][r] ? ordered_bits(VA ? wgt[u][r] : x[u][r]) : 0u;
+                key[u] = okr[u] ? ordered_bits(kv[u]) : 0u;
                 name[u] = static_cast<uint32_t>(flat[u]);
             }
             bool kept[SPL];
@@ -508,8 +534,12 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                 if (kept[u]) {
                     const int pos = before + lanes_below(mask);
                     a.sel_idx[orow + pos] = flat[u];
-                    a.sel_key[orow + pos] = VA ? wgt[u][r] : wgt[u][r] * inv_sum[r];
-                    if constexpr (VA) wgt[u][r] = 0.f;        // refined at the next level (Omega)
+                    a.sel_key[orow + pos] = VA ? kv[u] : __expf(kv[u] - mx[r]) * inv_sum[r];
+                    if constexpr (VA) {                       // refined at the next level (Omega)
+                        const int s = 64 * u + lane;
+                        if constexpr (kBf16) reinterpret_cast<uint16_t*>(Pb)[r * nsp + s] = 0;
+                        else reinterpret_cast<float*>(Pb)[r * nsp + s] = 0.f;
+                    }
                 }
                 before += __popcll(mask);
             }
@@ -519,34 +549,9 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
             }
         }
     }
-
-    // ---- 5. messages on MFMA ----
-    if constexpr (kPack) {
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-            const int row = 2 * p + (lane >> 5);
-            if constexpr (kBf16)
-                reinterpret_cast<uint16_t*>(Pb)[row * nsp + (lane & 31)] = static_cast<uint16_t>(f32_to_bf16_bits(wpk[p]));
-            else
-                reinterpret_cast<float*>(Pb)[row * nsp + (lane & 31)] = wpk[p];
-        }
-    } else {
-#pragma unroll
-        for (int u = 0; u < SPL; ++u) {
-            const int s = 64 * u + lane;
-            if (s < nsp) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    if constexpr (kBf16)
-                        reinterpret_cast<uint16_t*>(Pb)[r * nsp + s] = static_cast<uint16_t>(f32_to_bf16_bits(wgt[u][r]));
-                    else
-                        reinterpret_cast<float*>(Pb)[r * nsp + s] = wgt[u][r];
-                }
-            }
-        }
-    }
     wave_lds_sync();
 
+    // ---- 5b. messages on MFMA ----
     const int sph = nsp / NH;
     float4_t o = {0.f, 0.f, 0.f, 0.f};
     if constexpr (kBf16) {

@@ -171,6 +171,32 @@ __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcp
 // log-sum-exp of softmax sums, which are at least 1.
 __device__ __forceinline__ float fast_ln(float x) { return __builtin_amdgcn_logf(x) * 0.69314718056f; }
 
+// A 4x4 transpose across the wave's four 16-lane rows: on entry lane n of row i holds M[i][j] in
+// c[j]; on return lane n of row j holds M[i][j] in c[i]. Two rounds of row swaps: the first swaps
+// row pairs (0,1) and (2,3) between c[0]/c[1] and c[2]/c[3], the second the wave halves between
+// c[0]/c[2] and c[1]/c[3].
+__device__ __forceinline__ void rows_transpose4(float (&c)[4])
+{
+    const auto s01 = __builtin_amdgcn_permlane16_swap(__float_as_uint(c[0]), __float_as_uint(c[1]), false, false);
+    const auto s23 = __builtin_amdgcn_permlane16_swap(__float_as_uint(c[2]), __float_as_uint(c[3]), false, false);
+    const auto s02 = __builtin_amdgcn_permlane32_swap(s01[0], s23[0], false, false);
+    const auto s13 = __builtin_amdgcn_permlane32_swap(s01[1], s23[1], false, false);
+    c[0] = __uint_as_float(s02[0]);
+    c[1] = __uint_as_float(s13[0]);
+    c[2] = __uint_as_float(s02[1]);
+    c[3] = __uint_as_float(s13[1]);
+}
+
+// Butterfly all-reduce within each 16-lane row of the wave.
+template <typename Op>
+__device__ __forceinline__ float row_allreduce(float x, Op op)
+{
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppXor1, 0xF, 0xF, false)));
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppXor2, 0xF, 0xF, false)));
+    x = op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppRowHalfMirror, 0xF, 0xF, false)));
+    return op(x, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppRowMirror, 0xF, 0xF, false)));
+}
+
 // Butterfly all-reduce within each 32-lane half of the wave.
 template <typename Op>
 __device__ __forceinline__ float half_allreduce(float x, Op op)
