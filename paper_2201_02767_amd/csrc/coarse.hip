@@ -156,6 +156,31 @@ __global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
             load_v(p3_ks + NKS * kVBatch, vb2);
         }
     }
+    // The output element of this thread in the epilogue (Q*D <= the Q*64 threads: one each, or none),
+    // and for the fused position encoding its operands, requested now so that they arrive during
+    // the softmax: the 3x3 window of v around the query token (clamped addresses, zero outside the
+    // map through opaque masks), this channel's kernel and its bias.
+    static_assert(D <= kWave, "one output element per thread");
+    const int er = static_cast<int>(threadIdx.x) / D, ech = static_cast<int>(threadIdx.x) - er * D;
+    const int eqi = tile * Q + er;
+    float pev[9], pew[9], peb = 0.f;
+    if (a.pe_w) {                                    // uniform
+        const int Wc = a.Wc, Hc = N / Wc;
+        const int qc = min(eqi, N - 1);
+        const int qy = qc / Wc, qx = qc - qy * Wc;
+        const float* wk = a.pe_w + (static_cast<size_t>(h) * D + ech) * 9;
+#pragma unroll
+        for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+            for (int kx = 0; kx < 3; ++kx) {
+                const int yy = qy + ky - 1, xx = qx + kx - 1;
+                const int yc = min(max(yy, 0), Hc - 1), xc = min(max(xx, 0), Wc - 1);
+                const unsigned ok = opaque_mask(yy >= 0 && yy < Hc && xx >= 0 && xx < Wc);
+                pev[ky * 3 + kx] = masked(S::load1(a.v, (tok0 + yc * Wc + xc) * C + hoff + ech), ok);
+                pew[ky * 3 + kx] = wk[ky * 3 + kx];
+            }
+        peb = a.pe_b ? a.pe_b[h * D + ech] : 0.f;
+    }
     __syncthreads();
 
     // ---- phase 2: softmax and selection, one wave per query row ----
@@ -248,28 +273,18 @@ __global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
         for (int j = 0; j < 4; ++j) red[(wave * 16 + 4 * kgrp + j) * 16 + (lane & 15)] = acc[j];
     }
     __syncthreads();
-    for (int t = threadIdx.x; t < Q * D; t += blockDim.x) {
-        const int r = t / D, ch = t % D;
+    if (er < Q && eqi < N) {
+        const int r = er, ch = ech;
         const int ct = ch / 16, col = ch % 16;
         float s = 0.f;
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) s += red[((ks * NCT + ct) * 16 + r) * 16 + col];
-        const int qi = tile * Q + r;
-        if (qi >= N) continue;
+        const int qi = eqi;
         if (a.pe_w) {                                    // uniform: the fused position encoding
             // 3x3 depth-wise cross-correlation of v around token qi, zero outside the map, plus the bias
-            const int Wc = a.Wc, Hc = N / Wc;
-            const int qy = qi / Wc, qx = qi - qy * Wc;
-            const float* wk = a.pe_w + (static_cast<size_t>(h) * D + ch) * 9;
-            float pe = a.pe_b ? a.pe_b[h * D + ch] : 0.f;
+            float pe = peb;
 #pragma unroll
-            for (int ky = 0; ky < 3; ++ky)
-#pragma unroll
-                for (int kx = 0; kx < 3; ++kx) {
-                    const int yy = qy + ky - 1, xx = qx + kx - 1;
-                    if (yy < 0 || yy >= Hc || xx < 0 || xx >= Wc) continue;
-                    pe = fmaf(wk[ky * 3 + kx], S::load1(a.v, (tok0 + yy * Wc + xx) * C + hoff + ch), pe);
-                }
+            for (int k = 0; k < 9; ++k) pe = fmaf(pew[k], pev[k], pe);
             s += pe;
         }
         if (a.out) {

@@ -158,17 +158,6 @@ struct BwdRow {
 
 __device__ const float kUnitScale = 1.0f;   // stands in for w when QuadTree-B runs without it
 
-// All-ones if ok, else zero, in a form the compiler cannot see through. "ok ? load : 0" with a
-// visible condition is turned into a branch around the load, which then waits for it at once;
-// x & mask with an opaque mask keeps every load of a window row unconditional (their addresses
-// are clamped into the map) and in flight together.
-__device__ __forceinline__ unsigned opaque_mask(bool ok)
-{
-    unsigned m = ok ? 0xFFFFFFFFu : 0u;
-    asm volatile("" : "+v"(m));
-    return m;
-}
-__device__ __forceinline__ float masked(float x, unsigned m) { return __uint_as_float(__float_as_uint(x) & m); }
 
 // The work of one block; LEVEL0: a block of level 0 (dm from dout and w), else of a coarser level.
 template <typename T, bool LEVEL0>

@@ -171,6 +171,18 @@ __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcp
 // log-sum-exp of softmax sums, which are at least 1.
 __device__ __forceinline__ float fast_ln(float x) { return __builtin_amdgcn_logf(x) * 0.69314718056f; }
 
+// All-ones if ok, else zero, in a form the compiler cannot see through. A visible "ok ? load : 0"
+// is turned into a branch around the load, which then waits for it at once; x & mask with an
+// opaque mask keeps a batch of loads (at clamped, always valid addresses) unconditional and in
+// flight together.
+__device__ __forceinline__ unsigned opaque_mask(bool ok)
+{
+    unsigned m = ok ? 0xFFFFFFFFu : 0u;
+    asm volatile("" : "+v"(m));
+    return m;
+}
+__device__ __forceinline__ float masked(float x, unsigned m) { return __uint_as_float(__float_as_uint(x) & m); }
+
 // A 4x4 transpose across the wave's four 16-lane rows: on entry lane n of row i holds M[i][j] in
 // c[j]; on return lane n of row j holds M[i][j] in c[i]. Two rounds of row swaps: the first swaps
 // row pairs (0,1) and (2,3) between c[0]/c[1] and c[2]/c[3], the second the wave halves between
