@@ -265,6 +265,78 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
             }
         }
     };
+    // Output ownership (step 6): lane 4*blk + t4 with blk = cg*NH + hh owns channel 4*cg + t4 of
+    // queries hh*QPL .. hh*QPL + QPL-1.
+    const int blk = lane >> 2, t4 = lane & 3;
+    const int cg = blk / NH, hh = blk % NH;
+    const int ch = 4 * cg + t4;
+    constexpr int kPre = FINEST ? kPrefetchLevels : 1;
+    float anc[ROW ? QPL : 1][kPre];     // ROW: the two parents of a pair have different ancestors
+    float wq[FINEST ? QPL : 1][kPre + 1];
+    float peq[FINEST ? QPL : 1] = {};
+    const bool prefetch = FINEST && a.levels <= kPre + 1;
+    // the finest level's combination inputs (ancestors' messages, w, the encoding of level 0). With
+    // d = 64 they are requested before the gathers (backbone's layer 75.6 -> 72.5 us); with d = 32,
+    // or with the fused encoding's own early loads, that costs more occupancy than it saves (stereo
+    // +0.6 us, backbone_pe +3 us), so there they follow the gathers, and their latency overlaps the
+    // softmax and the messages
+    constexpr bool kEarlyCombination = D == 64 && !PE;
+    auto request_combination = [&]() {
+        if constexpr (FINEST) {
+            if (prefetch) {                                      // uniform
+                const int L = a.levels;
+#pragma unroll
+                for (int lev = 1; lev <= kPre; ++lev) {
+                    if (lev >= L) break;                         // uniform
+                    if constexpr (ROW) {
+#pragma unroll
+                        for (int u = 0; u < QPL; ++u) {
+                            const int qi = (NH == 2 ? hh * QPL : 0) + u;
+                            // clamped: a query off the map may lie past the last ancestor
+                            const uint32_t an = min((2 * P + qi) >> lev, a.lvl_W[lev] - 1);
+                            anc[u][lev - 1] = (a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C))
+                                                  [an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)];
+                        }
+                    } else {
+                        // the ancestor is shared by the four siblings: a uniform address plus the channel
+                        const uint32_t an = static_cast<uint32_t>(((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev));
+                        anc[0][lev - 1] = (a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C))
+                                              [an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)];
+                    }
+                }
+                if (a.pe0) {                                     // uniform
+                    const float* pb = a.pe0 + (static_cast<size_t>(b) * N * a.heads + h) * D + ch;
+#pragma unroll
+                    for (int u = 0; u < QPL; ++u) {
+                        const int qi = (NH == 2 ? hh * QPL : 0) + u;
+                        int py, px;
+                        query_yx(qi, py, px);
+                        py = min(py, H - 1);
+                        px = min(px, W - 1);
+                        peq[u] = pb[static_cast<uint32_t>(__mul24(py, W) + px) * static_cast<uint32_t>(a.heads * D)];
+                    }
+                }
+                if (!VA && a.w) {                                // uniform
+                    const float* wb = a.w + (static_cast<size_t>(b) * N * a.heads + h) * L;
+#pragma unroll
+                    for (int u = 0; u < QPL; ++u) {
+                        const int qi = (NH == 2 ? hh * QPL : 0) + u;
+                        int wy, wx;
+                        query_yx(qi, wy, wx);
+                        wy = min(wy, H - 1);
+                        wx = min(wx, W - 1);
+                        const float* wrow = wb + static_cast<uint32_t>(__mul24(wy, W) + wx) * static_cast<uint32_t>(a.heads * L);
+#pragma unroll
+                        for (int lev = 0; lev <= kPre; ++lev) {
+                            if (lev >= L) break;                 // uniform
+                            wq[u][lev] = wrow[lev];
+                        }
+                    }
+                }
+            }
+        }
+    };
+    if constexpr (kEarlyCombination) request_combination();
     load_tiles(0);
     int flat[SPL];
     bool ok[SPL];
@@ -333,16 +405,10 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
         load_tiles(t0);
         consume_tiles(t0);
     }
-    // Output ownership (step 6): lane 4*blk + t4 with blk = cg*NH + hh owns channel 4*cg + t4 of
-    // queries hh*QPL .. hh*QPL + QPL-1.
-    const int blk = lane >> 2, t4 = lane & 3;
-    const int cg = blk / NH, hh = blk % NH;
-    const int ch = 4 * cg + t4;
-    constexpr int kPre = FINEST ? kPrefetchLevels : 1;
     // fused position encoding: the 4x4 tokens (2Py-1 .. 2Py+2) x (2Px-1 .. 2Px+2) of v around the
     // sibling block, token n16 = (by, bx), chunks g, g+4, ... of its row (as in the gathers; tokens off
     // the map read a clamped row and count as zero), and this lane's channel's 3x3 kernel and bias,
-    // requested before the ancestors' rows so that their latency overlaps the weights and the messages
+    // requested here so that their latency overlaps the weights and the messages
     uint4 peb[PE ? NJ : 1];
     float pek[PE ? 9 : 1];
     float pebias = 0.f;
@@ -363,65 +429,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
         for (int i = 0; i < 9; ++i) pek[i] = wp[i];
         pebias = a.pe_b ? a.pe_b[h * D + ch] : 0.f;
     }
-    float anc[ROW ? QPL : 1][kPre];     // ROW: the two parents of a pair have different ancestors
-    float wq[FINEST ? QPL : 1][kPre + 1];
-    float peq[FINEST ? QPL : 1] = {};
-    const bool prefetch = FINEST && a.levels <= kPre + 1;
-    // the finest level's combination inputs, requested once the gathered registers are free; their
-    // latency overlaps the softmax and the messages
-    if constexpr (FINEST) {
-        if (prefetch) {                                      // uniform
-            const int L = a.levels;
-#pragma unroll
-            for (int lev = 1; lev <= kPre; ++lev) {
-                if (lev >= L) break;                         // uniform
-                if constexpr (ROW) {
-#pragma unroll
-                    for (int u = 0; u < QPL; ++u) {
-                        const int qi = (NH == 2 ? hh * QPL : 0) + u;
-                        // clamped: a query off the map may lie past the last ancestor
-                        const uint32_t an = min((2 * P + qi) >> lev, a.lvl_W[lev] - 1);
-                        anc[u][lev - 1] = (a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C))
-                                              [an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)];
-                    }
-                } else {
-                    // the ancestor is shared by the four siblings: a uniform address plus the channel
-                    const uint32_t an = static_cast<uint32_t>(((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev));
-                    anc[0][lev - 1] = (a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C))
-                                          [an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)];
-                }
-            }
-            if (a.pe0) {                                     // uniform
-                const float* pb = a.pe0 + (static_cast<size_t>(b) * N * a.heads + h) * D + ch;
-#pragma unroll
-                for (int u = 0; u < QPL; ++u) {
-                    const int qi = (NH == 2 ? hh * QPL : 0) + u;
-                    int py, px;
-                    query_yx(qi, py, px);
-                    py = min(py, H - 1);
-                    px = min(px, W - 1);
-                    peq[u] = pb[static_cast<uint32_t>(__mul24(py, W) + px) * static_cast<uint32_t>(a.heads * D)];
-                }
-            }
-            if (!VA && a.w) {                                // uniform
-                const float* wb = a.w + (static_cast<size_t>(b) * N * a.heads + h) * L;
-#pragma unroll
-                for (int u = 0; u < QPL; ++u) {
-                    const int qi = (NH == 2 ? hh * QPL : 0) + u;
-                    int wy, wx;
-                    query_yx(qi, wy, wx);
-                    wy = min(wy, H - 1);
-                    wx = min(wx, W - 1);
-                    const float* wrow = wb + static_cast<uint32_t>(__mul24(wy, W) + wx) * static_cast<uint32_t>(a.heads * L);
-#pragma unroll
-                    for (int lev = 0; lev <= kPre; ++lev) {
-                        if (lev >= L) break;                 // uniform
-                        wq[u][lev] = wrow[lev];
-                    }
-                }
-            }
-        }
-    }
+    if constexpr (!kEarlyCombination) request_combination();
     // this lane's query g and its slots 16t + n16 (ROW: only those of its own parent, half g >> 1)
     bool okt[NT];
     float xt[NT];
