@@ -24,7 +24,7 @@ __global__ __launch_bounds__(256) void fine_attn_kernel(FineArgs a)
     extern __shared__ __align__(16) unsigned char smem[];
     const int nsp = (4 * a.Kp + 15) & ~15;
     ItemHead<T, D, NSP, VA, ROW> hd;
-    item_head<T, D, NSP, VA, ROW>(a, item, hd);
+    item_head<T, D, NSP, VA, ROW, FINEST>(a, item, hd);
     fine_item<T, D, NSP, VA, FINEST, ROW, PE>(a, hd, smem + static_cast<size_t>(wave) * wave_lds<T, D>(nsp).total);
 }
 
@@ -101,6 +101,7 @@ hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool bf16_
 {
     const int nslot = 4 * a.Kp;
     if (nslot > kMaxSlots || (a.pe_w && nslot > kMaxSlotsPe)) return hipErrorInvalidValue;
+    if (finest && (a.q_blocked || a.kv_blocked)) return hipErrorInvalidValue;   // level 0 is NHWC
     FineArgs b = a;
     b.div_Wp = make_fastdiv(a.Wp);
     b.div_heads = make_fastdiv(a.heads);

@@ -101,7 +101,8 @@ struct ItemHead {
     uint4 qa[D * sizeof(T) / 64];
 };
 
-template <typename T, int D, int NSP, bool VA, bool ROW>
+// FINEST: the finest level, whose queries are always stored NHWC (the layout flag is not read).
+template <typename T, int D, int NSP, bool VA, bool ROW, bool FINEST>
 __device__ __forceinline__ void item_head(const FineArgs& a, const int item, ItemHead<T, D, NSP, VA, ROW>& hd)
 {
     constexpr int TB = sizeof(T);
@@ -147,13 +148,14 @@ __device__ __forceinline__ void item_head(const FineArgs& a, const int item, Ite
     const int qyc = qy < H ? qy : H - 1, qxc = qx < W ? qx : W - 1;
     // uniform base of this (batch, head) plus a 32-bit per-lane offset. ROW, blocked: query 4p + qi
     // is child qi & 1 of parent 2p + (qi >> 1)
+    const bool qb = !FINEST && a.q_blocked;
     const unsigned char* qbase = static_cast<const unsigned char*>(a.q) +
-        (a.q_blocked ? ((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 * RB
+        (qb ? ((static_cast<size_t>(b) * a.heads + h) * Np + P) * 4 * RB
                      : (static_cast<size_t>(b) * H * W * C + h * D) * TB);
     // (a query off the map may belong to a parent past the last one: read the first block instead)
     const int qblk = ROW ? (hd.q_ok ? (qi >> 1) * 4 + (qi & 1) : 0) : qi;
-    const uint32_t qoff = a.q_blocked ? static_cast<uint32_t>(qblk * RB)
-                                      : static_cast<uint32_t>(__mul24(qyc, W) + qxc) * static_cast<uint32_t>(C * TB);
+    const uint32_t qoff = qb ? static_cast<uint32_t>(qblk * RB)
+                                      : __umul24(static_cast<uint32_t>(__mul24(qyc, W) + qxc), static_cast<uint32_t>(C * TB));
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
         hd.qa[j] = *reinterpret_cast<const uint4*>(qbase + (qoff + static_cast<uint32_t>((g + 4 * j) * 16)));
@@ -201,16 +203,19 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
 
     // flat index at level l of child (s & 3) of kept key J (a level l+1 index), or -1. Map sizes are
     // below 2^24 tokens, so coordinate products fit the 24-bit multiplier. ROW: child s & 1 of J.
+    // Computed without branches: the early returns of a plain form became divergent branches per
+    // tile, with their exec-mask bookkeeping on the scalar unit.
     auto child_of_slot_J = [&](int J, int s) -> int {
-        if (s >= nslot || J < 0) return -1;
+        const int Jc = J < 0 ? 0 : J;
         if constexpr (ROW) {
-            if (!pair2 && s >= 2 * K) return -1;
-            const int cx = 2 * J + (s & 1);
-            return cx < W ? cx : -1;
+            const int cx = 2 * Jc + (s & 1);
+            const bool ok = s < nslot && J >= 0 && (pair2 || s < 2 * K) && cx < W;
+            return ok ? cx : -1;
         }
-        const int Jy = fast_div(J, a.div_Wp), Jx = J - __mul24(Jy, a.Wp);
+        const int Jy = fast_div(Jc, a.div_Wp), Jx = Jc - __mul24(Jy, a.Wp);
         const int cy = 2 * Jy + ((s >> 1) & 1), cx = 2 * Jx + (s & 1);
-        return (cy < H && cx < W) ? __mul24(cy, W) + cx : -1;
+        const bool ok = s < nslot && J >= 0 && cy < H && cx < W;
+        return ok ? __mul24(cy, W) + cx : -1;
     };
     // query r of the item: its map coordinates
     auto query_yx = [&](int r, int& qy, int& qx) {
@@ -225,6 +230,11 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
 
     // ---- 1. loads: item_head issued the phase A loads (kept keys, scores, query rows); phase B,
     //      the gathers, needs the kept keys ----
+    // With more tiles than one batch of registers holds, a compiler barrier: the kept keys of the
+    // later batches (gathered behind a uniform bound) would otherwise be sunk to those batches,
+    // leaving each a dependent load chain of its own (detection's 128-slot finest level +1.6 us).
+    // With a single batch the barrier only constrains the schedule (backbone's finest +2 us).
+    if constexpr (NT > kTB) asm volatile("" ::: "memory");
     const int n16 = lane & 15, g = lane >> 4;
     const int ntile = nsp / 16;
     const int (&J_g)[NT] = hd.J_g;
@@ -238,11 +248,14 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     const uint4 (&qa)[NJ] = hd.qa;
     // phase B: the gathers. NHWC: child f of this head at kg + f*C*TB. Blocked: the four children
     // of kept key J are the 4*RB bytes at kg + J*4*RB (this (batch, head)'s blocks start at kg).
-    const bool kvb = a.kv_blocked;
+    // The finest level's keys and values are always NHWC.
+    const bool kvb = !FINEST && a.kv_blocked;
     const size_t kv_base = kvb ? (static_cast<size_t>(b) * a.heads + h) * Np * 4 * RB
                                : (static_cast<size_t>(b) * N * C + h * D) * TB;
     const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base;
     const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base;
+    // at most 4 MiB (heads*d <= 2^20 by the host checks): token index times row bytes fits the
+    // 24-bit multiplier
     const uint32_t tok_bytes = static_cast<uint32_t>(C * TB);
     bool gok[NT];
 #pragma unroll
@@ -255,9 +268,16 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
             if (t >= NT || t >= ntile) break;                 // uniform
             const int f = child_of_slot_J(J_g[t], s);
             gok[t] = f >= 0;
-            // 32-bit byte offset within this (batch, head)'s map (below 2^31 by the host's checks)
-            const uint32_t goff = (!gok[t] ? 0u : (kvb ? static_cast<uint32_t>(J_g[t] * 4 + (ROW ? (s & 1) : (s & 3))) * RB
-                                                        : static_cast<uint32_t>(f) * tok_bytes)) + g * 16;
+            // 32-bit byte offset within this (batch, head)'s map (below 2^31 by the host's checks); a
+            // missing candidate reads the map's first row
+            uint32_t off = __umul24(static_cast<uint32_t>(gok[t] ? f : 0), tok_bytes);
+            if constexpr (!FINEST) {
+                // the layout as a mask, not a branch per tile
+                const unsigned kvb_m = opaque_mask(kvb);
+                const uint32_t boff = static_cast<uint32_t>(gok[t] ? J_g[t] * 4 + (ROW ? (s & 1) : (s & 3)) : 0) * RB;
+                off = (boff & kvb_m) | (off & ~kvb_m);
+            }
+            const uint32_t goff = off + g * 16;
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
                 kc[i][j] = *reinterpret_cast<const uint4*>(kg + (goff + 64 * j));
@@ -275,13 +295,15 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     float wq[FINEST ? QPL : 1][kPre + 1];
     float peq[FINEST ? QPL : 1] = {};
     const bool prefetch = FINEST && a.levels <= kPre + 1;
-    // the finest level's combination inputs (ancestors' messages, w, the encoding of level 0). With
-    // d = 64 they are requested before the gathers (backbone's layer 75.6 -> 72.5 us); with d = 32,
-    // or with the fused encoding's own early loads, that costs more occupancy than it saves (stereo
-    // +0.6 us, backbone_pe +3 us), so there they follow the gathers, and their latency overlaps the
-    // softmax and the messages
+    // the finest level's combination inputs: the ancestors' messages and the encoding of level 0,
+    // and w. With d = 64 (and no fused encoding) the ancestors and the encoding are requested before
+    // the gathers (backbone's layer 75.9 -> 73.2 us); with d = 32, or with the fused encoding's own
+    // early loads, that costs more occupancy than it saves (stereo +0.6 us, backbone_pe +3 us), so
+    // there they follow the gathers, and their latency overlaps the softmax and the messages. w
+    // always follows the gathers: its twenty scattered loads per lane ahead of them held the gathers
+    // back (backbone +1.9 us).
     constexpr bool kEarlyCombination = D == 64 && !PE;
-    auto request_combination = [&]() {
+    auto request_ancestors = [&]() {
         if constexpr (FINEST) {
             if (prefetch) {                                      // uniform
                 const int L = a.levels;
@@ -316,6 +338,13 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                         peq[u] = pb[static_cast<uint32_t>(__mul24(py, W) + px) * static_cast<uint32_t>(a.heads * D)];
                     }
                 }
+            }
+        }
+    };
+    auto request_weights = [&]() {
+        if constexpr (FINEST) {
+            if (prefetch) {                                      // uniform
+                const int L = a.levels;
                 if (!VA && a.w) {                                // uniform
                     const float* wb = a.w + (static_cast<size_t>(b) * N * a.heads + h) * L;
 #pragma unroll
@@ -336,7 +365,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
             }
         }
     };
-    if constexpr (kEarlyCombination) request_combination();
+    if constexpr (kEarlyCombination) request_ancestors();
     load_tiles(0);
     int flat[SPL];
     bool ok[SPL];
@@ -421,7 +450,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
         // parent block (by >> 1, bx >> 1)
         const uint32_t boff = (kvb ? static_cast<uint32_t>(((__mul24(byc >> 1, a.Wp) + (bxc >> 1)) * 4 + (byc & 1) * 2 +
                                                             (bxc & 1)) * RB)
-                                   : static_cast<uint32_t>(__mul24(byc, W) + bxc) * tok_bytes) + g * 16;
+                                   : __umul24(static_cast<uint32_t>(__mul24(byc, W) + bxc), tok_bytes)) + g * 16;
 #pragma unroll
         for (int j = 0; j < NJ; ++j) peb[j] = *reinterpret_cast<const uint4*>(vg + (boff + 64 * j));
         const float* wp = a.pe_w + static_cast<uint32_t>(h * D + ch) * 9u;
@@ -429,7 +458,8 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
         for (int i = 0; i < 9; ++i) pek[i] = wp[i];
         pebias = a.pe_b ? a.pe_b[h * D + ch] : 0.f;
     }
-    if constexpr (!kEarlyCombination) request_combination();
+    if constexpr (!kEarlyCombination) request_ancestors();
+    request_weights();
     // this lane's query g and its slots 16t + n16 (ROW: only those of its own parent, half g >> 1)
     bool okt[NT];
     float xt[NT];
