@@ -186,37 +186,60 @@ __global__ __launch_bounds__(256) void pyramid_pass2_kernel(PyramidPassArgs a, i
         S::pack(o);
 }
 
-// Three-level pass, workgroup = tpb top tokens (level s+3). A unit is one 16-byte chunk of one
-// level-1 token under a top token (NC * NC level-1 tokens each); a thread takes units tid,
-// tid + 256, ... (at most R), loads the 2x2 source chunks of all of them before pooling any, writes
-// the level-1 tokens and stages them in LDS; after a barrier the threads pool the staged level-1
-// tokens into level 2 (written and staged again), and after a second barrier into the top tokens.
-// ROW (maps of one row): two children per token, as in the two-level pass.
-template <typename T, bool ROW, int R>
-__global__ __launch_bounds__(256) void pyramid_pass3_kernel(PyramidPassArgs a, int tpb)
+// Three- or four-level pass (NLEV), workgroup = tpb top tokens (level s+NLEV). A unit is one
+// 16-byte chunk of one level-1 token under a top token (NC^(NLEV-1) level-1 tokens each); a thread
+// takes units tid, tid + 256, ... (at most R), loads the 2x2 source chunks of all of them before
+// pooling any, writes the level-1 tokens and stages them in LDS; after each barrier the threads pool
+// the staged tokens of one level into the next (written and staged again), up to the top tokens.
+// Staged tokens are in hierarchical order (top token, then the child index at each level below
+// it), so the NC children of staged token i of one level are tokens NC*i .. NC*i + NC-1 of the level
+// below. ROW (maps of one row): two children per token, as in the two-level pass.
+template <typename T, bool ROW, int R, int NLEV>
+__global__ __launch_bounds__(256) void pyramid_passn_kernel(PyramidPassArgs a, int tpb)
 {
+    static_assert(NLEV == 3 || NLEV == 4, "three- or four-level pass");
     using S = Storage<T>;
     constexpr int E = S::kPer16B;
     constexpr int NC = ROW ? 2 : 4;
+    constexpr int LNC = ROW ? 1 : 2;                   // log2(NC)
     __shared__ uint4 stage1[256 * R];
     __shared__ uint4 stage2[256 * R / NC];
+    __shared__ uint4 stage3[NLEV == 4 ? 256 * R / (NC * NC) : 1];
     const int tensor = blockIdx.y;
     const char* __restrict__ src = static_cast<const char*>(a.src[tensor]);
-    char* __restrict__ dst1 = static_cast<char*>(a.dst1[tensor]);
-    char* __restrict__ dst2 = static_cast<char*>(a.dst2[tensor]);
-    char* __restrict__ dst3 = static_cast<char*>(a.dst3[tensor]);
     const int chunks = a.chunks;
-    const int per2 = NC * chunks;                      // units of one level-2 token
-    const int U = NC * per2;                           // units of one top token
+    const int L1 = 1 << (LNC * (NLEV - 1));            // level-1 tokens under one top token
+    const int U = L1 * chunks;                         // units of one top token
     const int nunits = tpb * U;
-    const int ntop = a.B * a.H3 * a.W3;                // < 2^31, checked by the launcher
+    const int Ht = NLEV == 4 ? a.H4 : a.H3, Wt = NLEV == 4 ? a.W4 : a.W3;
+    const int ntop = a.B * Ht * Wt;                    // < 2^31, checked by the launcher
     const int top0 = static_cast<int>(blockIdx.x) * tpb;
-    // (b, Y, X) of the workgroup's top token t, clamped onto the last one past the end
-    auto top_pos = [&](int t, int& b, int& Y, int& X) {
+    // level j's map, destination and layout (j = 1 .. NLEV, compile-time after unrolling)
+    auto lvl_H = [&](int j) { return j == 1 ? a.H1 : j == 2 ? a.H2 : j == 3 ? a.H3 : a.H4; };
+    auto lvl_W = [&](int j) { return j == 1 ? a.W1 : j == 2 ? a.W2 : j == 3 ? a.W3 : a.W4; };
+    auto lvl_dst = [&](int j) {
+        return static_cast<char*>(j == 1 ? a.dst1[tensor] : j == 2 ? a.dst2[tensor] : j == 3 ? a.dst3[tensor]
+                                                                                                : a.dst4[tensor]);
+    };
+    auto lvl_blocked = [&](int j) {
+        return j == 1 ? a.dst1_blocked : j == 2 ? a.dst2_blocked : j == 3 ? a.dst3_blocked : a.dst4_blocked;
+    };
+    // (b, y, x) at level j of staged token `tok` of that level (hierarchical order); the top token is
+    // clamped onto the last one past the end. Returns whether the top token exists.
+    auto level_pos = [&](int j, int tok, int& b, int& y, int& x) {
+        const int sh = LNC * (NLEV - j);               // child digits below the top token
+        const int t = tok >> sh;
         const int top = min(top0 + t, ntop - 1);
-        X = top % a.W3;
-        Y = (top / a.W3) % a.H3;
-        b = top / (a.W3 * a.H3);
+        x = top % Wt;
+        y = (top / Wt) % Ht;
+        b = top / (Wt * Ht);
+#pragma unroll
+        for (int k = NLEV - j - 1; k >= 0; --k) {
+            const int q = (tok >> (LNC * k)) & (NC - 1);
+            y = ROW ? 0 : 2 * y + (q >> 1);
+            x = 2 * x + (ROW ? q : (q & 1));
+        }
+        return top0 + t < ntop;
     };
 
     int b1[R], y1[R], x1[R], ch1[R];
@@ -226,16 +249,10 @@ __global__ __launch_bounds__(256) void pyramid_pass3_kernel(PyramidPassArgs a, i
     for (int it = 0; it < R; ++it) {
         const int u0 = it * 256 + static_cast<int>(threadIdx.x);
         const int u = min(u0, nunits - 1);
-        const int t = u / U, r = u - t * U;
-        const int l1 = r / chunks;
-        ch1[it] = r - l1 * chunks;
-        const int q2 = l1 / NC, q1 = l1 - q2 * NC;
-        int Y, X;
-        top_pos(t, b1[it], Y, X);
-        const int y2 = ROW ? 0 : 2 * Y + (q2 >> 1), x2 = 2 * X + (ROW ? q2 : (q2 & 1));
-        y1[it] = ROW ? 0 : 2 * y2 + (q1 >> 1);
-        x1[it] = 2 * x2 + (ROW ? q1 : (q1 & 1));
-        ok1[it] = u0 < nunits && top0 + t < ntop && y1[it] < a.H1 && x1[it] < a.W1;
+        const int tok = u / chunks;
+        ch1[it] = u - tok * chunks;
+        const bool top_ok = level_pos(1, tok, b1[it], y1[it], x1[it]);
+        ok1[it] = u0 < nunits && top_ok && y1[it] < a.H1 && x1[it] < a.W1;
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             if (ROW && i == 1) {                           // no row below
@@ -252,6 +269,7 @@ __global__ __launch_bounds__(256) void pyramid_pass3_kernel(PyramidPassArgs a, i
             }
         }
     }
+    char* __restrict__ dst1 = lvl_dst(1);
 #pragma unroll
     for (int it = 0; it < R; ++it) {
         float c00[E], c01[E], c10[E], c11[E], mid[E];
@@ -268,78 +286,67 @@ __global__ __launch_bounds__(256) void pyramid_pass3_kernel(PyramidPassArgs a, i
                                                           ch1[it], chunks, a.head_chunks)) = packed;
         stage1[it * 256 + threadIdx.x] = packed;
     }
-    __syncthreads();
 
-    // level 2: one unit per (level-2 token, chunk); its children are staged at (q2 * NC + q1) * chunks
-    const int n2 = tpb * per2;
-    for (int u = threadIdx.x; u < n2; u += 256) {
-        const int t = u / per2, r = u - t * per2;
-        const int q2 = r / chunks, ch = r - q2 * chunks;
-        int b, Y, X;
-        top_pos(t, b, Y, X);
-        const int y2 = ROW ? 0 : 2 * Y + (q2 >> 1), x2 = 2 * X + (ROW ? q2 : (q2 & 1));
-        const int base = t * U + q2 * per2 + ch;
-        float m0[E], m1[E], m2[E], m3[E], o[E];
-        S::unpack(stage1[base], m0);
-        S::unpack(stage1[base + chunks], m1);
-        S::unpack(stage1[base + (ROW ? 0 : 2) * chunks], m2);   // ROW: unused (no row below)
-        S::unpack(stage1[base + (ROW ? 1 : 3) * chunks], m3);
-        pool_children<E>(m0, m1, m2, m3, 2 * x2 + 1 < a.W1, !ROW && 2 * y2 + 1 < a.H1, o);
+    // levels 2 .. NLEV: one unit per (staged token, chunk), its children staged at
+    // (NC * tok + q) * chunks + ch one level below
 #pragma unroll
-        for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
-        const uint4 packed = S::pack(o);
-        if (top0 + t < ntop && y2 < a.H2 && x2 < a.W2)
-            *reinterpret_cast<uint4*>(dst2 + chunk_offset(a.dst2_blocked, b, y2, x2, a.H2, a.W2, ch, chunks,
-                                                          a.head_chunks)) = packed;
-        stage2[u] = packed;
-    }
-    __syncthreads();
-
-    // top level: one unit per (top token, chunk); its children are staged at q2 * chunks
-    const int n3 = tpb * chunks;
-    for (int u = threadIdx.x; u < n3; u += 256) {
-        const int t = u / chunks, ch = u - t * chunks;
-        if (top0 + t >= ntop) break;
-        int b, Y, X;
-        top_pos(t, b, Y, X);
-        const int base = t * per2 + ch;
-        float m0[E], m1[E], m2[E], m3[E], o[E];
-        S::unpack(stage2[base], m0);
-        S::unpack(stage2[base + chunks], m1);
-        S::unpack(stage2[base + (ROW ? 0 : 2) * chunks], m2);
-        S::unpack(stage2[base + (ROW ? 1 : 3) * chunks], m3);
-        pool_children<E>(m0, m1, m2, m3, 2 * X + 1 < a.W2, !ROW && 2 * Y + 1 < a.H2, o);
+    for (int j = 2; j <= NLEV; ++j) {
+        __syncthreads();
+        const uint4* below = j == 2 ? stage1 : j == 3 ? stage2 : stage3;
+        uint4* here = j == 2 ? stage2 : stage3;          // (the top level is not staged)
+        const int n = (tpb << (LNC * (NLEV - j))) * chunks;
+        const int Hb = lvl_H(j - 1), Wb = lvl_W(j - 1), Hj = lvl_H(j), Wj = lvl_W(j);
+        char* __restrict__ dst = lvl_dst(j);
+        const bool blk = lvl_blocked(j);
+        for (int u = threadIdx.x; u < n; u += 256) {
+            const int tok = u / chunks, ch = u - tok * chunks;
+            int b, y, x;
+            const bool top_ok = level_pos(j, tok, b, y, x);
+            const int base = NC * tok * chunks + ch;
+            float m0[E], m1[E], m2[E], m3[E], o[E];
+            S::unpack(below[base], m0);
+            S::unpack(below[base + chunks], m1);
+            S::unpack(below[base + (ROW ? 0 : 2) * chunks], m2);   // ROW: unused (no row below)
+            S::unpack(below[base + (ROW ? 1 : 3) * chunks], m3);
+            pool_children<E>(m0, m1, m2, m3, 2 * x + 1 < Wb, !ROW && 2 * y + 1 < Hb, o);
 #pragma unroll
-        for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
-        *reinterpret_cast<uint4*>(dst3 + chunk_offset(a.dst3_blocked, b, Y, X, a.H3, a.W3, ch, chunks,
-                                                      a.head_chunks)) = S::pack(o);
+            for (int e = 0; e < E; ++e) o[e] = S::round(o[e]);
+            const uint4 packed = S::pack(o);
+            if (top_ok && y < Hj && x < Wj)
+                *reinterpret_cast<uint4*>(dst + chunk_offset(blk, b, y, x, Hj, Wj, ch, chunks, a.head_chunks)) = packed;
+            if (j < NLEV) here[u] = packed;
+        }
     }
 }
 
 }  // namespace
 
-template <typename T, bool ROW>
-static hipError_t launch_pass3(const PyramidPassArgs& a, int ntensors, hipStream_t stream)
+template <typename T, bool ROW, int NLEV>
+static hipError_t launch_passn(const PyramidPassArgs& a, int ntensors, hipStream_t stream)
 {
-    const int U = (ROW ? 4 : 16) * a.chunks;
+    const int U = (1 << ((ROW ? 1 : 2) * (NLEV - 1))) * a.chunks;
     const int tpb = U >= 256 ? 1 : 256 / U;
     const int R = (tpb * U + 255) / 256;
-    const long long ntop = static_cast<long long>(a.B) * a.H3 * a.W3;
+    const long long ntop = static_cast<long long>(a.B) * (NLEV == 4 ? a.H4 : a.H3) * (NLEV == 4 ? a.W4 : a.W3);
     if (ntop <= 0 || ntop > 0x7FFFFFFFLL || R > 4) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>((ntop + tpb - 1) / tpb), ntensors);
-    if (R == 1) hipLaunchKernelGGL((pyramid_pass3_kernel<T, ROW, 1>), grid, dim3(256), 0, stream, a, tpb);
-    else if (R == 2) hipLaunchKernelGGL((pyramid_pass3_kernel<T, ROW, 2>), grid, dim3(256), 0, stream, a, tpb);
-    else hipLaunchKernelGGL((pyramid_pass3_kernel<T, ROW, 4>), grid, dim3(256), 0, stream, a, tpb);
+    if (R == 1) hipLaunchKernelGGL((pyramid_passn_kernel<T, ROW, 1, NLEV>), grid, dim3(256), 0, stream, a, tpb);
+    else if (R == 2) hipLaunchKernelGGL((pyramid_passn_kernel<T, ROW, 2, NLEV>), grid, dim3(256), 0, stream, a, tpb);
+    else hipLaunchKernelGGL((pyramid_passn_kernel<T, ROW, 4, NLEV>), grid, dim3(256), 0, stream, a, tpb);
     return hipGetLastError();
 }
 
 hipError_t launch_pyramid_pass(const PyramidPassArgs& a, int nlev, int ntensors, bool use_bf16, hipStream_t stream)
 {
-    if (nlev == 3) {
+    if (nlev == 3 || nlev == 4) {
         const bool row = a.Hs == 1;
-        if (!pyramid_pass3_fits(a.chunks, row)) return hipErrorInvalidValue;
-        if (use_bf16) return row ? launch_pass3<bf16, true>(a, ntensors, stream) : launch_pass3<bf16, false>(a, ntensors, stream);
-        return row ? launch_pass3<float, true>(a, ntensors, stream) : launch_pass3<float, false>(a, ntensors, stream);
+        if (!pyramid_passn_fits(nlev, a.chunks, row)) return hipErrorInvalidValue;
+        if (nlev == 3) {
+            if (use_bf16) return row ? launch_passn<bf16, true, 3>(a, ntensors, stream) : launch_passn<bf16, false, 3>(a, ntensors, stream);
+            return row ? launch_passn<float, true, 3>(a, ntensors, stream) : launch_passn<float, false, 3>(a, ntensors, stream);
+        }
+        if (use_bf16) return row ? launch_passn<bf16, true, 4>(a, ntensors, stream) : launch_passn<bf16, false, 4>(a, ntensors, stream);
+        return row ? launch_passn<float, true, 4>(a, ntensors, stream) : launch_passn<float, false, 4>(a, ntensors, stream);
     }
     if (nlev == 2 && 4 * a.chunks <= 256) {
         const bool row = a.Hs == 1;                       // maps of one row: two children per token

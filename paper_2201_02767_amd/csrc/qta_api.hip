@@ -171,22 +171,25 @@ float resolve_scale(float scale, int d) { return scale > 0.f ? scale : 1.0f / __
 
 qta_status launch_status(hipError_t e) { return e == hipSuccess ? QTA_OK : QTA_ERR_HIP; }
 
-// Pyramid passes: from level s produce s+1, s+2 and s+3 when exactly those remain (and the tokens
-// fit the three-level pass), else s+1 and, when it exists, s+2; repeat from the last level made.
+// Pyramid passes: from level s produce s+1 .. s+4 when exactly those remain, or s+1 .. s+3 when
+// exactly those remain (and the tokens fit the four- or three-level pass), else s+1 and, when it
+// exists, s+2; repeat from the last level made.
 // `blocked` gives the storage of each level (level 0, the input, is NHWC).
 hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], int ntensors, int B,
                        const int* Hl, const int* Wl, const int* blocked, int levels, int chunks, int head_chunks,
                        bool use_bf16, hipStream_t stream)
 {
     for (int s = 0; s + 1 < levels;) {
-        const bool three = levels - s == 4 && pyramid_pass3_fits(chunks, Hl[s] == 1);
-        const int nlev = three ? 3 : (s + 2 < levels) ? 2 : 1;
+        const bool four = levels - s == 5 && pyramid_passn_fits(4, chunks, Hl[s] == 1);
+        const bool three = levels - s == 4 && pyramid_passn_fits(3, chunks, Hl[s] == 1);
+        const int nlev = four ? 4 : three ? 3 : (s + 2 < levels) ? 2 : 1;
         PyramidPassArgs a{};
         for (int t = 0; t < ntensors; ++t) {
             a.src[t] = s == 0 ? src0[t] : lvl[t][s];
             a.dst1[t] = lvl[t][s + 1];
             a.dst2[t] = nlev >= 2 ? lvl[t][s + 2] : nullptr;
-            a.dst3[t] = nlev == 3 ? lvl[t][s + 3] : nullptr;
+            a.dst3[t] = nlev >= 3 ? lvl[t][s + 3] : nullptr;
+            a.dst4[t] = nlev == 4 ? lvl[t][s + 4] : nullptr;
         }
         a.B = B;
         a.Hs = Hl[s];
@@ -195,14 +198,17 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], in
         a.W1 = Wl[s + 1];
         a.H2 = nlev >= 2 ? Hl[s + 2] : 0;
         a.W2 = nlev >= 2 ? Wl[s + 2] : 0;
-        a.H3 = nlev == 3 ? Hl[s + 3] : 0;
-        a.W3 = nlev == 3 ? Wl[s + 3] : 0;
+        a.H3 = nlev >= 3 ? Hl[s + 3] : 0;
+        a.W3 = nlev >= 3 ? Wl[s + 3] : 0;
+        a.H4 = nlev == 4 ? Hl[s + 4] : 0;
+        a.W4 = nlev == 4 ? Wl[s + 4] : 0;
         a.chunks = chunks;
         a.head_chunks = head_chunks;
         a.src_blocked = s > 0 && blocked[s];
         a.dst1_blocked = blocked[s + 1] != 0;
         a.dst2_blocked = nlev >= 2 && blocked[s + 2] != 0;
-        a.dst3_blocked = nlev == 3 && blocked[s + 3] != 0;
+        a.dst3_blocked = nlev >= 3 && blocked[s + 3] != 0;
+        a.dst4_blocked = nlev == 4 && blocked[s + 4] != 0;
         hipError_t e = launch_pyramid_pass(a, nlev, ntensors, use_bf16, stream);
         if (e != hipSuccess) return e;
         s += nlev;

@@ -48,15 +48,19 @@ struct PyramidPassArgs {
     void* dst1[3];
     void* dst2[3];
     void* dst3[3];
-    int B, Hs, Ws, H1, W1, H2, W2, H3, W3;
+    void* dst4[3];
+    int B, Hs, Ws, H1, W1, H2, W2, H3, W3, H4, W4;
     int chunks;                 // 16-byte chunks per token (C * sizeof(dtype) / 16)
     int head_chunks;            // 16-byte chunks per head row (d * sizeof(dtype) / 16)
-    bool src_blocked, dst1_blocked, dst2_blocked, dst3_blocked;
+    bool src_blocked, dst1_blocked, dst2_blocked, dst3_blocked, dst4_blocked;
 };
 
-// Whether the three-level pass takes tokens of `chunks` 16-byte chunks (maps of one row when
-// `row`): a top token's level-1 children must fit 1024 chunks, four per thread.
-inline bool pyramid_pass3_fits(int chunks, bool row) { return (row ? 4 : 16) * chunks <= 1024; }
+// Whether the three- or four-level pass (nlev) takes tokens of `chunks` 16-byte chunks (maps of
+// one row when `row`): a top token's level-1 children must fit 1024 chunks, four per thread.
+inline bool pyramid_passn_fits(int nlev, int chunks, bool row)
+{
+    return (1 << ((row ? 1 : 2) * (nlev - 1))) * chunks <= 1024;
+}
 
 struct CoarseArgs {
     const void* q;

@@ -114,6 +114,10 @@ def run_and_compare(dev, q, k, v, *, levels, K, variant, dtype, w=None, scale=No
     # three-level pass: 3 of 4 chunk slots per thread used; one-row maps with two level-2 rounds;
     # 8 top tokens per workgroup
     ("f32", 2, 21, 27, 160, 4), ("bf16", 3, 1, 45, 1600, 4), ("f32", 2, 9, 7, 8, 4),
+    # four-level pass: 2 top tokens per workgroup; 4 chunk slots per thread; one-row maps; a ragged
+    # map; after a two-level pass (7 levels)
+    ("f32", 2, 9, 7, 8, 5), ("f32", 1, 37, 29, 64, 5), ("bf16", 2, 1, 77, 64, 5), ("bf16", 1, 17, 35, 32, 5),
+    ("f32", 1, 70, 90, 32, 7),
 ])
 def test_pyramid_bit_exact(dev, dtype, B, H, W, C, L):
     rng = np.random.default_rng(H * W + C)
