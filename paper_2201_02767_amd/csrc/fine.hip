@@ -103,6 +103,7 @@ hipError_t launch_fine_attn(const FineArgs& a, int d, bool variant_a, bool bf16_
     if (nslot > kMaxSlots || (a.pe_w && nslot > kMaxSlotsPe)) return hipErrorInvalidValue;
     if (finest && (a.q_blocked || a.kv_blocked)) return hipErrorInvalidValue;   // level 0 is NHWC
     FineArgs b = a;
+    b.inv_levels = a.levels > 0 ? 1.0f / static_cast<float>(a.levels) : 0.f;
     b.div_Wp = make_fastdiv(a.Wp);
     b.div_heads = make_fastdiv(a.heads);
     const int np = a.Hp * a.Wp;

@@ -134,11 +134,13 @@ __device__ __forceinline__ void item_head(const FineArgs& a, const int item, Ite
     constexpr int kSlotShift = ROW ? 1 : 2;
     const int last_sel = (ROW && pair2 ? 2 * K : K) - 1;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) hd.J_g[t] = prow[min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)];
+    for (int t = 0; t < NT; ++t)
+        hd.J_g[t] = load_at<int32_t>(prow, static_cast<uint32_t>(min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)) * 4u);
     if constexpr (VA) {
         const float* pk = a.parent_key + ((static_cast<size_t>(b) * a.heads + h) * Np + P) * K;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) hd.pkey[t] = pk[min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)];
+        for (int t = 0; t < NT; ++t)
+            hd.pkey[t] = load_at<float>(pk, static_cast<uint32_t>(min(((16 * t) >> kSlotShift) + (n16 >> kSlotShift), last_sel)) * 4u);
     } else {
         hd.pkey[0] = 0.f;
     }
@@ -316,14 +318,14 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                             const int qi = (NH == 2 ? hh * QPL : 0) + u;
                             // clamped: a query off the map may lie past the last ancestor
                             const uint32_t an = min((2 * P + qi) >> lev, a.lvl_W[lev] - 1);
-                            anc[u][lev - 1] = (a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C))
-                                                  [an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)];
+                            anc[u][lev - 1] = load_at<float>(a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C),
+                                                             (an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)) * 4u);
                         }
                     } else {
                         // the ancestor is shared by the four siblings: a uniform address plus the channel
                         const uint32_t an = static_cast<uint32_t>(((2 * Py) >> lev) * a.lvl_W[lev] + ((2 * Px) >> lev));
-                        anc[0][lev - 1] = (a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C))
-                                              [an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)];
+                        anc[0][lev - 1] = load_at<float>(a.coarser_msg[lev] + static_cast<size_t>(b) * static_cast<uint32_t>(a.lvl_N[lev] * C),
+                                                         (an * static_cast<uint32_t>(C) + static_cast<uint32_t>(h * D + ch)) * 4u);
                     }
                 }
                 if (a.pe0) {                                     // uniform
@@ -354,11 +356,12 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                         query_yx(qi, wy, wx);
                         wy = min(wy, H - 1);
                         wx = min(wx, W - 1);
-                        const float* wrow = wb + static_cast<uint32_t>(__mul24(wy, W) + wx) * static_cast<uint32_t>(a.heads * L);
+                        // (a batch element's w is below 2^31 bytes: heads*L*4 <= heads*d*b)
+                        const uint32_t wrow = __umul24(static_cast<uint32_t>(__mul24(wy, W) + wx), static_cast<uint32_t>(a.heads * L));
 #pragma unroll
                         for (int lev = 0; lev <= kPre; ++lev) {
                             if (lev >= L) break;                 // uniform
-                            wq[u][lev] = wrow[lev];
+                            wq[u][lev] = load_at<float>(wb, (wrow + lev) * 4u);
                         }
                     }
                 }
@@ -693,11 +696,12 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
         const uint32_t qpos = static_cast<uint32_t>(__mul24(qy, W) + qx);      // token within the map
         if constexpr (!FINEST) {
             float* mb = a.msg + (static_cast<size_t>(b) * N * a.heads + h) * D;  // uniform
-            mb[qpos * static_cast<uint32_t>(a.heads * D) + ch] = PE ? m + pe_f[PE ? u : 0] : m;
+            // (a batch element's message is below 2^32 bytes: twice a bf16 map at most)
+            store_at<float>(mb, (qpos * static_cast<uint32_t>(a.heads * D) + ch) * 4u, PE ? m + pe_f[PE ? u : 0] : m);
         } else {
             const size_t qtok = static_cast<size_t>(b) * N + qpos;
             const int L = a.levels;
-            const float wdef = 1.0f / L;
+            const float wdef = a.inv_levels;
             float out;
             if (prefetch) {
                 out = (VA ? 1.0f : (a.w ? wq[u][0] : wdef)) * (m + (PE ? pe_f[PE ? u : 0] : peq[u]));
@@ -718,7 +722,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                 }
             }
             void* ob = static_cast<unsigned char*>(a.out) + (static_cast<size_t>(b) * N * C + h * D) * TB;  // uniform
-            S::store1(ob, qpos * static_cast<uint32_t>(C) + ch, out);
+            S::store1_at(ob, qpos * static_cast<uint32_t>(C) + ch, out);
         }
     }
 }

@@ -28,6 +28,20 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f)
     return u >> 16;
 }
 
+// An access at a 32-bit byte offset from a wave-uniform base: the address is the base in scalar
+// registers plus the zero-extended per-lane offset, the form the hardware takes directly (a signed
+// or 64-bit index costs a 64-bit add per lane). The offset must stay below 2^32.
+template <typename V>
+__device__ __forceinline__ V load_at(const void* base, uint32_t byte_off)
+{
+    return *reinterpret_cast<const V*>(static_cast<const unsigned char*>(base) + byte_off);
+}
+template <typename V>
+__device__ __forceinline__ void store_at(void* base, uint32_t byte_off, V x)
+{
+    *reinterpret_cast<V*>(static_cast<unsigned char*>(base) + byte_off) = x;
+}
+
 template <typename T> struct Storage;
 
 template <> struct Storage<float> {
@@ -52,6 +66,8 @@ template <> struct Storage<float> {
     {
         static_cast<float*>(base)[i] = x;
     }
+    // element i (below 2^30) of a wave-uniform base
+    __device__ static __forceinline__ void store1_at(void* base, uint32_t i, float x) { store_at<float>(base, i * 4u, x); }
     // Round an fp32 value to this storage type and back.
     __device__ static __forceinline__ float round(float x) { return x; }
 };
@@ -81,6 +97,11 @@ template <> struct Storage<bf16> {
     __device__ static __forceinline__ void store1(void* base, size_t i, float x)
     {
         static_cast<uint16_t*>(base)[i] = static_cast<uint16_t>(f32_to_bf16_bits(x));
+    }
+    // element i (below 2^31) of a wave-uniform base
+    __device__ static __forceinline__ void store1_at(void* base, uint32_t i, float x)
+    {
+        store_at<uint16_t>(base, i * 2u, static_cast<uint16_t>(f32_to_bf16_bits(x)));
     }
     __device__ static __forceinline__ float round(float x) { return __uint_as_float(f32_to_bf16_bits(x) << 16); }
 };

@@ -135,6 +135,7 @@ struct FineArgs {
                                 // [C][3][3], applied to v around each query and added to m0; or NULL
     const float* pe_b;          // its bias, fp32 [C], or NULL
     int levels;
+    float inv_levels;           // 1/levels, the weight of every level without w (set by the launcher)
     const float* coarser_msg[QTA_MAX_LEVELS];   // entry j: message of level j (j >= 1)
     int lvl_W[QTA_MAX_LEVELS];                  // map width of level j
     int lvl_N[QTA_MAX_LEVELS];                  // tokens of level j
