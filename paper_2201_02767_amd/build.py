@@ -30,10 +30,11 @@ FLAGS = [
 # IEEE mode asks for, which lets each butterfly step fuse into one DPP max.
 NO_NAN_SOURCES = {"fine.hip", "coarse.hip", "backward.hip", "coarse_bwd.hip"}
 
-# The fine kernels keep one accumulator per 16-slot tile; with the MFMA results in VGPRs instead of
-# AGPRs (the compiler's default) they hold the same values in fewer registers in total, which keeps
-# 8 waves per SIMD for 64 slots and raises the 128- and 256-slot instantiations by one or two.
-MFMA_VGPR_SOURCES = {"fine.hip"}
+# The fine kernels and the backward query pass keep one accumulator per 16-slot tile; with the MFMA
+# results in VGPRs instead of AGPRs (the compiler's default) they hold the same values in fewer
+# registers in total, which keeps 8 waves per SIMD for 64 slots in the forward and raises the
+# 128- and 256-slot instantiations, and the 64-slot backward query passes, by one or two.
+MFMA_VGPR_SOURCES = {"fine.hip", "backward.hip"}
 
 
 def _compile(src: str) -> str:

@@ -127,16 +127,16 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
     int J_g[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) J_g[t] = prow[min(4 * t + (n16 >> 2), last_sel)];
-    int J_own = -1;
+    // QuadTree-A: the parent's score of this lane's slot in each tile
+    float pkey[VA ? NT : 1];
+    if constexpr (VA) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t) J_own = g == t ? J_g[t] : J_own;
-    const int flat = child_of_slot_J(lane < nslot ? J_own : -1, lane);
-    const bool ok = flat >= 0;
-    float pkey = 0.f;
-    if constexpr (VA) pkey = a.parent_key[prow_off * K + min(lane >> 2, last_sel)];
+        for (int t = 0; t < NT; ++t) pkey[t] = a.parent_key[prow_off * K + min(4 * t + (n16 >> 2), last_sel)];
+    }
 
-    // queries: A operand row n16 holds query n16 & 3
-    const int qi = n16 & 3;
+    // queries: A operand rows 4g .. 4g+3 hold query g, so lane 16g + n receives query g's logit (and
+    // <dm, v>) of slot 16t + n from every tile t
+    const int qi = n16 >> 2;
     const int qy = 2 * Py + (qi >> 1), qx = 2 * Px + (qi & 1);
     const bool q_ok = qy < H && qx < W;
     const uint32_t qtok = static_cast<uint32_t>(__mul24(min(qy, H - 1), W) + min(qx, W - 1));
@@ -176,23 +176,18 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             }
         }
     }
-    // level 0: w_{r,0} of the four queries (QuadTree-B; 1/L without w; 1 for A). Per batch element a
-    // 64-bit base, within it 32-bit offsets (one element's map is below 2^31 bytes, and so are its
+    // level 0: w_{g,0} (QuadTree-B; 1/L without w; 1 for A), below. Per batch element
+    // a 64-bit base, within it 32-bit offsets (one element's map is below 2^31 bytes, and so are its
     // level weights and softmax statistics)
     const size_t wq_off = static_cast<size_t>(b) * static_cast<uint32_t>(N * a.heads * a.levels);
     const float* wq_b = a.w + wq_off;
     float* const st_b = a.stats + static_cast<size_t>(b * a.heads + h) * static_cast<uint32_t>(N * 2 * (VA ? K : 1));
-    float w0[4] = {1.f, 1.f, 1.f, 1.f};
-    bool qv[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
-        qv[r] = ry < H && rx < W;
-        if constexpr (FINEST && !VA) {
-            const uint32_t rt = static_cast<uint32_t>(__mul24(min(ry, H - 1), W) + min(rx, W - 1));
-            w0[r] = a.w ? wq_b[(rt * a.heads + h) * a.levels] : 1.0f / a.levels;
-        }
-    }
+    // the products' lanes hold query g (row g of the wave): its position, and w_{g,0}
+    const int ry_q = 2 * Py + (g >> 1), rx_q = 2 * Px + (g & 1);
+    const bool qv = ry_q < H && rx_q < W;                     // this lane's query lies on the map
+    const uint32_t qpos = static_cast<uint32_t>(__mul24(min(ry_q, H - 1), W) + min(rx_q, W - 1));
+    float w0 = 1.f;
+    if constexpr (FINEST && !VA) w0 = a.w ? wq_b[(qpos * a.heads + h) * a.levels] : 1.0f / a.levels;
     // how many parents kept each key of level l+1 (for the key pass's counting sort); the count a
     // pair finds is its place in the key's list
     if (lane < K) {
@@ -207,15 +202,25 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
     const unsigned char* kg = static_cast<const unsigned char*>(a.k) + kv_base;
     const unsigned char* vg = static_cast<const unsigned char*>(a.v) + kv_base;
     const uint32_t tok_bytes = static_cast<uint32_t>(C * TB);
-    float acc_x[4] = {0.f, 0.f, 0.f, 0.f}, acc_g[4] = {0.f, 0.f, 0.f, 0.f};
+    float acc_x[NT], acc_g[NT];
+    bool gok[NT];
+    int flat_t[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        acc_x[t] = 0.f;
+        acc_g[t] = 0.f;
+        gok[t] = false;
+        flat_t[t] = -1;
+    }
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         if (t >= ntile) break;                                // uniform
         const int s = 16 * t + n16;
         const int f = child_of_slot_J(J_g[t], s);
-        const bool gok = f >= 0;
-        const uint32_t goff = (!gok ? 0u : (kvb ? static_cast<uint32_t>(J_g[t] * 4 + (s & 3)) * RB
-                                                 : static_cast<uint32_t>(f) * tok_bytes)) + g * 16;
+        gok[t] = f >= 0;
+        flat_t[t] = f;
+        const uint32_t goff = (!gok[t] ? 0u : (kvb ? static_cast<uint32_t>(J_g[t] * 4 + (s & 3)) * RB
+                                                    : static_cast<uint32_t>(f) * tok_bytes)) + g * 16;
         uint4 kc[NJ], vc[NJ];
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
@@ -225,8 +230,8 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
         float4_t ax = {0.f, 0.f, 0.f, 0.f}, ag = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
-            const uint4 kk = gok ? kc[j] : make_uint4(0, 0, 0, 0);
-            const uint4 vv = gok ? vc[j] : make_uint4(0, 0, 0, 0);
+            const uint4 kk = gok[t] ? kc[j] : make_uint4(0, 0, 0, 0);
+            const uint4 vv = gok[t] ? vc[j] : make_uint4(0, 0, 0, 0);
             if constexpr (kBf16) {
                 ax = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qa[j]),
                                                              __builtin_bit_cast(bf16x8_t, kk), ax, 0, 0, 0);
@@ -258,83 +263,111 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
                 *reinterpret_cast<uint4*>(Ks + s * lay.kpitch + (g + 4 * j) * E) = kk;
             }
         }
-        // rows 4g + r of the products are query r for every g: lane 16g + n keeps tile g
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            acc_x[r] = g == t ? ax[r] : acc_x[r];
-            acc_g[r] = g == t ? ag[r] : acc_g[r];
-        }
+        // rows 4g .. 4g+3 of the products are all query g
+        acc_x[t] = ax[0];
+        acc_g[t] = ag[0];
     }
 
-    // ---- softmax gradients of slot `lane` for the four queries ----
-    float x[4], gsl[4];
+    // ---- softmax gradients of this lane's query g, slots 16t + n16 ----
+    float x[NT], gsl[NT], dxt[NT];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        x[r] = ok ? acc_x[r] * a.scale : -INFINITY;
-        gsl[r] = FINEST ? w0[r] * acc_g[r] : acc_g[r];      // dLoss/d(weight) on Omega
+    for (int t = 0; t < NT; ++t) {
+        const bool okt = t < ntile && gok[t];
+        x[t] = okt ? acc_x[t] * a.scale : -INFINITY;
+        gsl[t] = FINEST ? w0 * acc_g[t] : acc_g[t];        // dLoss/d(weight) on Omega
+        dxt[t] = 0.f;
     }
-    float dxr[4];
-    const size_t bh = static_cast<size_t>(b) * a.heads + h;
-    if constexpr (!VA) {
+    // The sum over the query's slots of one value per tile, in the order of a butterfly over the
+    // 64 slots (each tile over its 16-lane row, then tiles (0 + 1) + (2 + 3)), so that the softmax
+    // statistics round as a full-wave sum of one slot per lane does
+    auto slots_sum = [&](const float (&v)[NT]) -> float {
+        float r[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float m = wave_max_fast(x[r]);
-            const float e = ok ? __expf(x[r] - m) : 0.f;
-            const float sum = wave_sum_fast(e);
-            const float p = e * fast_rcp(sum);                // sum >= 1 (the maximum's term)
-            const float Dr = wave_sum_fast(p * gsl[r]);
-            dxr[r] = qv[r] ? p * (gsl[r] - Dr) : 0.f;
-            // the key pass recomputes p = exp(x - lse) and needs D
-            if (lane == 0 && qv[r]) {
-                const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
-                *reinterpret_cast<float2*>(st_b + static_cast<uint32_t>(__mul24(ry, W) + rx) * 2) =
-                    make_float2(m + fast_ln(sum), Dr);
-            }
-            if constexpr (FINEST) {
-                if (a.w && a.dw) {                            // uniform
-                    const float dw0 = wave_sum_fast(p * acc_g[r]);
-                    if (lane == 0 && qv[r]) {
-                        const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
-                        a.dw[wq_off + static_cast<uint32_t>(((ry * W + rx) * a.heads + h) * a.levels)] = dw0;
-                    }
-                }
+        for (int t = 0; t < NT; ++t) r[t] = row_allreduce(v[t], [](float u, float w) { return u + w; });
+        return (r[0] + r[1]) + (r[2] + r[3]);
+    };
+    if constexpr (!VA) {
+        static_assert(NT <= 4, "at most 64 candidate slots");
+        // a softmax per query over its 16-lane row and the lane's tiles
+        float m = x[0];
+#pragma unroll
+        for (int t = 1; t < NT; ++t) m = fmaxf(m, x[t]);
+        m = row_allreduce(m, [](float u, float v) { return fmaxf(u, v); });
+        float e[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) e[t] = (t < ntile && gok[t]) ? __expf(x[t] - m) : 0.f;
+        const float sum = slots_sum(e);
+        const float inv = fast_rcp(sum);                      // sum >= 1 (the maximum's term)
+        float pg[NT], pa[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const float p = e[t] * inv;
+            e[t] = p;
+            pg[t] = p * gsl[t];
+            pa[t] = p * acc_g[t];
+        }
+        const float Dr = slots_sum(pg);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) dxt[t] = qv ? e[t] * (gsl[t] - Dr) : 0.f;
+        // the key pass recomputes p = exp(x - lse) and needs D
+        if (n16 == 0 && qv) *reinterpret_cast<float2*>(st_b + qpos * 2) = make_float2(m + fast_ln(sum), Dr);
+        if constexpr (FINEST) {
+            if (a.w && a.dw) {                                // uniform
+                const float dw0 = slots_sum(pa);
+                if (n16 == 0 && qv) a.dw[wq_off + static_cast<uint32_t>((qpos * a.heads + h) * a.levels)] = dw0;
             }
         }
     } else {
-        float dsig_acc = 0.f;
+        // d sigma of each slot's key: a key this lane's query keeps is refined at level l-1, and its
+        // score's gradient comes from there
+        float dsT[NT];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float m = fmaxf(x[r], xchg_f32<1>(x[r]));
+        for (int t = 0; t < NT; ++t) dsT[t] = gsl[t];
+        if constexpr (!FINEST) {
+            const size_t srow = ((static_cast<size_t>(b) * a.heads + h) * N + qpos) * a.Ks;
+            for (int mm = 0; mm < a.Ks; ++mm) {
+                const int kept = a.sel_idx[srow + mm];
+                const float dv = a.dsig_in[srow + mm];
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    if (t < ntile && gok[t] && kept == flat_t[t]) dsT[t] = dv;
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            if (t >= ntile) break;                            // uniform
+            const bool okt = gok[t];
+            // a softmax over the children of one kept key (a lane quad)
+            float m = fmaxf(x[t], xchg_f32<1>(x[t]));
             m = fmaxf(m, xchg_f32<2>(m));
-            const float e = ok ? __expf(x[r] - m) : 0.f;
+            const float e = okt ? __expf(x[t] - m) : 0.f;
             float sum = e + xchg_f32<1>(e);
             sum += xchg_f32<2>(sum);
-            const float tt = ok ? e * fast_rcp(sum) : 0.f;   // sum >= 1
-            const float sc = pkey * tt;
-            float ds = gsl[r];
-            if constexpr (!FINEST) {
-                // a key this query keeps is refined at level l-1: its score's gradient comes from there
-                const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
-                const size_t srow = ((static_cast<size_t>(b) * a.heads + h) * N + __mul24(min(ry, H - 1), W) +
-                                     min(rx, W - 1)) * a.Ks;
-                for (int mm = 0; mm < a.Ks; ++mm)
-                    if (ok && a.sel_idx[srow + mm] == flat) ds = a.dsig_in[srow + mm];
-            }
+            const float tt = okt ? e * fast_rcp(sum) : 0.f;   // sum >= 1
+            const float sc = pkey[t] * tt;
+            const float ds = dsT[t];
             float dsq = tt * ds;                              // this query's d sigma of the kept key
             dsq += xchg_f32<1>(dsq);
             dsq += xchg_f32<2>(dsq);
-            dxr[r] = qv[r] ? sc * (ds - dsq) : 0.f;
-            dsig_acc += qv[r] ? dsq : 0.f;
+            dxt[t] = qv ? sc * (ds - dsq) : 0.f;
             // the key pass recomputes t = exp(x - lse) per kept parent key and needs sum t ds
-            if ((lane & 3) == 0 && (lane >> 2) < K && qv[r]) {
-                const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
-                *reinterpret_cast<float2*>(st_b + static_cast<uint32_t>((__mul24(ry, W) + rx) * K + (lane >> 2)) * 2) =
+            const int key = 4 * t + (n16 >> 2);
+            if ((n16 & 3) == 0 && key < K && qv)
+                *reinterpret_cast<float2*>(st_b + static_cast<uint32_t>(qpos * K + key) * 2) =
                     make_float2(m + fast_ln(sum), dsq);
-            }
+            // the four queries' sum, across the wave's rows
+            float dsig = qv ? dsq : 0.f;
+            dsig += xchg_f32<16>(dsig);
+            dsig += xchg_f32<32>(dsig);
+            if (g == 0 && (n16 & 3) == 0 && key < K) a.dsig_out[prow_off * K + key] = dsig;
         }
-        if ((lane & 3) == 0 && (lane >> 2) < K) a.dsig_out[prow_off * K + (lane >> 2)] = dsig_acc;
     }
-    if (lane < nsp) *reinterpret_cast<float4*>(dxs + lane * 4) = make_float4(dxr[0], dxr[1], dxr[2], dxr[3]);
+    // the logit gradients into LDS as [slot][query] (the B operand of dq)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        if (t >= ntile) break;                                // uniform
+        dxs[(16 * t + n16) * 4 + g] = dxt[t];
+    }
     wave_lds_sync();
 
     // ---- dq = scale * sum_s dx_s k_s on the 4x4 MFMA (blocks over 4-channel groups, slot halves) ----
@@ -373,7 +406,7 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
     if constexpr (FINEST) {
         const int L = a.levels;
         const bool want_dw = !VA && a.w && a.dw;
-        const size_t wrow = ((static_cast<size_t>(b) * N + qtok) * a.heads + h) * L;    // query n16 & 3
+        const size_t wrow = ((static_cast<size_t>(b) * N + qtok) * a.heads + h) * L;    // query n16 >> 2
         float gv[NJ][E];
 #pragma unroll
         for (int j = 0; j < NJ; ++j) S::unpack(da[j], gv[j]);                    // zero off the map
@@ -412,9 +445,8 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
                     float sv[E];
 #pragma unroll
                     for (int e = 0; e < E; ++e) {
-                        sv[e] = wl[i] * gv[j][e];
-                        sv[e] += xchg_f32<1>(sv[e]);                              // the four queries
-                        sv[e] += xchg_f32<2>(sv[e]);
+                        // the four queries: query n16 >> 2 on lanes 4 apart (each on four lanes)
+                        sv[e] = row_sum_stride4(wl[i] * gv[j][e]);
                     }
                     if (want_dw) {
 #pragma unroll
@@ -439,7 +471,7 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
                 if (want_dw) {
                     part += xchg_f32<16>(part);
                     part += xchg_f32<32>(part);
-                    if (g == 0 && n16 < 4 && q_ok) a.dw[wrow + lv] = part;
+                    if (g == 0 && (n16 & 3) == 0 && q_ok) a.dw[wrow + lv] = part;
                 }
             }
         }

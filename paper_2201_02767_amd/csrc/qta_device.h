@@ -139,6 +139,7 @@ constexpr int kDppXor1 = 0xB1;         // quad_perm [1,0,3,2]
 constexpr int kDppXor2 = 0x4E;         // quad_perm [2,3,0,1]
 constexpr int kDppRowShl4 = 0x104;
 constexpr int kDppRowShr4 = 0x114;
+constexpr int kDppRowRor4 = 0x124;     // within a 16-lane row: lane (lane + 4) mod 16
 constexpr int kDppRowRor8 = 0x128;     // within a 16-lane row: lane ^ 8
 constexpr int kDppRowMirror = 0x140;   // within a row: lane -> 15 - lane
 constexpr int kDppRowHalfMirror = 0x141;  // within 8 lanes: lane -> 7 - lane
@@ -169,6 +170,14 @@ __device__ __forceinline__ uint32_t xchg_u32(uint32_t x)
 
 template <int M>
 __device__ __forceinline__ float xchg_f32(float x) { return __uint_as_float(xchg_u32<M>(__float_as_uint(x))); }
+
+// Sum over the four lanes n, n+4, n+8, n+12 of each 16-lane row (every one of them ends with it):
+// two row rotations.
+__device__ __forceinline__ float row_sum_stride4(float x)
+{
+    x += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppRowRor4, 0xF, 0xF, false));
+    return x + __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), kDppRowRor8, 0xF, 0xF, false));
+}
 
 // Butterfly all-reduce over the 64 lanes (every lane ends with the same value).
 template <typename Op>
