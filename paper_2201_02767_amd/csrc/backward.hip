@@ -873,12 +873,11 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
                             : ((static_cast<size_t>(b) * N + kc_tok) * C + h * D) * TB;
     uint4 kA[NJ], vA[NJ];
     float vAf[NJF][4];
+    const unsigned km = opaque_mask(kc_ok);                   // (a key off the map reads a clamped row)
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-        const uint4 kr = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.k) + krow + (g + 4 * j) * 16);
-        const uint4 vr = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.v) + krow + (g + 4 * j) * 16);
-        kA[j] = kc_ok ? kr : make_uint4(0, 0, 0, 0);
-        vA[j] = kc_ok ? vr : make_uint4(0, 0, 0, 0);
+        kA[j] = masked4(*reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.k) + krow + (g + 4 * j) * 16), km);
+        vA[j] = masked4(*reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.v) + krow + (g + 4 * j) * 16), km);
     }
     if constexpr (!FINEST) {
         // V in 4-channel chunks g, g+4, ... to meet the fp32 dm rows channel for channel
@@ -899,7 +898,7 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
                 vAf[j][3] = vr.w;
             }
 #pragma unroll
-            for (int e = 0; e < 4; ++e) vAf[j][e] = kc_ok ? vAf[j][e] : 0.f;
+            for (int e = 0; e < 4; ++e) vAf[j][e] = masked(vAf[j][e], km);
         }
     }
 
@@ -918,6 +917,15 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
 
     const int ntile = (nent + 3) / 4;                         // tiles that hold parents
     const int nsp = 16 * ntile;
+    // uniform bases of this (batch, head): query rows (blocked: this (batch, head)'s parent blocks),
+    // dout or dm rows, w (a batch element's map, its messages and w are below 2^32 bytes)
+    const unsigned char* const qb_base = kvb ? qbase + static_cast<size_t>(bh) * Np * 4 * RB
+                                             : qbase + (static_cast<size_t>(b) * N * C + h * D) * TB;
+    const unsigned char* const d_base = FINEST ? static_cast<const unsigned char*>(a.dout) +
+                                                     (static_cast<size_t>(b) * N * C + h * D) * TB
+                                               : nullptr;
+    const float* const m_base = FINEST ? nullptr : a.dm + static_cast<size_t>(b) * N * C + h * D;
+    const float* const w_base = a.w ? a.w + static_cast<size_t>(b) * N * a.heads * a.levels : nullptr;
     float acc_x[4] = {0.f, 0.f, 0.f, 0.f}, acc_g[4] = {0.f, 0.f, 0.f, 0.f};
     // each tile's dm chunks (level 0: w_0 dout; bf16: dout as stored), kept for dv
     float mreg[NT][kRows16 ? 1 : (FINEST ? NJ * E : NJF * 4)];
@@ -930,18 +938,18 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
         int P, r, qtok;
         bool qv;
         slot_query(s, ent, P, r, qtok, qv);
-        const size_t qrow = kvb ? ((static_cast<size_t>(bh) * Np + P) * 4 + (s & 3)) * RB
-                                : ((static_cast<size_t>(b) * N + qtok) * C + h * D) * TB;
-        const size_t grow = (static_cast<size_t>(b) * N + qtok) * C + h * D;      // elements
+        // every load unconditional at a clamped, valid address and zeroed for a slot without a
+        // query by an opaque mask (a visible select on a loaded value became a branch around the
+        // load that waited for it at the join); uniform bases with 32-bit per-lane offsets
+        const unsigned qm = opaque_mask(qv);
+        const uint32_t qoff = kvb ? static_cast<uint32_t>((P * 4 + (s & 3)) * RB)
+                                  : static_cast<uint32_t>(qtok) * static_cast<uint32_t>(C * TB);
         uint4 qB[NJ];
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const uint4 raw = *reinterpret_cast<const uint4*>(qbase + qrow + (g + 4 * j) * 16);
-            qB[j] = qv ? raw : make_uint4(0, 0, 0, 0);
-        }
+        for (int j = 0; j < NJ; ++j) qB[j] = masked4(load_at<uint4>(qb_base, qoff + (g + 4 * j) * 16), qm);
         float w0 = 1.0f;
         if constexpr (FINEST && !VA)
-            w0 = a.w ? a.w[((static_cast<size_t>(b) * N + qtok) * a.heads + h) * a.levels] : 1.0f / a.levels;
+            w0 = a.w ? load_at<float>(w_base, (static_cast<uint32_t>(qtok) * a.heads + h) * a.levels * 4u) : 1.0f / a.levels;
         float4_t ax = {0.f, 0.f, 0.f, 0.f}, ag = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
@@ -970,9 +978,8 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
             // <dout, v> on the storage type (times w_0 below), and w_0 dout in fp32 for dv
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
-                const uint4 raw = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(a.dout) +
-                                                                  (grow + (g + 4 * j) * E) * TB);
-                const uint4 dd = qv ? raw : make_uint4(0, 0, 0, 0);
+                const uint4 dd = masked4(load_at<uint4>(d_base, static_cast<uint32_t>(qtok) * static_cast<uint32_t>(C * TB) +
+                                                                    (g + 4 * j) * 16), qm);
                 if constexpr (kBf16) {
                     ag = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vA[j]),
                                                                  __builtin_bit_cast(bf16x8_t, dd), ag, 0, 0, 0);
@@ -995,8 +1002,10 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
             // <dm, v> with dm in fp32, 4-channel chunks g, g+4, ...
 #pragma unroll
             for (int j = 0; j < NJF; ++j) {
-                const float4 raw = *reinterpret_cast<const float4*>(a.dm + grow + (g + 4 * j) * 4);
-                const float4 dm4 = qv ? raw : make_float4(0.f, 0.f, 0.f, 0.f);
+                const uint4 dr = masked4(load_at<uint4>(m_base, (static_cast<uint32_t>(qtok) * static_cast<uint32_t>(C) +
+                                                                 (g + 4 * j) * 4) * 4u), qm);
+                const float4 dm4 = make_float4(__uint_as_float(dr.x), __uint_as_float(dr.y), __uint_as_float(dr.z),
+                                               __uint_as_float(dr.w));
                 ag = __builtin_amdgcn_mfma_f32_16x16x4f32(vAf[j][0], dm4.x, ag, 0, 0, 0);
                 ag = __builtin_amdgcn_mfma_f32_16x16x4f32(vAf[j][1], dm4.y, ag, 0, 0, 0);
                 ag = __builtin_amdgcn_mfma_f32_16x16x4f32(vAf[j][2], dm4.z, ag, 0, 0, 0);

@@ -212,6 +212,7 @@ __device__ __forceinline__ unsigned opaque_mask(bool ok)
     return m;
 }
 __device__ __forceinline__ float masked(float x, unsigned m) { return __uint_as_float(__float_as_uint(x) & m); }
+__device__ __forceinline__ uint4 masked4(uint4 v, unsigned m) { return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m); }
 
 // A 4x4 transpose across the wave's four 16-lane rows: on entry lane n of row i holds M[i][j] in
 // c[j]; on return lane n of row j holds M[i][j] in c[i]. Two rounds of row swaps: the first swaps
