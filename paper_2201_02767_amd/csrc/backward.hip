@@ -82,6 +82,13 @@ __device__ __forceinline__ float pick4(const float4_t& v, int i)
     return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
 }
 
+// v[off + i] for i in 0..3 (off a compile-time constant), by selects
+template <int N>
+__device__ __forceinline__ float pick4_at(const float (&v)[N], int off, int i)
+{
+    return i == 0 ? v[off] : i == 1 ? v[off + 1] : i == 2 ? v[off + 2] : v[off + 3];
+}
+
 // One work item: parent query P at level l+1 and head h (item = (b*Np + P)*heads + h); its four
 // children at level l share the candidate slots 4r + c (child c of the parent's kept key r).
 template <typename T, int D, int NSP, bool VA, bool FINEST>
@@ -372,6 +379,7 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
 
     // ---- dq = scale * sum_s dx_s k_s on the 4x4 MFMA (blocks over 4-channel groups, slot halves) ----
     {
+        float* const dq_b = a.dq + static_cast<size_t>(b) * N * C + h * D;
         const int blk = lane >> 2, t4 = lane & 3;
         const int cg = blk / NH, hh = blk % NH;
         const int ch = 4 * cg + t4;
@@ -395,7 +403,9 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
             const int r = (NH == 2 ? hh * QPL : 0) + u;
             const int ry = 2 * Py + (r >> 1), rx = 2 * Px + (r & 1);
             if (ry >= H || rx >= W) continue;
-            a.dq[(static_cast<size_t>(b) * N + __mul24(ry, W) + rx) * C + h * D + ch] = a.scale * pick4(o, r);
+            // (uniform base, 32-bit offset: a batch element's fp32 gradient is below 2^32 bytes)
+            store_at<float>(dq_b, (static_cast<uint32_t>(__mul24(ry, W) + rx) * static_cast<uint32_t>(C) + ch) * 4u,
+                            a.scale * pick4(o, r));
         }
     }
 
@@ -406,7 +416,9 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
     if constexpr (FINEST) {
         const int L = a.levels;
         const bool want_dw = !VA && a.w && a.dw;
-        const size_t wrow = ((static_cast<size_t>(b) * N + qtok) * a.heads + h) * L;    // query n16 >> 2
+        // w of query n16 >> 2: a uniform base and a 32-bit offset (a batch element's w is below 2^31 bytes)
+        const float* const w_b = a.w ? a.w + static_cast<size_t>(b) * N * a.heads * L : nullptr;
+        const uint32_t wrow = (qtok * static_cast<uint32_t>(a.heads) + h) * static_cast<uint32_t>(L);
         float gv[NJ][E];
 #pragma unroll
         for (int j = 0; j < NJ; ++j) S::unpack(da[j], gv[j]);                    // zero off the map
@@ -421,7 +433,7 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
 #pragma unroll
             for (int i = 0; i < kBlk; ++i) {
                 const int lv = min(lv0 + i, L - 1);                               // clamped: unused past L-1
-                wl[i] = VA ? 1.0f : (a.w ? a.w[wrow + lv] : 1.0f / L);
+                wl[i] = VA ? 1.0f : (a.w ? load_at<float>(w_b, (wrow + lv) * 4u) : 1.0f / L);
                 const size_t anc = static_cast<size_t>(b) * a.lvl_N[lv] +
                                    static_cast<size_t>((2 * Py) >> lv) * a.lvl_W[lv] + ((2 * Px) >> lv);
                 arow[i] = (anc * a.heads + h) * D;
@@ -431,7 +443,7 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
 #pragma unroll
                         for (int e4 = 0; e4 < E; e4 += 4)
                             mq[i][(j * E + e4) / 4] =
-                                *reinterpret_cast<const float4*>(a.msg_fwd[lv] + arow[i] + (g + 4 * j) * E + e4);
+                                load_at<float4>(a.msg_fwd[lv] + arow[i], ((g + 4 * j) * E + e4) * 4u);
                 }
             }
 #pragma unroll
@@ -442,12 +454,6 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
 #pragma unroll
                 for (int j = 0; j < NJ; ++j) {
                     const int c0 = (g + 4 * j) * E;
-                    float sv[E];
-#pragma unroll
-                    for (int e = 0; e < E; ++e) {
-                        // the four queries: query n16 >> 2 on lanes 4 apart (each on four lanes)
-                        sv[e] = row_sum_stride4(wl[i] * gv[j][e]);
-                    }
                     if (want_dw) {
 #pragma unroll
                         for (int e4 = 0; e4 < E; e4 += 4) {
@@ -455,11 +461,17 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
                             part += gv[j][e4] * m4.x + gv[j][e4 + 1] * m4.y + gv[j][e4 + 2] * m4.z + gv[j][e4 + 3] * m4.w;
                         }
                     }
-                    // every lane of group g holds the sums of chunk g + 4j: lane 16g + e stores
-                    // element e, so one instruction covers the head's channels contiguously
-                    float mine = sv[0];
-#pragma unroll
-                    for (int e = 1; e < E; ++e) mine = n16 == e ? sv[e] : mine;
+                    // lane 16g + e stores element e of chunk g + 4j (one instruction covers the head's
+                    // channels contiguously): the sum over the four queries (query n16 >> 2, on lanes
+                    // 4 apart). Lane 4q + i contributes its query's elements i (and, with eight per
+                    // chunk, i + 4); after the sums over lanes 4 apart, lanes 0-3 hold elements 0-3
+                    // and lanes 4-7 elements 4-7
+                    const int ei = n16 & 3;
+                    float mine = row_sum_stride4(wl[i] * pick4_at(gv[j], 0, ei));
+                    if constexpr (E == 8) {
+                        const float hi = row_sum_stride4(wl[i] * pick4_at(gv[j], 4, ei));
+                        mine = n16 < 4 ? mine : hi;
+                    }
                     if (n16 < E) {
                         float* dst = a.dm_out[lv] + arow[i] + c0 + n16;
                         if (lv == 1)
@@ -471,7 +483,7 @@ __device__ __forceinline__ void bwd_item(const BwdLevelArgs& a, const int item, 
                 if (want_dw) {
                     part += xchg_f32<16>(part);
                     part += xchg_f32<32>(part);
-                    if (g == 0 && (n16 & 3) == 0 && q_ok) a.dw[wrow + lv] = part;
+                    if (g == 0 && (n16 & 3) == 0 && q_ok) store_at<float>(a.dw + static_cast<size_t>(b) * N * a.heads * L, (wrow + lv) * 4u, part);
                 }
             }
         }
