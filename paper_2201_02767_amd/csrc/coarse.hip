@@ -24,7 +24,7 @@ namespace qta {
 
 namespace {
 
-typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
 
@@ -64,6 +64,13 @@ __global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6)), lane = threadIdx.x & 63;
     const size_t tok0 = static_cast<size_t>(b) * N;           // first token of this batch element
     const size_t hoff = static_cast<size_t>(h) * D;
+    // this map's rows as wave-uniform bases; a row's offset from them, below N * C elements
+    // (N <= 1024 and C <= 2^20, so under 2^32 bytes), is a 32-bit lane offset
+    const size_t map0 = tok0 * C + hoff;
+    const unsigned char* qmap = static_cast<const unsigned char*>(a.q) + map0 * sizeof(T);
+    const unsigned char* kmap = static_cast<const unsigned char*>(a.k) + map0 * sizeof(T);
+    const unsigned char* vmap = static_cast<const unsigned char*>(a.v) + map0 * sizeof(T);
+    const uint32_t row_bytes = static_cast<uint32_t>(C) * sizeof(T);   // <= 2^22
 
     // V operands of phase 3's first two key batches, requested after the logits' operands so that
     // their latency overlaps the logits and the selection (phase 3 layout: lane (kgrp, col) holds
@@ -80,7 +87,7 @@ __global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
 #pragma unroll
         for (int u = 0; u < kVBatch; ++u) {
             const int cand = min((st0 + u * NKS) * 4 + (lane >> 4), N - 1);    // clamped; weight 0 beyond N
-            dst[u] = S::load1(a.v, (tok0 + cand) * C + hoff + p3_ch);
+            dst[u] = S::load1_at(vmap, __umul24(static_cast<uint32_t>(cand), static_cast<uint32_t>(C)) + p3_ch);
         }
     };
 
@@ -94,11 +101,13 @@ __global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
         const int arow = lane & 15, kgrp = lane >> 4;
         const int qi = min(tile * Q + (arow & (Q - 1)), N - 1);   // rows past N are computed and ignored
         constexpr int NJ = D * static_cast<int>(sizeof(T)) / 64;   // 16-byte chunks per lane and row
-        constexpr int kTileBatch = 4;
+        // key tiles a wave takes (N <= 64 * kPerLane, so at most 4 * kPerLane tiles over Q waves),
+        // loaded as one batch where that is at most four: no registers held for tiles no wave has
+        constexpr int kTileBatch = (4 * kPerLane + Q - 1) / Q < 4 ? (4 * kPerLane + Q - 1) / Q : 4;
         uint4 qa[NJ];
-        const unsigned char* qrow = static_cast<const unsigned char*>(a.q) + ((tok0 + qi) * C + hoff) * sizeof(T);
+        const uint32_t qoff = __umul24(static_cast<uint32_t>(qi), row_bytes) + kgrp * 16;
 #pragma unroll
-        for (int jj = 0; jj < NJ; ++jj) qa[jj] = *reinterpret_cast<const uint4*>(qrow + (kgrp + 4 * jj) * 16);
+        for (int jj = 0; jj < NJ; ++jj) qa[jj] = load_at<uint4>(qmap, qoff + 64 * jj);
         bool first = true;
         for (int t0 = wave; t0 < ktiles; t0 += kWaves * kTileBatch) {             // uniform
             uint4 kb[kTileBatch][NJ];
@@ -106,9 +115,9 @@ __global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
             for (int it = 0; it < kTileBatch; ++it) {
                 if (t0 + kWaves * it >= ktiles) break;                            // uniform
                 const int n = min((t0 + kWaves * it) * 16 + arow, N - 1);         // columns past N set to -inf
-                const unsigned char* krow = static_cast<const unsigned char*>(a.k) + ((tok0 + n) * C + hoff) * sizeof(T);
+                const uint32_t koff = __umul24(static_cast<uint32_t>(n), row_bytes) + kgrp * 16;
 #pragma unroll
-                for (int jj = 0; jj < NJ; ++jj) kb[it][jj] = *reinterpret_cast<const uint4*>(krow + (kgrp + 4 * jj) * 16);
+                for (int jj = 0; jj < NJ; ++jj) kb[it][jj] = load_at<uint4>(kmap, koff + 64 * jj);
             }
             if (first) {
                 load_v(p3_ks, vb);
@@ -123,19 +132,9 @@ __global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
 #pragma unroll
                 for (int jj = 0; jj < NJ; ++jj) {
                     if constexpr (kBf16) {
-                        // 8 bf16 per chunk: k-steps 2*jj and 2*jj+1, four channels each
-                        const uint4 qq = qa[jj], kk = kb[it][jj];
-                        short4_t a0, b0, a1, b1;
-                        a0[0] = static_cast<short>(qq.x); a0[1] = static_cast<short>(qq.x >> 16);
-                        a0[2] = static_cast<short>(qq.y); a0[3] = static_cast<short>(qq.y >> 16);
-                        a1[0] = static_cast<short>(qq.z); a1[1] = static_cast<short>(qq.z >> 16);
-                        a1[2] = static_cast<short>(qq.w); a1[3] = static_cast<short>(qq.w >> 16);
-                        b0[0] = static_cast<short>(kk.x); b0[1] = static_cast<short>(kk.x >> 16);
-                        b0[2] = static_cast<short>(kk.y); b0[3] = static_cast<short>(kk.y >> 16);
-                        b1[0] = static_cast<short>(kk.z); b1[1] = static_cast<short>(kk.z >> 16);
-                        b1[2] = static_cast<short>(kk.w); b1[3] = static_cast<short>(kk.w >> 16);
-                        acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, b0, acc, 0, 0, 0);
-                        acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, b1, acc, 0, 0, 0);
+                        // 8 bf16 per chunk: one k-step of 32 (eight channels per lane)
+                        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qa[jj]),
+                                                                      __builtin_bit_cast(bf16x8_t, kb[it][jj]), acc, 0, 0, 0);
                     } else {
                         // 4 floats per chunk: four k-steps
                         const uint4 qq = qa[jj], kk = kb[it][jj];
@@ -176,7 +175,7 @@ __global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
                 const int yy = qy + ky - 1, xx = qx + kx - 1;
                 const int yc = min(max(yy, 0), Hc - 1), xc = min(max(xx, 0), Wc - 1);
                 const unsigned ok = opaque_mask(yy >= 0 && yy < Hc && xx >= 0 && xx < Wc);
-                pev[ky * 3 + kx] = masked(S::load1(a.v, (tok0 + yc * Wc + xc) * C + hoff + ech), ok);
+                pev[ky * 3 + kx] = masked(S::load1_at(vmap, __umul24(static_cast<uint32_t>(yc * Wc + xc), static_cast<uint32_t>(C)) + ech), ok);
                 pew[ky * 3 + kx] = wk[ky * 3 + kx];
             }
         peb = a.pe_b ? a.pe_b[h * D + ech] : 0.f;
@@ -291,9 +290,9 @@ __global__ __launch_bounds__(Q * kWave) void coarse_attn_kernel(CoarseArgs a)
             float wl = 1.0f;
             if (!VA) wl = a.w ? a.w[((tok0 + qi) * a.heads + h) * a.levels] : 1.0f / a.levels;
             const float pe = a.pe0 ? a.pe0[((tok0 + qi) * a.heads + h) * D + ch] : 0.f;
-            S::store1(a.out, (tok0 + qi) * C + hoff + ch, wl * (s + pe));
+            S::store1_at(static_cast<unsigned char*>(a.out) + map0 * sizeof(T), __umul24(static_cast<uint32_t>(qi), static_cast<uint32_t>(C)) + ch, wl * (s + pe));
         } else {
-            a.msg[((tok0 + qi) * a.heads + h) * D + ch] = s;
+            store_at<float>(a.msg + map0, (__umul24(static_cast<uint32_t>(qi), static_cast<uint32_t>(C)) + ch) * 4u, s);
         }
     }
 }

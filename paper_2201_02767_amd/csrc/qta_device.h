@@ -67,6 +67,7 @@ template <> struct Storage<float> {
         static_cast<float*>(base)[i] = x;
     }
     // element i (below 2^30) of a wave-uniform base
+    __device__ static __forceinline__ float load1_at(const void* base, uint32_t i) { return load_at<float>(base, i * 4u); }
     __device__ static __forceinline__ void store1_at(void* base, uint32_t i, float x) { store_at<float>(base, i * 4u, x); }
     // Round an fp32 value to this storage type and back.
     __device__ static __forceinline__ float round(float x) { return x; }
@@ -99,6 +100,10 @@ template <> struct Storage<bf16> {
         static_cast<uint16_t*>(base)[i] = static_cast<uint16_t>(f32_to_bf16_bits(x));
     }
     // element i (below 2^31) of a wave-uniform base
+    __device__ static __forceinline__ float load1_at(const void* base, uint32_t i)
+    {
+        return bf16_bits_to_f32(load_at<uint16_t>(base, i * 2u));
+    }
     __device__ static __forceinline__ void store1_at(void* base, uint32_t i, float x)
     {
         store_at<uint16_t>(base, i * 2u, static_cast<uint16_t>(f32_to_bf16_bits(x)));
