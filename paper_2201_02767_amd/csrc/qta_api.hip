@@ -180,8 +180,8 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], in
                        bool use_bf16, hipStream_t stream)
 {
     for (int s = 0; s + 1 < levels;) {
-        const bool four = levels - s == 5 && pyramid_passn_fits(4, chunks, Hl[s] == 1);
-        const bool three = levels - s == 4 && pyramid_passn_fits(3, chunks, Hl[s] == 1);
+        const bool four = levels - s == 5 && pyramid_tree_fits(4, chunks, head_chunks, Hl[s] == 1, Hl[s], Wl[s]);
+        const bool three = levels - s == 4 && pyramid_tree_fits(3, chunks, head_chunks, Hl[s] == 1, Hl[s], Wl[s]);
         const int nlev = four ? 4 : three ? 3 : (s + 2 < levels) ? 2 : 1;
         PyramidPassArgs a{};
         for (int t = 0; t < ntensors; ++t) {
@@ -204,6 +204,8 @@ hipError_t run_pyramid(const void* const* src0, void* (*lvl)[QTA_MAX_LEVELS], in
         a.W4 = nlev == 4 ? Wl[s + 4] : 0;
         a.chunks = chunks;
         a.head_chunks = head_chunks;
+        a.lg_head_chunks = 0;
+        while ((2 << a.lg_head_chunks) <= head_chunks) ++a.lg_head_chunks;
         a.src_blocked = s > 0 && blocked[s];
         a.dst1_blocked = blocked[s + 1] != 0;
         a.dst2_blocked = nlev >= 2 && blocked[s + 2] != 0;

@@ -52,14 +52,56 @@ struct PyramidPassArgs {
     int B, Hs, Ws, H1, W1, H2, W2, H3, W3, H4, W4;
     int chunks;                 // 16-byte chunks per token (C * sizeof(dtype) / 16)
     int head_chunks;            // 16-byte chunks per head row (d * sizeof(dtype) / 16)
+    int lg_head_chunks;         // log2(head_chunks) (a power of two for every supported d)
     bool src_blocked, dst1_blocked, dst2_blocked, dst3_blocked, dst4_blocked;
 };
 
-// Whether the three- or four-level pass (nlev) takes tokens of `chunks` 16-byte chunks (maps of
-// one row when `row`): a top token's level-1 children must fit 1024 chunks, four per thread.
-inline bool pyramid_passn_fits(int nlev, int chunks, bool row)
+// LDS chunks staged per level-1 level of the multi-level pyramid pass (16 KiB).
+constexpr int kPyramidStage = 1024;
+
+// Workgroup of the multi-level pyramid pass over nlev levels (2..4): `by` token rows of `chunks`
+// threads, each taking up to R level-1 tokens, and tpb top tokens per workgroup (a top token has
+// NC^(nlev-1) level-1 tokens, NC = 4, or 2 for maps of one row). About 256 threads, more when a
+// top token's level-1 tokens would need more than four per thread.
+struct PyramidTreeShape {
+    bool ok;
+    int by, tpb, R;
+};
+inline PyramidTreeShape pyramid_tree_shape(int nlev, int chunks, bool row)
 {
-    return (1 << ((row ? 1 : 2) * (nlev - 1))) * chunks <= 1024;
+    PyramidTreeShape g{false, 0, 0, 0};
+    if (nlev < 2 || nlev > 4 || chunks <= 0 || chunks > 1024) return g;
+    const int L1 = 1 << ((row ? 1 : 2) * (nlev - 1));
+    if (static_cast<long long>(L1) * chunks > kPyramidStage) return g;
+    int by = 256 / chunks > 1 ? 256 / chunks : 1;
+    if (L1 >= by) {
+        g.tpb = 1;
+        g.R = (L1 + by - 1) / by;
+        if (g.R > 4) {
+            by = (L1 + 3) / 4;
+            g.R = (L1 + by - 1) / by;
+        }
+    } else {
+        g.tpb = by / L1;
+        by = g.tpb * L1;
+        g.R = 1;
+    }
+    if (g.R == 3) g.R = 4;                                 // instantiated for 1, 2 and 4
+    g.by = by;
+    g.ok = static_cast<long long>(by) * chunks <= 1024;
+    return g;
+}
+
+// Whether the multi-level pyramid pass takes a pass over nlev levels from an Hs x Ws source: the
+// shape above exists, head_chunks is a power of two, and one batch element's map of any level of
+// the pass (parent-blocked padding included) is addressed with 32-bit offsets and 24-bit products.
+inline bool pyramid_tree_fits(int nlev, int chunks, int head_chunks, bool row, int Hs, int Ws)
+{
+    if (!pyramid_tree_shape(nlev, chunks, row).ok) return false;
+    if (head_chunks <= 0 || (head_chunks & (head_chunks - 1)) != 0 || chunks % head_chunks != 0) return false;
+    const long long tokens = static_cast<long long>(Hs + 2) * (Ws + 2);
+    const long long side = Hs > Ws ? Hs : Ws;
+    return tokens < (1LL << 24) && tokens * chunks * 16 < (1LL << 32) && side * chunks < (1LL << 24);
 }
 
 struct CoarseArgs {
