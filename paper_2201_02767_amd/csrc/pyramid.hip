@@ -217,7 +217,11 @@ __global__ __launch_bounds__(1024) void pyramid_tree_kernel(PyramidPassArgs a, i
         char* dst = const_cast<char*>(batch_base(a.dst1[tensor], a.dst1_blocked, a.H1, a.W1));
 #pragma unroll
         for (int it = 0; it < R; ++it) {
-            const int tk = ty + it * by;
+            // rows past the last token repeat it (same loads, same value, same staging slot), so the
+            // pooling and the staging are unconditional: a pooling under a branch leaves the loads
+            // pending on the path that skips it, and the compiler then makes the next level wait for
+            // every outstanding memory operation, the global stores of this level included
+            const int tk = min(ty + it * by, ntok1 - 1);
             float c00[E], c01[E], c10[E], c11[E], mid[E];
             S::unpack(raw[it][0][0], c00);
             S::unpack(raw[it][0][1], c01);
@@ -225,11 +229,9 @@ __global__ __launch_bounds__(1024) void pyramid_tree_kernel(PyramidPassArgs a, i
             S::unpack(raw[it][1][1], c11);
             pool_children<E>(c00, c01, c10, c11, 2 * x1[it] + 1 < a.Ws, !ROW && 2 * y1[it] + 1 < a.Hs, mid);
             const uint4 packed = S::pack(mid);               // rounds to the storage type
-            if (tk < ntok1) {
-                if (y1[it] < a.H1 && x1[it] < a.W1)
-                    store_at<uint4>(dst, offset(a.dst1_blocked, a.H1, a.W1, y1[it], x1[it]), packed);
-                stage1[tk * chunks + ch] = packed;
-            }
+            stage1[tk * chunks + ch] = packed;
+            if (y1[it] < a.H1 && x1[it] < a.W1)
+                store_at<uint4>(dst, offset(a.dst1_blocked, a.H1, a.W1, y1[it], x1[it]), packed);
         }
     }
 
