@@ -42,6 +42,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
 constexpr int kMaxSlots = 256;         // candidate slots of one item: 4 K_l for K_l <= 64, up to four per lane
 constexpr int kMaxSlotsPe = 64;        // with a fused position encoding: one slot per lane
+constexpr int kSplitSlots = 64;        // bf16 value rows staged per round when a group has 65 .. 128 slots
 constexpr int kPrefetchLevels = 4;    // the finest level prefetches up to this many ancestors
 // LDS pitch (elements) of one channel's 16 tokens in the fused position encoding: 20 puts the four lane
 // groups' writes and neighbouring channels' row reads in different banks (16 would stack them)
@@ -62,7 +63,9 @@ __host__ __device__ inline WaveLds wave_lds(int nsp)
     L.v = 0;
     int vbytes;
     if (TB == 2) {
-        L.vpitch = nsp + 8;                 // Vt[channel][slot]
+        // Vt[channel][slot]; with 65 .. 128 slots the rows are staged in two rounds of at most 64
+        // slots (half the LDS per wave, so that registers rather than LDS bound the occupancy)
+        L.vpitch = (nsp > kSplitSlots && nsp <= 2 * kSplitSlots ? kSplitSlots : nsp) + 8;
         vbytes = D * L.vpitch * 2;
     } else {
         L.vpitch = D + 4;                   // Vs[slot][channel]
@@ -187,6 +190,10 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     constexpr int NH = 16 / NCG;           // PV: slot halves (2 for d = 32, 1 for d = 64)
     constexpr int QPL = 4 / NH;            // output queries per lane
     constexpr int SPL = NSP > 64 ? NSP / 64 : 1;   // candidate slots per lane: lane + 64u
+    // bf16 with 65 .. 128 slots: slots 0 .. 63 are staged as their tiles are consumed, the value rows
+    // of slots 64 .. are held in registers and staged after the first round of messages
+    constexpr bool kSplitV = kBf16 && NSP == 2 * kSplitSlots;
+    constexpr int kTS = kSplitSlots / 16;           // tiles of the first round
     static_assert(!PE || !ROW, "the fused position encoding is for maps of more than one row");
     static_assert(NSP <= kMaxSlotsPe || !PE, "a fused position encoding takes at most 64 slots");
 
@@ -384,6 +391,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     float xs[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) xs[t] = 0.f;
+    uint4 vkeep[kSplitV ? NT - kTS : 1][NJ];
     auto consume_tiles = [&](int t0) {
 #pragma unroll
         for (int i = 0; i < kTB; ++i) {
@@ -416,7 +424,9 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                 // (a missing candidate's row gets weight 0 in the messages)
                 const uint4 vv = (D == 32 || gok[t]) ? vc[i][j] : make_uint4(0, 0, 0, 0);
                 const int c0 = (g + 4 * j) * E;               // first channel of this chunk
-                if constexpr (kBf16) {
+                if (kSplitV && t >= kTS) {                    // compile-time after unrolling
+                    vkeep[kSplitV ? t - kTS : 0][j] = vv;
+                } else if constexpr (kBf16) {
                     uint16_t* vt = reinterpret_cast<uint16_t*>(Vb);
                     const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
 #pragma unroll
@@ -593,22 +603,51 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     wave_lds_sync();
 
     // ---- 5b. messages on MFMA ----
-    const int sph = nsp / NH;
     float4_t o = {0.f, 0.f, 0.f, 0.f};
     if constexpr (kBf16) {
-        const uint16_t* prow_l = reinterpret_cast<const uint16_t*>(Pb) + t4 * nsp + hh * sph;
-        const uint16_t* vrow_l = reinterpret_cast<const uint16_t*>(Vb) + (4 * cg + t4) * lay.vpitch + hh * sph;
-        for (int st = 0; st < sph; st += 4) {
-            const uint2 pa = *reinterpret_cast<const uint2*>(prow_l + st);
-            const uint2 vb = *reinterpret_cast<const uint2*>(vrow_l + st);
-            short4_t av, bv;
-            av[0] = static_cast<short>(pa.x); av[1] = static_cast<short>(pa.x >> 16);
-            av[2] = static_cast<short>(pa.y); av[3] = static_cast<short>(pa.y >> 16);
-            bv[0] = static_cast<short>(vb.x); bv[1] = static_cast<short>(vb.x >> 16);
-            bv[2] = static_cast<short>(vb.y); bv[3] = static_cast<short>(vb.y >> 16);
-            o = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(av, bv, o, 0, 0, 0);
+        // slots [s0, s0 + n) staged at Vt columns 0 .. n-1; lane half hh sums its half of them
+        auto pv_round = [&](int s0, int n) {
+            const int sph = n / NH;
+            const uint16_t* prow_l = reinterpret_cast<const uint16_t*>(Pb) + t4 * nsp + s0 + hh * sph;
+            const uint16_t* vrow_l = reinterpret_cast<const uint16_t*>(Vb) + (4 * cg + t4) * lay.vpitch + hh * sph;
+            for (int st = 0; st < sph; st += 4) {
+                const uint2 pa = *reinterpret_cast<const uint2*>(prow_l + st);
+                const uint2 vb = *reinterpret_cast<const uint2*>(vrow_l + st);
+                short4_t av, bv;
+                av[0] = static_cast<short>(pa.x); av[1] = static_cast<short>(pa.x >> 16);
+                av[2] = static_cast<short>(pa.y); av[3] = static_cast<short>(pa.y >> 16);
+                bv[0] = static_cast<short>(vb.x); bv[1] = static_cast<short>(vb.x >> 16);
+                bv[2] = static_cast<short>(vb.y); bv[3] = static_cast<short>(vb.y >> 16);
+                o = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(av, bv, o, 0, 0, 0);
+            }
+        };
+        if constexpr (kSplitV) {
+            pv_round(0, kSplitSlots);
+            // the second round's value rows over the first's (same lane layout as in the tiles)
+            wave_lds_sync();
+            uint16_t* vt = reinterpret_cast<uint16_t*>(Vb);
+#pragma unroll
+            for (int t = kTS; t < NT; ++t) {
+                if (t >= ntile) break;                        // uniform
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const uint4 vv = vkeep[t - kTS][j];
+                    const int c0 = (g + 4 * j) * E;
+                    const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const uint32_t bits = (e & 1) ? (w4[e >> 1] >> 16) : (w4[e >> 1] & 0xFFFFu);
+                        vt[(c0 + e) * lay.vpitch + 16 * (t - kTS) + n16] = static_cast<uint16_t>(bits);
+                    }
+                }
+            }
+            wave_lds_sync();
+            pv_round(kSplitSlots, nsp - kSplitSlots);
+        } else {
+            pv_round(0, nsp);
         }
     } else {
+        const int sph = nsp / NH;
         const float* prow_l = reinterpret_cast<const float*>(Pb) + t4 * nsp + hh * sph;
         const float* vcol = reinterpret_cast<const float*>(Vb) + 4 * cg + t4;
         for (int st = 0; st < sph; ++st)
