@@ -815,8 +815,8 @@ __host__ __device__ inline KeyLds key_lds()
     const int mbytes = L.mslots * L.mpitch * (bf && FINEST ? 2 : 4);
     L.rows = 0;
     L.dx = L.rows + (qbytes > mbytes ? qbytes : mbytes);
-    L.vw = L.dx + 4 * kKeyChunk * 16;
-    L.total = L.vw + 4 * kKeyChunk * 16;
+    L.vw = L.dx;                                           // the weights replace dx once dk is done
+    L.total = L.dx + 4 * kKeyChunk * 16;
     return L;
 }
 
@@ -1041,6 +1041,7 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
     }
 
     // ---- slot `lane`: its query's statistics and the weights of the four keys ----
+    float4 vw_lane;                       // staged over dx once dk has read it
     {
         const int s = lane;
         int P, r, qtok;
@@ -1083,7 +1084,7 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
             for (int c = 0; c < 4; ++c) vw[c] *= w0;         // the dout rows are stored without w_0
         }
         *reinterpret_cast<float4*>(dxs + s * 4) = make_float4(dx[0], dx[1], dx[2], dx[3]);
-        *reinterpret_cast<float4*>(vws + s * 4) = make_float4(vw[0], vw[1], vw[2], vw[3]);
+        vw_lane = make_float4(vw[0], vw[1], vw[2], vw[3]);
     }
     wave_lds_sync();
 
@@ -1105,6 +1106,7 @@ __global__ __launch_bounds__(64) void bwd_key_kernel(BwdLevelArgs a)
         const int first = pass * lay.mslots;
         if (first >= nsp) break;                              // uniform
         wave_lds_sync();
+        if (pass == 0) *reinterpret_cast<float4*>(vws + lane * 4) = vw_lane;   // (vws aliases dxs)
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             if (t >= ntile) break;                            // uniform
