@@ -71,9 +71,10 @@ __host__ __device__ inline BwdLds bwd_lds(int nsp)
     constexpr int TB = sizeof(T);
     BwdLds L;
     // rows of 16-byte multiples; bf16 rows with d = 32 unpadded: the dq loop's two slot halves are 32
-    // rows apart and meet the same banks with a padded pitch as well, and the 5 KB a wave then takes
-    // with 64 slots lets LDS hold 8 waves per SIMD instead of 6 (d = 64 keeps its padding: unpadded
-    // it measured slower, with registers, not LDS, bounding its occupancy)
+    // rows apart and meet the same banks with a padded pitch as well, the row writes conflict more,
+    // and the 5 KB a wave then takes with 64 slots lets LDS hold 8 waves per SIMD instead of 6, which
+    // outweighs that (d = 64 keeps its padding: unpadded it measured slower, with registers, not
+    // LDS, bounding its occupancy)
     L.kpitch = TB == 2 ? (D == 32 ? D : D + 8) : D + 4;
     L.ks = 0;
     L.dx = L.ks + nsp * L.kpitch * TB;
