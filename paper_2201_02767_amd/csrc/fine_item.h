@@ -42,7 +42,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
 constexpr int kMaxSlots = 256;         // candidate slots of one item: 4 K_l for K_l <= 64, up to four per lane
 constexpr int kMaxSlotsPe = 64;        // with a fused position encoding: one slot per lane
-constexpr int kSplitSlots = 64;        // bf16 value rows staged per round when a group has 65 .. 128 slots
+constexpr int kSplitSlots = 64;        // bf16 value rows staged at a time when a group has 65 .. 128 slots
 constexpr int kPrefetchLevels = 4;    // the finest level prefetches up to this many ancestors
 // LDS pitch (elements) of one channel's 16 tokens in the fused position encoding: 20 puts the four lane
 // groups' writes and neighbouring channels' row reads in different banks (16 would stack them)
@@ -63,7 +63,7 @@ __host__ __device__ inline WaveLds wave_lds(int nsp)
     L.v = 0;
     int vbytes;
     if (TB == 2) {
-        // Vt[channel][slot]; with 65 .. 128 slots the rows are staged in two rounds of at most 64
+        // Vt[channel][slot]; with 65 .. 128 slots the rows are staged in two halves of at most 64
         // slots (half the LDS per wave, so that registers rather than LDS bound the occupancy)
         L.vpitch = (nsp > kSplitSlots && nsp <= 2 * kSplitSlots ? kSplitSlots : nsp) + 8;
         vbytes = D * L.vpitch * 2;
@@ -191,9 +191,9 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     constexpr int QPL = 4 / NH;            // output queries per lane
     constexpr int SPL = NSP > 64 ? NSP / 64 : 1;   // candidate slots per lane: lane + 64u
     // bf16 with 65 .. 128 slots: slots 0 .. 63 are staged as their tiles are consumed, the value rows
-    // of slots 64 .. are held in registers and staged after the first round of messages
+    // of slots 64 .. are held in registers and staged after the first half of the messages
     constexpr bool kSplitV = kBf16 && NSP == 2 * kSplitSlots;
-    constexpr int kTS = kSplitSlots / 16;           // tiles of the first round
+    constexpr int kTS = kSplitSlots / 16;           // tiles of the first half
     static_assert(!PE || !ROW, "the fused position encoding is for maps of more than one row");
     static_assert(NSP <= kMaxSlotsPe || !PE, "a fused position encoding takes at most 64 slots");
 
@@ -606,7 +606,7 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
     float4_t o = {0.f, 0.f, 0.f, 0.f};
     if constexpr (kBf16) {
         // slots [s0, s0 + n) staged at Vt columns 0 .. n-1; lane half hh sums its half of them
-        auto pv_round = [&](int s0, int n) {
+        auto pv_part = [&](int s0, int n) {
             const int sph = n / NH;
             const uint16_t* prow_l = reinterpret_cast<const uint16_t*>(Pb) + t4 * nsp + s0 + hh * sph;
             const uint16_t* vrow_l = reinterpret_cast<const uint16_t*>(Vb) + (4 * cg + t4) * lay.vpitch + hh * sph;
@@ -622,8 +622,8 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
             }
         };
         if constexpr (kSplitV) {
-            pv_round(0, kSplitSlots);
-            // the second round's value rows over the first's (same lane layout as in the tiles)
+            pv_part(0, kSplitSlots);
+            // the second half's value rows over the first's (same lane layout as in the tiles)
             wave_lds_sync();
             uint16_t* vt = reinterpret_cast<uint16_t*>(Vb);
 #pragma unroll
@@ -642,9 +642,9 @@ __device__ __forceinline__ void fine_item(const FineArgs& a, const ItemHead<T, D
                 }
             }
             wave_lds_sync();
-            pv_round(kSplitSlots, nsp - kSplitSlots);
+            pv_part(kSplitSlots, nsp - kSplitSlots);
         } else {
-            pv_round(0, nsp);
+            pv_part(0, nsp);
         }
     } else {
         const int sph = nsp / NH;
